@@ -1,0 +1,173 @@
+"""CPU oracle for the GaLore 2 hot path -- TEST INFRASTRUCTURE ONLY.
+
+Plain fp64 C (``galore_oracle.c``) behind ctypes. Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may import
+this package; the product library never does.  It shares no code with the HIP
+path.  Every function takes and returns float64 numpy arrays; callers widen the
+exact stored fp32/bf16 values (and fp32 hyper-parameters) before calling.
+
+What each function follows (paper = "GaLore 2", Su et al. 2025):
+  sketch           Gaussian test matrix of Halko, Martinsson & Tropp 2011 (§4),
+                   drawn by Philox4x64-10 + Box-Muller
+  householder_qr   thin QR, Golub & Van Loan §5.2
+  jacobi_left_svd  one-sided (Hestenes) Jacobi SVD, left singular vectors
+  rsvd_update      paper §3 / Alg. 1 subspace selection with the randomized SVD
+                   of paper §4.1.2 (Halko et al. Alg. 4.4 + Alg. 5.1)
+  project          paper §3, R = P^T G
+  adam             paper §3 moments + Alg. 1 bias correction
+  project_back     paper §3, W <- W + eta alpha P N (applied as W -= lr alpha P N
+                   for the autograd gradient)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "galore_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_f64p = ctypes.POINTER(ctypes.c_double)
+_u64p = ctypes.POINTER(ctypes.c_uint64)
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (plain -O2 + OpenMP)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+        lib.orc_philox4x64_10.argtypes = [_u64p, _u64p, _u64p]
+        lib.orc_philox4x64_10.restype = None
+        lib.orc_normal_from_words.argtypes = [u64, u64]
+        lib.orc_normal_from_words.restype = ctypes.c_double
+        lib.orc_sketch.argtypes = [i64, i64, u64, u64, _f64p]
+        lib.orc_sketch.restype = None
+        lib.orc_householder_qr.argtypes = [i64, i64, _f64p, _f64p, _f64p]
+        lib.orc_householder_qr.restype = None
+        lib.orc_jacobi_left_svd.argtypes = [i64, i64, _f64p, _f64p, _f64p, ctypes.c_int]
+        lib.orc_jacobi_left_svd.restype = ctypes.c_int
+        lib.orc_canonical_signs.argtypes = [_f64p, i64, i64]
+        lib.orc_canonical_signs.restype = None
+        lib.orc_rsvd_update.argtypes = [_f64p, i64, i64, i32, i32, i32, u64, u64, _f64p, _f64p]
+        lib.orc_rsvd_update.restype = ctypes.c_int
+        lib.orc_project.argtypes = [_f64p, _f64p, i64, i64, i32, _f64p]
+        lib.orc_project.restype = None
+        lib.orc_adam.argtypes = [_f64p, _f64p, _f64p, _f64p, i64, ctypes.c_double, ctypes.c_double,
+                                 ctypes.c_double, i64]
+        lib.orc_adam.restype = None
+        lib.orc_project_back.argtypes = [_f64p, _f64p, _f64p, i64, i64, i32, ctypes.c_double,
+                                         ctypes.c_double]
+        lib.orc_project_back.restype = None
+        _lib = lib
+    return _lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(_f64p)
+
+
+def philox4x64_10(counter, key) -> np.ndarray:
+    lib = _load()
+    c = np.ascontiguousarray(np.asarray(counter, dtype=np.uint64).reshape(4))
+    k = np.ascontiguousarray(np.asarray(key, dtype=np.uint64).reshape(2))
+    out = np.zeros(4, dtype=np.uint64)
+    lib.orc_philox4x64_10(c.ctypes.data_as(_u64p), k.ctypes.data_as(_u64p), out.ctypes.data_as(_u64p))
+    return out
+
+
+def normal_from_words(x0: int, x1: int) -> float:
+    return float(_load().orc_normal_from_words(int(x0), int(x1)))
+
+
+def sketch(l: int, k: int, seed: int, sketch_index: int = 0) -> np.ndarray:
+    """Omega (l x k) as fp64 holding fp32-rounded N(0,1) draws."""
+    out = np.zeros((l, k), dtype=np.float64)
+    _load().orc_sketch(l, k, seed, sketch_index, _ptr(out))
+    return out
+
+
+def householder_qr(Y):
+    Y = _f64(Y)
+    s, k = Y.shape
+    assert s >= k
+    Q = np.zeros((s, k))
+    R = np.zeros((k, k))
+    _load().orc_householder_qr(s, k, _ptr(Y), _ptr(Q), _ptr(R))
+    return Q, R
+
+
+def jacobi_left_svd(B, max_sweeps: int = 60):
+    """Left singular vectors U (k x k) and sigma (k) of B (k x l, k <= l); sweeps (-1 = no conv.)."""
+    B = _f64(B)
+    k, l = B.shape
+    assert k <= l
+    U = np.zeros((k, k))
+    sig = np.zeros(k)
+    sweeps = _load().orc_jacobi_left_svd(k, l, _ptr(B), _ptr(U), _ptr(sig), max_sweeps)
+    return U, sig, sweeps
+
+
+def canonical_signs(P) -> np.ndarray:
+    P = _f64(P).copy()
+    _load().orc_canonical_signs(_ptr(P), P.shape[0], P.shape[1])
+    return P
+
+
+def rsvd_update(G, r: int, p: int, q: int, seed: int, sketch_index: int = 0):
+    """(P (s x r), sigma (r), sweeps) for the m x n gradient G."""
+    G = _f64(G)
+    m, n = G.shape
+    s = min(m, n)
+    P = np.zeros((s, r))
+    sig = np.zeros(r)
+    sweeps = _load().orc_rsvd_update(_ptr(G), m, n, r, p, q, seed, sketch_index, _ptr(P), _ptr(sig))
+    return P, sig, sweeps
+
+
+def project(P, G) -> np.ndarray:
+    P = _f64(P)
+    G = _f64(G)
+    m, n = G.shape
+    r = P.shape[1]
+    R = np.zeros((r, max(m, n)))
+    _load().orc_project(_ptr(P), _ptr(G), m, n, r, _ptr(R))
+    return R
+
+
+def adam(R, M, V, beta1: float, beta2: float, eps: float, t: int):
+    """Returns (M_new, V_new, N); inputs are not modified."""
+    R = _f64(R)
+    M = _f64(M).copy()
+    V = _f64(V).copy()
+    N = np.zeros_like(R)
+    _load().orc_adam(_ptr(R), _ptr(M), _ptr(V), _ptr(N), R.size, beta1, beta2, eps, t)
+    return M, V, N
+
+
+def project_back(P, N, W, lr: float, alpha: float) -> np.ndarray:
+    """Returns the updated W (input not modified)."""
+    P = _f64(P)
+    N = _f64(N)
+    W = _f64(W).copy()
+    m, n = W.shape
+    r = P.shape[1]
+    _load().orc_project_back(_ptr(P), _ptr(N), _ptr(W), m, n, r, lr, alpha)
+    return W

@@ -1,0 +1,379 @@
+"""Pins for the CPU oracle: each check is fixed by the mathematics, a library
+routine or a published value -- never by re-typing the oracle's own formula.
+
+Paper = "GaLore 2" (Su et al. 2025); Halko = Halko, Martinsson & Tropp 2011.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import galore_inputs as gi
+from metrics import proj_dist
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+U64 = (1 << 64) - 1
+
+
+# ---------------------------------------------------------------- Philox / sketch
+
+
+def test_philox_known_answer(orc):
+    """Published known-answer vector of Philox4x64-10 (Salmon et al. 2011)."""
+    rows = [ln.split() for ln in open(os.path.join(GOLDEN, "philox4x64_10_kat.txt")) if ln.strip() and not ln.startswith("#")]
+    assert rows
+    for row in rows:
+        v = [int(x, 16) for x in row]
+        out = orc.philox4x64_10(v[0:4], v[4:6])
+        assert [int(x) for x in out] == v[6:10]
+
+
+@pytest.mark.parametrize("seed", [0, 1, 20250429, 2**63 + 12345])
+def test_philox_matches_numpy_bit_generator(orc, seed):
+    """numpy.random.Philox is Philox4x64-10; it increments the counter before each block."""
+    rng = np.random.default_rng(seed)
+    for _ in range(8):
+        key = [int(x) for x in rng.integers(0, 2**63, size=2, dtype=np.int64)]
+        ctr = [int(x) for x in rng.integers(0, 2**63, size=4, dtype=np.int64)]
+        bg = np.random.Philox(key=np.array(key, dtype=np.uint64), counter=np.array(ctr, dtype=np.uint64))
+        ref = bg.random_raw(8)
+        c1 = [(ctr[0] + 1) & U64] + ctr[1:]
+        c2 = [(ctr[0] + 2) & U64] + ctr[1:]
+        got = np.concatenate([orc.philox4x64_10(c1, key), orc.philox4x64_10(c2, key)])
+        assert np.array_equal(got.astype(np.uint64), ref.astype(np.uint64))
+
+
+def test_box_muller_edges(orc):
+    # u1 = 1 exactly (all top bits set) -> radius 0
+    assert orc.normal_from_words(U64, 12345) == 0.0
+    # u2 = 0 -> cos = 1 -> z = sqrt(-2 ln u1) > 0 ; smallest u1 = 2^-53 -> largest radius
+    z = orc.normal_from_words(0, 0)
+    assert abs(z - np.sqrt(2.0 * 53.0 * np.log(2.0))) < 1e-12
+    # u2 = 1/2 -> cos = -1
+    z = orc.normal_from_words(0, 1 << 63)
+    assert abs(z + np.sqrt(2.0 * 53.0 * np.log(2.0))) < 1e-12
+
+
+def test_sketch_is_standard_normal(orc):
+    """Halko §4 needs i.i.d. N(0,1) entries: moments and a KS test on 1e6 draws."""
+    from scipy import stats
+    om = orc.sketch(1000, 1000, seed=7, sketch_index=3)
+    x = om.ravel()
+    assert abs(x.mean()) < 5e-3
+    assert abs(x.var() - 1.0) < 5e-3
+    assert abs(stats.skew(x)) < 1e-2 and abs(stats.kurtosis(x)) < 2e-2
+    assert stats.kstest(x, "norm").pvalue > 1e-3
+    # independent columns / rows: the sample correlation of neighbours is tiny
+    assert abs(np.corrcoef(om[:, 0], om[:, 1])[0, 1]) < 0.15
+    assert abs(np.mean(om[:-1, :] * om[1:, :])) < 5e-3
+
+
+def test_sketch_structure(orc):
+    a = orc.sketch(37, 9, seed=11, sketch_index=0)
+    b = orc.sketch(37, 5, seed=11, sketch_index=0)
+    assert np.array_equal(a[:, :5], b)                      # columns do not depend on k
+    assert np.array_equal(a.astype(np.float32).astype(np.float64), a)   # fp32 values
+    c = orc.sketch(37, 9, seed=11, sketch_index=1)
+    d = orc.sketch(37, 9, seed=12, sketch_index=0)
+    assert not np.any(a == c) or np.mean(a == c) < 0.05
+    assert np.mean(a == d) < 0.05
+    # entry (i, j) uses counter e = j*l + i, key (seed, 0), words 0 and 1
+    w = orc.philox4x64_10([4 * 37 + 10, 0, 0, 0], [11, 0])
+    assert a[10, 4] == np.float64(np.float32(orc.normal_from_words(int(w[0]), int(w[1]))))
+
+
+# ---------------------------------------------------------------- Householder QR
+
+
+@pytest.mark.parametrize("shape", [(50, 12), (12, 12), (300, 40), (7, 1)])
+def test_householder_qr_against_lapack(orc, shape):
+    rng = np.random.default_rng(sum(shape))
+    Y = rng.standard_normal(shape)
+    Q, R = orc.householder_qr(Y)
+    k = shape[1]
+    assert np.abs(Q.T @ Q - np.eye(k)).max() < 1e-13
+    assert np.abs(Q @ R - Y).max() < 1e-13 * max(1.0, np.abs(Y).max())
+    assert np.allclose(np.tril(R, -1), 0.0)
+    Ql, Rl = np.linalg.qr(Y)
+    assert np.abs(Q @ Q.T - Ql @ Ql.T).max() < 1e-12
+    assert np.allclose(np.abs(np.diag(R)), np.abs(np.diag(Rl)), rtol=1e-12, atol=1e-13)
+
+
+def test_householder_qr_degenerate(orc):
+    Q, R = orc.householder_qr(np.zeros((9, 4)))
+    assert np.array_equal(Q, np.eye(9)[:, :4]) and np.array_equal(R, np.zeros((4, 4)))
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((20, 2))
+    Y = np.column_stack([x[:, 0], 2 * x[:, 0], x[:, 1], np.zeros(20)])   # rank 2
+    Q, R = orc.householder_qr(Y)
+    assert np.abs(Q.T @ Q - np.eye(4)).max() < 1e-13
+    assert np.abs(Q @ R - Y).max() < 1e-13
+
+
+# ---------------------------------------------------------------- Jacobi SVD
+
+
+@pytest.mark.parametrize("shape", [(8, 20), (20, 20), (40, 688), (1, 5)])
+def test_jacobi_against_lapack(orc, shape):
+    rng = np.random.default_rng(shape[0] * 31 + shape[1])
+    B = rng.standard_normal(shape)
+    U, s, sw = orc.jacobi_left_svd(B)
+    assert sw >= 0          # -1 would mean no convergence
+    sl = np.linalg.svd(B, compute_uv=False)
+    assert np.abs(s - sl).max() <= 1e-12 * sl[0]
+    assert np.all(np.diff(s) <= 0)
+    assert np.abs(U.T @ U - np.eye(shape[0])).max() < 1e-13
+    # reconstruction: B = U diag(s) Vhat^T with Vhat = B^T U diag(1/s)
+    Vh = (B.T @ U) / s
+    assert np.abs(U @ np.diag(s) @ Vh.T - B).max() < 1e-12
+    assert np.abs(Vh.T @ Vh - np.eye(shape[0])).max() < 1e-11
+    Ul, _, _ = np.linalg.svd(B)
+    for j in range(shape[0]):
+        if j + 1 < shape[0] and (sl[j] - sl[j + 1]) < 1e-6 * sl[0]:
+            continue
+        if j > 0 and (sl[j - 1] - sl[j]) < 1e-6 * sl[0]:
+            continue
+        assert abs(abs(U[:, j] @ Ul[:, j]) - 1.0) < 1e-10
+
+
+def test_jacobi_closed_forms(orc):
+    d = np.array([0.5, -3.0, 2.0, 0.0])
+    B = np.zeros((4, 6))
+    B[np.arange(4), np.arange(4)] = d
+    U, s, _ = orc.jacobi_left_svd(B)
+    assert np.array_equal(s, np.array([3.0, 2.0, 0.5, 0.0]))
+    assert np.array_equal(np.abs(U), np.eye(4)[:, [1, 2, 0, 3]])
+    rng = np.random.default_rng(9)
+    x, y = rng.standard_normal(5), rng.standard_normal(11)
+    U, s, _ = orc.jacobi_left_svd(np.outer(x, y))
+    assert abs(s[0] - np.linalg.norm(x) * np.linalg.norm(y)) < 1e-13 * s[0]
+    assert np.all(s[1:] < 1e-13 * s[0])
+    assert abs(abs(U[:, 0] @ x) / np.linalg.norm(x) - 1.0) < 1e-13
+
+
+def test_canonical_signs(orc):
+    P = np.array([[0.1, -0.9, 0.5], [-0.8, 0.2, -0.5], [0.3, 0.1, 0.1]])
+    C = orc.canonical_signs(P)
+    assert np.array_equal(C[:, 0], -P[:, 0])       # largest |.| is -0.8
+    assert np.array_equal(C[:, 1], -P[:, 1])       # largest |.| is -0.9
+    assert np.array_equal(C[:, 2], P[:, 2])        # tie 0.5/-0.5: lowest row (+) wins
+
+
+# ---------------------------------------------------------------- randomized SVD
+
+
+def test_rsvd_full_sketch_equals_exact_svd(orc):
+    """k = min(r+p, s) = s: the sketch spans the whole range, so the rSVD is the
+    exact SVD (textbook reduction)."""
+    rng = np.random.default_rng(3)
+    for (m, n, r, p) in [(6, 9, 4, 2), (9, 6, 3, 5), (8, 8, 5, 3)]:
+        G = rng.standard_normal((m, n))
+        P, sig, sw = orc.rsvd_update(G, r, p, 1, seed=5)
+        u, ss, vt = np.linalg.svd(G)
+        ref = u[:, :r] if m <= n else vt.T[:, :r]
+        assert np.abs(sig - ss[:r]).max() < 1e-12 * ss[0]
+        assert proj_dist(P, ref) < 1e-10
+        for j in range(r):
+            assert abs(abs(P[:, j] @ ref[:, j]) - 1.0) < 1e-10
+
+
+@pytest.mark.parametrize("m,n,rank,r,p,q", [(256, 688, 32, 32, 8, 2), (256, 688, 36, 32, 8, 1),
+                                             (688, 256, 20, 32, 8, 2), (64, 64, 10, 12, 4, 0)])
+def test_rsvd_exact_recovery(orc, m, n, rank, r, p, q):
+    """rank(G) <= k (noiseless): range(Y) = range(G), so the planted spectrum and
+    the planted singular subspace are recovered exactly."""
+    s = 10.0 * 0.85 ** np.arange(min(m, n))
+    G = gi.planted_gradient(m, n, s, 0.0, seed=rank, rank=rank)
+    P, sig, sw = orc.rsvd_update(G, r, p, q, seed=99)
+    nr = min(r, rank)
+    assert np.abs(sig[:nr] - s[:nr]).max() < 1e-12 * s[0]
+    assert np.all(np.abs(sig[nr:]) < 1e-12 * s[0])
+    u, ss, vt = np.linalg.svd(G)
+    ref = (u if m <= n else vt.T)[:, :nr]
+    assert proj_dist(P[:, :nr], ref) < 1e-10
+    assert np.abs(P.T @ P - np.eye(r)).max() < 1e-12
+
+
+def test_rsvd_zero_gradient(orc):
+    P, sig, sw = orc.rsvd_update(np.zeros((20, 30)), 5, 3, 2, seed=1)
+    assert np.array_equal(sig, np.zeros(5))
+    assert np.array_equal(P, np.eye(20)[:, :5])
+
+
+@pytest.mark.parametrize("q", [0, 1, 2])
+def test_rsvd_invariants_and_halko_bound(orc, q):
+    """Interlacing (B = Q^T G), orthonormal P, canonical signs, and the mean of
+    ||(I - P P^T) A||_2 within Halko's average-case bound for the power scheme
+    (their Cor. 10.10) plus the truncation term sigma_{r+1} (their §9.3)."""
+    m, n, r, p = 120, 300, 10, 6
+    s = 1.0 / (1.0 + np.arange(m)) ** 0.7
+    G = gi.planted_gradient(m, n, s, 1e-3, seed=17)
+    sg = np.linalg.svd(G, compute_uv=False)
+    errs = []
+    for seed in range(20):
+        P, sig, sw = orc.rsvd_update(G, r, p, q, seed=seed)
+        assert np.all(sig <= sg[:r] * (1 + 1e-12))
+        assert np.abs(P.T @ P - np.eye(r)).max() < 1e-12
+        idx = np.argmax(np.abs(P), axis=0)
+        assert np.all(P[idx, np.arange(r)] > 0)
+        errs.append(np.linalg.norm(G - P @ (P.T @ G), 2))
+    kk = r
+    pp = p
+    tail = sg[kk:]
+    e = np.e
+    bound = ((1 + np.sqrt(kk / (pp - 1))) * sg[kk] ** (2 * q + 1)
+             + e * np.sqrt(kk + pp) / pp * np.sqrt(np.sum(tail ** (2 * (2 * q + 1))))) ** (1.0 / (2 * q + 1))
+    assert np.mean(errs) <= sg[r] + 2.0 * bound
+    assert np.mean(errs) >= sg[r] * (1 - 1e-9)            # Eckart-Young lower bound
+
+
+def test_rsvd_orientation(orc):
+    """m > n uses the right singular vectors (rule of paper §3 / Alg. 1 applied to G^T)."""
+    rng = np.random.default_rng(21)
+    s = 2.0 * 0.6 ** np.arange(40)
+    G = gi.planted_gradient(90, 40, s, 0.0, seed=4, rank=9)     # rank <= k: exact
+    P1, s1, _ = orc.rsvd_update(G, 6, 4, 2, seed=8)
+    P2, s2, _ = orc.rsvd_update(G.T.copy(), 6, 4, 2, seed=8)
+    assert np.array_equal(P1, P2) and np.array_equal(s1, s2)
+    u, ss, vt = np.linalg.svd(G)
+    assert proj_dist(P1, vt.T[:, :6]) < 1e-9
+    assert P1.shape == (40, 6)
+
+
+def test_rsvd_planted_spectrum_weyl(orc):
+    """c1-shaped case with noise: |sigma_i(G) - s_i| <= ||E||_2 (Weyl), and the
+    rSVD values never exceed sigma_i(G)."""
+    m, n = 256, 688
+    s = gi.spectrum_geometric_cut(m)
+    rng = np.random.default_rng(1)
+    Ghaar = gi.planted_gradient(m, n, s, 0.0, seed=2)
+    E = 1e-3 * rng.standard_normal((m, n))
+    G = Ghaar + E
+    P, sig, sw = orc.rsvd_update(G, 32, 8, 2, seed=20250429)
+    sg = np.linalg.svd(G, compute_uv=False)
+    e2 = np.linalg.norm(E, 2)
+    assert np.all(np.abs(sg[:32] - s[:32]) <= e2 * (1 + 1e-9))
+    assert np.all(sig <= sg[:32] * (1 + 1e-12))
+    assert np.abs(sig - sg[:32]).max() < 5e-3 * sg[0]
+    # residual of the rank-32 projection: Eckart-Young floor sigma_33 and a small excess
+    res = np.linalg.norm(G - P @ (P.T @ G), 2)
+    assert sg[32] * (1 - 1e-9) <= res <= 1.5 * sg[32]
+
+
+# ---------------------------------------------------------------- per-step path
+
+
+def test_adam_first_step_closed_form(orc):
+    """t = 1 from zero moments: bias correction cancels (1-b1) and (1-b2), so
+    N = R / (|R| + eps) exactly (paper Alg. 1)."""
+    rng = np.random.default_rng(0)
+    R = rng.standard_normal((3, 7)) * 1e-3
+    b1, b2, eps = float(np.float32(0.9)), float(np.float32(0.999)), float(np.float32(1e-8))
+    M, V, N = orc.adam(R, np.zeros_like(R), np.zeros_like(R), b1, b2, eps, 1)
+    assert np.allclose(M, (1 - b1) * R, rtol=1e-15, atol=0)
+    assert np.allclose(V, (1 - b2) * R * R, rtol=1e-15, atol=0)
+    assert np.allclose(N, R / (np.abs(R) + eps), rtol=1e-13, atol=0)
+
+
+def test_galore_two_steps_2x3(orc):
+    """Hand-derivable 2x3 example: G1 = [[3,0,-4],[0,1,0]], r = 1, p = 1 (so the
+    sketch is exact): sigma = 5, P = e1; two projected Adam steps."""
+    b1, b2, eps, lr, al = 0.9, 0.999, 1e-8, 1e-3, 0.25
+    G1 = np.array([[3.0, 0.0, -4.0], [0.0, 1.0, 0.0]])
+    W0 = np.array([[0.01, -0.02, 0.03], [0.04, 0.05, -0.06]])
+    P, sig, _ = orc.rsvd_update(G1, 1, 1, 2, seed=3)
+    assert abs(sig[0] - 5.0) < 1e-14
+    assert np.allclose(P, [[1.0], [0.0]], atol=1e-15)
+    P = np.array([[1.0], [0.0]])
+    R = orc.project(P, G1)
+    assert np.array_equal(R, [[3.0, 0.0, -4.0]])
+    M, V, N = orc.adam(R, np.zeros_like(R), np.zeros_like(R), b1, b2, eps, 1)
+    assert np.allclose(N, [[3 / (3 + eps), 0.0, -4 / (4 + eps)]], rtol=1e-15)
+    W1 = orc.project_back(P, N, W0, lr, al)
+    assert np.allclose(W1[0], W0[0] - lr * al * N[0], rtol=0, atol=1e-18)
+    assert np.array_equal(W1[1], W0[1])
+    G2 = np.array([[1.0, 2.0, 0.0], [0.0, -1.0, 5.0]])
+    R2 = orc.project(P, G2)
+    assert np.array_equal(R2, [[1.0, 2.0, 0.0]])
+    M2, V2, N2 = orc.adam(R2, M, V, b1, b2, eps, 2)
+    # moments by hand: M = 0.9*0.1*R1 + 0.1*R2, V = 0.999*0.001*R1^2 + 0.001*R2^2
+    assert np.allclose(M2, [[0.37, 0.2, -0.36]], rtol=1e-14)
+    assert np.allclose(V2, [[0.009991, 0.004, 0.015984]], rtol=1e-13)
+    # bias corrections 1-0.81 = 0.19 and 1-0.998001 = 0.001999
+    want = (np.array([0.37, 0.2, -0.36]) / 0.19) / (np.sqrt(np.array([0.009991, 0.004, 0.015984]) / 0.001999) + eps)
+    assert np.allclose(N2[0], want, rtol=1e-12)
+
+
+def test_identity_projector_is_textbook_adam(orc):
+    """P = I (r = m) reduces GaLore-Adam to plain Adam with step size lr*alpha
+    (torch.optim.Adam on CPU fp64, weight_decay = 0)."""
+    import torch
+    rng = np.random.default_rng(4)
+    m, n = 5, 8
+    lr, al = 1e-2, 0.5
+    b1, b2, eps = float(np.float32(0.9)), float(np.float32(0.999)), float(np.float32(1e-8))
+    W0 = rng.standard_normal((m, n))
+    grads = [rng.standard_normal((m, n)) for _ in range(4)]
+    w = torch.tensor(W0.copy(), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([w], lr=lr * al, betas=(b1, b2), eps=eps, weight_decay=0.0)
+    P = np.eye(m)
+    W = W0.copy()
+    M = np.zeros((m, n))
+    V = np.zeros((m, n))
+    for t, g in enumerate(grads, start=1):
+        w.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        R = orc.project(P, g)
+        M, V, N = orc.adam(R, M, V, b1, b2, eps, t)
+        W = orc.project_back(P, N, W, lr, al)
+    assert np.abs(W - w.detach().numpy()).max() < 1e-14
+
+
+def test_adam_sign_and_permutation_equivariance(orc):
+    rng = np.random.default_rng(6)
+    Rs = [rng.standard_normal((4, 6)) for _ in range(3)]
+    def run(seq):
+        M = np.zeros((4, 6)); V = np.zeros((4, 6)); N = None
+        for t, R in enumerate(seq, start=1):
+            M, V, N = orc.adam(R, M, V, 0.9, 0.999, 1e-8, t)
+        return N
+    N = run(Rs)
+    assert np.array_equal(run([-R for R in Rs]), -N)
+    perm = rng.permutation(4)
+    assert np.array_equal(run([R[perm] for R in Rs]), N[perm])
+
+
+@pytest.mark.parametrize("m,n", [(7, 13), (13, 7), (9, 9)])
+def test_projection_and_back_projection(orc, m, n):
+    rng = np.random.default_rng(m * n)
+    s, l = min(m, n), max(m, n)
+    r = 4
+    G = rng.standard_normal((m, n))
+    P = np.linalg.qr(rng.standard_normal((s, r)))[0]
+    A = G if m <= n else G.T
+    R = orc.project(P, G)
+    assert np.abs(R - P.T @ A).max() < 1e-13
+    # P = I gives R = A
+    assert np.array_equal(orc.project(np.eye(s), G), A)
+    # G = P X (left) / G = (P X)^T (right) is recovered: P R = A
+    X = rng.standard_normal((r, l))
+    Gx = P @ X if m <= n else (P @ X).T
+    assert np.abs(P @ orc.project(P, Gx) - (P @ X)).max() < 1e-13
+    # linearity
+    G2 = rng.standard_normal((m, n))
+    assert np.abs(orc.project(P, 2 * G - 3 * G2) - (2 * orc.project(P, G) - 3 * orc.project(P, G2))).max() < 1e-12
+    N = rng.standard_normal((r, l))
+    W = rng.standard_normal((m, n))
+    Wn = orc.project_back(P, N, W, 1e-3, 0.25)
+    upd = P @ N if m <= n else (P @ N).T
+    assert np.abs(Wn - (W - 2.5e-4 * upd)).max() < 1e-15 * 10
+
+
+def test_memory_accounting():
+    """Paper §3: GaLore keeps mn + mr + 2nr numbers for an m x n layer (m <= n):
+    the weight, P (m x r) and the two moments (r x n); plus nr for R."""
+    m, n, r = 4096, 11008, 1024
+    s, l = min(m, n), max(m, n)
+    P_elems, MV_elems, R_elems = s * r, 2 * r * l, r * l
+    assert m * n + P_elems + MV_elems == m * n + m * r + 2 * n * r
+    assert R_elems == n * r
