@@ -1,0 +1,151 @@
+/*
+ * galore.h -- C ABI of the MI355X (gfx950) GaLore 2 gradient-subspace library.
+ *
+ * Paper: "GaLore 2: Large-Scale LLM Pre-Training by Gradient Low-Rank
+ * Projection" (Su, Gu, Xu, Tian, Zhao, 2025).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All matrix pointers are DEVICE pointers, row-major, owned by the caller.
+ *    The library never allocates or frees device memory and never
+ *    synchronises the device: work is enqueued on `stream` and every entry
+ *    point returns as soon as it is enqueued.
+ *  - G is the m x n gradient as produced by autograd (+grad). s = min(m, n) is
+ *    the projected side, l = max(m, n). A denotes G when m <= n and G^T when
+ *    m > n, so A is always s x l (paper §3: left singular vectors when m <= n,
+ *    right ones otherwise).
+ *  - Batching: `batch` matrices of identical shape sit at fixed element strides
+ *    (`stride_*`); matrix b of a batch is at base + b * stride.
+ *  - ld* is the leading dimension (row pitch, in elements) of a row-major
+ *    matrix and must be >= its row length.
+ *  - Status: every call validates its arguments on the host before enqueuing
+ *    anything and returns a galore_status_t (< 0 on error, nothing enqueued).
+ *    A launch failure reported by the HIP runtime returns GALORE_ERR_HIP.
+ *    NaN/Inf inputs are not checked: they propagate to the outputs.
+ */
+#ifndef GALORE_H_
+#define GALORE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GALORE_F32 = 0,   /* IEEE binary32                                  */
+    GALORE_BF16 = 1   /* bfloat16 storage, widened exactly to fp32       */
+} galore_dtype_t;
+
+typedef enum {
+    GALORE_OK = 0,
+    GALORE_ERR_INVALID_ARG = -1,  /* null pointer, bad scalar, bad dtype     */
+    GALORE_ERR_SHAPE = -2,        /* sizes, ranks or leading dims invalid    */
+    GALORE_ERR_WORKSPACE = -3,    /* workspace missing or too small          */
+    GALORE_ERR_HIP = -4           /* the HIP runtime reported a failure      */
+} galore_status_t;
+
+/* Human-readable name of a status code (static storage). */
+const char* galore_status_string(int status);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int galore_version(void);
+
+/*
+ * Gaussian sketch (randomized range finder of Halko, Martinsson & Tropp 2011,
+ * adopted by paper §4.1.2): writes the l x k fp32 matrix Omega (row-major,
+ * ld = k). Entry (i, j) draws Philox4x64-10 (Salmon et al. 2011) with key
+ * (seed, 0) and counter (j*l + i, sketch_index, 0, 0); the top 53 bits of
+ * output words 0 and 1 give u1 in (0,1] and u2 in [0,1), and the entry is the
+ * fp32 rounding of sqrt(-2 ln u1) cos(2 pi u2) computed in fp64 (Box-Muller).
+ * Exposed so that callers and tests can inspect the sketch the subspace
+ * update uses. Errors: omega NULL -> INVALID_ARG; l < 1 or k < 1 -> SHAPE.
+ */
+int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index,
+                  hipStream_t stream);
+
+/*
+ * Bytes of workspace galore_rsvd_update needs for `batch` m x n matrices with
+ * rank r and oversampling p. Returns 0 for invalid sizes.
+ */
+size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch);
+
+/*
+ * Subspace update (paper §3 and Alg. 1: P = top-r singular vectors of G on
+ * its shorter side; paper §4.1.2: computed by the randomized SVD of Halko et
+ * al. 2011 -- randomized subspace iteration followed by the direct SVD of the
+ * small projected matrix).
+ *
+ *   k = min(r + p, s); Omega (l x k) from (seed, sketch_index0 + b)
+ *   Y = A Omega; Q = orth(Y)
+ *   q times: Z = A^T Q; Z = orth(Z); Y = A Z; Q = orth(Y)
+ *   B = Q^T A (k x l); B = U_B Sigma V^T
+ *   P = Q U_B[:, :r] (s x r) with each column's largest-magnitude entry made
+ *   positive (sign convention, paper §4.1.3); sigma = Sigma[:r], descending.
+ *
+ * Inputs:  G (g_dtype, m x n, ld ldg, batch stride stride_g elements).
+ * Outputs: P (fp32, s x r, ld ldp >= r, stride stride_p);
+ *          sigma (fp32, r values per matrix at stride stride_sigma; may be NULL);
+ *          info (device int32[batch]; may be NULL): 0 = converged, > 0 = the
+ *          small SVD did not converge within its sweep limit (value = sweeps).
+ * Workspace: device buffer of at least galore_rsvd_workspace_size(...) bytes,
+ *          256-byte aligned; contents are scratch and may be reused afterwards.
+ * Errors:  NULL G/P/workspace -> INVALID_ARG; m,n,r < 1, r > s, p < 0, q < 0,
+ *          r + p > 4096 (largest supported sketch width), ldg < n, ldp < r,
+ *          batch < 1 -> SHAPE; workspace_bytes too small -> WORKSPACE.
+ */
+int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
+                       int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
+                       uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
+                       float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Projection R = P^T A (paper §3, R_t = P_t^T G_t; paper Alg. 1).
+ * P: fp32 s x r (ld ldp); G: g_dtype m x n (ld ldg); R: fp32 r x l (ld ldr).
+ * For m > n this is R = (G P)^T.
+ * Errors: NULL pointers -> INVALID_ARG; sizes/ld invalid, r > s -> SHAPE.
+ */
+int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
+                   int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
+                   int64_t ldr, int64_t stride_r, int32_t batch, hipStream_t stream);
+
+/*
+ * Low-rank Adam on the rows x cols projected state (paper §3 moment equations;
+ * paper Alg. 1 with its bias correction applied to temporaries, the stored
+ * moments staying uncorrected):
+ *   M <- beta1 M + (1 - beta1) R;  V <- beta2 V + (1 - beta2) R^2
+ *   N  = (M / (1 - beta1^t)) / (sqrt(V / (1 - beta2^t)) + eps)
+ * R, M, V, N: fp32, same shape, ld and batch stride. M and V are updated in
+ * place; N may alias R. t >= 1 is the step number (the bias terms are formed
+ * on the host in fp64 from the fp32 betas).
+ * Errors: NULL pointers -> INVALID_ARG; beta outside [0,1), eps <= 0, non-finite
+ * scalars, t < 1 -> INVALID_ARG; rows/cols < 1, ld < cols -> SHAPE.
+ */
+int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64_t rows,
+                             int64_t cols, int64_t ld, int64_t stride, int32_t batch, float beta1,
+                             float beta2, float eps, int64_t t, hipStream_t stream);
+
+/*
+ * Back-projection and weight update (paper §3: G~ = alpha P N, W <- W + eta G~;
+ * paper Alg. 1). The library works with the autograd gradient, so it applies
+ *   W <- W - (lr * alpha) * P N         (m <= n)
+ *   W <- W - (lr * alpha) * (P N)^T     (m > n)
+ * P: fp32 s x r (ld ldp); N: fp32 r x l (ld ldn); W: fp32 m x n (ld ldw),
+ * updated in place.
+ * Errors: NULL pointers -> INVALID_ARG; non-finite lr/alpha -> INVALID_ARG;
+ * sizes/ld invalid, r > s -> SHAPE.
+ */
+int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const float* N,
+                        int64_t ldn, int64_t stride_n, float* W, int64_t m, int64_t n,
+                        int64_t ldw, int64_t stride_w, int32_t r, float lr, float alpha,
+                        int32_t batch, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GALORE_H_ */

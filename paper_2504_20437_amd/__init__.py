@@ -1,0 +1,186 @@
+"""Python binding of the MI355X GaLore 2 hot-path library (``libgalore.so``).
+
+Argument marshalling only: every step runs in the HIP kernels behind the C ABI
+declared in ``include/galore.h``; torch tensors supply device memory and the
+current stream. There is no fallback: if the shared object is missing, importing
+the binding raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgalore.so")
+
+GALORE_F32 = 0
+GALORE_BF16 = 1
+GALORE_OK = 0
+
+EXPORTED = (
+    "galore_status_string", "galore_version", "galore_sketch", "galore_rsvd_workspace_size",
+    "galore_rsvd_update", "galore_project", "galore_lowrank_adam_step", "galore_project_back",
+)
+
+
+class GaloreError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s failed: %s (%d)" % (where, status_string(status), status))
+        self.status = status
+
+
+def _declare(lib):
+    vp, i64, i32, u64, f32, sz = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64,
+                                  ctypes.c_float, ctypes.c_size_t)
+    lib.galore_status_string.argtypes = [ctypes.c_int]
+    lib.galore_status_string.restype = ctypes.c_char_p
+    lib.galore_version.argtypes = []
+    lib.galore_version.restype = ctypes.c_int
+    lib.galore_sketch.argtypes = [vp, i64, i64, u64, u64, vp]
+    lib.galore_sketch.restype = ctypes.c_int
+    lib.galore_rsvd_workspace_size.argtypes = [i64, i64, i32, i32, i32]
+    lib.galore_rsvd_workspace_size.restype = sz
+    lib.galore_rsvd_update.argtypes = [vp, i32, i64, i64, i64, i64, i32, i32, i32, u64, u64,
+                                       vp, i64, i64, vp, i64, vp, i32, vp, sz, vp]
+    lib.galore_rsvd_update.restype = ctypes.c_int
+    lib.galore_project.argtypes = [vp, i64, i64, vp, i32, i64, i64, i64, i64, i32, vp, i64, i64,
+                                   i32, vp]
+    lib.galore_project.restype = ctypes.c_int
+    lib.galore_lowrank_adam_step.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, f32, f32, f32,
+                                             i64, vp]
+    lib.galore_lowrank_adam_step.restype = ctypes.c_int
+    lib.galore_project_back.argtypes = [vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i64, i32,
+                                        f32, f32, i32, vp]
+    lib.galore_project_back.restype = ctypes.c_int
+    return lib
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libgalore.so is not built (run __graft_entry__.build()); "
+                          "there is no fallback path")
+    return _declare(ctypes.CDLL(LIB_PATH))
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.galore_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != GALORE_OK:
+        raise GaloreError(status, where)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _mat(t: torch.Tensor, name: str):
+    """(ptr, rows, cols, ld, batch_stride, batch) of a 2-D or 3-D row-major tensor."""
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dim() == 2:
+        if t.stride(1) != 1:
+            raise ValueError("%s must be row-major" % name)
+        rows, cols = t.shape
+        return t.data_ptr(), rows, cols, t.stride(0), rows * t.stride(0), 1
+    if t.dim() == 3:
+        if t.stride(2) != 1:
+            raise ValueError("%s must be row-major" % name)
+        b, rows, cols = t.shape
+        return t.data_ptr(), rows, cols, t.stride(1), t.stride(0), b
+    raise ValueError("%s must be 2-D or 3-D" % name)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return GALORE_F32
+    if t.dtype == torch.bfloat16:
+        return GALORE_BF16
+    raise ValueError("gradient dtype must be float32 or bfloat16")
+
+
+def galore_version() -> int:
+    return lib.galore_version()
+
+
+def galore_sketch(l: int, k: int, seed: int, sketch_index: int = 0, out=None, stream=None, device="cuda"):
+    """Omega (l x k, fp32) as the subspace update draws it."""
+    if out is None:
+        out = torch.empty((l, k), dtype=torch.float32, device=device)
+    _check(lib.galore_sketch(out.data_ptr(), l, k, seed, sketch_index, _stream(stream)), "galore_sketch")
+    return out
+
+
+def galore_rsvd_workspace_size(m: int, n: int, r: int, p: int, batch: int = 1) -> int:
+    return int(lib.galore_rsvd_workspace_size(m, n, r, p, batch))
+
+
+def galore_rsvd_update(G: torch.Tensor, r: int, p: int, q: int, seed: int, sketch_index0: int = 0,
+                       P=None, sigma=None, info=None, workspace=None, stream=None):
+    """Subspace update of G ((m, n) or (batch, m, n)); returns (P, sigma, info)."""
+    gp, m, n, ldg, sg, batch = _mat(G, "G")
+    s = min(m, n)
+    dev = G.device
+    if P is None:
+        P = torch.empty((batch, s, r) if G.dim() == 3 else (s, r), dtype=torch.float32, device=dev)
+    pp, prow, pcol, ldp, sp, pb = _mat(P, "P")
+    if sigma is None:
+        sigma = torch.empty((batch, r) if G.dim() == 3 else (r,), dtype=torch.float32, device=dev)
+    if info is None:
+        info = torch.empty((batch,), dtype=torch.int32, device=dev)
+    need = galore_rsvd_workspace_size(m, n, r, p, batch)
+    if workspace is None:
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
+    st = lib.galore_rsvd_update(gp, _dtype_code(G), m, n, ldg, sg, r, p, q, seed, sketch_index0,
+                                pp, ldp, sp, sigma.data_ptr(), sigma.stride(0) if sigma.dim() == 2 else r,
+                                info.data_ptr(), batch, workspace.data_ptr(), workspace.numel(),
+                                _stream(stream))
+    _check(st, "galore_rsvd_update")
+    return P, sigma, info
+
+
+def galore_project(P: torch.Tensor, G: torch.Tensor, R=None, stream=None):
+    """R = P^T A ((r, l) or (batch, r, l))."""
+    pp, s, r, ldp, sp, pb = _mat(P, "P")
+    gp, m, n, ldg, sg, batch = _mat(G, "G")
+    l = max(m, n)
+    if R is None:
+        R = torch.empty((batch, r, l) if G.dim() == 3 else (r, l), dtype=torch.float32, device=G.device)
+    rp, _, _, ldr, sr, _ = _mat(R, "R")
+    _check(lib.galore_project(pp, ldp, sp, gp, _dtype_code(G), m, n, ldg, sg, r, rp, ldr, sr, batch,
+                              _stream(stream)), "galore_project")
+    return R
+
+
+def galore_lowrank_adam_step(R: torch.Tensor, M: torch.Tensor, V: torch.Tensor, N=None, beta1=0.9,
+                             beta2=0.999, eps=1e-8, t=1, stream=None):
+    """In-place M, V; returns N (may be R itself for an in-place update)."""
+    if N is None:
+        N = torch.empty_like(R)
+    rp, rows, cols, ld, st_, batch = _mat(R, "R")
+    for x, nm in ((M, "M"), (V, "V"), (N, "N")):
+        if x.shape != R.shape or x.stride() != R.stride() or x.dtype != torch.float32:
+            raise ValueError("%s must match R in shape, strides and dtype" % nm)
+    _check(lib.galore_lowrank_adam_step(rp, M.data_ptr(), V.data_ptr(), N.data_ptr(), rows, cols, ld,
+                                        st_, batch, beta1, beta2, eps, t, _stream(stream)),
+           "galore_lowrank_adam_step")
+    return N
+
+
+def galore_project_back(P: torch.Tensor, N: torch.Tensor, W: torch.Tensor, lr: float, alpha: float,
+                        stream=None):
+    """W <- W - lr*alpha*(P N) (m <= n) or its transpose (m > n), in place."""
+    pp, s, r, ldp, sp, _ = _mat(P, "P")
+    np_, _, _, ldn, sn, _ = _mat(N, "N")
+    wp, m, n, ldw, sw, batch = _mat(W, "W")
+    _check(lib.galore_project_back(pp, ldp, sp, np_, ldn, sn, wp, m, n, ldw, sw, r, lr, alpha, batch,
+                                   _stream(stream)), "galore_project_back")
+    return W

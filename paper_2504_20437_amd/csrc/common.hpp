@@ -1,0 +1,84 @@
+// Internal helpers shared by the gfx950 kernels of the GaLore 2 library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace galore {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+struct bf16_t {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16_t x) {
+    return __uint_as_float(static_cast<uint32_t>(x.bits) << 16);
+}
+
+// Operand layouts of the GEMM kernels.
+//   A operand (M x K): kKContig -> A[i*lda + kk]   kMContig -> A[kk*lda + i]
+//   B operand (K x N): kNContig -> B[kk*ldb + j]   kKContigB -> B[j*ldb + kk]
+enum class ALayout { kKContig, kMContig };
+enum class BLayout { kNContig, kKContig };
+
+struct GemmArgs {
+    const void* A;
+    int64_t lda, strideA;
+    const void* B;
+    int64_t ldb, strideB;
+    float* C;
+    int64_t ldc, strideC;
+    int M, N, K;
+    float alpha, beta;   // C = alpha * op(A) op(B) + beta * C  (beta == 0: C not read)
+};
+
+struct Gram64Args {
+    const float* X;      // rows x cols, row-major
+    int64_t ldx, strideX;
+    double* C;           // cols x cols, row-major, ld = cols
+    int64_t strideC;
+    int rows, cols;
+};
+
+// Launchers (defined in the .hip files). All return hipError_t of the launch.
+hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const GemmArgs& g, int batch,
+                       hipStream_t stream);
+hipError_t launch_gram64(const Gram64Args& g, int batch, hipStream_t stream);
+
+hipError_t launch_sketch(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
+                         uint64_t sketch_index0, int batch, hipStream_t stream);
+
+// Cholesky of the k x k fp64 Gram (in place, upper factor R in the upper
+// triangle). If rinv32 != nullptr, also writes the fp32 inverse of R' (R with
+// rank-deficient rows replaced by unit rows) into rinv32 (k x k), using xinv
+// (k x k fp64) as scratch. defic[b*k + j] = 1 marks deficient pivots.
+hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, double* xinv,
+                           int64_t strideInv, int* defic, double tau_rel, int batch,
+                           hipStream_t stream);
+// Replace columns flagged deficient by a deterministic generic unit vector.
+hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, const int* defic,
+                                 int batch, hipStream_t stream);
+// Xt (k x k, transposed storage) = R^T in fp32 from the fp64 factor; Vt = I.
+hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Xt, float* Vt,
+                                 int64_t strideX, int* rot, int max_sweeps, int batch,
+                                 hipStream_t stream);
+hipError_t launch_jacobi_step(float* Xt, float* Vt, int k, int64_t strideX, int nblocks, int step,
+                              int sweep, int* rot, int max_sweeps, double tol, int batch,
+                              hipStream_t stream);
+hipError_t launch_jacobi_finalize(const float* Xt, const float* Vt, int k, int64_t strideX,
+                                  int r, float* Ur, int64_t strideUr, float* sigma,
+                                  int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
+                                  int batch, hipStream_t stream);
+hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strideP, int batch,
+                           hipStream_t stream);
+hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t rows, int64_t cols,
+                       int64_t ld, int64_t stride, int batch, float beta1, float beta2, float eps,
+                       float bc1, float bc2, hipStream_t stream);
+
+constexpr int kJacobiBlock = 16;     // columns per Jacobi block (pairs of 32)
+
+}  // namespace galore

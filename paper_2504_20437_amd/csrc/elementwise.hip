@@ -1,0 +1,165 @@
+// Memory-bound kernels of the hot path.
+//
+//  * sign_fix: canonical sign of each projector column (paper §4.1.3 and its
+//    footnote: singular vectors are defined up to sign; the entry of largest
+//    magnitude, lowest row on exact ties, is made positive).
+//  * lowrank_adam: the low-rank Adam update (paper §3 moment equations and the
+//    bias correction of paper Alg. 1) streaming R, M, V in and M, V, N out:
+//    24 bytes per element, one pass over HBM, 16-byte vector accesses.
+#include "common.hpp"
+
+namespace galore {
+namespace {
+
+constexpr int SF_COLS = 64;
+constexpr int SF_GROUPS = 4;
+
+__global__ __launch_bounds__(SF_COLS* SF_GROUPS) void sign_fix_kernel(float* Pb, int rows, int r,
+                                                                      int64_t ldp, int64_t strideP) {
+    const int b = blockIdx.y;
+    float* P = Pb + static_cast<int64_t>(b) * strideP;
+    const int tc = threadIdx.x & (SF_COLS - 1);
+    const int grp = threadIdx.x / SF_COLS;
+    const int c = blockIdx.x * SF_COLS + tc;
+    __shared__ float best_abs[SF_GROUPS][SF_COLS];
+    __shared__ int best_row[SF_GROUPS][SF_COLS];
+    __shared__ float flip[SF_COLS];
+    float ba = -1.0f;
+    int br = 0x7fffffff;
+    if (c < r) {
+        for (int i = grp; i < rows; i += SF_GROUPS) {
+            const float a = fabsf(P[static_cast<int64_t>(i) * ldp + c]);
+            if (a > ba) { ba = a; br = i; }          // rows visited in increasing order
+        }
+    }
+    best_abs[grp][tc] = ba;
+    best_row[grp][tc] = br;
+    __syncthreads();
+    if (grp == 0) {
+        float a = best_abs[0][tc];
+        int rr = best_row[0][tc];
+        for (int g = 1; g < SF_GROUPS; ++g) {
+            const float a2 = best_abs[g][tc];
+            const int r2 = best_row[g][tc];
+            if (a2 > a || (a2 == a && r2 < rr)) { a = a2; rr = r2; }
+        }
+        float f = 1.0f;
+        if (c < r && rr < rows && P[static_cast<int64_t>(rr) * ldp + c] < 0.0f) f = -1.0f;
+        flip[tc] = f;
+    }
+    __syncthreads();
+    if (c < r && flip[tc] < 0.0f) {
+        for (int i = grp; i < rows; i += SF_GROUPS) {
+            float* q = P + static_cast<int64_t>(i) * ldp + c;
+            *q = -*q;
+        }
+    }
+}
+
+__device__ __forceinline__ void adam_elem(float g, float& m, float& v, float& n, float beta1,
+                                          float beta2, float om1, float om2, float bc1, float bc2,
+                                          float eps) {
+    m = beta1 * m + om1 * g;
+    v = beta2 * v + om2 * (g * g);
+    const float mhat = m / bc1;
+    const float vhat = v / bc2;
+    n = mhat / (sqrtf(vhat) + eps);
+}
+
+// Contiguous state: flat index over batch * rows * cols, 16-byte vectors.
+__global__ __launch_bounds__(256) void adam_flat_kernel(const float* R, float* M, float* V, float* N,
+                                                       int64_t total, float beta1, float beta2,
+                                                       float eps, float bc1, float bc2) {
+    const float om1 = 1.0f - beta1;
+    const float om2 = 1.0f - beta2;
+    const int64_t nvec = total / 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    const f32x4* R4 = reinterpret_cast<const f32x4*>(R);
+    f32x4* M4 = reinterpret_cast<f32x4*>(M);
+    f32x4* V4 = reinterpret_cast<f32x4*>(V);
+    f32x4* N4 = reinterpret_cast<f32x4*>(N);
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < nvec; i += stride) {
+        const f32x4 g = __builtin_nontemporal_load(R4 + i);
+        f32x4 m = __builtin_nontemporal_load(M4 + i);
+        f32x4 v = __builtin_nontemporal_load(V4 + i);
+        f32x4 n;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            float me = m[e], ve = v[e], ne;
+            adam_elem(g[e], me, ve, ne, beta1, beta2, om1, om2, bc1, bc2, eps);
+            m[e] = me;
+            v[e] = ve;
+            n[e] = ne;
+        }
+        __builtin_nontemporal_store(m, M4 + i);
+        __builtin_nontemporal_store(v, V4 + i);
+        __builtin_nontemporal_store(n, N4 + i);
+    }
+    // tail (total % 4 elements)
+    const int64_t tail0 = nvec * 4;
+    const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (gid < total - tail0) {
+        const int64_t i = tail0 + gid;
+        float m = M[i], v = V[i], n;
+        adam_elem(R[i], m, v, n, beta1, beta2, om1, om2, bc1, bc2, eps);
+        M[i] = m;
+        V[i] = v;
+        N[i] = n;
+    }
+}
+
+// Strided state (ld > cols or padded batch stride).
+__global__ __launch_bounds__(256) void adam_strided_kernel(const float* R, float* M, float* V, float* N,
+                                                          int64_t rows, int64_t cols, int64_t ld,
+                                                          int64_t stride, float beta1, float beta2,
+                                                          float eps, float bc1, float bc2) {
+    const float om1 = 1.0f - beta1;
+    const float om2 = 1.0f - beta2;
+    const int64_t b = blockIdx.y;
+    const int64_t per = rows * cols;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < per;
+         e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t i = e / cols;
+        const int64_t j = e - i * cols;
+        const int64_t off = b * stride + i * ld + j;
+        float m = M[off], v = V[off], n;
+        adam_elem(R[off], m, v, n, beta1, beta2, om1, om2, bc1, bc2, eps);
+        M[off] = m;
+        V[off] = v;
+        N[off] = n;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strideP, int batch,
+                           hipStream_t stream) {
+    dim3 grid((r + SF_COLS - 1) / SF_COLS, batch);
+    hipLaunchKernelGGL(sign_fix_kernel, grid, dim3(SF_COLS * SF_GROUPS), 0, stream, P, rows, r, ldp,
+                       strideP);
+    return hipGetLastError();
+}
+
+hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t rows, int64_t cols,
+                       int64_t ld, int64_t stride, int batch, float beta1, float beta2, float eps,
+                       float bc1, float bc2, hipStream_t stream) {
+    const bool contiguous = (ld == cols) && (stride == rows * cols);
+    const bool aligned = ((reinterpret_cast<uintptr_t>(R) | reinterpret_cast<uintptr_t>(M) |
+                           reinterpret_cast<uintptr_t>(V) | reinterpret_cast<uintptr_t>(N)) & 15) == 0;
+    if (contiguous && aligned) {
+        const int64_t total = rows * cols * batch;
+        int64_t blocks = (total / 4 + 255) / 256;
+        if (blocks < 1) blocks = 1;
+        if (blocks > 65536) blocks = 65536;
+        hipLaunchKernelGGL(adam_flat_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
+                           R, M, V, N, total, beta1, beta2, eps, bc1, bc2);
+    } else {
+        int64_t blocks = (rows * cols + 255) / 256;
+        if (blocks > 8192) blocks = 8192;
+        hipLaunchKernelGGL(adam_strided_kernel, dim3(static_cast<unsigned>(blocks), batch), dim3(256),
+                           0, stream, R, M, V, N, rows, cols, ld, stride, beta1, beta2, eps, bc1, bc2);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace galore

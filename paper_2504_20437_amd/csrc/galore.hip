@@ -1,0 +1,430 @@
+// Host side of the GaLore 2 library: argument validation, workspace carving and
+// the launch sequence of each C-ABI entry point. Everything is enqueued on the
+// caller's stream; nothing here allocates device memory or synchronises.
+#include <math.h>
+#include <string.h>
+
+#include "../../include/galore.h"
+#include "common.hpp"
+
+using namespace galore;
+
+namespace {
+
+constexpr int kMaxK = 4096;          // largest sketch width supported by the small-SVD kernels
+constexpr int kMaxSweeps = 24;       // Jacobi sweep limit of the small SVD
+constexpr double kJacobiTol = 1e-6;  // relative off-diagonal below which a pair is orthogonal
+constexpr double kDeficTol = 1e-10;  // relative pivot below which a column is dependent
+constexpr size_t kAlign = 256;
+
+#define GALORE_TRY(expr)                                   \
+    do {                                                   \
+        hipError_t e_ = (expr);                            \
+        if (e_ != hipSuccess) return GALORE_ERR_HIP;       \
+    } while (0)
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+int64_t pad_elems(int64_t n) { return (n + 63) / 64 * 64; }   // per-matrix stride, 256-B multiple
+
+struct Shape {
+    int64_t m, n, s, l;
+    int k;
+    bool left;   // m <= n: A = G; otherwise A = G^T
+};
+
+Shape make_shape(int64_t m, int64_t n, int r, int p) {
+    Shape sh;
+    sh.m = m;
+    sh.n = n;
+    sh.left = (m <= n);
+    sh.s = sh.left ? m : n;
+    sh.l = sh.left ? n : m;
+    int64_t k = static_cast<int64_t>(r) + p;
+    if (k > sh.s) k = sh.s;
+    sh.k = static_cast<int>(k);
+    return sh;
+}
+
+// Workspace regions, each holding `batch` matrices at a fixed element stride.
+struct Layout {
+    int64_t strideL, strideS, strideKK, strideUr;
+    size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offXt, offVt, offUr, offDef, offRot;
+    size_t total;
+};
+
+Layout make_layout(const Shape& sh, int r, int batch) {
+    Layout L;
+    const int64_t k = sh.k;
+    L.strideL = pad_elems(sh.l * k);
+    L.strideS = pad_elems(sh.s * k);
+    L.strideKK = pad_elems(k * k);
+    L.strideUr = pad_elems(k * r);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align_up(off + bytes, kAlign);
+        return o;
+    };
+    const size_t B = static_cast<size_t>(batch);
+    L.offL1 = take(B * L.strideL * sizeof(float));
+    L.offL2 = take(B * L.strideL * sizeof(float));
+    L.offS1 = take(B * L.strideS * sizeof(float));
+    L.offS2 = take(B * L.strideS * sizeof(float));
+    L.offC = take(B * L.strideKK * sizeof(double));
+    L.offXinv = take(B * L.strideKK * sizeof(double));
+    L.offRinv = take(B * L.strideKK * sizeof(float));
+    L.offXt = take(B * L.strideKK * sizeof(float));
+    L.offVt = take(B * L.strideKK * sizeof(float));
+    L.offUr = take(B * L.strideUr * sizeof(float));
+    L.offDef = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(int));
+    L.offRot = take(B * kMaxSweeps * sizeof(int));
+    L.total = off;
+    return L;
+}
+
+bool finite_f(float x) { return isfinite(x) != 0; }
+
+// The gradient operand of a GEMM: G itself or its transpose, in its storage dtype.
+struct GradOp {
+    const void* G;
+    bool bf16;
+    int64_t ldg, stride;
+};
+
+// Y (s x k, ld k) = A X, X (l x k, ld k)
+hipError_t gemm_A_times(const Shape& sh, const GradOp& g, const float* X, int64_t strideX, float* Y,
+                        int64_t strideY, int batch, hipStream_t st) {
+    GemmArgs a{};
+    a.A = g.G;
+    a.lda = g.ldg;
+    a.strideA = g.stride;
+    a.B = X;
+    a.ldb = sh.k;
+    a.strideB = strideX;
+    a.C = Y;
+    a.ldc = sh.k;
+    a.strideC = strideY;
+    a.M = static_cast<int>(sh.s);
+    a.N = sh.k;
+    a.K = static_cast<int>(sh.l);
+    a.alpha = 1.0f;
+    a.beta = 0.0f;
+    // left: A = G (s x l, K contiguous); right: A(i, kk) = G[kk][i] (M contiguous)
+    return launch_gemm(sh.left ? ALayout::kKContig : ALayout::kMContig, BLayout::kNContig, g.bf16,
+                       false, a, batch, st);
+}
+
+// Z (l x k, ld k) = A^T Q, Q (s x k, ld k)
+hipError_t gemm_At_times(const Shape& sh, const GradOp& g, const float* Q, int64_t strideQ, float* Z,
+                         int64_t strideZ, int batch, hipStream_t st) {
+    GemmArgs a{};
+    a.A = g.G;
+    a.lda = g.ldg;
+    a.strideA = g.stride;
+    a.B = Q;
+    a.ldb = sh.k;
+    a.strideB = strideQ;
+    a.C = Z;
+    a.ldc = sh.k;
+    a.strideC = strideZ;
+    a.M = static_cast<int>(sh.l);
+    a.N = sh.k;
+    a.K = static_cast<int>(sh.s);
+    a.alpha = 1.0f;
+    a.beta = 0.0f;
+    // left: A^T(i, kk) = G[kk][i] (M contiguous); right: A^T = G (K contiguous)
+    return launch_gemm(sh.left ? ALayout::kMContig : ALayout::kKContig, BLayout::kNContig, g.bf16,
+                       false, a, batch, st);
+}
+
+// Out (rows x k) = In (rows x k) * Rinv (k x k)
+hipError_t gemm_right_tri(const float* In, float* Out, int64_t stride, int rows, int k,
+                          const float* Rinv, int64_t strideKK, int batch, hipStream_t st) {
+    GemmArgs a{};
+    a.A = In;
+    a.lda = k;
+    a.strideA = stride;
+    a.B = Rinv;
+    a.ldb = k;
+    a.strideB = strideKK;
+    a.C = Out;
+    a.ldc = k;
+    a.strideC = stride;
+    a.M = rows;
+    a.N = k;
+    a.K = k;
+    a.alpha = 1.0f;
+    a.beta = 0.0f;
+    return launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, st);
+}
+
+struct Work {
+    const Layout* L;
+    char* base;
+    float* f(size_t off) const { return reinterpret_cast<float*>(base + off); }
+    double* d(size_t off) const { return reinterpret_cast<double*>(base + off); }
+    int* i(size_t off) const { return reinterpret_cast<int*>(base + off); }
+};
+
+// One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In (fp64 Gram and factor);
+// columns found dependent are replaced by generic unit vectors.
+hipError_t orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k,
+                     int batch, hipStream_t st) {
+    const Layout& L = *w.L;
+    Gram64Args gg{};
+    gg.X = In;
+    gg.ldx = k;
+    gg.strideX = stride;
+    gg.C = w.d(L.offC);
+    gg.strideC = L.strideKK;
+    gg.rows = rows;
+    gg.cols = k;
+    hipError_t e = launch_gram64(gg, batch, st);
+    if (e != hipSuccess) return e;
+    e = launch_cholesky(w.d(L.offC), k, L.strideKK, w.f(L.offRinv), w.d(L.offXinv), L.strideKK,
+                        w.i(L.offDef), kDeficTol, batch, st);
+    if (e != hipSuccess) return e;
+    e = gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st);
+    if (e != hipSuccess) return e;
+    return launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* galore_status_string(int status) {
+    switch (status) {
+        case GALORE_OK: return "GALORE_OK";
+        case GALORE_ERR_INVALID_ARG: return "GALORE_ERR_INVALID_ARG";
+        case GALORE_ERR_SHAPE: return "GALORE_ERR_SHAPE";
+        case GALORE_ERR_WORKSPACE: return "GALORE_ERR_WORKSPACE";
+        case GALORE_ERR_HIP: return "GALORE_ERR_HIP";
+        default: return "GALORE_UNKNOWN_STATUS";
+    }
+}
+
+int galore_version(void) { return 100; }
+
+int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index,
+                  hipStream_t stream) {
+    if (omega == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (l < 1 || k < 1) return GALORE_ERR_SHAPE;
+    GALORE_TRY(launch_sketch(omega, l, k, l * k, seed, sketch_index, 1, stream));
+    return GALORE_OK;
+}
+
+size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch) {
+    if (m < 1 || n < 1 || r < 1 || p < 0 || batch < 1) return 0;
+    const Shape sh = make_shape(m, n, r, p);
+    if (r > sh.s || sh.k > kMaxK) return 0;
+    return make_layout(sh, r, batch).total;
+}
+
+int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
+                       int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
+                       uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
+                       float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (G == nullptr || P == nullptr || workspace == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1) return GALORE_ERR_SHAPE;
+    if (m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, p);
+    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK) return GALORE_ERR_SHAPE;
+    if (ldg < n || ldp < r) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_g < m * ldg || stride_p < sh.s * ldp)) return GALORE_ERR_SHAPE;
+    if (sigma != nullptr && batch > 1 && stride_sigma < r) return GALORE_ERR_SHAPE;
+    const Layout L = make_layout(sh, r, batch);
+    if (workspace_bytes < L.total) return GALORE_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return GALORE_ERR_WORKSPACE;
+
+    Work w{&L, static_cast<char*>(workspace)};
+    const GradOp gop{G, g_dtype == GALORE_BF16, ldg, stride_g};
+    const int k = sh.k;
+    const int s = static_cast<int>(sh.s);
+    const int l = static_cast<int>(sh.l);
+    float* L1 = w.f(L.offL1);
+    float* L2 = w.f(L.offL2);
+    float* Sa = w.f(L.offS1);
+    float* Sb = w.f(L.offS2);
+
+    // a1-a3: sketch, range sample, orthonormalise
+    GALORE_TRY(launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
+    GALORE_TRY(gemm_A_times(sh, gop, L1, L.strideL, Sa, L.strideS, batch, stream));
+    float* Q = Sa;
+    float* Qtmp = Sb;
+    auto orth_s = [&](int passes) -> hipError_t {
+        for (int ps = 0; ps < passes; ++ps) {
+            hipError_t e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream);
+            if (e != hipSuccess) return e;
+            float* t = Q;
+            Q = Qtmp;
+            Qtmp = t;
+        }
+        return hipSuccess;
+    };
+    GALORE_TRY(orth_s(q == 0 ? 2 : 1));
+    // a4: power iterations with re-orthonormalisation after every product
+    for (int it = 0; it < q; ++it) {
+        GALORE_TRY(gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
+        GALORE_TRY(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream));
+        GALORE_TRY(gemm_A_times(sh, gop, L2, L.strideL, Qtmp, L.strideS, batch, stream));
+        {
+            float* t = Q;
+            Q = Qtmp;
+            Qtmp = t;
+        }
+        GALORE_TRY(orth_s(it == q - 1 ? 2 : 1));
+    }
+    // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
+    GALORE_TRY(gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
+    {
+        Gram64Args gg{};
+        gg.X = L1;
+        gg.ldx = k;
+        gg.strideX = L.strideL;
+        gg.C = w.d(L.offC);
+        gg.strideC = L.strideKK;
+        gg.rows = l;
+        gg.cols = k;
+        GALORE_TRY(launch_gram64(gg, batch, stream));
+        GALORE_TRY(launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, nullptr, L.strideKK,
+                                   w.i(L.offDef), kDeficTol, batch, stream));
+    }
+    // a6: one-sided Jacobi on R: R V = U Sigma, V = left singular vectors of B
+    float* Xt = w.f(L.offXt);
+    float* Vt = w.f(L.offVt);
+    int* rot = w.i(L.offRot);
+    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Xt, Vt, L.strideKK, rot,
+                                     kMaxSweeps, batch, stream));
+    const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
+    const int nb = nblk_real + (nblk_real & 1);
+    if (nb >= 2) {
+        for (int sw = 0; sw < kMaxSweeps; ++sw)
+            for (int stp = 0; stp < nb - 1; ++stp)
+                GALORE_TRY(launch_jacobi_step(Xt, Vt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps,
+                                              kJacobiTol, batch, stream));
+    }
+    float* Ur = w.f(L.offUr);
+    GALORE_TRY(launch_jacobi_finalize(Xt, Vt, k, L.strideKK, r, Ur, L.strideUr, sigma,
+                                      stride_sigma, rot, kMaxSweeps, info, batch, stream));
+    // a7: P = Q U_B[:, :r], canonical signs
+    {
+        GemmArgs a{};
+        a.A = Q;
+        a.lda = k;
+        a.strideA = L.strideS;
+        a.B = Ur;
+        a.ldb = r;
+        a.strideB = L.strideUr;
+        a.C = P;
+        a.ldc = ldp;
+        a.strideC = stride_p;
+        a.M = s;
+        a.N = r;
+        a.K = k;
+        a.alpha = 1.0f;
+        a.beta = 0.0f;
+        GALORE_TRY(launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, stream));
+    }
+    GALORE_TRY(launch_sign_fix(P, s, r, ldp, stride_p, batch, stream));
+    return GALORE_OK;
+}
+
+int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
+                   int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
+                   int64_t ldr, int64_t stride_r, int32_t batch, hipStream_t stream) {
+    if (P == nullptr || G == nullptr || R == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s || ldp < r || ldg < n || ldr < sh.l) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_p < sh.s * ldp || stride_g < m * ldg || stride_r < r * ldr))
+        return GALORE_ERR_SHAPE;
+    GemmArgs a{};
+    // R (r x l) = P^T A : A-operand P^T (P[kk][i], M contiguous), B-operand A
+    a.A = P;
+    a.lda = ldp;
+    a.strideA = stride_p;
+    a.B = G;
+    a.ldb = ldg;
+    a.strideB = stride_g;
+    a.C = R;
+    a.ldc = ldr;
+    a.strideC = stride_r;
+    a.M = r;
+    a.N = static_cast<int>(sh.l);
+    a.K = static_cast<int>(sh.s);
+    a.alpha = 1.0f;
+    a.beta = 0.0f;
+    // left: A = G (K x N rows, N contiguous); right: A(kk, j) = G[j][kk] (K contiguous)
+    GALORE_TRY(launch_gemm(ALayout::kMContig, sh.left ? BLayout::kNContig : BLayout::kKContig, false,
+                           g_dtype == GALORE_BF16, a, batch, stream));
+    return GALORE_OK;
+}
+
+int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64_t rows,
+                             int64_t cols, int64_t ld, int64_t stride, int32_t batch, float beta1,
+                             float beta2, float eps, int64_t t, hipStream_t stream) {
+    if (R == nullptr || M == nullptr || V == nullptr || N == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (!finite_f(beta1) || !finite_f(beta2) || !finite_f(eps)) return GALORE_ERR_INVALID_ARG;
+    if (beta1 < 0.0f || beta1 >= 1.0f || beta2 < 0.0f || beta2 >= 1.0f || eps <= 0.0f || t < 1)
+        return GALORE_ERR_INVALID_ARG;
+    if (rows < 1 || cols < 1 || ld < cols || batch < 1) return GALORE_ERR_SHAPE;
+    if (batch > 1 && stride < rows * ld) return GALORE_ERR_SHAPE;
+    // bias terms in fp64 from the fp32 betas, rounded once to fp32
+    const double bc1 = 1.0 - pow(static_cast<double>(beta1), static_cast<double>(t));
+    const double bc2 = 1.0 - pow(static_cast<double>(beta2), static_cast<double>(t));
+    if (!(bc1 > 0.0) || !(bc2 > 0.0)) return GALORE_ERR_INVALID_ARG;
+    const int64_t st = (batch > 1) ? stride : rows * ld;
+    GALORE_TRY(launch_adam(R, M, V, N, rows, cols, ld, st, batch, beta1, beta2, eps,
+                           static_cast<float>(bc1), static_cast<float>(bc2), stream));
+    return GALORE_OK;
+}
+
+int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const float* N,
+                        int64_t ldn, int64_t stride_n, float* W, int64_t m, int64_t n,
+                        int64_t ldw, int64_t stride_w, int32_t r, float lr, float alpha,
+                        int32_t batch, hipStream_t stream) {
+    if (P == nullptr || N == nullptr || W == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (!finite_f(lr) || !finite_f(alpha)) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s || ldp < r || ldn < sh.l || ldw < n) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_p < sh.s * ldp || stride_n < r * ldn || stride_w < m * ldw))
+        return GALORE_ERR_SHAPE;
+    GemmArgs a{};
+    a.C = W;
+    a.ldc = ldw;
+    a.strideC = stride_w;
+    a.K = r;
+    a.alpha = -(lr * alpha);
+    a.beta = 1.0f;
+    if (sh.left) {
+        // W (s x l) -= c * P N : A = P (K contiguous), B = N (N contiguous)
+        a.A = P;
+        a.lda = ldp;
+        a.strideA = stride_p;
+        a.B = N;
+        a.ldb = ldn;
+        a.strideB = stride_n;
+        a.M = static_cast<int>(sh.s);
+        a.N = static_cast<int>(sh.l);
+        GALORE_TRY(launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, stream));
+    } else {
+        // W (l x s) -= c * N^T P^T : A(i, kk) = N[kk][i] (M contiguous), B(kk, j) = P[j][kk]
+        a.A = N;
+        a.lda = ldn;
+        a.strideA = stride_n;
+        a.B = P;
+        a.ldb = ldp;
+        a.strideB = stride_p;
+        a.M = static_cast<int>(sh.l);
+        a.N = static_cast<int>(sh.s);
+        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kKContig, false, false, a, batch, stream));
+    }
+    return GALORE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,383 @@
+// Dense contractions of the subspace update and the projection steps, on the
+// CDNA4 matrix cores.
+//
+//  * gemm_f32: C = alpha * op(A) op(B) + beta * C in fp32 with
+//    v_mfma_f32_32x32x2_f32. gfx950 has no TF32 matrix path, so fp32 MFMA is
+//    the precision the method is computed in. bf16-stored gradients are
+//    widened exactly to fp32 while staging into LDS.
+//    Workgroup tile 128 x 128 x 32, four wave64s in a 2 x 2 arrangement, each
+//    wave owning a 64 x 64 sub-tile (2 x 2 MFMA 32x32 blocks). LDS holds A^T
+//    and B tiles in M-/N-contiguous order so that the per-lane MFMA operand
+//    reads are consecutive addresses; double-buffered with one barrier per
+//    K step, the next tile's global loads in flight during the MFMAs.
+//  * gram64: C = X^T X in fp64 with v_mfma_f64_16x16x4_f64 (the Gram matrices
+//    of the Cholesky-based orthonormalisation), only the upper tiles computed
+//    and mirrored.
+#include "common.hpp"
+
+namespace galore {
+namespace {
+
+constexpr int BM = 128;
+constexpr int BN = 128;
+constexpr int BK = 32;
+constexpr int NT = 256;
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* base, int64_t idx) {
+    return to_f32(base[idx]);
+}
+
+template <ALayout LA, BLayout LB, typename TA, typename TB>
+__global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, int b_vec) {
+    __shared__ float As[2][BK][BM];
+    __shared__ float Bs[2][BK][BN];
+
+    const int bz = blockIdx.z;
+    const TA* A = static_cast<const TA*>(g.A) + static_cast<int64_t>(bz) * g.strideA;
+    const TB* B = static_cast<const TB*>(g.B) + static_cast<int64_t>(bz) * g.strideB;
+    float* C = g.C + static_cast<int64_t>(bz) * g.strideC;
+    const int M = g.M, N = g.N, K = g.K;
+    const int row0 = blockIdx.y * BM;
+    const int col0 = blockIdx.x * BN;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    float ra[16];
+    float rb[16];
+
+    // ---- global -> registers ------------------------------------------------
+    auto load_a = [&](int k0) {
+        if constexpr (LA == ALayout::kKContig) {
+            const int i = t >> 1;
+            const int kk0 = (t & 1) * 16;
+            const int gi = row0 + i;
+            const int gk = k0 + kk0;
+            if (gi < M && gk + 16 <= K && a_vec) {
+                const TA* src = A + static_cast<int64_t>(gi) * g.lda + gk;
+                if constexpr (sizeof(TA) == 4) {
+                    const f32x4* v = reinterpret_cast<const f32x4*>(src);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        f32x4 x = v[q];
+                        ra[4 * q + 0] = x[0];
+                        ra[4 * q + 1] = x[1];
+                        ra[4 * q + 2] = x[2];
+                        ra[4 * q + 3] = x[3];
+                    }
+                } else {
+                    const uint4* v = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        uint4 x = v[q];
+                        uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            ra[8 * q + 2 * e + 0] = __uint_as_float(w[e] << 16);
+                            ra[8 * q + 2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    ra[e] = (gi < M && gk + e < K)
+                                ? load_elem(A, static_cast<int64_t>(gi) * g.lda + gk + e)
+                                : 0.0f;
+                }
+            }
+        } else {
+            const int i = t & (BM - 1);
+            const int kb = t >> 7;
+            const int gi = row0 + i;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int gk = k0 + kb + 2 * e;
+                ra[e] = (gi < M && gk < K) ? load_elem(A, static_cast<int64_t>(gk) * g.lda + gi)
+                                           : 0.0f;
+            }
+        }
+    };
+    auto load_b = [&](int k0) {
+        if constexpr (LB == BLayout::kNContig) {
+            const int j = t & (BN - 1);
+            const int kb = t >> 7;
+            const int gj = col0 + j;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int gk = k0 + kb + 2 * e;
+                rb[e] = (gj < N && gk < K) ? load_elem(B, static_cast<int64_t>(gk) * g.ldb + gj)
+                                           : 0.0f;
+            }
+        } else {
+            const int j = t >> 1;
+            const int kk0 = (t & 1) * 16;
+            const int gj = col0 + j;
+            const int gk = k0 + kk0;
+            if (gj < N && gk + 16 <= K && b_vec) {
+                const TB* src = B + static_cast<int64_t>(gj) * g.ldb + gk;
+                if constexpr (sizeof(TB) == 4) {
+                    const f32x4* v = reinterpret_cast<const f32x4*>(src);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        f32x4 x = v[q];
+                        rb[4 * q + 0] = x[0];
+                        rb[4 * q + 1] = x[1];
+                        rb[4 * q + 2] = x[2];
+                        rb[4 * q + 3] = x[3];
+                    }
+                } else {
+                    const uint4* v = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        uint4 x = v[q];
+                        uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            rb[8 * q + 2 * e + 0] = __uint_as_float(w[e] << 16);
+                            rb[8 * q + 2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    rb[e] = (gj < N && gk + e < K)
+                                ? load_elem(B, static_cast<int64_t>(gj) * g.ldb + gk + e)
+                                : 0.0f;
+                }
+            }
+        }
+    };
+    // ---- registers -> LDS ---------------------------------------------------
+    auto store_a = [&](int buf) {
+        if constexpr (LA == ALayout::kKContig) {
+            const int i = t >> 1;
+            const int kk0 = (t & 1) * 16;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) As[buf][kk0 + e][i] = ra[e];
+        } else {
+            const int i = t & (BM - 1);
+            const int kb = t >> 7;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) As[buf][kb + 2 * e][i] = ra[e];
+        }
+    };
+    auto store_b = [&](int buf) {
+        if constexpr (LB == BLayout::kNContig) {
+            const int j = t & (BN - 1);
+            const int kb = t >> 7;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) Bs[buf][kb + 2 * e][j] = rb[e];
+        } else {
+            const int j = t >> 1;
+            const int kk0 = (t & 1) * 16;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) Bs[buf][kk0 + e][j] = rb[e];
+        }
+    };
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
+
+    const int KT = (K + BK - 1) / BK;
+    load_a(0);
+    load_b(0);
+    store_a(0);
+    store_b(0);
+    __syncthreads();
+
+    const int lrow = lane & 31;
+    const int lk = lane >> 5;
+    for (int kt = 0; kt < KT; ++kt) {
+        const int cur = kt & 1;
+        const bool more = (kt + 1 < KT);
+        if (more) {
+            load_a((kt + 1) * BK);
+            load_b((kt + 1) * BK);
+        }
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const float a0 = As[cur][kk + lk][wm * 64 + lrow];
+            const float a1 = As[cur][kk + lk][wm * 64 + 32 + lrow];
+            const float b0 = Bs[cur][kk + lk][wn * 64 + lrow];
+            const float b1 = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+        }
+        if (more) {
+            store_a(cur ^ 1);
+            store_b(cur ^ 1);
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: 32x32 block layout, lane holds column (lane & 31) and rows
+    //      (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
+    const float alpha = g.alpha, beta = g.beta;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi) {
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+            const int c = col0 + wn * 64 + ni * 32 + lrow;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int r = row0 + wm * 64 + mi * 32 + (v & 3) + 8 * (v >> 2) + 4 * lk;
+                if (r < M && c < N) {
+                    float* dst = C + static_cast<int64_t>(r) * g.ldc + c;
+                    float val = alpha * acc[mi][ni][v];
+                    if (beta != 0.0f) val += beta * (*dst);
+                    *dst = val;
+                }
+            }
+        }
+    }
+}
+
+template <ALayout LA, BLayout LB, typename TA, typename TB>
+hipError_t launch_one(const GemmArgs& g, int batch, hipStream_t stream) {
+    dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, batch);
+    int a_vec = 0, b_vec = 0;
+    const int amul = (sizeof(TA) == 4) ? 4 : 8;   // elements per 16-byte vector
+    const int bmul = (sizeof(TB) == 4) ? 4 : 8;
+    if (LA == ALayout::kKContig)
+        a_vec = (g.lda % amul == 0) && (g.strideA % amul == 0) &&
+                (reinterpret_cast<uintptr_t>(g.A) % 16 == 0);
+    if (LB == BLayout::kKContig)
+        b_vec = (g.ldb % bmul == 0) && (g.strideB % bmul == 0) &&
+                (reinterpret_cast<uintptr_t>(g.B) % 16 == 0);
+    hipLaunchKernelGGL((gemm_f32_kernel<LA, LB, TA, TB>), grid, dim3(NT), 0, stream, g, a_vec, b_vec);
+    return hipGetLastError();
+}
+
+template <ALayout LA, BLayout LB>
+hipError_t dispatch_types(bool a_bf16, bool b_bf16, const GemmArgs& g, int batch, hipStream_t s) {
+    if (a_bf16 && b_bf16) return hipErrorInvalidValue;
+    if (a_bf16) return launch_one<LA, LB, bf16_t, float>(g, batch, s);
+    if (b_bf16) return launch_one<LA, LB, float, bf16_t>(g, batch, s);
+    return launch_one<LA, LB, float, float>(g, batch, s);
+}
+
+// --------------------------------------------------------------------------
+// fp64 Gram C = X^T X (cols x cols), X rows x cols fp32.
+// --------------------------------------------------------------------------
+constexpr int GB = 64;   // tile
+constexpr int GK = 16;   // k step
+
+__global__ __launch_bounds__(256) void gram64_kernel(Gram64Args g) {
+    const int tm = blockIdx.y * GB;
+    const int tn = blockIdx.x * GB;
+    if (tn < tm) return;                      // lower tiles come from the mirror
+    __shared__ double As[2][GK][GB];
+    __shared__ double Bs[2][GK][GB];
+    const int bz = blockIdx.z;
+    const float* X = g.X + static_cast<int64_t>(bz) * g.strideX;
+    double* C = g.C + static_cast<int64_t>(bz) * g.strideC;
+    const int rows = g.rows, cols = g.cols;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int li = t & 63;
+    const int lkb = t >> 6;
+
+    double ra[4], rb[4];
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int kk = k0 + lkb + 4 * e;
+            const bool kin = kk < rows;
+            const int64_t base = static_cast<int64_t>(kk) * g.ldx;
+            ra[e] = (kin && tm + li < cols) ? static_cast<double>(X[base + tm + li]) : 0.0;
+            rb[e] = (kin && tn + li < cols) ? static_cast<double>(X[base + tn + li]) : 0.0;
+        }
+    };
+    auto store = [&](int buf) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            As[buf][lkb + 4 * e][li] = ra[e];
+            Bs[buf][lkb + 4 * e][li] = rb[e];
+        }
+    };
+
+    f64x4 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) acc[a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
+
+    const int KT = (rows + GK - 1) / GK;
+    load(0);
+    store(0);
+    __syncthreads();
+    const int l16 = lane & 15;
+    const int lk = lane >> 4;
+    for (int kt = 0; kt < KT; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < KT;
+        if (more) load((kt + 1) * GK);
+#pragma unroll
+        for (int kk = 0; kk < GK; kk += 4) {
+            const double a0 = As[cur][kk + lk][wm * 32 + l16];
+            const double a1 = As[cur][kk + lk][wm * 32 + 16 + l16];
+            const double b0 = Bs[cur][kk + lk][wn * 32 + l16];
+            const double b1 = Bs[cur][kk + lk][wn * 32 + 16 + l16];
+            acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+        }
+        if (more) store(cur ^ 1);
+        __syncthreads();
+    }
+    // 16x16 block layout: lane holds column (lane & 15), rows 4 (lane >> 4) + v.
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi) {
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni) {
+            const int j = tn + wn * 32 + ni * 16 + l16;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int i = tm + wm * 32 + mi * 16 + 4 * lk + v;
+                if (i < cols && j < cols) {
+                    C[static_cast<int64_t>(i) * cols + j] = acc[mi][ni][v];
+                    if (tn != tm) C[static_cast<int64_t>(j) * cols + i] = acc[mi][ni][v];
+                }
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const GemmArgs& g, int batch,
+                       hipStream_t stream) {
+    if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
+    if (la == ALayout::kKContig && lb == BLayout::kNContig)
+        return dispatch_types<ALayout::kKContig, BLayout::kNContig>(a_bf16, b_bf16, g, batch, stream);
+    if (la == ALayout::kMContig && lb == BLayout::kNContig)
+        return dispatch_types<ALayout::kMContig, BLayout::kNContig>(a_bf16, b_bf16, g, batch, stream);
+    if (la == ALayout::kKContig && lb == BLayout::kKContig)
+        return dispatch_types<ALayout::kKContig, BLayout::kKContig>(a_bf16, b_bf16, g, batch, stream);
+    return dispatch_types<ALayout::kMContig, BLayout::kKContig>(a_bf16, b_bf16, g, batch, stream);
+}
+
+hipError_t launch_gram64(const Gram64Args& g, int batch, hipStream_t stream) {
+    if (g.cols <= 0 || batch <= 0) return hipSuccess;
+    const int tiles = (g.cols + GB - 1) / GB;
+    dim3 grid(tiles, tiles, batch);
+    hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, stream, g);
+    return hipGetLastError();
+}
+
+}  // namespace galore

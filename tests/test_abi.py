@@ -1,0 +1,130 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+function include/galore.h declares, and rejects invalid arguments on the host
+before enqueuing anything (each call below has exactly one invalid argument;
+the pointers are never dereferenced because validation fails first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "galore.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(galore_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_hot_path_calls():
+    names = declared_functions()
+    for fn in ("galore_rsvd_update", "galore_project", "galore_lowrank_adam_step", "galore_project_back"):
+        assert fn in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2504_20437_amd as gl
+    lib = ctypes.CDLL(gl.LIB_PATH)
+    for fn in declared_functions():
+        assert hasattr(lib, fn), fn
+    assert set(gl.EXPORTED) == set(declared_functions())
+
+
+def test_status_strings_and_version():
+    import paper_2504_20437_amd as gl
+    assert gl.status_string(0) == "GALORE_OK"
+    assert gl.status_string(-3) == "GALORE_ERR_WORKSPACE"
+    assert gl.galore_version() >= 100
+
+
+def test_workspace_size():
+    import paper_2504_20437_amd as gl
+    one = gl.galore_rsvd_workspace_size(4096, 11008, 1024, 32, 1)
+    assert one > 0
+    assert gl.galore_rsvd_workspace_size(4096, 11008, 1024, 32, 4) >= 4 * one - 4096
+    assert gl.galore_rsvd_workspace_size(11008, 4096, 1024, 32, 1) == one       # orientation
+    assert gl.galore_rsvd_workspace_size(10, 20, 11, 0, 1) == 0                  # r > s
+    assert gl.galore_rsvd_workspace_size(0, 20, 1, 0, 1) == 0
+    assert gl.galore_rsvd_workspace_size(5000, 9000, 4090, 10, 1) == 0           # sketch too wide
+
+
+FAKE = 0x1000   # never dereferenced: every call below fails validation first
+NULL = None
+
+
+def rsvd(**kw):
+    import paper_2504_20437_amd as gl
+    a = dict(G=FAKE, g_dtype=0, m=64, n=96, ldg=96, stride_g=64 * 96, r=8, p=4, q=1, seed=1, si=0,
+             P=FAKE, ldp=8, stride_p=64 * 8, sigma=FAKE, stride_sigma=8, info=FAKE, batch=1,
+             ws=FAKE - FAKE % 256 + 256, ws_bytes=1 << 40, stream=NULL)
+    a.update(kw)
+    return gl.lib.galore_rsvd_update(a["G"], a["g_dtype"], a["m"], a["n"], a["ldg"], a["stride_g"], a["r"],
+                                     a["p"], a["q"], a["seed"], a["si"], a["P"], a["ldp"], a["stride_p"],
+                                     a["sigma"], a["stride_sigma"], a["info"], a["batch"], a["ws"],
+                                     a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(G=NULL), -1), (dict(P=NULL), -1), (dict(ws=NULL), -1), (dict(g_dtype=7), -1),
+    (dict(m=0), -2), (dict(n=-3), -2), (dict(r=0), -2), (dict(r=65), -2), (dict(p=-1), -2),
+    (dict(q=-1), -2), (dict(ldg=95), -2), (dict(ldp=7), -2), (dict(batch=0), -2),
+    (dict(batch=2, stride_g=10), -2), (dict(r=8, p=5000), -2),
+    (dict(ws_bytes=1000), -3), (dict(ws=FAKE + 8), -3),
+])
+def test_rsvd_rejects(kw, code):
+    assert rsvd(**kw) == code
+
+
+def test_project_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_project
+    ok = dict(P=FAKE, ldp=8, sp=0, G=FAKE, dt=0, m=64, n=96, ldg=96, sg=0, r=8, R=FAKE, ldr=96, sr=0, b=1)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(a["P"], a["ldp"], a["sp"], a["G"], a["dt"], a["m"], a["n"], a["ldg"], a["sg"], a["r"],
+                 a["R"], a["ldr"], a["sr"], a["b"], None)
+    assert call(P=NULL) == -1 and call(G=NULL) == -1 and call(R=NULL) == -1 and call(dt=3) == -1
+    assert call(r=65) == -2 and call(ldr=95) == -2 and call(ldp=7) == -2 and call(ldg=10) == -2
+    assert call(m=0) == -2 and call(b=0) == -2 and call(b=2) == -2
+    # right projector: l = m
+    assert call(m=200, n=96, ldr=199) == -2
+
+
+def test_adam_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_lowrank_adam_step
+    ok = dict(R=FAKE, M=FAKE, V=FAKE, N=FAKE, rows=4, cols=8, ld=8, st=32, b=1, b1=0.9, b2=0.999,
+              eps=1e-8, t=1)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(a["R"], a["M"], a["V"], a["N"], a["rows"], a["cols"], a["ld"], a["st"], a["b"],
+                 a["b1"], a["b2"], a["eps"], a["t"], None)
+    for kw in (dict(R=NULL), dict(M=NULL), dict(V=NULL), dict(N=NULL), dict(b1=1.0), dict(b1=-0.1),
+               dict(b2=1.0), dict(eps=0.0), dict(eps=float("nan")), dict(b1=float("inf")), dict(t=0)):
+        assert call(**kw) == -1, kw
+    for kw in (dict(rows=0), dict(cols=0), dict(ld=7), dict(b=0), dict(b=2, st=31)):
+        assert call(**kw) == -2, kw
+
+
+def test_project_back_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_project_back
+    ok = dict(P=FAKE, ldp=8, sp=0, N=FAKE, ldn=96, sn=0, W=FAKE, m=64, n=96, ldw=96, sw=0, r=8,
+              lr=1e-3, al=0.25, b=1)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(a["P"], a["ldp"], a["sp"], a["N"], a["ldn"], a["sn"], a["W"], a["m"], a["n"], a["ldw"],
+                 a["sw"], a["r"], a["lr"], a["al"], a["b"], None)
+    for kw in (dict(P=NULL), dict(N=NULL), dict(W=NULL), dict(lr=float("nan")), dict(al=float("inf"))):
+        assert call(**kw) == -1, kw
+    for kw in (dict(r=65), dict(ldn=95), dict(ldw=95), dict(ldp=7), dict(m=0), dict(b=0), dict(b=2)):
+        assert call(**kw) == -2, kw
+
+
+def test_sketch_rejects():
+    import paper_2504_20437_amd as gl
+    assert gl.lib.galore_sketch(NULL, 10, 4, 1, 0, None) == -1
+    assert gl.lib.galore_sketch(FAKE, 0, 4, 1, 0, None) == -2
+    assert gl.lib.galore_sketch(FAKE, 10, 0, 1, 0, None) == -2

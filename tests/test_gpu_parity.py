@@ -1,0 +1,287 @@
+"""GPU-vs-oracle parity through the C ABI (run on an MI355X with -m gpu).
+
+Tolerances (fp32 GPU path vs fp64 oracle on the same stored inputs):
+  * projector distance ||P P^T - Pref Pref^T||_F <= 1e-3 on spectra with a gap at r
+  * singular values: rtol 1e-4
+  * projection / Adam / back-projection, per kernel on identical fp32 inputs:
+    |x - ref| <= 1e-6 + 1e-5 |ref| element-wise
+"""
+import numpy as np
+import pytest
+
+import galore_inputs as gi
+from metrics import max_rel_violation, orth_err, proj_dist
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def gl():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    import paper_2504_20437_amd as g
+    return g
+
+
+def dev(x, dtype=None):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.cuda()
+
+
+def dev_stored(st):
+    """device tensor holding the exact stored bits of a galore_inputs.Stored"""
+    import torch
+    if st.dtype == "f32":
+        return dev(st.data)
+    return dev(st.data.view(np.int16)).view(torch.bfloat16)
+
+
+def host(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+# ---------------------------------------------------------------- sketch
+
+
+@pytest.mark.parametrize("l,k,seed,idx", [(688, 40, 20250429, 0), (1376, 136, 7, 3), (37, 5, 2**63 + 5, 9)])
+def test_sketch_matches_oracle(gl, orc, l, k, seed, idx):
+    om = host(gl.galore_sketch(l, k, seed, idx))
+    ref = orc.sketch(l, k, seed, idx)
+    assert om.shape == ref.shape
+    diff = om != ref
+    # both sides round the same fp64 Box-Muller value to fp32; independent libm
+    # implementations may differ in the last fp64 bit, which can flip the fp32
+    # rounding only in rare boundary cases
+    assert diff.mean() < 1e-4
+    if diff.any():
+        a = om[diff].astype(np.float32).view(np.int32).astype(np.int64)
+        b = ref[diff].astype(np.float32).view(np.int32).astype(np.int64)
+        assert np.abs(a - b).max() <= 1
+
+
+# ---------------------------------------------------------------- projection
+
+
+@pytest.mark.parametrize("m,n,r,dtype", [(300, 517, 37, "f32"), (517, 300, 37, "f32"), (256, 688, 32, "bf16"),
+                                         (1376, 512, 128, "bf16"), (129, 129, 1, "f32"), (64, 2000, 64, "f32")])
+def test_project_matches_oracle(gl, orc, m, n, r, dtype):
+    s = min(m, n)
+    G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.8), 1e-4, seed=m + n), dtype)
+    P = np.linalg.qr(np.random.default_rng(r).standard_normal((s, r)))[0].astype(np.float32)
+    R = host(gl.galore_project(dev(P), dev_stored(G)))
+    ref = orc.project(P.astype(np.float64), G.exact)
+    assert R.shape == ref.shape == (r, max(m, n))
+    assert max_rel_violation(R, ref, 1e-5, 1e-6) <= 1.0
+
+
+def test_project_batched_strided(gl, orc):
+    import torch
+    m, n, r, b = 200, 333, 24, 3
+    Gs = [gi.store(gi.planted_gradient(m, n, gi.spectrum_power(m, 1.0), 1e-4, seed=i), "f32") for i in range(b)]
+    Gd = torch.zeros((b, m, n + 5), dtype=torch.float32, device="cuda")     # padded ld
+    for i in range(b):
+        Gd[i, :, :n] = dev(Gs[i].data)
+    Ps = np.stack([np.linalg.qr(np.random.default_rng(i).standard_normal((m, r)))[0] for i in range(b)]).astype(np.float32)
+    R = host(gl.galore_project(dev(Ps), Gd[:, :, :n]))
+    for i in range(b):
+        assert max_rel_violation(R[i], orc.project(Ps[i].astype(np.float64), Gs[i].exact), 1e-5, 1e-6) <= 1.0
+
+
+# ---------------------------------------------------------------- Adam
+
+
+@pytest.mark.parametrize("rows,cols,t", [(32, 688, 1), (7, 1001, 5), (128, 1376, 200), (1, 3, 2)])
+def test_adam_matches_oracle(gl, orc, rows, cols, t):
+    R, M, V = gi.lowrank_state(rows, cols, seed=rows * cols + t)
+    if t == 1:
+        M[:] = 0
+        V[:] = 0
+    b1, b2, eps = np.float32(0.9), np.float32(0.999), np.float32(1e-8)
+    Rd, Md, Vd = dev(R), dev(M), dev(V)
+    N = gl.galore_lowrank_adam_step(Rd, Md, Vd, None, float(b1), float(b2), float(eps), t)
+    Mr, Vr, Nr = orc.adam(R, M, V, float(b1), float(b2), float(eps), t)
+    assert max_rel_violation(host(Md), Mr, 1e-5, 1e-6) <= 1.0
+    assert max_rel_violation(host(Vd), Vr, 1e-5, 1e-6) <= 1.0
+    assert max_rel_violation(host(N), Nr, 1e-5, 1e-6) <= 1.0
+
+
+def test_adam_in_place_and_strided(gl, orc):
+    import torch
+    rows, cols, b, t = 17, 250, 3, 3
+    base = [gi.lowrank_state(rows, cols, seed=i) for i in range(b)]
+    R = np.stack([x[0] for x in base]); M = np.stack([x[1] for x in base]); V = np.stack([x[2] for x in base])
+    pad = lambda a: torch.nn.functional.pad(dev(a), (0, 6))[:, :, :cols]   # ld = cols + 6
+    Rd, Md, Vd = pad(R), pad(M), pad(V)
+    N = gl.galore_lowrank_adam_step(Rd, Md, Vd, Rd, 0.9, 0.999, 1e-8, t)   # N aliases R
+    assert N.data_ptr() == Rd.data_ptr()
+    for i in range(b):
+        Mr, Vr, Nr = orc.adam(R[i], M[i], V[i], float(np.float32(0.9)), float(np.float32(0.999)),
+                              float(np.float32(1e-8)), t)
+        assert max_rel_violation(host(Md[i]), Mr, 1e-5, 1e-6) <= 1.0
+        assert max_rel_violation(host(Vd[i]), Vr, 1e-5, 1e-6) <= 1.0
+        assert max_rel_violation(host(Rd[i]), Nr, 1e-5, 1e-6) <= 1.0
+
+
+# ---------------------------------------------------------------- back-projection
+
+
+@pytest.mark.parametrize("m,n,r", [(256, 688, 32), (688, 256, 32), (300, 300, 17), (1376, 512, 128)])
+def test_project_back_matches_oracle(gl, orc, m, n, r):
+    s, l = min(m, n), max(m, n)
+    rng = np.random.default_rng(m * 7 + n)
+    P = np.linalg.qr(rng.standard_normal((s, r)))[0].astype(np.float32)
+    N = rng.standard_normal((r, l)).astype(np.float32)
+    W = gi.weights(m, n, seed=3)
+    Wd = dev(W)
+    gl.galore_project_back(dev(P), dev(N), Wd, 1e-3, 0.25)
+    ref = orc.project_back(P.astype(np.float64), N.astype(np.float64), W.astype(np.float64),
+                           float(np.float32(1e-3)), float(np.float32(0.25)))
+    assert max_rel_violation(host(Wd), ref, 1e-5, 1e-6) <= 1.0
+
+
+# ---------------------------------------------------------------- subspace update
+
+
+def _check_rsvd(gl, orc, G, r, p, q, seed, graded=True, idx=0):
+    Gd = dev_stored(G)
+    P, sig, info = gl.galore_rsvd_update(Gd, r, p, q, seed, idx)
+    P, sig = host(P), host(sig)
+    info = int(info.cpu()[0])
+    Pr, sr, sw = orc.rsvd_update(G.exact, r, p, q, seed, idx)
+    assert info == 0
+    assert orth_err(P) < 1e-4
+    assert np.all(np.diff(sig) <= 1e-6 * sig[0])
+    idx_max = np.argmax(np.abs(P), axis=0)
+    assert np.all(P[idx_max, np.arange(r)] > 0)
+    assert max_rel_violation(sig, sr, 1e-4, 1e-30) <= 1.0
+    d = proj_dist(P, Pr)
+    if graded:
+        assert d <= 1e-3, d
+    return P, sig, Pr, sr, d
+
+
+def test_rsvd_single_256x688(gl, orc):
+    """The single-matrix case: 256 x 688 fp32, s_i = 10 * 0.85^i (i < 64), 1e-3
+    noise, r = 32, p = 8, q = 2 (relative gap at r about 0.14)."""
+    w = gi.WORKLOADS["single-256x688"]
+    G = gi.store(gi.planted_gradient(256, 688, w.spectrum(256), w.noise, seed=1000), "f32")
+    _check_rsvd(gl, orc, G, 32, 8, 2, seed=gi.sketch_seed(0))
+
+
+@pytest.mark.parametrize("m,n,r,p,q,dtype", [
+    (688, 256, 32, 8, 2, "f32"),        # right projector
+    (512, 512, 64, 8, 1, "f32"),        # square (left projector)
+    (512, 1376, 128, 8, 2, "bf16"),     # bf16 storage
+    (300, 517, 37, 11, 0, "f32"),       # ragged sizes, no power iteration
+])
+def test_rsvd_gapped_spectra(gl, orc, m, n, r, p, q, dtype):
+    s = min(m, n)
+    spec = gi.spectrum_gapped(gi.spectrum_power(s, 0.8), r)
+    G = gi.store(gi.planted_gradient(m, n, spec, 1e-6, seed=m * 3 + n), dtype)
+    _check_rsvd(gl, orc, G, r, p, q, seed=11)
+
+
+def test_rsvd_batched_matches_single(gl, orc):
+    import torch
+    m, n, r, p, q, b = 200, 400, 16, 8, 1, 3
+    Gs = [gi.store(gi.planted_gradient(m, n, gi.spectrum_gapped(gi.spectrum_power(m, 1.0), r), 1e-6, seed=i), "f32")
+          for i in range(b)]
+    Gd = torch.stack([dev(x.data) for x in Gs])
+    P, sig, info = gl.galore_rsvd_update(Gd, r, p, q, seed=5, sketch_index0=10)
+    P, sig = host(P), host(sig)
+    assert (info.cpu().numpy() == 0).all()
+    for i in range(b):
+        Pr, sr, _ = orc.rsvd_update(Gs[i].exact, r, p, q, 5, 10 + i)
+        assert proj_dist(P[i], Pr) <= 1e-3
+        assert max_rel_violation(sig[i], sr, 1e-4, 1e-30) <= 1.0
+
+
+def test_rsvd_exact_recovery(gl, orc):
+    """rank(G) = 32 <= r (noiseless): sigma equals the planted values and P spans
+    the planted range; the deficient directions of the sketch get filled."""
+    m, n, r, p = 256, 688, 32, 8
+    s_pl = 10.0 * 0.85 ** np.arange(m)
+    G = gi.store(gi.planted_gradient(m, n, s_pl, 0.0, seed=4, rank=32), "f32")
+    P, sig, info = gl.galore_rsvd_update(dev(G.data), r, p, 2, 3)
+    P, sig = host(P), host(sig)
+    u, ss, _ = np.linalg.svd(G.exact)
+    assert max_rel_violation(sig, ss[:32], 1e-4, 1e-30) <= 1.0
+    assert proj_dist(P, u[:, :32]) <= 1e-3
+    assert orth_err(P) < 1e-4
+
+
+def test_rsvd_rank_below_r(gl, orc):
+    m, n, r, p = 128, 300, 24, 8
+    G = gi.store(gi.planted_gradient(m, n, 2.0 * 0.8 ** np.arange(m), 0.0, seed=6, rank=10), "f32")
+    P, sig, info = gl.galore_rsvd_update(dev(G.data), r, p, 1, 3)
+    P, sig = host(P), host(sig)
+    u, ss, _ = np.linalg.svd(G.exact)
+    assert max_rel_violation(sig[:10], ss[:10], 1e-4, 1e-30) <= 1.0
+    assert np.all(sig[10:] <= 1e-5 * ss[0])
+    assert proj_dist(P[:, :10], u[:, :10]) <= 1e-3          # unique part
+    assert orth_err(P) < 1e-4                               # the rest: any orthonormal completion
+
+
+def test_rsvd_zero_gradient(gl):
+    import torch
+    G = torch.zeros((40, 70), dtype=torch.float32, device="cuda")
+    P, sig, info = gl.galore_rsvd_update(G, 8, 4, 2, 1)
+    P, sig = host(P), host(sig)
+    assert np.all(sig == 0.0)
+    assert orth_err(P) < 1e-5
+
+
+def test_rsvd_full_sketch_is_exact_svd(gl, orc):
+    """k = min(r + p, s) = s: the randomized SVD equals the SVD."""
+    rng = np.random.default_rng(0)
+    G = gi.store(rng.standard_normal((24, 50)) * (0.7 ** np.arange(24))[:, None], "f32")
+    P, sig, info = gl.galore_rsvd_update(dev(G.data), 6, 30, 1, 9)
+    P, sig = host(P), host(sig)
+    u, ss, _ = np.linalg.svd(G.exact)
+    assert max_rel_violation(sig, ss[:6], 1e-4, 1e-30) <= 1.0
+    assert proj_dist(P, u[:, :6]) <= 1e-3
+
+
+def test_rsvd_deterministic(gl):
+    w = gi.WORKLOADS["single-256x688"]
+    G = dev(gi.store(gi.planted_gradient(256, 688, w.spectrum(256), w.noise, seed=1000), "f32").data)
+    P1, s1, _ = gl.galore_rsvd_update(G, 32, 8, 2, 77)
+    P2, s2, _ = gl.galore_rsvd_update(G, 32, 8, 2, 77)
+    assert np.array_equal(host(P1), host(P2)) and np.array_equal(host(s1), host(s2))
+
+
+# ---------------------------------------------------------------- one GaLore step end to end
+
+
+def test_galore_step_end_to_end(gl, orc):
+    """Subspace update, projection, Adam and weight update on the 256 x 688 case;
+    W is graded end to end, each kernel also on identical inputs."""
+    w = gi.WORKLOADS["single-256x688"]
+    G = gi.store(gi.planted_gradient(256, 688, w.spectrum(256), w.noise, seed=1000), "f32")
+    W0 = gi.weights(256, 688, seed=1)
+    Gd, Wd = dev(G.data), dev(W0)
+    P, sig, info = gl.galore_rsvd_update(Gd, w.r, w.p, w.q, gi.sketch_seed(0))
+    R = gl.galore_project(P, Gd)
+    import torch
+    M = torch.zeros_like(R)
+    V = torch.zeros_like(R)
+    N = gl.galore_lowrank_adam_step(R, M, V, None, w.beta1, w.beta2, w.eps, 1)
+    gl.galore_project_back(P, N, Wd, w.lr, w.alpha)
+    Ph, Rh, Nh = host(P), host(R), host(N)
+    f32 = lambda x: float(np.float32(x))
+    assert max_rel_violation(Rh, orc.project(Ph, G.exact), 1e-5, 1e-6) <= 1.0
+    _, _, Nr = orc.adam(Rh, np.zeros_like(Rh), np.zeros_like(Rh), f32(w.beta1), f32(w.beta2), f32(w.eps), 1)
+    assert max_rel_violation(Nh, Nr, 1e-5, 1e-6) <= 1.0
+    Wr = orc.project_back(Ph, Nh, W0.astype(np.float64), f32(w.lr), f32(w.alpha))
+    assert max_rel_violation(host(Wd), Wr, 1e-5, 1e-6) <= 1.0
+    # end to end: oracle W from the oracle's own P (sign-canonical, same subspace)
+    Pr, _, _ = orc.rsvd_update(G.exact, w.r, w.p, w.q, gi.sketch_seed(0))
+    Rr = orc.project(Pr, G.exact)
+    _, _, Nr2 = orc.adam(Rr, np.zeros_like(Rr), np.zeros_like(Rr), f32(w.beta1), f32(w.beta2), f32(w.eps), 1)
+    Wr2 = orc.project_back(Pr, Nr2, W0.astype(np.float64), f32(w.lr), f32(w.alpha))
+    assert max_rel_violation(host(Wd), Wr2, 1e-5, 1e-6) <= 1.0
