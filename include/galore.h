@@ -31,6 +31,12 @@
 
 #include <hip/hip_runtime_api.h>
 
+#if defined(__GNUC__) || defined(__clang__)
+#define GALORE_API __attribute__((visibility("default")))
+#else
+#define GALORE_API
+#endif
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -49,10 +55,10 @@ typedef enum {
 } galore_status_t;
 
 /* Human-readable name of a status code (static storage). */
-const char* galore_status_string(int status);
+GALORE_API const char* galore_status_string(int status);
 
 /* Library version: major * 10000 + minor * 100 + patch. */
-int galore_version(void);
+GALORE_API int galore_version(void);
 
 /*
  * Gaussian sketch (randomized range finder of Halko, Martinsson & Tropp 2011,
@@ -64,14 +70,14 @@ int galore_version(void);
  * Exposed so that callers and tests can inspect the sketch the subspace
  * update uses. Errors: omega NULL -> INVALID_ARG; l < 1 or k < 1 -> SHAPE.
  */
-int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index,
+GALORE_API int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index,
                   hipStream_t stream);
 
 /*
  * Bytes of workspace galore_rsvd_update needs for `batch` m x n matrices with
  * rank r and oversampling p. Returns 0 for invalid sizes.
  */
-size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch);
+GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch);
 
 /*
  * Subspace update (paper §3 and Alg. 1: P = top-r singular vectors of G on
@@ -97,7 +103,7 @@ size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, in
  *          r + p > 4096 (largest supported sketch width), ldg < n, ldp < r,
  *          batch < 1 -> SHAPE; workspace_bytes too small -> WORKSPACE.
  */
-int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
+GALORE_API int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                        int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
                        uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
                        float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
@@ -109,7 +115,7 @@ int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int
  * For m > n this is R = (G P)^T.
  * Errors: NULL pointers -> INVALID_ARG; sizes/ld invalid, r > s -> SHAPE.
  */
-int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
+GALORE_API int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
                    int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
                    int64_t ldr, int64_t stride_r, int32_t batch, hipStream_t stream);
 
@@ -125,7 +131,7 @@ int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G,
  * Errors: NULL pointers -> INVALID_ARG; beta outside [0,1), eps <= 0, non-finite
  * scalars, t < 1 -> INVALID_ARG; rows/cols < 1, ld < cols -> SHAPE.
  */
-int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64_t rows,
+GALORE_API int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64_t rows,
                              int64_t cols, int64_t ld, int64_t stride, int32_t batch, float beta1,
                              float beta2, float eps, int64_t t, hipStream_t stream);
 
@@ -139,7 +145,7 @@ int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64
  * Errors: NULL pointers -> INVALID_ARG; non-finite lr/alpha -> INVALID_ARG;
  * sizes/ld invalid, r > s -> SHAPE.
  */
-int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const float* N,
+GALORE_API int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const float* N,
                         int64_t ldn, int64_t stride_n, float* W, int64_t m, int64_t n,
                         int64_t ldw, int64_t stride_w, int32_t r, float lr, float alpha,
                         int32_t batch, hipStream_t stream);

@@ -15,6 +15,7 @@ HIPCC_FLAGS = [
     "-std=c++17",
     "-fPIC",
     "-shared",
+    "-fvisibility=hidden",
     # keep the compiler from emitting packed fp32 vector ops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]

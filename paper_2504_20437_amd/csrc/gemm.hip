@@ -340,7 +340,8 @@ __global__ __launch_bounds__(256) void gram64_kernel(Gram64Args g) {
         if (more) store(cur ^ 1);
         __syncthreads();
     }
-    // 16x16 block layout: lane holds column (lane & 15), rows 4 (lane >> 4) + v.
+    // fp64 16x16 block layout: lane holds column (lane & 15); accumulator
+    // register v holds row 4 v + (lane >> 4).
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi) {
 #pragma unroll
@@ -348,7 +349,7 @@ __global__ __launch_bounds__(256) void gram64_kernel(Gram64Args g) {
             const int j = tn + wn * 32 + ni * 16 + l16;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int i = tm + wm * 32 + mi * 16 + 4 * lk + v;
+                const int i = tm + wm * 32 + mi * 16 + 4 * v + lk;
                 if (i < cols && j < cols) {
                     C[static_cast<int64_t>(i) * cols + j] = acc[mi][ni][v];
                     if (tn != tm) C[static_cast<int64_t>(j) * cols + i] = acc[mi][ni][v];
