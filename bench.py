@@ -1,0 +1,235 @@
+"""Throughput of the GaLore 2 gradient-subspace hot path on one MI355X.
+
+One step is one pass of the whole path over a batch of same-shape gradients:
+the randomized-SVD subspace update (sketch, power iterations with
+re-orthonormalisation, small SVD, projector), the projection R = P^T A, the
+low-rank Adam step and the back-projected weight update.
+
+Workload (default): the 64 gate/up projection gradients of a Llama-7B-shaped
+model, 4096 x 11008 each, stored bf16 and computed in fp32, power-law planted
+spectrum s_i = (i+1)^-0.7 plus 1e-4 Gaussian noise; rank r = 1024,
+oversampling p = 32, q = 2 power iterations; Adam beta = (0.9, 0.999),
+eps = 1e-8, lr = 1e-3, scale alpha = 0.25. Inputs are synthetic, generated on
+the device and resident in HBM before the timed region starts.
+
+Prints ONE JSON line. `value` is subspace updates per second (each matrix of
+the batch gets one update, one projection, one Adam step and one weight update
+per step). Per-stage times come from HIP events recorded on the stream the
+library launches on; the Adam stage is one kernel launch, so its duration gives
+the achieved HBM bandwidth of that kernel.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0         # MI355X HBM3E, GB/s
+FP32_MFMA_PEAK_TFS = 157.3    # MI355X dense fp32 matrix, TFLOP/s
+ADAM_BYTES_PER_ELEM = 24      # read R, M, V; write M, V, N (fp32)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--m", type=int, default=4096)
+    ap.add_argument("--n", type=int, default=11008)
+    ap.add_argument("--batch", type=int, default=64)
+    ap.add_argument("--r", type=int, default=1024)
+    ap.add_argument("--p", type=int, default=32)
+    ap.add_argument("--q", type=int, default=2)
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--cpu-baseline", type=int, default=1, help="time the oracle on the host (0/1)")
+    ap.add_argument("--roofline-kernel", default="auto", choices=["auto", "adam", "project", "project_back"])
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="per-launch HBM bytes from rocprofv3 counters (optional)")
+    return ap.parse_args()
+
+
+def cpu_baseline(args):
+    """The oracle timed on the host on a bounded sample of the workload: one
+    planted-spectrum matrix with every dimension of the unit halved
+    (m/2 x n/2, r/2, p/2, same q), which is 1/8 of the unit's flops in every
+    term of the path, run through subspace update, projection, Adam and the
+    weight update; the rate is scaled by that factor to updates/s of the unit."""
+    import numpy as np
+
+    import galore_inputs as gi
+    import oracle
+
+    m, n, r, p, q = args.m // 2, args.n // 2, args.r // 2, args.p // 2, args.q
+    s = min(m, n)
+    G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.7), 1e-4, seed=7000), args.dtype)
+    W = gi.weights(m, n, seed=7001).astype(np.float64)
+    f32 = lambda x: float(np.float32(x))
+    t0 = time.perf_counter()
+    P, sig, _ = oracle.rsvd_update(G.exact, r, p, q, gi.sketch_seed(0))
+    R = oracle.project(P, G.exact)
+    Mz = np.zeros_like(R)
+    _, _, N = oracle.adam(R, Mz, Mz, f32(0.9), f32(0.999), f32(1e-8), 1)
+    oracle.project_back(P, N, W, f32(1e-3), f32(0.25))
+    dt = time.perf_counter() - t0
+    scale = (args.m * args.n * (args.r + args.p)) / float(m * n * (r + p))
+    return {
+        "value": 1.0 / (dt * scale),
+        "unit": "updates/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": "one %dx%d %s matrix, r=%d p=%d q=%d, full path (update, project, Adam, weight "
+                  "update) in %.1f s; every dimension of the %dx%d r=%d p=%d unit halved, so the "
+                  "rate is divided by the flop ratio %.2f" % (m, n, args.dtype, r, p, q, dt, args.m,
+                                                             args.n, args.r, args.p, scale),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's share "
+              "(one process, no collectives); --gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import galore_inputs as gi
+    import paper_2504_20437_amd as gl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    m, n, B, r, p, q = args.m, args.n, args.batch, args.r, args.p, args.q
+    s, l = min(m, n), max(m, n)
+    k = min(r + p, s)
+
+    print("bench: generating %d x %dx%d %s gradients" % (B, m, n, args.dtype), file=sys.stderr, flush=True)
+    G = gi.torch_planted_group(m, n, B, gi.spectrum_power(s, 0.7), 1e-4, seed=5000, dtype=args.dtype)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5001)
+    W = torch.empty((B, m, n), dtype=torch.float32, device=dev)
+    for i in range(B):
+        W[i].normal_(0.0, 0.02, generator=gen)
+    P = torch.empty((B, s, r), dtype=torch.float32, device=dev)
+    sigma = torch.empty((B, r), dtype=torch.float32, device=dev)
+    info = torch.empty((B,), dtype=torch.int32, device=dev)
+    R = torch.empty((B, r, l), dtype=torch.float32, device=dev)
+    M = torch.zeros_like(R)
+    V = torch.zeros_like(R)
+    N = torch.empty_like(R)
+    ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B),), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    stages = ("rsvd", "project", "adam", "project_back")
+
+    def step(t, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        gl.galore_rsvd_update(G, r, p, q, gi.sketch_seed(t), 0, P=P, sigma=sigma, info=info, workspace=ws,
+                              stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        gl.galore_project(P, G, R=R, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, t + 1, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+        gl.galore_project_back(P, N, W, 1e-3, 0.25, stream=stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for w in range(args.warmup):
+        step(w)
+        torch.cuda.synchronize()
+        print("bench: warmup %d done" % w, file=sys.stderr, flush=True)
+    if int((info != 0).sum()) != 0:
+        raise RuntimeError("small SVD did not converge for %d matrices" % int((info != 0).sum()))
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_stage = {st: 0.0 for st in stages}
+    for ev in events:
+        for j, st in enumerate(stages):
+            per_stage[st] += ev[j].elapsed_time(ev[j + 1])
+    per_stage = {st: v / args.steps for st, v in per_stage.items()}    # ms per step
+    ms_per_step = wall * 1000.0 / args.steps
+    bad = int((info != 0).sum())
+    if bad:
+        raise RuntimeError("small SVD did not converge for %d matrices" % bad)
+
+    # algorithmic work per launch of the single-kernel stages
+    adam_bytes = ADAM_BYTES_PER_ELEM * B * r * l
+    adam_gbs = adam_bytes / (per_stage["adam"] * 1e-3) / 1e9
+    proj_flops = 2.0 * r * s * l * B
+    proj_tfs = proj_flops / (per_stage["project"] * 1e-3) / 1e12
+    back_tfs = proj_flops / (per_stage["project_back"] * 1e-3) / 1e12
+
+    kern = args.roofline_kernel
+    if kern == "auto":
+        kern = max(("project", "adam", "project_back"), key=lambda st: per_stage[st])
+    traffic = None
+    try:
+        with open(args.traffic_json) as f:
+            tj = json.load(f)
+        key = "%s:%dx%dx%d:r%d:%s" % (kern, B, m, n, r, args.dtype)
+        traffic = tj.get(key)
+    except (OSError, ValueError):
+        traffic = None
+    if kern == "adam":
+        roof = {"kernel": "lowrank_adam", "bound": "hbm", "achieved": round(adam_gbs, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(adam_gbs / HBM_PEAK_GBS, 4),
+                "traffic": traffic}
+    else:
+        tf = proj_tfs if kern == "project" else back_tfs
+        roof = {"kernel": "gemm_f32 (%s)" % kern, "bound": "mfma", "achieved": round(tf, 2),
+                "peak": FP32_MFMA_PEAK_TFS, "unit": "TFLOP/s", "frac": round(tf / FP32_MFMA_PEAK_TFS, 4),
+                "traffic": traffic}
+
+    out = {
+        "metric": "rSVD subspace updates/sec at 4096x11008 r=1024; low-rank Adam step HBM GB/s",
+        "value": round(B / (ms_per_step * 1e-3), 3),
+        "unit": "updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if args.dtype == "f32" else "f32 (bf16-stored gradients)",
+        "data": "synthetic",
+        "config": {"workload": "Llama-7B-shaped gate/up gradients: %d x %dx%d %s, planted spectrum "
+                               "(i+1)^-0.7 + 1e-4 noise, r=%d p=%d q=%d (k=%d)"
+                               % (B, m, n, args.dtype, r, p, q, k),
+                   "batch": B, "m": m, "n": n, "r": r, "p": p, "q": q},
+        "adam_hbm_gbs": round(adam_gbs, 1),
+        "stage_ms": {st: round(v, 3) for st, v in per_stage.items()},
+        "project_tflops": round(proj_tfs, 2),
+        "project_back_tflops": round(back_tfs, 2),
+        "roofline": roof,
+    }
+    del G, W, R, M, V, N, ws
+    torch.cuda.empty_cache()
+    if args.cpu_baseline:
+        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(args)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -50,6 +50,8 @@ def _load():
         build()
         lib = ctypes.CDLL(_LIB_PATH)
         i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
+        lib.orc_num_threads.argtypes = []
+        lib.orc_num_threads.restype = ctypes.c_int
         lib.orc_philox4x64_10.argtypes = [_u64p, _u64p, _u64p]
         lib.orc_philox4x64_10.restype = None
         lib.orc_normal_from_words.argtypes = [u64, u64]
@@ -82,6 +84,11 @@ def _f64(a) -> np.ndarray:
 
 def _ptr(a: np.ndarray):
     return a.ctypes.data_as(_f64p)
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's loops run on."""
+    return int(_load().orc_num_threads())
 
 
 def philox4x64_10(counter, key) -> np.ndarray:

@@ -24,8 +24,12 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#include <omp.h>
 
 #define ORC_API __attribute__((visibility("default")))
+
+/* Threads the OpenMP loops of the oracle use (for reporting only). */
+ORC_API int orc_num_threads(void) { return omp_get_max_threads(); }
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x64-10 counter-based generator (Salmon, Moraes, Dror, Shaw,        */
