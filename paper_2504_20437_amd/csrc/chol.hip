@@ -5,11 +5,18 @@
 // ises after every application of A or A^T), and for the square factor the
 // small SVD works on.
 //
-// One workgroup (512 threads) per matrix; matrices of a batch run side by side.
-// Left-looking by blocks of 16 rows: each thread owns one column c of the
-// current block row, accumulates the 16 inner products against the rows above
-// (their 16-wide slice staged in LDS), the 16 x 16 diagonal block is factored
-// in LDS, then each thread finishes its column by forward substitution.
+// Right-looking, blocked by CB = 64 rows; every launch covers all matrices of
+// the batch (grid z / y = matrix), so the chip is filled by (tiles x batch)
+// workgroups rather than one workgroup per matrix:
+//   for each block row J:
+//     diag     factor the 64 x 64 diagonal block in LDS (unblocked, fp64) and
+//              invert it (D_J = R'_JJ^-1, kept in the fp64 inverse buffer);
+//     panel    R_JT = D_J^T C_JT for every block column T > J;
+//     trailing C_T1T2 -= R_JT1^T R_JT2 on the upper tiles T1 <= T2 right of J.
+//   inverse  X = R'^-1 by levels d = T - I: X_IT = -D_I sum_{I<U<=T} R_IU X_UT,
+//            written in fp64 and as fp32 (lower triangle zero) for the GEMM
+//            that applies it.
+// R overwrites the upper triangle of C; the lower triangle is not used.
 //
 // Semi-definite inputs: a pivot d <= tau_rel * (original diagonal) marks the
 // column as numerically dependent on the previous ones. Its row of R is set to
@@ -21,180 +28,236 @@
 namespace galore {
 namespace {
 
-constexpr int CB = 16;    // block rows
-constexpr int CT = 512;   // threads
-constexpr int CH = 64;    // staged rows per chunk
+constexpr int CB = 64;     // block size
+constexpr int CT = 256;    // threads per workgroup (16 x 16, 4 x 4 outputs each)
+constexpr int LP = CB + 1; // padded LDS row
 
-__global__ __launch_bounds__(CT) void cholesky_kernel(double* Cb, int k, int64_t strideC,
-                                                      float* rinvB, double* xinvB,
-                                                      int64_t strideInv, int* deficB,
-                                                      double tau_rel) {
+// acc[i][j] += sum_t As[t][ty + 16 i] * Bs[t][tx + 16 j], t < kk
+__device__ __forceinline__ void tile_tn(double (*As)[LP], double (*Bs)[LP], int kk, double acc[4][4],
+                                        int ty, int tx) {
+    for (int t = 0; t < kk; ++t) {
+        double a[4], b[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a[i] = As[t][ty + 16 * i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b[j] = Bs[t][tx + 16 * j];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = fma(a[i], b[j], acc[i][j]);
+    }
+}
+
+// S[r][c] = M[(r0 + r) * ld + c0 + c] for r < nr, c < nc; zero elsewhere
+__device__ __forceinline__ void load_tile(double (*S)[LP], const double* M, int64_t ld, int r0, int c0,
+                                          int nr, int nc) {
+    for (int idx = threadIdx.x; idx < CB * CB; idx += CT) {
+        const int r = idx / CB, c = idx % CB;
+        S[r][c] = (r < nr && c < nc) ? M[static_cast<int64_t>(r0 + r) * ld + c0 + c] : 0.0;
+    }
+}
+
+// S[c][r] = M[(r0 + r) * ld + c0 + c] (transposed load)
+__device__ __forceinline__ void load_tile_t(double (*S)[LP], const double* M, int64_t ld, int r0, int c0,
+                                            int nr, int nc) {
+    for (int idx = threadIdx.x; idx < CB * CB; idx += CT) {
+        const int r = idx / CB, c = idx % CB;
+        S[c][r] = (r < nr && c < nc) ? M[static_cast<int64_t>(r0 + r) * ld + c0 + c] : 0.0;
+    }
+}
+
+__global__ __launch_bounds__(CT) void chol_diag_kernel(double* Cb, int k, int64_t strideC, int J,
+                                                       double* diag0b, int* deficB, double* Xb,
+                                                       float* Rib, int64_t strideInv, double tau_rel) {
     const int b = blockIdx.x;
     double* C = Cb + static_cast<int64_t>(b) * strideC;
+    double* diag0 = diag0b + static_cast<int64_t>(b) * k;
     int* defic = deficB + static_cast<int64_t>(b) * k;
+    double* X = Xb + static_cast<int64_t>(b) * strideInv;
     const int tid = threadIdx.x;
-    __shared__ double Rs[CH][CB + 1];
-    __shared__ double Sd[CB][CB + 1];
+    const int j0 = J * CB;
+    const int jb = min(CB, k - j0);
+    __shared__ double S[CB][LP];
+    __shared__ double T[CB][LP];
     __shared__ double pinv;
     __shared__ int dfl[CB];
 
-    // ------------------------------------------------------------ factor
-    for (int J = 0; J < k; J += CB) {
-        const int jb = min(CB, k - J);
-        for (int cg = 0; cg < k - J; cg += CT) {
-            const int c = J + cg + tid;
-            const bool active = c < k;
-            double acc[CB];
-#pragma unroll
-            for (int i = 0; i < CB; ++i) acc[i] = 0.0;
-            for (int t0 = 0; t0 < J; t0 += CH) {
-                const int tc = min(CH, J - t0);
-                for (int idx = tid; idx < CH * CB; idx += CT) {
-                    const int tt = idx / CB, i = idx % CB;
-                    Rs[tt][i] = (tt < tc && i < jb)
-                                    ? C[static_cast<int64_t>(t0 + tt) * k + J + i] : 0.0;
-                }
-                __syncthreads();
-                if (active) {
-                    for (int tt = 0; tt < tc; ++tt) {
-                        const double rv = C[static_cast<int64_t>(t0 + tt) * k + c];
-#pragma unroll
-                        for (int i = 0; i < CB; ++i) acc[i] += Rs[tt][i] * rv;
-                    }
-                }
-                __syncthreads();
-            }
-            if (active) {
-#pragma unroll
-                for (int i = 0; i < CB; ++i)
-                    if (i < jb) acc[i] = C[static_cast<int64_t>(J + i) * k + c] - acc[i];
-            }
-            if (cg == 0) {
-                if (tid < jb) {
-#pragma unroll
-                    for (int i = 0; i < CB; ++i)
-                        if (i < jb) Sd[i][tid] = acc[i];
-                }
-                __syncthreads();
-                for (int i = 0; i < jb; ++i) {
-                    if (tid == 0) {
-                        const double d = Sd[i][i];
-                        const double corig = C[static_cast<int64_t>(J + i) * k + J + i];
-                        const bool def = (d <= tau_rel * corig);   // NaN compares false
-                        dfl[i] = def ? 1 : 0;
-                        const double rii = def ? 0.0 : sqrt(d);
-                        Sd[i][i] = rii;
-                        pinv = def ? 0.0 : 1.0 / rii;
-                    }
-                    __syncthreads();
-                    if (tid > i && tid < jb) Sd[i][tid] *= pinv;
-                    __syncthreads();
-                    if (tid < CB * CB) {
-                        const int i2 = i + 1 + tid / CB;
-                        const int c2 = tid % CB;
-                        if (i2 < jb && c2 >= i2 && c2 < jb) Sd[i2][c2] -= Sd[i][i2] * Sd[i][c2];
-                    }
-                    __syncthreads();
-                }
-            }
-            if (active) {
-                if (c < J + jb) {
-                    const int cc = c - J;
-#pragma unroll
-                    for (int i = 0; i < CB; ++i)
-                        if (i <= cc) C[static_cast<int64_t>(J + i) * k + c] = Sd[i][cc];
-                } else {
-#pragma unroll
-                    for (int i = 0; i < CB; ++i) {
-                        if (i < jb) {
-                            double x = acc[i];
-#pragma unroll
-                            for (int tt = 0; tt < CB; ++tt)
-                                if (tt < i) x -= Sd[tt][i] * acc[tt];
-                            acc[i] = dfl[i] ? 0.0 : x / Sd[i][i];
-                            C[static_cast<int64_t>(J + i) * k + c] = acc[i];
-                        }
-                    }
-                }
-            }
-            __syncthreads();
+    if (J == 0) {
+        for (int i = tid; i < k; i += CT) diag0[i] = C[static_cast<int64_t>(i) * k + i];
+    }
+    load_tile(S, C, k, j0, j0, jb, jb);
+    __syncthreads();
+    for (int i = 0; i < jb; ++i) {
+        if (tid == 0) {
+            const double d = S[i][i];
+            const double corig = (J == 0) ? C[static_cast<int64_t>(j0 + i) * k + j0 + i] : diag0[j0 + i];
+            const bool def = (d <= tau_rel * corig);   // NaN compares false
+            dfl[i] = def ? 1 : 0;
+            const double rii = def ? 0.0 : sqrt(d);
+            S[i][i] = rii;
+            pinv = def ? 0.0 : 1.0 / rii;
         }
-        if (tid < jb) defic[J + tid] = dfl[tid];
+        __syncthreads();
+        if (tid > i && tid < jb) S[i][tid] *= pinv;
+        __syncthreads();
+        const int n = jb - i - 1;
+        for (int idx = tid; idx < n * n; idx += CT) {
+            const int a = i + 1 + idx / n;
+            const int c = i + 1 + idx % n;
+            if (c >= a) S[a][c] -= S[i][a] * S[i][c];
+        }
         __syncthreads();
     }
-
-    if (rinvB == nullptr) return;
-
-    // ------------------------------------------------------------ inverse of R'
-    double* X = xinvB + static_cast<int64_t>(b) * strideInv;
-    float* Ri = rinvB + static_cast<int64_t>(b) * strideInv;
-    const int nblk = (k + CB - 1) / CB;
-    for (int bi = nblk - 1; bi >= 0; --bi) {
-        const int I = bi * CB;
-        const int ib = min(CB, k - I);
-        for (int idx = tid; idx < CB * CB; idx += CT) {
-            const int i = idx / CB, c2 = idx % CB;
-            double v = 0.0;
-            if (i < ib && c2 < ib && c2 >= i) {
-                if (defic[I + i]) v = (i == c2) ? 1.0 : 0.0;
-                else v = C[static_cast<int64_t>(I + i) * k + I + c2];
+    for (int idx = tid; idx < CB * CB; idx += CT) {
+        const int r = idx / CB, c = idx % CB;
+        if (r < jb && c < jb && c >= r) C[static_cast<int64_t>(j0 + r) * k + j0 + c] = S[r][c];
+    }
+    if (tid < jb) defic[j0 + tid] = dfl[tid];
+    // D = R'^-1 of the block (unit rows for deficient pivots), column c by
+    // back substitution; upper triangular.
+    if (tid < jb) {
+        const int c = tid;
+        for (int i = c; i >= 0; --i) {
+            double v = (i == c) ? 1.0 : 0.0;
+            if (!dfl[i]) {
+                for (int t = i + 1; t <= c; ++t) v -= S[i][t] * T[t][c];
+                v /= S[i][i];
+            } else if (i != c) {
+                v = 0.0;   // unit row: x_i = delta_ic
             }
-            Sd[i][c2] = v;
+            T[i][c] = v;
         }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < CB * CB; idx += CT) {
+        const int r = idx / CB, c = idx % CB;
+        if (r < jb && c < jb) {
+            const double v = (c >= r) ? T[r][c] : 0.0;
+            X[static_cast<int64_t>(j0 + r) * k + j0 + c] = v;
+            if (Rib != nullptr) Rib[static_cast<int64_t>(b) * strideInv + static_cast<int64_t>(j0 + r) * k + j0 + c] =
+                static_cast<float>(v);
+        }
+    }
+}
+
+// R_JT = D_J^T C_JT (deficient rows zero), in place in C, for T = J + 1 + blockIdx.x
+__global__ __launch_bounds__(CT) void chol_panel_kernel(double* Cb, int k, int64_t strideC, int J,
+                                                        const int* deficB, const double* Xb,
+                                                        int64_t strideInv) {
+    const int b = blockIdx.y;
+    double* C = Cb + static_cast<int64_t>(b) * strideC;
+    const int* defic = deficB + static_cast<int64_t>(b) * k;
+    const double* X = Xb + static_cast<int64_t>(b) * strideInv;
+    const int j0 = J * CB;
+    const int jb = min(CB, k - j0);
+    const int c0 = (J + 1 + blockIdx.x) * CB;
+    const int cb = min(CB, k - c0);
+    __shared__ double As[CB][LP];
+    __shared__ double Bs[CB][LP];
+    load_tile(As, X, k, j0, j0, jb, jb);   // As[t][i] = D[t][i]
+    load_tile(Bs, C, k, j0, c0, jb, cb);   // Bs[t][c] = C_JT[t][c]
+    __syncthreads();
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    double acc[4][4] = {};
+    tile_tn(As, Bs, jb, acc, ty, tx);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = ty + 16 * i;
+        if (r >= jb) continue;
+        const bool def = defic[j0 + r] != 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = tx + 16 * j;
+            if (c < cb) C[static_cast<int64_t>(j0 + r) * k + c0 + c] = def ? 0.0 : acc[i][j];
+        }
+    }
+}
+
+// C_T1T2 -= R_JT1^T R_JT2 for J < T1 <= T2; blockIdx.x enumerates the upper tiles
+__global__ __launch_bounds__(CT) void chol_trailing_kernel(double* Cb, int k, int64_t strideC, int J,
+                                                           int nb) {
+    const int b = blockIdx.y;
+    double* C = Cb + static_cast<int64_t>(b) * strideC;
+    const int n = nb - J - 1;
+    // blockIdx.x -> (u, v) with 0 <= u <= v < n, row-major over the upper triangle
+    int idx = blockIdx.x, u = 0;
+    while (idx >= n - u) {
+        idx -= n - u;
+        ++u;
+    }
+    const int v = u + idx;
+    const int j0 = J * CB;
+    const int jb = min(CB, k - j0);
+    const int r0 = (J + 1 + u) * CB, rb = min(CB, k - r0);
+    const int c0 = (J + 1 + v) * CB, cb = min(CB, k - c0);
+    __shared__ double As[CB][LP];
+    __shared__ double Bs[CB][LP];
+    load_tile(As, C, k, j0, r0, jb, rb);
+    load_tile(Bs, C, k, j0, c0, jb, cb);
+    __syncthreads();
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    double acc[4][4] = {};
+    tile_tn(As, Bs, jb, acc, ty, tx);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = ty + 16 * i;
+        if (r >= rb) continue;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = tx + 16 * j;
+            if (c < cb && (u != v || c >= r)) C[static_cast<int64_t>(r0 + r) * k + c0 + c] -= acc[i][j];
+        }
+    }
+}
+
+// Level d of the inverse: tile (I, I + d) for I = blockIdx.x.
+__global__ __launch_bounds__(CT) void chol_inverse_level_kernel(const double* Cb, int k, int64_t strideC,
+                                                                int d, double* Xb, float* Rib,
+                                                                int64_t strideInv) {
+    const int b = blockIdx.y;
+    const double* C = Cb + static_cast<int64_t>(b) * strideC;
+    double* X = Xb + static_cast<int64_t>(b) * strideInv;
+    float* Ri = Rib + static_cast<int64_t>(b) * strideInv;
+    const int I = blockIdx.x, Jc = I + d;
+    const int i0 = I * CB, ib = min(CB, k - i0);
+    const int c0 = Jc * CB, cb = min(CB, k - c0);
+    __shared__ double As[CB][LP];
+    __shared__ double Bs[CB][LP];
+    const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+    // S = sum_{U = I+1 .. Jc} R_IU X_UJc
+    double acc[4][4] = {};
+    for (int U = I + 1; U <= Jc; ++U) {
+        const int u0 = U * CB, ub = min(CB, k - u0);
+        load_tile_t(As, C, k, i0, u0, ib, ub);   // As[t][a] = R_IU[a][t]
+        load_tile(Bs, X, k, u0, c0, ub, cb);     // Bs[t][c] = X_UJc[t][c]
         __syncthreads();
-        for (int cg = 0; cg < k; cg += CT) {
-            const int c = cg + tid;
-            const bool active = c < k;
-            double acc[CB];
+        tile_tn(As, Bs, ub, acc, ty, tx);
+        __syncthreads();
+    }
+    // X_IJc = -D_I S
+    load_tile_t(As, X, k, i0, i0, ib, ib);       // As[t][a] = D_I[a][t]
 #pragma unroll
-            for (int i = 0; i < CB; ++i) acc[i] = 0.0;
-            for (int t0 = I + ib; t0 < k; t0 += CH) {
-                const int tc = min(CH, k - t0);
-                for (int idx = tid; idx < CH * CB; idx += CT) {
-                    const int tt = idx / CB, i = idx % CB;
-                    Rs[tt][i] = (tt < tc && i < ib && !defic[I + i])
-                                    ? C[static_cast<int64_t>(I + i) * k + t0 + tt] : 0.0;
-                }
-                __syncthreads();
-                if (active && c >= I) {
-                    for (int tt = 0; tt < tc; ++tt) {
-                        const int t = t0 + tt;
-                        if (t > c) break;
-                        const double xv = X[static_cast<int64_t>(t) * k + c];
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-                        for (int i = 0; i < CB; ++i) acc[i] += Rs[tt][i] * xv;
-                    }
-                }
-                __syncthreads();
-            }
-            if (active) {
-                if (c < I) {
+        for (int j = 0; j < 4; ++j) Bs[ty + 16 * i][tx + 16 * j] = acc[i][j];
+    __syncthreads();
+    double out[4][4] = {};
+    tile_tn(As, Bs, ib, out, ty, tx);
 #pragma unroll
-                    for (int i = 0; i < CB; ++i)
-                        if (i < ib) Ri[static_cast<int64_t>(I + i) * k + c] = 0.0f;
-                } else {
-                    double x[CB];
+    for (int i = 0; i < 4; ++i) {
+        const int r = ty + 16 * i;
 #pragma unroll
-                    for (int i = CB - 1; i >= 0; --i) {
-                        x[i] = 0.0;
-                        if (i < ib) {
-                            double v = ((I + i) == c ? 1.0 : 0.0) - acc[i];
-#pragma unroll
-                            for (int t2 = 0; t2 < CB; ++t2)
-                                if (t2 > i && t2 < ib) v -= Sd[i][t2] * x[t2];
-                            x[i] = v / Sd[i][i];
-                        }
-                    }
-#pragma unroll
-                    for (int i = 0; i < CB; ++i) {
-                        if (i < ib) {
-                            X[static_cast<int64_t>(I + i) * k + c] = x[i];
-                            Ri[static_cast<int64_t>(I + i) * k + c] = static_cast<float>(x[i]);
-                        }
-                    }
+        for (int j = 0; j < 4; ++j) {
+            const int c = tx + 16 * j;
+            if (r < ib && c < cb) {
+                const double v = -out[i][j];
+                X[static_cast<int64_t>(i0 + r) * k + c0 + c] = v;
+                if (Rib != nullptr) {
+                    Ri[static_cast<int64_t>(i0 + r) * k + c0 + c] = static_cast<float>(v);
                 }
             }
-            __syncthreads();
+            // the mirrored (lower) tile of the fp32 inverse is zero
+            if (Rib != nullptr && r < cb && c < ib) Ri[static_cast<int64_t>(c0 + r) * k + i0 + c] = 0.0f;
         }
     }
 }
@@ -223,10 +286,25 @@ __global__ __launch_bounds__(256) void fill_deficient_kernel(float* Qb, int rows
 }  // namespace
 
 hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, double* xinv,
-                           int64_t strideInv, int* defic, double tau_rel, int batch,
+                           int64_t strideInv, int* defic, double* diag0, double tau_rel, int batch,
                            hipStream_t stream) {
-    hipLaunchKernelGGL(cholesky_kernel, dim3(batch), dim3(CT), 0, stream, C, k, strideC, rinv32,
-                       xinv, strideInv, defic, tau_rel);
+    const int nb = (k + CB - 1) / CB;
+    for (int J = 0; J < nb; ++J) {
+        hipLaunchKernelGGL(chol_diag_kernel, dim3(batch), dim3(CT), 0, stream, C, k, strideC, J, diag0,
+                           defic, xinv, rinv32, strideInv, tau_rel);
+        const int n = nb - J - 1;
+        if (n > 0) {
+            hipLaunchKernelGGL(chol_panel_kernel, dim3(n, batch), dim3(CT), 0, stream, C, k, strideC, J,
+                               defic, xinv, strideInv);
+            hipLaunchKernelGGL(chol_trailing_kernel, dim3(n * (n + 1) / 2, batch), dim3(CT), 0, stream, C,
+                               k, strideC, J, nb);
+        }
+    }
+    if (rinv32 != nullptr) {
+        for (int d = 1; d < nb; ++d)
+            hipLaunchKernelGGL(chol_inverse_level_kernel, dim3(nb - d, batch), dim3(CT), 0, stream, C, k,
+                               strideC, d, xinv, rinv32, strideInv);
+    }
     return hipGetLastError();
 }
 

@@ -53,11 +53,13 @@ hipError_t launch_sketch(float* omega, int64_t l, int64_t k, int64_t stride, uin
                          uint64_t sketch_index0, int batch, hipStream_t stream);
 
 // Cholesky of the k x k fp64 Gram (in place, upper factor R in the upper
-// triangle). If rinv32 != nullptr, also writes the fp32 inverse of R' (R with
-// rank-deficient rows replaced by unit rows) into rinv32 (k x k), using xinv
-// (k x k fp64) as scratch. defic[b*k + j] = 1 marks deficient pivots.
+// triangle). xinv (k x k fp64) receives the inverses of the diagonal blocks
+// and, if rinv32 != nullptr, the whole inverse of R' (R with rank-deficient
+// rows replaced by unit rows), also written in fp32 into rinv32 (k x k, lower
+// triangle zero). defic[b*k + j] = 1 marks deficient pivots; diag0 (k fp64 per
+// matrix) keeps the original diagonal for the deficiency test.
 hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, double* xinv,
-                           int64_t strideInv, int* defic, double tau_rel, int batch,
+                           int64_t strideInv, int* defic, double* diag0, double tau_rel, int batch,
                            hipStream_t stream);
 // Replace columns flagged deficient by a deterministic generic unit vector.
 hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, const int* defic,
@@ -79,6 +81,6 @@ hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t row
                        int64_t ld, int64_t stride, int batch, float beta1, float beta2, float eps,
                        float bc1, float bc2, hipStream_t stream);
 
-constexpr int kJacobiBlock = 16;     // columns per Jacobi block (pairs of 32)
+constexpr int kJacobiBlock = 32;     // columns per Jacobi block (pairs of 64)
 
 }  // namespace galore

@@ -48,7 +48,7 @@ Shape make_shape(int64_t m, int64_t n, int r, int p) {
 // Workspace regions, each holding `batch` matrices at a fixed element stride.
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
-    size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offXt, offVt, offUr, offDef, offRot;
+    size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offXt, offVt, offUr, offDef, offDiag0, offRot;
     size_t total;
 };
 
@@ -77,6 +77,7 @@ Layout make_layout(const Shape& sh, int r, int batch) {
     L.offVt = take(B * L.strideKK * sizeof(float));
     L.offUr = take(B * L.strideUr * sizeof(float));
     L.offDef = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(int));
+    L.offDiag0 = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(double));
     L.offRot = take(B * kMaxSweeps * sizeof(int));
     L.total = off;
     return L;
@@ -182,7 +183,7 @@ hipError_t orth_pass(const Work& w, const float* In, float* Out, int64_t stride,
     hipError_t e = launch_gram64(gg, batch, st);
     if (e != hipSuccess) return e;
     e = launch_cholesky(w.d(L.offC), k, L.strideKK, w.f(L.offRinv), w.d(L.offXinv), L.strideKK,
-                        w.i(L.offDef), kDeficTol, batch, st);
+                        w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, st);
     if (e != hipSuccess) return e;
     e = gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st);
     if (e != hipSuccess) return e;
@@ -289,8 +290,8 @@ int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int
         gg.rows = l;
         gg.cols = k;
         GALORE_TRY(launch_gram64(gg, batch, stream));
-        GALORE_TRY(launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, nullptr, L.strideKK,
-                                   w.i(L.offDef), kDeficTol, batch, stream));
+        GALORE_TRY(launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, w.d(L.offXinv), L.strideKK,
+                                   w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, stream));
     }
     // a6: one-sided Jacobi on R: R V = U Sigma, V = left singular vectors of B
     float* Xt = w.f(L.offXt);

@@ -13,6 +13,8 @@
 //  * gram64: C = X^T X in fp64 with v_mfma_f64_16x16x4_f64 (the Gram matrices
 //    of the Cholesky-based orthonormalisation), only the upper tiles computed
 //    and mirrored.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace galore {
@@ -27,6 +29,85 @@ template <typename T>
 __device__ __forceinline__ float load_elem(const T* base, int64_t idx) {
     return to_f32(base[idx]);
 }
+
+// Four (fp32) or eight (bf16) consecutive elements from one 16-byte load.
+__device__ __forceinline__ void load_vec16(const float* src, float* out) {
+    const f32x4 x = *reinterpret_cast<const f32x4*>(src);
+    out[0] = x[0];
+    out[1] = x[1];
+    out[2] = x[2];
+    out[3] = x[3];
+}
+__device__ __forceinline__ void load_vec16(const bf16_t* src, float* out) {
+    const uint4 x = *reinterpret_cast<const uint4*>(src);
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        out[2 * e + 0] = __uint_as_float(w[e] << 16);
+        out[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+}
+
+// A BK x 128 operand tile v(kk, c) = base[(k0 + kk) * ld + c0 + c] whose
+// second index runs along memory (A stored M-contiguous, B N-contiguous):
+// each thread moves E rows of one 16-byte vector.
+template <typename T>
+struct ContigTile {
+    static constexpr int V = 16 / static_cast<int>(sizeof(T));   // elements per vector
+    static constexpr int CQ = 128 / V;                           // vectors per tile row
+    static constexpr int KR = NT / CQ;                           // rows per pass
+    static constexpr int E = BK / KR;                            // passes (V * E == 16)
+    __device__ static void load(const T* base, int64_t ld, int k0, int K, int c0, int C, bool vec, int t,
+                                float* r) {
+        const int cq = t % CQ, kr = t / CQ;
+        const int c = c0 + V * cq;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int gk = k0 + kr + KR * e;
+            const T* src = base + static_cast<int64_t>(gk) * ld + c;
+            if (gk < K && vec && c + V <= C) {
+                load_vec16(src, r + V * e);
+            } else {
+#pragma unroll
+                for (int v = 0; v < V; ++v) r[V * e + v] = (gk < K && c + v < C) ? to_f32(src[v]) : 0.0f;
+            }
+        }
+    }
+    __device__ static void store(float (*S)[128], int t, const float* r) {
+        const int cq = t % CQ, kr = t / CQ;
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+#pragma unroll
+            for (int v = 0; v < V; ++v) S[kr + KR * e][V * cq + v] = r[V * e + v];
+    }
+};
+
+// A BK x 128 operand tile v(kk, c) = base[(c0 + c) * ld + k0 + kk] whose
+// first (reduction) index runs along memory (A stored K-contiguous, B stored
+// K-contiguous): each thread moves 16 consecutive k of one row.
+template <typename T>
+struct KContigTile {
+    static constexpr int V = 16 / static_cast<int>(sizeof(T));
+    __device__ static void load(const T* base, int64_t ld, int k0, int K, int c0, int C, bool vec, int t,
+                                float* r) {
+        const int c = c0 + (t >> 1);
+        const int gk = k0 + (t & 1) * 16;
+        const T* src = base + static_cast<int64_t>(c) * ld + gk;
+        if (c < C && gk + 16 <= K && vec) {
+#pragma unroll
+            for (int q = 0; q < 16 / V; ++q) load_vec16(src + V * q, r + V * q);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) r[e] = (c < C && gk + e < K) ? to_f32(src[e]) : 0.0f;
+        }
+    }
+    __device__ static void store(float (*S)[128], int t, const float* r) {
+        const int c = t >> 1;
+        const int kk0 = (t & 1) * 16;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S[kk0 + e][c] = r[e];
+    }
+};
 
 template <ALayout LA, BLayout LB, typename TA, typename TB>
 __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, int b_vec) {
@@ -46,139 +127,16 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
     const int wm = wave >> 1;
     const int wn = wave & 1;
 
+    // A tile: rows i of op(A), B tile: columns j of op(B), both BK deep
+    using TileA = typename std::conditional<LA == ALayout::kKContig, KContigTile<TA>, ContigTile<TA>>::type;
+    using TileB = typename std::conditional<LB == BLayout::kKContig, KContigTile<TB>, ContigTile<TB>>::type;
+
     float ra[16];
     float rb[16];
-
-    // ---- global -> registers ------------------------------------------------
-    auto load_a = [&](int k0) {
-        if constexpr (LA == ALayout::kKContig) {
-            const int i = t >> 1;
-            const int kk0 = (t & 1) * 16;
-            const int gi = row0 + i;
-            const int gk = k0 + kk0;
-            if (gi < M && gk + 16 <= K && a_vec) {
-                const TA* src = A + static_cast<int64_t>(gi) * g.lda + gk;
-                if constexpr (sizeof(TA) == 4) {
-                    const f32x4* v = reinterpret_cast<const f32x4*>(src);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        f32x4 x = v[q];
-                        ra[4 * q + 0] = x[0];
-                        ra[4 * q + 1] = x[1];
-                        ra[4 * q + 2] = x[2];
-                        ra[4 * q + 3] = x[3];
-                    }
-                } else {
-                    const uint4* v = reinterpret_cast<const uint4*>(src);
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        uint4 x = v[q];
-                        uint32_t w[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            ra[8 * q + 2 * e + 0] = __uint_as_float(w[e] << 16);
-                            ra[8 * q + 2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
-                        }
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    ra[e] = (gi < M && gk + e < K)
-                                ? load_elem(A, static_cast<int64_t>(gi) * g.lda + gk + e)
-                                : 0.0f;
-                }
-            }
-        } else {
-            const int i = t & (BM - 1);
-            const int kb = t >> 7;
-            const int gi = row0 + i;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int gk = k0 + kb + 2 * e;
-                ra[e] = (gi < M && gk < K) ? load_elem(A, static_cast<int64_t>(gk) * g.lda + gi)
-                                           : 0.0f;
-            }
-        }
-    };
-    auto load_b = [&](int k0) {
-        if constexpr (LB == BLayout::kNContig) {
-            const int j = t & (BN - 1);
-            const int kb = t >> 7;
-            const int gj = col0 + j;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int gk = k0 + kb + 2 * e;
-                rb[e] = (gj < N && gk < K) ? load_elem(B, static_cast<int64_t>(gk) * g.ldb + gj)
-                                           : 0.0f;
-            }
-        } else {
-            const int j = t >> 1;
-            const int kk0 = (t & 1) * 16;
-            const int gj = col0 + j;
-            const int gk = k0 + kk0;
-            if (gj < N && gk + 16 <= K && b_vec) {
-                const TB* src = B + static_cast<int64_t>(gj) * g.ldb + gk;
-                if constexpr (sizeof(TB) == 4) {
-                    const f32x4* v = reinterpret_cast<const f32x4*>(src);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        f32x4 x = v[q];
-                        rb[4 * q + 0] = x[0];
-                        rb[4 * q + 1] = x[1];
-                        rb[4 * q + 2] = x[2];
-                        rb[4 * q + 3] = x[3];
-                    }
-                } else {
-                    const uint4* v = reinterpret_cast<const uint4*>(src);
-#pragma unroll
-                    for (int q = 0; q < 2; ++q) {
-                        uint4 x = v[q];
-                        uint32_t w[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            rb[8 * q + 2 * e + 0] = __uint_as_float(w[e] << 16);
-                            rb[8 * q + 2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
-                        }
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    rb[e] = (gj < N && gk + e < K)
-                                ? load_elem(B, static_cast<int64_t>(gj) * g.ldb + gk + e)
-                                : 0.0f;
-                }
-            }
-        }
-    };
-    // ---- registers -> LDS ---------------------------------------------------
-    auto store_a = [&](int buf) {
-        if constexpr (LA == ALayout::kKContig) {
-            const int i = t >> 1;
-            const int kk0 = (t & 1) * 16;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) As[buf][kk0 + e][i] = ra[e];
-        } else {
-            const int i = t & (BM - 1);
-            const int kb = t >> 7;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) As[buf][kb + 2 * e][i] = ra[e];
-        }
-    };
-    auto store_b = [&](int buf) {
-        if constexpr (LB == BLayout::kNContig) {
-            const int j = t & (BN - 1);
-            const int kb = t >> 7;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) Bs[buf][kb + 2 * e][j] = rb[e];
-        } else {
-            const int j = t >> 1;
-            const int kk0 = (t & 1) * 16;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) Bs[buf][kk0 + e][j] = rb[e];
-        }
-    };
+    auto load_a = [&](int k0) { TileA::load(A, g.lda, k0, K, row0, M, a_vec != 0, t, ra); };
+    auto load_b = [&](int k0) { TileB::load(B, g.ldb, k0, K, col0, N, b_vec != 0, t, rb); };
+    auto store_a = [&](int buf) { TileA::store(As[buf], t, ra); };
+    auto store_b = [&](int buf) { TileB::store(Bs[buf], t, rb); };
 
     f32x16 acc[2][2];
 #pragma unroll
@@ -247,15 +205,13 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
 template <ALayout LA, BLayout LB, typename TA, typename TB>
 hipError_t launch_one(const GemmArgs& g, int batch, hipStream_t stream) {
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, batch);
-    int a_vec = 0, b_vec = 0;
+    // 16-byte vector loads need every row start 16-byte aligned
     const int amul = (sizeof(TA) == 4) ? 4 : 8;   // elements per 16-byte vector
     const int bmul = (sizeof(TB) == 4) ? 4 : 8;
-    if (LA == ALayout::kKContig)
-        a_vec = (g.lda % amul == 0) && (g.strideA % amul == 0) &&
-                (reinterpret_cast<uintptr_t>(g.A) % 16 == 0);
-    if (LB == BLayout::kKContig)
-        b_vec = (g.ldb % bmul == 0) && (g.strideB % bmul == 0) &&
-                (reinterpret_cast<uintptr_t>(g.B) % 16 == 0);
+    const int a_vec = (g.lda % amul == 0) && (batch == 1 || g.strideA % amul == 0) &&
+                      (reinterpret_cast<uintptr_t>(g.A) % 16 == 0);
+    const int b_vec = (g.ldb % bmul == 0) && (batch == 1 || g.strideB % bmul == 0) &&
+                      (reinterpret_cast<uintptr_t>(g.B) % 16 == 0);
     hipLaunchKernelGGL((gemm_f32_kernel<LA, LB, TA, TB>), grid, dim3(NT), 0, stream, g, a_vec, b_vec);
     return hipGetLastError();
 }

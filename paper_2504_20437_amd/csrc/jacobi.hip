@@ -7,12 +7,19 @@
 // found by one-sided (Hestenes) Jacobi on the columns of X = R, accumulating
 // the rotations in V (X V = U Sigma, V = left singular vectors of B).
 //
-// Blocked for the GPU: the k columns form blocks of 16; a round-robin
+// Blocked for the GPU: the k columns form blocks of 32; a round-robin
 // tournament pairs the blocks so that every step is a set of disjoint pairs,
-// one workgroup per (pair, matrix). A workgroup forms the 32 x 32 fp64 Gram of
-// its two blocks, skips the pair if every column pair is already orthogonal to
-// the tolerance, otherwise diagonalises the small Gram with cyclic two-sided
-// Jacobi in LDS and applies the resulting rotation to its columns of X and V.
+// one workgroup per (pair, matrix). A workgroup
+//   1. forms the 64 x 64 fp64 Gram of its two blocks on the fp64 matrix cores
+//      (v_mfma_f64_16x16x4f64) from row chunks staged in LDS;
+//   2. skips the pair if every column pair is already orthogonal to the
+//      tolerance (relative off-diagonal), otherwise
+//   3. reduces the small Gram with cyclic two-sided Jacobi in LDS (fp64,
+//      parallel ordering: 63 rounds of 32 disjoint rotations per inner sweep,
+//      each round one read-modify-write of the Gram and of the accumulated
+//      rotation Theta), and
+//   4. applies Theta to its 64 columns of X and of V on the fp32 matrix cores
+//      (v_mfma_f32_32x32x2f32), 64-row chunks staged through LDS.
 // A sweep is nb - 1 steps; the matrix has converged when a whole sweep
 // rotates nothing (rotation counts per sweep live in device memory, so no
 // host synchronisation is needed). X and V are stored transposed (column c
@@ -23,9 +30,14 @@ namespace galore {
 namespace {
 
 constexpr int JB = kJacobiBlock;   // columns per block
-constexpr int JW = 2 * JB;         // columns per pair
-constexpr int JT = 256;            // threads
-constexpr int JR = 64;             // rows per staged chunk
+constexpr int JW = 2 * JB;         // columns per pair (64)
+constexpr int JT = 256;            // threads (4 waves)
+constexpr int GR = 32;             // rows per Gram chunk
+constexpr int AR = 64;             // rows per apply chunk
+constexpr int PD = JW + 1;         // padded LDS row
+constexpr int kInnerSweeps = 1;    // inner sweeps over the 64 x 64 Gram per step
+
+static_assert(JW == 64, "the pair kernels assume 64 columns per pair");
 
 __device__ __forceinline__ int ring_slot(int pos, int step, int n) {
     // circle method: slot 0 fixed, the others rotate by one per step
@@ -55,14 +67,19 @@ __global__ __launch_bounds__(256) void jacobi_prepare_kernel(const double* Rb, i
     }
 }
 
-__global__ __launch_bounds__(JT) void jacobi_step_kernel(float* Xtb, float* Vtb, int k,
-                                                         int64_t strideX, int nb, int step,
-                                                         int sweep, int* rotb, int max_sweeps,
-                                                         double tol) {
+// LDS plan (two 64 x 65 fp64 regions, 66.6 KB, two workgroups per CU):
+//   region A: Gram G (phases 1-3), then fp32 Theta + fp32 X chunk (phase 4)
+//   region B: fp64 row chunks for the Gram (phase 1), then Theta (phase 3)
+__global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* Vtb, int k,
+                                                            int64_t strideX, int nb, int step,
+                                                            int sweep, int* rotb, int max_sweeps,
+                                                            double tol) {
     const int b = blockIdx.y;
     int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
     if (sweep > 0 && rot[sweep - 1] == 0) return;     // converged in an earlier sweep
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
     const int h = blockIdx.x;
     const int bi = ring_slot(h, step, nb);
     const int bj = ring_slot(nb - 1 - h, step, nb);
@@ -70,9 +87,8 @@ __global__ __launch_bounds__(JT) void jacobi_step_kernel(float* Xtb, float* Vtb,
     float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
     float* Vt = Vtb + static_cast<int64_t>(b) * strideX;
 
-    __shared__ double Xs[JW][JR + 1];
-    __shared__ double Gs[JW][JW + 1];
-    __shared__ double Th[JW][JW + 1];
+    __shared__ double regA[JW][PD];
+    __shared__ double regB[JW][PD];
     __shared__ int col[JW];
     __shared__ double red[JT / 64];
     __shared__ double cs[JW / 2], sn[JW / 2];
@@ -86,66 +102,99 @@ __global__ __launch_bounds__(JT) void jacobi_step_kernel(float* Xtb, float* Vtb,
     }
     __syncthreads();
 
-    // ---- Gram of the pair's columns (fp64) ---------------------------------
-    const int gp = tid >> 3;
-    const int gq0 = (tid & 7) * 4;
-    double g[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int r0 = 0; r0 < k; r0 += JR) {
-        const int rc = min(JR, k - r0);
-        for (int idx = tid; idx < JW * JR; idx += JT) {
-            const int w = idx / JR, rr = idx % JR;
-            const int c = col[w];
-            Xs[w][rr] = (c >= 0 && rr < rc) ? static_cast<double>(Xt[static_cast<int64_t>(c) * k + r0 + rr])
-                                            : 0.0;
-        }
-        __syncthreads();
-        for (int rr = 0; rr < rc; ++rr) {
-            const double xp = Xs[gp][rr];
+    // ---- 1. Gram of the pair's 64 columns on the fp64 matrix cores ---------
+    double (*G)[PD] = regA;
+    double (*Xs)[PD] = regB;            // Xs[t][w], t < GR
+    {
+        // waves 0, 1, 2 own the quadrants (0,0), (0,1), (1,1) of the 64 x 64 Gram
+        const int qa = (wave == 2) ? 1 : 0;
+        const int qb = (wave == 0) ? 0 : 1;
+        f64x4 acc[2][2];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) g[e] += xp * Xs[gq0 + e][rr];
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+            for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+        const int l16 = lane & 15;
+        const int lk = lane >> 4;
+        for (int r0 = 0; r0 < k; r0 += GR) {
+            const int rc = min(GR, k - r0);
+            for (int idx = tid; idx < JW * GR; idx += JT) {
+                const int w = idx / GR, t = idx % GR;
+                const int c = col[w];
+                Xs[t][w] = (c >= 0 && t < rc) ? static_cast<double>(Xt[static_cast<int64_t>(c) * k + r0 + t]) : 0.0;
+            }
+            __syncthreads();
+            if (wave < 3) {
+#pragma unroll
+                for (int kk = 0; kk < GR; kk += 4) {
+                    const double a0 = Xs[kk + lk][32 * qa + l16];
+                    const double a1 = Xs[kk + lk][32 * qa + 16 + l16];
+                    const double b0 = Xs[kk + lk][32 * qb + l16];
+                    const double b1 = Xs[kk + lk][32 * qb + 16 + l16];
+                    acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
+                    acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
+                    acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
+                    acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+                }
+            }
+            __syncthreads();
+        }
+        // fp64 16x16 block layout: lane holds column (lane & 15); accumulator
+        // register v holds row 4 v + (lane >> 4).
+        if (wave < 3) {
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int i = 32 * qa + 16 * x + 4 * v + lk;
+                        const int j = 32 * qb + 16 * y + l16;
+                        G[i][j] = acc[x][y][v];
+                        if (qa != qb) G[j][i] = acc[x][y][v];
+                    }
         }
         __syncthreads();
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) Gs[gp][gq0 + e] = g[e];
-    __syncthreads();
 
-    // ---- convergence test: largest relative off-diagonal -------------------
-    double off = 0.0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const int q = gq0 + e;
-        if (q > gp) {
-            const double dd = Gs[gp][gp] * Gs[q][q];
-            if (dd > 0.0) {
-                const double rel = fabs(Gs[gp][q]) / sqrt(dd);
-                off = (rel > off || rel != rel) ? rel : off;
+    // ---- 2. convergence test: largest relative off-diagonal ----------------
+    {
+        double off = 0.0;
+        for (int idx = tid; idx < JW * JW; idx += JT) {
+            const int p = idx / JW, q = idx % JW;
+            if (q > p) {
+                const double dd = G[p][p] * G[q][q];
+                if (dd > 0.0) {
+                    const double rel = fabs(G[p][q]) / sqrt(dd);
+                    off = (rel > off || rel != rel) ? rel : off;
+                }
             }
         }
+        for (int o = 32; o > 0; o >>= 1) {
+            const double other = __shfl_xor(off, o);
+            off = (other > off || other != other) ? other : off;
+        }
+        if (lane == 0) red[wave] = off;
+        __syncthreads();
+        if (tid == 0) {
+            double m = red[0];
+            for (int w = 1; w < JT / 64; ++w) m = (red[w] > m || red[w] != red[w]) ? red[w] : m;
+            red[0] = m;
+        }
+        __syncthreads();
+        const double off_all = red[0];
+        if (!(off_all > tol) && off_all == off_all) return;   // already orthogonal
+        if (tid == 0) atomicAdd(&rot[sweep], 1);
     }
-    for (int o = 32; o > 0; o >>= 1) {
-        const double other = __shfl_xor(off, o);
-        off = (other > off || other != other) ? other : off;
-    }
-    if ((tid & 63) == 0) red[tid >> 6] = off;
-    __syncthreads();
-    if (tid == 0) {
-        double m = red[0];
-        for (int w = 1; w < JT / 64; ++w) m = (red[w] > m || red[w] != red[w]) ? red[w] : m;
-        red[0] = m;
-    }
-    __syncthreads();
-    const double off_all = red[0];
-    if (!(off_all > tol) && off_all == off_all) return;   // already orthogonal
-    if (tid == 0) atomicAdd(&rot[sweep], 1);
 
-    // ---- diagonalise the 32 x 32 Gram: cyclic parallel-order Jacobi --------
+    // ---- 3. reduce the 64 x 64 Gram: cyclic two-sided Jacobi ---------------
+    double (*Th)[PD] = regB;
     for (int idx = tid; idx < JW * JW; idx += JT) {
         const int i = idx / JW, j = idx % JW;
         Th[i][j] = (i == j) ? 1.0 : 0.0;
     }
     __syncthreads();
-    for (int isw = 0; isw < 16; ++isw) {
+    for (int isw = 0; isw < kInnerSweeps; ++isw) {
         if (tid == 0) any_rot = 0;
         __syncthreads();
         for (int st = 0; st < JW - 1; ++st) {
@@ -153,9 +202,9 @@ __global__ __launch_bounds__(JT) void jacobi_step_kernel(float* Xtb, float* Vtb,
                 int p = ring_slot(tid, st, JW);
                 int q = ring_slot(JW - 1 - tid, st, JW);
                 if (p > q) { const int tmp = p; p = q; q = tmp; }
-                const double a = Gs[p][p], bb = Gs[q][q], gm = Gs[p][q];
+                const double a = G[p][p], bb = G[q][q], gm = G[p][q];
                 double c = 1.0, s = 0.0;
-                if (fabs(gm) > 1e-14 * sqrt(a * bb)) {
+                if (fabs(gm) > 1e-15 * sqrt(a * bb)) {
                     const double zeta = (bb - a) / (2.0 * gm);
                     const double sg = (zeta >= 0.0) ? 1.0 : -1.0;
                     const double tt = sg / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
@@ -169,27 +218,28 @@ __global__ __launch_bounds__(JT) void jacobi_step_kernel(float* Xtb, float* Vtb,
                 qq[tid] = q;
             }
             __syncthreads();
-            // columns p, q of G and of Theta: x_p' = c x_p - s x_q, x_q' = s x_p + c x_q
+            // G <- J^T G J by 2 x 2 blocks (row pair ha, column pair hb);
+            // column p' = c p - s q, column q' = s p + c q
+            for (int idx = tid; idx < (JW / 2) * (JW / 2); idx += JT) {
+                const int ha = idx / (JW / 2), hb = idx % (JW / 2);
+                const int pa = pp[ha], qa2 = qq[ha], pb = pp[hb], qb2 = qq[hb];
+                const double ca = cs[ha], sa = sn[ha], cb = cs[hb], sb = sn[hb];
+                const double g00 = G[pa][pb], g01 = G[pa][qb2], g10 = G[qa2][pb], g11 = G[qa2][qb2];
+                const double r00 = ca * g00 - sa * g10, r01 = ca * g01 - sa * g11;
+                const double r10 = sa * g00 + ca * g10, r11 = sa * g01 + ca * g11;
+                G[pa][pb] = cb * r00 - sb * r01;
+                G[pa][qb2] = sb * r00 + cb * r01;
+                G[qa2][pb] = cb * r10 - sb * r11;
+                G[qa2][qb2] = sb * r10 + cb * r11;
+            }
+            // Theta <- Theta J
             for (int idx = tid; idx < (JW / 2) * JW; idx += JT) {
                 const int hh = idx / JW, row = idx % JW;
                 const int p = pp[hh], q = qq[hh];
                 const double c = cs[hh], s = sn[hh];
-                const double gpv = Gs[row][p], gqv = Gs[row][q];
-                Gs[row][p] = c * gpv - s * gqv;
-                Gs[row][q] = s * gpv + c * gqv;
                 const double tp = Th[row][p], tq = Th[row][q];
                 Th[row][p] = c * tp - s * tq;
                 Th[row][q] = s * tp + c * tq;
-            }
-            __syncthreads();
-            // rows p, q of G
-            for (int idx = tid; idx < (JW / 2) * JW; idx += JT) {
-                const int hh = idx / JW, cc = idx % JW;
-                const int p = pp[hh], q = qq[hh];
-                const double c = cs[hh], s = sn[hh];
-                const double gpv = Gs[p][cc], gqv = Gs[q][cc];
-                Gs[p][cc] = c * gpv - s * gqv;
-                Gs[q][cc] = s * gpv + c * gqv;
             }
             __syncthreads();
         }
@@ -198,35 +248,48 @@ __global__ __launch_bounds__(JT) void jacobi_step_kernel(float* Xtb, float* Vtb,
         if (done) break;
     }
 
-    // ---- apply Theta to the pair's columns of X and V ----------------------
-    const int ar = tid & (JR - 1);
-    const int acg = tid >> 6;          // 4 groups of 8 output columns
+    // ---- 4. X_P <- X_P Theta, V_P <- V_P Theta on the fp32 matrix cores ----
+    float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&regA[0][0]);            // 64 x 65 fp32
+    float (*Xc)[PD] = reinterpret_cast<float (*)[PD]>(&regA[0][0]) + JW;       // 64 x 65 fp32
+    for (int idx = tid; idx < JW * JW; idx += JT) {
+        const int i = idx / JW, j = idx % JW;
+        Tf[i][j] = static_cast<float>(Th[i][j]);
+    }
+    __syncthreads();
+    const int tm = wave >> 1, tn = wave & 1;
+    const int l32 = lane & 31, lk2 = lane >> 5;
     for (int pass = 0; pass < 2; ++pass) {
         float* M = (pass == 0) ? Xt : Vt;
-        for (int r0 = 0; r0 < k; r0 += JR) {
-            const int rc = min(JR, k - r0);
-            for (int idx = tid; idx < JW * JR; idx += JT) {
-                const int w = idx / JR, rr = idx % JR;
+        for (int r0 = 0; r0 < k; r0 += AR) {
+            const int rc = min(AR, k - r0);
+            for (int idx = tid; idx < JW * AR; idx += JT) {
+                const int w = idx / AR, t = idx % AR;
                 const int c = col[w];
-                Xs[w][rr] = (c >= 0 && rr < rc) ? static_cast<double>(M[static_cast<int64_t>(c) * k + r0 + rr])
-                                                : 0.0;
+                Xc[w][t] = (c >= 0 && t < rc) ? M[static_cast<int64_t>(c) * k + r0 + t] : 0.0f;
             }
             __syncthreads();
-            if (ar < rc) {
-                double out[8];
+            f32x16 acc;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) out[e] = 0.0;
-#pragma unroll 2
-                for (int p = 0; p < JW; ++p) {
-                    const double xv = Xs[p][ar];
+            for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+#pragma unroll 8
+            for (int kk = 0; kk < JW; kk += 2) {
+                const float a = Xc[kk + lk2][32 * tm + l32];   // A[t][w] = X[t][w]
+                const float bv = Tf[kk + lk2][32 * tn + l32];  // B[w][c] = Theta[w][c]
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
+            }
+            __syncthreads();
+            // 32x32 block layout: lane holds column (lane & 31) and rows
+            // (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) out[e] += xv * Th[p][acg * 8 + e];
-                }
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int c = col[acg * 8 + e];
-                    if (c >= 0) M[static_cast<int64_t>(c) * k + r0 + ar] = static_cast<float>(out[e]);
-                }
+            for (int v = 0; v < 16; ++v) {
+                const int t = 32 * tm + (v & 3) + 8 * (v >> 2) + 4 * lk2;
+                Xc[32 * tn + l32][t] = acc[v];
+            }
+            __syncthreads();
+            for (int idx = tid; idx < JW * AR; idx += JT) {
+                const int w = idx / AR, t = idx % AR;
+                const int c = col[w];
+                if (c >= 0 && t < rc) M[static_cast<int64_t>(c) * k + r0 + t] = Xc[w][t];
             }
             __syncthreads();
         }
