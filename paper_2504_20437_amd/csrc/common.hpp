@@ -64,17 +64,18 @@ hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, dou
 // Replace columns flagged deficient by a deterministic generic unit vector.
 hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, const int* defic,
                                  int batch, hipStream_t stream);
-// Xt (k x k, transposed storage) = R^T in fp32 from the fp64 factor; Vt = I.
-hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Xt, float* Vt,
-                                 int64_t strideX, int* rot, int max_sweeps, int batch,
-                                 hipStream_t stream);
-hipError_t launch_jacobi_step(float* Xt, float* Vt, int k, int64_t strideX, int nblocks, int step,
-                              int sweep, int* rot, int max_sweeps, double tol, int batch,
+// Yt (k x k, column c contiguous) = columns of Y = R^T in fp32 from the fp64
+// factor (the row-major upper triangle of R); clears the rotation counters.
+hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Yt, int64_t strideX,
+                                 int* rot, int max_sweeps, int batch, hipStream_t stream);
+// theta: (nblocks / 2) x 64 x 64 fp32 per matrix; flags: nblocks / 2 ints per matrix
+hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
+                              int max_sweeps, double tol, float* theta, int* flags, int batch,
                               hipStream_t stream);
-hipError_t launch_jacobi_finalize(const float* Xt, const float* Vt, int k, int64_t strideX,
-                                  int r, float* Ur, int64_t strideUr, float* sigma,
-                                  int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
-                                  int batch, hipStream_t stream);
+// scratch: at least 2 k + r doubles per matrix at stride strideScratch (doubles)
+hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
+                                  float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
+                                  double* scratch, int64_t strideScratch, int batch, hipStream_t stream);
 hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strideP, int batch,
                            hipStream_t stream);
 hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t rows, int64_t cols,

@@ -48,7 +48,9 @@ Shape make_shape(int64_t m, int64_t n, int r, int p) {
 // Workspace regions, each holding `batch` matrices at a fixed element stride.
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
-    size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offXt, offVt, offUr, offDef, offDiag0, offRot;
+    size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
+        offTheta, offFlag;
+    int64_t strideTheta, strideFlag;
     size_t total;
 };
 
@@ -73,12 +75,17 @@ Layout make_layout(const Shape& sh, int r, int batch) {
     L.offC = take(B * L.strideKK * sizeof(double));
     L.offXinv = take(B * L.strideKK * sizeof(double));
     L.offRinv = take(B * L.strideKK * sizeof(float));
-    L.offXt = take(B * L.strideKK * sizeof(float));
-    L.offVt = take(B * L.strideKK * sizeof(float));
+    L.offYt = take(B * L.strideKK * sizeof(float));
     L.offUr = take(B * L.strideUr * sizeof(float));
     L.offDef = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(int));
     L.offDiag0 = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(double));
     L.offRot = take(B * kMaxSweeps * sizeof(int));
+    const int64_t nblk = (k + kJacobiBlock - 1) / kJacobiBlock;
+    const int64_t npairs = (nblk + (nblk & 1)) / 2;
+    L.strideTheta = npairs * (2 * kJacobiBlock) * (2 * kJacobiBlock);
+    L.strideFlag = npairs;
+    L.offTheta = take(B * L.strideTheta * sizeof(float));
+    L.offFlag = take(B * L.strideFlag * sizeof(int));
     L.total = off;
     return L;
 }
@@ -293,23 +300,23 @@ int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int
         GALORE_TRY(launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, w.d(L.offXinv), L.strideKK,
                                    w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, stream));
     }
-    // a6: one-sided Jacobi on R: R V = U Sigma, V = left singular vectors of B
-    float* Xt = w.f(L.offXt);
-    float* Vt = w.f(L.offVt);
+    // a6: one-sided Jacobi on the columns of Y = R^T: Y W = U Sigma, U = left
+    // singular vectors of B
+    float* Yt = w.f(L.offYt);
     int* rot = w.i(L.offRot);
-    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Xt, Vt, L.strideKK, rot,
-                                     kMaxSweeps, batch, stream));
+    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Yt, L.strideKK, rot, kMaxSweeps, batch,
+                                     stream));
     const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
     const int nb = nblk_real + (nblk_real & 1);
-    if (nb >= 2) {
-        for (int sw = 0; sw < kMaxSweeps; ++sw)
-            for (int stp = 0; stp < nb - 1; ++stp)
-                GALORE_TRY(launch_jacobi_step(Xt, Vt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps,
-                                              kJacobiTol, batch, stream));
-    }
+    for (int sw = 0; sw < kMaxSweeps; ++sw)
+        for (int stp = 0; stp < nb - 1; ++stp)
+            GALORE_TRY(launch_jacobi_step(Yt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol,
+                                          w.f(L.offTheta), w.i(L.offFlag), batch, stream));
     float* Ur = w.f(L.offUr);
-    GALORE_TRY(launch_jacobi_finalize(Xt, Vt, k, L.strideKK, r, Ur, L.strideUr, sigma,
-                                      stride_sigma, rot, kMaxSweeps, info, batch, stream));
+    // the rotation buffers are free again: scratch of the orthonormal completion
+    GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
+                                      kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
+                                      L.strideTheta / 2, batch, stream));
     // a7: P = Q U_B[:, :r], canonical signs
     {
         GemmArgs a{};

@@ -3,13 +3,17 @@
 //
 // The left singular vectors of B are the eigenvectors of B B^T = Z^T Z with
 // Z = A^T Q = B^T. The host factors that Gram in fp64 as R^T R (Cholesky), so
-// they are also the right singular vectors of the k x k factor R. They are
-// found by one-sided (Hestenes) Jacobi on the columns of X = R, accumulating
-// the rotations in V (X V = U Sigma, V = left singular vectors of B).
+// they are also the left singular vectors of Y = R^T (k x k). One-sided
+// (Hestenes) Jacobi rotates the columns of Y until they are mutually
+// orthogonal: Y W = U Sigma, so sigma_j is the norm of column j and u_j the
+// column divided by it; no rotation needs to be accumulated. Y is stored by
+// columns (column c contiguous), which is exactly the row-major upper
+// triangle of R.
 //
 // Blocked for the GPU: the k columns form blocks of 32; a round-robin
-// tournament pairs the blocks so that every step is a set of disjoint pairs,
-// one workgroup per (pair, matrix). A workgroup
+// tournament pairs the blocks so that every step is a set of disjoint pairs.
+// A step is two launches over all pairs of all matrices of the batch:
+//   pair kernel (one workgroup per pair and matrix)
 //   1. forms the 64 x 64 fp64 Gram of its two blocks on the fp64 matrix cores
 //      (v_mfma_f64_16x16x4f64) from row chunks staged in LDS;
 //   2. skips the pair if every column pair is already orthogonal to the
@@ -17,13 +21,19 @@
 //   3. reduces the small Gram with cyclic two-sided Jacobi in LDS (fp64,
 //      parallel ordering: 63 rounds of 32 disjoint rotations per inner sweep,
 //      each round one read-modify-write of the Gram and of the accumulated
-//      rotation Theta), and
-//   4. applies Theta to its 64 columns of X and of V on the fp32 matrix cores
-//      (v_mfma_f32_32x32x2f32), 64-row chunks staged through LDS.
+//      rotation Theta) and writes Theta;
+//   apply kernel (one workgroup per pair, 64-row chunk and matrix)
+//   4. applies Theta to its rows of the pair's 64 columns of Y on the fp32
+//      matrix cores (v_mfma_f32_32x32x2f32).
 // A sweep is nb - 1 steps; the matrix has converged when a whole sweep
 // rotates nothing (rotation counts per sweep live in device memory, so no
-// host synchronisation is needed). X and V are stored transposed (column c
-// contiguous) so that a block of columns is a contiguous slab.
+// host synchronisation is needed).
+//
+// Rank deficiency: a pivot the Cholesky found dependent zeroes a row of R,
+// i.e. a column of Y; zero columns are never rotated and stay exactly zero.
+// If one of them is among the r leading columns, the finalize kernel replaces
+// it by an orthonormal completion (unit vectors orthogonalised twice against
+// the columns already kept), the singular value staying 0.
 #include "common.hpp"
 
 namespace galore {
@@ -48,32 +58,32 @@ __device__ __forceinline__ int ring_slot(int pos, int step, int n) {
 }
 
 __global__ __launch_bounds__(256) void jacobi_prepare_kernel(const double* Rb, int k,
-                                                             int64_t strideR, float* Xtb,
-                                                             float* Vtb, int64_t strideX, int* rotb,
+                                                             int64_t strideR, float* Ytb,
+                                                             int64_t strideX, int* rotb,
                                                              int max_sweeps) {
     const int b = blockIdx.y;
     const double* R = Rb + static_cast<int64_t>(b) * strideR;
-    float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
-    float* Vt = Vtb + static_cast<int64_t>(b) * strideX;
+    float* Yt = Ytb + static_cast<int64_t>(b) * strideX;
     if (blockIdx.x == 0 && threadIdx.x < static_cast<unsigned>(max_sweeps))
         rotb[static_cast<int64_t>(b) * max_sweeps + threadIdx.x] = 0;
     const int64_t total = static_cast<int64_t>(k) * k;
+    // column c of Y = R^T is row c of R
     for (int64_t pos = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; pos < total;
          pos += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int c = static_cast<int>(pos / k);
         const int i = static_cast<int>(pos - static_cast<int64_t>(c) * k);
-        Xt[pos] = (i <= c) ? static_cast<float>(R[static_cast<int64_t>(i) * k + c]) : 0.0f;
-        Vt[pos] = (i == c) ? 1.0f : 0.0f;
+        Yt[pos] = (i >= c) ? static_cast<float>(R[pos]) : 0.0f;
     }
 }
 
-// LDS plan (two 64 x 65 fp64 regions, 66.6 KB, two workgroups per CU):
-//   region A: Gram G (phases 1-3), then fp32 Theta + fp32 X chunk (phase 4)
-//   region B: fp64 row chunks for the Gram (phase 1), then Theta (phase 3)
-__global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* Vtb, int k,
-                                                            int64_t strideX, int nb, int step,
-                                                            int sweep, int* rotb, int max_sweeps,
-                                                            double tol) {
+// Step of the block Jacobi, part 1 (one workgroup per pair and matrix):
+// Gram of the pair's 64 columns, convergence test, reduction of the small
+// Gram; writes Theta (fp32, 64 x 64) and whether the pair rotates.
+// LDS: region A holds the Gram (fp64, 64 x 65), region B first the two
+// fp64 staging buffers of the Gram's row chunks, then Theta (fp64).
+__global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(const float* Xtb, int k, int64_t strideX, int nb,
+                                                            int step, int sweep, int* rotb, int max_sweeps,
+                                                            double tol, float* thetab, int* flagb) {
     const int b = blockIdx.y;
     int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
     if (sweep > 0 && rot[sweep - 1] == 0) return;     // converged in an earlier sweep
@@ -81,13 +91,13 @@ __global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* V
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int h = blockIdx.x;
+    const int npairs = nb / 2;
     const int bi = ring_slot(h, step, nb);
     const int bj = ring_slot(nb - 1 - h, step, nb);
+    const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
+    int* flag = flagb + static_cast<int64_t>(b) * npairs + h;
 
-    float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
-    float* Vt = Vtb + static_cast<int64_t>(b) * strideX;
-
-    __shared__ double regA[JW][PD];
+    __shared__ double G[JW][PD];
     __shared__ double regB[JW][PD];
     __shared__ int col[JW];
     __shared__ double red[JT / 64];
@@ -102,57 +112,75 @@ __global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* V
     }
     __syncthreads();
 
-    // ---- 1. Gram of the pair's 64 columns on the fp64 matrix cores ---------
-    double (*G)[PD] = regA;
-    double (*Xs)[PD] = regB;            // Xs[t][w], t < GR
+    // ---- 1. Gram of the pair's columns: the 10 upper 16 x 16 tiles of the
+    //         64 x 64 result spread over the 4 waves, row chunks of GR rows
+    //         double-buffered in LDS with the next chunk prefetched in registers.
     {
-        // waves 0, 1, 2 own the quadrants (0,0), (0,1), (1,1) of the 64 x 64 Gram
-        const int qa = (wave == 2) ? 1 : 0;
-        const int qb = (wave == 0) ? 0 : 1;
-        f64x4 acc[2][2];
+        double (*Xs0)[PD] = regB;            // rows 0 .. GR-1
+        double (*Xs1)[PD] = regB + GR;       // rows GR .. 2GR-1
+        // tiles (ti, tj), ti <= tj, per wave; -1 = none
+        const int tiles[4][3][2] = {{{0, 0}, {0, 1}, {0, 2}}, {{0, 3}, {1, 1}, {1, 2}},
+                                    {{1, 3}, {2, 2}, {-1, -1}}, {{2, 3}, {3, 3}, {-1, -1}}};
+        f64x4 acc[3];
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
-#pragma unroll
-            for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+        for (int x = 0; x < 3; ++x) acc[x] = f64x4{0.0, 0.0, 0.0, 0.0};
         const int l16 = lane & 15;
         const int lk = lane >> 4;
-        for (int r0 = 0; r0 < k; r0 += GR) {
-            const int rc = min(GR, k - r0);
-            for (int idx = tid; idx < JW * GR; idx += JT) {
+        constexpr int PER = JW * GR / JT;    // values per thread per chunk (8)
+        float pre[PER];
+        auto fetch = [&](int r0) {
+#pragma unroll
+            for (int e = 0; e < PER; ++e) {
+                const int idx = tid + JT * e;
                 const int w = idx / GR, t = idx % GR;
                 const int c = col[w];
-                Xs[t][w] = (c >= 0 && t < rc) ? static_cast<double>(Xt[static_cast<int64_t>(c) * k + r0 + t]) : 0.0;
+                pre[e] = (c >= 0 && r0 + t < k) ? Xt[static_cast<int64_t>(c) * k + r0 + t] : 0.0f;
             }
-            __syncthreads();
-            if (wave < 3) {
+        };
+        auto stash = [&](double (*Xs)[PD]) {
 #pragma unroll
-                for (int kk = 0; kk < GR; kk += 4) {
-                    const double a0 = Xs[kk + lk][32 * qa + l16];
-                    const double a1 = Xs[kk + lk][32 * qa + 16 + l16];
-                    const double b0 = Xs[kk + lk][32 * qb + l16];
-                    const double b1 = Xs[kk + lk][32 * qb + 16 + l16];
-                    acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
-                    acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
-                    acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
-                    acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+            for (int e = 0; e < PER; ++e) {
+                const int idx = tid + JT * e;
+                Xs[idx % GR][idx / GR] = static_cast<double>(pre[e]);
+            }
+        };
+        const int nchunk = (k + GR - 1) / GR;
+        fetch(0);
+        stash(Xs0);
+        __syncthreads();
+        for (int ch = 0; ch < nchunk; ++ch) {
+            double (*cur)[PD] = (ch & 1) ? Xs1 : Xs0;
+            double (*nxt)[PD] = (ch & 1) ? Xs0 : Xs1;
+            if (ch + 1 < nchunk) fetch((ch + 1) * GR);
+#pragma unroll
+            for (int x = 0; x < 3; ++x) {
+                const int ti = tiles[wave][x][0], tj = tiles[wave][x][1];
+                if (ti >= 0) {
+#pragma unroll
+                    for (int kk = 0; kk < GR; kk += 4) {
+                        const double a = cur[kk + lk][16 * ti + l16];
+                        const double bv = cur[kk + lk][16 * tj + l16];
+                        acc[x] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, bv, acc[x], 0, 0, 0);
+                    }
                 }
             }
+            if (ch + 1 < nchunk) stash(nxt);
             __syncthreads();
         }
         // fp64 16x16 block layout: lane holds column (lane & 15); accumulator
         // register v holds row 4 v + (lane >> 4).
-        if (wave < 3) {
 #pragma unroll
-            for (int x = 0; x < 2; ++x)
+        for (int x = 0; x < 3; ++x) {
+            const int ti = tiles[wave][x][0], tj = tiles[wave][x][1];
+            if (ti >= 0) {
 #pragma unroll
-                for (int y = 0; y < 2; ++y)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int i = 32 * qa + 16 * x + 4 * v + lk;
-                        const int j = 32 * qb + 16 * y + l16;
-                        G[i][j] = acc[x][y][v];
-                        if (qa != qb) G[j][i] = acc[x][y][v];
-                    }
+                for (int v = 0; v < 4; ++v) {
+                    const int i = 16 * ti + 4 * v + lk;
+                    const int j = 16 * tj + l16;
+                    G[i][j] = acc[x][v];
+                    G[j][i] = acc[x][v];
+                }
+            }
         }
         __syncthreads();
     }
@@ -183,8 +211,12 @@ __global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* V
         }
         __syncthreads();
         const double off_all = red[0];
-        if (!(off_all > tol) && off_all == off_all) return;   // already orthogonal
-        if (tid == 0) atomicAdd(&rot[sweep], 1);
+        const bool skip = !(off_all > tol) && off_all == off_all;   // already orthogonal
+        if (tid == 0) {
+            *flag = skip ? 0 : 1;
+            if (!skip) atomicAdd(&rot[sweep], 1);
+        }
+        if (skip) return;
     }
 
     // ---- 3. reduce the 64 x 64 Gram: cyclic two-sided Jacobi ---------------
@@ -220,26 +252,31 @@ __global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* V
             __syncthreads();
             // G <- J^T G J by 2 x 2 blocks (row pair ha, column pair hb);
             // column p' = c p - s q, column q' = s p + c q
-            for (int idx = tid; idx < (JW / 2) * (JW / 2); idx += JT) {
-                const int ha = idx / (JW / 2), hb = idx % (JW / 2);
-                const int pa = pp[ha], qa2 = qq[ha], pb = pp[hb], qb2 = qq[hb];
-                const double ca = cs[ha], sa = sn[ha], cb = cs[hb], sb = sn[hb];
-                const double g00 = G[pa][pb], g01 = G[pa][qb2], g10 = G[qa2][pb], g11 = G[qa2][qb2];
-                const double r00 = ca * g00 - sa * g10, r01 = ca * g01 - sa * g11;
-                const double r10 = sa * g00 + ca * g10, r11 = sa * g01 + ca * g11;
-                G[pa][pb] = cb * r00 - sb * r01;
-                G[pa][qb2] = sb * r00 + cb * r01;
-                G[qa2][pb] = cb * r10 - sb * r11;
-                G[qa2][qb2] = sb * r10 + cb * r11;
-            }
-            // Theta <- Theta J
-            for (int idx = tid; idx < (JW / 2) * JW; idx += JT) {
-                const int hh = idx / JW, row = idx % JW;
-                const int p = pp[hh], q = qq[hh];
-                const double c = cs[hh], s = sn[hh];
-                const double tp = Th[row][p], tq = Th[row][q];
-                Th[row][p] = c * tp - s * tq;
-                Th[row][q] = s * tp + c * tq;
+            {
+                const int hb = tid & 31;
+                const int pb = pp[hb], qb2 = qq[hb];
+                const double cb = cs[hb], sb = sn[hb];
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int ha = (tid >> 5) + 8 * m;
+                    const int pa = pp[ha], qa2 = qq[ha];
+                    const double ca = cs[ha], sa = sn[ha];
+                    const double g00 = G[pa][pb], g01 = G[pa][qb2], g10 = G[qa2][pb], g11 = G[qa2][qb2];
+                    const double r00 = ca * g00 - sa * g10, r01 = ca * g01 - sa * g11;
+                    const double r10 = sa * g00 + ca * g10, r11 = sa * g01 + ca * g11;
+                    G[pa][pb] = cb * r00 - sb * r01;
+                    G[pa][qb2] = sb * r00 + cb * r01;
+                    G[qa2][pb] = cb * r10 - sb * r11;
+                    G[qa2][qb2] = sb * r10 + cb * r11;
+                }
+                // Theta <- Theta J: rows (tid >> 5) + 8 m of column pair hb
+#pragma unroll
+                for (int m = 0; m < 8; ++m) {
+                    const int row = (tid >> 5) + 8 * m;
+                    const double tp = Th[row][pb], tq = Th[row][qb2];
+                    Th[row][pb] = cb * tp - sb * tq;
+                    Th[row][qb2] = sb * tp + cb * tq;
+                }
             }
             __syncthreads();
         }
@@ -247,77 +284,102 @@ __global__ __launch_bounds__(JT, 2) void jacobi_step_kernel(float* Xtb, float* V
         __syncthreads();
         if (done) break;
     }
+    float* theta = thetab + (static_cast<int64_t>(b) * npairs + h) * (JW * JW);
+    for (int idx = tid; idx < JW * JW; idx += JT) theta[idx] = static_cast<float>(Th[idx / JW][idx % JW]);
+}
 
-    // ---- 4. X_P <- X_P Theta, V_P <- V_P Theta on the fp32 matrix cores ----
-    float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&regA[0][0]);            // 64 x 65 fp32
-    float (*Xc)[PD] = reinterpret_cast<float (*)[PD]>(&regA[0][0]) + JW;       // 64 x 65 fp32
-    for (int idx = tid; idx < JW * JW; idx += JT) {
-        const int i = idx / JW, j = idx % JW;
-        Tf[i][j] = static_cast<float>(Th[i][j]);
+// Step of the block Jacobi, part 2 (one workgroup per pair, 64-row chunk and
+// matrix): Y_P <- Y_P Theta on the fp32 matrix cores.
+__global__ __launch_bounds__(JT) void jacobi_apply_kernel(float* Xtb, int k, int64_t strideX,
+                                                          int nb, int step, int sweep, const int* rotb,
+                                                          int max_sweeps, const float* thetab,
+                                                          const int* flagb) {
+    const int b = blockIdx.z;
+    const int h = blockIdx.x;
+    const int npairs = nb / 2;
+    const int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
+    if (sweep > 0 && rot[sweep - 1] == 0) return;
+    if (flagb[static_cast<int64_t>(b) * npairs + h] == 0) return;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int bi = ring_slot(h, step, nb);
+    const int bj = ring_slot(nb - 1 - h, step, nb);
+    const int r0 = blockIdx.y * AR;
+    const int rc = min(AR, k - r0);
+
+    __shared__ float Tf[JW][PD];
+    __shared__ float Xc[JW][PD];
+    __shared__ int col[JW];
+    if (tid < JW) {
+        const int blk = (tid < JB) ? bi : bj;
+        const int c = blk * JB + (tid & (JB - 1));
+        col[tid] = (c < k) ? c : -1;
     }
+    const float* theta = thetab + (static_cast<int64_t>(b) * npairs + h) * (JW * JW);
+    for (int idx = tid; idx < JW * JW; idx += JT) Tf[idx / JW][idx % JW] = theta[idx];
     __syncthreads();
     const int tm = wave >> 1, tn = wave & 1;
     const int l32 = lane & 31, lk2 = lane >> 5;
-    for (int pass = 0; pass < 2; ++pass) {
-        float* M = (pass == 0) ? Xt : Vt;
-        for (int r0 = 0; r0 < k; r0 += AR) {
-            const int rc = min(AR, k - r0);
-            for (int idx = tid; idx < JW * AR; idx += JT) {
-                const int w = idx / AR, t = idx % AR;
-                const int c = col[w];
-                Xc[w][t] = (c >= 0 && t < rc) ? M[static_cast<int64_t>(c) * k + r0 + t] : 0.0f;
-            }
-            __syncthreads();
-            f32x16 acc;
+    {
+        float* M = Xtb + static_cast<int64_t>(b) * strideX;
+        for (int idx = tid; idx < JW * AR; idx += JT) {
+            const int w = idx / AR, t = idx % AR;
+            const int c = col[w];
+            Xc[w][t] = (c >= 0 && t < rc) ? M[static_cast<int64_t>(c) * k + r0 + t] : 0.0f;
+        }
+        __syncthreads();
+        f32x16 acc;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+        for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
 #pragma unroll 8
-            for (int kk = 0; kk < JW; kk += 2) {
-                const float a = Xc[kk + lk2][32 * tm + l32];   // A[t][w] = X[t][w]
-                const float bv = Tf[kk + lk2][32 * tn + l32];  // B[w][c] = Theta[w][c]
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
-            }
-            __syncthreads();
-            // 32x32 block layout: lane holds column (lane & 31) and rows
-            // (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
+        for (int kk = 0; kk < JW; kk += 2) {
+            const float a = Xc[kk + lk2][32 * tm + l32];   // A[t][w] = X[t][w]
+            const float bv = Tf[kk + lk2][32 * tn + l32];  // B[w][c] = Theta[w][c]
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
+        }
+        __syncthreads();
+        // 32x32 block layout: lane holds column (lane & 31) and rows
+        // (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int t = 32 * tm + (v & 3) + 8 * (v >> 2) + 4 * lk2;
-                Xc[32 * tn + l32][t] = acc[v];
-            }
-            __syncthreads();
-            for (int idx = tid; idx < JW * AR; idx += JT) {
-                const int w = idx / AR, t = idx % AR;
-                const int c = col[w];
-                if (c >= 0 && t < rc) M[static_cast<int64_t>(c) * k + r0 + t] = Xc[w][t];
-            }
-            __syncthreads();
+        for (int v = 0; v < 16; ++v) {
+            const int t = 32 * tm + (v & 3) + 8 * (v >> 2) + 4 * lk2;
+            Xc[32 * tn + l32][t] = acc[v];
+        }
+        __syncthreads();
+        for (int idx = tid; idx < JW * AR; idx += JT) {
+            const int w = idx / AR, t = idx % AR;
+            const int c = col[w];
+            if (c >= 0 && t < rc) M[static_cast<int64_t>(c) * k + r0 + t] = Xc[w][t];
         }
     }
 }
 
-__global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Xtb, const float* Vtb,
-                                                              int k, int64_t strideX, int r,
-                                                              float* Urb, int64_t strideUr,
+// sigma_j = |y_j| (fp64), order descending (ties by index, NaN last);
+// Ur[:, j] = y_perm(j) / sigma_perm(j) for the r leading columns, zero columns
+// completed orthonormally. scratch: 2 k + r doubles per matrix.
+__global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, int k, int64_t strideX,
+                                                              int r, float* Urb, int64_t strideUr,
                                                               float* sigma, int64_t stride_sigma,
-                                                              const int* rotb, int max_sweeps,
-                                                              int* info) {
+                                                              const int* rotb, int max_sweeps, int* info,
+                                                              double* scratchb, int64_t strideScratch) {
     extern __shared__ unsigned char smem[];
     double* sig = reinterpret_cast<double*>(smem);
     int* perm = reinterpret_cast<int*>(sig + k);
+    __shared__ double red[4];
+    __shared__ int nkeep_s;
     const int b = blockIdx.x;
-    const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
-    const float* Vt = Vtb + static_cast<int64_t>(b) * strideX;
+    const float* Yt = Ytb + static_cast<int64_t>(b) * strideX;
     float* Ur = Urb + static_cast<int64_t>(b) * strideUr;
     const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
     for (int c = tid; c < k; c += blockDim.x) {
         double s = 0.0;
-        const float* x = Xt + static_cast<int64_t>(c) * k;
-        for (int i = 0; i < k; ++i) s += static_cast<double>(x[i]) * static_cast<double>(x[i]);
+        const float* y = Yt + static_cast<int64_t>(c) * k;
+        for (int i = 0; i < k; ++i) s += static_cast<double>(y[i]) * static_cast<double>(y[i]);
         sig[c] = sqrt(s);
     }
     __syncthreads();
-    // descending by value, ties by index; NaN sorts last
     for (int c = tid; c < k; c += blockDim.x) {
         const double vc = (sig[c] == sig[c]) ? sig[c] : -1.0;
         int rank = 0;
@@ -328,15 +390,25 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Xtb, 
         perm[rank] = c;
     }
     __syncthreads();
-    if (sigma != nullptr) {
-        for (int j = tid; j < r; j += blockDim.x)
-            sigma[static_cast<int64_t>(b) * stride_sigma + j] = static_cast<float>(sig[perm[j]]);
+    if (tid == 0) {
+        int nk = 0;
+        while (nk < r && sig[perm[nk]] > 0.0) ++nk;      // NaN and zero columns end the run
+        nkeep_s = nk;
     }
-    const int64_t total = static_cast<int64_t>(k) * r;
+    if (sigma != nullptr) {
+        for (int j = tid; j < r; j += blockDim.x) {
+            const double v = sig[perm[j]];
+            sigma[static_cast<int64_t>(b) * stride_sigma + j] = (v > 0.0 || v != v) ? static_cast<float>(v) : 0.0f;
+        }
+    }
+    __syncthreads();
+    const int nkeep = nkeep_s;
+    const int64_t total = static_cast<int64_t>(k) * nkeep;
     for (int64_t pos = tid; pos < total; pos += blockDim.x) {
-        const int i = static_cast<int>(pos / r);
-        const int j = static_cast<int>(pos - static_cast<int64_t>(i) * r);
-        Ur[pos] = Vt[static_cast<int64_t>(perm[j]) * k + i];
+        const int i = static_cast<int>(pos / nkeep);
+        const int j = static_cast<int>(pos - static_cast<int64_t>(i) * nkeep);
+        const int c = perm[j];
+        Ur[static_cast<int64_t>(i) * r + j] = static_cast<float>(static_cast<double>(Yt[static_cast<int64_t>(c) * k + i]) / sig[c]);
     }
     if (tid == 0 && info != nullptr) {
         const int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
@@ -346,35 +418,105 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Xtb, 
         }
         info[b] = result;
     }
+    if (nkeep >= r) return;
+    // ---- orthonormal completion of columns nkeep .. r-1 (rank-deficient B) ----
+    // Each new column starts from the unit vector e_i least covered by the
+    // columns kept so far (smallest squared row norm rn2[i], so its residual
+    // 1 - rn2[i] is the largest, at least (k - j) / k), is orthogonalised twice
+    // against them (classical Gram-Schmidt) and normalised.
+    __syncthreads();
+    double* v = scratchb + static_cast<int64_t>(b) * strideScratch;   // k
+    double* dots = v + k;                                              // r
+    double* rn2 = dots + r;                                            // k
+    __shared__ double bestv[4];
+    __shared__ int besti[4];
+    for (int i = tid; i < k; i += blockDim.x) {
+        double a = 0.0;
+        for (int m = 0; m < nkeep; ++m) {
+            const double u = Ur[static_cast<int64_t>(i) * r + m];
+            a += u * u;
+        }
+        rn2[i] = a;
+    }
+    __syncthreads();
+    for (int j = nkeep; j < r; ++j) {
+        // argmin of rn2 (lowest index on ties)
+        double bv = 1e300;
+        int bi = k;
+        for (int i = tid; i < k; i += blockDim.x)
+            if (rn2[i] < bv) { bv = rn2[i]; bi = i; }
+        for (int o = 32; o > 0; o >>= 1) {
+            const double ov = __shfl_xor(bv, o);
+            const int oi = __shfl_xor(bi, o);
+            if (ov < bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+        }
+        if (lane == 0) { bestv[wave] = bv; besti[wave] = bi; }
+        __syncthreads();
+        int cand = besti[0];
+        double cv = bestv[0];
+        for (int w = 1; w < 4; ++w)
+            if (bestv[w] < cv || (bestv[w] == cv && besti[w] < cand)) { cv = bestv[w]; cand = besti[w]; }
+        for (int i = tid; i < k; i += blockDim.x) v[i] = (i == cand) ? 1.0 : 0.0;
+        __syncthreads();
+        for (int pass = 0; pass < 2; ++pass) {
+            for (int m = tid; m < j; m += blockDim.x) {
+                double d = 0.0;
+                for (int i = 0; i < k; ++i) d += static_cast<double>(Ur[static_cast<int64_t>(i) * r + m]) * v[i];
+                dots[m] = d;
+            }
+            __syncthreads();
+            for (int i = tid; i < k; i += blockDim.x) {
+                double x = v[i];
+                for (int m = 0; m < j; ++m) x -= dots[m] * static_cast<double>(Ur[static_cast<int64_t>(i) * r + m]);
+                v[i] = x;
+            }
+            __syncthreads();
+        }
+        double nn = 0.0;
+        for (int i = tid; i < k; i += blockDim.x) nn += v[i] * v[i];
+        for (int o = 32; o > 0; o >>= 1) nn += __shfl_xor(nn, o);
+        if (lane == 0) red[wave] = nn;
+        __syncthreads();
+        const double norm = sqrt(red[0] + red[1] + red[2] + red[3]);
+        const double inv = (norm > 0.0) ? 1.0 / norm : 0.0;
+        for (int i = tid; i < k; i += blockDim.x) {
+            const double u = v[i] * inv;
+            Ur[static_cast<int64_t>(i) * r + j] = static_cast<float>(u);
+            rn2[i] += u * u;
+        }
+        __syncthreads();
+    }
 }
 
 }  // namespace
 
-hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Xt, float* Vt,
-                                 int64_t strideX, int* rot, int max_sweeps, int batch,
-                                 hipStream_t stream) {
+hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Yt, int64_t strideX,
+                                 int* rot, int max_sweeps, int batch, hipStream_t stream) {
     int64_t blocks = (static_cast<int64_t>(k) * k + 255) / 256;
     if (blocks > 4096) blocks = 4096;
     hipLaunchKernelGGL(jacobi_prepare_kernel, dim3(static_cast<unsigned>(blocks), batch), dim3(256),
-                       0, stream, R, k, strideR, Xt, Vt, strideX, rot, max_sweeps);
+                       0, stream, R, k, strideR, Yt, strideX, rot, max_sweeps);
     return hipGetLastError();
 }
 
-hipError_t launch_jacobi_step(float* Xt, float* Vt, int k, int64_t strideX, int nblocks, int step,
-                              int sweep, int* rot, int max_sweeps, double tol, int batch,
+hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
+                              int max_sweeps, double tol, float* theta, int* flags, int batch,
                               hipStream_t stream) {
-    hipLaunchKernelGGL(jacobi_step_kernel, dim3(nblocks / 2, batch), dim3(JT), 0, stream, Xt, Vt, k,
-                       strideX, nblocks, step, sweep, rot, max_sweeps, tol);
+    const int npairs = nblocks / 2;
+    hipLaunchKernelGGL(jacobi_pair_kernel, dim3(npairs, batch), dim3(JT), 0, stream, Yt, k, strideX,
+                       nblocks, step, sweep, rot, max_sweeps, tol, theta, flags);
+    const int chunks = (k + AR - 1) / AR;
+    hipLaunchKernelGGL(jacobi_apply_kernel, dim3(npairs, chunks, batch), dim3(JT), 0, stream, Yt, k,
+                       strideX, nblocks, step, sweep, rot, max_sweeps, theta, flags);
     return hipGetLastError();
 }
 
-hipError_t launch_jacobi_finalize(const float* Xt, const float* Vt, int k, int64_t strideX, int r,
-                                  float* Ur, int64_t strideUr, float* sigma, int64_t stride_sigma,
-                                  const int* rot, int max_sweeps, int* info, int batch,
-                                  hipStream_t stream) {
+hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
+                                  float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
+                                  double* scratch, int64_t strideScratch, int batch, hipStream_t stream) {
     const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
-    hipLaunchKernelGGL(jacobi_finalize_kernel, dim3(batch), dim3(256), shmem, stream, Xt, Vt, k,
-                       strideX, r, Ur, strideUr, sigma, stride_sigma, rot, max_sweeps, info);
+    hipLaunchKernelGGL(jacobi_finalize_kernel, dim3(batch), dim3(256), shmem, stream, Yt, k, strideX, r, Ur,
+                       strideUr, sigma, stride_sigma, rot, max_sweeps, info, scratch, strideScratch);
     return hipGetLastError();
 }
 
