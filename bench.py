@@ -32,6 +32,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0         # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3    # MI355X dense fp32 matrix, TFLOP/s
+FP64_MFMA_PEAK_TFS = 78.6     # MI355X dense fp64 matrix, TFLOP/s
 ADAM_BYTES_PER_ELEM = 24      # read R, M, V; write M, V, N (fp32)
 
 
@@ -48,24 +49,27 @@ def parse():
     ap.add_argument("--q", type=int, default=2)
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the oracle on the host (0/1)")
-    ap.add_argument("--roofline-kernel", default="auto", choices=["auto", "adam", "project", "project_back"])
+    ap.add_argument("--roofline-kernel", default="auto",
+                    choices=["auto", "product_A", "product_At", "gram", "triangular", "projector", "project",
+                             "project_back", "adam"])
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="before the workload, copy a buffer of this many MiB device to device once (a "
+                         "plain copy of known size, to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-launch HBM bytes from rocprofv3 counters (optional)")
     return ap.parse_args()
 
 
 def cpu_baseline(args):
-    """The oracle timed on the host on a bounded sample of the workload: one
-    planted-spectrum matrix with every dimension of the unit halved
-    (m/2 x n/2, r/2, p/2, same q), which is 1/8 of the unit's flops in every
-    term of the path, run through subspace update, projection, Adam and the
-    weight update; the rate is scaled by that factor to updates/s of the unit."""
+    """The oracle timed on the host on a bounded sample of the workload: one of
+    its matrices (same shape, spectrum and storage, r, p, q), run through the
+    whole path: subspace update, projection, Adam step and weight update."""
     import numpy as np
 
     import galore_inputs as gi
     import oracle
 
-    m, n, r, p, q = args.m // 2, args.n // 2, args.r // 2, args.p // 2, args.q
+    m, n, r, p, q = args.m, args.n, args.r, args.p, args.q
     s = min(m, n)
     G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.7), 1e-4, seed=7000), args.dtype)
     W = gi.weights(m, n, seed=7001).astype(np.float64)
@@ -77,16 +81,13 @@ def cpu_baseline(args):
     _, _, N = oracle.adam(R, Mz, Mz, f32(0.9), f32(0.999), f32(1e-8), 1)
     oracle.project_back(P, N, W, f32(1e-3), f32(0.25))
     dt = time.perf_counter() - t0
-    scale = (args.m * args.n * (args.r + args.p)) / float(m * n * (r + p))
     return {
-        "value": 1.0 / (dt * scale),
+        "value": 1.0 / dt,
         "unit": "updates/s",
         "cores": oracle.num_threads(),
         "kind": "oracle",
-        "sample": "one %dx%d %s matrix, r=%d p=%d q=%d, full path (update, project, Adam, weight "
-                  "update) in %.1f s; every dimension of the %dx%d r=%d p=%d unit halved, so the "
-                  "rate is divided by the flop ratio %.2f" % (m, n, args.dtype, r, p, q, dt, args.m,
-                                                             args.n, args.r, args.p, scale),
+        "sample": "one %dx%d %s matrix of the workload, r=%d p=%d q=%d, whole path (update, projection, "
+                  "Adam step, weight update) once: %.1f s" % (m, n, args.dtype, r, p, q, dt),
     }
 
 
@@ -110,6 +111,14 @@ def main():
     s, l = min(m, n), max(m, n)
     k = min(r + p, s)
 
+    if args.copy_probe_mib > 0:
+        src = torch.ones((args.copy_probe_mib, 1 << 18), dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print("bench: copy probe of %d MiB done" % args.copy_probe_mib, file=sys.stderr, flush=True)
+        del src, dst
     print("bench: generating %d x %dx%d %s gradients" % (B, m, n, args.dtype), file=sys.stderr, flush=True)
     G = gi.torch_planted_group(m, n, B, gi.spectrum_power(s, 0.7), 1e-4, seed=5000, dtype=args.dtype)
     gen = torch.Generator(device=dev)
@@ -127,13 +136,19 @@ def main():
     ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B),), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    stages = ("rsvd", "project", "adam", "project_back")
+    outer = ("rsvd", "project", "adam", "project_back")
+    cap = 96   # stage instances recorded per subspace update
 
-    def step(t, ev=None):
+    def step(t, ev=None, sev=None):
         if ev is not None:
             ev[0].record(stream)
-        gl.galore_rsvd_update(G, r, p, q, gi.sketch_seed(t), 0, P=P, sigma=sigma, info=info, workspace=ws,
-                              stream=stream)
+        if sev is None:
+            gl.galore_rsvd_update(G, r, p, q, gi.sketch_seed(t), 0, P=P, sigma=sigma, info=info, workspace=ws,
+                                  stream=stream)
+            stages = None
+        else:
+            _, _, _, stages = gl.galore_rsvd_update_traced(G, r, p, q, gi.sketch_seed(t), sev, 0, P=P, sigma=sigma,
+                                                           info=info, workspace=ws, stream=stream)
         if ev is not None:
             ev[1].record(stream)
         gl.galore_project(P, G, R=R, stream=stream)
@@ -145,6 +160,7 @@ def main():
         gl.galore_project_back(P, N, W, 1e-3, 0.25, stream=stream)
         if ev is not None:
             ev[4].record(stream)
+        return stages
 
     for w in range(args.warmup):
         step(w)
@@ -153,50 +169,90 @@ def main():
     if int((info != 0).sum()) != 0:
         raise RuntimeError("small SVD did not converge for %d matrices" % int((info != 0).sum()))
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    events = [[mk() for _ in range(5)] for _ in range(args.steps)]
+    sevents = [[mk() for _ in range(2 * cap)] for _ in range(args.steps)]
+    for evs in sevents:
+        for e in evs:
+            e.record(stream)     # torch creates the HIP event on its first record
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    stage_lists = []
     for i in range(args.steps):
-        step(args.warmup + i, events[i])
+        stage_lists.append(step(args.warmup + i, events[i], sevents[i]))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_stage = {st: 0.0 for st in stages}
-    for ev in events:
-        for j, st in enumerate(stages):
-            per_stage[st] += ev[j].elapsed_time(ev[j + 1])
-    per_stage = {st: v / args.steps for st, v in per_stage.items()}    # ms per step
-    ms_per_step = wall * 1000.0 / args.steps
     bad = int((info != 0).sum())
     if bad:
         raise RuntimeError("small SVD did not converge for %d matrices" % bad)
 
-    # algorithmic work per launch of the single-kernel stages
-    adam_bytes = ADAM_BYTES_PER_ELEM * B * r * l
-    adam_gbs = adam_bytes / (per_stage["adam"] * 1e-3) / 1e9
-    proj_flops = 2.0 * r * s * l * B
-    proj_tfs = proj_flops / (per_stage["project"] * 1e-3) / 1e12
-    back_tfs = proj_flops / (per_stage["project_back"] * 1e-3) / 1e12
+    # ---- per-stage times (ms per step) and per-launch durations ---------------
+    per_stage = {st: 0.0 for st in outer}
+    sub = {}
+    launches = {}    # single-launch kernel class -> list of durations (ms)
+    for ev, sev, stl in zip(events, sevents, stage_lists):
+        for j, st in enumerate(outer):
+            d = ev[j].elapsed_time(ev[j + 1])
+            per_stage[st] += d
+            if st != "rsvd":
+                launches.setdefault(st, []).append(d)
+        for i, name in enumerate(stl):
+            d = sev[2 * i].elapsed_time(sev[2 * i + 1])
+            sub[name] = sub.get(name, 0.0) + d
+            launches.setdefault(name, []).append(d)
+    per_stage = {st: v / args.steps for st, v in per_stage.items()}
+    sub = {st: v / args.steps for st, v in sub.items()}
+    ms_per_step = wall * 1000.0 / args.steps
 
+    # algorithmic work of one launch of each single-launch kernel class
+    # (flops, except bytes for Adam), for the whole batch
+    n_gram_s = (2 if q == 0 else q + 2)          # Grams of s x k blocks per update
+    n_gram_l = q + 1                              # Grams of l x k blocks per update
+    work = {
+        "product_A": ("mfma", 2.0 * s * l * k * B),
+        "product_At": ("mfma", 2.0 * s * l * k * B),
+        "projector": ("mfma", 2.0 * s * k * r * B),
+        "project": ("mfma", 2.0 * r * s * l * B),
+        "project_back": ("mfma", 2.0 * r * s * l * B),
+        "adam": ("hbm", float(ADAM_BYTES_PER_ELEM * B * r * l)),
+        # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches
+        "gram": ("mfma64", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * B / (n_gram_s + n_gram_l)),
+        # Q = Y R^-1 with triangular R^-1: rows * k * (k + 1) flops, averaged
+        "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * B
+                                / max(1, n_gram_s + n_gram_l - 1))),
+    }
     kern = args.roofline_kernel
     if kern == "auto":
-        kern = max(("project", "adam", "project_back"), key=lambda st: per_stage[st])
+        cand = [c for c in work if c in launches]
+        kern = max(cand, key=lambda c: sum(launches[c]))
+    durs = launches[kern]
+    avg_ms = sum(durs) / len(durs)
+    bound, units = work[kern]
     traffic = None
     try:
         with open(args.traffic_json) as f:
             tj = json.load(f)
-        key = "%s:%dx%dx%d:r%d:%s" % (kern, B, m, n, r, args.dtype)
-        traffic = tj.get(key)
+        traffic = tj.get("%s:%dx%dx%d:r%d:p%d:%s" % (kern, B, m, n, r, p, args.dtype))
     except (OSError, ValueError):
         traffic = None
-    if kern == "adam":
-        roof = {"kernel": "lowrank_adam", "bound": "hbm", "achieved": round(adam_gbs, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(adam_gbs / HBM_PEAK_GBS, 4),
-                "traffic": traffic}
+    if bound == "hbm":
+        ach = units / (avg_ms * 1e-3) / 1e9
+        roof = {"kernel": kern, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
     else:
-        tf = proj_tfs if kern == "project" else back_tfs
-        roof = {"kernel": "gemm_f32 (%s)" % kern, "bound": "mfma", "achieved": round(tf, 2),
-                "peak": FP32_MFMA_PEAK_TFS, "unit": "TFLOP/s", "frac": round(tf / FP32_MFMA_PEAK_TFS, 4),
-                "traffic": traffic}
+        peak = FP32_MFMA_PEAK_TFS if bound == "mfma" else FP64_MFMA_PEAK_TFS
+        ach = units / (avg_ms * 1e-3) / 1e12
+        roof = {"kernel": kern, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": traffic}
+    roof["launches_timed"] = len(durs)
+    roof["avg_launch_ms"] = round(avg_ms, 3)
+    roof["work_per_launch"] = units
+    adam_gbs = work["adam"][1] / (per_stage["adam"] * 1e-3) / 1e9
+    rates = {}
+    for c, (bd, units_c) in work.items():
+        if c in launches:
+            a = sum(launches[c]) / len(launches[c])
+            rates[c] = round(units_c / (a * 1e-3) / (1e9 if bd == "hbm" else 1e12), 2)
 
     out = {
         "metric": "rSVD subspace updates/sec at 4096x11008 r=1024; low-rank Adam step HBM GB/s",
@@ -217,8 +273,8 @@ def main():
                    "batch": B, "m": m, "n": n, "r": r, "p": p, "q": q},
         "adam_hbm_gbs": round(adam_gbs, 1),
         "stage_ms": {st: round(v, 3) for st, v in per_stage.items()},
-        "project_tflops": round(proj_tfs, 2),
-        "project_back_tflops": round(back_tfs, 2),
+        "rsvd_stage_ms": {st: round(v, 3) for st, v in sorted(sub.items(), key=lambda x: -x[1])},
+        "kernel_rates": rates,
         "roofline": roof,
     }
     del G, W, R, M, V, N, ws

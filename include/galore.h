@@ -110,6 +110,41 @@ GALORE_API int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int
                        void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Stages of the subspace update reported by galore_rsvd_update_traced.
+ */
+typedef enum {
+    GALORE_STAGE_SKETCH = 0,      /* Omega from the counter-based generator (1 launch)         */
+    GALORE_STAGE_PRODUCT_A = 1,   /* Y = A X, fp32 matrix cores (1 launch)                      */
+    GALORE_STAGE_PRODUCT_AT = 2,  /* Z = A^T Q, fp32 matrix cores (1 launch)                    */
+    GALORE_STAGE_GRAM = 3,        /* fp64 Gram X^T X of a tall-skinny block (1 launch)          */
+    GALORE_STAGE_CHOLESKY = 4,    /* blocked Cholesky of the Gram (+ inverse of the factor)     */
+    GALORE_STAGE_TRIANGULAR = 5,  /* Q = Y R^-1, fp32 matrix cores (1 launch)                   */
+    GALORE_STAGE_JACOBI = 6,      /* small SVD: all Jacobi sweeps and the sort                  */
+    GALORE_STAGE_PROJECTOR = 7,   /* P = Q U_B[:, :r], fp32 matrix cores (1 launch)             */
+    GALORE_STAGE_OTHER = 8        /* small kernels: dependent-column fill, sign convention      */
+} galore_stage_t;
+
+/*
+ * galore_rsvd_update with stage timing: the same work on the same stream;
+ * in addition, for the i-th stage instance enqueued (i < capacity), events[2i]
+ * is recorded on `stream` just before it and events[2i+1] just after it, and
+ * stages[i] receives its galore_stage_t. *count receives the number of
+ * instances recorded (stages past `capacity` run untimed). `events` (2 *
+ * capacity handles created by the caller, e.g. with timing enabled) and
+ * `stages`/`count` are host arrays; read the events after the stream has
+ * reached them. For profiling callers: a run of the subspace update broken
+ * down by stage, and the per-launch duration of its single-launch stages.
+ * Errors: those of galore_rsvd_update; capacity < 0, count NULL, or
+ * capacity > 0 with NULL events/stages or a NULL handle -> INVALID_ARG.
+ */
+GALORE_API int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
+                              int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
+                              uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
+                              float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream,
+                              hipEvent_t* events, int32_t* stages, int32_t capacity, int32_t* count);
+
+/*
  * Projection R = P^T A (paper §3, R_t = P_t^T G_t; paper Alg. 1).
  * P: fp32 s x r (ld ldp); G: g_dtype m x n (ld ldg); R: fp32 r x l (ld ldr).
  * For m > n this is R = (G P)^T.

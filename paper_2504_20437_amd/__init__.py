@@ -21,8 +21,13 @@ GALORE_OK = 0
 
 EXPORTED = (
     "galore_status_string", "galore_version", "galore_sketch", "galore_rsvd_workspace_size",
-    "galore_rsvd_update", "galore_project", "galore_lowrank_adam_step", "galore_project_back",
+    "galore_rsvd_update", "galore_rsvd_update_traced", "galore_project", "galore_lowrank_adam_step",
+    "galore_project_back",
 )
+
+# galore_stage_t
+STAGES = ("sketch", "product_A", "product_At", "gram", "cholesky", "triangular", "jacobi", "projector",
+          "other")
 
 
 class GaloreError(RuntimeError):
@@ -45,6 +50,9 @@ def _declare(lib):
     lib.galore_rsvd_update.argtypes = [vp, i32, i64, i64, i64, i64, i32, i32, i32, u64, u64,
                                        vp, i64, i64, vp, i64, vp, i32, vp, sz, vp]
     lib.galore_rsvd_update.restype = ctypes.c_int
+    lib.galore_rsvd_update_traced.argtypes = lib.galore_rsvd_update.argtypes + [
+        ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_int32), i32, ctypes.POINTER(ctypes.c_int32)]
+    lib.galore_rsvd_update_traced.restype = ctypes.c_int
     lib.galore_project.argtypes = [vp, i64, i64, vp, i32, i64, i64, i64, i64, i32, vp, i64, i64,
                                    i32, vp]
     lib.galore_project.restype = ctypes.c_int
@@ -123,9 +131,7 @@ def galore_rsvd_workspace_size(m: int, n: int, r: int, p: int, batch: int = 1) -
     return int(lib.galore_rsvd_workspace_size(m, n, r, p, batch))
 
 
-def galore_rsvd_update(G: torch.Tensor, r: int, p: int, q: int, seed: int, sketch_index0: int = 0,
-                       P=None, sigma=None, info=None, workspace=None, stream=None):
-    """Subspace update of G ((m, n) or (batch, m, n)); returns (P, sigma, info)."""
+def _rsvd_args(G, r, p, q, seed, sketch_index0, P, sigma, info, workspace, stream):
     gp, m, n, ldg, sg, batch = _mat(G, "G")
     s = min(m, n)
     dev = G.device
@@ -139,12 +145,35 @@ def galore_rsvd_update(G: torch.Tensor, r: int, p: int, q: int, seed: int, sketc
     need = galore_rsvd_workspace_size(m, n, r, p, batch)
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
-    st = lib.galore_rsvd_update(gp, _dtype_code(G), m, n, ldg, sg, r, p, q, seed, sketch_index0,
-                                pp, ldp, sp, sigma.data_ptr(), sigma.stride(0) if sigma.dim() == 2 else r,
-                                info.data_ptr(), batch, workspace.data_ptr(), workspace.numel(),
-                                _stream(stream))
-    _check(st, "galore_rsvd_update")
+    args = (gp, _dtype_code(G), m, n, ldg, sg, r, p, q, seed, sketch_index0, pp, ldp, sp, sigma.data_ptr(),
+            sigma.stride(0) if sigma.dim() == 2 else r, info.data_ptr(), batch, workspace.data_ptr(),
+            workspace.numel(), _stream(stream))
+    return args, P, sigma, info
+
+
+def galore_rsvd_update(G: torch.Tensor, r: int, p: int, q: int, seed: int, sketch_index0: int = 0,
+                       P=None, sigma=None, info=None, workspace=None, stream=None):
+    """Subspace update of G ((m, n) or (batch, m, n)); returns (P, sigma, info)."""
+    args, P, sigma, info = _rsvd_args(G, r, p, q, seed, sketch_index0, P, sigma, info, workspace, stream)
+    _check(lib.galore_rsvd_update(*args), "galore_rsvd_update")
     return P, sigma, info
+
+
+def galore_rsvd_update_traced(G: torch.Tensor, r: int, p: int, q: int, seed: int, events, sketch_index0: int = 0,
+                              P=None, sigma=None, info=None, workspace=None, stream=None):
+    """galore_rsvd_update that also records ``events`` (an even-length list of
+    torch.cuda.Event with timing enabled) around its stages; returns
+    (P, sigma, info, stages) with stages[i] the stage name of the pair
+    (events[2 i], events[2 i + 1])."""
+    if len(events) % 2:
+        raise ValueError("events must come in (start, end) pairs")
+    cap = len(events) // 2
+    args, P, sigma, info = _rsvd_args(G, r, p, q, seed, sketch_index0, P, sigma, info, workspace, stream)
+    ev = (ctypes.c_void_p * max(1, 2 * cap))(*[e.cuda_event for e in events])
+    st = (ctypes.c_int32 * max(1, cap))()
+    cnt = ctypes.c_int32(0)
+    _check(lib.galore_rsvd_update_traced(*args, ev, st, cap, ctypes.byref(cnt)), "galore_rsvd_update_traced")
+    return P, sigma, info, [STAGES[st[i]] for i in range(cnt.value)]
 
 
 def galore_project(P: torch.Tensor, G: torch.Tensor, R=None, stream=None):

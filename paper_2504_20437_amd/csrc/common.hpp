@@ -34,6 +34,7 @@ struct GemmArgs {
     int64_t ldc, strideC;
     int M, N, K;
     float alpha, beta;   // C = alpha * op(A) op(B) + beta * C  (beta == 0: C not read)
+    int b_upper;         // op(B) upper triangular: column tile j0 only needs k < j0 + tile width
 };
 
 struct Gram64Args {

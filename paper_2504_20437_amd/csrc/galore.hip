@@ -163,6 +163,7 @@ hipError_t gemm_right_tri(const float* In, float* Out, int64_t stride, int rows,
     a.K = k;
     a.alpha = 1.0f;
     a.beta = 0.0f;
+    a.b_upper = 1;
     return launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, st);
 }
 
@@ -174,10 +175,38 @@ struct Work {
     int* i(size_t off) const { return reinterpret_cast<int*>(base + off); }
 };
 
+// Optional stage tracing of the subspace update: events recorded on the
+// caller's stream around each stage instance (no-op when capacity is 0).
+struct Tracer {
+    hipEvent_t* events;
+    int32_t* stages;
+    int32_t capacity;
+    int32_t count;
+    hipStream_t stream;
+    hipError_t begin(int stage) {
+        if (count >= capacity) return hipSuccess;
+        stages[count] = stage;
+        return hipEventRecord(events[2 * count], stream);
+    }
+    hipError_t end() {
+        if (count >= capacity) return hipSuccess;
+        const hipError_t e = hipEventRecord(events[2 * count + 1], stream);
+        ++count;
+        return e;
+    }
+};
+
+#define GALORE_TRACED(tr, stage, expr)                        \
+    do {                                                      \
+        if ((tr).begin(stage) != hipSuccess) return GALORE_ERR_HIP; \
+        GALORE_TRY(expr);                                     \
+        if ((tr).end() != hipSuccess) return GALORE_ERR_HIP;  \
+    } while (0)
+
 // One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In (fp64 Gram and factor);
 // columns found dependent are replaced by generic unit vectors.
-hipError_t orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k,
-                     int batch, hipStream_t st) {
+int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
+              hipStream_t st, Tracer& tr) {
     const Layout& L = *w.L;
     Gram64Args gg{};
     gg.X = In;
@@ -187,14 +216,134 @@ hipError_t orth_pass(const Work& w, const float* In, float* Out, int64_t stride,
     gg.strideC = L.strideKK;
     gg.rows = rows;
     gg.cols = k;
-    hipError_t e = launch_gram64(gg, batch, st);
-    if (e != hipSuccess) return e;
-    e = launch_cholesky(w.d(L.offC), k, L.strideKK, w.f(L.offRinv), w.d(L.offXinv), L.strideKK,
-                        w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, st);
-    if (e != hipSuccess) return e;
-    e = gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st);
-    if (e != hipSuccess) return e;
-    return launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st);
+    GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram64(gg, batch, st));
+    GALORE_TRACED(tr, GALORE_STAGE_CHOLESKY,
+                  launch_cholesky(w.d(L.offC), k, L.strideKK, w.f(L.offRinv), w.d(L.offXinv), L.strideKK,
+                                  w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, st));
+    GALORE_TRACED(tr, GALORE_STAGE_TRIANGULAR,
+                  gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st));
+    GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st));
+    return GALORE_OK;
+}
+
+#define GALORE_CHECK(expr)               \
+    do {                                 \
+        const int st_ = (expr);          \
+        if (st_ != GALORE_OK) return st_; \
+    } while (0)
+
+int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r,
+              int32_t p, int32_t q, uint64_t seed, uint64_t sketch_index0, float* P, int64_t ldp,
+              int64_t stride_p, float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
+              void* workspace, size_t workspace_bytes, hipStream_t stream, Tracer& tr) {
+    if (G == nullptr || P == nullptr || workspace == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1) return GALORE_ERR_SHAPE;
+    if (m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, p);
+    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK) return GALORE_ERR_SHAPE;
+    if (ldg < n || ldp < r) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_g < m * ldg || stride_p < sh.s * ldp)) return GALORE_ERR_SHAPE;
+    if (sigma != nullptr && batch > 1 && stride_sigma < r) return GALORE_ERR_SHAPE;
+    const Layout L = make_layout(sh, r, batch);
+    if (workspace_bytes < L.total) return GALORE_ERR_WORKSPACE;
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return GALORE_ERR_WORKSPACE;
+
+    Work w{&L, static_cast<char*>(workspace)};
+    const GradOp gop{G, g_dtype == GALORE_BF16, ldg, stride_g};
+    const int k = sh.k;
+    const int s = static_cast<int>(sh.s);
+    const int l = static_cast<int>(sh.l);
+    float* L1 = w.f(L.offL1);
+    float* L2 = w.f(L.offL2);
+    float* Sa = w.f(L.offS1);
+    float* Sb = w.f(L.offS2);
+
+    // a1-a3: sketch, range sample, orthonormalise
+    GALORE_TRACED(tr, GALORE_STAGE_SKETCH, launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
+    GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A, gemm_A_times(sh, gop, L1, L.strideL, Sa, L.strideS, batch, stream));
+    float* Q = Sa;
+    float* Qtmp = Sb;
+    auto orth_s = [&](int passes) -> int {
+        for (int ps = 0; ps < passes; ++ps) {
+            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, tr);
+            if (e != GALORE_OK) return e;
+            float* t = Q;
+            Q = Qtmp;
+            Qtmp = t;
+        }
+        return GALORE_OK;
+    };
+    GALORE_CHECK(orth_s(q == 0 ? 2 : 1));
+    // a4: power iterations with re-orthonormalisation after every product
+    for (int it = 0; it < q; ++it) {
+        GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT, gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
+        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, tr));
+        GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A, gemm_A_times(sh, gop, L2, L.strideL, Qtmp, L.strideS, batch, stream));
+        {
+            float* t = Q;
+            Q = Qtmp;
+            Qtmp = t;
+        }
+        GALORE_CHECK(orth_s(it == q - 1 ? 2 : 1));
+    }
+    // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
+    GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT, gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
+    {
+        Gram64Args gg{};
+        gg.X = L1;
+        gg.ldx = k;
+        gg.strideX = L.strideL;
+        gg.C = w.d(L.offC);
+        gg.strideC = L.strideKK;
+        gg.rows = l;
+        gg.cols = k;
+        GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram64(gg, batch, stream));
+        GALORE_TRACED(tr, GALORE_STAGE_CHOLESKY,
+                      launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, w.d(L.offXinv), L.strideKK,
+                                      w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, stream));
+    }
+    // a6: one-sided Jacobi on the columns of Y = R^T: Y W = U Sigma, U = left
+    // singular vectors of B
+    float* Yt = w.f(L.offYt);
+    int* rot = w.i(L.offRot);
+    float* Ur = w.f(L.offUr);
+    if (tr.begin(GALORE_STAGE_JACOBI) != hipSuccess) return GALORE_ERR_HIP;
+    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Yt, L.strideKK, rot, kMaxSweeps, batch,
+                                     stream));
+    const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
+    const int nb = nblk_real + (nblk_real & 1);
+    for (int sw = 0; sw < kMaxSweeps; ++sw)
+        for (int stp = 0; stp < nb - 1; ++stp)
+            GALORE_TRY(launch_jacobi_step(Yt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol,
+                                          w.f(L.offTheta), w.i(L.offFlag), batch, stream));
+    // the rotation buffers are free again: scratch of the orthonormal completion
+    GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
+                                      kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
+                                      L.strideTheta / 2, batch, stream));
+    if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
+    // a7: P = Q U_B[:, :r], canonical signs
+    {
+        GemmArgs a{};
+        a.A = Q;
+        a.lda = k;
+        a.strideA = L.strideS;
+        a.B = Ur;
+        a.ldb = r;
+        a.strideB = L.strideUr;
+        a.C = P;
+        a.ldc = ldp;
+        a.strideC = stride_p;
+        a.M = s;
+        a.N = r;
+        a.K = k;
+        a.alpha = 1.0f;
+        a.beta = 0.0f;
+        GALORE_TRACED(tr, GALORE_STAGE_PROJECTOR,
+                      launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, stream));
+    }
+    GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_sign_fix(P, s, r, ldp, stride_p, batch, stream));
+    return GALORE_OK;
 }
 
 }  // namespace
@@ -234,110 +383,26 @@ int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int
                        uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
                        float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    if (G == nullptr || P == nullptr || workspace == nullptr) return GALORE_ERR_INVALID_ARG;
-    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
-    if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1) return GALORE_ERR_SHAPE;
-    if (m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
-    const Shape sh = make_shape(m, n, r, p);
-    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK) return GALORE_ERR_SHAPE;
-    if (ldg < n || ldp < r) return GALORE_ERR_SHAPE;
-    if (batch > 1 && (stride_g < m * ldg || stride_p < sh.s * ldp)) return GALORE_ERR_SHAPE;
-    if (sigma != nullptr && batch > 1 && stride_sigma < r) return GALORE_ERR_SHAPE;
-    const Layout L = make_layout(sh, r, batch);
-    if (workspace_bytes < L.total) return GALORE_ERR_WORKSPACE;
-    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return GALORE_ERR_WORKSPACE;
+    Tracer tr{nullptr, nullptr, 0, 0, stream};
+    return rsvd_impl(G, g_dtype, m, n, ldg, stride_g, r, p, q, seed, sketch_index0, P, ldp, stride_p, sigma,
+                     stride_sigma, info, batch, workspace, workspace_bytes, stream, tr);
+}
 
-    Work w{&L, static_cast<char*>(workspace)};
-    const GradOp gop{G, g_dtype == GALORE_BF16, ldg, stride_g};
-    const int k = sh.k;
-    const int s = static_cast<int>(sh.s);
-    const int l = static_cast<int>(sh.l);
-    float* L1 = w.f(L.offL1);
-    float* L2 = w.f(L.offL2);
-    float* Sa = w.f(L.offS1);
-    float* Sb = w.f(L.offS2);
-
-    // a1-a3: sketch, range sample, orthonormalise
-    GALORE_TRY(launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
-    GALORE_TRY(gemm_A_times(sh, gop, L1, L.strideL, Sa, L.strideS, batch, stream));
-    float* Q = Sa;
-    float* Qtmp = Sb;
-    auto orth_s = [&](int passes) -> hipError_t {
-        for (int ps = 0; ps < passes; ++ps) {
-            hipError_t e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream);
-            if (e != hipSuccess) return e;
-            float* t = Q;
-            Q = Qtmp;
-            Qtmp = t;
-        }
-        return hipSuccess;
-    };
-    GALORE_TRY(orth_s(q == 0 ? 2 : 1));
-    // a4: power iterations with re-orthonormalisation after every product
-    for (int it = 0; it < q; ++it) {
-        GALORE_TRY(gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
-        GALORE_TRY(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream));
-        GALORE_TRY(gemm_A_times(sh, gop, L2, L.strideL, Qtmp, L.strideS, batch, stream));
-        {
-            float* t = Q;
-            Q = Qtmp;
-            Qtmp = t;
-        }
-        GALORE_TRY(orth_s(it == q - 1 ? 2 : 1));
-    }
-    // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
-    GALORE_TRY(gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
-    {
-        Gram64Args gg{};
-        gg.X = L1;
-        gg.ldx = k;
-        gg.strideX = L.strideL;
-        gg.C = w.d(L.offC);
-        gg.strideC = L.strideKK;
-        gg.rows = l;
-        gg.cols = k;
-        GALORE_TRY(launch_gram64(gg, batch, stream));
-        GALORE_TRY(launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, w.d(L.offXinv), L.strideKK,
-                                   w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, stream));
-    }
-    // a6: one-sided Jacobi on the columns of Y = R^T: Y W = U Sigma, U = left
-    // singular vectors of B
-    float* Yt = w.f(L.offYt);
-    int* rot = w.i(L.offRot);
-    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Yt, L.strideKK, rot, kMaxSweeps, batch,
-                                     stream));
-    const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
-    const int nb = nblk_real + (nblk_real & 1);
-    for (int sw = 0; sw < kMaxSweeps; ++sw)
-        for (int stp = 0; stp < nb - 1; ++stp)
-            GALORE_TRY(launch_jacobi_step(Yt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol,
-                                          w.f(L.offTheta), w.i(L.offFlag), batch, stream));
-    float* Ur = w.f(L.offUr);
-    // the rotation buffers are free again: scratch of the orthonormal completion
-    GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
-                                      kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
-                                      L.strideTheta / 2, batch, stream));
-    // a7: P = Q U_B[:, :r], canonical signs
-    {
-        GemmArgs a{};
-        a.A = Q;
-        a.lda = k;
-        a.strideA = L.strideS;
-        a.B = Ur;
-        a.ldb = r;
-        a.strideB = L.strideUr;
-        a.C = P;
-        a.ldc = ldp;
-        a.strideC = stride_p;
-        a.M = s;
-        a.N = r;
-        a.K = k;
-        a.alpha = 1.0f;
-        a.beta = 0.0f;
-        GALORE_TRY(launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, stream));
-    }
-    GALORE_TRY(launch_sign_fix(P, s, r, ldp, stride_p, batch, stream));
-    return GALORE_OK;
+int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
+                              int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
+                              uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
+                              float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream,
+                              hipEvent_t* events, int32_t* stages, int32_t capacity, int32_t* count) {
+    if (capacity < 0 || (capacity > 0 && (events == nullptr || stages == nullptr)) || count == nullptr)
+        return GALORE_ERR_INVALID_ARG;
+    for (int32_t i = 0; i < 2 * capacity; ++i)
+        if (events[i] == nullptr) return GALORE_ERR_INVALID_ARG;
+    Tracer tr{events, stages, capacity, 0, stream};
+    const int st = rsvd_impl(G, g_dtype, m, n, ldg, stride_g, r, p, q, seed, sketch_index0, P, ldp, stride_p,
+                             sigma, stride_sigma, info, batch, workspace, workspace_bytes, stream, tr);
+    *count = tr.count;
+    return st;
 }
 
 int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,

@@ -146,7 +146,8 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
 
-    const int KT = (K + BK - 1) / BK;
+    const int Keff = g.b_upper ? min(K, col0 + BN) : K;   // rows of op(B) that can be nonzero
+    const int KT = (Keff + BK - 1) / BK;
     load_a(0);
     load_b(0);
     store_a(0);

@@ -128,3 +128,24 @@ def test_sketch_rejects():
     assert gl.lib.galore_sketch(NULL, 10, 4, 1, 0, None) == -1
     assert gl.lib.galore_sketch(FAKE, 0, 4, 1, 0, None) == -2
     assert gl.lib.galore_sketch(FAKE, 10, 0, 1, 0, None) == -2
+
+
+def test_rsvd_traced_rejects():
+    """The traced variant validates its own arguments first, then those of the
+    subspace update (capacity 0 records nothing)."""
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_rsvd_update_traced
+    base = [FAKE, 0, 64, 96, 96, 64 * 96, 8, 4, 1, 1, 0, FAKE, 8, 64 * 8, FAKE, 8, FAKE, 1,
+            FAKE - FAKE % 256 + 256, 1 << 40, None]
+    cnt = ctypes.c_int32(-1)
+    ev = (ctypes.c_void_p * 2)(FAKE, None)          # second handle missing
+    st = (ctypes.c_int32 * 1)()
+    assert f(*base, ev, st, 1, ctypes.byref(cnt)) == -1
+    assert f(*base, None, st, 1, ctypes.byref(cnt)) == -1
+    assert f(*base, ev, None, 1, ctypes.byref(cnt)) == -1
+    assert f(*base, ev, st, -1, ctypes.byref(cnt)) == -1
+    assert f(*base, ev, st, 0, None) == -1
+    bad = list(base)
+    bad[6] = 65                                      # r > s: rejected by the update itself
+    assert f(*bad, None, None, 0, ctypes.byref(cnt)) == -2
+    assert cnt.value == 0

@@ -285,3 +285,30 @@ def test_galore_step_end_to_end(gl, orc):
     _, _, Nr2 = orc.adam(Rr, np.zeros_like(Rr), np.zeros_like(Rr), f32(w.beta1), f32(w.beta2), f32(w.eps), 1)
     Wr2 = orc.project_back(Pr, Nr2, W0.astype(np.float64), f32(w.lr), f32(w.alpha))
     assert max_rel_violation(host(Wd), Wr2, 1e-5, 1e-6) <= 1.0
+
+
+def test_rsvd_traced_matches_untraced(gl):
+    """The traced subspace update does the same work (bitwise-equal P and
+    sigma) and reports its stages in launch order with non-negative times."""
+    import torch
+    w = gi.WORKLOADS["single-256x688"]
+    G = dev(gi.store(gi.planted_gradient(256, 688, w.spectrum(256), w.noise, seed=1000), "f32").data)
+    P1, s1, _ = gl.galore_rsvd_update(G, 32, 8, 2, 77)
+    events = [torch.cuda.Event(enable_timing=True) for _ in range(2 * 64)]
+    for e in events:
+        e.record()
+    P2, s2, info, stages = gl.galore_rsvd_update_traced(G, 32, 8, 2, 77, events)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(P1), host(P2)) and np.array_equal(host(s1), host(s2))
+    assert int(info.cpu()[0]) == 0
+    # q = 2: 3 products with A, 3 with A^T, 4 + 3 Grams, 7 Cholesky, 6 triangular products
+    assert stages[:2] == ["sketch", "product_A"]
+    assert stages.count("product_A") == 3 and stages.count("product_At") == 3
+    assert stages.count("gram") == 7 and stages.count("cholesky") == 7 and stages.count("triangular") == 6
+    assert stages.count("jacobi") == 1 and stages.count("projector") == 1
+    for i in range(len(stages)):
+        assert events[2 * i].elapsed_time(events[2 * i + 1]) >= 0.0
+    # capacity smaller than the number of stages: the rest runs untimed
+    P3, _, _, st3 = gl.galore_rsvd_update_traced(G, 32, 8, 2, 77, events[:6])
+    assert st3 == stages[:3]
+    assert np.array_equal(host(P1), host(P3))
