@@ -166,7 +166,7 @@ def main():
         step(w)
         torch.cuda.synchronize()
         print("bench: warmup %d done" % w, file=sys.stderr, flush=True)
-    if int((info != 0).sum()) != 0:
+    if args.warmup > 0 and int((info != 0).sum()) != 0:
         raise RuntimeError("small SVD did not converge for %d matrices" % int((info != 0).sum()))
 
     mk = lambda: torch.cuda.Event(enable_timing=True)

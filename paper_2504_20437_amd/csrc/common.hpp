@@ -19,6 +19,32 @@ __device__ __forceinline__ float to_f32(bf16_t x) {
     return __uint_as_float(static_cast<uint32_t>(x.bits) << 16);
 }
 
+// MI355X deals workgroups to its 8 XCDs round-robin by linear id (x fastest,
+// then y, then z) and every XCD has its own L2. xcd_logical_id remaps the
+// linear id so that XCD x receives the contiguous range [x * per, (x+1) * per)
+// of logical ids (per = total / 8; ids past the last multiple of 8 keep their
+// value): workgroups with neighbouring logical ids share an L2.
+__device__ __forceinline__ int xcd_logical_id(int lin, int total) {
+    constexpr int kXcd = 8;
+    const int main = total - total % kXcd;
+    if (lin >= main) return lin;
+    const int per = main / kXcd;
+    return (lin % kXcd) * per + lin / kXcd;
+}
+
+// Logical tile id -> (m, n) tile of one matrix, grouped by `group` tile rows:
+// consecutive ids walk the rows of a group first, so that the tiles in flight
+// on one XCD share both their A rows and their B columns.
+__device__ __forceinline__ void grouped_tile(int t, int num_m, int num_n, int group, int& m, int& n) {
+    const int per_group = group * num_n;
+    const int g = t / per_group;
+    const int first = g * group;
+    const int gsize = min(group, num_m - first);
+    const int r = t - g * per_group;
+    m = first + r % gsize;
+    n = r / gsize;
+}
+
 // Operand layouts of the GEMM kernels.
 //   A operand (M x K): kKContig -> A[i*lda + kk]   kMContig -> A[kk*lda + i]
 //   B operand (K x N): kNContig -> B[kk*ldb + j]   kKContigB -> B[j*ldb + kk]

@@ -73,6 +73,13 @@ struct ContigTile {
             }
         }
     }
+    // whole tile in range and 16-byte aligned rows: unconditional vector loads
+    __device__ static void load_fast(const T* base, int64_t ld, int k0, int c0, int t, float* r) {
+        const int cq = t % CQ, kr = t / CQ;
+        const T* src = base + static_cast<int64_t>(k0 + kr) * ld + c0 + V * cq;
+#pragma unroll
+        for (int e = 0; e < E; ++e) load_vec16(src + static_cast<int64_t>(KR * e) * ld, r + V * e);
+    }
     __device__ static void store(float (*S)[128], int t, const float* r) {
         const int cq = t % CQ, kr = t / CQ;
 #pragma unroll
@@ -101,6 +108,11 @@ struct KContigTile {
             for (int e = 0; e < 16; ++e) r[e] = (c < C && gk + e < K) ? to_f32(src[e]) : 0.0f;
         }
     }
+    __device__ static void load_fast(const T* base, int64_t ld, int k0, int c0, int t, float* r) {
+        const T* src = base + static_cast<int64_t>(c0 + (t >> 1)) * ld + k0 + (t & 1) * 16;
+#pragma unroll
+        for (int q = 0; q < 16 / V; ++q) load_vec16(src + V * q, r + V * q);
+    }
     __device__ static void store(float (*S)[128], int t, const float* r) {
         const int c = t >> 1;
         const int kk0 = (t & 1) * 16;
@@ -114,13 +126,20 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
     __shared__ float As[2][BK][BM];
     __shared__ float Bs[2][BK][BN];
 
-    const int bz = blockIdx.z;
+    // XCD-aware, row-grouped tile order (grid = n tiles x m tiles x batch)
+    const int num_n = gridDim.x, num_m = gridDim.y;
+    const int tiles = num_n * num_m;
+    const int lin = blockIdx.x + num_n * (blockIdx.y + num_m * blockIdx.z);
+    const int logical = xcd_logical_id(lin, tiles * gridDim.z);
+    const int bz = logical / tiles;
+    int tm, tn;
+    grouped_tile(logical - bz * tiles, num_m, num_n, 8, tm, tn);
     const TA* A = static_cast<const TA*>(g.A) + static_cast<int64_t>(bz) * g.strideA;
     const TB* B = static_cast<const TB*>(g.B) + static_cast<int64_t>(bz) * g.strideB;
     float* C = g.C + static_cast<int64_t>(bz) * g.strideC;
     const int M = g.M, N = g.N, K = g.K;
-    const int row0 = blockIdx.y * BM;
-    const int col0 = blockIdx.x * BN;
+    const int row0 = tm * BM;
+    const int col0 = tn * BN;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = t >> 6;
@@ -133,8 +152,17 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
 
     float ra[16];
     float rb[16];
-    auto load_a = [&](int k0) { TileA::load(A, g.lda, k0, K, row0, M, a_vec != 0, t, ra); };
-    auto load_b = [&](int k0) { TileB::load(B, g.ldb, k0, K, col0, N, b_vec != 0, t, rb); };
+    // interior tiles (uniform per workgroup) take the unconditional vector path
+    const bool a_full = a_vec && row0 + BM <= M;
+    const bool b_full = b_vec && col0 + BN <= N;
+    auto load_a = [&](int k0) {
+        if (a_full && k0 + BK <= K) TileA::load_fast(A, g.lda, k0, row0, t, ra);
+        else TileA::load(A, g.lda, k0, K, row0, M, a_vec != 0, t, ra);
+    };
+    auto load_b = [&](int k0) {
+        if (b_full && k0 + BK <= K) TileB::load_fast(B, g.ldb, k0, col0, t, rb);
+        else TileB::load(B, g.ldb, k0, K, col0, N, b_vec != 0, t, rb);
+    };
     auto store_a = [&](int buf) { TileA::store(As[buf], t, ra); };
     auto store_b = [&](int buf) { TileB::store(Bs[buf], t, rb); };
 
@@ -227,17 +255,33 @@ hipError_t dispatch_types(bool a_bf16, bool b_bf16, const GemmArgs& g, int batch
 
 // --------------------------------------------------------------------------
 // fp64 Gram C = X^T X (cols x cols), X rows x cols fp32.
+// 128 x 128 output tiles, upper triangle only (mirrored on store), enumerated
+// XCD-aware; 32-row chunks of the two column panels staged in LDS as fp32
+// (converted to fp64 when read) with the next chunk prefetched in registers;
+// four waves each own a 64 x 64 quadrant = 4 x 4 v_mfma_f64_16x16x4f64 tiles.
+// On diagonal tiles both operands are the same panel and are loaded once.
 // --------------------------------------------------------------------------
-constexpr int GB = 64;   // tile
-constexpr int GK = 16;   // k step
+constexpr int GB = 128;  // tile
+constexpr int GK = 32;   // rows per chunk
+constexpr int GP = GB + 16;   // padded LDS row (floats)
 
-__global__ __launch_bounds__(256) void gram64_kernel(Gram64Args g) {
-    const int tm = blockIdx.y * GB;
-    const int tn = blockIdx.x * GB;
-    if (tn < tm) return;                      // lower tiles come from the mirror
-    __shared__ double As[2][GK][GB];
-    __shared__ double Bs[2][GK][GB];
-    const int bz = blockIdx.z;
+__global__ __launch_bounds__(256, 2) void gram64_kernel(Gram64Args g) {
+    // grid = (upper tiles, batch); XCD-aware order, tile rows u-major
+    const int nt = (g.cols + GB - 1) / GB;
+    const int ntri = nt * (nt + 1) / 2;
+    const int logical = xcd_logical_id(blockIdx.x + ntri * blockIdx.y, ntri * gridDim.y);
+    const int bz = logical / ntri;
+    int idx = logical - bz * ntri, u = 0;
+    while (idx >= nt - u) {
+        idx -= nt - u;
+        ++u;
+    }
+    const int tm = u * GB;
+    const int tn = (u + idx) * GB;
+    const bool diag = (tm == tn);
+
+    __shared__ float As[2][GK][GP];
+    __shared__ float Bs[2][GK][GP];
     const float* X = g.X + static_cast<int64_t>(bz) * g.strideX;
     double* C = g.C + static_cast<int64_t>(bz) * g.strideC;
     const int rows = g.rows, cols = g.cols;
@@ -245,71 +289,86 @@ __global__ __launch_bounds__(256) void gram64_kernel(Gram64Args g) {
     const int lane = t & 63;
     const int wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int li = t & 63;
-    const int lkb = t >> 6;
+    // loader: 32 rows x 128 columns per panel = 4 float4 per thread
+    const int lc = (t & 31) * 4;
+    const int lr = t >> 5;                     // 0..7, rows lr + 8 e
+    const bool vec_ok = (g.ldx % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+    const bool a_cols_in = tm + GB <= cols;
+    const bool b_cols_in = tn + GB <= cols;
 
-    double ra[4], rb[4];
-    auto load = [&](int k0) {
+    f32x4 pa[4], pb[4];
+    auto fetch_panel = [&](int r0, int c0, bool cols_in, f32x4* out) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const int kk = k0 + lkb + 4 * e;
-            const bool kin = kk < rows;
-            const int64_t base = static_cast<int64_t>(kk) * g.ldx;
-            ra[e] = (kin && tm + li < cols) ? static_cast<double>(X[base + tm + li]) : 0.0;
-            rb[e] = (kin && tn + li < cols) ? static_cast<double>(X[base + tn + li]) : 0.0;
+            const int rr = r0 + lr + 8 * e;
+            const float* src = X + static_cast<int64_t>(rr) * g.ldx + c0 + lc;
+            if (rr < rows && cols_in && vec_ok) {
+                out[e] = *reinterpret_cast<const f32x4*>(src);
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) out[e][v] = (rr < rows && c0 + lc + v < cols) ? src[v] : 0.0f;
+            }
         }
     };
-    auto store = [&](int buf) {
+    auto fetch = [&](int r0) {
+        fetch_panel(r0, tm, a_cols_in, pa);
+        if (!diag) fetch_panel(r0, tn, b_cols_in, pb);
+    };
+    auto stash = [&](int buf) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            As[buf][lkb + 4 * e][li] = ra[e];
-            Bs[buf][lkb + 4 * e][li] = rb[e];
+            *reinterpret_cast<f32x4*>(&As[buf][lr + 8 * e][lc]) = pa[e];
+            if (!diag) *reinterpret_cast<f32x4*>(&Bs[buf][lr + 8 * e][lc]) = pb[e];
         }
     };
 
-    f64x4 acc[2][2];
+    f64x4 acc[4][4];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
+        for (int b = 0; b < 4; ++b) acc[a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
 
     const int KT = (rows + GK - 1) / GK;
-    load(0);
-    store(0);
+    fetch(0);
+    stash(0);
     __syncthreads();
     const int l16 = lane & 15;
     const int lk = lane >> 4;
     for (int kt = 0; kt < KT; ++kt) {
         const int cur = kt & 1;
         const bool more = kt + 1 < KT;
-        if (more) load((kt + 1) * GK);
+        if (more) fetch((kt + 1) * GK);
+        const float (*Ab)[GP] = As[cur];
+        const float (*Bb)[GP] = diag ? As[cur] : Bs[cur];
 #pragma unroll
         for (int kk = 0; kk < GK; kk += 4) {
-            const double a0 = As[cur][kk + lk][wm * 32 + l16];
-            const double a1 = As[cur][kk + lk][wm * 32 + 16 + l16];
-            const double b0 = Bs[cur][kk + lk][wn * 32 + l16];
-            const double b1 = Bs[cur][kk + lk][wn * 32 + 16 + l16];
-            acc[0][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f64_16x16x4f64(a1, b1, acc[1][1], 0, 0, 0);
+            double a[4], b[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = static_cast<double>(Ab[kk + lk][wm * 64 + 16 * i + l16]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) b[j] = static_cast<double>(Bb[kk + lk][wn * 64 + 16 * j + l16]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
         }
-        if (more) store(cur ^ 1);
+        if (more) stash(cur ^ 1);
         __syncthreads();
     }
     // fp64 16x16 block layout: lane holds column (lane & 15); accumulator
     // register v holds row 4 v + (lane >> 4).
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-            const int j = tn + wn * 32 + ni * 16 + l16;
+        for (int j = 0; j < 4; ++j) {
+            const int cj = tn + wn * 64 + 16 * j + l16;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int i = tm + wm * 32 + mi * 16 + 4 * v + lk;
-                if (i < cols && j < cols) {
-                    C[static_cast<int64_t>(i) * cols + j] = acc[mi][ni][v];
-                    if (tn != tm) C[static_cast<int64_t>(j) * cols + i] = acc[mi][ni][v];
+                const int ri = tm + wm * 64 + 16 * i + 4 * v + lk;
+                if (ri < cols && cj < cols) {
+                    C[static_cast<int64_t>(ri) * cols + cj] = acc[i][j][v];
+                    if (!diag) C[static_cast<int64_t>(cj) * cols + ri] = acc[i][j][v];
                 }
             }
         }
@@ -332,8 +391,8 @@ hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const G
 
 hipError_t launch_gram64(const Gram64Args& g, int batch, hipStream_t stream) {
     if (g.cols <= 0 || batch <= 0) return hipSuccess;
-    const int tiles = (g.cols + GB - 1) / GB;
-    dim3 grid(tiles, tiles, batch);
+    const int nt = (g.cols + GB - 1) / GB;
+    dim3 grid(nt * (nt + 1) / 2, batch);
     hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, stream, g);
     return hipGetLastError();
 }
