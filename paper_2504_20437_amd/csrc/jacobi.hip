@@ -76,6 +76,29 @@ __global__ __launch_bounds__(256) void jacobi_prepare_kernel(const double* Rb, i
     }
 }
 
+// Jacobi rotation (c, s) that zeroes the off-diagonal of [[a, g], [g, b]]
+// under column p' = c p - s q, q' = s p + c q: t = tan(theta) is the smaller
+// root of t^2 + 2 zeta t - 1 = 0, zeta = (b - a) / (2 g) (Rutishauser's
+// form). The angle only has to be close (a residual off-diagonal is removed
+// by later sweeps), so zeta and t use the hardware fp64 reciprocal and fp32
+// square root; the rotation itself must be orthogonal to fp64 rounding, so
+// c = 1 / sqrt(1 + t^2) is refined by two Newton steps from v_rsq_f64 and
+// s = c t, giving c^2 + s^2 = 1 to within a few ulp.
+__device__ __forceinline__ void rotation(double a, double b, double g, double& c, double& s) {
+    const double zeta = (b - a) * 0.5 * __builtin_amdgcn_rcp(g);
+    const float zf = static_cast<float>(zeta);
+    const float az = fabsf(zf);
+    float tf = __builtin_amdgcn_rcpf(az + __builtin_amdgcn_sqrtf(fmaf(az, az, 1.0f)));   // |zeta| huge: 0
+    tf = (zf >= 0.0f) ? tf : -tf;                                                         // sign(0) = +1
+    const double t = static_cast<double>(tf);
+    const double x = fma(t, t, 1.0);
+    double y = __builtin_amdgcn_rsq(x);
+    y = y * fma(-0.5 * x * y, y, 1.5);
+    y = y * fma(-0.5 * x * y, y, 1.5);
+    c = y;
+    s = y * t;
+}
+
 // Step of the block Jacobi, part 1 (one workgroup per pair and matrix):
 // Gram of the pair's 64 columns, convergence test, reduction of the small
 // Gram; writes Theta (fp32, 64 x 64) and whether the pair rotates.
@@ -236,12 +259,8 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(const float* Xtb, in
                 if (p > q) { const int tmp = p; p = q; q = tmp; }
                 const double a = G[p][p], bb = G[q][q], gm = G[p][q];
                 double c = 1.0, s = 0.0;
-                if (fabs(gm) > 1e-15 * sqrt(a * bb)) {
-                    const double zeta = (bb - a) / (2.0 * gm);
-                    const double sg = (zeta >= 0.0) ? 1.0 : -1.0;
-                    const double tt = sg / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-                    c = 1.0 / sqrt(1.0 + tt * tt);
-                    s = c * tt;
+                if (gm * gm > 1e-30 * (a * bb)) {
+                    rotation(a, bb, gm, c, s);
                     any_rot = 1;
                 }
                 cs[tid] = c;
