@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0         # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3    # MI355X dense fp32 matrix, TFLOP/s
 FP64_MFMA_PEAK_TFS = 78.6     # MI355X dense fp64 matrix, TFLOP/s
+BF16_MFMA_PEAK_TFS = 2500.0   # MI355X dense bf16 matrix, TFLOP/s
 ADAM_BYTES_PER_ELEM = 24      # read R, M, V; write M, V, N (fp32)
 
 
@@ -133,7 +134,7 @@ def main():
     M = torch.zeros_like(R)
     V = torch.zeros_like(R)
     N = torch.empty_like(R)
-    ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B),), dtype=torch.uint8, device=dev)
+    ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B, G.dtype),), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     outer = ("rsvd", "project", "adam", "project_back")
@@ -208,9 +209,13 @@ def main():
     # (flops, except bytes for Adam), for the whole batch
     n_gram_s = (2 if q == 0 else q + 2)          # Grams of s x k blocks per update
     n_gram_l = q + 1                              # Grams of l x k blocks per update
+    # products with a bf16-stored G run on the bf16 matrix cores as three exact
+    # bf16 products per fp32-accurate one (bf16x3.hip): bf16 peak, 3 MFMA flops
+    # per algorithmic flop
+    prod_bound = "mfma_bf16x3" if args.dtype == "bf16" else "mfma"
     work = {
-        "product_A": ("mfma", 2.0 * s * l * k * B),
-        "product_At": ("mfma", 2.0 * s * l * k * B),
+        "product_A": (prod_bound, 2.0 * s * l * k * B),
+        "product_At": (prod_bound, 2.0 * s * l * k * B),
         "projector": ("mfma", 2.0 * s * k * r * B),
         "project": ("mfma", 2.0 * r * s * l * B),
         "project_back": ("mfma", 2.0 * r * s * l * B),
@@ -240,10 +245,13 @@ def main():
         roof = {"kernel": kern, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
     else:
-        peak = FP32_MFMA_PEAK_TFS if bound == "mfma" else FP64_MFMA_PEAK_TFS
+        peak = {"mfma": FP32_MFMA_PEAK_TFS, "mfma64": FP64_MFMA_PEAK_TFS, "mfma_bf16x3": BF16_MFMA_PEAK_TFS}[bound]
         ach = units / (avg_ms * 1e-3) / 1e12
         roof = {"kernel": kern, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4), "traffic": traffic}
+        if bound == "mfma_bf16x3":
+            roof["mfma_dtype"] = "bf16 (3 exact bf16 products per fp32-accurate product)"
+            roof["frac_of_3x_ceiling"] = round(3.0 * ach / peak, 4)
     roof["launches_timed"] = len(durs)
     roof["avg_launch_ms"] = round(avg_ms, 3)
     roof["work_per_launch"] = units

@@ -75,9 +75,12 @@ GALORE_API int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, 
 
 /*
  * Bytes of workspace galore_rsvd_update needs for `batch` m x n matrices with
- * rank r and oversampling p. Returns 0 for invalid sizes.
+ * rank r, oversampling p and gradient storage g_dtype (a bf16 gradient also
+ * holds its transposed copy and the bf16 split of the fp32 sketch operands).
+ * Returns 0 for invalid sizes or dtype.
  */
-GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch);
+GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch,
+                                             int32_t g_dtype);
 
 /*
  * Subspace update (paper §3 and Alg. 1: P = top-r singular vectors of G on
@@ -121,7 +124,9 @@ typedef enum {
     GALORE_STAGE_TRIANGULAR = 5,  /* Q = Y R^-1, fp32 matrix cores (1 launch)                   */
     GALORE_STAGE_JACOBI = 6,      /* small SVD: all Jacobi sweeps and the sort                  */
     GALORE_STAGE_PROJECTOR = 7,   /* P = Q U_B[:, :r], fp32 matrix cores (1 launch)             */
-    GALORE_STAGE_OTHER = 8        /* small kernels: dependent-column fill, sign convention      */
+    GALORE_STAGE_OTHER = 8,       /* small kernels: dependent-column fill, sign convention      */
+    GALORE_STAGE_OPERAND = 9      /* bf16 G only: transposed copy of G, bf16 split of an fp32    */
+                                  /* operand (1 launch each)                                    */
 } galore_stage_t;
 
 /*

@@ -27,7 +27,7 @@ EXPORTED = (
 
 # galore_stage_t
 STAGES = ("sketch", "product_A", "product_At", "gram", "cholesky", "triangular", "jacobi", "projector",
-          "other")
+          "other", "operand")
 
 
 class GaloreError(RuntimeError):
@@ -45,7 +45,7 @@ def _declare(lib):
     lib.galore_version.restype = ctypes.c_int
     lib.galore_sketch.argtypes = [vp, i64, i64, u64, u64, vp]
     lib.galore_sketch.restype = ctypes.c_int
-    lib.galore_rsvd_workspace_size.argtypes = [i64, i64, i32, i32, i32]
+    lib.galore_rsvd_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32]
     lib.galore_rsvd_workspace_size.restype = sz
     lib.galore_rsvd_update.argtypes = [vp, i32, i64, i64, i64, i64, i32, i32, i32, u64, u64,
                                        vp, i64, i64, vp, i64, vp, i32, vp, sz, vp]
@@ -127,8 +127,9 @@ def galore_sketch(l: int, k: int, seed: int, sketch_index: int = 0, out=None, st
     return out
 
 
-def galore_rsvd_workspace_size(m: int, n: int, r: int, p: int, batch: int = 1) -> int:
-    return int(lib.galore_rsvd_workspace_size(m, n, r, p, batch))
+def galore_rsvd_workspace_size(m: int, n: int, r: int, p: int, batch: int = 1, dtype=torch.float32) -> int:
+    code = GALORE_BF16 if dtype in (torch.bfloat16, GALORE_BF16, "bf16") else GALORE_F32
+    return int(lib.galore_rsvd_workspace_size(m, n, r, p, batch, code))
 
 
 def _rsvd_args(G, r, p, q, seed, sketch_index0, P, sigma, info, workspace, stream):
@@ -142,7 +143,7 @@ def _rsvd_args(G, r, p, q, seed, sketch_index0, P, sigma, info, workspace, strea
         sigma = torch.empty((batch, r) if G.dim() == 3 else (r,), dtype=torch.float32, device=dev)
     if info is None:
         info = torch.empty((batch,), dtype=torch.int32, device=dev)
-    need = galore_rsvd_workspace_size(m, n, r, p, batch)
+    need = galore_rsvd_workspace_size(m, n, r, p, batch, G.dtype)
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
     args = (gp, _dtype_code(G), m, n, ldg, sg, r, p, q, seed, sketch_index0, pp, ldp, sp, sigma.data_ptr(),

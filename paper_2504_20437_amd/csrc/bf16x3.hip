@@ -1,0 +1,282 @@
+// Products with a bf16-stored gradient on the bf16 matrix cores, exact to
+// fp32 accumulation.
+//
+// When G is stored in bf16, every product A X (or A^T Q) of the subspace
+// update has one operand that is exactly bf16. The fp32 operand X is split
+// into three bf16 terms, X = X1 + X2 + X3 (X1 = bf16(X), X2 = bf16(X - X1),
+// X3 = bf16(X - X1 - X2): 3 x 8 significand bits cover the 24 of fp32), so
+//   A X = A X1 + A X2 + A X3
+// is three v_mfma_f32_32x32x16_bf16 products with exact bf16 x bf16 partial
+// products accumulated in fp32: the same arithmetic class as an fp32 GEMM, on
+// a unit with 16x the fp32 matrix rate.
+//
+// Operand layouts (both with the reduction index contiguous, so that a lane's
+// eight consecutive k values are one 16-byte LDS read):
+//   A: bf16, M x K rows (G itself, or its transposed copy made by
+//      transpose_bf16 for the products with A^T);
+//   B: three bf16 planes, each N x K rows (made by split3_transpose from the
+//      fp32 K x N operand).
+// C = alpha * A B + beta * C in fp32, M x N row-major.
+//
+// Tile 128 x 128 x 32, four wave64s each owning 64 x 64 (2 x 2 blocks of
+// 32 x 32), LDS rows padded to 40 bf16 (80 bytes: the 16 lanes of a 16-byte
+// read fall on distinct banks), next tile prefetched in registers, XCD-aware
+// row-grouped tile order.
+#include "common.hpp"
+
+namespace galore {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int XM = 128;
+constexpr int XN = 128;
+constexpr int XK = 32;
+constexpr int XKP = XK + 8;     // padded LDS row (bf16)
+constexpr int XT = 256;
+
+__device__ __forceinline__ uint16_t bf16_bits_rn(float x) {
+    // round to nearest even (inputs here are finite or propagate NaN)
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7f800000u) == 0x7f800000u) return static_cast<uint16_t>((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// --------------------------------------------------------------------------
+// dst (cols x rows, ld ldd) = src^T (src rows x cols, ld lds), bf16, 64 x 64 tiles
+// --------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* srcb, int64_t lds, int64_t strideS,
+                                                             uint16_t* dstb, int64_t ldd, int64_t strideD, int rows,
+                                                             int cols) {
+    __shared__ uint16_t tile[64][66];
+    const int b = blockIdx.z;
+    const uint16_t* src = srcb + static_cast<int64_t>(b) * strideS;
+    uint16_t* dst = dstb + static_cast<int64_t>(b) * strideD;
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int r = r0 + i, c = c0 + tx;
+        tile[i][tx] = (r < rows && c < cols) ? src[static_cast<int64_t>(r) * lds + c] : 0;
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int c = c0 + i, r = r0 + tx;
+        if (c < cols && r < rows) dst[static_cast<int64_t>(c) * ldd + r] = tile[tx][i];
+    }
+}
+
+// --------------------------------------------------------------------------
+// plane_p (cols x rows, ld ldp) = split_p(src)^T, src fp32 rows x cols (ld lds);
+// planes at planeStride elements from each other; rows..ldp-1 zero-filled
+// --------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void split3_transpose_kernel(const float* srcb, int64_t lds, int64_t strideS,
+                                                               uint16_t* planesb, int64_t ldp, int64_t planeStride,
+                                                               int64_t strideP, int rows, int cols, int rows_pad) {
+    __shared__ float tile[64][65];
+    const int b = blockIdx.z;
+    const float* src = srcb + static_cast<int64_t>(b) * strideS;
+    uint16_t* planes = planesb + static_cast<int64_t>(b) * strideP;
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int r = r0 + i, c = c0 + tx;
+        tile[i][tx] = (r < rows && c < cols) ? src[static_cast<int64_t>(r) * lds + c] : 0.0f;
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int c = c0 + i, r = r0 + tx;
+        if (c < cols && r < rows_pad) {
+            const float x = tile[tx][i];
+            const uint16_t h1 = bf16_bits_rn(x);
+            const float r1 = x - bf16_bits_to_f32(h1);
+            const uint16_t h2 = bf16_bits_rn(r1);
+            const float r2 = r1 - bf16_bits_to_f32(h2);
+            const uint16_t h3 = bf16_bits_rn(r2);
+            const int64_t o = static_cast<int64_t>(c) * ldp + r;
+            planes[o] = h1;
+            planes[o + planeStride] = h2;
+            planes[o + 2 * planeStride] = h3;
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// C (M x N) = alpha * A (M x K bf16 rows) * B^T (3 planes, N x K bf16 rows) + beta * C
+// --------------------------------------------------------------------------
+struct Bx3Args {
+    const uint16_t* A;
+    int64_t lda, strideA;
+    const uint16_t* B;          // plane 0; planes p at B + p * planeStride
+    int64_t ldb, planeStride, strideB;
+    float* C;
+    int64_t ldc, strideC;
+    int M, N, K;
+    float alpha, beta;
+};
+
+__global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) {
+    __shared__ __attribute__((aligned(16))) uint16_t As[XM][XKP];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[3][XN][XKP];
+
+    const int num_n = gridDim.x, num_m = gridDim.y;
+    const int tiles = num_n * num_m;
+    const int lin = blockIdx.x + num_n * (blockIdx.y + num_m * blockIdx.z);
+    const int logical = xcd_logical_id(lin, tiles * gridDim.z);
+    const int bz = logical / tiles;
+    int tm, tn;
+    grouped_tile(logical - bz * tiles, num_m, num_n, 8, tm, tn);
+    const uint16_t* A = g.A + static_cast<int64_t>(bz) * g.strideA;
+    const uint16_t* B = g.B + static_cast<int64_t>(bz) * g.strideB;
+    float* C = g.C + static_cast<int64_t>(bz) * g.strideC;
+    const int M = g.M, N = g.N, K = g.K;
+    const int row0 = tm * XM, col0 = tn * XN;
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // loader: a 128 x 32 bf16 tile is 512 segments of 8 (16 bytes); thread t
+    // moves segments t and t + 256 (row seg / 4, k offset 8 (seg % 4))
+    uint4 ra[2], rb[3][2];
+    const bool a_in = vec && row0 + XM <= M;
+    const bool b_in = vec && col0 + XN <= N;
+    auto load_rows = [&](const uint16_t* base, int64_t ld, int r0, int R, int k0, bool fast, uint4* out) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int seg = t + XT * e;
+            const int rr = r0 + (seg >> 2), kk = k0 + 8 * (seg & 3);
+            const uint16_t* src = base + static_cast<int64_t>(rr) * ld + kk;
+            if (fast && kk + 8 <= K) {
+                out[e] = *reinterpret_cast<const uint4*>(src);
+            } else {
+                uint16_t v[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v[q] = (rr < R && kk + q < K) ? src[q] : 0;
+                out[e] = make_uint4(v[0] | (uint32_t(v[1]) << 16), v[2] | (uint32_t(v[3]) << 16),
+                                    v[4] | (uint32_t(v[5]) << 16), v[6] | (uint32_t(v[7]) << 16));
+            }
+        }
+    };
+    auto fetch = [&](int k0) {
+        load_rows(A, g.lda, row0, M, k0, a_in, ra);
+#pragma unroll
+        for (int p = 0; p < 3; ++p) load_rows(B + p * g.planeStride, g.ldb, col0, N, k0, b_in, rb[p]);
+    };
+    auto stash = [&]() {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int seg = t + XT * e;
+            *reinterpret_cast<uint4*>(&As[seg >> 2][8 * (seg & 3)]) = ra[e];
+#pragma unroll
+            for (int p = 0; p < 3; ++p) *reinterpret_cast<uint4*>(&Bs[p][seg >> 2][8 * (seg & 3)]) = rb[p][e];
+        }
+    };
+
+    f32x16 acc[2][2];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+
+    const int KT = (K + XK - 1) / XK;
+    const int l32 = lane & 31, lk = lane >> 5;
+    fetch(0);
+    for (int kt = 0; kt < KT; ++kt) {
+        stash();
+        __syncthreads();
+        if (kt + 1 < KT) fetch((kt + 1) * XK);
+#pragma unroll
+        for (int ks = 0; ks < XK; ks += 16) {
+            bf16x8 a[2], bq[3][2];
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+                a[x] = *reinterpret_cast<const bf16x8*>(&As[wm * 64 + 32 * x + l32][ks + 8 * lk]);
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+                    bq[p][y] = *reinterpret_cast<const bf16x8*>(&Bs[p][wn * 64 + 32 * y + l32][ks + 8 * lk]);
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int y = 0; y < 2; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[x], bq[p][y], acc[x][y], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+
+    // 32x32 block layout: lane holds column (lane & 31) and rows
+    // (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
+    const float alpha = g.alpha, beta = g.beta;
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int c = col0 + wn * 64 + 32 * y + l32;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int r = row0 + wm * 64 + 32 * x + (v & 3) + 8 * (v >> 2) + 4 * lk;
+                if (r < M && c < N) {
+                    float* dst = C + static_cast<int64_t>(r) * g.ldc + c;
+                    float val = alpha * acc[x][y][v];
+                    if (beta != 0.0f) val += beta * (*dst);
+                    *dst = val;
+                }
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, void* dst, int64_t ldd,
+                                 int64_t strideD, int rows, int cols, int batch, hipStream_t stream) {
+    dim3 grid((cols + 63) / 64, (rows + 63) / 64, batch);
+    hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(src), lds,
+                       strideS, static_cast<uint16_t*>(dst), ldd, strideD, rows, cols);
+    return hipGetLastError();
+}
+
+hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
+                                   int64_t planeStride, int64_t strideP, int rows, int cols, int rows_pad,
+                                   int batch, hipStream_t stream) {
+    dim3 grid((cols + 63) / 64, (rows_pad + 63) / 64, batch);
+    hipLaunchKernelGGL(split3_transpose_kernel, grid, dim3(256), 0, stream, src, lds, strideS,
+                       static_cast<uint16_t*>(planes), ldp, planeStride, strideP, rows, cols, rows_pad);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
+                              int64_t planeStride, int64_t strideB, float* C, int64_t ldc, int64_t strideC, int M,
+                              int N, int K, float alpha, float beta, int batch, hipStream_t stream) {
+    if (M <= 0 || N <= 0 || batch <= 0) return hipSuccess;
+    Bx3Args g;
+    g.A = static_cast<const uint16_t*>(A);
+    g.lda = lda;
+    g.strideA = strideA;
+    g.B = static_cast<const uint16_t*>(Bplanes);
+    g.ldb = ldb;
+    g.planeStride = planeStride;
+    g.strideB = strideB;
+    g.C = C;
+    g.ldc = ldc;
+    g.strideC = strideC;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.alpha = alpha;
+    g.beta = beta;
+    // 16-byte loads need 16-byte aligned rows in A and in every plane
+    const int vec = (lda % 8 == 0) && (ldb % 8 == 0) && (planeStride % 8 == 0) &&
+                    (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
+                    (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
+    dim3 grid((N + XN - 1) / XN, (M + XM - 1) / XM, batch);
+    hipLaunchKernelGGL(gemm_bf16x3_kernel, grid, dim3(XT), 0, stream, g, vec);
+    return hipGetLastError();
+}
+
+}  // namespace galore

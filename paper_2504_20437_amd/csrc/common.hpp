@@ -109,6 +109,16 @@ hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t row
                        int64_t ld, int64_t stride, int batch, float beta1, float beta2, float eps,
                        float bc1, float bc2, hipStream_t stream);
 
+// bf16 matrix-core products with an exactly bf16 operand (bf16x3.hip)
+hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, void* dst, int64_t ldd,
+                                 int64_t strideD, int rows, int cols, int batch, hipStream_t stream);
+hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
+                                   int64_t planeStride, int64_t strideP, int rows, int cols, int rows_pad,
+                                   int batch, hipStream_t stream);
+hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
+                              int64_t planeStride, int64_t strideB, float* C, int64_t ldc, int64_t strideC, int M,
+                              int N, int K, float alpha, float beta, int batch, hipStream_t stream);
+
 constexpr int kJacobiBlock = 32;     // columns per Jacobi block (pairs of 64)
 
 }  // namespace galore

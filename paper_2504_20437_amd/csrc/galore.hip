@@ -51,10 +51,17 @@ struct Layout {
     size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
         offTheta, offFlag;
     int64_t strideTheta, strideFlag;
+    // bf16-stored gradients only: transposed copy of G (n x ldgt) and three
+    // bf16 planes of the split fp32 operand (k x ldpl each)
+    bool bf16;
+    int64_t ldgt, strideGt, ldpl, planeStride, stridePl;
+    size_t offGt, offPl;
     size_t total;
 };
 
-Layout make_layout(const Shape& sh, int r, int batch) {
+int64_t pad8(int64_t x) { return (x + 7) / 8 * 8; }
+
+Layout make_layout(const Shape& sh, int r, int batch, bool bf16) {
     Layout L;
     const int64_t k = sh.k;
     L.strideL = pad_elems(sh.l * k);
@@ -86,6 +93,14 @@ Layout make_layout(const Shape& sh, int r, int batch) {
     L.strideFlag = npairs;
     L.offTheta = take(B * L.strideTheta * sizeof(float));
     L.offFlag = take(B * L.strideFlag * sizeof(int));
+    L.bf16 = bf16;
+    L.ldgt = pad8(sh.m);
+    L.strideGt = pad_elems(sh.n * L.ldgt);
+    L.ldpl = pad8(sh.l);
+    L.planeStride = pad_elems(k * L.ldpl);
+    L.stridePl = 3 * L.planeStride;
+    L.offGt = bf16 ? take(B * L.strideGt * sizeof(uint16_t)) : 0;
+    L.offPl = bf16 ? take(B * L.stridePl * sizeof(uint16_t)) : 0;
     L.total = off;
     return L;
 }
@@ -145,6 +160,20 @@ hipError_t gemm_At_times(const Shape& sh, const GradOp& g, const float* Q, int64
                        false, a, batch, st);
 }
 
+// The products of the subspace update with the gradient. For fp32 G they run
+// on the fp32 matrix cores reading G in place; for bf16 G the fp32 operand is
+// split into three bf16 planes and the product runs on the bf16 matrix cores
+// (bf16x3.hip) with the rows of A (G or its transposed copy) K-contiguous.
+struct Products {
+    const Shape* sh;
+    const Layout* L;
+    GradOp g;
+    uint16_t* gt;       // transposed copy of G, n x ldgt (bf16 path)
+    uint16_t* planes;   // split planes (bf16 path)
+    int batch;
+    hipStream_t st;
+};
+
 // Out (rows x k) = In (rows x k) * Rinv (k x k)
 hipError_t gemm_right_tri(const float* In, float* Out, int64_t stride, int rows, int k,
                           const float* Rinv, int64_t strideKK, int batch, hipStream_t st) {
@@ -203,6 +232,48 @@ struct Tracer {
         if ((tr).end() != hipSuccess) return GALORE_ERR_HIP;  \
     } while (0)
 
+// Y (s x k) = A X, X (l x k)
+int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, float* Y, int64_t strideY) {
+    const Shape& sh = *P.sh;
+    const Layout& L = *P.L;
+    if (!L.bf16) {
+        GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A, gemm_A_times(sh, P.g, X, strideX, Y, strideY, P.batch, P.st));
+        return GALORE_OK;
+    }
+    const int k = sh.k, s = static_cast<int>(sh.s), l = static_cast<int>(sh.l);
+    GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
+                  launch_split3_transpose(X, k, strideX, P.planes, L.ldpl, L.planeStride, L.stridePl, l, k,
+                                          static_cast<int>(L.ldpl), P.batch, P.st));
+    const void* A = sh.left ? P.g.G : static_cast<const void*>(P.gt);
+    const int64_t lda = sh.left ? P.g.ldg : L.ldgt;
+    const int64_t strideA = sh.left ? P.g.stride : L.strideGt;
+    GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A,
+                  launch_gemm_bf16x3(A, lda, strideA, P.planes, L.ldpl, L.planeStride, L.stridePl, Y, k, strideY,
+                                     s, k, l, 1.0f, 0.0f, P.batch, P.st));
+    return GALORE_OK;
+}
+
+// Z (l x k) = A^T Q, Q (s x k)
+int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, float* Z, int64_t strideZ) {
+    const Shape& sh = *P.sh;
+    const Layout& L = *P.L;
+    if (!L.bf16) {
+        GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT, gemm_At_times(sh, P.g, Q, strideQ, Z, strideZ, P.batch, P.st));
+        return GALORE_OK;
+    }
+    const int k = sh.k, s = static_cast<int>(sh.s), l = static_cast<int>(sh.l);
+    GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
+                  launch_split3_transpose(Q, k, strideQ, P.planes, L.ldpl, L.planeStride, L.stridePl, s, k,
+                                          static_cast<int>(pad8(s)), P.batch, P.st));
+    const void* At = sh.left ? static_cast<const void*>(P.gt) : P.g.G;
+    const int64_t ldat = sh.left ? L.ldgt : P.g.ldg;
+    const int64_t strideAt = sh.left ? L.strideGt : P.g.stride;
+    GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT,
+                  launch_gemm_bf16x3(At, ldat, strideAt, P.planes, L.ldpl, L.planeStride, L.stridePl, Z, k,
+                                     strideZ, l, k, s, 1.0f, 0.0f, P.batch, P.st));
+    return GALORE_OK;
+}
+
 // One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In (fp64 Gram and factor);
 // columns found dependent are replaced by generic unit vectors.
 int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
@@ -245,7 +316,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     if (ldg < n || ldp < r) return GALORE_ERR_SHAPE;
     if (batch > 1 && (stride_g < m * ldg || stride_p < sh.s * ldp)) return GALORE_ERR_SHAPE;
     if (sigma != nullptr && batch > 1 && stride_sigma < r) return GALORE_ERR_SHAPE;
-    const Layout L = make_layout(sh, r, batch);
+    const Layout L = make_layout(sh, r, batch, g_dtype == GALORE_BF16);
     if (workspace_bytes < L.total) return GALORE_ERR_WORKSPACE;
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return GALORE_ERR_WORKSPACE;
 
@@ -259,9 +330,16 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     float* Sa = w.f(L.offS1);
     float* Sb = w.f(L.offS2);
 
+    Products prod{&sh, &L, gop, L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offGt) : nullptr,
+                  L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offPl) : nullptr, batch, stream};
+    if (L.bf16)   // A^T (left) or A (right) as K-contiguous bf16 rows: G^T, n x m
+        GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
+                      launch_transpose_bf16(G, ldg, stride_g, prod.gt, L.ldgt, L.strideGt, static_cast<int>(m),
+                                            static_cast<int>(n), batch, stream));
+
     // a1-a3: sketch, range sample, orthonormalise
     GALORE_TRACED(tr, GALORE_STAGE_SKETCH, launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
-    GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A, gemm_A_times(sh, gop, L1, L.strideL, Sa, L.strideS, batch, stream));
+    GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Sa, L.strideS));
     float* Q = Sa;
     float* Qtmp = Sb;
     auto orth_s = [&](int passes) -> int {
@@ -277,9 +355,9 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(orth_s(q == 0 ? 2 : 1));
     // a4: power iterations with re-orthonormalisation after every product
     for (int it = 0; it < q; ++it) {
-        GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT, gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
+        GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL));
         GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, tr));
-        GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A, gemm_A_times(sh, gop, L2, L.strideL, Qtmp, L.strideS, batch, stream));
+        GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS));
         {
             float* t = Q;
             Q = Qtmp;
@@ -288,7 +366,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
         GALORE_CHECK(orth_s(it == q - 1 ? 2 : 1));
     }
     // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
-    GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT, gemm_At_times(sh, gop, Q, L.strideS, L1, L.strideL, batch, stream));
+    GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL));
     {
         Gram64Args gg{};
         gg.X = L1;
@@ -371,11 +449,13 @@ int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, uint64_t sk
     return GALORE_OK;
 }
 
-size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch) {
+size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch, int32_t g_dtype) {
     if (m < 1 || n < 1 || r < 1 || p < 0 || batch < 1) return 0;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return 0;
+    if (m > INT32_MAX || n > INT32_MAX) return 0;
     const Shape sh = make_shape(m, n, r, p);
-    if (r > sh.s || sh.k > kMaxK) return 0;
-    return make_layout(sh, r, batch).total;
+    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK) return 0;
+    return make_layout(sh, r, batch, g_dtype == GALORE_BF16).total;
 }
 
 int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,

@@ -48,6 +48,12 @@ def test_workspace_size():
     assert gl.galore_rsvd_workspace_size(10, 20, 11, 0, 1) == 0                  # r > s
     assert gl.galore_rsvd_workspace_size(0, 20, 1, 0, 1) == 0
     assert gl.galore_rsvd_workspace_size(5000, 9000, 4090, 10, 1) == 0           # sketch too wide
+    # a bf16 gradient also keeps its transposed copy and the split sketch operand
+    import torch
+    bf = gl.galore_rsvd_workspace_size(4096, 11008, 1024, 32, 1, torch.bfloat16)
+    assert bf >= one + 2 * 4096 * 11008 + 3 * 2 * 1056 * 11008
+    assert gl.galore_rsvd_workspace_size(11008, 4096, 1024, 32, 1, torch.bfloat16) == bf
+    assert gl.lib.galore_rsvd_workspace_size(64, 96, 8, 4, 1, 7) == 0            # bad dtype
 
 
 FAKE = 0x1000   # never dereferenced: every call below fails validation first

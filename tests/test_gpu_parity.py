@@ -178,6 +178,10 @@ def test_rsvd_single_256x688(gl, orc):
     (512, 512, 64, 8, 1, "f32"),        # square (left projector)
     (512, 1376, 128, 8, 2, "bf16"),     # bf16 storage
     (300, 517, 37, 11, 0, "f32"),       # ragged sizes, no power iteration
+    (1376, 512, 64, 8, 1, "bf16"),      # bf16 storage, right projector
+    (300, 700, 20, 4, 2, "bf16"),       # bf16, rows not 16-byte aligned (700 % 8 != 0)
+    (700, 300, 20, 4, 1, "bf16"),       # bf16, right projector, ragged
+    (520, 1100, 130, 7, 2, "bf16"),     # bf16, sketch width 137 (ragged against every tile)
 ])
 def test_rsvd_gapped_spectra(gl, orc, m, n, r, p, q, dtype):
     s = min(m, n)
@@ -312,3 +316,17 @@ def test_rsvd_traced_matches_untraced(gl):
     P3, _, _, st3 = gl.galore_rsvd_update_traced(G, 32, 8, 2, 77, events[:6])
     assert st3 == stages[:3]
     assert np.array_equal(host(P1), host(P3))
+
+
+def test_rsvd_bf16_exact_recovery(gl, orc):
+    """bf16 storage on the bf16 matrix-core path, rank(G) = 24 <= r (noiseless):
+    the planted values and subspace are recovered."""
+    m, n, r, p = 256, 688, 24, 8
+    s_pl = 4.0 * 0.8 ** np.arange(m)
+    G = gi.store(gi.planted_gradient(m, n, s_pl, 0.0, seed=14, rank=24), "bf16")
+    P, sig, info = gl.galore_rsvd_update(dev_stored(G), r, p, 2, 3)
+    P, sig = host(P), host(sig)
+    u, ss, _ = np.linalg.svd(G.exact)
+    assert max_rel_violation(sig, ss[:24], 1e-4, 1e-30) <= 1.0
+    assert proj_dist(P, u[:, :24]) <= 1e-3
+    assert orth_err(P) < 1e-4
