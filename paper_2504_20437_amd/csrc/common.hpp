@@ -95,10 +95,8 @@ hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, con
 // factor (the row-major upper triangle of R); clears the rotation counters.
 hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Yt, int64_t strideX,
                                  int* rot, int max_sweeps, int batch, hipStream_t stream);
-// theta: (nblocks / 2) x 64 x 64 fp32 per matrix; flags: nblocks / 2 ints per matrix
 hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
-                              int max_sweeps, double tol, float* theta, int* flags, int batch,
-                              hipStream_t stream);
+                              int max_sweeps, double tol, int batch, hipStream_t stream);
 // scratch: at least 2 k + r doubles per matrix at stride strideScratch (doubles)
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
                                   float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,

@@ -49,8 +49,8 @@ Shape make_shape(int64_t m, int64_t n, int r, int p) {
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
     size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
-        offTheta, offFlag;
-    int64_t strideTheta, strideFlag;
+        offTheta;
+    int64_t strideTheta;
     // bf16-stored gradients only: transposed copy of G (n x ldgt) and three
     // bf16 planes of the split fp32 operand (k x ldpl each)
     bool bf16;
@@ -87,12 +87,9 @@ Layout make_layout(const Shape& sh, int r, int batch, bool bf16) {
     L.offDef = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(int));
     L.offDiag0 = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(double));
     L.offRot = take(B * kMaxSweeps * sizeof(int));
-    const int64_t nblk = (k + kJacobiBlock - 1) / kJacobiBlock;
-    const int64_t npairs = (nblk + (nblk & 1)) / 2;
-    L.strideTheta = npairs * (2 * kJacobiBlock) * (2 * kJacobiBlock);
-    L.strideFlag = npairs;
+    // scratch of the orthonormal completion in the small-SVD finalize: 2k + r doubles
+    L.strideTheta = 2 * pad_elems(2 * k + r);
     L.offTheta = take(B * L.strideTheta * sizeof(float));
-    L.offFlag = take(B * L.strideFlag * sizeof(int));
     L.bf16 = bf16;
     L.ldgt = pad8(sh.m);
     L.strideGt = pad_elems(sh.n * L.ldgt);
@@ -393,9 +390,8 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     const int nb = nblk_real + (nblk_real & 1);
     for (int sw = 0; sw < kMaxSweeps; ++sw)
         for (int stp = 0; stp < nb - 1; ++stp)
-            GALORE_TRY(launch_jacobi_step(Yt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol,
-                                          w.f(L.offTheta), w.i(L.offFlag), batch, stream));
-    // the rotation buffers are free again: scratch of the orthonormal completion
+            GALORE_TRY(launch_jacobi_step(Yt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol, batch,
+                                          stream));
     GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
                                       kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
                                       L.strideTheta / 2, batch, stream));

@@ -12,8 +12,7 @@
 //
 // Blocked for the GPU: the k columns form blocks of 32; a round-robin
 // tournament pairs the blocks so that every step is a set of disjoint pairs.
-// A step is two launches over all pairs of all matrices of the batch:
-//   pair kernel (one workgroup per pair and matrix)
+// A step is one launch, one workgroup per pair and matrix, which
 //   1. forms the 64 x 64 fp64 Gram of its two blocks on the fp64 matrix cores
 //      (v_mfma_f64_16x16x4f64) from row chunks staged in LDS;
 //   2. skips the pair if every column pair is already orthogonal to the
@@ -21,10 +20,9 @@
 //   3. reduces the small Gram with cyclic two-sided Jacobi in LDS (fp64,
 //      parallel ordering: 63 rounds of 32 disjoint rotations per inner sweep,
 //      each round one read-modify-write of the Gram and of the accumulated
-//      rotation Theta) and writes Theta;
-//   apply kernel (one workgroup per pair, 64-row chunk and matrix)
-//   4. applies Theta to its rows of the pair's 64 columns of Y on the fp32
-//      matrix cores (v_mfma_f32_32x32x2f32).
+//      rotation Theta), and
+//   4. applies Theta to the pair's 64 columns of Y on the fp32 matrix cores
+//      (v_mfma_f32_32x32x2f32), 64-row chunks staged through LDS.
 // A sweep is nb - 1 steps; the matrix has converged when a whole sweep
 // rotates nothing (rotation counts per sweep live in device memory, so no
 // host synchronisation is needed).
@@ -99,14 +97,14 @@ __device__ __forceinline__ void rotation(double a, double b, double g, double& c
     s = y * t;
 }
 
-// Step of the block Jacobi, part 1 (one workgroup per pair and matrix):
-// Gram of the pair's 64 columns, convergence test, reduction of the small
-// Gram; writes Theta (fp32, 64 x 64) and whether the pair rotates.
-// LDS: region A holds the Gram (fp64, 64 x 65), region B first the two
-// fp64 staging buffers of the Gram's row chunks, then Theta (fp64).
-__global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(const float* Xtb, int k, int64_t strideX, int nb,
+// Step of the block Jacobi (one workgroup per pair and matrix): Gram of the
+// pair's 64 columns, convergence test, reduction of the small Gram, rotation
+// of the columns. LDS: region A holds the Gram (fp64, 64 x 65), then the fp32
+// Theta and row chunk of the rotation; region B first the two fp64 staging
+// buffers of the Gram's row chunks, then Theta (fp64).
+__global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
                                                             int step, int sweep, int* rotb, int max_sweeps,
-                                                            double tol, float* thetab, int* flagb) {
+                                                            double tol) {
     const int b = blockIdx.y;
     int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
     if (sweep > 0 && rot[sweep - 1] == 0) return;     // converged in an earlier sweep
@@ -114,11 +112,9 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(const float* Xtb, in
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int h = blockIdx.x;
-    const int npairs = nb / 2;
     const int bi = ring_slot(h, step, nb);
     const int bj = ring_slot(nb - 1 - h, step, nb);
     const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
-    int* flag = flagb + static_cast<int64_t>(b) * npairs + h;
 
     __shared__ double G[JW][PD];
     __shared__ double regB[JW][PD];
@@ -235,10 +231,7 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(const float* Xtb, in
         __syncthreads();
         const double off_all = red[0];
         const bool skip = !(off_all > tol) && off_all == off_all;   // already orthogonal
-        if (tid == 0) {
-            *flag = skip ? 0 : 1;
-            if (!skip) atomicAdd(&rot[sweep], 1);
-        }
+        if (tid == 0 && !skip) atomicAdd(&rot[sweep], 1);
         if (skip) return;
     }
 
@@ -303,74 +296,75 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(const float* Xtb, in
         __syncthreads();
         if (done) break;
     }
-    float* theta = thetab + (static_cast<int64_t>(b) * npairs + h) * (JW * JW);
-    for (int idx = tid; idx < JW * JW; idx += JT) theta[idx] = static_cast<float>(Th[idx / JW][idx % JW]);
-}
-
-// Step of the block Jacobi, part 2 (one workgroup per pair, 64-row chunk and
-// matrix): Y_P <- Y_P Theta on the fp32 matrix cores.
-__global__ __launch_bounds__(JT) void jacobi_apply_kernel(float* Xtb, int k, int64_t strideX,
-                                                          int nb, int step, int sweep, const int* rotb,
-                                                          int max_sweeps, const float* thetab,
-                                                          const int* flagb) {
-    const int b = blockIdx.z;
-    const int h = blockIdx.x;
-    const int npairs = nb / 2;
-    const int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
-    if (sweep > 0 && rot[sweep - 1] == 0) return;
-    if (flagb[static_cast<int64_t>(b) * npairs + h] == 0) return;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int bi = ring_slot(h, step, nb);
-    const int bj = ring_slot(nb - 1 - h, step, nb);
-    const int r0 = blockIdx.y * AR;
-    const int rc = min(AR, k - r0);
-
-    __shared__ float Tf[JW][PD];
-    __shared__ float Xc[JW][PD];
-    __shared__ int col[JW];
-    if (tid < JW) {
-        const int blk = (tid < JB) ? bi : bj;
-        const int c = blk * JB + (tid & (JB - 1));
-        col[tid] = (c < k) ? c : -1;
+    // ---- 4. Y_P <- Y_P Theta on the fp32 matrix cores: 64-row chunks through
+    //         LDS (the next chunk in flight in registers), results stored from
+    //         the accumulators (a lane writes four consecutive rows of a column)
+    float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);          // 64 x 65 fp32 (G is dead)
+    float (*Xc)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]) + JW;     // Xc[w][t]: column w, row t
+    for (int idx = tid; idx < JW * JW; idx += JT) {
+        const int i = idx / JW, j = idx % JW;
+        Tf[i][j] = static_cast<float>(Th[i][j]);
     }
-    const float* theta = thetab + (static_cast<int64_t>(b) * npairs + h) * (JW * JW);
-    for (int idx = tid; idx < JW * JW; idx += JT) Tf[idx / JW][idx % JW] = theta[idx];
-    __syncthreads();
+    float* Y = Xtb + static_cast<int64_t>(b) * strideX;
+    const bool vec4 = (k & 3) == 0;
+    // loader: thread t moves rows 4 (t % 16) .. +3 of columns t / 16 + 16 e, e < 4
+    const int aq = tid & 15, aw = tid >> 4;
+    f32x4 pre[4];
+    auto fetch = [&](int r0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int w = aw + 16 * e;
+            const int c = col[w];
+            const int rr = r0 + 4 * aq;
+            const int64_t base = static_cast<int64_t>(c) * k + rr;
+            if (c >= 0 && vec4 && rr + 4 <= k) {
+                pre[e] = *reinterpret_cast<const f32x4*>(Y + base);
+            } else {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) pre[e][v] = (c >= 0 && rr + v < k) ? Y[base + v] : 0.0f;
+            }
+        }
+    };
     const int tm = wave >> 1, tn = wave & 1;
     const int l32 = lane & 31, lk2 = lane >> 5;
-    {
-        float* M = Xtb + static_cast<int64_t>(b) * strideX;
-        for (int idx = tid; idx < JW * AR; idx += JT) {
-            const int w = idx / AR, t = idx % AR;
-            const int c = col[w];
-            Xc[w][t] = (c >= 0 && t < rc) ? M[static_cast<int64_t>(c) * k + r0 + t] : 0.0f;
-        }
+    const int nch = (k + AR - 1) / AR;
+    fetch(0);
+    for (int ch = 0; ch < nch; ++ch) {
+        const int r0 = ch * AR;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) Xc[aw + 16 * e][4 * aq + v] = pre[e][v];
         __syncthreads();
+        if (ch + 1 < nch) fetch(r0 + AR);
         f32x16 acc;
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
 #pragma unroll 8
         for (int kk = 0; kk < JW; kk += 2) {
-            const float a = Xc[kk + lk2][32 * tm + l32];   // A[t][w] = X[t][w]
+            const float a = Xc[kk + lk2][32 * tm + l32];   // A[t][w] = Y[t][w]
             const float bv = Tf[kk + lk2][32 * tn + l32];  // B[w][c] = Theta[w][c]
             acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
         }
-        __syncthreads();
         // 32x32 block layout: lane holds column (lane & 31) and rows
         // (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
+        const int c = col[32 * tn + l32];
+        if (c >= 0) {
+            float* dst = Y + static_cast<int64_t>(c) * k + r0;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int t = 32 * tm + (v & 3) + 8 * (v >> 2) + 4 * lk2;
-            Xc[32 * tn + l32][t] = acc[v];
+            for (int g4 = 0; g4 < 4; ++g4) {
+                const int t0 = 32 * tm + 8 * g4 + 4 * lk2;
+                if (vec4 && r0 + t0 + 4 <= k) {
+                    *reinterpret_cast<f32x4*>(dst + t0) =
+                        f32x4{acc[4 * g4 + 0], acc[4 * g4 + 1], acc[4 * g4 + 2], acc[4 * g4 + 3]};
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (r0 + t0 + v < k) dst[t0 + v] = acc[4 * g4 + v];
+                }
+            }
         }
         __syncthreads();
-        for (int idx = tid; idx < JW * AR; idx += JT) {
-            const int w = idx / AR, t = idx % AR;
-            const int c = col[w];
-            if (c >= 0 && t < rc) M[static_cast<int64_t>(c) * k + r0 + t] = Xc[w][t];
-        }
     }
 }
 
@@ -519,14 +513,9 @@ hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float*
 }
 
 hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
-                              int max_sweeps, double tol, float* theta, int* flags, int batch,
-                              hipStream_t stream) {
-    const int npairs = nblocks / 2;
-    hipLaunchKernelGGL(jacobi_pair_kernel, dim3(npairs, batch), dim3(JT), 0, stream, Yt, k, strideX,
-                       nblocks, step, sweep, rot, max_sweeps, tol, theta, flags);
-    const int chunks = (k + AR - 1) / AR;
-    hipLaunchKernelGGL(jacobi_apply_kernel, dim3(npairs, chunks, batch), dim3(JT), 0, stream, Yt, k,
-                       strideX, nblocks, step, sweep, rot, max_sweeps, theta, flags);
+                              int max_sweeps, double tol, int batch, hipStream_t stream) {
+    hipLaunchKernelGGL(jacobi_pair_kernel, dim3(nblocks / 2, batch), dim3(JT), 0, stream, Yt, k, strideX, nblocks,
+                       step, sweep, rot, max_sweeps, tol);
     return hipGetLastError();
 }
 
