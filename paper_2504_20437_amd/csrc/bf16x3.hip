@@ -18,8 +18,8 @@
 //      fp32 K x N operand).
 // C = alpha * A B + beta * C in fp32, M x N row-major.
 //
-// Tile 128 x 128 x 32, four wave64s each owning 64 x 64 (2 x 2 blocks of
-// 32 x 32), LDS rows padded to 40 bf16 (80 bytes: the 16 lanes of a 16-byte
+// Tile 128 x 128 x 64, four wave64s each owning 64 x 64 (2 x 2 blocks of
+// 32 x 32), LDS rows padded to 72 bf16 (144 bytes: the 16 lanes of a 16-byte
 // read fall on distinct banks), next tile prefetched in registers, XCD-aware
 // row-grouped tile order.
 #include "common.hpp"
@@ -31,8 +31,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int XM = 128;
 constexpr int XN = 128;
-constexpr int XK = 32;
-constexpr int XKP = XK + 8;     // padded LDS row (bf16)
+constexpr int XK = 64;
+constexpr int XKP = XK + 8;     // padded LDS row (bf16): 144 bytes, 16-byte lane reads conflict-free
 constexpr int XT = 256;
 
 __device__ __forceinline__ uint16_t bf16_bits_rn(float x) {
@@ -135,16 +135,18 @@ __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) 
     const int lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // loader: a 128 x 32 bf16 tile is 512 segments of 8 (16 bytes); thread t
-    // moves segments t and t + 256 (row seg / 4, k offset 8 (seg % 4))
-    uint4 ra[2], rb[3][2];
+    // loader: a 128 x 64 bf16 tile is 1024 segments of 8 (16 bytes); thread t
+    // moves segments t + 256 e, e < 4 (row seg / 8, k offset 8 (seg % 8))
+    constexpr int SEGS = XM * XK / 8 / XT;
+    constexpr int SPR = XK / 8;     // segments per row
+    uint4 ra[SEGS], rb[3][SEGS];
     const bool a_in = vec && row0 + XM <= M;
     const bool b_in = vec && col0 + XN <= N;
     auto load_rows = [&](const uint16_t* base, int64_t ld, int r0, int R, int k0, bool fast, uint4* out) {
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
+        for (int e = 0; e < SEGS; ++e) {
             const int seg = t + XT * e;
-            const int rr = r0 + (seg >> 2), kk = k0 + 8 * (seg & 3);
+            const int rr = r0 + seg / SPR, kk = k0 + 8 * (seg % SPR);
             const uint16_t* src = base + static_cast<int64_t>(rr) * ld + kk;
             if (fast && kk + 8 <= K) {
                 out[e] = *reinterpret_cast<const uint4*>(src);
@@ -164,11 +166,11 @@ __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) 
     };
     auto stash = [&]() {
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
+        for (int e = 0; e < SEGS; ++e) {
             const int seg = t + XT * e;
-            *reinterpret_cast<uint4*>(&As[seg >> 2][8 * (seg & 3)]) = ra[e];
+            *reinterpret_cast<uint4*>(&As[seg / SPR][8 * (seg % SPR)]) = ra[e];
 #pragma unroll
-            for (int p = 0; p < 3; ++p) *reinterpret_cast<uint4*>(&Bs[p][seg >> 2][8 * (seg & 3)]) = rb[p][e];
+            for (int p = 0; p < 3; ++p) *reinterpret_cast<uint4*>(&Bs[p][seg / SPR][8 * (seg % SPR)]) = rb[p][e];
         }
     };
 
