@@ -36,6 +36,83 @@ FP64_MFMA_PEAK_TFS = 78.6     # MI355X dense fp64 matrix, TFLOP/s
 BF16_MFMA_PEAK_TFS = 2500.0   # MI355X dense bf16 matrix, TFLOP/s
 ADAM_BYTES_PER_ELEM = 24      # read R, M, V; write M, V, N (fp32)
 
+# kernel classes of the roofline: launch classes (traced stages or outer calls)
+# that run one kernel each, the kernel's symbol and its source file (a stored
+# counter reading is used only while that source is unchanged)
+KERNEL_CLASSES = {
+    "products": (("product_A", "product_At"), "gemm_bf16x3_kernel", "bf16x3.hip"),
+    "gram": (("gram",), "gram64_kernel", "gemm.hip"),
+    "triangular": (("triangular",), None, "gemm.hip"),
+    "projector": (("projector",), None, "gemm.hip"),
+    "project": (("project",), None, "gemm.hip"),
+    "project_back": (("project_back",), None, "gemm.hip"),
+    "adam": (("adam",), "adam_flat_kernel", "elementwise.hip"),
+}
+CSRC = os.path.join(ROOT, "paper_2504_20437_amd", "csrc")
+
+
+def kernel_class(cls, dtype):
+    members, sym, src = KERNEL_CLASSES[cls]
+    if cls == "products" and dtype == "f32":      # fp32-stored G: the fp32 GEMM kernel
+        sym, src = None, "gemm.hip"
+    return members, sym, src
+
+
+def source_hash(fname):
+    import hashlib
+    h = hashlib.sha256()
+    for f in (fname, "common.hpp"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def workload_key(cls, args):
+    return "%s:%dx%dx%d:r%d:p%d:q%d:%s" % (cls, args.batch, args.m, args.n, args.r, args.p, args.q, args.dtype)
+
+
+def write_traffic(args):
+    """Per-launch HBM bytes of each kernel class from two rocprofv3 counter
+    runs. FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are scaled by what they
+    read for the plain device-to-device copy of --copy-probe-mib MiB that the
+    profiled run made first (a copy reads and writes exactly that many bytes)."""
+    import csv
+
+    def load(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not copies or args.copy_probe_mib <= 0:
+            raise SystemExit("%s: no copy-probe dispatch (run the profiled bench with --copy-probe-mib)" % path)
+        factor = args.copy_probe_mib * 1024.0 / max(copies)      # true KiB per counted KiB
+        return rows, factor
+
+    frows, ff = load(args.write_traffic[0], "FETCH_SIZE")
+    wrows, fw = load(args.write_traffic[1], "WRITE_SIZE")
+    try:
+        with open(args.traffic_json) as f:
+            out = json.load(f)
+    except (OSError, ValueError):
+        out = {}
+    for cls in KERNEL_CLASSES:
+        _, sym, src = kernel_class(cls, args.dtype)
+        if sym is None:
+            continue
+        fv = [float(r["Counter_Value"]) for r in frows if sym in r["Kernel_Name"]]
+        wv = [float(r["Counter_Value"]) for r in wrows if sym in r["Kernel_Name"]]
+        if not fv or not wv:
+            continue
+        fetch = sum(fv) / len(fv) * ff * 1024.0
+        write = sum(wv) / len(wv) * fw * 1024.0
+        out[workload_key(cls, args)] = {
+            "kernel": sym, "dispatches": len(fv), "fetch_bytes": round(fetch), "write_bytes": round(write),
+            "bytes_per_launch": round(fetch + write), "fetch_factor": round(ff, 4), "write_factor": round(fw, 4),
+            "source_sha256": source_hash(src), "command": args.command,
+        }
+    with open(args.traffic_json, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+        f.write("\n")
+    print(json.dumps({k: v["bytes_per_launch"] for k, v in out.items()}))
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -50,14 +127,18 @@ def parse():
     ap.add_argument("--q", type=int, default=2)
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the oracle on the host (0/1)")
-    ap.add_argument("--roofline-kernel", default="auto",
-                    choices=["auto", "product_A", "product_At", "gram", "triangular", "projector", "project",
-                             "project_back", "adam"])
+    ap.add_argument("--roofline-kernel", default="auto", choices=["auto"] + sorted(KERNEL_CLASSES))
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before the workload, copy a buffer of this many MiB device to device once (a "
                          "plain copy of known size, to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="per-launch HBM bytes from rocprofv3 counters (optional)")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no benchmark: read the counter_collection.csv of a rocprofv3 --pmc FETCH_SIZE run "
+                         "and of a --pmc WRITE_SIZE run of this script (same workload flags, with "
+                         "--copy-probe-mib), and record the per-launch HBM bytes of each kernel class in "
+                         "--traffic-json")
+    ap.add_argument("--command", default="", help="with --write-traffic: the profiling command, recorded")
     return ap.parse_args()
 
 
@@ -94,6 +175,9 @@ def cpu_baseline(args):
 
 def main():
     args = parse()
+    if args.write_traffic:
+        write_traffic(args)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the hot path is measured on one GPU's share "
               "(one process, no collectives); --gpus %d is not supported" % args.gpus, file=sys.stderr)
@@ -226,20 +310,32 @@ def main():
         "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * B
                                 / max(1, n_gram_s + n_gram_l - 1))),
     }
+    work["products"] = work["product_A"]          # both products run the same kernel on the same work
+    for cls, (members, _, _) in KERNEL_CLASSES.items():
+        durs_c = [d for mname in members for d in launches.get(mname, [])]
+        if durs_c:
+            launches.setdefault(cls, durs_c)
     kern = args.roofline_kernel
     if kern == "auto":
-        cand = [c for c in work if c in launches]
+        cand = [c for c in KERNEL_CLASSES if c in launches]
         kern = max(cand, key=lambda c: sum(launches[c]))
     durs = launches[kern]
     avg_ms = sum(durs) / len(durs)
     bound, units = work[kern]
     traffic = None
+    traffic_note = "no counter reading for this kernel and workload"
     try:
         with open(args.traffic_json) as f:
-            tj = json.load(f)
-        traffic = tj.get("%s:%dx%dx%d:r%d:p%d:%s" % (kern, B, m, n, r, p, args.dtype))
+            rec = json.load(f).get(workload_key(kern, args))
+        if rec is not None:
+            if rec.get("source_sha256") == source_hash(kernel_class(kern, args.dtype)[2]):
+                traffic = rec["bytes_per_launch"]
+                traffic_note = "rocprofv3 FETCH_SIZE x %.3g + WRITE_SIZE x %.3g per launch" % (
+                    rec["fetch_factor"], rec["write_factor"])
+            else:
+                traffic_note = "counter reading is of an earlier version of the kernel"
     except (OSError, ValueError):
-        traffic = None
+        pass
     if bound == "hbm":
         ach = units / (avg_ms * 1e-3) / 1e9
         roof = {"kernel": kern, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -252,6 +348,7 @@ def main():
         if bound == "mfma_bf16x3":
             roof["mfma_dtype"] = "bf16 (3 exact bf16 products per fp32-accurate product)"
             roof["frac_of_3x_ceiling"] = round(3.0 * ach / peak, 4)
+    roof["traffic_note"] = traffic_note
     roof["launches_timed"] = len(durs)
     roof["avg_launch_ms"] = round(avg_ms, 3)
     roof["work_per_launch"] = units
