@@ -43,7 +43,6 @@ constexpr int JT = 256;            // threads (4 waves)
 constexpr int GR = 32;             // rows per Gram chunk
 constexpr int AR = 64;             // rows per apply chunk
 constexpr int PD = JW + 1;         // padded LDS row
-constexpr int kInnerSweeps = 1;    // inner sweeps over the 64 x 64 Gram per step
 
 static_assert(JW == 64, "the pair kernels assume 64 columns per pair");
 
@@ -97,6 +96,24 @@ __device__ __forceinline__ void rotation(double a, double b, double g, double& c
     s = y * t;
 }
 
+// Cross-lane moves of an fp64 value within a wave (DPP, no LDS traffic).
+// dpp_swap_pairs: lane x receives lane x ^ 1. dpp_odd_partner: an odd lane x
+// receives lane x + 1, an even lane x - 1 (lanes 0 and 63 get their own value).
+__device__ __forceinline__ double dpp_swap_pairs(double v) {
+    const int lo = __double2loint(v), hi = __double2hiint(v);
+    const int l2 = __builtin_amdgcn_update_dpp(lo, lo, 0xB1, 0xf, 0xf, false);   // quad_perm [1,0,3,2]
+    const int h2 = __builtin_amdgcn_update_dpp(hi, hi, 0xB1, 0xf, 0xf, false);
+    return __hiloint2double(h2, l2);
+}
+__device__ __forceinline__ double dpp_odd_partner(double v, bool odd) {
+    const int lo = __double2loint(v), hi = __double2hiint(v);
+    const int ll = __builtin_amdgcn_update_dpp(lo, lo, 0x130, 0xf, 0xf, false);  // wave_shl:1 (from x + 1)
+    const int hl = __builtin_amdgcn_update_dpp(hi, hi, 0x130, 0xf, 0xf, false);
+    const int lr = __builtin_amdgcn_update_dpp(lo, lo, 0x138, 0xf, 0xf, false);  // wave_shr:1 (from x - 1)
+    const int hr = __builtin_amdgcn_update_dpp(hi, hi, 0x138, 0xf, 0xf, false);
+    return __hiloint2double(odd ? hl : hr, odd ? ll : lr);
+}
+
 // Step of the block Jacobi (one workgroup per pair and matrix): Gram of the
 // pair's 64 columns, convergence test, reduction of the small Gram, rotation
 // of the columns. LDS: region A holds the Gram (fp64, 64 x 65), then the fp32
@@ -119,10 +136,6 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, i
     __shared__ double G[JW][PD];
     __shared__ double regB[JW][PD];
     __shared__ int col[JW];
-    __shared__ double red[JT / 64];
-    __shared__ double cs[JW / 2], sn[JW / 2];
-    __shared__ int pp[JW / 2], qq[JW / 2];
-    __shared__ int any_rot;
 
     if (tid < JW) {
         const int blk = (tid < JB) ? bi : bj;
@@ -204,107 +217,186 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, i
         __syncthreads();
     }
 
-    // ---- 2. convergence test: largest relative off-diagonal ----------------
+    // ---- 2. convergence test: every column pair orthogonal to the tolerance?
+    //         |g_pq| <= tol sqrt(g_pp g_qq), compared squared; zero columns
+    //         never count, a NaN entry does (it must not pass as converged)
     {
-        double off = 0.0;
+        const double tol2 = tol * tol;
+        int need = 0;
         for (int idx = tid; idx < JW * JW; idx += JT) {
             const int p = idx / JW, q = idx % JW;
             if (q > p) {
                 const double dd = G[p][p] * G[q][q];
-                if (dd > 0.0) {
-                    const double rel = fabs(G[p][q]) / sqrt(dd);
-                    off = (rel > off || rel != rel) ? rel : off;
-                }
+                const double gpq = G[p][q];
+                if (dd > 0.0 && !(gpq * gpq <= tol2 * dd)) need = 1;
             }
         }
-        for (int o = 32; o > 0; o >>= 1) {
-            const double other = __shfl_xor(off, o);
-            off = (other > off || other != other) ? other : off;
-        }
-        if (lane == 0) red[wave] = off;
-        __syncthreads();
-        if (tid == 0) {
-            double m = red[0];
-            for (int w = 1; w < JT / 64; ++w) m = (red[w] > m || red[w] != red[w]) ? red[w] : m;
-            red[0] = m;
-        }
-        __syncthreads();
-        const double off_all = red[0];
-        const bool skip = !(off_all > tol) && off_all == off_all;   // already orthogonal
-        if (tid == 0 && !skip) atomicAdd(&rot[sweep], 1);
-        if (skip) return;
+        need = __syncthreads_or(need);
+        if (tid == 0 && need) atomicAdd(&rot[sweep], 1);
+        if (!need) return;
     }
 
-    // ---- 3. reduce the 64 x 64 Gram: cyclic two-sided Jacobi ---------------
-    double (*Th)[PD] = regB;
-    for (int idx = tid; idx < JW * JW; idx += JT) {
-        const int i = idx / JW, j = idx % JW;
-        Th[i][j] = (i == j) ? 1.0 : 0.0;
-    }
-    __syncthreads();
-    for (int isw = 0; isw < kInnerSweeps; ++isw) {
-        if (tid == 0) any_rot = 0;
-        __syncthreads();
-        for (int st = 0; st < JW - 1; ++st) {
-            if (tid < JW / 2) {
-                int p = ring_slot(tid, st, JW);
-                int q = ring_slot(JW - 1 - tid, st, JW);
-                if (p > q) { const int tmp = p; p = q; q = tmp; }
-                const double a = G[p][p], bb = G[q][q], gm = G[p][q];
-                double c = 1.0, s = 0.0;
-                if (gm * gm > 1e-30 * (a * bb)) {
-                    rotation(a, bb, gm, c, s);
-                    any_rot = 1;
-                }
-                cs[tid] = c;
-                sn[tid] = s;
-                pp[tid] = p;
-                qq[tid] = q;
+    // ---- 3. reduce the 64 x 64 Gram by one sweep of two-sided Jacobi, held
+    //         in registers: lane x holds row x, wave w the columns
+    //         16 w .. 16 w + 15 of it and of the accumulated rotation Theta.
+    //         Odd-even ordering: round t pairs the slots (p, p + 1) with
+    //         p = t mod 2, t mod 2 + 2, ...; every rotation also swaps its two
+    //         slots, so that after 64 rounds every pair of columns has met once
+    //         and the slot order is reversed. Row exchanges are lane shuffles,
+    //         column exchanges register moves; the columns at a wave's slab
+    //         edges come from its neighbours (halo copies) in odd rounds. The
+    //         pair's diagonal entries are carried along exactly (2 x 2 formulas),
+    //         its off-diagonal entry is read back from the holder each round.
+    {
+        double* Dv = &regB[0][0];                  // [2][64]: diagonal, ping-pong by round
+        double* CSw = Dv + 2 * JW;                 // [4 waves][64][2]: (c, s) by first slot, wave-private
+        double* Band = CSw + 4 * JW * 2;           // [2][4][16][16]: rows whose (x, x+1) entry a wave holds
+        double* Halo = Band + 2 * 4 * 16 * 16;     // [4 waves][4][64]: edge columns (G left/right, Theta left/right)
+        const int x = lane;
+        const int c0 = 16 * wave;
+        double gv[16], tv[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            gv[j] = G[x][c0 + j];
+            tv[j] = (x == c0 + j) ? 1.0 : 0.0;
+        }
+        if (wave == 0) Dv[x] = G[x][x];
+        // round 0 reads (x, x+1) for even x straight from G: stage it in Band[0]
+        {
+            const int jj = x + 1 - c0;
+            if (!(x & 1) && jj >= 0 && jj < 16) {
+                double* row = Band + ((0 * 4 + wave) * 16 + jj) * 16;
+                row[jj] = G[x][x + 1];
             }
-            __syncthreads();
-            // G <- J^T G J by 2 x 2 blocks (row pair ha, column pair hb);
-            // column p' = c p - s q, column q' = s p + c q
-            {
-                const int hb = tid & 31;
-                const int pb = pp[hb], qb2 = qq[hb];
-                const double cb = cs[hb], sb = sn[hb];
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const int ha = (tid >> 5) + 8 * m;
-                    const int pa = pp[ha], qa2 = qq[ha];
-                    const double ca = cs[ha], sa = sn[ha];
-                    const double g00 = G[pa][pb], g01 = G[pa][qb2], g10 = G[qa2][pb], g11 = G[qa2][qb2];
-                    const double r00 = ca * g00 - sa * g10, r01 = ca * g01 - sa * g11;
-                    const double r10 = sa * g00 + ca * g10, r11 = sa * g01 + ca * g11;
-                    G[pa][pb] = cb * r00 - sb * r01;
-                    G[pa][qb2] = sb * r00 + cb * r01;
-                    G[qa2][pb] = cb * r10 - sb * r11;
-                    G[qa2][qb2] = sb * r10 + cb * r11;
+        }
+        __syncthreads();
+        double hgL = 0.0, hgR = 0.0, htL = 0.0, htR = 0.0;
+        for (int t = 0; t < JW; ++t) {
+            const int par = t & 1;
+            const double* Dc = Dv + par * JW;
+            double* Dn = Dv + (par ^ 1) * JW;
+            const double* Bc = Band + par * (4 * 16 * 16);
+            double* Bn = Band + (par ^ 1) * (4 * 16 * 16);
+            if (par) {
+                // halo columns 16 w - 1 and 16 w + 16 as the neighbours left them
+                if (wave > 0) {
+                    hgL = Halo[((wave - 1) * 4 + 1) * JW + x];
+                    htL = Halo[((wave - 1) * 4 + 3) * JW + x];
                 }
-                // Theta <- Theta J: rows (tid >> 5) + 8 m of column pair hb
+                if (wave < 3) {
+                    hgR = Halo[((wave + 1) * 4 + 0) * JW + x];
+                    htR = Halo[((wave + 1) * 4 + 2) * JW + x];
+                }
+            }
+            // the pair of row x and its rotation (every lane computes its own)
+            const int p = par ? ((x & 1) ? x : x - 1) : (x & ~1);
+            const bool idle = par && (x == 0 || x == JW - 1);
+            double c = 0.0, sg = 1.0;          // idle rows stay as they are
+            if (!idle) {
+                const int q = p + 1;
+                const int wq = q >> 4, jq = q & 15;
+                const double a = Dc[p], b = Dc[q];
+                const double g = Bc[(wq * 16 + jq) * 16 + jq];
+                double cr = 1.0, sr = 0.0;
+                if (g * g > 1e-30 * (a * b)) rotation(a, b, g, cr, sr);
+                // rotated slot p' = c p - s q goes to slot q, q' = s p + c q to slot p
+                if (x == p) {
+                    if ((p >> 4) == wave) {
+                        const double cs2 = 2.0 * cr * sr * g;
+                        Dn[p] = sr * sr * a + cs2 + cr * cr * b;
+                        Dn[q] = cr * cr * a - cs2 + sr * sr * b;
+                    }
+                    CSw[(wave * JW + p) * 2 + 0] = cr;
+                    CSw[(wave * JW + p) * 2 + 1] = sr;
+                }
+                c = cr;
+                sg = (x == p) ? sr : -sr;
+            } else if ((x >> 4) == wave) {
+                Dn[x] = Dc[x];
+            }
+            // rows: new row p = s row_p + c row_q, new row q = c row_p - s row_q;
+            // the partner row is lane x ^ 1 (even rounds) or x -/+ 1 (odd rounds)
+            if (!par) {
 #pragma unroll
-                for (int m = 0; m < 8; ++m) {
-                    const int row = (tid >> 5) + 8 * m;
-                    const double tp = Th[row][pb], tq = Th[row][qb2];
-                    Th[row][pb] = cb * tp - sb * tq;
-                    Th[row][qb2] = sb * tp + cb * tq;
+                for (int j = 0; j < 16; ++j) gv[j] = sg * gv[j] + c * dpp_swap_pairs(gv[j]);
+            } else {
+                const bool odd = (x & 1) != 0;
+#pragma unroll
+                for (int j = 0; j < 16; ++j) gv[j] = sg * gv[j] + c * dpp_odd_partner(gv[j], odd);
+                hgL = sg * hgL + c * dpp_odd_partner(hgL, odd);
+                hgR = sg * hgR + c * dpp_odd_partner(hgR, odd);
+            }
+            // (c, s) of this wave's column pairs, published by their first rows
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const double* cw = CSw + wave * JW * 2;
+            // columns: new col p = s col_p + c col_q, new col q = c col_p - s col_q
+            if (!par) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const double cc = cw[(c0 + 2 * i) * 2 + 0], ss = cw[(c0 + 2 * i) * 2 + 1];
+                    const double g0 = gv[2 * i], g1 = gv[2 * i + 1];
+                    gv[2 * i] = ss * g0 + cc * g1;
+                    gv[2 * i + 1] = cc * g0 - ss * g1;
+                    const double t0 = tv[2 * i], t1 = tv[2 * i + 1];
+                    tv[2 * i] = ss * t0 + cc * t1;
+                    tv[2 * i + 1] = cc * t0 - ss * t1;
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 7; ++i) {
+                    const double cc = cw[(c0 + 2 * i + 1) * 2 + 0], ss = cw[(c0 + 2 * i + 1) * 2 + 1];
+                    const double g0 = gv[2 * i + 1], g1 = gv[2 * i + 2];
+                    gv[2 * i + 1] = ss * g0 + cc * g1;
+                    gv[2 * i + 2] = cc * g0 - ss * g1;
+                    const double t0 = tv[2 * i + 1], t1 = tv[2 * i + 2];
+                    tv[2 * i + 1] = ss * t0 + cc * t1;
+                    tv[2 * i + 2] = cc * t0 - ss * t1;
+                }
+                if (wave > 0) {      // pair (16 w - 1, 16 w): this wave keeps the second slot
+                    const double cc = cw[(c0 - 1) * 2 + 0], ss = cw[(c0 - 1) * 2 + 1];
+                    gv[0] = cc * hgL - ss * gv[0];
+                    tv[0] = cc * htL - ss * tv[0];
+                }
+                if (wave < 3) {      // pair (16 w + 15, 16 w + 16): this wave keeps the first slot
+                    const double cc = cw[(c0 + 15) * 2 + 0], ss = cw[(c0 + 15) * 2 + 1];
+                    gv[15] = ss * gv[15] + cc * hgR;
+                    tv[15] = ss * tv[15] + cc * htR;
+                }
+            }
+            // publish for the next round: the rows whose (x, x+1) entry lies in
+            // this wave's slab, and after an even round the slab's edge columns
+            {
+                const int jj = x + 1 - c0;
+                const int np = (par ^ 1) ? ((x & 1) ? x : -1) : ((x & 1) ? -1 : x);   // x first of a next pair?
+                if (np >= 0 && x + 1 < JW && jj >= 0 && jj < 16) {
+                    double* row = Bn + (wave * 16 + jj) * 16;
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) row[j] = gv[j];
+                }
+                if (!par) {
+                    Halo[(wave * 4 + 0) * JW + x] = gv[0];
+                    Halo[(wave * 4 + 1) * JW + x] = gv[15];
+                    Halo[(wave * 4 + 2) * JW + x] = tv[0];
+                    Halo[(wave * 4 + 3) * JW + x] = tv[15];
                 }
             }
             __syncthreads();
         }
-        const int done = (any_rot == 0);
+        // ---- Theta to LDS in fp32 for the matrix cores; the sweep reversed the
+        //      slot order, so output column j is slot 63 - j (a pair whose
+        //      rotations are all small keeps its columns in place)
+        float (*Tf0)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) Tf0[x][JW - 1 - (c0 + j)] = static_cast<float>(tv[j]);
         __syncthreads();
-        if (done) break;
     }
     // ---- 4. Y_P <- Y_P Theta on the fp32 matrix cores: 64-row chunks through
     //         LDS (the next chunk in flight in registers), results stored from
     //         the accumulators (a lane writes four consecutive rows of a column)
     float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);          // 64 x 65 fp32 (G is dead)
     float (*Xc)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]) + JW;     // Xc[w][t]: column w, row t
-    for (int idx = tid; idx < JW * JW; idx += JT) {
-        const int i = idx / JW, j = idx % JW;
-        Tf[i][j] = static_cast<float>(Th[i][j]);
-    }
     float* Y = Xtb + static_cast<int64_t>(b) * strideX;
     const bool vec4 = (k & 3) == 0;
     // loader: thread t moves rows 4 (t % 16) .. +3 of columns t / 16 + 16 e, e < 4
