@@ -11,16 +11,16 @@
 // triangle of R.
 //
 // Blocked for the GPU: the k columns form blocks of 32; a round-robin
-// tournament pairs the blocks so that every step is a set of disjoint pairs.
-// A step is one launch, one workgroup per pair and matrix, which
+// tournament pairs the blocks so that every step is a set of disjoint pairs
+// (with an odd number of blocks, the pair with the padding block is not
+// launched). A step is one launch, one workgroup per pair and matrix, which
 //   1. forms the 64 x 64 fp64 Gram of its two blocks on the fp64 matrix cores
 //      (v_mfma_f64_16x16x4f64) from row chunks staged in LDS;
 //   2. skips the pair if every column pair is already orthogonal to the
 //      tolerance (relative off-diagonal), otherwise
-//   3. reduces the small Gram with cyclic two-sided Jacobi in LDS (fp64,
-//      parallel ordering: 63 rounds of 32 disjoint rotations per inner sweep,
-//      each round one read-modify-write of the Gram and of the accumulated
-//      rotation Theta), and
+//   3. reduces the small Gram by one sweep of two-sided Jacobi held in
+//      registers (fp64; odd-even ordering, 64 rounds of up to 32 disjoint
+//      rotations, accumulating the rotation Theta), and
 //   4. applies Theta to the pair's 64 columns of Y on the fp32 matrix cores
 //      (v_mfma_f32_32x32x2f32), 64-row chunks staged through LDS.
 // A sweep is nb - 1 steps; the matrix has converged when a whole sweep
@@ -121,14 +121,22 @@ __device__ __forceinline__ double dpp_odd_partner(double v, bool odd) {
 // buffers of the Gram's row chunks, then Theta (fp64).
 __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
                                                             int step, int sweep, int* rotb, int max_sweeps,
-                                                            double tol) {
+                                                            double tol, int skip_dummy) {
     const int b = blockIdx.y;
     int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
     if (sweep > 0 && rot[sweep - 1] == 0) return;     // converged in an earlier sweep
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int h = blockIdx.x;
+    int h = blockIdx.x;
+    if (skip_dummy) {
+        // the padding block nb - 1 holds no columns: its pair is not launched
+        // (every column pair inside a real block is still reduced by the inner
+        // sweeps of that block's other pairs)
+        const int pos = 1 + (step + nb - 2) % (nb - 1);
+        const int hd = (pos < nb / 2) ? pos : nb - 1 - pos;
+        h += (h >= hd) ? 1 : 0;
+    }
     const int bi = ring_slot(h, step, nb);
     const int bj = ring_slot(nb - 1 - h, step, nb);
     const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
@@ -606,8 +614,11 @@ hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float*
 
 hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
                               int max_sweeps, double tol, int batch, hipStream_t stream) {
-    hipLaunchKernelGGL(jacobi_pair_kernel, dim3(nblocks / 2, batch), dim3(JT), 0, stream, Yt, k, strideX, nblocks,
-                       step, sweep, rot, max_sweeps, tol);
+    // an odd number of real blocks (at least 3) leaves one padding block
+    const int nreal = (k + JB - 1) / JB;
+    const int skip_dummy = (nblocks > nreal && nreal >= 3) ? 1 : 0;
+    hipLaunchKernelGGL(jacobi_pair_kernel, dim3(nblocks / 2 - skip_dummy, batch), dim3(JT), 0, stream, Yt, k,
+                       strideX, nblocks, step, sweep, rot, max_sweeps, tol, skip_dummy);
     return hipGetLastError();
 }
 
