@@ -119,7 +119,7 @@ __device__ __forceinline__ double dpp_odd_partner(double v, bool odd) {
 // of the columns. LDS: region A holds the Gram (fp64, 64 x 65), then the fp32
 // Theta and row chunk of the rotation; region B first the two fp64 staging
 // buffers of the Gram's row chunks, then Theta (fp64).
-__global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
+__global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
                                                             int step, int sweep, int* rotb, int max_sweeps,
                                                             double tol, int skip_dummy) {
     const int b = blockIdx.y;
@@ -141,8 +141,11 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, i
     const int bj = ring_slot(nb - 1 - h, step, nb);
     const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
 
+    // one 64 x 65 fp64 LDS buffer, reused phase by phase: the Gram's staged row
+    // chunks, then the Gram, then the inner sweep's exchange arrays, then the
+    // fp32 Theta and row chunks of the rotation
     __shared__ double G[JW][PD];
-    __shared__ double regB[JW][PD];
+    double (*regB)[PD] = G;
     __shared__ int col[JW];
 
     if (tid < JW) {
@@ -268,13 +271,16 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, i
             gv[j] = G[x][c0 + j];
             tv[j] = (x == c0 + j) ? 1.0 : 0.0;
         }
-        if (wave == 0) Dv[x] = G[x][x];
-        // round 0 reads (x, x+1) for even x straight from G: stage it in Band[0]
+        const double dxx = G[x][x];
+        const double exx = (x & 1) ? 0.0 : G[x][x + 1];
+        __syncthreads();                       // the exchange arrays overwrite the Gram
+        if (wave == 0) Dv[x] = dxx;
+        // round 0 reads (x, x+1) for even x: stage it in Band[0]
         {
             const int jj = x + 1 - c0;
             if (!(x & 1) && jj >= 0 && jj < 16) {
                 double* row = Band + ((0 * 4 + wave) * 16 + jj) * 16;
-                row[jj] = G[x][x + 1];
+                row[jj] = exx;
             }
         }
         __syncthreads();
@@ -403,7 +409,7 @@ __global__ __launch_bounds__(JT, 2) void jacobi_pair_kernel(float* Xtb, int k, i
     // ---- 4. Y_P <- Y_P Theta on the fp32 matrix cores: 64-row chunks through
     //         LDS (the next chunk in flight in registers), results stored from
     //         the accumulators (a lane writes four consecutive rows of a column)
-    float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);          // 64 x 65 fp32 (G is dead)
+    float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);          // 64 x 65 fp32
     float (*Xc)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]) + JW;     // Xc[w][t]: column w, row t
     float* Y = Xtb + static_cast<int64_t>(b) * strideX;
     const bool vec4 = (k & 3) == 0;
