@@ -233,6 +233,154 @@ __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) 
     }
 }
 
+// --------------------------------------------------------------------------
+// Same product, pipelined through LDS by direct loads (K a multiple of 32,
+// 16-byte aligned rows): tile 256 x 128 x 32, four wave64s each owning
+// 128 x 64 (4 x 2 blocks of 32 x 32, times three planes: 24 MFMAs per 16-deep
+// step against 10 fragment reads). Global memory goes straight to LDS
+// (global_load_lds_dwordx4: lane i of an instruction fills bytes 16 i .. 16 i
+// + 15 after the instruction's base), two stages of 40 KB in flight, so no
+// registers stage the operands and two workgroups share a CU's 160 KB. In a
+// stage a row holds four 16-byte chunks, chunk c of row r at slot
+// c ^ ((r >> 2) & 3): the 16 lanes of a fragment read (16 rows, one chunk)
+// fall on distinct banks of the 64-bank LDS. Rows past M (or N) load row
+// M - 1 (N - 1) instead and are never stored.
+// --------------------------------------------------------------------------
+constexpr int YM = 256;
+constexpr int YN = 128;
+constexpr int YK = 32;
+constexpr int YT = 256;
+constexpr int kStageA = YM * YK * 2;                 // bytes
+constexpr int kStageB = 3 * YN * YK * 2;
+constexpr int kStage = kStageA + kStageB;            // 40 KB
+constexpr int kLoadsA = kStageA / 1024 / (YT / 64);  // direct loads per wave per stage (1 KB each)
+constexpr int kLoadsB = kStageB / 1024 / (YT / 64);
+static_assert(kLoadsA == 4 && kLoadsB == 6, "loader split assumes 4 + 6 loads per wave");
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+__device__ __forceinline__ void load_lds16(const void* src, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)lds_base, 16, 0, 0);
+}
+
+__global__ __launch_bounds__(YT, 2) void gemm_bf16x3_direct_kernel(Bx3Args g) {
+    __shared__ __attribute__((aligned(16))) unsigned char ysm[2 * kStage];   // two stages
+
+    const int num_n = gridDim.x, num_m = gridDim.y;
+    const int tiles = num_n * num_m;
+    const int lin = blockIdx.x + num_n * (blockIdx.y + num_m * blockIdx.z);
+    const int logical = xcd_logical_id(lin, tiles * gridDim.z);
+    const int bz = logical / tiles;
+    int tm, tn;
+    grouped_tile(logical - bz * tiles, num_m, num_n, 8, tm, tn);
+    const uint16_t* A = g.A + static_cast<int64_t>(bz) * g.strideA;
+    const uint16_t* B = g.B + static_cast<int64_t>(bz) * g.strideB;
+    float* C = g.C + static_cast<int64_t>(bz) * g.strideC;
+    const int M = g.M, N = g.N, K = g.K;
+    const int row0 = tm * YM, col0 = tn * YN;
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    // this lane's source rows and chunks: a direct load fills 16 rows (4 lanes
+    // per row); lane -> (row 16 j + lane / 4, slot lane % 4), chunk = slot ^ (lane / 16)
+    const int lrow = lane >> 2;
+    const int lchunk = (lane & 3) ^ (lane >> 4);
+    const uint16_t* srcA[kLoadsA];
+#pragma unroll
+    for (int i = 0; i < kLoadsA; ++i) {
+        const int j = wave * kLoadsA + i;                 // 16-row block of the A stage
+        const int r = min(row0 + 16 * j + lrow, M - 1);
+        srcA[i] = A + static_cast<int64_t>(r) * g.lda + 8 * lchunk;
+    }
+    const uint16_t* srcB[kLoadsB];
+#pragma unroll
+    for (int i = 0; i < kLoadsB; ++i) {
+        const int q = wave * kLoadsB + i;                 // plane q / 8, 16-row block q % 8
+        const int pl = q >> 3, j = q & 7;
+        const int r = min(col0 + 16 * j + lrow, N - 1);
+        srcB[i] = B + pl * g.planeStride + static_cast<int64_t>(r) * g.ldb + 8 * lchunk;
+    }
+    auto issue = [&](int stage, int k0) {
+        unsigned char* base = ysm + stage * kStage;
+#pragma unroll
+        for (int i = 0; i < kLoadsA; ++i) load_lds16(srcA[i] + k0, base + (wave * kLoadsA + i) * 1024);
+#pragma unroll
+        for (int i = 0; i < kLoadsB; ++i)
+            load_lds16(srcB[i] + k0, base + kStageA + (wave * kLoadsB + i) * 1024);
+    };
+
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.0f;
+
+    // fragment read offsets (bytes within a stage region): row r, chunk c at
+    // r * 64 + 16 (c ^ ((r >> 2) & 3)); rows of a fragment are r0 + (lane & 31)
+    const int l32 = lane & 31, lk = lane >> 5;
+    const int KT = K / YK;
+    issue(0, 0);
+    for (int kt = 0; kt < KT; ++kt) {
+        if (kt + 1 < KT) {
+            issue((kt + 1) & 1, (kt + 1) * YK);
+            asm volatile("s_waitcnt vmcnt(10)" ::: "memory");       // this stage's 10 loads landed
+        } else {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        asm volatile("s_barrier" ::: "memory");                     // ... and every wave's
+        const unsigned char* sa = ysm + (kt & 1) * kStage;
+        const unsigned char* sb = sa + kStageA;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int c = 2 * ks + lk;
+            bf16x8 a[4], bq[3][2];
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+                const int r = wm * 128 + 32 * x + l32;
+                a[x] = *reinterpret_cast<const bf16x8*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+            }
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+#pragma unroll
+                for (int y = 0; y < 2; ++y) {
+                    const int r = wn * 64 + 32 * y + l32;
+                    bq[p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * 64) + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+                }
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+#pragma unroll
+                for (int x = 0; x < 4; ++x)
+#pragma unroll
+                    for (int y = 0; y < 2; ++y)
+                        acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[x], bq[p][y], acc[x][y], 0, 0, 0);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");   // stage free for reuse
+    }
+
+    const float alpha = g.alpha, beta = g.beta;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const int c = col0 + wn * 64 + 32 * y + l32;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int r = row0 + wm * 128 + 32 * x + (v & 3) + 8 * (v >> 2) + 4 * lk;
+                if (r < M && c < N) {
+                    float* dst = C + static_cast<int64_t>(r) * g.ldc + c;
+                    float val = alpha * acc[x][y][v];
+                    if (beta != 0.0f) val += beta * (*dst);
+                    *dst = val;
+                }
+            }
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, void* dst, int64_t ldd,
@@ -276,6 +424,11 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, const
     const int vec = (lda % 8 == 0) && (ldb % 8 == 0) && (planeStride % 8 == 0) &&
                     (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
                     (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
+    if (vec && K % YK == 0 && K > 0) {
+        dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
+        hipLaunchKernelGGL(gemm_bf16x3_direct_kernel, grid, dim3(YT), 0, stream, g);
+        return hipGetLastError();
+    }
     dim3 grid((N + XN - 1) / XN, (M + XM - 1) / XM, batch);
     hipLaunchKernelGGL(gemm_bf16x3_kernel, grid, dim3(XT), 0, stream, g, vec);
     return hipGetLastError();
