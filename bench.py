@@ -219,6 +219,8 @@ def main():
     V = torch.zeros_like(R)
     N = torch.empty_like(R)
     ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B, G.dtype),), dtype=torch.uint8, device=dev)
+    pws_bytes = gl.galore_project_workspace_size(m, n, r, B, G.dtype)
+    pws = torch.empty((pws_bytes,), dtype=torch.uint8, device=dev) if pws_bytes > 0 else False
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     outer = ("rsvd", "project", "adam", "project_back")
@@ -236,7 +238,7 @@ def main():
                                                            info=info, workspace=ws, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        gl.galore_project(P, G, R=R, stream=stream)
+        gl.galore_project(P, G, R=R, workspace=pws, stream=stream)
         if ev is not None:
             ev[2].record(stream)
         gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, t + 1, stream=stream)
@@ -301,7 +303,7 @@ def main():
         "product_A": (prod_bound, 2.0 * s * l * k * B),
         "product_At": (prod_bound, 2.0 * s * l * k * B),
         "projector": ("mfma", 2.0 * s * k * r * B),
-        "project": ("mfma", 2.0 * r * s * l * B),
+        "project": (prod_bound, 2.0 * r * s * l * B),
         "project_back": ("mfma", 2.0 * r * s * l * B),
         "adam": ("hbm", float(ADAM_BYTES_PER_ELEM * B * r * l)),
         # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches
@@ -382,7 +384,7 @@ def main():
         "kernel_rates": rates,
         "roofline": roof,
     }
-    del G, W, R, M, V, N, ws
+    del G, W, R, M, V, N, ws, pws
     torch.cuda.empty_cache()
     if args.cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)

@@ -150,14 +150,32 @@ GALORE_API int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t
                               hipEvent_t* events, int32_t* stages, int32_t capacity, int32_t* count);
 
 /*
+ * Bytes of workspace galore_project uses for `batch` m x n matrices with rank
+ * r and gradient storage g_dtype: for a bf16 gradient, the three bf16 planes
+ * of P^T that feed the bf16 matrix cores; 0 for an fp32 gradient (which needs
+ * none) and for invalid sizes or dtype.
+ */
+GALORE_API size_t galore_project_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch, int32_t g_dtype);
+
+/*
  * Projection R = P^T A (paper §3, R_t = P_t^T G_t; paper Alg. 1).
  * P: fp32 s x r (ld ldp); G: g_dtype m x n (ld ldg); R: fp32 r x l (ld ldr).
  * For m > n this is R = (G P)^T.
- * Errors: NULL pointers -> INVALID_ARG; sizes/ld invalid, r > s -> SHAPE.
+ * Workspace (optional, device, 256-byte aligned, scratch): with a bf16
+ * gradient and at least galore_project_workspace_size(...) bytes, P is split
+ * there into three bf16 planes (P = P1 + P2 + P3 exactly to fp32 rounding)
+ * and the product runs on the bf16 matrix cores with fp32 accumulation
+ * (16-byte aligned rows of G and s a multiple of 32; otherwise, and with
+ * workspace NULL, it runs on the fp32 matrix cores). The result is the
+ * fp32-accurate product either way.
+ * Errors: NULL P/G/R -> INVALID_ARG; sizes/ld invalid, r > s -> SHAPE;
+ * misaligned workspace, or bf16 G with a non-NULL workspace shorter than
+ * galore_project_workspace_size(...) -> WORKSPACE.
  */
 GALORE_API int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
                    int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
-                   int64_t ldr, int64_t stride_r, int32_t batch, hipStream_t stream);
+                   int64_t ldr, int64_t stride_r, int32_t batch, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream);
 
 /*
  * Low-rank Adam on the rows x cols projected state (paper §3 moment equations;

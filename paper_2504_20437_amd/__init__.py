@@ -21,7 +21,8 @@ GALORE_OK = 0
 
 EXPORTED = (
     "galore_status_string", "galore_version", "galore_sketch", "galore_rsvd_workspace_size",
-    "galore_rsvd_update", "galore_rsvd_update_traced", "galore_project", "galore_lowrank_adam_step",
+    "galore_rsvd_update", "galore_rsvd_update_traced", "galore_project_workspace_size", "galore_project",
+    "galore_lowrank_adam_step",
     "galore_project_back",
 )
 
@@ -53,8 +54,10 @@ def _declare(lib):
     lib.galore_rsvd_update_traced.argtypes = lib.galore_rsvd_update.argtypes + [
         ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_int32), i32, ctypes.POINTER(ctypes.c_int32)]
     lib.galore_rsvd_update_traced.restype = ctypes.c_int
+    lib.galore_project_workspace_size.argtypes = [i64, i64, i32, i32, i32]
+    lib.galore_project_workspace_size.restype = sz
     lib.galore_project.argtypes = [vp, i64, i64, vp, i32, i64, i64, i64, i64, i32, vp, i64, i64,
-                                   i32, vp]
+                                   i32, vp, sz, vp]
     lib.galore_project.restype = ctypes.c_int
     lib.galore_lowrank_adam_step.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, f32, f32, f32,
                                              i64, vp]
@@ -177,15 +180,26 @@ def galore_rsvd_update_traced(G: torch.Tensor, r: int, p: int, q: int, seed: int
     return P, sigma, info, [STAGES[st[i]] for i in range(cnt.value)]
 
 
-def galore_project(P: torch.Tensor, G: torch.Tensor, R=None, stream=None):
-    """R = P^T A ((r, l) or (batch, r, l))."""
+def galore_project_workspace_size(m: int, n: int, r: int, batch: int = 1, dtype=torch.float32) -> int:
+    code = GALORE_BF16 if dtype in (torch.bfloat16, GALORE_BF16, "bf16") else GALORE_F32
+    return int(lib.galore_project_workspace_size(m, n, r, batch, code))
+
+
+def galore_project(P: torch.Tensor, G: torch.Tensor, R=None, workspace=None, stream=None):
+    """R = P^T A ((r, l) or (batch, r, l)). A bf16 G gets a workspace of
+    galore_project_workspace_size bytes unless one is passed; workspace=False
+    passes none."""
     pp, s, r, ldp, sp, pb = _mat(P, "P")
     gp, m, n, ldg, sg, batch = _mat(G, "G")
     l = max(m, n)
     if R is None:
         R = torch.empty((batch, r, l) if G.dim() == 3 else (r, l), dtype=torch.float32, device=G.device)
     rp, _, _, ldr, sr, _ = _mat(R, "R")
-    _check(lib.galore_project(pp, ldp, sp, gp, _dtype_code(G), m, n, ldg, sg, r, rp, ldr, sr, batch,
+    if workspace is None:
+        need = galore_project_workspace_size(m, n, r, batch, G.dtype)
+        workspace = torch.empty((need,), dtype=torch.uint8, device=G.device) if need > 0 else False
+    wp, wb = (None, 0) if workspace is False else (workspace.data_ptr(), workspace.numel())
+    _check(lib.galore_project(pp, ldp, sp, gp, _dtype_code(G), m, n, ldg, sg, r, rp, ldr, sr, batch, wp, wb,
                               _stream(stream)), "galore_project")
     return R
 

@@ -28,6 +28,7 @@ namespace galore {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int XM = 128;
 constexpr int XN = 128;
@@ -113,6 +114,7 @@ struct Bx3Args {
     int64_t ldc, strideC;
     int M, N, K;
     float alpha, beta;
+    int c_trans;                // direct kernel only: store C^T (C[n * ldc + m])
 };
 
 __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) {
@@ -248,14 +250,7 @@ __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) 
 // --------------------------------------------------------------------------
 constexpr int YM = 256;
 constexpr int YN = 128;
-constexpr int YK = 32;
 constexpr int YT = 256;
-constexpr int kStageA = YM * YK * 2;                 // bytes
-constexpr int kStageB = 3 * YN * YK * 2;
-constexpr int kStage = kStageA + kStageB;            // 40 KB
-constexpr int kLoadsA = kStageA / 1024 / (YT / 64);  // direct loads per wave per stage (1 KB each)
-constexpr int kLoadsB = kStageB / 1024 / (YT / 64);
-static_assert(kLoadsA == 4 && kLoadsB == 6, "loader split assumes 4 + 6 loads per wave");
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
@@ -264,8 +259,33 @@ __device__ __forceinline__ void load_lds16(const void* src, void* lds_base) {
     __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)lds_base, 16, 0, 0);
 }
 
-__global__ __launch_bounds__(YT, 2) void gemm_bf16x3_direct_kernel(Bx3Args g) {
-    __shared__ __attribute__((aligned(16))) unsigned char ysm[2 * kStage];   // two stages
+// wait until at most n direct loads of this wave are outstanding
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(n) : "memory");
+}
+template <int L, int S>
+__device__ __forceinline__ void wait_stages(int ahead) {
+    // ahead = stages issued after the one needed now (0 .. S - 1)
+    if constexpr (S >= 4) { if (ahead >= 3) { wait_vm<3 * L>(); return; } }
+    if constexpr (S >= 3) { if (ahead == 2) { wait_vm<2 * L>(); return; } }
+    if (ahead >= 1) { wait_vm<L>(); return; }
+    wait_vm<0>();
+}
+
+template <int YK, int S, bool AT>
+__global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
+    static_assert(!AT || YK == 32, "the M-contiguous A stage assumes 32-deep stages");
+    constexpr int CPR = YK / 8;                          // 16-byte chunks per row
+    constexpr int RB = YK * 2;                           // bytes per row
+    constexpr int kStageA = YM * RB;
+    constexpr int kStageB = 3 * YN * RB;
+    constexpr int kStage = kStageA + kStageB;
+    constexpr int LA = kStageA / 1024 / (YT / 64);       // direct loads per wave per stage (1 KB each)
+    constexpr int LB = kStageB / 1024 / (YT / 64);
+    constexpr int RPI = 64 / CPR;                        // rows per direct load
+    constexpr int RPB = 256 / RB;                        // rows per 256 bytes (one sweep of the 64 banks)
+    __shared__ __attribute__((aligned(16))) unsigned char ysm[S * kStage];
 
     const int num_n = gridDim.x, num_m = gridDim.y;
     const int tiles = num_n * num_m;
@@ -283,32 +303,45 @@ __global__ __launch_bounds__(YT, 2) void gemm_bf16x3_direct_kernel(Bx3Args g) {
     const int lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // this lane's source rows and chunks: a direct load fills 16 rows (4 lanes
-    // per row); lane -> (row 16 j + lane / 4, slot lane % 4), chunk = slot ^ (lane / 16)
-    const int lrow = lane >> 2;
-    const int lchunk = (lane & 3) ^ (lane >> 4);
-    const uint16_t* srcA[kLoadsA];
+    // chunk c of stage row r sits at slot c ^ ((r / RPB) % CPR). A direct load
+    // fills RPI rows; lane i -> (row RPI j + i / CPR, slot i % CPR), so it
+    // fetches the chunk whose slot that is
+    const int lrow = lane / CPR;
+    const uint16_t* srcA[LA];
 #pragma unroll
-    for (int i = 0; i < kLoadsA; ++i) {
-        const int j = wave * kLoadsA + i;                 // 16-row block of the A stage
-        const int r = min(row0 + 16 * j + lrow, M - 1);
-        srcA[i] = A + static_cast<int64_t>(r) * g.lda + 8 * lchunk;
+    for (int i = 0; i < LA; ++i) {
+        const int j = wave * LA + i;
+        if constexpr (AT) {
+            // M-contiguous A (A[kk * lda + i]): a stage row is one kk, 256 m
+            // (32 chunks, 512 bytes), chunk c at slot c ^ (4 (kk % 4)); a direct
+            // load fills 2 rows; chunks past M load the last chunk (M % 8 == 0)
+            const int sr = 2 * j + (lane >> 5);
+            const int slot = lane & 31;
+            const int m = min(row0 + 8 * (slot ^ (4 * (sr & 3))), M - 8);
+            srcA[i] = A + static_cast<int64_t>(sr) * g.lda + m;
+        } else {
+            const int sr = RPI * j + lrow;               // row within the stage
+            const int r = min(row0 + sr, M - 1);
+            srcA[i] = A + static_cast<int64_t>(r) * g.lda + 8 * ((lane % CPR) ^ ((sr / RPB) % CPR));
+        }
     }
-    const uint16_t* srcB[kLoadsB];
+    const int64_t kstepA = AT ? static_cast<int64_t>(YK) * g.lda : YK;   // A advance per stage
+    const uint16_t* srcB[LB];
 #pragma unroll
-    for (int i = 0; i < kLoadsB; ++i) {
-        const int q = wave * kLoadsB + i;                 // plane q / 8, 16-row block q % 8
-        const int pl = q >> 3, j = q & 7;
-        const int r = min(col0 + 16 * j + lrow, N - 1);
-        srcB[i] = B + pl * g.planeStride + static_cast<int64_t>(r) * g.ldb + 8 * lchunk;
+    for (int i = 0; i < LB; ++i) {
+        const int q = wave * LB + i;                     // plane q / (YN / RPI), block q % (YN / RPI)
+        const int pl = q / (YN / RPI), j = q % (YN / RPI);
+        const int sr = RPI * j + lrow;
+        const int r = min(col0 + sr, N - 1);
+        srcB[i] = B + pl * g.planeStride + static_cast<int64_t>(r) * g.ldb + 8 * ((lane % CPR) ^ ((sr / RPB) % CPR));
     }
     auto issue = [&](int stage, int k0) {
         unsigned char* base = ysm + stage * kStage;
+        const int64_t offA = (k0 / YK) * kstepA;
 #pragma unroll
-        for (int i = 0; i < kLoadsA; ++i) load_lds16(srcA[i] + k0, base + (wave * kLoadsA + i) * 1024);
+        for (int i = 0; i < LA; ++i) load_lds16(srcA[i] + offA, base + (wave * LA + i) * 1024);
 #pragma unroll
-        for (int i = 0; i < kLoadsB; ++i)
-            load_lds16(srcB[i] + k0, base + kStageA + (wave * kLoadsB + i) * 1024);
+        for (int i = 0; i < LB; ++i) load_lds16(srcB[i] + k0, base + kStageA + (wave * LB + i) * 1024);
     };
 
     f32x16 acc[4][2];
@@ -319,36 +352,55 @@ __global__ __launch_bounds__(YT, 2) void gemm_bf16x3_direct_kernel(Bx3Args g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.0f;
 
-    // fragment read offsets (bytes within a stage region): row r, chunk c at
-    // r * 64 + 16 (c ^ ((r >> 2) & 3)); rows of a fragment are r0 + (lane & 31)
     const int l32 = lane & 31, lk = lane >> 5;
     const int KT = K / YK;
-    issue(0, 0);
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st)
+        if (st < KT) issue(st, st * YK);
     for (int kt = 0; kt < KT; ++kt) {
-        if (kt + 1 < KT) {
-            issue((kt + 1) & 1, (kt + 1) * YK);
-            asm volatile("s_waitcnt vmcnt(10)" ::: "memory");       // this stage's 10 loads landed
-        } else {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        }
-        asm volatile("s_barrier" ::: "memory");                     // ... and every wave's
-        const unsigned char* sa = ysm + (kt & 1) * kStage;
+        // stage kt landed for this wave, then for every wave; past the barrier
+        // every wave has also finished iteration kt - 1, so its stage is refilled
+        wait_stages<LA + LB, S>(min(S - 2, KT - 1 - kt));
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
+        const unsigned char* sa = ysm + (kt % S) * kStage;
         const unsigned char* sb = sa + kStageA;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int ks = 0; ks < YK / 16; ++ks) {
             const int c = 2 * ks + lk;
             bf16x8 a[4], bq[3][2];
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
-                const int r = wm * 128 + 32 * x + l32;
-                a[x] = *reinterpret_cast<const bf16x8*>(sa + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+                if constexpr (AT) {
+                    // transposing LDS reads: in each group of 16 lanes, lane j
+                    // receives element j % 4 of lanes 4 e + j / 4 (e = 0..3). Lane
+                    // L of the group points at row kk = kb + L / 4, m = mb + 4 (L % 4),
+                    // so lane j gets A[mb + j][kb .. kb + 3]
+                    const int L = lane & 15;
+                    const int m = wm * 128 + 32 * x + 16 * ((lane >> 4) & 1) + 4 * (L & 3);
+                    bf16x4 h2[2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int kk = 16 * ks + 8 * lk + 4 * h + (L >> 2);
+                        const int off = kk * 512 + 16 * ((m >> 3) ^ (4 * (kk & 3))) + 2 * (m & 7);
+                        h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                            reinterpret_cast<__attribute__((address_space(3))) bf16x4*>(
+                                reinterpret_cast<__attribute__((address_space(3))) unsigned char*>(
+                                    reinterpret_cast<size_t>(sa)) + off));
+                    }
+                    a[x] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
+                } else {
+                    const int r = wm * 128 + 32 * x + l32;
+                    a[x] = *reinterpret_cast<const bf16x8*>(sa + r * RB + 16 * (c ^ ((r / RPB) % CPR)));
+                }
             }
 #pragma unroll
             for (int p = 0; p < 3; ++p)
 #pragma unroll
                 for (int y = 0; y < 2; ++y) {
                     const int r = wn * 64 + 32 * y + l32;
-                    bq[p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * 64) + r * 64 + 16 * (c ^ ((r >> 2) & 3)));
+                    bq[p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * RB) + r * RB +
+                                                                16 * (c ^ ((r / RPB) % CPR)));
                 }
 #pragma unroll
             for (int p = 0; p < 3; ++p)
@@ -358,10 +410,37 @@ __global__ __launch_bounds__(YT, 2) void gemm_bf16x3_direct_kernel(Bx3Args g) {
                     for (int y = 0; y < 2; ++y)
                         acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[x], bq[p][y], acc[x][y], 0, 0, 0);
         }
-        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");   // stage free for reuse
     }
 
     const float alpha = g.alpha, beta = g.beta;
+    if (g.c_trans) {
+        // C^T: a lane's registers v = 4 q .. 4 q + 3 hold four consecutive m of
+        // one n, i.e. four consecutive entries of row n of the stored matrix
+        const bool v4 = (g.ldc % 4) == 0 && (reinterpret_cast<uintptr_t>(C) % 16) == 0;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+                const int c = col0 + wn * 64 + 32 * y + l32;
+                if (c >= N) continue;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int r = row0 + wm * 128 + 32 * x + 8 * q + 4 * lk;
+                    float* dst = C + static_cast<int64_t>(c) * g.ldc + r;
+                    f32x4 val = {alpha * acc[x][y][4 * q], alpha * acc[x][y][4 * q + 1], alpha * acc[x][y][4 * q + 2],
+                                 alpha * acc[x][y][4 * q + 3]};
+                    if (v4 && r + 4 <= M && beta == 0.0f) {
+                        *reinterpret_cast<f32x4*>(dst) = val;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (r + e < M) dst[e] = (beta != 0.0f) ? val[e] + beta * dst[e] : val[e];
+                    }
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
 #pragma unroll
@@ -380,6 +459,15 @@ __global__ __launch_bounds__(YT, 2) void gemm_bf16x3_direct_kernel(Bx3Args g) {
         }
     }
 }
+
+#ifndef GALORE_BX3_K
+#define GALORE_BX3_K 32
+#endif
+#ifndef GALORE_BX3_S
+#define GALORE_BX3_S 2
+#endif
+constexpr int kDirectK = GALORE_BX3_K;     // K depth of a stage
+constexpr int kDirectS = GALORE_BX3_S;     // stages in LDS
 
 }  // namespace
 
@@ -400,9 +488,20 @@ hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t stride
     return hipGetLastError();
 }
 
-hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
-                              int64_t planeStride, int64_t strideB, float* C, int64_t ldc, int64_t strideC, int M,
-                              int N, int K, float alpha, float beta, int batch, hipStream_t stream) {
+bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
+                      int64_t planeStride, int64_t strideB, int M, int K, int batch, int a_mcontig) {
+    // 16-byte direct loads need 16-byte aligned rows in A and in every plane
+    const bool vec = (lda % 8 == 0) && (ldb % 8 == 0) && (planeStride % 8 == 0) &&
+                     (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
+                     (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
+    const bool mc = !a_mcontig || (M >= 8 && M % 8 == 0);
+    return vec && mc && K > 0 && K % kDirectK == 0;
+}
+
+hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
+                              int64_t ldb, int64_t planeStride, int64_t strideB, float* C, int64_t ldc,
+                              int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
+                              hipStream_t stream) {
     if (M <= 0 || N <= 0 || batch <= 0) return hipSuccess;
     Bx3Args g;
     g.A = static_cast<const uint16_t*>(A);
@@ -420,15 +519,20 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, const
     g.K = K;
     g.alpha = alpha;
     g.beta = beta;
-    // 16-byte loads need 16-byte aligned rows in A and in every plane
+    g.c_trans = c_trans;
+    if (bf16x3_direct_ok(A, lda, strideA, Bplanes, ldb, planeStride, strideB, M, K, batch, a_mcontig)) {
+        dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
+        if (a_mcontig)
+            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, true>), grid, dim3(YT), 0, stream, g);
+        else
+            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false>), grid, dim3(YT), 0, stream, g);
+        return hipGetLastError();
+    }
+    // the register-staged kernel: K-contiguous A, row-major C only
+    if (a_mcontig || c_trans) return hipErrorInvalidValue;
     const int vec = (lda % 8 == 0) && (ldb % 8 == 0) && (planeStride % 8 == 0) &&
                     (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
                     (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
-    if (vec && K % YK == 0 && K > 0) {
-        dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
-        hipLaunchKernelGGL(gemm_bf16x3_direct_kernel, grid, dim3(YT), 0, stream, g);
-        return hipGetLastError();
-    }
     dim3 grid((N + XN - 1) / XN, (M + XM - 1) / XM, batch);
     hipLaunchKernelGGL(gemm_bf16x3_kernel, grid, dim3(XT), 0, stream, g, vec);
     return hipGetLastError();

@@ -113,9 +113,17 @@ hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, 
 hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
                                    int64_t planeStride, int64_t strideP, int rows, int cols, int rows_pad,
                                    int batch, hipStream_t stream);
-hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
-                              int64_t planeStride, int64_t strideB, float* C, int64_t ldc, int64_t strideC, int M,
-                              int N, int K, float alpha, float beta, int batch, hipStream_t stream);
+// C (M x N, or its transpose when c_trans) = alpha A B + beta C with A bf16
+// (rows K-contiguous, A[i * lda + kk], or M-contiguous when a_mcontig,
+// A[kk * lda + i]) and B given as three bf16 planes, each N x K rows.
+// M-contiguous A and transposed C need the direct-load kernel: check
+// bf16x3_direct_ok first (hipErrorInvalidValue otherwise).
+bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
+                      int64_t planeStride, int64_t strideB, int M, int K, int batch, int a_mcontig);
+hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
+                              int64_t ldb, int64_t planeStride, int64_t strideB, float* C, int64_t ldc,
+                              int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
+                              hipStream_t stream);
 
 constexpr int kJacobiBlock = 32;     // columns per Jacobi block (pairs of 64)
 

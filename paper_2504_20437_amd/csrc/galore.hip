@@ -165,8 +165,9 @@ struct Products {
     const Shape* sh;
     const Layout* L;
     GradOp g;
-    uint16_t* gt;       // transposed copy of G, n x ldgt (bf16 path)
+    uint16_t* gt;       // transposed copy of G, n x ldgt (bf16 path without direct loads)
     uint16_t* planes;   // split planes (bf16 path)
+    bool direct;        // bf16: both products read G in place (direct-load kernel)
     int batch;
     hipStream_t st;
 };
@@ -241,12 +242,16 @@ int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, fl
     GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
                   launch_split3_transpose(X, k, strideX, P.planes, L.ldpl, L.planeStride, L.stridePl, l, k,
                                           static_cast<int>(L.ldpl), P.batch, P.st));
-    const void* A = sh.left ? P.g.G : static_cast<const void*>(P.gt);
-    const int64_t lda = sh.left ? P.g.ldg : L.ldgt;
-    const int64_t strideA = sh.left ? P.g.stride : L.strideGt;
+    // left: A = G (K-contiguous); right: A = G^T, read in place (M-contiguous)
+    // or from the transposed copy
+    const bool inplace = sh.left || P.direct;
+    const void* A = inplace ? P.g.G : static_cast<const void*>(P.gt);
+    const int64_t lda = inplace ? P.g.ldg : L.ldgt;
+    const int64_t strideA = inplace ? P.g.stride : L.strideGt;
     GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A,
-                  launch_gemm_bf16x3(A, lda, strideA, P.planes, L.ldpl, L.planeStride, L.stridePl, Y, k, strideY,
-                                     s, k, l, 1.0f, 0.0f, P.batch, P.st));
+                  launch_gemm_bf16x3(A, lda, strideA, sh.left ? 0 : (P.direct ? 1 : 0), P.planes, L.ldpl,
+                                     L.planeStride, L.stridePl, Y, k, strideY, 0, s, k, l, 1.0f, 0.0f, P.batch,
+                                     P.st));
     return GALORE_OK;
 }
 
@@ -262,12 +267,16 @@ int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, f
     GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
                   launch_split3_transpose(Q, k, strideQ, P.planes, L.ldpl, L.planeStride, L.stridePl, s, k,
                                           static_cast<int>(pad8(s)), P.batch, P.st));
-    const void* At = sh.left ? static_cast<const void*>(P.gt) : P.g.G;
-    const int64_t ldat = sh.left ? L.ldgt : P.g.ldg;
-    const int64_t strideAt = sh.left ? L.strideGt : P.g.stride;
+    // left: A^T = G^T, read in place (M-contiguous) or from the transposed
+    // copy; right: A^T = G (K-contiguous)
+    const bool inplace = !sh.left || P.direct;
+    const void* At = inplace ? P.g.G : static_cast<const void*>(P.gt);
+    const int64_t ldat = inplace ? P.g.ldg : L.ldgt;
+    const int64_t strideAt = inplace ? P.g.stride : L.strideGt;
     GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT,
-                  launch_gemm_bf16x3(At, ldat, strideAt, P.planes, L.ldpl, L.planeStride, L.stridePl, Z, k,
-                                     strideZ, l, k, s, 1.0f, 0.0f, P.batch, P.st));
+                  launch_gemm_bf16x3(At, ldat, strideAt, sh.left ? (P.direct ? 1 : 0) : 0, P.planes, L.ldpl,
+                                     L.planeStride, L.stridePl, Z, k, strideZ, 0, l, k, s, 1.0f, 0.0f, P.batch,
+                                     P.st));
     return GALORE_OK;
 }
 
@@ -328,11 +337,20 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     float* Sb = w.f(L.offS2);
 
     Products prod{&sh, &L, gop, L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offGt) : nullptr,
-                  L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offPl) : nullptr, batch, stream};
-    if (L.bf16)   // A^T (left) or A (right) as K-contiguous bf16 rows: G^T, n x m
-        GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
-                      launch_transpose_bf16(G, ldg, stride_g, prod.gt, L.ldgt, L.strideGt, static_cast<int>(m),
-                                            static_cast<int>(n), batch, stream));
+                  L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offPl) : nullptr, false, batch, stream};
+    if (L.bf16) {
+        // both products read G in place when the direct-load kernel takes them:
+        // G rows are K-contiguous for one product and M-contiguous for the other
+        const bool kc_ok = bf16x3_direct_ok(G, ldg, stride_g, prod.planes, L.ldpl, L.planeStride, L.stridePl,
+                                            static_cast<int>(m), static_cast<int>(n), batch, 0);
+        const bool mc_ok = bf16x3_direct_ok(G, ldg, stride_g, prod.planes, L.ldpl, L.planeStride, L.stridePl,
+                                            static_cast<int>(n), static_cast<int>(m), batch, 1);
+        prod.direct = kc_ok && mc_ok;
+        if (!prod.direct)   // A^T (left) or A (right) as K-contiguous bf16 rows: G^T, n x m
+            GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
+                          launch_transpose_bf16(G, ldg, stride_g, prod.gt, L.ldgt, L.strideGt, static_cast<int>(m),
+                                                static_cast<int>(n), batch, stream));
+    }
 
     // a1-a3: sketch, range sample, orthonormalise
     GALORE_TRACED(tr, GALORE_STAGE_SKETCH, launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
@@ -481,9 +499,34 @@ int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t m, int64_t
     return st;
 }
 
+// Workspace of the projection with a bf16 gradient: the three bf16 planes of
+// P^T (r x pad8(s) each) per matrix.
+struct ProjLayout {
+    int64_t ldpl, planeStride, stridePl;
+    size_t total;
+};
+
+ProjLayout make_proj_layout(const Shape& sh, int r, int batch) {
+    ProjLayout pl;
+    pl.ldpl = pad8(sh.s);
+    pl.planeStride = pad_elems(static_cast<int64_t>(r) * pl.ldpl);
+    pl.stridePl = 3 * pl.planeStride;
+    pl.total = align_up(static_cast<size_t>(batch) * pl.stridePl * sizeof(uint16_t), kAlign);
+    return pl;
+}
+
+size_t galore_project_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch, int32_t g_dtype) {
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return 0;
+    if (g_dtype != GALORE_BF16) return 0;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s) return 0;
+    return make_proj_layout(sh, r, batch).total;
+}
+
 int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
                    int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
-                   int64_t ldr, int64_t stride_r, int32_t batch, hipStream_t stream) {
+                   int64_t ldr, int64_t stride_r, int32_t batch, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
     if (P == nullptr || G == nullptr || R == nullptr) return GALORE_ERR_INVALID_ARG;
     if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
     if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
@@ -491,6 +534,25 @@ int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G,
     if (r > sh.s || ldp < r || ldg < n || ldr < sh.l) return GALORE_ERR_SHAPE;
     if (batch > 1 && (stride_p < sh.s * ldp || stride_g < m * ldg || stride_r < r * ldr))
         return GALORE_ERR_SHAPE;
+    if (workspace != nullptr && (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0) return GALORE_ERR_WORKSPACE;
+    if (g_dtype == GALORE_BF16 && workspace != nullptr) {
+        const ProjLayout pl = make_proj_layout(sh, r, batch);
+        if (workspace_bytes < pl.total) return GALORE_ERR_WORKSPACE;
+        uint16_t* planes = static_cast<uint16_t*>(workspace);
+        // R^T (l x r) = A^T P on the bf16 matrix cores, stored transposed into R:
+        // left: A^T = G^T (G read M-contiguous); right: A^T = G (K-contiguous)
+        const int a_mc = sh.left ? 1 : 0;
+        if (bf16x3_direct_ok(G, ldg, stride_g, planes, pl.ldpl, pl.planeStride, pl.stridePl,
+                             static_cast<int>(sh.l), static_cast<int>(sh.s), batch, a_mc)) {
+            GALORE_TRY(launch_split3_transpose(P, ldp, (batch > 1) ? stride_p : sh.s * ldp, planes, pl.ldpl,
+                                               pl.planeStride, pl.stridePl, static_cast<int>(sh.s), r,
+                                               static_cast<int>(pl.ldpl), batch, stream));
+            GALORE_TRY(launch_gemm_bf16x3(G, ldg, stride_g, a_mc, planes, pl.ldpl, pl.planeStride, pl.stridePl, R,
+                                          ldr, stride_r, 1, static_cast<int>(sh.l), r, static_cast<int>(sh.s),
+                                          1.0f, 0.0f, batch, stream));
+            return GALORE_OK;
+        }
+    }
     GemmArgs a{};
     // R (r x l) = P^T A : A-operand P^T (P[kk][i], M contiguous), B-operand A
     a.A = P;

@@ -90,12 +90,27 @@ def test_project_rejects():
     def call(**kw):
         a = dict(ok); a.update(kw)
         return f(a["P"], a["ldp"], a["sp"], a["G"], a["dt"], a["m"], a["n"], a["ldg"], a["sg"], a["r"],
-                 a["R"], a["ldr"], a["sr"], a["b"], None)
+                 a["R"], a["ldr"], a["sr"], a["b"], a.get("ws"), a.get("wb", 0), None)
     assert call(P=NULL) == -1 and call(G=NULL) == -1 and call(R=NULL) == -1 and call(dt=3) == -1
     assert call(r=65) == -2 and call(ldr=95) == -2 and call(ldp=7) == -2 and call(ldg=10) == -2
     assert call(m=0) == -2 and call(b=0) == -2 and call(b=2) == -2
     # right projector: l = m
     assert call(m=200, n=96, ldr=199) == -2
+    # bf16 gradient: a workspace, when given, must be aligned and large enough
+    need = gl.galore_project_workspace_size(64, 96, 8, 1, "bf16")
+    assert call(dt=1, ws=FAKE, wb=need - 1) == -3 and call(dt=1, ws=FAKE + 8, wb=need) == -3
+
+
+def test_project_workspace_size():
+    import paper_2504_20437_amd as gl
+    assert gl.galore_project_workspace_size(64, 96, 8, 1, "f32") == 0
+    one = gl.galore_project_workspace_size(64, 96, 8, 1, "bf16")
+    assert one >= 3 * 8 * 64 * 2 and one % 256 == 0
+    assert gl.galore_project_workspace_size(64, 96, 8, 4, "bf16") >= 4 * 3 * 8 * 64 * 2
+    # right projector: planes of P^T span s = n
+    assert gl.galore_project_workspace_size(96, 64, 8, 1, "bf16") == one
+    assert gl.galore_project_workspace_size(64, 96, 65, 1, "bf16") == 0
+    assert gl.galore_project_workspace_size(0, 96, 8, 1, "bf16") == 0
 
 
 def test_adam_rejects():

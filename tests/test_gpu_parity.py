@@ -67,8 +67,12 @@ def test_sketch_matches_oracle(gl, orc, l, k, seed, idx):
 # ---------------------------------------------------------------- projection
 
 
+# bf16 cases with s a multiple of 32 run on the bf16 matrix cores (three-plane
+# split of P, G read in place), the others on the fp32 matrix cores
 @pytest.mark.parametrize("m,n,r,dtype", [(300, 517, 37, "f32"), (517, 300, 37, "f32"), (256, 688, 32, "bf16"),
-                                         (1376, 512, 128, "bf16"), (129, 129, 1, "f32"), (64, 2000, 64, "f32")])
+                                         (1376, 512, 128, "bf16"), (129, 129, 1, "f32"), (64, 2000, 64, "f32"),
+                                         (300, 517, 37, "bf16"), (320, 1000, 37, "bf16"), (1000, 320, 37, "bf16"),
+                                         (64, 2000, 64, "bf16"), (96, 96, 1, "bf16")])
 def test_project_matches_oracle(gl, orc, m, n, r, dtype):
     s = min(m, n)
     G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.8), 1e-4, seed=m + n), dtype)
@@ -90,6 +94,24 @@ def test_project_batched_strided(gl, orc):
     R = host(gl.galore_project(dev(Ps), Gd[:, :, :n]))
     for i in range(b):
         assert max_rel_violation(R[i], orc.project(Ps[i].astype(np.float64), Gs[i].exact), 1e-5, 1e-6) <= 1.0
+
+
+def test_project_bf16_paths_agree(gl):
+    """The bf16 matrix-core projection (workspace given) and the fp32 one
+    (no workspace) on the same batched bf16 gradients."""
+    import torch
+    m, n, r, b = 448, 1160, 100, 3
+    G = torch.stack([dev_stored(gi.store(gi.planted_gradient(m, n, gi.spectrum_power(m, 0.8), 1e-4, seed=40 + i),
+                                         "bf16")) for i in range(b)])
+    P = dev(np.stack([np.linalg.qr(np.random.default_rng(i).standard_normal((m, r)))[0]
+                      for i in range(b)]).astype(np.float32))
+    Rw = host(gl.galore_project(P, G))
+    Rf = host(gl.galore_project(P, G, workspace=False))
+    assert max_rel_violation(Rw, Rf, 2e-6, 1e-6 * np.abs(Rf).max()) <= 1.0
+    Gt = G.transpose(1, 2).contiguous()          # right projector on the transposed gradients
+    Rw = host(gl.galore_project(P, Gt))
+    Rf = host(gl.galore_project(P, Gt, workspace=False))
+    assert max_rel_violation(Rw, Rf, 2e-6, 1e-6 * np.abs(Rf).max()) <= 1.0
 
 
 # ---------------------------------------------------------------- Adam
