@@ -221,6 +221,7 @@ def main():
     ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B, G.dtype),), dtype=torch.uint8, device=dev)
     pws_bytes = gl.galore_project_workspace_size(m, n, r, B, G.dtype)
     pws = torch.empty((pws_bytes,), dtype=torch.uint8, device=dev) if pws_bytes > 0 else False
+    bws = torch.empty((gl.galore_project_back_workspace_size(m, n, r, B),), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     outer = ("rsvd", "project", "adam", "project_back")
@@ -244,7 +245,7 @@ def main():
         gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, t + 1, stream=stream)
         if ev is not None:
             ev[3].record(stream)
-        gl.galore_project_back(P, N, W, 1e-3, 0.25, stream=stream)
+        gl.galore_project_back(P, N, W, 1e-3, 0.25, workspace=bws, stream=stream)
         if ev is not None:
             ev[4].record(stream)
         return stages
@@ -304,7 +305,7 @@ def main():
         "product_At": (prod_bound, 2.0 * s * l * k * B),
         "projector": ("mfma", 2.0 * s * k * r * B),
         "project": (prod_bound, 2.0 * r * s * l * B),
-        "project_back": ("mfma", 2.0 * r * s * l * B),
+        "project_back": ("mfma_bf16x6", 2.0 * r * s * l * B),
         "adam": ("hbm", float(ADAM_BYTES_PER_ELEM * B * r * l)),
         # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches
         "gram": ("mfma64", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * B / (n_gram_s + n_gram_l)),
@@ -343,13 +344,17 @@ def main():
         roof = {"kernel": kern, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
     else:
-        peak = {"mfma": FP32_MFMA_PEAK_TFS, "mfma64": FP64_MFMA_PEAK_TFS, "mfma_bf16x3": BF16_MFMA_PEAK_TFS}[bound]
+        peak = {"mfma": FP32_MFMA_PEAK_TFS, "mfma64": FP64_MFMA_PEAK_TFS, "mfma_bf16x3": BF16_MFMA_PEAK_TFS,
+                "mfma_bf16x6": BF16_MFMA_PEAK_TFS}[bound]
         ach = units / (avg_ms * 1e-3) / 1e12
         roof = {"kernel": kern, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4), "traffic": traffic}
         if bound == "mfma_bf16x3":
             roof["mfma_dtype"] = "bf16 (3 exact bf16 products per fp32-accurate product)"
             roof["frac_of_3x_ceiling"] = round(3.0 * ach / peak, 4)
+        if bound == "mfma_bf16x6":
+            roof["mfma_dtype"] = "bf16 (6 bf16 plane products per fp32-accurate product)"
+            roof["frac_of_6x_ceiling"] = round(6.0 * ach / peak, 4)
     roof["traffic_note"] = traffic_note
     roof["launches_timed"] = len(durs)
     roof["avg_launch_ms"] = round(avg_ms, 3)
@@ -384,7 +389,7 @@ def main():
         "kernel_rates": rates,
         "roofline": roof,
     }
-    del G, W, R, M, V, N, ws, pws
+    del G, W, R, M, V, N, ws, pws, bws
     torch.cuda.empty_cache()
     if args.cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)

@@ -194,19 +194,32 @@ GALORE_API int galore_lowrank_adam_step(const float* R, float* M, float* V, floa
                              float beta2, float eps, int64_t t, hipStream_t stream);
 
 /*
+ * Bytes of workspace galore_project_back uses for `batch` m x n matrices with
+ * rank r: three bf16 planes of P and of N^T per matrix. 0 for invalid sizes.
+ */
+GALORE_API size_t galore_project_back_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch);
+
+/*
  * Back-projection and weight update (paper §3: G~ = alpha P N, W <- W + eta G~;
  * paper Alg. 1). The library works with the autograd gradient, so it applies
  *   W <- W - (lr * alpha) * P N         (m <= n)
  *   W <- W - (lr * alpha) * (P N)^T     (m > n)
  * P: fp32 s x r (ld ldp); N: fp32 r x l (ld ldn); W: fp32 m x n (ld ldw),
  * updated in place.
+ * Workspace (optional, device, 256-byte aligned, scratch): with at least
+ * galore_project_back_workspace_size(...) bytes, P and N are split there into
+ * three bf16 planes each (exact to fp32 rounding) and P N runs on the bf16
+ * matrix cores as the six plane products whose size reaches fp32 rounding,
+ * accumulated in fp32 (r a multiple of 32; otherwise, and with workspace NULL,
+ * on the fp32 matrix cores).
  * Errors: NULL pointers -> INVALID_ARG; non-finite lr/alpha -> INVALID_ARG;
- * sizes/ld invalid, r > s -> SHAPE.
+ * sizes/ld invalid, r > s -> SHAPE; misaligned or short non-NULL workspace ->
+ * WORKSPACE.
  */
 GALORE_API int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const float* N,
                         int64_t ldn, int64_t stride_n, float* W, int64_t m, int64_t n,
                         int64_t ldw, int64_t stride_w, int32_t r, float lr, float alpha,
-                        int32_t batch, hipStream_t stream);
+                        int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,7 @@ EXPORTED = (
     "galore_status_string", "galore_version", "galore_sketch", "galore_rsvd_workspace_size",
     "galore_rsvd_update", "galore_rsvd_update_traced", "galore_project_workspace_size", "galore_project",
     "galore_lowrank_adam_step",
-    "galore_project_back",
+    "galore_project_back_workspace_size", "galore_project_back",
 )
 
 # galore_stage_t
@@ -62,8 +62,10 @@ def _declare(lib):
     lib.galore_lowrank_adam_step.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, f32, f32, f32,
                                              i64, vp]
     lib.galore_lowrank_adam_step.restype = ctypes.c_int
+    lib.galore_project_back_workspace_size.argtypes = [i64, i64, i32, i32]
+    lib.galore_project_back_workspace_size.restype = sz
     lib.galore_project_back.argtypes = [vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i64, i32,
-                                        f32, f32, i32, vp]
+                                        f32, f32, i32, vp, sz, vp]
     lib.galore_project_back.restype = ctypes.c_int
     return lib
 
@@ -219,12 +221,22 @@ def galore_lowrank_adam_step(R: torch.Tensor, M: torch.Tensor, V: torch.Tensor, 
     return N
 
 
+def galore_project_back_workspace_size(m: int, n: int, r: int, batch: int = 1) -> int:
+    return int(lib.galore_project_back_workspace_size(m, n, r, batch))
+
+
 def galore_project_back(P: torch.Tensor, N: torch.Tensor, W: torch.Tensor, lr: float, alpha: float,
-                        stream=None):
-    """W <- W - lr*alpha*(P N) (m <= n) or its transpose (m > n), in place."""
+                        workspace=None, stream=None):
+    """W <- W - lr*alpha*(P N) (m <= n) or its transpose (m > n), in place. A
+    workspace of galore_project_back_workspace_size bytes is allocated unless
+    one is passed; workspace=False passes none."""
     pp, s, r, ldp, sp, _ = _mat(P, "P")
     np_, _, _, ldn, sn, _ = _mat(N, "N")
     wp, m, n, ldw, sw, batch = _mat(W, "W")
-    _check(lib.galore_project_back(pp, ldp, sp, np_, ldn, sn, wp, m, n, ldw, sw, r, lr, alpha, batch,
+    if workspace is None:
+        need = galore_project_back_workspace_size(m, n, r, batch)
+        workspace = torch.empty((need,), dtype=torch.uint8, device=W.device) if need > 0 else False
+    wsp, wsb = (None, 0) if workspace is False else (workspace.data_ptr(), workspace.numel())
+    _check(lib.galore_project_back(pp, ldp, sp, np_, ldn, sn, wp, m, n, ldw, sw, r, lr, alpha, batch, wsp, wsb,
                                    _stream(stream)), "galore_project_back")
     return W

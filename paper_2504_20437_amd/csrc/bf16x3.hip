@@ -103,6 +103,57 @@ __global__ __launch_bounds__(256) void split3_transpose_kernel(const float* srcb
 }
 
 // --------------------------------------------------------------------------
+// plane_p (rows x ldp) = split_p(src), src fp32 rows x cols (ld lds), columns
+// cols..cols_pad-1 zero-filled; four consecutive columns per thread (one
+// 16-byte load, one 8-byte store per plane when aligned)
+// --------------------------------------------------------------------------
+__device__ __forceinline__ void split3(float x, uint16_t& h1, uint16_t& h2, uint16_t& h3) {
+    h1 = bf16_bits_rn(x);
+    const float r1 = x - bf16_bits_to_f32(h1);
+    h2 = bf16_bits_rn(r1);
+    const float r2 = r1 - bf16_bits_to_f32(h2);
+    h3 = bf16_bits_rn(r2);
+}
+
+__global__ __launch_bounds__(256) void split3_rows_kernel(const float* srcb, int64_t lds, int64_t strideS,
+                                                          uint16_t* planesb, int64_t ldp, int64_t planeStride,
+                                                          int64_t strideP, int rows, int cols, int cols_pad,
+                                                          int vec) {
+    const int b = blockIdx.z;
+    const float* src = srcb + static_cast<int64_t>(b) * strideS;
+    uint16_t* planes = planesb + static_cast<int64_t>(b) * strideP;
+    const int r = blockIdx.y;
+    const int c0 = 4 * (blockIdx.x * blockDim.x + threadIdx.x);
+    if (r >= rows || c0 >= cols_pad) return;
+    const float* srow = src + static_cast<int64_t>(r) * lds;
+    float x[4];
+    if (vec && c0 + 4 <= cols) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(srow + c0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = v[e];
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = (c0 + e < cols) ? srow[c0 + e] : 0.0f;
+    }
+    uint16_t h[3][4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) split3(x[e], h[0][e], h[1][e], h[2][e]);
+    const int64_t o = static_cast<int64_t>(r) * ldp + c0;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) {
+        uint16_t* dst = planes + o + p * planeStride;
+        if (vec && c0 + 4 <= cols_pad) {
+            *reinterpret_cast<uint2*>(dst) = make_uint2(h[p][0] | (uint32_t(h[p][1]) << 16),
+                                                        h[p][2] | (uint32_t(h[p][3]) << 16));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (c0 + e < cols_pad) dst[e] = h[p][e];
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
 // C (M x N) = alpha * A (M x K bf16 rows) * B^T (3 planes, N x K bf16 rows) + beta * C
 // --------------------------------------------------------------------------
 struct Bx3Args {
@@ -115,6 +166,8 @@ struct Bx3Args {
     int M, N, K;
     float alpha, beta;
     int c_trans;                // direct kernel only: store C^T (C[n * ldc + m])
+    int64_t planeStrideA;       // direct kernel with three A planes: plane p at A + p * planeStrideA
+    int b_upper;                // direct kernel: B upper triangular (B[kk][n] = 0 for kk > n)
 };
 
 __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) {
@@ -273,12 +326,17 @@ __device__ __forceinline__ void wait_stages(int ahead) {
     wait_vm<0>();
 }
 
-template <int YK, int S, bool AT>
-__global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
+// PA = 1: A is exactly bf16 and B holds three planes (three products).
+// PA = 3: both operands hold three planes (fp32 x fp32): the six products
+// A_i B_j with i + j <= 4 (planes counted from 1); the three left out are below
+// 2^-26 of |A||B| in size, under fp32 rounding.
+template <int YK, int S, bool AT, int PA>
+__global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
     static_assert(!AT || YK == 32, "the M-contiguous A stage assumes 32-deep stages");
+    static_assert(PA == 1 || (PA == 3 && !AT), "three A planes are K-contiguous");
     constexpr int CPR = YK / 8;                          // 16-byte chunks per row
     constexpr int RB = YK * 2;                           // bytes per row
-    constexpr int kStageA = YM * RB;
+    constexpr int kStageA = PA * YM * RB;
     constexpr int kStageB = 3 * YN * RB;
     constexpr int kStage = kStageA + kStageB;
     constexpr int LA = kStageA / 1024 / (YT / 64);       // direct loads per wave per stage (1 KB each)
@@ -320,9 +378,11 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
             const int m = min(row0 + 8 * (slot ^ (4 * (sr & 3))), M - 8);
             srcA[i] = A + static_cast<int64_t>(sr) * g.lda + m;
         } else {
-            const int sr = RPI * j + lrow;               // row within the stage
+            const int pl = j / (YM / RPI), jb = j % (YM / RPI);   // plane, block of RPI rows
+            const int sr = RPI * jb + lrow;              // row within the plane's stage
             const int r = min(row0 + sr, M - 1);
-            srcA[i] = A + static_cast<int64_t>(r) * g.lda + 8 * ((lane % CPR) ^ ((sr / RPB) % CPR));
+            srcA[i] = A + pl * g.planeStrideA + static_cast<int64_t>(r) * g.lda +
+                      8 * ((lane % CPR) ^ ((sr / RPB) % CPR));
         }
     }
     const int64_t kstepA = AT ? static_cast<int64_t>(YK) * g.lda : YK;   // A advance per stage
@@ -353,7 +413,7 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
             for (int v = 0; v < 16; ++v) acc[x][y][v] = 0.0f;
 
     const int l32 = lane & 31, lk = lane >> 5;
-    const int KT = K / YK;
+    const int KT = (g.b_upper ? min(K, col0 + YN) : K) / YK;
 #pragma unroll
     for (int st = 0; st < S - 1; ++st)
         if (st < KT) issue(st, st * YK);
@@ -368,7 +428,7 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
 #pragma unroll
         for (int ks = 0; ks < YK / 16; ++ks) {
             const int c = 2 * ks + lk;
-            bf16x8 a[4], bq[3][2];
+            bf16x8 a[PA][4], bq[3][2];
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
                 if constexpr (AT) {
@@ -388,10 +448,13 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
                                 reinterpret_cast<__attribute__((address_space(3))) unsigned char*>(
                                     reinterpret_cast<size_t>(sa)) + off));
                     }
-                    a[x] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
+                    a[0][x] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
                 } else {
                     const int r = wm * 128 + 32 * x + l32;
-                    a[x] = *reinterpret_cast<const bf16x8*>(sa + r * RB + 16 * (c ^ ((r / RPB) % CPR)));
+#pragma unroll
+                    for (int pa = 0; pa < PA; ++pa)
+                        a[pa][x] = *reinterpret_cast<const bf16x8*>(sa + pa * (YM * RB) + r * RB +
+                                                                    16 * (c ^ ((r / RPB) % CPR)));
                 }
             }
 #pragma unroll
@@ -402,13 +465,25 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
                     bq[p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * RB) + r * RB +
                                                                 16 * (c ^ ((r / RPB) % CPR)));
                 }
+            if constexpr (PA == 1) {
 #pragma unroll
-            for (int p = 0; p < 3; ++p)
+                for (int p = 0; p < 3; ++p)
 #pragma unroll
-                for (int x = 0; x < 4; ++x)
+                    for (int x = 0; x < 4; ++x)
 #pragma unroll
-                    for (int y = 0; y < 2; ++y)
-                        acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[x], bq[p][y], acc[x][y], 0, 0, 0);
+                        for (int y = 0; y < 2; ++y)
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][x], bq[p][y], acc[x][y], 0, 0, 0);
+            } else {
+                constexpr int pairs[6][2] = {{0, 0}, {0, 1}, {1, 0}, {0, 2}, {1, 1}, {2, 0}};
+#pragma unroll
+                for (int q = 0; q < 6; ++q)
+#pragma unroll
+                    for (int x = 0; x < 4; ++x)
+#pragma unroll
+                        for (int y = 0; y < 2; ++y)
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pairs[q][0]][x], bq[pairs[q][1]][y],
+                                                                                 acc[x][y], 0, 0, 0);
+            }
         }
     }
 
@@ -429,7 +504,12 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
                     float* dst = C + static_cast<int64_t>(c) * g.ldc + r;
                     f32x4 val = {alpha * acc[x][y][4 * q], alpha * acc[x][y][4 * q + 1], alpha * acc[x][y][4 * q + 2],
                                  alpha * acc[x][y][4 * q + 3]};
-                    if (v4 && r + 4 <= M && beta == 0.0f) {
+                    if (v4 && r + 4 <= M) {
+                        if (beta != 0.0f) {
+                            const f32x4 old = *reinterpret_cast<const f32x4*>(dst);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) val[e] += beta * old[e];
+                        }
                         *reinterpret_cast<f32x4*>(dst) = val;
                     } else {
 #pragma unroll
@@ -468,6 +548,14 @@ __global__ __launch_bounds__(YT, (S * (YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) 
 #endif
 constexpr int kDirectK = GALORE_BX3_K;     // K depth of a stage
 constexpr int kDirectS = GALORE_BX3_S;     // stages in LDS
+#ifndef GALORE_BX6_K
+#define GALORE_BX6_K 16
+#endif
+#ifndef GALORE_BX6_S
+#define GALORE_BX6_S 2
+#endif
+constexpr int kX6K = GALORE_BX6_K;         // the same for three A planes (two 72 KB stages at K = 16:
+constexpr int kX6S = GALORE_BX6_S;         // two workgroups per CU)
 
 }  // namespace
 
@@ -520,12 +608,14 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
     g.alpha = alpha;
     g.beta = beta;
     g.c_trans = c_trans;
+    g.planeStrideA = 0;
+    g.b_upper = 0;
     if (bf16x3_direct_ok(A, lda, strideA, Bplanes, ldb, planeStride, strideB, M, K, batch, a_mcontig)) {
         dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
         if (a_mcontig)
-            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, true>), grid, dim3(YT), 0, stream, g);
+            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, true, 1>), grid, dim3(YT), 0, stream, g);
         else
-            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false>), grid, dim3(YT), 0, stream, g);
+            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false, 1>), grid, dim3(YT), 0, stream, g);
         return hipGetLastError();
     }
     // the register-staged kernel: K-contiguous A, row-major C only
@@ -535,6 +625,59 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
                     (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
     dim3 grid((N + XN - 1) / XN, (M + XM - 1) / XM, batch);
     hipLaunchKernelGGL(gemm_bf16x3_kernel, grid, dim3(XT), 0, stream, g, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_split3_rows(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
+                              int64_t planeStride, int64_t strideP, int rows, int cols, int cols_pad, int batch,
+                              hipStream_t stream) {
+    if (rows <= 0 || cols_pad <= 0 || batch <= 0) return hipSuccess;
+    // 16-byte source rows and 8-byte plane rows
+    const int vec = (lds % 4 == 0) && (batch == 1 || strideS % 4 == 0) && (reinterpret_cast<uintptr_t>(src) % 16 == 0) &&
+                    (ldp % 4 == 0) && (planeStride % 4 == 0) && (batch == 1 || strideP % 4 == 0) &&
+                    (reinterpret_cast<uintptr_t>(planes) % 8 == 0);
+    dim3 grid((cols_pad + 1023) / 1024, rows, batch);
+    hipLaunchKernelGGL(split3_rows_kernel, grid, dim3(256), 0, stream, src, lds, strideS,
+                       static_cast<uint16_t*>(planes), ldp, planeStride, strideP, rows, cols, cols_pad, vec);
+    return hipGetLastError();
+}
+
+bool bf16x6_ok(const void* Aplanes, int64_t lda, int64_t planeStrideA, int64_t strideA, const void* Bplanes,
+               int64_t ldb, int64_t planeStrideB, int64_t strideB, int K, int batch) {
+    return (lda % 8 == 0) && (planeStrideA % 8 == 0) && (ldb % 8 == 0) && (planeStrideB % 8 == 0) &&
+           (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
+           (reinterpret_cast<uintptr_t>(Aplanes) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0) &&
+           K > 0 && K % kX6K == 0;
+}
+
+hipError_t launch_gemm_bf16x6(const void* Aplanes, int64_t lda, int64_t planeStrideA, int64_t strideA,
+                              const void* Bplanes, int64_t ldb, int64_t planeStrideB, int64_t strideB, float* C,
+                              int64_t ldc, int64_t strideC, int c_trans, int b_upper, int M, int N, int K,
+                              float alpha, float beta, int batch, hipStream_t stream) {
+    if (M <= 0 || N <= 0 || batch <= 0) return hipSuccess;
+    if (!bf16x6_ok(Aplanes, lda, planeStrideA, strideA, Bplanes, ldb, planeStrideB, strideB, K, batch))
+        return hipErrorInvalidValue;
+    Bx3Args g;
+    g.A = static_cast<const uint16_t*>(Aplanes);
+    g.lda = lda;
+    g.strideA = strideA;
+    g.B = static_cast<const uint16_t*>(Bplanes);
+    g.ldb = ldb;
+    g.planeStride = planeStrideB;
+    g.strideB = strideB;
+    g.C = C;
+    g.ldc = ldc;
+    g.strideC = strideC;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.alpha = alpha;
+    g.beta = beta;
+    g.c_trans = c_trans;
+    g.planeStrideA = planeStrideA;
+    g.b_upper = b_upper;
+    dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
+    hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kX6K, kX6S, false, 3>), grid, dim3(YT), 0, stream, g);
     return hipGetLastError();
 }
 

@@ -125,6 +125,21 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
                               int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
                               hipStream_t stream);
 
+// fp32 x fp32 products on the bf16 matrix cores: both operands given as three
+// bf16 planes with K-contiguous rows (A: M rows, B: N rows), six plane products
+// accumulated in fp32 (error below fp32 rounding of the products). C as for
+// launch_gemm_bf16x3; b_upper: B[kk][n] = 0 for kk > n (the K loop stops at
+// the tile's last column). Needs bf16x6_ok (hipErrorInvalidValue otherwise).
+hipError_t launch_split3_rows(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
+                              int64_t planeStride, int64_t strideP, int rows, int cols, int cols_pad, int batch,
+                              hipStream_t stream);
+bool bf16x6_ok(const void* Aplanes, int64_t lda, int64_t planeStrideA, int64_t strideA, const void* Bplanes,
+               int64_t ldb, int64_t planeStrideB, int64_t strideB, int K, int batch);
+hipError_t launch_gemm_bf16x6(const void* Aplanes, int64_t lda, int64_t planeStrideA, int64_t strideA,
+                              const void* Bplanes, int64_t ldb, int64_t planeStrideB, int64_t strideB, float* C,
+                              int64_t ldc, int64_t strideC, int c_trans, int b_upper, int M, int N, int K,
+                              float alpha, float beta, int batch, hipStream_t stream);
+
 constexpr int kJacobiBlock = 32;     // columns per Jacobi block (pairs of 64)
 
 }  // namespace galore

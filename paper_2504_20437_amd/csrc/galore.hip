@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include "../../include/galore.h"
+
 #include "common.hpp"
 
 using namespace galore;
@@ -594,10 +595,34 @@ int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64
     return GALORE_OK;
 }
 
+// Workspace of the back-projection: three bf16 planes of P (s x pad8(r) each)
+// and of N^T (l x pad8(r) each) per matrix.
+struct BackLayout {
+    int64_t ldr, planeP, planeN;
+    size_t offN, total;
+};
+
+BackLayout make_back_layout(const Shape& sh, int r, int batch) {
+    BackLayout bl;
+    bl.ldr = pad8(r);
+    bl.planeP = pad_elems(sh.s * bl.ldr);
+    bl.planeN = pad_elems(sh.l * bl.ldr);
+    bl.offN = align_up(static_cast<size_t>(batch) * 3 * bl.planeP * sizeof(uint16_t), kAlign);
+    bl.total = bl.offN + align_up(static_cast<size_t>(batch) * 3 * bl.planeN * sizeof(uint16_t), kAlign);
+    return bl;
+}
+
+size_t galore_project_back_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch) {
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return 0;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s) return 0;
+    return make_back_layout(sh, r, batch).total;
+}
+
 int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const float* N,
                         int64_t ldn, int64_t stride_n, float* W, int64_t m, int64_t n,
                         int64_t ldw, int64_t stride_w, int32_t r, float lr, float alpha,
-                        int32_t batch, hipStream_t stream) {
+                        int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     if (P == nullptr || N == nullptr || W == nullptr) return GALORE_ERR_INVALID_ARG;
     if (!finite_f(lr) || !finite_f(alpha)) return GALORE_ERR_INVALID_ARG;
     if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
@@ -605,6 +630,28 @@ int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const flo
     if (r > sh.s || ldp < r || ldn < sh.l || ldw < n) return GALORE_ERR_SHAPE;
     if (batch > 1 && (stride_p < sh.s * ldp || stride_n < r * ldn || stride_w < m * ldw))
         return GALORE_ERR_SHAPE;
+    if (workspace != nullptr) {
+        if ((reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0) return GALORE_ERR_WORKSPACE;
+        const BackLayout bl = make_back_layout(sh, r, batch);
+        if (workspace_bytes < bl.total) return GALORE_ERR_WORKSPACE;
+        uint16_t* ppl = static_cast<uint16_t*>(workspace);
+        uint16_t* npl = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + bl.offN);
+        if (bf16x6_ok(ppl, bl.ldr, bl.planeP, 3 * bl.planeP, npl, bl.ldr, bl.planeN, 3 * bl.planeN, r, batch)) {
+            // C = P N (s x l) on the bf16 matrix cores, P and N^T split into three
+            // planes each; W += -(lr alpha) C, or its transpose for m > n
+            GALORE_TRY(launch_split3_rows(P, ldp, (batch > 1) ? stride_p : sh.s * ldp, ppl, bl.ldr, bl.planeP,
+                                          3 * bl.planeP, static_cast<int>(sh.s), r, static_cast<int>(bl.ldr), batch,
+                                          stream));
+            GALORE_TRY(launch_split3_transpose(N, ldn, (batch > 1) ? stride_n : r * ldn, npl, bl.ldr, bl.planeN,
+                                               3 * bl.planeN, r, static_cast<int>(sh.l), static_cast<int>(bl.ldr),
+                                               batch, stream));
+            GALORE_TRY(launch_gemm_bf16x6(ppl, bl.ldr, bl.planeP, 3 * bl.planeP, npl, bl.ldr, bl.planeN,
+                                          3 * bl.planeN, W, ldw, stride_w, sh.left ? 0 : 1, 0,
+                                          static_cast<int>(sh.s), static_cast<int>(sh.l), r, -(lr * alpha), 1.0f,
+                                          batch, stream));
+            return GALORE_OK;
+        }
+    }
     GemmArgs a{};
     a.C = W;
     a.ldc = ldw;

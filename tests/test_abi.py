@@ -48,7 +48,7 @@ def test_workspace_size():
     assert gl.galore_rsvd_workspace_size(10, 20, 11, 0, 1) == 0                  # r > s
     assert gl.galore_rsvd_workspace_size(0, 20, 1, 0, 1) == 0
     assert gl.galore_rsvd_workspace_size(5000, 9000, 4090, 10, 1) == 0           # sketch too wide
-    # a bf16 gradient also keeps its transposed copy and the split sketch operand
+    # a bf16 gradient also keeps room for its transposed copy and the split sketch operand
     import torch
     bf = gl.galore_rsvd_workspace_size(4096, 11008, 1024, 32, 1, torch.bfloat16)
     assert bf >= one + 2 * 4096 * 11008 + 3 * 2 * 1056 * 11008
@@ -137,11 +137,23 @@ def test_project_back_rejects():
     def call(**kw):
         a = dict(ok); a.update(kw)
         return f(a["P"], a["ldp"], a["sp"], a["N"], a["ldn"], a["sn"], a["W"], a["m"], a["n"], a["ldw"],
-                 a["sw"], a["r"], a["lr"], a["al"], a["b"], None)
+                 a["sw"], a["r"], a["lr"], a["al"], a["b"], a.get("ws"), a.get("wb", 0), None)
     for kw in (dict(P=NULL), dict(N=NULL), dict(W=NULL), dict(lr=float("nan")), dict(al=float("inf"))):
         assert call(**kw) == -1, kw
     for kw in (dict(r=65), dict(ldn=95), dict(ldw=95), dict(ldp=7), dict(m=0), dict(b=0), dict(b=2)):
         assert call(**kw) == -2, kw
+    need = gl.galore_project_back_workspace_size(64, 96, 8, 1)
+    assert call(ws=FAKE, wb=need - 1) == -3 and call(ws=FAKE + 8, wb=need) == -3
+
+
+def test_project_back_workspace_size():
+    import paper_2504_20437_amd as gl
+    one = gl.galore_project_back_workspace_size(64, 96, 8, 1)
+    assert one >= 3 * 2 * 8 * (64 + 96) and one % 256 == 0
+    assert gl.galore_project_back_workspace_size(96, 64, 8, 1) == one        # orientation
+    assert gl.galore_project_back_workspace_size(64, 96, 8, 3) >= 3 * 3 * 2 * 8 * (64 + 96)
+    assert gl.galore_project_back_workspace_size(64, 96, 65, 1) == 0        # r > s
+    assert gl.galore_project_back_workspace_size(64, 0, 8, 1) == 0
 
 
 def test_sketch_rejects():

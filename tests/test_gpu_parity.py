@@ -152,7 +152,10 @@ def test_adam_in_place_and_strided(gl, orc):
 # ---------------------------------------------------------------- back-projection
 
 
-@pytest.mark.parametrize("m,n,r", [(256, 688, 32), (688, 256, 32), (300, 300, 17), (1376, 512, 128)])
+# r a multiple of 32 runs on the bf16 matrix cores (six plane products), the
+# others on the fp32 matrix cores
+@pytest.mark.parametrize("m,n,r", [(256, 688, 32), (688, 256, 32), (300, 300, 17), (1376, 512, 128),
+                                   (200, 1000, 64), (1000, 200, 96), (64, 64, 64)])
 def test_project_back_matches_oracle(gl, orc, m, n, r):
     s, l = min(m, n), max(m, n)
     rng = np.random.default_rng(m * 7 + n)
@@ -164,6 +167,25 @@ def test_project_back_matches_oracle(gl, orc, m, n, r):
     ref = orc.project_back(P.astype(np.float64), N.astype(np.float64), W.astype(np.float64),
                            float(np.float32(1e-3)), float(np.float32(0.25)))
     assert max_rel_violation(host(Wd), ref, 1e-5, 1e-6) <= 1.0
+
+
+def test_project_back_paths_agree(gl):
+    """Back-projection with the workspace (bf16 matrix cores) and without (fp32
+    matrix cores) on the same batched inputs, both orientations; the weight
+    change itself is compared, not only W."""
+    import torch
+    b, r = 3, 96
+    for m, n in ((320, 900), (900, 320)):
+        s, l = min(m, n), max(m, n)
+        rng = np.random.default_rng(m)
+        P = dev(np.stack([np.linalg.qr(rng.standard_normal((s, r)))[0] for _ in range(b)]).astype(np.float32))
+        N = dev(rng.standard_normal((b, r, l)).astype(np.float32))
+        W0 = torch.zeros((b, m, n), dtype=torch.float32, device="cuda")
+        Ww, Wf = W0.clone(), W0.clone()
+        gl.galore_project_back(P, N, Ww, 1.0, 1.0)
+        gl.galore_project_back(P, N, Wf, 1.0, 1.0, workspace=False)
+        dw, df = host(Ww), host(Wf)
+        assert max_rel_violation(dw, df, 2e-6, 2e-6 * np.abs(df).max()) <= 1.0
 
 
 # ---------------------------------------------------------------- subspace update
