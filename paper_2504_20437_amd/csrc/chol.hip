@@ -79,53 +79,73 @@ __global__ __launch_bounds__(CT) void chol_diag_kernel(double* Cb, int k, int64_
     const int jb = min(CB, k - j0);
     __shared__ double S[CB][LP];
     __shared__ double T[CB][LP];
-    __shared__ double pinv;
     __shared__ int dfl[CB];
+    __shared__ double corig[CB];
 
     if (J == 0) {
         for (int i = tid; i < k; i += CT) diag0[i] = C[static_cast<int64_t>(i) * k + i];
     }
     load_tile(S, C, k, j0, j0, jb, jb);
+    // the original diagonal of this block, staged once (the pivot loop below
+    // is serial and must not wait on global memory)
+    if (tid < jb) corig[tid] = (J == 0) ? C[static_cast<int64_t>(j0 + tid) * k + j0 + tid] : diag0[j0 + tid];
     __syncthreads();
+    // one barrier per column: every thread derives the pivot itself, the
+    // trailing update reads row i unscaled and scales it on the fly, and row i
+    // is rescaled in place after the barrier (no later column reads it)
+    const int tx = tid & 15, ty = tid >> 4;
     for (int i = 0; i < jb; ++i) {
+        const double d = S[i][i];
+        const bool def = (d <= tau_rel * corig[i]);   // NaN compares false
+        const double rii = def ? 0.0 : sqrt(d);
+        const double pv = def ? 0.0 : 1.0 / rii;
+        // rank-1 update of the trailing upper triangle, 16 x 16 threads
+        // striding over it (no division by the runtime extent)
+        for (int a = i + 1 + ty; a < jb; a += 16) {
+            const double sa = S[i][a] * pv;
+            for (int c = i + 1 + tx; c < jb; c += 16)
+                if (c >= a) S[a][c] -= sa * (S[i][c] * pv);
+        }
+        __syncthreads();
+        if (tid > i && tid < jb) S[i][tid] *= pv;
         if (tid == 0) {
-            const double d = S[i][i];
-            const double corig = (J == 0) ? C[static_cast<int64_t>(j0 + i) * k + j0 + i] : diag0[j0 + i];
-            const bool def = (d <= tau_rel * corig);   // NaN compares false
-            dfl[i] = def ? 1 : 0;
-            const double rii = def ? 0.0 : sqrt(d);
             S[i][i] = rii;
-            pinv = def ? 0.0 : 1.0 / rii;
+            dfl[i] = def ? 1 : 0;
         }
-        __syncthreads();
-        if (tid > i && tid < jb) S[i][tid] *= pinv;
-        __syncthreads();
-        const int n = jb - i - 1;
-        for (int idx = tid; idx < n * n; idx += CT) {
-            const int a = i + 1 + idx / n;
-            const int c = i + 1 + idx % n;
-            if (c >= a) S[a][c] -= S[i][a] * S[i][c];
-        }
-        __syncthreads();
     }
+    __syncthreads();
     for (int idx = tid; idx < CB * CB; idx += CT) {
         const int r = idx / CB, c = idx % CB;
         if (r < jb && c < jb && c >= r) C[static_cast<int64_t>(j0 + r) * k + j0 + c] = S[r][c];
     }
     if (tid < jb) defic[j0 + tid] = dfl[tid];
-    // D = R'^-1 of the block (unit rows for deficient pivots), column c by
-    // back substitution; upper triangular.
-    if (tid < jb) {
+    // D = R'^-1 of the block (unit rows for deficient pivots), upper
+    // triangular, by rows from the bottom: lane c of the first wave owns column
+    // c and forms D[i][c] from the entries D[t][c], t > i, it wrote before
+    // (D[t][c] = 0 for t > c, so every lane runs the same loop).
+    if (tid < CB) {
         const int c = tid;
-        for (int i = c; i >= 0; --i) {
-            double v = (i == c) ? 1.0 : 0.0;
-            if (!dfl[i]) {
-                for (int t = i + 1; t <= c; ++t) v -= S[i][t] * T[t][c];
-                v /= S[i][i];
-            } else if (i != c) {
-                v = 0.0;   // unit row: x_i = delta_ic
+        for (int t = 0; t < CB; ++t) T[t][c] = 0.0;
+        for (int i = jb - 1; i >= 0; --i) {
+            // four partial sums, eight independent LDS reads in flight
+            double acc4[4] = {0.0, 0.0, 0.0, 0.0};
+            int t = i + 1;
+            for (; t + 8 <= jb; t += 8) {
+                double sv[8], tv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    sv[e] = S[i][t + e];
+                    tv[e] = T[t + e][c];
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc4[e & 3] = fma(sv[e], tv[e], acc4[e & 3]);
             }
-            T[i][c] = v;
+            for (; t < jb; ++t) acc4[0] = fma(S[i][t], T[t][c], acc4[0]);
+            const double acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
+            double v;
+            if (dfl[i]) v = (c == i) ? 1.0 : 0.0;                     // unit row: x_i = delta_ic
+            else v = (c < i) ? 0.0 : (((c == i) ? 1.0 : 0.0) - acc) / S[i][i];
+            if (c < jb) T[i][c] = v;
         }
     }
     __syncthreads();
