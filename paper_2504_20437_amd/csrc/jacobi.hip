@@ -19,8 +19,9 @@
 //   2. skips the pair if every column pair is already orthogonal to the
 //      tolerance (relative off-diagonal), otherwise
 //   3. reduces the small Gram by one sweep of two-sided Jacobi held in
-//      registers (fp64; odd-even ordering, 64 rounds of up to 32 disjoint
-//      rotations, accumulating the rotation Theta), and
+//      registers (fp32 entries, fp64 diagonal and angles; odd-even ordering,
+//      64 rounds of up to 32 disjoint rotations, accumulating the rotation
+//      Theta), and
 //   4. applies Theta to the pair's 64 columns of Y on the fp32 matrix cores
 //      (v_mfma_f32_32x32x2f32), 64-row chunks staged through LDS.
 // A sweep is nb - 1 steps; the matrix has converged when a whole sweep
@@ -113,6 +114,25 @@ __device__ __forceinline__ double dpp_odd_partner(double v, bool odd) {
     const int hr = __builtin_amdgcn_update_dpp(hi, hi, 0x138, 0xf, 0xf, false);
     return __hiloint2double(odd ? hl : hr, odd ? ll : lr);
 }
+
+__device__ __forceinline__ float dpp_swap_pairs(float v) {
+    const int i = __float_as_int(v);
+    return __int_as_float(__builtin_amdgcn_update_dpp(i, i, 0xB1, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float dpp_odd_partner(float v, bool odd) {
+    const int i = __float_as_int(v);
+    const int l = __builtin_amdgcn_update_dpp(i, i, 0x130, 0xf, 0xf, false);
+    const int r = __builtin_amdgcn_update_dpp(i, i, 0x138, 0xf, 0xf, false);
+    return __int_as_float(odd ? l : r);
+}
+
+// Element type of the inner sweep's Gram and accumulated rotation. fp32: the
+// rotation is applied to fp32 columns on the fp32 matrix cores anyway, the
+// sweep only has to produce an orthogonal Theta that reduces the pair's
+// off-diagonal; the pair Gram, the convergence test, the diagonal the sweep
+// carries and the rotation angles stay fp64, so pairs are judged converged
+// (and the last sweeps are steered) at fp64 accuracy.
+typedef float jreal;
 
 // Step of the block Jacobi (one workgroup per pair and matrix): Gram of the
 // pair's 64 columns, convergence test, reduction of the small Gram, rotation
@@ -260,37 +280,37 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
     //         its off-diagonal entry is read back from the holder each round.
     {
         double* Dv = &regB[0][0];                  // [2][64]: diagonal, ping-pong by round
-        double* CSw = Dv + 2 * JW;                 // [4 waves][64][2]: (c, s) by first slot, wave-private
-        double* Band = CSw + 4 * JW * 2;           // [2][4][16][16]: rows whose (x, x+1) entry a wave holds
-        double* Halo = Band + 2 * 4 * 16 * 16;     // [4 waves][4][64]: edge columns (G left/right, Theta left/right)
+        jreal* CSw = reinterpret_cast<jreal*>(Dv + 2 * JW);   // [4 waves][64][2]: (c, s) by first slot, wave-private
+        jreal* Band = CSw + 4 * JW * 2;            // [2][4][16][16]: rows whose (x, x+1) entry a wave holds
+        jreal* Halo = Band + 2 * 4 * 16 * 16;      // [4 waves][4][64]: edge columns (G left/right, Theta left/right)
         const int x = lane;
         const int c0 = 16 * wave;
-        double gv[16], tv[16];
+        jreal gv[16], tv[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            gv[j] = G[x][c0 + j];
-            tv[j] = (x == c0 + j) ? 1.0 : 0.0;
+            gv[j] = static_cast<jreal>(G[x][c0 + j]);
+            tv[j] = (x == c0 + j) ? jreal(1) : jreal(0);
         }
         const double dxx = G[x][x];
-        const double exx = (x & 1) ? 0.0 : G[x][x + 1];
+        const jreal exx = (x & 1) ? jreal(0) : static_cast<jreal>(G[x][x + 1]);
         __syncthreads();                       // the exchange arrays overwrite the Gram
         if (wave == 0) Dv[x] = dxx;
         // round 0 reads (x, x+1) for even x: stage it in Band[0]
         {
             const int jj = x + 1 - c0;
             if (!(x & 1) && jj >= 0 && jj < 16) {
-                double* row = Band + ((0 * 4 + wave) * 16 + jj) * 16;
+                jreal* row = Band + ((0 * 4 + wave) * 16 + jj) * 16;
                 row[jj] = exx;
             }
         }
         __syncthreads();
-        double hgL = 0.0, hgR = 0.0, htL = 0.0, htR = 0.0;
+        jreal hgL = 0, hgR = 0, htL = 0, htR = 0;
         for (int t = 0; t < JW; ++t) {
             const int par = t & 1;
             const double* Dc = Dv + par * JW;
             double* Dn = Dv + (par ^ 1) * JW;
-            const double* Bc = Band + par * (4 * 16 * 16);
-            double* Bn = Band + (par ^ 1) * (4 * 16 * 16);
+            const jreal* Bc = Band + par * (4 * 16 * 16);
+            jreal* Bn = Band + (par ^ 1) * (4 * 16 * 16);
             if (par) {
                 // halo columns 16 w - 1 and 16 w + 16 as the neighbours left them
                 if (wave > 0) {
@@ -305,12 +325,12 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
             // the pair of row x and its rotation (every lane computes its own)
             const int p = par ? ((x & 1) ? x : x - 1) : (x & ~1);
             const bool idle = par && (x == 0 || x == JW - 1);
-            double c = 0.0, sg = 1.0;          // idle rows stay as they are
+            jreal c = 0, sg = 1;               // idle rows stay as they are
             if (!idle) {
                 const int q = p + 1;
                 const int wq = q >> 4, jq = q & 15;
                 const double a = Dc[p], b = Dc[q];
-                const double g = Bc[(wq * 16 + jq) * 16 + jq];
+                const double g = static_cast<double>(Bc[(wq * 16 + jq) * 16 + jq]);
                 double cr = 1.0, sr = 0.0;
                 if (g * g > 1e-30 * (a * b)) rotation(a, b, g, cr, sr);
                 // rotated slot p' = c p - s q goes to slot q, q' = s p + c q to slot p
@@ -320,11 +340,11 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
                         Dn[p] = sr * sr * a + cs2 + cr * cr * b;
                         Dn[q] = cr * cr * a - cs2 + sr * sr * b;
                     }
-                    CSw[(wave * JW + p) * 2 + 0] = cr;
-                    CSw[(wave * JW + p) * 2 + 1] = sr;
+                    CSw[(wave * JW + p) * 2 + 0] = static_cast<jreal>(cr);
+                    CSw[(wave * JW + p) * 2 + 1] = static_cast<jreal>(sr);
                 }
-                c = cr;
-                sg = (x == p) ? sr : -sr;
+                c = static_cast<jreal>(cr);
+                sg = static_cast<jreal>((x == p) ? sr : -sr);
             } else if ((x >> 4) == wave) {
                 Dn[x] = Dc[x];
             }
@@ -344,37 +364,37 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_wave_barrier();
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            const double* cw = CSw + wave * JW * 2;
+            const jreal* cw = CSw + wave * JW * 2;
             // columns: new col p = s col_p + c col_q, new col q = c col_p - s col_q
             if (!par) {
 #pragma unroll
                 for (int i = 0; i < 8; ++i) {
-                    const double cc = cw[(c0 + 2 * i) * 2 + 0], ss = cw[(c0 + 2 * i) * 2 + 1];
-                    const double g0 = gv[2 * i], g1 = gv[2 * i + 1];
+                    const jreal cc = cw[(c0 + 2 * i) * 2 + 0], ss = cw[(c0 + 2 * i) * 2 + 1];
+                    const jreal g0 = gv[2 * i], g1 = gv[2 * i + 1];
                     gv[2 * i] = ss * g0 + cc * g1;
                     gv[2 * i + 1] = cc * g0 - ss * g1;
-                    const double t0 = tv[2 * i], t1 = tv[2 * i + 1];
+                    const jreal t0 = tv[2 * i], t1 = tv[2 * i + 1];
                     tv[2 * i] = ss * t0 + cc * t1;
                     tv[2 * i + 1] = cc * t0 - ss * t1;
                 }
             } else {
 #pragma unroll
                 for (int i = 0; i < 7; ++i) {
-                    const double cc = cw[(c0 + 2 * i + 1) * 2 + 0], ss = cw[(c0 + 2 * i + 1) * 2 + 1];
-                    const double g0 = gv[2 * i + 1], g1 = gv[2 * i + 2];
+                    const jreal cc = cw[(c0 + 2 * i + 1) * 2 + 0], ss = cw[(c0 + 2 * i + 1) * 2 + 1];
+                    const jreal g0 = gv[2 * i + 1], g1 = gv[2 * i + 2];
                     gv[2 * i + 1] = ss * g0 + cc * g1;
                     gv[2 * i + 2] = cc * g0 - ss * g1;
-                    const double t0 = tv[2 * i + 1], t1 = tv[2 * i + 2];
+                    const jreal t0 = tv[2 * i + 1], t1 = tv[2 * i + 2];
                     tv[2 * i + 1] = ss * t0 + cc * t1;
                     tv[2 * i + 2] = cc * t0 - ss * t1;
                 }
                 if (wave > 0) {      // pair (16 w - 1, 16 w): this wave keeps the second slot
-                    const double cc = cw[(c0 - 1) * 2 + 0], ss = cw[(c0 - 1) * 2 + 1];
+                    const jreal cc = cw[(c0 - 1) * 2 + 0], ss = cw[(c0 - 1) * 2 + 1];
                     gv[0] = cc * hgL - ss * gv[0];
                     tv[0] = cc * htL - ss * tv[0];
                 }
                 if (wave < 3) {      // pair (16 w + 15, 16 w + 16): this wave keeps the first slot
-                    const double cc = cw[(c0 + 15) * 2 + 0], ss = cw[(c0 + 15) * 2 + 1];
+                    const jreal cc = cw[(c0 + 15) * 2 + 0], ss = cw[(c0 + 15) * 2 + 1];
                     gv[15] = ss * gv[15] + cc * hgR;
                     tv[15] = ss * tv[15] + cc * htR;
                 }
@@ -385,7 +405,7 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
                 const int jj = x + 1 - c0;
                 const int np = (par ^ 1) ? ((x & 1) ? x : -1) : ((x & 1) ? -1 : x);   // x first of a next pair?
                 if (np >= 0 && x + 1 < JW && jj >= 0 && jj < 16) {
-                    double* row = Bn + (wave * 16 + jj) * 16;
+                    jreal* row = Bn + (wave * 16 + jj) * 16;
 #pragma unroll
                     for (int j = 0; j < 16; ++j) row[j] = gv[j];
                 }
