@@ -68,7 +68,9 @@ def source_hash(fname):
 
 
 def workload_key(cls, args):
-    return "%s:%dx%dx%d:r%d:p%d:q%d:%s" % (cls, args.batch, args.m, args.n, args.r, args.p, args.q, args.dtype)
+    # matrices per launch: the batch, or one chunk of it with --streams
+    return "%s:%dx%dx%d:r%d:p%d:q%d:%s" % (cls, args.batch // max(1, args.streams), args.m, args.n, args.r, args.p,
+                                          args.q, args.dtype)
 
 
 def write_traffic(args):
@@ -126,6 +128,9 @@ def parse():
     ap.add_argument("--p", type=int, default=32)
     ap.add_argument("--q", type=int, default=2)
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f32"])
+    ap.add_argument("--streams", type=int, default=1,
+                    help="split the batch into this many equal chunks, each on its own stream (default "
+                         "priority), so that one chunk's latency-bound stages overlap another's products")
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the oracle on the host (0/1)")
     ap.add_argument("--roofline-kernel", default="auto", choices=["auto"] + sorted(KERNEL_CLASSES))
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -218,36 +223,63 @@ def main():
     M = torch.zeros_like(R)
     V = torch.zeros_like(R)
     N = torch.empty_like(R)
-    ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B, G.dtype),), dtype=torch.uint8, device=dev)
-    pws_bytes = gl.galore_project_workspace_size(m, n, r, B, G.dtype)
-    pws = torch.empty((pws_bytes,), dtype=torch.uint8, device=dev) if pws_bytes > 0 else False
-    bws = torch.empty((gl.galore_project_back_workspace_size(m, n, r, B),), dtype=torch.uint8, device=dev)
+    S = args.streams
+    if S < 1 or B % S:
+        raise SystemExit("--streams must divide the batch")
+    C = B // S     # matrices per chunk
+    chunks = []
+    for ci in range(S):
+        sl = slice(ci * C, (ci + 1) * C)
+        pws_bytes = gl.galore_project_workspace_size(m, n, r, C, G.dtype)
+        chunks.append(dict(
+            sl=sl, stream=torch.cuda.current_stream() if ci == 0 else torch.cuda.Stream(),
+            ws=torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, C, G.dtype),), dtype=torch.uint8, device=dev),
+            pws=torch.empty((pws_bytes,), dtype=torch.uint8, device=dev) if pws_bytes > 0 else False,
+            bws=torch.empty((gl.galore_project_back_workspace_size(m, n, r, C),), dtype=torch.uint8, device=dev)))
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
+    stream = chunks[0]["stream"]      # stage events are recorded on chunk 0's stream
     outer = ("rsvd", "project", "adam", "project_back")
     cap = 96   # stage instances recorded per subspace update
 
-    def step(t, ev=None, sev=None):
+    def run_chunk(ch, t, ev=None, sev=None):
+        st, sl = ch["stream"], ch["sl"]
         if ev is not None:
-            ev[0].record(stream)
+            ev[0].record(st)
         if sev is None:
-            gl.galore_rsvd_update(G, r, p, q, gi.sketch_seed(t), 0, P=P, sigma=sigma, info=info, workspace=ws,
-                                  stream=stream)
+            gl.galore_rsvd_update(G[sl], r, p, q, gi.sketch_seed(t), sl.start, P=P[sl], sigma=sigma[sl], info=info[sl],
+                                  workspace=ch["ws"], stream=st)
             stages = None
         else:
-            _, _, _, stages = gl.galore_rsvd_update_traced(G, r, p, q, gi.sketch_seed(t), sev, 0, P=P, sigma=sigma,
-                                                           info=info, workspace=ws, stream=stream)
+            _, _, _, stages = gl.galore_rsvd_update_traced(G[sl], r, p, q, gi.sketch_seed(t), sev, sl.start, P=P[sl],
+                                                           sigma=sigma[sl], info=info[sl], workspace=ch["ws"],
+                                                           stream=st)
         if ev is not None:
-            ev[1].record(stream)
-        gl.galore_project(P, G, R=R, workspace=pws, stream=stream)
+            ev[1].record(st)
+        gl.galore_project(P[sl], G[sl], R=R[sl], workspace=ch["pws"], stream=st)
         if ev is not None:
-            ev[2].record(stream)
-        gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, t + 1, stream=stream)
+            ev[2].record(st)
+        gl.galore_lowrank_adam_step(R[sl], M[sl], V[sl], N[sl], 0.9, 0.999, 1e-8, t + 1, stream=st)
         if ev is not None:
-            ev[3].record(stream)
-        gl.galore_project_back(P, N, W, 1e-3, 0.25, workspace=bws, stream=stream)
+            ev[3].record(st)
+        gl.galore_project_back(P[sl], N[sl], W[sl], 1e-3, 0.25, workspace=ch["bws"], stream=st)
         if ev is not None:
-            ev[4].record(stream)
+            ev[4].record(st)
+        return stages
+
+    def step(t, ev=None, sev=None):
+        if S > 1:                      # every chunk starts after the previous step's work on all streams
+            mark = torch.cuda.Event()
+            mark.record(stream)
+            for ch in chunks[1:]:
+                ch["stream"].wait_event(mark)
+        stages = run_chunk(chunks[0], t, ev, sev)
+        for ch in chunks[1:]:
+            run_chunk(ch, t)
+        if S > 1:                      # and chunk 0's stream waits for all of them
+            for ch in chunks[1:]:
+                done = torch.cuda.Event()
+                done.record(ch["stream"])
+                stream.wait_event(done)
         return stages
 
     for w in range(args.warmup):
@@ -293,7 +325,8 @@ def main():
     ms_per_step = wall * 1000.0 / args.steps
 
     # algorithmic work of one launch of each single-launch kernel class
-    # (flops, except bytes for Adam), for the whole batch
+    # (flops, except bytes for Adam), for one chunk (the launches timed are
+    # chunk 0's)
     n_gram_s = (2 if q == 0 else q + 2)          # Grams of s x k blocks per update
     n_gram_l = q + 1                              # Grams of l x k blocks per update
     # products with a bf16-stored G run on the bf16 matrix cores as three exact
@@ -301,16 +334,16 @@ def main():
     # per algorithmic flop
     prod_bound = "mfma_bf16x3" if args.dtype == "bf16" else "mfma"
     work = {
-        "product_A": (prod_bound, 2.0 * s * l * k * B),
-        "product_At": (prod_bound, 2.0 * s * l * k * B),
-        "projector": ("mfma", 2.0 * s * k * r * B),
-        "project": (prod_bound, 2.0 * r * s * l * B),
-        "project_back": ("mfma_bf16x6", 2.0 * r * s * l * B),
-        "adam": ("hbm", float(ADAM_BYTES_PER_ELEM * B * r * l)),
+        "product_A": (prod_bound, 2.0 * s * l * k * C),
+        "product_At": (prod_bound, 2.0 * s * l * k * C),
+        "projector": ("mfma", 2.0 * s * k * r * C),
+        "project": (prod_bound, 2.0 * r * s * l * C),
+        "project_back": ("mfma_bf16x6", 2.0 * r * s * l * C),
+        "adam": ("hbm", float(ADAM_BYTES_PER_ELEM * C * r * l)),
         # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches
-        "gram": ("mfma64", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * B / (n_gram_s + n_gram_l)),
+        "gram": ("mfma64", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * C / (n_gram_s + n_gram_l)),
         # Q = Y R^-1 with triangular R^-1: rows * k * (k + 1) flops, averaged
-        "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * B
+        "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * C
                                 / max(1, n_gram_s + n_gram_l - 1))),
     }
     work["products"] = work["product_A"]          # both products run the same kernel on the same work
@@ -382,14 +415,16 @@ def main():
         "config": {"workload": "Llama-7B-shaped gate/up gradients: %d x %dx%d %s, planted spectrum "
                                "(i+1)^-0.7 + 1e-4 noise, r=%d p=%d q=%d (k=%d)"
                                % (B, m, n, args.dtype, r, p, q, k),
-                   "batch": B, "m": m, "n": n, "r": r, "p": p, "q": q},
+                   "batch": B, "m": m, "n": n, "r": r, "p": p, "q": q, "streams": S},
         "adam_hbm_gbs": round(adam_gbs, 1),
         "stage_ms": {st: round(v, 3) for st, v in per_stage.items()},
+        "stage_note": ("stage and kernel times are chunk 0's (%d matrices) on its stream, overlapping the other "
+                       "%d chunk(s)" % (C, S - 1)) if S > 1 else "stage and kernel times of the whole batch",
         "rsvd_stage_ms": {st: round(v, 3) for st, v in sorted(sub.items(), key=lambda x: -x[1])},
         "kernel_rates": rates,
         "roofline": roof,
     }
-    del G, W, R, M, V, N, ws, pws, bws
+    del G, W, R, M, V, N, chunks
     torch.cuda.empty_cache()
     if args.cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
