@@ -148,9 +148,12 @@ hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t row
                            reinterpret_cast<uintptr_t>(V) | reinterpret_cast<uintptr_t>(N)) & 15) == 0;
     if (contiguous && aligned) {
         const int64_t total = rows * cols * batch;
+        // One 16-byte vector per thread and a grid that covers the whole array: a
+        // capped grid-stride launch (65536 workgroups) streams about 11% slower
+        // at 64 x 1024 x 11008 (5.19 vs 5.83 TB/s measured).
         int64_t blocks = (total / 4 + 255) / 256;
         if (blocks < 1) blocks = 1;
-        if (blocks > 65536) blocks = 65536;
+        if (blocks > 0x7fffffff) blocks = 0x7fffffff;
         hipLaunchKernelGGL(adam_flat_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream,
                            R, M, V, N, total, beta1, beta2, eps, bc1, bc2);
     } else {
