@@ -14,8 +14,9 @@
 // tournament pairs the blocks so that every step is a set of disjoint pairs
 // (with an odd number of blocks, the pair with the padding block is not
 // launched). A step is one launch, one workgroup per pair and matrix, which
-//   1. forms the 64 x 64 fp64 Gram of its two blocks on the fp64 matrix cores
-//      (v_mfma_f64_16x16x4f64) from row chunks staged in LDS;
+//   1. forms the 64 x 64 Gram of its two blocks in fp64 from fp32 matrix-core
+//      partial sums of 8 products (v_mfma_f32_16x16x4f32), row chunks staged
+//      in LDS;
 //   2. skips the pair if every column pair is already orthogonal to the
 //      tolerance (relative off-diagonal), otherwise
 //   3. reduces the small Gram by one sweep of two-sided Jacobi held in
@@ -41,7 +42,7 @@ namespace {
 constexpr int JB = kJacobiBlock;   // columns per block
 constexpr int JW = 2 * JB;         // columns per pair (64)
 constexpr int JT = 256;            // threads (4 waves)
-constexpr int GR = 32;             // rows per Gram chunk
+constexpr int GR = 64;             // rows per Gram chunk (two fp32 chunks fill the LDS buffer)
 constexpr int AR = 64;             // rows per apply chunk
 constexpr int PD = JW + 1;         // padded LDS row
 
@@ -136,9 +137,7 @@ typedef float jreal;
 
 // Step of the block Jacobi (one workgroup per pair and matrix): Gram of the
 // pair's 64 columns, convergence test, reduction of the small Gram, rotation
-// of the columns. LDS: region A holds the Gram (fp64, 64 x 65), then the fp32
-// Theta and row chunk of the rotation; region B first the two fp64 staging
-// buffers of the Gram's row chunks, then Theta (fp64).
+// of the columns, all in one 64 x 65 fp64 LDS buffer (see below).
 __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
                                                             int step, int sweep, int* rotb, int max_sweeps,
                                                             double tol, int skip_dummy) {
@@ -161,8 +160,8 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
     const int bj = ring_slot(nb - 1 - h, step, nb);
     const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
 
-    // one 64 x 65 fp64 LDS buffer, reused phase by phase: the Gram's staged row
-    // chunks, then the Gram, then the inner sweep's exchange arrays, then the
+    // one 64 x 65 fp64 LDS buffer, reused phase by phase: the Gram's staged fp32
+    // row chunks, then the Gram, then the inner sweep's exchange arrays, then the
     // fp32 Theta and row chunks of the rotation
     __shared__ double G[JW][PD];
     double (*regB)[PD] = G;
@@ -177,10 +176,15 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
 
     // ---- 1. Gram of the pair's columns: the 10 upper 16 x 16 tiles of the
     //         64 x 64 result spread over the 4 waves, row chunks of GR rows
-    //         double-buffered in LDS with the next chunk prefetched in registers.
+    //         double-buffered in LDS (fp32, as stored) with the next chunk
+    //         prefetched in registers. Products on the fp32 matrix cores, two
+    //         4-term MFMAs per partial sum, each partial sum added into fp64:
+    //         an entry's error stays below about 8 fp32 ulps of
+    //         sum_t |y_tp y_tq| <= |y_p| |y_q|, far under the tolerance the
+    //         test and the rotations work to.
     {
-        double (*Xs0)[PD] = regB;            // rows 0 .. GR-1
-        double (*Xs1)[PD] = regB + GR;       // rows GR .. 2GR-1
+        float (*Xs0)[PD] = reinterpret_cast<float (*)[PD]>(&regB[0][0]);   // rows 0 .. GR-1
+        float (*Xs1)[PD] = Xs0 + GR;                                      // rows GR .. 2GR-1
         // tiles (ti, tj), ti <= tj, per wave; -1 = none
         const int tiles[4][3][2] = {{{0, 0}, {0, 1}, {0, 2}}, {{0, 3}, {1, 1}, {1, 2}},
                                     {{1, 3}, {2, 2}, {-1, -1}}, {{2, 3}, {3, 3}, {-1, -1}}};
@@ -189,22 +193,32 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
         for (int x = 0; x < 3; ++x) acc[x] = f64x4{0.0, 0.0, 0.0, 0.0};
         const int l16 = lane & 15;
         const int lk = lane >> 4;
-        constexpr int PER = JW * GR / JT;    // values per thread per chunk (8)
-        float pre[PER];
+        // loader: thread t moves rows 4 q .. 4 q + 3 (q = t % 16) of columns
+        // t / 16 + 16 e, e < 4, as 16-byte vectors (lanes of a column read
+        // 256 contiguous bytes; the LDS writes hit 64 distinct banks)
+        const bool vec4 = (k & 3) == 0;
+        f32x4 pre[4];
         auto fetch = [&](int r0) {
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                const int idx = tid + JT * e;
-                const int w = idx / GR, t = idx % GR;
+            for (int e = 0; e < 4; ++e) {
+                const int w = (tid >> 4) + 16 * e, q = tid & 15;
                 const int c = col[w];
-                pre[e] = (c >= 0 && r0 + t < k) ? Xt[static_cast<int64_t>(c) * k + r0 + t] : 0.0f;
+                const int rr = r0 + 4 * q;
+                const int64_t base = static_cast<int64_t>(c) * k + rr;
+                if (c >= 0 && vec4 && rr + 4 <= k) {
+                    pre[e] = *reinterpret_cast<const f32x4*>(Xt + base);
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) pre[e][v] = (c >= 0 && rr + v < k) ? Xt[base + v] : 0.0f;
+                }
             }
         };
-        auto stash = [&](double (*Xs)[PD]) {
+        auto stash = [&](float (*Xs)[PD]) {
 #pragma unroll
-            for (int e = 0; e < PER; ++e) {
-                const int idx = tid + JT * e;
-                Xs[idx % GR][idx / GR] = static_cast<double>(pre[e]);
+            for (int e = 0; e < 4; ++e) {
+                const int w = (tid >> 4) + 16 * e, q = tid & 15;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) Xs[4 * q + v][w] = pre[e][v];
             }
         };
         const int nchunk = (k + GR - 1) / GR;
@@ -212,33 +226,37 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
         stash(Xs0);
         __syncthreads();
         for (int ch = 0; ch < nchunk; ++ch) {
-            double (*cur)[PD] = (ch & 1) ? Xs1 : Xs0;
-            double (*nxt)[PD] = (ch & 1) ? Xs0 : Xs1;
+            float (*cur)[PD] = (ch & 1) ? Xs1 : Xs0;
+            float (*nxt)[PD] = (ch & 1) ? Xs0 : Xs1;
             if (ch + 1 < nchunk) fetch((ch + 1) * GR);
 #pragma unroll
             for (int x = 0; x < 3; ++x) {
                 const int ti = tiles[wave][x][0], tj = tiles[wave][x][1];
                 if (ti >= 0) {
 #pragma unroll
-                    for (int kk = 0; kk < GR; kk += 4) {
-                        const double a = cur[kk + lk][16 * ti + l16];
-                        const double bv = cur[kk + lk][16 * tj + l16];
-                        acc[x] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, bv, acc[x], 0, 0, 0);
+                    for (int kk = 0; kk < GR; kk += 8) {
+                        f32x4 part = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            cur[kk + lk][16 * ti + l16], cur[kk + lk][16 * tj + l16], f32x4{0.0f, 0.0f, 0.0f, 0.0f},
+                            0, 0, 0);
+                        part = __builtin_amdgcn_mfma_f32_16x16x4f32(cur[kk + 4 + lk][16 * ti + l16],
+                                                                    cur[kk + 4 + lk][16 * tj + l16], part, 0, 0, 0);
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) acc[x][v] += static_cast<double>(part[v]);
                     }
                 }
             }
             if (ch + 1 < nchunk) stash(nxt);
             __syncthreads();
         }
-        // fp64 16x16 block layout: lane holds column (lane & 15); accumulator
-        // register v holds row 4 v + (lane >> 4).
+        // fp32 16x16 block layout: lane holds column (lane & 15); accumulator
+        // register v holds row 4 (lane >> 4) + v.
 #pragma unroll
         for (int x = 0; x < 3; ++x) {
             const int ti = tiles[wave][x][0], tj = tiles[wave][x][1];
             if (ti >= 0) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int i = 16 * ti + 4 * v + lk;
+                    const int i = 16 * ti + 4 * lk + v;
                     const int j = 16 * tj + l16;
                     G[i][j] = acc[x][v];
                     G[j][i] = acc[x][v];
