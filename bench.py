@@ -34,6 +34,7 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E, GB/s
 FP32_MFMA_PEAK_TFS = 157.3    # MI355X dense fp32 matrix, TFLOP/s
 FP64_MFMA_PEAK_TFS = 78.6     # MI355X dense fp64 matrix, TFLOP/s
 BF16_MFMA_PEAK_TFS = 2500.0   # MI355X dense bf16 matrix, TFLOP/s
+INT8_MFMA_PEAK_TOPS = 5000.0  # MI355X dense int8 matrix, TOP/s
 ADAM_BYTES_PER_ELEM = 24      # read R, M, V; write M, V, N (fp32)
 
 # kernel classes of the roofline: launch classes (traced stages or outer calls)
@@ -41,7 +42,7 @@ ADAM_BYTES_PER_ELEM = 24      # read R, M, V; write M, V, N (fp32)
 # counter reading is used only while that source is unchanged)
 KERNEL_CLASSES = {
     "products": (("product_A", "product_At"), "gemm_bf16x3_kernel", "bf16x3.hip"),
-    "gram": (("gram",), "gram64_kernel", "gemm.hip"),
+    "gram": (("gram",), "gram_i8_kernel", "gram_i8.hip"),
     "triangular": (("triangular",), None, "gemm.hip"),
     "projector": (("projector",), None, "gemm.hip"),
     "project": (("project",), None, "gemm.hip"),
@@ -340,8 +341,9 @@ def main():
         "project": (prod_bound, 2.0 * r * s * l * C),
         "project_back": ("mfma_bf16x6", 2.0 * r * s * l * C),
         "adam": ("hbm", float(ADAM_BYTES_PER_ELEM * C * r * l)),
-        # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches
-        "gram": ("mfma64", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * C / (n_gram_s + n_gram_l)),
+        # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches;
+        # exact on the int8 matrix cores as nine digit-plane products (gram_i8.hip)
+        "gram": ("mfma_i8x9", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * C / (n_gram_s + n_gram_l)),
         # Q = Y R^-1 with triangular R^-1: rows * k * (k + 1) flops, averaged
         "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * C
                                 / max(1, n_gram_s + n_gram_l - 1))),
@@ -378,13 +380,16 @@ def main():
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
     else:
         peak = {"mfma": FP32_MFMA_PEAK_TFS, "mfma64": FP64_MFMA_PEAK_TFS, "mfma_bf16x3": BF16_MFMA_PEAK_TFS,
-                "mfma_bf16x6": BF16_MFMA_PEAK_TFS}[bound]
+                "mfma_bf16x6": BF16_MFMA_PEAK_TFS, "mfma_i8x9": INT8_MFMA_PEAK_TOPS}[bound]
         ach = units / (avg_ms * 1e-3) / 1e12
         roof = {"kernel": kern, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(ach / peak, 4), "traffic": traffic}
         if bound == "mfma_bf16x3":
             roof["mfma_dtype"] = "bf16 (3 exact bf16 products per fp32-accurate product)"
             roof["frac_of_3x_ceiling"] = round(3.0 * ach / peak, 4)
+        if bound == "mfma_i8x9":
+            roof["mfma_dtype"] = "int8 (9 exact digit-plane products per fp32-input Gram entry)"
+            roof["frac_of_9x_ceiling"] = round(9.0 * ach / peak, 4)
         if bound == "mfma_bf16x6":
             roof["mfma_dtype"] = "bf16 (6 bf16 plane products per fp32-accurate product)"
             roof["frac_of_6x_ceiling"] = round(6.0 * ach / peak, 4)

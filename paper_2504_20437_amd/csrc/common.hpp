@@ -63,18 +63,27 @@ struct GemmArgs {
     int b_upper;         // op(B) upper triangular: column tile j0 only needs k < j0 + tile width
 };
 
-struct Gram64Args {
+// Exact Gram of the fixed-point image of X on the int8 matrix cores (gram_i8.hip):
+// upper triangle of C (cols x cols, row-major, ld = ldc) only.
+struct GramI8Args {
     const float* X;      // rows x cols, row-major
     int64_t ldx, strideX;
-    double* C;           // cols x cols, row-major, ld = cols
-    int64_t strideC;
     int rows, cols;
+    unsigned* cmax;      // per matrix: strideCM >= cols column maxima (scratch)
+    int64_t strideCM;
+    int8_t* D;           // per matrix: strideD >= gram_i8_digit_bytes(rows, cols) bytes (scratch)
+    int64_t strideD;
+    double* C;
+    int64_t ldc, strideC;
 };
+int64_t gram_i8_ld(int rows);          // bytes per digit row (rows padded to 128)
+int gram_i8_cols_pad(int cols);        // digit rows per plane (cols padded to 64)
+inline int64_t gram_i8_digit_bytes(int rows, int cols) { return 3 * gram_i8_cols_pad(cols) * gram_i8_ld(rows); }
 
 // Launchers (defined in the .hip files). All return hipError_t of the launch.
+hipError_t launch_gram_i8(const GramI8Args& g, int batch, hipStream_t stream);
 hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const GemmArgs& g, int batch,
                        hipStream_t stream);
-hipError_t launch_gram64(const Gram64Args& g, int batch, hipStream_t stream);
 
 hipError_t launch_sketch(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
                          uint64_t sketch_index0, int batch, hipStream_t stream);

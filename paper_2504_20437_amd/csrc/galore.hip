@@ -57,6 +57,9 @@ struct Layout {
     bool bf16;
     int64_t ldgt, strideGt, ldpl, planeStride, stridePl;
     size_t offGt, offPl;
+    // digit planes and column maxima of the exact int8 Gram
+    int64_t strideQ, strideCM;
+    size_t offQ, offCM;
     size_t total;
 };
 
@@ -99,6 +102,10 @@ Layout make_layout(const Shape& sh, int r, int batch, bool bf16) {
     L.stridePl = 3 * L.planeStride;
     L.offGt = bf16 ? take(B * L.strideGt * sizeof(uint16_t)) : 0;
     L.offPl = bf16 ? take(B * L.stridePl * sizeof(uint16_t)) : 0;
+    L.strideQ = static_cast<int64_t>(align_up(gram_i8_digit_bytes(static_cast<int>(sh.l), sh.k), kAlign));
+    L.strideCM = pad_elems(k);
+    L.offQ = take(B * L.strideQ);
+    L.offCM = take(B * L.strideCM * sizeof(unsigned));
     L.total = off;
     return L;
 }
@@ -281,20 +288,32 @@ int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, f
     return GALORE_OK;
 }
 
-// One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In (fp64 Gram and factor);
+// C (the k x k Gram region) = X^T X for a rows x k panel X of the workspace
+GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, int k) {
+    const Layout& L = *w.L;
+    GramI8Args g{};
+    g.X = X;
+    g.ldx = k;
+    g.strideX = strideX;
+    g.rows = rows;
+    g.cols = k;
+    g.cmax = reinterpret_cast<unsigned*>(w.base + L.offCM);
+    g.strideCM = L.strideCM;
+    g.D = reinterpret_cast<int8_t*>(w.base + L.offQ);
+    g.strideD = L.strideQ;
+    g.C = w.d(L.offC);
+    g.ldc = k;
+    g.strideC = L.strideKK;
+    return g;
+}
+
+// One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In (exact Gram of the
+// fixed-point image of In, fp64 factor);
 // columns found dependent are replaced by generic unit vectors.
 int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
               hipStream_t st, Tracer& tr) {
     const Layout& L = *w.L;
-    Gram64Args gg{};
-    gg.X = In;
-    gg.ldx = k;
-    gg.strideX = stride;
-    gg.C = w.d(L.offC);
-    gg.strideC = L.strideKK;
-    gg.rows = rows;
-    gg.cols = k;
-    GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram64(gg, batch, st));
+    GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k), batch, st));
     GALORE_TRACED(tr, GALORE_STAGE_CHOLESKY,
                   launch_cholesky(w.d(L.offC), k, L.strideKK, w.f(L.offRinv), w.d(L.offXinv), L.strideKK,
                                   w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, st));
@@ -384,15 +403,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
     GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL));
     {
-        Gram64Args gg{};
-        gg.X = L1;
-        gg.ldx = k;
-        gg.strideX = L.strideL;
-        gg.C = w.d(L.offC);
-        gg.strideC = L.strideKK;
-        gg.rows = l;
-        gg.cols = k;
-        GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram64(gg, batch, stream));
+        GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, L1, L.strideL, l, k), batch, stream));
         GALORE_TRACED(tr, GALORE_STAGE_CHOLESKY,
                       launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, w.d(L.offXinv), L.strideKK,
                                       w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, stream));

@@ -10,9 +10,6 @@
 //    and B tiles in M-/N-contiguous order so that the per-lane MFMA operand
 //    reads are consecutive addresses; double-buffered with one barrier per
 //    K step, the next tile's global loads in flight during the MFMAs.
-//  * gram64: C = X^T X in fp64 with v_mfma_f64_16x16x4_f64 (the Gram matrices
-//    of the Cholesky-based orthonormalisation), only the upper tiles computed
-//    and mirrored.
 #include <type_traits>
 
 #include "common.hpp"
@@ -253,140 +250,6 @@ hipError_t dispatch_types(bool a_bf16, bool b_bf16, const GemmArgs& g, int batch
     return launch_one<LA, LB, float, float>(g, batch, s);
 }
 
-// --------------------------------------------------------------------------
-// fp64 Gram C = X^T X (cols x cols), X rows x cols fp32.
-// 96 x 96 output tiles (1056 = 11 x 96 columns: no padding at the Llama
-// widths), upper triangle only (mirrored on store), enumerated XCD-aware;
-// 32-row chunks of the two column panels staged in LDS as fp32 (converted to
-// fp64 when read) with the next chunk prefetched in registers; four waves each
-// own a 48 x 48 quadrant = 3 x 3 v_mfma_f64_16x16x4f64 tiles. On diagonal
-// tiles both operands are the same panel, loaded once, and the wave of the
-// lower-left quadrant has nothing to compute (its block is the mirror of the
-// upper-right one).
-// --------------------------------------------------------------------------
-constexpr int GB = 96;   // tile
-constexpr int GK = 32;   // rows per chunk
-constexpr int GP = GB + 16;   // padded LDS row (floats): 16 lanes x 4 rows of a read hit distinct banks
-constexpr int GQ = GK * GB / 4 / 256;   // float4 per thread per panel and chunk (3)
-static_assert(GK * GB % (4 * 256) == 0, "panel chunk must split evenly over the threads");
-
-__global__ __launch_bounds__(256, 2) void gram64_kernel(Gram64Args g) {
-    // grid = (upper tiles, batch); XCD-aware order, tile rows u-major
-    const int nt = (g.cols + GB - 1) / GB;
-    const int ntri = nt * (nt + 1) / 2;
-    const int logical = xcd_logical_id(blockIdx.x + ntri * blockIdx.y, ntri * gridDim.y);
-    const int bz = logical / ntri;
-    int idx = logical - bz * ntri, u = 0;
-    while (idx >= nt - u) {
-        idx -= nt - u;
-        ++u;
-    }
-    const int tm = u * GB;
-    const int tn = (u + idx) * GB;
-    const bool diag = (tm == tn);
-
-    __shared__ float As[2][GK][GP];
-    __shared__ float Bs[2][GK][GP];
-    const float* X = g.X + static_cast<int64_t>(bz) * g.strideX;
-    double* C = g.C + static_cast<int64_t>(bz) * g.strideC;
-    const int rows = g.rows, cols = g.cols;
-    const int t = threadIdx.x;
-    const int lane = t & 63;
-    const int wave = t >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const bool idle = diag && wm > wn;         // mirror quadrant of a diagonal tile
-    const bool vec_ok = (g.ldx % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
-    const bool a_cols_in = tm + GB <= cols;
-    const bool b_cols_in = tn + GB <= cols;
-
-    // loader: float4 q = t + 256 e of a 32 x 96 chunk: row q / 24, columns 4 (q % 24) ..
-    f32x4 pa[GQ], pb[GQ];
-    auto fetch_panel = [&](int r0, int c0, bool cols_in, f32x4* out) {
-#pragma unroll
-        for (int e = 0; e < GQ; ++e) {
-            const int q = t + 256 * e;
-            const int rr = r0 + q / (GB / 4), cc = c0 + 4 * (q % (GB / 4));
-            const float* src = X + static_cast<int64_t>(rr) * g.ldx + cc;
-            if (rr < rows && cols_in && vec_ok) {
-                out[e] = *reinterpret_cast<const f32x4*>(src);
-            } else {
-#pragma unroll
-                for (int v = 0; v < 4; ++v) out[e][v] = (rr < rows && cc + v < cols) ? src[v] : 0.0f;
-            }
-        }
-    };
-    auto fetch = [&](int r0) {
-        fetch_panel(r0, tm, a_cols_in, pa);
-        if (!diag) fetch_panel(r0, tn, b_cols_in, pb);
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int e = 0; e < GQ; ++e) {
-            const int q = t + 256 * e;
-            const int rr = q / (GB / 4), cc = 4 * (q % (GB / 4));
-            *reinterpret_cast<f32x4*>(&As[buf][rr][cc]) = pa[e];
-            if (!diag) *reinterpret_cast<f32x4*>(&Bs[buf][rr][cc]) = pb[e];
-        }
-    };
-
-    f64x4 acc[3][3];
-#pragma unroll
-    for (int a = 0; a < 3; ++a)
-#pragma unroll
-        for (int b = 0; b < 3; ++b) acc[a][b] = f64x4{0.0, 0.0, 0.0, 0.0};
-
-    const int KT = (rows + GK - 1) / GK;
-    fetch(0);
-    stash(0);
-    __syncthreads();
-    const int l16 = lane & 15;
-    const int lk = lane >> 4;
-    for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < KT;
-        if (more) fetch((kt + 1) * GK);
-        const float (*Ab)[GP] = As[cur];
-        const float (*Bb)[GP] = diag ? As[cur] : Bs[cur];
-        if (!idle) {
-#pragma unroll
-            for (int kk = 0; kk < GK; kk += 4) {
-                double a[3], b[3];
-#pragma unroll
-                for (int i = 0; i < 3; ++i) a[i] = static_cast<double>(Ab[kk + lk][wm * 48 + 16 * i + l16]);
-#pragma unroll
-                for (int j = 0; j < 3; ++j) b[j] = static_cast<double>(Bb[kk + lk][wn * 48 + 16 * j + l16]);
-#pragma unroll
-                for (int i = 0; i < 3; ++i)
-#pragma unroll
-                    for (int j = 0; j < 3; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[i], b[j], acc[i][j], 0, 0, 0);
-            }
-        }
-        if (more) stash(cur ^ 1);
-        __syncthreads();
-    }
-    if (idle) return;
-    // fp64 16x16 block layout: lane holds column (lane & 15); accumulator
-    // register v holds row 4 v + (lane >> 4). Off-diagonal quadrants of a
-    // diagonal tile, and every block of an off-diagonal tile, are mirrored.
-    const bool mirror = !diag || wm != wn;
-#pragma unroll
-    for (int i = 0; i < 3; ++i) {
-#pragma unroll
-        for (int j = 0; j < 3; ++j) {
-            const int cj = tn + wn * 48 + 16 * j + l16;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int ri = tm + wm * 48 + 16 * i + 4 * v + lk;
-                if (ri < cols && cj < cols) {
-                    C[static_cast<int64_t>(ri) * cols + cj] = acc[i][j][v];
-                    if (mirror) C[static_cast<int64_t>(cj) * cols + ri] = acc[i][j][v];
-                }
-            }
-        }
-    }
-}
-
 }  // namespace
 
 hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const GemmArgs& g, int batch,
@@ -399,14 +262,6 @@ hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const G
     if (la == ALayout::kKContig && lb == BLayout::kKContig)
         return dispatch_types<ALayout::kKContig, BLayout::kKContig>(a_bf16, b_bf16, g, batch, stream);
     return dispatch_types<ALayout::kMContig, BLayout::kKContig>(a_bf16, b_bf16, g, batch, stream);
-}
-
-hipError_t launch_gram64(const Gram64Args& g, int batch, hipStream_t stream) {
-    if (g.cols <= 0 || batch <= 0) return hipSuccess;
-    const int nt = (g.cols + GB - 1) / GB;
-    dim3 grid(nt * (nt + 1) / 2, batch);
-    hipLaunchKernelGGL(gram64_kernel, grid, dim3(256), 0, stream, g);
-    return hipGetLastError();
 }
 
 }  // namespace galore
