@@ -117,9 +117,9 @@ GALORE_API int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int
  */
 typedef enum {
     GALORE_STAGE_SKETCH = 0,      /* Omega from the counter-based generator (1 launch)         */
-    GALORE_STAGE_PRODUCT_A = 1,   /* Y = A X, fp32 matrix cores (1 launch)                      */
-    GALORE_STAGE_PRODUCT_AT = 2,  /* Z = A^T Q, fp32 matrix cores (1 launch)                    */
-    GALORE_STAGE_GRAM = 3,        /* fp64 Gram X^T X of a tall-skinny block (1 launch)          */
+    GALORE_STAGE_PRODUCT_A = 1,   /* Y = A X, matrix cores (bf16 planes for a bf16 G; 1 launch) */
+    GALORE_STAGE_PRODUCT_AT = 2,  /* Z = A^T Q, as PRODUCT_A (1 launch)                         */
+    GALORE_STAGE_GRAM = 3,        /* exact Gram X^T X of a tall-skinny block (4 launches)       */
     GALORE_STAGE_CHOLESKY = 4,    /* blocked Cholesky of the Gram (+ inverse of the factor)     */
     GALORE_STAGE_TRIANGULAR = 5,  /* Q = Y R^-1, fp32 matrix cores (1 launch)                   */
     GALORE_STAGE_JACOBI = 6,      /* small SVD: all Jacobi sweeps and the sort                  */

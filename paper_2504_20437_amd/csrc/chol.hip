@@ -1,4 +1,4 @@
-// Cholesky factorisation of the k x k fp64 Gram matrices and the inverse of the
+// Cholesky factorisation of the k x k Gram matrices (fp64) and the inverse of the
 // factor, for the Cholesky-based orthonormalisation (Q = Y R^-1 with
 // R^T R = Y^T Y) that keeps the sketch well conditioned between the products
 // of the randomized subspace iteration (Halko et al. 2011, §4.5 re-orthonormal-
