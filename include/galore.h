@@ -9,7 +9,8 @@
  *  - All matrix pointers are DEVICE pointers, row-major, owned by the caller.
  *    The library never allocates or frees device memory and never
  *    synchronises the device: work is enqueued on `stream` and every entry
- *    point returns as soon as it is enqueued.
+ *    point returns as soon as it is enqueued (galore_rsvd_update also uses one
+ *    stream of its own, joined back into `stream`; see there).
  *  - G is the m x n gradient as produced by autograd (+grad). s = min(m, n) is
  *    the projected side, l = max(m, n). A denotes G when m <= n and G^T when
  *    m > n, so A is always s x l (paper §3: left singular vectors when m <= n,
@@ -102,6 +103,12 @@ GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, in
  *          small SVD did not converge within its sweep limit (value = sweeps).
  * Workspace: device buffer of at least galore_rsvd_workspace_size(...) bytes,
  *          256-byte aligned; contents are scratch and may be reused afterwards.
+ * Streams: with batch >= 2 the small SVD's sweeps for the second half of the
+ *          batch run on a library-owned stream of the current device (created
+ *          on first use with default priority, kept for the process), forked
+ *          from `stream` and joined back into it with events; everything else,
+ *          and all completion, is ordered on `stream`. Calls from several host
+ *          threads are safe; they serialise only while enqueuing the sweeps.
  * Errors:  NULL G/P/workspace -> INVALID_ARG; m,n,r < 1, r > s, p < 0, q < 0,
  *          r + p > 4096 (largest supported sketch width), ldg < n, ldp < r,
  *          batch < 1 -> SHAPE; workspace_bytes too small -> WORKSPACE.

@@ -304,6 +304,16 @@ __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) 
 constexpr int YM = 256;
 constexpr int YN = 128;
 constexpr int YT = 256;
+// tile order (measured on 64 x 4096x11008: XCD-contiguous ids 55 ms per
+// product launch set vs 68 without; groups of 8 or 16 tile rows equal, 1-4 slower)
+#ifndef GALORE_BX3_GROUP
+#define GALORE_BX3_GROUP 8
+#endif
+#ifndef GALORE_BX3_XCD
+#define GALORE_BX3_XCD 1
+#endif
+constexpr int kDirectGroup = GALORE_BX3_GROUP;   // tile rows per group of the tile order
+constexpr bool kDirectXcd = GALORE_BX3_XCD != 0;  // XCD-contiguous logical tile ids
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
@@ -348,10 +358,10 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
     const int num_n = gridDim.x, num_m = gridDim.y;
     const int tiles = num_n * num_m;
     const int lin = blockIdx.x + num_n * (blockIdx.y + num_m * blockIdx.z);
-    const int logical = xcd_logical_id(lin, tiles * gridDim.z);
+    const int logical = kDirectXcd ? xcd_logical_id(lin, tiles * gridDim.z) : lin;
     const int bz = logical / tiles;
     int tm, tn;
-    grouped_tile(logical - bz * tiles, num_m, num_n, 8, tm, tn);
+    grouped_tile(logical - bz * tiles, num_m, num_n, kDirectGroup, tm, tn);
     const uint16_t* A = g.A + static_cast<int64_t>(bz) * g.strideA;
     const uint16_t* B = g.B + static_cast<int64_t>(bz) * g.strideB;
     float* C = g.C + static_cast<int64_t>(bz) * g.strideC;

@@ -4,6 +4,9 @@
 #include <math.h>
 #include <string.h>
 
+#include <map>
+#include <mutex>
+
 #include "../../include/galore.h"
 
 #include "common.hpp"
@@ -329,6 +332,55 @@ int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int ro
         if (st_ != GALORE_OK) return st_; \
     } while (0)
 
+// The Jacobi sweeps of the second half of the batch run on a library-owned
+// stream (one per device, default priority, non-blocking), forked from and
+// joined back into the caller's stream with events: the two halves' launches
+// then run side by side and their phases (matrix-core Gram, VALU-bound rotation
+// sweep, memory-bound apply) overlap instead of running in lockstep
+// (measured on 64 x 4096x11008: 103 -> 95 ms; four streams 91 ms, eight far
+// slower once the process's hardware queues are oversubscribed). The enqueue
+// sequence holds a lock, so concurrent callers on one device cannot interleave
+// their fork and join events.
+struct AuxStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_aux_mutex;
+std::map<int, AuxStream> g_aux;   // by device
+
+int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, int batch, hipStream_t stream) {
+    if (batch < 2) {
+        for (int sw = 0; sw < kMaxSweeps; ++sw)
+            for (int stp = 0; stp < nb - 1; ++stp)
+                GALORE_TRY(launch_jacobi_step(Yt, k, strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol, batch,
+                                              stream));
+        return GALORE_OK;
+    }
+    std::lock_guard<std::mutex> lock(g_aux_mutex);
+    int dev = 0;
+    GALORE_TRY(hipGetDevice(&dev));
+    AuxStream& aux = g_aux[dev];
+    if (aux.stream == nullptr) {
+        GALORE_TRY(hipStreamCreateWithFlags(&aux.stream, hipStreamNonBlocking));
+        GALORE_TRY(hipEventCreateWithFlags(&aux.fork, hipEventDisableTiming));
+        GALORE_TRY(hipEventCreateWithFlags(&aux.join, hipEventDisableTiming));
+    }
+    const int h1 = batch / 2, h2 = batch - h1;
+    float* Yt2 = Yt + h1 * strideKK;
+    int* rot2 = rot + h1 * kMaxSweeps;
+    GALORE_TRY(hipEventRecord(aux.fork, stream));
+    GALORE_TRY(hipStreamWaitEvent(aux.stream, aux.fork, 0));
+    for (int sw = 0; sw < kMaxSweeps; ++sw)
+        for (int stp = 0; stp < nb - 1; ++stp) {
+            GALORE_TRY(launch_jacobi_step(Yt, k, strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol, h1, stream));
+            GALORE_TRY(launch_jacobi_step(Yt2, k, strideKK, nb, stp, sw, rot2, kMaxSweeps, kJacobiTol, h2,
+                                          aux.stream));
+        }
+    GALORE_TRY(hipEventRecord(aux.join, aux.stream));
+    GALORE_TRY(hipStreamWaitEvent(stream, aux.join, 0));
+    return GALORE_OK;
+}
+
 int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r,
               int32_t p, int32_t q, uint64_t seed, uint64_t sketch_index0, float* P, int64_t ldp,
               int64_t stride_p, float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
@@ -418,10 +470,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                                      stream));
     const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
     const int nb = nblk_real + (nblk_real & 1);
-    for (int sw = 0; sw < kMaxSweeps; ++sw)
-        for (int stp = 0; stp < nb - 1; ++stp)
-            GALORE_TRY(launch_jacobi_step(Yt, k, L.strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol, batch,
-                                          stream));
+    GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, batch, stream));
     GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
                                       kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
                                       L.strideTheta / 2, batch, stream));

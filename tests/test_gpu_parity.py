@@ -249,6 +249,52 @@ def test_rsvd_batched_matches_single(gl, orc):
         assert max_rel_violation(sig[i], sr, 1e-4, 1e-30) <= 1.0
 
 
+def test_rsvd_batch_split_is_bitwise(gl):
+    """A batch's small-SVD sweeps run in two halves on two streams; every
+    matrix's arithmetic is its own, so a batch of 3 equals three single calls
+    bit for bit."""
+    import torch
+    m, n, r, p, q, b = 256, 520, 24, 8, 2, 3
+    Gs = [gi.store(gi.planted_gradient(m, n, gi.spectrum_power(m, 0.8), 1e-4, seed=40 + i), "bf16")
+          for i in range(b)]
+    Gd = torch.stack([dev_stored(x) for x in Gs])
+    P, sig, info = gl.galore_rsvd_update(Gd, r, p, q, seed=9, sketch_index0=4)
+    P, sig = host(P), host(sig)
+    assert (info.cpu().numpy() == 0).all()
+    for i in range(b):
+        P1, s1, _ = gl.galore_rsvd_update(Gd[i:i + 1].contiguous(), r, p, q, seed=9, sketch_index0=4 + i)
+        assert np.array_equal(P[i], host(P1)[0]) and np.array_equal(sig[i], host(s1)[0])
+
+
+def test_rsvd_concurrent_callers(gl):
+    """Two host threads enqueue subspace updates on their own streams at the
+    same time; each result equals the same call made alone."""
+    import threading
+    import torch
+    m, n, r, p, q, b = 200, 600, 16, 8, 1, 4
+    Gd = [torch.stack([dev(gi.store(gi.planted_gradient(m, n, gi.spectrum_power(m, 1.0), 1e-4, seed=60 + 10 * t + i),
+                                    "f32").data) for i in range(b)]) for t in range(2)]
+    ref = [gl.galore_rsvd_update(Gd[t], r, p, q, seed=3 + t) for t in range(2)]
+    ref = [(host(x[0]), host(x[1])) for x in ref]
+    out = [None, None]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+
+    def run(t):
+        with torch.cuda.stream(streams[t]):
+            for _ in range(3):
+                P, s, _ = gl.galore_rsvd_update(Gd[t], r, p, q, seed=3 + t, stream=streams[t])
+            streams[t].synchronize()
+            out[t] = (P.cpu().numpy().astype(np.float64), s.cpu().numpy().astype(np.float64))
+
+    th = [threading.Thread(target=run, args=(t,)) for t in range(2)]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    for t in range(2):
+        assert np.array_equal(out[t][0], ref[t][0]) and np.array_equal(out[t][1], ref[t][1])
+
+
 def test_rsvd_exact_recovery(gl, orc):
     """rank(G) = 32 <= r (noiseless): sigma equals the planted values and P spans
     the planted range; the deficient directions of the sketch get filled."""
