@@ -291,6 +291,67 @@ int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, f
     return GALORE_OK;
 }
 
+// Latency-bound stages (the small SVD's sweeps, the blocked Cholesky) run the
+// second half of the batch on a library-owned stream (one per device, default
+// priority, non-blocking), forked from and joined back into the caller's
+// stream with events: the two halves' launch sequences then run side by side,
+// so that one half's small or phase-bound launches overlap the other's
+// (measured on 64 x 4096x11008: Jacobi 103 -> 95 ms; four streams 91 ms, eight
+// far slower once the process's hardware queues are oversubscribed). The
+// enqueue sequence holds a lock, so concurrent callers on one device cannot
+// interleave their fork and join events.
+struct AuxStream {
+    hipStream_t stream = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_aux_mutex;
+std::map<int, AuxStream> g_aux;   // by device
+
+// f(first, count, stream) enqueues the work of matrices [first, first + count)
+template <typename F>
+int on_two_streams(int batch, hipStream_t stream, F&& f) {
+    if (batch < 2) return f(0, batch, stream);
+    std::lock_guard<std::mutex> lock(g_aux_mutex);
+    int dev = 0;
+    GALORE_TRY(hipGetDevice(&dev));
+    AuxStream& aux = g_aux[dev];
+    if (aux.stream == nullptr) {
+        GALORE_TRY(hipStreamCreateWithFlags(&aux.stream, hipStreamNonBlocking));
+        GALORE_TRY(hipEventCreateWithFlags(&aux.fork, hipEventDisableTiming));
+        GALORE_TRY(hipEventCreateWithFlags(&aux.join, hipEventDisableTiming));
+    }
+    const int h1 = batch / 2;
+    GALORE_TRY(hipEventRecord(aux.fork, stream));
+    GALORE_TRY(hipStreamWaitEvent(aux.stream, aux.fork, 0));
+    int e = f(0, h1, stream);
+    if (e == GALORE_OK) e = f(h1, batch - h1, aux.stream);
+    GALORE_TRY(hipEventRecord(aux.join, aux.stream));
+    GALORE_TRY(hipStreamWaitEvent(stream, aux.join, 0));
+    return e;
+}
+
+int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, int batch, hipStream_t stream) {
+    return on_two_streams(batch, stream, [&](int b0, int cnt, hipStream_t st) -> int {
+        for (int sw = 0; sw < kMaxSweeps; ++sw)
+            for (int stp = 0; stp < nb - 1; ++stp)
+                GALORE_TRY(launch_jacobi_step(Yt + b0 * strideKK, k, strideKK, nb, stp, sw, rot + b0 * kMaxSweeps,
+                                              kMaxSweeps, kJacobiTol, cnt, st));
+        return GALORE_OK;
+    });
+}
+
+// Cholesky of the k x k Gram region (and, with rinv, the inverse of the factor)
+int enqueue_cholesky(const Work& w, int k, bool with_inverse, int batch, hipStream_t stream) {
+    const Layout& L = *w.L;
+    return on_two_streams(batch, stream, [&](int b0, int cnt, hipStream_t st) -> int {
+        const int64_t o = b0 * L.strideKK;
+        GALORE_TRY(launch_cholesky(w.d(L.offC) + o, k, L.strideKK, with_inverse ? w.f(L.offRinv) + o : nullptr,
+                                   w.d(L.offXinv) + o, L.strideKK, w.i(L.offDef) + static_cast<int64_t>(b0) * k,
+                                   w.d(L.offDiag0) + static_cast<int64_t>(b0) * k, kDeficTol, cnt, st));
+        return GALORE_OK;
+    });
+}
+
 // C (the k x k Gram region) = X^T X for a rows x k panel X of the workspace
 GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, int k) {
     const Layout& L = *w.L;
@@ -317,9 +378,12 @@ int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int ro
               hipStream_t st, Tracer& tr) {
     const Layout& L = *w.L;
     GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k), batch, st));
-    GALORE_TRACED(tr, GALORE_STAGE_CHOLESKY,
-                  launch_cholesky(w.d(L.offC), k, L.strideKK, w.f(L.offRinv), w.d(L.offXinv), L.strideKK,
-                                  w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, st));
+    if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
+    {
+        const int e = enqueue_cholesky(w, k, true, batch, st);
+        if (e != GALORE_OK) return e;
+    }
+    if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
     GALORE_TRACED(tr, GALORE_STAGE_TRIANGULAR,
                   gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st));
     GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st));
@@ -331,55 +395,6 @@ int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int ro
         const int st_ = (expr);          \
         if (st_ != GALORE_OK) return st_; \
     } while (0)
-
-// The Jacobi sweeps of the second half of the batch run on a library-owned
-// stream (one per device, default priority, non-blocking), forked from and
-// joined back into the caller's stream with events: the two halves' launches
-// then run side by side and their phases (matrix-core Gram, VALU-bound rotation
-// sweep, memory-bound apply) overlap instead of running in lockstep
-// (measured on 64 x 4096x11008: 103 -> 95 ms; four streams 91 ms, eight far
-// slower once the process's hardware queues are oversubscribed). The enqueue
-// sequence holds a lock, so concurrent callers on one device cannot interleave
-// their fork and join events.
-struct AuxStream {
-    hipStream_t stream = nullptr;
-    hipEvent_t fork = nullptr, join = nullptr;
-};
-std::mutex g_aux_mutex;
-std::map<int, AuxStream> g_aux;   // by device
-
-int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, int batch, hipStream_t stream) {
-    if (batch < 2) {
-        for (int sw = 0; sw < kMaxSweeps; ++sw)
-            for (int stp = 0; stp < nb - 1; ++stp)
-                GALORE_TRY(launch_jacobi_step(Yt, k, strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol, batch,
-                                              stream));
-        return GALORE_OK;
-    }
-    std::lock_guard<std::mutex> lock(g_aux_mutex);
-    int dev = 0;
-    GALORE_TRY(hipGetDevice(&dev));
-    AuxStream& aux = g_aux[dev];
-    if (aux.stream == nullptr) {
-        GALORE_TRY(hipStreamCreateWithFlags(&aux.stream, hipStreamNonBlocking));
-        GALORE_TRY(hipEventCreateWithFlags(&aux.fork, hipEventDisableTiming));
-        GALORE_TRY(hipEventCreateWithFlags(&aux.join, hipEventDisableTiming));
-    }
-    const int h1 = batch / 2, h2 = batch - h1;
-    float* Yt2 = Yt + h1 * strideKK;
-    int* rot2 = rot + h1 * kMaxSweeps;
-    GALORE_TRY(hipEventRecord(aux.fork, stream));
-    GALORE_TRY(hipStreamWaitEvent(aux.stream, aux.fork, 0));
-    for (int sw = 0; sw < kMaxSweeps; ++sw)
-        for (int stp = 0; stp < nb - 1; ++stp) {
-            GALORE_TRY(launch_jacobi_step(Yt, k, strideKK, nb, stp, sw, rot, kMaxSweeps, kJacobiTol, h1, stream));
-            GALORE_TRY(launch_jacobi_step(Yt2, k, strideKK, nb, stp, sw, rot2, kMaxSweeps, kJacobiTol, h2,
-                                          aux.stream));
-        }
-    GALORE_TRY(hipEventRecord(aux.join, aux.stream));
-    GALORE_TRY(hipStreamWaitEvent(stream, aux.join, 0));
-    return GALORE_OK;
-}
 
 int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r,
               int32_t p, int32_t q, uint64_t seed, uint64_t sketch_index0, float* P, int64_t ldp,
@@ -456,9 +471,9 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL));
     {
         GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, L1, L.strideL, l, k), batch, stream));
-        GALORE_TRACED(tr, GALORE_STAGE_CHOLESKY,
-                      launch_cholesky(w.d(L.offC), k, L.strideKK, nullptr, w.d(L.offXinv), L.strideKK,
-                                      w.i(L.offDef), w.d(L.offDiag0), kDeficTol, batch, stream));
+        if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
+        GALORE_CHECK(enqueue_cholesky(w, k, false, batch, stream));
+        if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
     }
     // a6: one-sided Jacobi on the columns of Y = R^T: Y W = U Sigma, U = left
     // singular vectors of B
