@@ -558,6 +558,10 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
 #endif
 constexpr int kDirectK = GALORE_BX3_K;     // K depth of a stage
 constexpr int kDirectS = GALORE_BX3_S;     // stages in LDS
+#ifndef GALORE_BX3T_S
+#define GALORE_BX3T_S 2
+#endif
+constexpr int kDirectST = GALORE_BX3T_S;   // stages of the M-contiguous-A kernel (32 deep each)
 #ifndef GALORE_BX6_K
 #define GALORE_BX6_K 16
 #endif
@@ -593,7 +597,7 @@ bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* B
                      (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
                      (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
     const bool mc = !a_mcontig || (M >= 8 && M % 8 == 0);
-    return vec && mc && K > 0 && K % kDirectK == 0;
+    return vec && mc && K > 0 && K % (a_mcontig ? 32 : kDirectK) == 0;
 }
 
 hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
@@ -623,7 +627,7 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
     if (bf16x3_direct_ok(A, lda, strideA, Bplanes, ldb, planeStride, strideB, M, K, batch, a_mcontig)) {
         dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
         if (a_mcontig)
-            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, true, 1>), grid, dim3(YT), 0, stream, g);
+            hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<32, kDirectST, true, 1>), grid, dim3(YT), 0, stream, g);
         else
             hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false, 1>), grid, dim3(YT), 0, stream, g);
         return hipGetLastError();

@@ -34,6 +34,8 @@
 // If one of them is among the r leading columns, the finalize kernel replaces
 // it by an orthonormal completion (unit vectors orthogonalised twice against
 // the columns already kept), the singular value staying 0.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace galore {
@@ -116,14 +118,17 @@ __device__ __forceinline__ double dpp_odd_partner(double v, bool odd) {
     return __hiloint2double(odd ? hl : hr, odd ? ll : lr);
 }
 
+// fp32 versions: lanes without a source (0 and 63 in the odd pattern) read 0,
+// which only idle lanes consume; a zero old value and bound_ctrl let the
+// compiler fold the lane move into the multiply that uses it
 __device__ __forceinline__ float dpp_swap_pairs(float v) {
     const int i = __float_as_int(v);
-    return __int_as_float(__builtin_amdgcn_update_dpp(i, i, 0xB1, 0xf, 0xf, false));
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, i, 0xB1, 0xf, 0xf, true));
 }
 __device__ __forceinline__ float dpp_odd_partner(float v, bool odd) {
     const int i = __float_as_int(v);
-    const int l = __builtin_amdgcn_update_dpp(i, i, 0x130, 0xf, 0xf, false);
-    const int r = __builtin_amdgcn_update_dpp(i, i, 0x138, 0xf, 0xf, false);
+    const int l = __builtin_amdgcn_update_dpp(0, i, 0x130, 0xf, 0xf, true);
+    const int r = __builtin_amdgcn_update_dpp(0, i, 0x138, 0xf, 0xf, true);
     return __int_as_float(odd ? l : r);
 }
 
@@ -138,7 +143,7 @@ typedef float jreal;
 // Step of the block Jacobi (one workgroup per pair and matrix): Gram of the
 // pair's 64 columns, convergence test, reduction of the small Gram, rotation
 // of the columns, all in one 64 x 65 fp64 LDS buffer (see below).
-__global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
+__global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, int64_t strideX, int nb,
                                                             int step, int sweep, int* rotb, int max_sweeps,
                                                             double tol, int skip_dummy) {
     const int b = blockIdx.y;
@@ -323,8 +328,11 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
         }
         __syncthreads();
         jreal hgL = 0, hgR = 0, htL = 0, htR = 0;
-        for (int t = 0; t < JW; ++t) {
-            const int par = t & 1;
+        // rounds in (even, odd) pairs: the parity is a compile-time constant of
+        // each half, so the parity branches vanish and the loop-carried
+        // registers need no copies between rounds
+        auto round = [&](auto parc) {
+            constexpr int par = decltype(parc)::value;
             const double* Dc = Dv + par * JW;
             double* Dn = Dv + (par ^ 1) * JW;
             const jreal* Bc = Band + par * (4 * 16 * 16);
@@ -435,6 +443,10 @@ __global__ __launch_bounds__(JT, 3) void jacobi_pair_kernel(float* Xtb, int k, i
                 }
             }
             __syncthreads();
+                };
+        for (int t = 0; t < JW; t += 2) {
+            round(std::integral_constant<int, 0>());
+            round(std::integral_constant<int, 1>());
         }
         // ---- Theta to LDS in fp32 for the matrix cores; the sweep reversed the
         //      slot order, so output column j is slot 63 - j (a pair whose
