@@ -168,6 +168,8 @@ struct Bx3Args {
     int c_trans;                // direct kernel only: store C^T (C[n * ldc + m])
     int64_t planeStrideA;       // direct kernel with three A planes: plane p at A + p * planeStrideA
     int b_upper;                // direct kernel: B upper triangular (B[kk][n] = 0 for kk > n)
+    unsigned* cmax;             // direct kernel, row-major C: per-column max of |C| (bits; atomicMax), or null
+    int64_t strideCM;
 };
 
 __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) {
@@ -531,6 +533,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
         }
         return;
     }
+    unsigned mx[2] = {0u, 0u};   // bits of the largest |C| of this lane's two columns
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
 #pragma unroll
@@ -544,8 +547,21 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
                     float val = alpha * acc[x][y][v];
                     if (beta != 0.0f) val += beta * (*dst);
                     *dst = val;
+                    mx[y] = max(mx[y], __float_as_uint(fabsf(val)));
                 }
             }
+        }
+    }
+    if (g.cmax != nullptr) {
+        // column maxima for the exact Gram of C (non-negative floats order like
+        // their bit patterns; NaN/Inf win): the two lane halves hold the same
+        // columns, one atomic per column and wave
+        unsigned* cm = g.cmax + static_cast<int64_t>(bz) * g.strideCM;
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+            const unsigned m = max(mx[y], static_cast<unsigned>(__shfl_xor(static_cast<int>(mx[y]), 32)));
+            const int c = col0 + wn * 64 + 32 * y + l32;
+            if (lk == 0 && c < N) atomicMax(cm + c, m);
         }
     }
 }
@@ -603,7 +619,7 @@ bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* B
 hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
                               int64_t ldb, int64_t planeStride, int64_t strideB, float* C, int64_t ldc,
                               int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
-                              hipStream_t stream) {
+                              hipStream_t stream, unsigned* cmax, int64_t strideCM) {
     if (M <= 0 || N <= 0 || batch <= 0) return hipSuccess;
     Bx3Args g;
     g.A = static_cast<const uint16_t*>(A);
@@ -624,6 +640,8 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
     g.c_trans = c_trans;
     g.planeStrideA = 0;
     g.b_upper = 0;
+    g.cmax = c_trans ? nullptr : cmax;
+    g.strideCM = strideCM;
     if (bf16x3_direct_ok(A, lda, strideA, Bplanes, ldb, planeStride, strideB, M, K, batch, a_mcontig)) {
         dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
         if (a_mcontig)
@@ -632,8 +650,8 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
             hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false, 1>), grid, dim3(YT), 0, stream, g);
         return hipGetLastError();
     }
-    // the register-staged kernel: K-contiguous A, row-major C only
-    if (a_mcontig || c_trans) return hipErrorInvalidValue;
+    // the register-staged kernel: K-contiguous A, row-major C only, no column maxima
+    if (a_mcontig || c_trans || cmax != nullptr) return hipErrorInvalidValue;
     const int vec = (lda % 8 == 0) && (ldb % 8 == 0) && (planeStride % 8 == 0) &&
                     (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
                     (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
@@ -690,6 +708,8 @@ hipError_t launch_gemm_bf16x6(const void* Aplanes, int64_t lda, int64_t planeStr
     g.c_trans = c_trans;
     g.planeStrideA = planeStrideA;
     g.b_upper = b_upper;
+    g.cmax = nullptr;
+    g.strideCM = 0;
     dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
     hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kX6K, kX6S, false, 3>), grid, dim3(YT), 0, stream, g);
     return hipGetLastError();

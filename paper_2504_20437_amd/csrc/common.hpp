@@ -75,6 +75,7 @@ struct GramI8Args {
     int64_t strideD;
     double* C;
     int64_t ldc, strideC;
+    int cmax_ready;      // cmax already holds the column maxima of X (its producer wrote them)
 };
 int64_t gram_i8_ld(int rows);          // bytes per digit row (rows padded to 128)
 int gram_i8_cols_pad(int cols);        // digit rows per plane (cols padded to 64)
@@ -82,6 +83,8 @@ inline int64_t gram_i8_digit_bytes(int rows, int cols) { return 3 * gram_i8_cols
 
 // Launchers (defined in the .hip files). All return hipError_t of the launch.
 hipError_t launch_gram_i8(const GramI8Args& g, int batch, hipStream_t stream);
+// zero n unsigned (the column-maximum buffer before a producer fills it)
+hipError_t launch_fill_u32(unsigned* p, int64_t n, hipStream_t stream);
 hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const GemmArgs& g, int batch,
                        hipStream_t stream);
 
@@ -129,10 +132,13 @@ hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t stride
 // bf16x3_direct_ok first (hipErrorInvalidValue otherwise).
 bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* Bplanes, int64_t ldb,
                       int64_t planeStride, int64_t strideB, int M, int K, int batch, int a_mcontig);
+// cmax (row-major C on the direct-load kernel only, else hipErrorInvalidValue):
+// per matrix strideCM unsigned, atomicMax'ed with the bits of |C| per column
+// (the caller zeroes it first); null for none.
 hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
                               int64_t ldb, int64_t planeStride, int64_t strideB, float* C, int64_t ldc,
                               int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
-                              hipStream_t stream);
+                              hipStream_t stream, unsigned* cmax = nullptr, int64_t strideCM = 0);
 
 // fp32 x fp32 products on the bf16 matrix cores: both operands given as three
 // bf16 planes with K-contiguous rows (A: M rows, B: N rows), six plane products

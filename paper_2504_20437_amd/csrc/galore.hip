@@ -181,7 +181,16 @@ struct Products {
     bool direct;        // bf16: both products read G in place (direct-load kernel)
     int batch;
     hipStream_t st;
+    unsigned* cmax;     // column maxima of the product for the next Gram (direct-load kernel only)
+    int64_t strideCM;
 };
+
+// Zero the column-maximum buffer for a product that fills it; false when the
+// product cannot (its Gram then takes the maxima itself).
+bool cmax_prepare(const Products& P) {
+    if (!P.direct || P.cmax == nullptr) return false;
+    return launch_fill_u32(P.cmax, P.strideCM * P.batch, P.st) == hipSuccess;
+}
 
 // Out (rows x k) = In (rows x k) * Rinv (k x k)
 hipError_t gemm_right_tri(const float* In, float* Out, int64_t stride, int rows, int k,
@@ -242,9 +251,11 @@ struct Tracer {
     } while (0)
 
 // Y (s x k) = A X, X (l x k)
-int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, float* Y, int64_t strideY) {
+int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, float* Y, int64_t strideY,
+              bool& cmax_ready) {
     const Shape& sh = *P.sh;
     const Layout& L = *P.L;
+    cmax_ready = false;
     if (!L.bf16) {
         GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A, gemm_A_times(sh, P.g, X, strideX, Y, strideY, P.batch, P.st));
         return GALORE_OK;
@@ -259,17 +270,20 @@ int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, fl
     const void* A = inplace ? P.g.G : static_cast<const void*>(P.gt);
     const int64_t lda = inplace ? P.g.ldg : L.ldgt;
     const int64_t strideA = inplace ? P.g.stride : L.strideGt;
+    cmax_ready = cmax_prepare(P);
     GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A,
                   launch_gemm_bf16x3(A, lda, strideA, sh.left ? 0 : (P.direct ? 1 : 0), P.planes, L.ldpl,
                                      L.planeStride, L.stridePl, Y, k, strideY, 0, s, k, l, 1.0f, 0.0f, P.batch,
-                                     P.st));
+                                     P.st, cmax_ready ? P.cmax : nullptr, P.strideCM));
     return GALORE_OK;
 }
 
 // Z (l x k) = A^T Q, Q (s x k)
-int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, float* Z, int64_t strideZ) {
+int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, float* Z, int64_t strideZ,
+               bool& cmax_ready) {
     const Shape& sh = *P.sh;
     const Layout& L = *P.L;
+    cmax_ready = false;
     if (!L.bf16) {
         GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT, gemm_At_times(sh, P.g, Q, strideQ, Z, strideZ, P.batch, P.st));
         return GALORE_OK;
@@ -284,10 +298,11 @@ int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, f
     const void* At = inplace ? P.g.G : static_cast<const void*>(P.gt);
     const int64_t ldat = inplace ? P.g.ldg : L.ldgt;
     const int64_t strideAt = inplace ? P.g.stride : L.strideGt;
+    cmax_ready = cmax_prepare(P);
     GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_AT,
                   launch_gemm_bf16x3(At, ldat, strideAt, sh.left ? (P.direct ? 1 : 0) : 0, P.planes, L.ldpl,
                                      L.planeStride, L.stridePl, Z, k, strideZ, 0, l, k, s, 1.0f, 0.0f, P.batch,
-                                     P.st));
+                                     P.st, cmax_ready ? P.cmax : nullptr, P.strideCM));
     return GALORE_OK;
 }
 
@@ -353,9 +368,10 @@ int enqueue_cholesky(const Work& w, int k, bool with_inverse, int batch, hipStre
 }
 
 // C (the k x k Gram region) = X^T X for a rows x k panel X of the workspace
-GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, int k) {
+GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, int k, bool cmax_ready) {
     const Layout& L = *w.L;
     GramI8Args g{};
+    g.cmax_ready = cmax_ready ? 1 : 0;
     g.X = X;
     g.ldx = k;
     g.strideX = strideX;
@@ -375,9 +391,9 @@ GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, i
 // fixed-point image of In, fp64 factor);
 // columns found dependent are replaced by generic unit vectors.
 int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
-              hipStream_t st, Tracer& tr) {
+              hipStream_t st, Tracer& tr, bool cmax_ready) {
     const Layout& L = *w.L;
-    GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k), batch, st));
+    GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k, cmax_ready), batch, st));
     if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
     {
         const int e = enqueue_cholesky(w, k, true, batch, st);
@@ -424,7 +440,9 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     float* Sb = w.f(L.offS2);
 
     Products prod{&sh, &L, gop, L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offGt) : nullptr,
-                  L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offPl) : nullptr, false, batch, stream};
+                  L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offPl) : nullptr, false, batch, stream,
+                  reinterpret_cast<unsigned*>(w.base + L.offCM), L.strideCM};
+    bool ready = false;   // the last product left the column maxima of its output
     if (L.bf16) {
         // both products read G in place when the direct-load kernel takes them:
         // G rows are K-contiguous for one product and M-contiguous for the other
@@ -441,12 +459,12 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
 
     // a1-a3: sketch, range sample, orthonormalise
     GALORE_TRACED(tr, GALORE_STAGE_SKETCH, launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
-    GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Sa, L.strideS));
+    GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Sa, L.strideS, ready));
     float* Q = Sa;
     float* Qtmp = Sb;
     auto orth_s = [&](int passes) -> int {
         for (int ps = 0; ps < passes; ++ps) {
-            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, tr);
+            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, tr, ps == 0 && ready);
             if (e != GALORE_OK) return e;
             float* t = Q;
             Q = Qtmp;
@@ -457,9 +475,9 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(orth_s(q == 0 ? 2 : 1));
     // a4: power iterations with re-orthonormalisation after every product
     for (int it = 0; it < q; ++it) {
-        GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL));
-        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, tr));
-        GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS));
+        GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready));
+        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, tr, ready));
+        GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS, ready));
         {
             float* t = Q;
             Q = Qtmp;
@@ -468,9 +486,10 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
         GALORE_CHECK(orth_s(it == q - 1 ? 2 : 1));
     }
     // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
-    GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL));
+    GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready));
     {
-        GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, L1, L.strideL, l, k), batch, stream));
+        GALORE_TRACED(tr, GALORE_STAGE_GRAM,
+                      launch_gram_i8(gram_args(w, L1, L.strideL, l, k, ready), batch, stream));
         if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
         GALORE_CHECK(enqueue_cholesky(w, k, false, batch, stream));
         if (tr.end() != hipSuccess) return GALORE_ERR_HIP;

@@ -20,7 +20,8 @@
 //
 // Three launches per Gram:
 //   colmax    the bit pattern of max_i |x_ij| per column (unsigned atomicMax
-//             over row blocks; a NaN or Inf wins and marks the column);
+//             over row blocks; a NaN or Inf wins and marks the column), unless
+//             the kernel that produced X already wrote them;
 //   quantize  64 x 64 tiles of X -> digit planes D_a stored by columns
 //             (column j of X is row j of each plane, rows padded with zeros),
 //             so that the Gram reads K-contiguous 16-byte fragments;
@@ -284,18 +285,21 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
 int64_t gram_i8_ld(int rows) { return (static_cast<int64_t>(rows) + 127) / 128 * 128; }
 int gram_i8_cols_pad(int cols) { return (cols + GT - 1) / GT * GT; }
 
+hipError_t launch_fill_u32(unsigned* p, int64_t n, hipStream_t stream) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, p, n);
+    return hipGetLastError();
+}
+
 hipError_t launch_gram_i8(const GramI8Args& g, int batch, hipStream_t stream) {
     const int64_t ldq = gram_i8_ld(g.rows);
     const int cpad = gram_i8_cols_pad(g.cols);
     const int64_t planeStride = static_cast<int64_t>(cpad) * ldq;
     const int64_t strideD = 3 * planeStride;
     if (strideD > g.strideD || g.ldc < g.cols) return hipErrorInvalidValue;
-    {
-        const int64_t n = g.strideCM * batch;
-        hipLaunchKernelGGL(fill_u32_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream,
-                           g.cmax, n);
-    }
-    {
+    if (!g.cmax_ready) {
+        const hipError_t e = launch_fill_u32(g.cmax, g.strideCM * batch, stream);
+        if (e != hipSuccess) return e;
         const int rb = 128;
         dim3 grid((g.rows + rb - 1) / rb, batch);
         hipLaunchKernelGGL(colmax_kernel, grid, dim3(256), 0, stream, g.X, g.ldx, g.strideX, g.rows, g.cols, rb,
