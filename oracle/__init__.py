@@ -17,6 +17,9 @@ What each function follows (paper = "GaLore 2", Su et al. 2025):
   adam             paper §3 moments + Alg. 1 bias correction
   project_back     paper §3, W <- W + eta alpha P N (applied as W -= lr alpha P N
                    for the autograd gradient)
+  align_projector  subspace switch: signs of a new P matched to the previous P
+                   (paper §4.1.3 sign indeterminacy, Alg. 1 schedule), optional
+                   first-moment re-expression in the new basis
 """
 from __future__ import annotations
 
@@ -74,6 +77,9 @@ def _load():
         lib.orc_project_back.argtypes = [_f64p, _f64p, _f64p, i64, i64, i32, ctypes.c_double,
                                          ctypes.c_double]
         lib.orc_project_back.restype = None
+        lib.orc_align_projector.argtypes = [_f64p, _f64p, i64, i64, ctypes.POINTER(ctypes.c_int32), _f64p, _f64p,
+                                            i64]
+        lib.orc_align_projector.restype = None
         _lib = lib
     return _lib
 
@@ -178,3 +184,23 @@ def project_back(P, N, W, lr: float, alpha: float) -> np.ndarray:
     r = P.shape[1]
     _load().orc_project_back(_ptr(P), _ptr(N), _ptr(W), m, n, r, lr, alpha)
     return W
+
+
+def align_projector(P_old, P_new, M=None):
+    """Subspace switch: (P_new with each column's sign matched to P_old's,
+    flips (r, 1 = negated), M re-expressed in the new basis (P_new^T P_old) M
+    or None). Inputs are not modified."""
+    P_old = _f64(P_old)
+    P_new = _f64(P_new).copy()
+    s, r = P_old.shape
+    assert P_new.shape == (s, r)
+    flips = np.zeros(r, dtype=np.int32)
+    fp = flips.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    if M is None:
+        _load().orc_align_projector(_ptr(P_old), _ptr(P_new), s, r, fp, None, None, 0)
+        return P_new, flips, None
+    M = _f64(M)
+    assert M.shape[0] == r
+    M_out = np.zeros_like(M)
+    _load().orc_align_projector(_ptr(P_old), _ptr(P_new), s, r, fp, _ptr(M), _ptr(M_out), M.shape[1])
+    return P_new, flips, M_out

@@ -443,3 +443,41 @@ ORC_API void orc_project_back(const double* P, const double* N, double* W, int64
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Subspace switch (paper §4.1.3: singular vectors are defined only up to    */
+/* sign, and the randomized SVD adds its own randomness, so consecutive      */
+/* projectors can disagree in sign; paper Alg. 1 replaces P every T steps).  */
+/* Column j of the new projector is negated when its overlap with column j  */
+/* of the previous one, <p_old_j, p_new_j>, is negative (zero or NaN keeps   */
+/* it). Optionally the first moment is re-expressed in the new basis:       */
+/* M_out = (P_new^T P_old) M_in with the aligned P_new (r x r times r x l).  */
+/* P_old, P_new: s x r; flips: r ints (1 = negated); M_in, M_out: r x l.     */
+/* ------------------------------------------------------------------------ */
+ORC_API void orc_align_projector(const double* P_old, double* P_new, int64_t s, int64_t r, int32_t* flips,
+                                 const double* M_in, double* M_out, int64_t l) {
+    for (int64_t j = 0; j < r; ++j) {
+        double ov = 0.0;
+        for (int64_t i = 0; i < s; ++i) ov += P_old[i * r + j] * P_new[i * r + j];
+        flips[j] = (ov < 0.0) ? 1 : 0;
+        if (flips[j])
+            for (int64_t i = 0; i < s; ++i) P_new[i * r + j] = -P_new[i * r + j];
+    }
+    if (M_in == NULL || M_out == NULL) return;
+    double* O = (double*)malloc(sizeof(double) * (size_t)(r * r));   /* O = P_new^T P_old */
+    #pragma omp parallel for schedule(static)
+    for (int64_t a = 0; a < r; ++a)
+        for (int64_t b = 0; b < r; ++b) {
+            double acc = 0.0;
+            for (int64_t i = 0; i < s; ++i) acc += P_new[i * r + a] * P_old[i * r + b];
+            O[a * r + b] = acc;
+        }
+    #pragma omp parallel for schedule(static)
+    for (int64_t a = 0; a < r; ++a)
+        for (int64_t c = 0; c < l; ++c) {
+            double acc = 0.0;
+            for (int64_t b = 0; b < r; ++b) acc += O[a * r + b] * M_in[b * l + c];
+            M_out[a * l + c] = acc;
+        }
+    free(O);
+}

@@ -377,3 +377,72 @@ def test_memory_accounting():
     P_elems, MV_elems, R_elems = s * r, 2 * r * l, r * l
     assert m * n + P_elems + MV_elems == m * n + m * r + 2 * n * r
     assert R_elems == n * r
+
+
+# ---------------------------------------------------------------- subspace switch
+
+
+def _haar(rng, n, k):
+    q, r = np.linalg.qr(rng.standard_normal((n, k)))
+    return q * np.sign(np.diag(r))
+
+
+def test_align_recovers_sign_flipped_projector(orc):
+    """A new projector that differs from the old one only by column signs (the
+    sign indeterminacy of paper §4.1.3) is mapped back onto the old one
+    exactly, and the flips are exactly the negated columns."""
+    rng = np.random.default_rng(21)
+    P_old = _haar(rng, 120, 17)
+    d = np.where(rng.random(17) < 0.5, -1.0, 1.0)
+    P_new, flips, M_out = orc.align_projector(P_old, P_old * d)
+    assert np.array_equal(P_new, P_old)
+    assert np.array_equal(flips, (d < 0).astype(np.int32))
+    assert M_out is None
+
+
+def test_align_rotated_basis_invariants(orc):
+    """For P_new = P_old Q (Q orthogonal r x r): every aligned column has a
+    non-negative overlap with its predecessor, the aligned P_new spans the same
+    space, and flipping changes nothing but signs."""
+    rng = np.random.default_rng(22)
+    s, r = 90, 12
+    P_old = _haar(rng, s, r)
+    Q = _haar(rng, r, r)
+    P_raw = P_old @ Q
+    P_new, flips, _ = orc.align_projector(P_old, P_raw)
+    assert np.all(np.einsum("ij,ij->j", P_old, P_new) >= 0)
+    assert np.allclose(np.abs(P_new), np.abs(P_raw), rtol=0, atol=0)
+    assert np.allclose(P_new @ P_new.T, P_old @ P_old.T, atol=1e-12)
+    # the flips are exactly the columns whose overlap (diag of Q) was negative
+    assert np.array_equal(flips, (np.diag(Q) < 0).astype(np.int32))
+
+
+def test_align_moment_reexpression_in_shared_span(orc):
+    """Coordinates in the old basis, re-expressed with (P_new^T P_old), equal
+    the coordinates in the new basis for any matrix inside the shared span:
+    for G = P_old X, (P_new^T P_old)(P_old^T G) = P_new^T G. Identity when the
+    projector does not change."""
+    rng = np.random.default_rng(23)
+    s, r, l = 70, 9, 31
+    P_old = _haar(rng, s, r)
+    P_raw = P_old @ _haar(rng, r, r)
+    G = P_old @ rng.standard_normal((r, l))
+    R_old = P_old.T @ G
+    P_new, _, M_out = orc.align_projector(P_old, P_raw, R_old)
+    assert np.allclose(M_out, P_new.T @ G, rtol=0, atol=1e-12)
+    _, flips, M_same = orc.align_projector(P_old, P_old, R_old)
+    assert not flips.any()
+    assert np.allclose(M_same, R_old, rtol=0, atol=1e-12)
+
+
+def test_align_zero_overlap_keeps_sign(orc):
+    """A column orthogonal to its predecessor (overlap exactly 0) is kept."""
+    P_old = np.zeros((4, 2))
+    P_old[0, 0] = 1.0
+    P_old[1, 1] = 1.0
+    P_raw = np.zeros((4, 2))
+    P_raw[2, 0] = -1.0
+    P_raw[1, 1] = -1.0
+    P_new, flips, _ = orc.align_projector(P_old, P_raw)
+    assert list(flips) == [0, 1]
+    assert P_new[2, 0] == -1.0 and P_new[1, 1] == 1.0
