@@ -228,6 +228,39 @@ GALORE_API int galore_project_back(const float* P, int64_t ldp, int64_t stride_p
                         int64_t ldw, int64_t stride_w, int32_t r, float lr, float alpha,
                         int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Bytes of workspace galore_align_projector needs to re-express the first
+ * moment for `batch` projectors of rank r (one r x r overlap matrix each).
+ * 0 for invalid sizes.
+ */
+GALORE_API size_t galore_align_workspace_size(int32_t r, int32_t batch);
+
+/*
+ * Subspace switch (paper §4.1.3: singular vectors are defined only up to sign
+ * and the randomized SVD adds randomness, so a new projector can disagree in
+ * sign with the one it replaces; paper Alg. 1 replaces P every T steps).
+ * Column j of P_new is negated in place when its overlap with column j of
+ * P_old, <p_old_j, p_new_j> (summed in fp64 from the exact fp32 products), is
+ * negative; an overlap of zero (or NaN) keeps the sign. Optionally the first
+ * moment is re-expressed in the new basis: M_out = (P_new^T P_old) M_in with
+ * the aligned P_new, on the fp32 matrix cores.
+ * P_old, P_new: fp32 s x r (ld ld_old / ld_new >= r, batch strides stride_old /
+ *          stride_new); flips: device int32[batch * r] or NULL, 1 where a column
+ *          was negated.
+ * M_in, M_out: fp32 r x l (ld ldm >= l, batch stride stride_m), both NULL (no
+ *          re-expression) or both set and not overlapping.
+ * Workspace: with M_in, at least galore_align_workspace_size(r, batch) bytes,
+ *          device, 256-byte aligned, scratch; unused otherwise (may be NULL).
+ * Errors: NULL P_old/P_new, only one of M_in/M_out, or M_out overlapping M_in ->
+ *          INVALID_ARG; s, r < 1, r > s, ld/stride too small, l < 1 -> SHAPE;
+ *          missing, misaligned or short workspace when re-expressing -> WORKSPACE.
+ */
+GALORE_API int galore_align_projector(const float* P_old, int64_t ld_old, int64_t stride_old, float* P_new,
+                                      int64_t ld_new, int64_t stride_new, int64_t s, int32_t r, int32_t* flips,
+                                      const float* M_in, float* M_out, int64_t ldm, int64_t stride_m, int64_t l,
+                                      int32_t batch, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,6 +24,7 @@ EXPORTED = (
     "galore_rsvd_update", "galore_rsvd_update_traced", "galore_project_workspace_size", "galore_project",
     "galore_lowrank_adam_step",
     "galore_project_back_workspace_size", "galore_project_back",
+    "galore_align_workspace_size", "galore_align_projector",
 )
 
 # galore_stage_t
@@ -67,6 +68,11 @@ def _declare(lib):
     lib.galore_project_back.argtypes = [vp, i64, i64, vp, i64, i64, vp, i64, i64, i64, i64, i32,
                                         f32, f32, i32, vp, sz, vp]
     lib.galore_project_back.restype = ctypes.c_int
+    lib.galore_align_workspace_size.argtypes = [i32, i32]
+    lib.galore_align_workspace_size.restype = sz
+    lib.galore_align_projector.argtypes = [vp, i64, i64, vp, i64, i64, i64, i32, vp, vp, vp, i64, i64, i64, i32,
+                                           vp, sz, vp]
+    lib.galore_align_projector.restype = ctypes.c_int
     return lib
 
 
@@ -240,3 +246,42 @@ def galore_project_back(P: torch.Tensor, N: torch.Tensor, W: torch.Tensor, lr: f
     _check(lib.galore_project_back(pp, ldp, sp, np_, ldn, sn, wp, m, n, ldw, sw, r, lr, alpha, batch, wsp, wsb,
                                    _stream(stream)), "galore_project_back")
     return W
+
+
+def galore_align_workspace_size(r: int, batch: int = 1) -> int:
+    return int(lib.galore_align_workspace_size(r, batch))
+
+
+def galore_align_projector(P_old: torch.Tensor, P_new: torch.Tensor, M=None, M_out=None, flips=None,
+                           workspace=None, stream=None):
+    """Subspace switch: negate in place the columns of P_new whose overlap with
+    P_old is negative; with M (r x l, or batched), also return M re-expressed in
+    the new basis, (P_new^T P_old) M, into M_out (allocated unless given).
+    Returns (P_new, flips, M_out or None); flips is int32 (r,) or (batch, r)."""
+    for t, nm in ((P_old, "P_old"), (P_new, "P_new"), (M, "M"), (M_out, "M_out")):
+        if t is not None and t.dtype != torch.float32:
+            raise ValueError("%s must be float32" % nm)
+    po, s, r, ldo, so, batch = _mat(P_old, "P_old")
+    pn, s2, r2, ldn, sn, batch2 = _mat(P_new, "P_new")
+    if (s2, r2, batch2) != (s, r, batch):
+        raise ValueError("P_new must match P_old in shape")
+    if flips is None:
+        flips = torch.empty((batch, r) if P_old.dim() == 3 else (r,), dtype=torch.int32, device=P_old.device)
+    mi = mo = None
+    ldm = sm = l = 0
+    wsp, wsb = None, 0
+    if M is not None:
+        mi, mr, l, ldm, sm, mb = _mat(M, "M")
+        if mr != r or mb != batch:
+            raise ValueError("M must be r x l per projector")
+        if M_out is None:
+            M_out = torch.empty_like(M)
+        mo, _, _, ldo2, so2, _ = _mat(M_out, "M_out")
+        if M_out.shape != M.shape or (ldo2, so2) != (ldm, sm):
+            raise ValueError("M_out must match M in shape and strides")
+        if workspace is None:
+            workspace = torch.empty((galore_align_workspace_size(r, batch),), dtype=torch.uint8, device=M.device)
+        wsp, wsb = workspace.data_ptr(), workspace.numel()
+    _check(lib.galore_align_projector(po, ldo, so, pn, ldn, sn, s, r, flips.data_ptr(), mi, mo, ldm, sm, l, batch,
+                                      wsp, wsb, _stream(stream)), "galore_align_projector")
+    return P_new, flips, (M_out if M is not None else None)

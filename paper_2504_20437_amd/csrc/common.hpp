@@ -113,6 +113,11 @@ hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, in
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
                                   float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
                                   double* scratch, int64_t strideScratch, int batch, hipStream_t stream);
+// Subspace switch: negate the columns of P_new whose overlap with the same
+// column of P_old is negative (rows x r each); flips (batch x r, may be null)
+// receives 1 for a negated column.
+hipError_t launch_align(const float* P_old, int64_t ldo, int64_t strideO, float* P_new, int64_t ldn, int64_t strideN,
+                        int rows, int r, int* flips, int batch, hipStream_t stream);
 hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strideP, int batch,
                            hipStream_t stream);
 hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t rows, int64_t cols,

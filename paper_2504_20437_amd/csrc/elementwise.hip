@@ -56,6 +56,46 @@ __global__ __launch_bounds__(SF_COLS* SF_GROUPS) void sign_fix_kernel(float* Pb,
     }
 }
 
+// Subspace switch: a workgroup owns 64 columns of one matrix (4 row groups);
+// the overlap <p_old_j, p_new_j> is summed in fp64 from the exact fp32
+// products, and column j of the new projector is negated in place when it is
+// negative (zero or NaN keeps the sign; paper §4.1.3 sign indeterminacy).
+__global__ __launch_bounds__(SF_COLS* SF_GROUPS) void align_kernel(const float* Pob, int64_t ldo, int64_t strideO,
+                                                                   float* Pnb, int64_t ldn, int64_t strideN,
+                                                                   int rows, int r, int* flipsb) {
+    const int b = blockIdx.y;
+    const float* Po = Pob + static_cast<int64_t>(b) * strideO;
+    float* Pn = Pnb + static_cast<int64_t>(b) * strideN;
+    const int tc = threadIdx.x & (SF_COLS - 1);
+    const int grp = threadIdx.x / SF_COLS;
+    const int c = blockIdx.x * SF_COLS + tc;
+    __shared__ double part[SF_GROUPS][SF_COLS];
+    __shared__ float flip[SF_COLS];
+    double acc = 0.0;
+    if (c < r) {
+#pragma unroll 8
+        for (int i = grp; i < rows; i += SF_GROUPS)
+            acc += static_cast<double>(Po[static_cast<int64_t>(i) * ldo + c]) *
+                   static_cast<double>(Pn[static_cast<int64_t>(i) * ldn + c]);
+    }
+    part[grp][tc] = acc;
+    __syncthreads();
+    if (grp == 0) {
+        double ov = part[0][tc];
+        for (int g = 1; g < SF_GROUPS; ++g) ov += part[g][tc];
+        const int f = (ov < 0.0) ? 1 : 0;
+        flip[tc] = f ? -1.0f : 1.0f;
+        if (c < r && flipsb != nullptr) flipsb[static_cast<int64_t>(b) * r + c] = f;
+    }
+    __syncthreads();
+    if (c < r && flip[tc] < 0.0f) {
+        for (int i = grp; i < rows; i += SF_GROUPS) {
+            float* q = Pn + static_cast<int64_t>(i) * ldn + c;
+            *q = -*q;
+        }
+    }
+}
+
 __device__ __forceinline__ void adam_elem(float g, float& m, float& v, float& n, float beta1,
                                           float beta2, float om1, float om2, float bc1, float bc2,
                                           float eps) {
@@ -137,6 +177,14 @@ hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strid
     dim3 grid((r + SF_COLS - 1) / SF_COLS, batch);
     hipLaunchKernelGGL(sign_fix_kernel, grid, dim3(SF_COLS * SF_GROUPS), 0, stream, P, rows, r, ldp,
                        strideP);
+    return hipGetLastError();
+}
+
+hipError_t launch_align(const float* P_old, int64_t ldo, int64_t strideO, float* P_new, int64_t ldn, int64_t strideN,
+                        int rows, int r, int* flips, int batch, hipStream_t stream) {
+    dim3 grid((r + SF_COLS - 1) / SF_COLS, batch);
+    hipLaunchKernelGGL(align_kernel, grid, dim3(SF_COLS * SF_GROUPS), 0, stream, P_old, ldo, strideO, P_new, ldn,
+                       strideN, rows, r, flips);
     return hipGetLastError();
 }
 

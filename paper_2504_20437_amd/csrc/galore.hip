@@ -670,6 +670,81 @@ int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G,
     return GALORE_OK;
 }
 
+size_t galore_align_workspace_size(int32_t r, int32_t batch) {
+    if (r < 1 || batch < 1) return 0;
+    return align_up(static_cast<size_t>(batch) * pad_elems(static_cast<int64_t>(r) * r) * sizeof(float), kAlign);
+}
+
+int galore_align_projector(const float* P_old, int64_t ld_old, int64_t stride_old, float* P_new, int64_t ld_new,
+                           int64_t stride_new, int64_t s, int32_t r, int32_t* flips, const float* M_in,
+                           float* M_out, int64_t ldm, int64_t stride_m, int64_t l, int32_t batch,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (P_old == nullptr || P_new == nullptr) return GALORE_ERR_INVALID_ARG;
+    if ((M_in == nullptr) != (M_out == nullptr)) return GALORE_ERR_INVALID_ARG;
+    if (s < 1 || r < 1 || r > s || s > INT32_MAX || batch < 1) return GALORE_ERR_SHAPE;
+    if (ld_old < r || ld_new < r) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_old < s * ld_old || stride_new < s * ld_new)) return GALORE_ERR_SHAPE;
+    const int64_t so = (batch > 1) ? stride_old : s * ld_old;
+    const int64_t sn = (batch > 1) ? stride_new : s * ld_new;
+    const bool reexpress = (M_in != nullptr);
+    int64_t sm = 0;
+    if (reexpress) {
+        if (l < 1 || l > INT32_MAX || ldm < l) return GALORE_ERR_SHAPE;
+        if (batch > 1 && stride_m < r * ldm) return GALORE_ERR_SHAPE;
+        sm = (batch > 1) ? stride_m : r * ldm;
+        // M_out must not overlap M_in (the product reads all of M_in)
+        const char* a0 = reinterpret_cast<const char*>(M_in);
+        const char* a1 = a0 + ((batch - 1) * sm + (r - 1) * ldm + l) * sizeof(float);
+        const char* b0 = reinterpret_cast<const char*>(M_out);
+        const char* b1 = b0 + ((batch - 1) * sm + (r - 1) * ldm + l) * sizeof(float);
+        if (a0 < b1 && b0 < a1) return GALORE_ERR_INVALID_ARG;
+        if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0) return GALORE_ERR_WORKSPACE;
+        if (workspace_bytes < galore_align_workspace_size(r, batch)) return GALORE_ERR_WORKSPACE;
+    }
+    GALORE_TRY(launch_align(P_old, ld_old, so, P_new, ld_new, sn, static_cast<int>(s), r, flips, batch, stream));
+    if (!reexpress) return GALORE_OK;
+    // O^T = P_old^T P_new (r x r, aligned P_new), then M_out = O M_in = (O^T)^T M_in
+    float* Ot = static_cast<float*>(workspace);
+    const int64_t strideO = pad_elems(static_cast<int64_t>(r) * r);
+    {
+        GemmArgs a{};
+        a.A = P_old;        // A(i, kk) = P_old[kk][i]: M contiguous
+        a.lda = ld_old;
+        a.strideA = so;
+        a.B = P_new;
+        a.ldb = ld_new;
+        a.strideB = sn;
+        a.C = Ot;
+        a.ldc = r;
+        a.strideC = strideO;
+        a.M = r;
+        a.N = r;
+        a.K = static_cast<int>(s);
+        a.alpha = 1.0f;
+        a.beta = 0.0f;
+        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kNContig, false, false, a, batch, stream));
+    }
+    {
+        GemmArgs a{};
+        a.A = Ot;           // A(i, kk) = O^T[kk][i] = O[i][kk]: M contiguous
+        a.lda = r;
+        a.strideA = strideO;
+        a.B = M_in;
+        a.ldb = ldm;
+        a.strideB = sm;
+        a.C = M_out;
+        a.ldc = ldm;
+        a.strideC = sm;
+        a.M = r;
+        a.N = static_cast<int>(l);
+        a.K = r;
+        a.alpha = 1.0f;
+        a.beta = 0.0f;
+        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kNContig, false, false, a, batch, stream));
+    }
+    return GALORE_OK;
+}
+
 int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64_t rows,
                              int64_t cols, int64_t ld, int64_t stride, int32_t batch, float beta1,
                              float beta2, float eps, int64_t t, hipStream_t stream) {

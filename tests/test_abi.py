@@ -182,3 +182,33 @@ def test_rsvd_traced_rejects():
     bad[6] = 65                                      # r > s: rejected by the update itself
     assert f(*bad, None, None, 0, ctypes.byref(cnt)) == -2
     assert cnt.value == 0
+
+
+def test_align_workspace_size():
+    import paper_2504_20437_amd as gl
+    one = gl.galore_align_workspace_size(32, 1)
+    assert one >= 32 * 32 * 4 and one % 256 == 0
+    assert gl.galore_align_workspace_size(32, 5) == 5 * one
+    assert gl.galore_align_workspace_size(0, 1) == 0
+    assert gl.galore_align_workspace_size(32, 0) == 0
+
+
+def test_align_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_align_projector
+    ws = FAKE - FAKE % 256 + 256
+    need = gl.galore_align_workspace_size(8, 1)
+    ok = dict(Po=FAKE, ldo=8, so=0, Pn=FAKE + 4096, ldn=8, sn=0, s=64, r=8, fl=None, Mi=FAKE + 8192,
+              Mo=FAKE + 65536, ldm=96, sm=0, l=96, b=1, ws=ws, wb=need)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(a["Po"], a["ldo"], a["so"], a["Pn"], a["ldn"], a["sn"], a["s"], a["r"], a["fl"], a["Mi"],
+                 a["Mo"], a["ldm"], a["sm"], a["l"], a["b"], a["ws"], a["wb"], None)
+    for kw in (dict(Po=NULL), dict(Pn=NULL), dict(Mi=NULL), dict(Mo=NULL),
+               dict(Mo=FAKE + 8192 + 4 * 96 * 7)):                            # M_out overlaps M_in
+        assert call(**kw) == -1, kw
+    for kw in (dict(s=0), dict(r=0), dict(r=65), dict(ldo=7), dict(ldn=7), dict(b=0), dict(b=2),
+               dict(b=2, so=64 * 8, sn=64 * 8, sm=8 * 96 - 1), dict(l=0), dict(ldm=95)):
+        assert call(**kw) == -2, kw
+    for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
+        assert call(**kw) == -3, kw

@@ -420,3 +420,96 @@ def test_rsvd_bf16_exact_recovery(gl, orc):
     assert max_rel_violation(sig, ss[:24], 1e-4, 1e-30) <= 1.0
     assert proj_dist(P, u[:, :24]) <= 1e-3
     assert orth_err(P) < 1e-4
+
+
+# ---------------------------------------------------------------- subspace switch
+
+
+def _haar(rng, n, k):
+    q, r = np.linalg.qr(rng.standard_normal((n, k)))
+    return q * np.sign(np.diag(r))
+
+
+def _switch_pair(rng, s, r, noise):
+    """old projector and a new one spanning a nearby subspace, with random column signs (fp32)"""
+    P_old = _haar(rng, s, r)
+    q, _ = np.linalg.qr(P_old + noise * rng.standard_normal((s, r)))
+    d = np.where(rng.random(r) < 0.5, -1.0, 1.0)
+    return P_old.astype(np.float32), (q * d).astype(np.float32)
+
+
+def _moment_bound(P_new, P_old, M):
+    """elementwise |P_new|^T |P_old| |M|: bounds both rounding terms of (P_new^T P_old) M"""
+    return (np.abs(P_new.astype(np.float64)).T @ np.abs(P_old.astype(np.float64))) @ np.abs(M.astype(np.float64))
+
+
+@pytest.mark.parametrize("s,r,l,batch", [(256, 32, 130, 1), (300, 17, 1, 1), (1000, 96, 257, 3),
+                                         (4096, 128, 64, 2)])
+def test_align_matches_oracle(gl, orc, s, r, l, batch):
+    """Flips and the aligned projector are bit-exact (a negation); the
+    re-expressed first moment is within 1e-5 of the rounding bound
+    |P_new|^T |P_old| |M| elementwise."""
+    import torch
+    rng = np.random.default_rng(4100 + s + r)
+    pairs = [_switch_pair(rng, s, r, 0.4) for _ in range(batch)]
+    Ms = [rng.standard_normal((r, l)).astype(np.float32) for _ in range(batch)]
+    Po = dev(np.stack([p[0] for p in pairs]))
+    Pn = dev(np.stack([p[1] for p in pairs]))
+    M = dev(np.stack(Ms))
+    if batch == 1:
+        Po, Pn, M = Po[0], Pn[0], M[0]
+    Pn2, flips, Mo = gl.galore_align_projector(Po, Pn, M)
+    Pn2h, Moh = host(Pn2).reshape(batch, s, r), host(Mo).reshape(batch, r, l)
+    fl = flips.cpu().numpy().reshape(batch, r)
+    for i in range(batch):
+        Pr, fr, Mr = orc.align_projector(pairs[i][0], pairs[i][1], Ms[i])
+        assert np.array_equal(fl[i], fr)
+        assert np.array_equal(Pn2h[i], Pr)
+        err = np.abs(Moh[i] - Mr)
+        assert (err <= 1e-5 * _moment_bound(Pr, pairs[i][0], Ms[i]) + 1e-30).all()
+
+
+def test_align_without_moment_and_strided(gl, orc):
+    """M = NULL aligns the projector only; padded leading dimensions and batch
+    strides leave the padding untouched."""
+    import torch
+    rng = np.random.default_rng(77)
+    s, r, batch = 520, 40, 2
+    pairs = [_switch_pair(rng, s, r, 0.2) for _ in range(batch)]
+    Po = torch.full((batch, s + 3, 48), 7.0, device="cuda")
+    Pn = torch.full((batch, s + 1, 64), 9.0, device="cuda")
+    for i in range(batch):
+        Po[i, :s, :r] = dev(pairs[i][0])
+        Pn[i, :s, :r] = dev(pairs[i][1])
+    Pnv = Pn[:, :s, :r]
+    _, flips, Mo = gl.galore_align_projector(Po[:, :s, :r], Pnv)
+    assert Mo is None
+    out = host(Pn)
+    for i in range(batch):
+        Pr, fr, _ = orc.align_projector(pairs[i][0], pairs[i][1])
+        assert np.array_equal(out[i, :s, :r], Pr)
+        assert np.array_equal(flips.cpu().numpy()[i], fr)
+    assert (out[:, :s, r:] == 9.0).all() and (out[:, s:, :] == 9.0).all()
+
+
+def test_align_exact_cases(gl):
+    """A sign-flipped copy is mapped back exactly; a column orthogonal to the
+    old one (overlap exactly zero) keeps its sign."""
+    import torch
+    rng = np.random.default_rng(5)
+    s, r = 200, 24
+    P_old = _haar(rng, s, r).astype(np.float32)
+    d = np.where(rng.random(r) < 0.5, -1.0, 1.0).astype(np.float32)
+    Pn = dev(P_old * d)
+    _, flips, _ = gl.galore_align_projector(dev(P_old), Pn)
+    assert np.array_equal(host(Pn), P_old.astype(np.float64))
+    assert np.array_equal(flips.cpu().numpy(), (d < 0).astype(np.int32))
+    E = np.zeros((s, 2), np.float32)
+    E[0, 0] = E[1, 1] = 1.0
+    F = np.zeros((s, 2), np.float32)
+    F[2, 0] = -1.0
+    F[1, 1] = -1.0
+    Fd = dev(F)
+    _, flips, _ = gl.galore_align_projector(dev(E), Fd)
+    assert flips.cpu().numpy().tolist() == [0, 1]
+    assert host(Fd)[2, 0] == -1.0 and host(Fd)[1, 1] == 1.0
