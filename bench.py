@@ -404,6 +404,21 @@ def main():
             a = sum(launches[c]) / len(launches[c])
             rates[c] = round(units_c / (a * 1e-3) / (1e9 if bd == "hbm" else 1e12), 2)
 
+    # subspace switch (once per T steps): signs of a new projector matched to
+    # the previous one and the first moment re-expressed in the new basis;
+    # timed outside the step on a copy of the current projector
+    P_new = P.clone()
+    M_sw = torch.empty_like(M)
+    aws = torch.empty((gl.galore_align_workspace_size(r, B),), dtype=torch.uint8, device=dev)
+    sw = [mk() for _ in range(4)]
+    for j in range(2):
+        sw[2 * j].record(stream)
+        gl.galore_align_projector(P, P_new, M, M_out=M_sw, workspace=aws, stream=stream)
+        sw[2 * j + 1].record(stream)
+    torch.cuda.synchronize()
+    switch_ms = sw[2].elapsed_time(sw[3])
+    del P_new, M_sw, aws
+
     out = {
         "metric": "rSVD subspace updates/sec at 4096x11008 r=1024; low-rank Adam step HBM GB/s",
         "value": round(B / (ms_per_step * 1e-3), 3),
@@ -428,6 +443,9 @@ def main():
         "rsvd_stage_ms": {st: round(v, 3) for st, v in sorted(sub.items(), key=lambda x: -x[1])},
         "kernel_rates": rates,
         "roofline": roof,
+        "switch_ms": round(switch_ms, 3),
+        "switch_note": ("subspace switch of the whole batch (sign alignment + first-moment re-expression), "
+                        "once per T steps: %.4f ms per step at T=200" % (switch_ms / 200.0)),
     }
     del G, W, R, M, V, N, chunks
     torch.cuda.empty_cache()
