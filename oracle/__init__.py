@@ -20,6 +20,9 @@ What each function follows (paper = "GaLore 2", Su et al. 2025):
   align_projector  subspace switch: signs of a new P matched to the previous P
                    (paper §4.1.3 sign indeterminacy, Alg. 1 schedule), optional
                    first-moment re-expression in the new basis
+  galore_step      one step of paper Alg. 1: a new projector every T steps
+                   (optionally followed by the subspace switch), projection,
+                   Adam with bias exponent tau + 1, back-projection
 """
 from __future__ import annotations
 
@@ -204,3 +207,28 @@ def align_projector(P_old, P_new, M=None):
     M_out = np.zeros_like(M)
     _load().orc_align_projector(_ptr(P_old), _ptr(P_new), s, r, fp, _ptr(M), _ptr(M_out), M.shape[1])
     return P_new, flips, M_out
+
+
+def galore_step(G, W, P, M, V, r: int, p: int, q: int, seed: int, tau: int, T: int, sketch_index: int = 0,
+                beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8, lr: float = 1e-3, alpha: float = 0.25,
+                align: bool = False, reexpress: bool = False, P_given=None):
+    """One step of paper Alg. 1 at 0-based step tau for one m x n matrix.
+    Returns (W, P, M, V) after the step (inputs are not modified). P may be
+    None when tau is an update step. P_given, if set, replaces the subspace
+    update's raw projector (a test that injects the projector of another
+    implementation); alignment and re-expression still apply to it."""
+    W = _f64(W).copy()
+    M = _f64(M).copy()
+    V = _f64(V).copy()
+    if tau % T == 0:
+        P_new = _f64(P_given) if P_given is not None else rsvd_update(G, r, p, q, seed, sketch_index)[0]
+        if align and tau > 0:
+            P_new, _, M_re = align_projector(P, P_new, M if reexpress else None)
+            if reexpress:
+                M = M_re
+        P = P_new
+    P = _f64(P)
+    R = project(P, G)
+    M, V, N = adam(R, M, V, beta1, beta2, eps, tau + 1)
+    W = project_back(P, N, W, lr, alpha)
+    return W, P, M, V

@@ -446,3 +446,57 @@ def test_align_zero_overlap_keeps_sign(orc):
     P_new, flips, _ = orc.align_projector(P_old, P_raw)
     assert list(flips) == [0, 1]
     assert P_new[2, 0] == -1.0 and P_new[1, 1] == 1.0
+
+
+# ---------------------------------------------------------------- scheduled step (Alg. 1)
+
+
+@pytest.mark.parametrize("m,n", [(6, 9), (9, 6)])
+def test_step_full_rank_permutation_projector_is_adam(orc, m, n):
+    """Gradients whose short-side singular vectors are the coordinate axes in a
+    fixed non-sorted order give, at r = s, a projector that is a permutation
+    matrix at every update; Adam commutes with row permutations, so the
+    scheduled steps (updates every T = 2 steps, switch and re-expression on)
+    equal torch.optim.Adam (CPU fp64) with step size lr*alpha from step 1 on:
+    this fixes the schedule, the bias exponent tau + 1 and both orientations."""
+    import torch
+    rng = np.random.default_rng(31)
+    s, l = min(m, n), max(m, n)
+    d = np.array([3.0, 1.0, 5.0, 2.0, 4.0, 0.5, 6.0, 1.5, 2.5][:s])
+    lr, al = 1e-2, 0.5
+    b1, b2, eps = 0.9, 0.999, 1e-8
+    W0 = rng.standard_normal((m, n))
+    w = torch.tensor(W0.copy(), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([w], lr=lr * al, betas=(b1, b2), eps=eps, weight_decay=0.0)
+    W, P, M, V = W0.copy(), None, np.zeros((s, l)), np.zeros((s, l))
+    for tau in range(5):
+        Qrows = gi.haar_columns(rng, l, s).T                 # s x l, orthonormal rows
+        A = d[:, None] * Qrows                                # A A^T = diag(d^2)
+        G = A if m <= n else A.T
+        w.grad = torch.tensor(G, dtype=torch.float64)
+        opt.step()
+        W, P, M, V = orc.galore_step(G, W, P, M, V, s, 2, 1, 7, tau, 2, beta1=b1, beta2=b2, eps=eps, lr=lr,
+                                     alpha=al, align=True, reexpress=True)
+        assert np.allclose(np.abs(P), np.eye(s)[:, np.argsort(-d)], atol=1e-12)
+    assert np.abs(W - w.detach().numpy()).max() < 1e-11
+
+
+def test_step_update_lies_in_last_projector_span(orc):
+    """Every step moves W only inside the span of the projector computed at the
+    last update step (tau mod T == 0), fixed by LAPACK's SVD of that step's
+    gradient; each step's gradient has its own random singular vectors, so a
+    projector refreshed at the wrong step moves W elsewhere."""
+    rng = np.random.default_rng(32)
+    m, n, r, T = 24, 40, 4, 3
+    spec = gi.spectrum_gapped(gi.spectrum_geometric(m, 0.8), r)
+    W, P, M, V = rng.standard_normal((m, n)), None, np.zeros((r, n)), np.zeros((r, n))
+    basis = None
+    for tau in range(7):
+        G = gi.planted_gradient(m, n, spec, 1e-3, seed=900 + tau)
+        if tau % T == 0:
+            basis = np.linalg.svd(G)[0][:, :r]
+        W1, P, M, V = orc.galore_step(G, W, P, M, V, r, 4, 2, 11, tau, T, align=True)
+        dW = W1 - W
+        W = W1
+        assert np.linalg.norm(dW - basis @ (basis.T @ dW)) <= 1e-6 * np.linalg.norm(dW)
+        assert np.linalg.norm(P @ P.T - basis @ basis.T) < 1e-6
