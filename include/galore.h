@@ -261,6 +261,58 @@ GALORE_API int galore_align_projector(const float* P_old, int64_t ld_old, int64_
                                       int32_t batch, void* workspace, size_t workspace_bytes,
                                       hipStream_t stream);
 
+/* Options of galore_step (bit flags). */
+typedef enum {
+    GALORE_STEP_ALIGN = 1,      /* after each update but the first, match the new projector's column
+                                   signs to the previous projector's (galore_align_projector)        */
+    GALORE_STEP_REEXPRESS = 2   /* with ALIGN: also re-express M in the new basis, (P_new^T P_old) M  */
+} galore_step_flags_t;
+
+/*
+ * Bytes of workspace galore_step needs for `batch` m x n matrices with rank r,
+ * oversampling p, gradient storage g_dtype and the given flags. 0 for invalid
+ * sizes, dtype or flags.
+ */
+GALORE_API size_t galore_step_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch,
+                                             int32_t g_dtype, int32_t flags);
+
+/*
+ * One GaLore optimizer step on a batch of weight matrices (paper Alg. 1, with
+ * the readings of the moment and step-index questions that galore_lowrank_adam_step
+ * and galore_align_projector state):
+ *   if tau mod T == 0: P <- subspace update of G (galore_rsvd_update with
+ *                      seed, sketch_index0, r, p, q); with GALORE_STEP_ALIGN and
+ *                      tau > 0 the new P's column signs are matched to the
+ *                      previous P, and with GALORE_STEP_REEXPRESS M is replaced
+ *                      by (P_new^T P_old) M (V is kept)
+ *   R = P^T A; Adam on (M, V) with bias exponent t = tau + 1 gives N;
+ *   W <- W - lr * alpha * P N (transposed for m > n)
+ * tau >= 0 is the 0-based step index and T >= 1 the update interval; at tau = 0
+ * the step must be an update step (tau mod T == 0 always holds there), so P
+ * needs no initial value. The kernels and their results are those of the
+ * separate entry points called in this order.
+ * G: g_dtype m x n (ld ldg, stride stride_g); W: fp32 m x n (ld ldw, stride
+ * stride_w), updated in place; P: fp32 s x r (ld ldp, stride stride_p), the
+ * projector state, rewritten at update steps; M, V: fp32 r x l (ld ldm >= l,
+ * stride stride_m), the moments, updated in place; info: device int32[batch]
+ * or NULL, written at update steps (as galore_rsvd_update).
+ * Workspace: at least galore_step_workspace_size(...) bytes, device, 256-byte
+ * aligned, scratch (holds the projected gradient, the update's workspace and,
+ * with the flags, copies of the previous P and M).
+ * Streams: as galore_rsvd_update.
+ * Errors: NULL G/W/P/M/V, bad dtype, tau < 0, T < 1, unknown flags or
+ *         REEXPRESS without ALIGN, betas/eps/lr/alpha as galore_lowrank_adam_step
+ *         and galore_project_back -> INVALID_ARG; sizes, ld or strides invalid,
+ *         r > s, r + p > 4096 -> SHAPE; missing, misaligned or short workspace
+ *         -> WORKSPACE.
+ */
+GALORE_API int galore_step(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g,
+                           float* W, int64_t ldw, int64_t stride_w, float* P, int64_t ldp, int64_t stride_p,
+                           float* M, float* V, int64_t ldm, int64_t stride_m, int32_t r, int32_t p, int32_t q,
+                           uint64_t seed, uint64_t sketch_index0, int64_t tau, int32_t T, float beta1,
+                           float beta2, float eps, float lr, float alpha, int32_t flags, int32_t* info,
+                           int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,11 @@ EXPORTED = (
     "galore_lowrank_adam_step",
     "galore_project_back_workspace_size", "galore_project_back",
     "galore_align_workspace_size", "galore_align_projector",
+    "galore_step_workspace_size", "galore_step",
 )
+
+GALORE_STEP_ALIGN = 1
+GALORE_STEP_REEXPRESS = 2
 
 # galore_stage_t
 STAGES = ("sketch", "product_A", "product_At", "gram", "cholesky", "triangular", "jacobi", "projector",
@@ -73,6 +77,11 @@ def _declare(lib):
     lib.galore_align_projector.argtypes = [vp, i64, i64, vp, i64, i64, i64, i32, vp, vp, vp, i64, i64, i64, i32,
                                            vp, sz, vp]
     lib.galore_align_projector.restype = ctypes.c_int
+    lib.galore_step_workspace_size.argtypes = [i64, i64, i32, i32, i32, i32, i32]
+    lib.galore_step_workspace_size.restype = sz
+    lib.galore_step.argtypes = [vp, i32, i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, vp, i64, i64,
+                                i32, i32, i32, u64, u64, i64, i32, f32, f32, f32, f32, f32, i32, vp, i32, vp, sz, vp]
+    lib.galore_step.restype = ctypes.c_int
     return lib
 
 
@@ -285,3 +294,40 @@ def galore_align_projector(P_old: torch.Tensor, P_new: torch.Tensor, M=None, M_o
     _check(lib.galore_align_projector(po, ldo, so, pn, ldn, sn, s, r, flips.data_ptr(), mi, mo, ldm, sm, l, batch,
                                       wsp, wsb, _stream(stream)), "galore_align_projector")
     return P_new, flips, (M_out if M is not None else None)
+
+
+def galore_step_workspace_size(m: int, n: int, r: int, p: int, batch: int = 1, dtype=torch.float32,
+                               flags: int = 0) -> int:
+    code = GALORE_BF16 if dtype in (torch.bfloat16, GALORE_BF16, "bf16") else GALORE_F32
+    return int(lib.galore_step_workspace_size(m, n, r, p, batch, code, flags))
+
+
+def galore_step(G: torch.Tensor, W: torch.Tensor, P: torch.Tensor, M: torch.Tensor, V: torch.Tensor, r: int,
+                p: int, q: int, seed: int, tau: int, T: int, sketch_index0: int = 0, beta1: float = 0.9,
+                beta2: float = 0.999, eps: float = 1e-8, lr: float = 1e-3, alpha: float = 0.25, flags: int = 0,
+                info=None, workspace=None, stream=None):
+    """One scheduled GaLore step (subspace update when tau % T == 0, then
+    projection, low-rank Adam and back-projection); W, P, M, V are updated in
+    place. Returns info (int32 per matrix, written at update steps)."""
+    gp, m, n, ldg, sg, batch = _mat(G, "G")
+    for t, nm in ((W, "W"), (P, "P"), (M, "M"), (V, "V")):
+        if t.dtype != torch.float32:
+            raise ValueError("%s must be float32" % nm)
+    wp, wm, wn, ldw, sw, wb = _mat(W, "W")
+    pp, ps, pr, ldp, sp, pb = _mat(P, "P")
+    mp, mr, ml, ldm, sm, mb = _mat(M, "M")
+    vp_, vr, vl, ldv, sv, vb = _mat(V, "V")
+    s, l = min(m, n), max(m, n)
+    if (wm, wn, wb) != (m, n, batch) or (ps, pr, pb) != (s, r, batch) or (mr, ml, mb) != (r, l, batch):
+        raise ValueError("W, P, M must match G in shape (m x n, s x r, r x l)")
+    if (vr, vl, vb, ldv, sv) != (mr, ml, mb, ldm, sm):
+        raise ValueError("V must have M's shape and strides")
+    if info is None:
+        info = torch.zeros((batch,), dtype=torch.int32, device=G.device)
+    if workspace is None:
+        need = galore_step_workspace_size(m, n, r, p, batch, G.dtype, flags)
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=G.device)
+    _check(lib.galore_step(gp, _dtype_code(G), m, n, ldg, sg, wp, ldw, sw, pp, ldp, sp, mp, vp_, ldm, sm, r, p, q,
+                           seed, sketch_index0, tau, T, beta1, beta2, eps, lr, alpha, flags, info.data_ptr(), batch,
+                           workspace.data_ptr(), workspace.numel(), _stream(stream)), "galore_step")
+    return info

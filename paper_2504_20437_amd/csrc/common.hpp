@@ -123,6 +123,12 @@ hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strid
 hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t rows, int64_t cols,
                        int64_t ld, int64_t stride, int batch, float beta1, float beta2, float eps,
                        float bc1, float bc2, hipStream_t stream);
+// Adam with R and N in one layout (ldrn, srn) and M and V in another (ldmv, smv).
+hipError_t launch_adam2(const float* R, float* N, int64_t ldrn, int64_t srn, float* M, float* V, int64_t ldmv,
+                        int64_t smv, int64_t rows, int64_t cols, int batch, float beta1, float beta2, float eps,
+                        float bc1, float bc2, hipStream_t stream);
+hipError_t launch_copy_rows(const float* src, int64_t lds, int64_t strideS, float* dst, int64_t ldd,
+                            int64_t strideD, int rows, int cols, int batch, hipStream_t stream);
 
 // bf16 matrix-core products with an exactly bf16 operand (bf16x3.hip)
 hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, void* dst, int64_t ldd,

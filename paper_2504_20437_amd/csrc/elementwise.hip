@@ -148,10 +148,11 @@ __global__ __launch_bounds__(256) void adam_flat_kernel(const float* R, float* M
     }
 }
 
-// Strided state (ld > cols or padded batch stride).
-__global__ __launch_bounds__(256) void adam_strided_kernel(const float* R, float* M, float* V, float* N,
-                                                          int64_t rows, int64_t cols, int64_t ld,
-                                                          int64_t stride, float beta1, float beta2,
+// Strided state (ld > cols or padded batch stride); R and N share one layout,
+// M and V another.
+__global__ __launch_bounds__(256) void adam_strided_kernel(const float* R, float* N, int64_t ldrn, int64_t srn,
+                                                          float* M, float* V, int64_t ldmv, int64_t smv,
+                                                          int64_t rows, int64_t cols, float beta1, float beta2,
                                                           float eps, float bc1, float bc2) {
     const float om1 = 1.0f - beta1;
     const float om2 = 1.0f - beta2;
@@ -161,12 +162,24 @@ __global__ __launch_bounds__(256) void adam_strided_kernel(const float* R, float
          e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int64_t i = e / cols;
         const int64_t j = e - i * cols;
-        const int64_t off = b * stride + i * ld + j;
-        float m = M[off], v = V[off], n;
-        adam_elem(R[off], m, v, n, beta1, beta2, om1, om2, bc1, bc2, eps);
-        M[off] = m;
-        V[off] = v;
-        N[off] = n;
+        const int64_t o = b * srn + i * ldrn + j;
+        const int64_t om = b * smv + i * ldmv + j;
+        float m = M[om], v = V[om], n;
+        adam_elem(R[o], m, v, n, beta1, beta2, om1, om2, bc1, bc2, eps);
+        M[om] = m;
+        V[om] = v;
+        N[o] = n;
+    }
+}
+
+// Batched row copy: rows x cols of each matrix from (lds, strideS) to (ldd, strideD).
+__global__ __launch_bounds__(256) void copy_rows_kernel(const float* src, int64_t lds, int64_t strideS, float* dst,
+                                                       int64_t ldd, int64_t strideD, int rows, int cols) {
+    const int64_t b = blockIdx.y;
+    for (int i = blockIdx.x; i < rows; i += gridDim.x) {
+        const float* s = src + b * strideS + static_cast<int64_t>(i) * lds;
+        float* d = dst + b * strideD + static_cast<int64_t>(i) * ldd;
+        for (int j = threadIdx.x; j < cols; j += blockDim.x) d[j] = s[j];
     }
 }
 
@@ -188,10 +201,24 @@ hipError_t launch_align(const float* P_old, int64_t ldo, int64_t strideO, float*
     return hipGetLastError();
 }
 
+hipError_t launch_copy_rows(const float* src, int64_t lds, int64_t strideS, float* dst, int64_t ldd,
+                            int64_t strideD, int rows, int cols, int batch, hipStream_t stream) {
+    const int blocks = rows < 65536 ? rows : 65536;
+    hipLaunchKernelGGL(copy_rows_kernel, dim3(blocks, batch), dim3(256), 0, stream, src, lds, strideS, dst, ldd,
+                       strideD, rows, cols);
+    return hipGetLastError();
+}
+
 hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t rows, int64_t cols,
                        int64_t ld, int64_t stride, int batch, float beta1, float beta2, float eps,
                        float bc1, float bc2, hipStream_t stream) {
-    const bool contiguous = (ld == cols) && (stride == rows * cols);
+    return launch_adam2(R, N, ld, stride, M, V, ld, stride, rows, cols, batch, beta1, beta2, eps, bc1, bc2, stream);
+}
+
+hipError_t launch_adam2(const float* R, float* N, int64_t ldrn, int64_t srn, float* M, float* V, int64_t ldmv,
+                        int64_t smv, int64_t rows, int64_t cols, int batch, float beta1, float beta2, float eps,
+                        float bc1, float bc2, hipStream_t stream) {
+    const bool contiguous = (ldrn == cols) && (ldmv == cols) && (srn == rows * cols) && (smv == rows * cols);
     const bool aligned = ((reinterpret_cast<uintptr_t>(R) | reinterpret_cast<uintptr_t>(M) |
                            reinterpret_cast<uintptr_t>(V) | reinterpret_cast<uintptr_t>(N)) & 15) == 0;
     if (contiguous && aligned) {
@@ -208,7 +235,7 @@ hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t row
         int64_t blocks = (rows * cols + 255) / 256;
         if (blocks > 8192) blocks = 8192;
         hipLaunchKernelGGL(adam_strided_kernel, dim3(static_cast<unsigned>(blocks), batch), dim3(256),
-                           0, stream, R, M, V, N, rows, cols, ld, stride, beta1, beta2, eps, bc1, bc2);
+                           0, stream, R, N, ldrn, srn, M, V, ldmv, smv, rows, cols, beta1, beta2, eps, bc1, bc2);
     }
     return hipGetLastError();
 }

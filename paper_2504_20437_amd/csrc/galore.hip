@@ -4,6 +4,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 
@@ -533,6 +534,51 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     return GALORE_OK;
 }
 
+// First moment in the new basis: O^T = P_old^T P_new (r x r per matrix, into
+// Ot), then M_out = O M_in = (O^T)^T M_in, both on the fp32 matrix cores.
+int reexpress_moment(const float* P_old, int64_t ldo, int64_t so, const float* P_new, int64_t ldn, int64_t sn,
+                     int64_t s, int r, const float* M_in, int64_t ldmi, int64_t smi, float* M_out, int64_t ldmo,
+                     int64_t smo, int64_t l, float* Ot, int batch, hipStream_t stream) {
+    const int64_t strideO = pad_elems(static_cast<int64_t>(r) * r);
+    {
+        GemmArgs a{};
+        a.A = P_old;        // A(i, kk) = P_old[kk][i]: M contiguous
+        a.lda = ldo;
+        a.strideA = so;
+        a.B = P_new;
+        a.ldb = ldn;
+        a.strideB = sn;
+        a.C = Ot;
+        a.ldc = r;
+        a.strideC = strideO;
+        a.M = r;
+        a.N = r;
+        a.K = static_cast<int>(s);
+        a.alpha = 1.0f;
+        a.beta = 0.0f;
+        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kNContig, false, false, a, batch, stream));
+    }
+    {
+        GemmArgs a{};
+        a.A = Ot;           // A(i, kk) = O^T[kk][i] = O[i][kk]: M contiguous
+        a.lda = r;
+        a.strideA = strideO;
+        a.B = M_in;
+        a.ldb = ldmi;
+        a.strideB = smi;
+        a.C = M_out;
+        a.ldc = ldmo;
+        a.strideC = smo;
+        a.M = r;
+        a.N = static_cast<int>(l);
+        a.K = r;
+        a.alpha = 1.0f;
+        a.beta = 0.0f;
+        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kNContig, false, false, a, batch, stream));
+    }
+    return GALORE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -703,46 +749,8 @@ int galore_align_projector(const float* P_old, int64_t ld_old, int64_t stride_ol
     }
     GALORE_TRY(launch_align(P_old, ld_old, so, P_new, ld_new, sn, static_cast<int>(s), r, flips, batch, stream));
     if (!reexpress) return GALORE_OK;
-    // O^T = P_old^T P_new (r x r, aligned P_new), then M_out = O M_in = (O^T)^T M_in
-    float* Ot = static_cast<float*>(workspace);
-    const int64_t strideO = pad_elems(static_cast<int64_t>(r) * r);
-    {
-        GemmArgs a{};
-        a.A = P_old;        // A(i, kk) = P_old[kk][i]: M contiguous
-        a.lda = ld_old;
-        a.strideA = so;
-        a.B = P_new;
-        a.ldb = ld_new;
-        a.strideB = sn;
-        a.C = Ot;
-        a.ldc = r;
-        a.strideC = strideO;
-        a.M = r;
-        a.N = r;
-        a.K = static_cast<int>(s);
-        a.alpha = 1.0f;
-        a.beta = 0.0f;
-        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kNContig, false, false, a, batch, stream));
-    }
-    {
-        GemmArgs a{};
-        a.A = Ot;           // A(i, kk) = O^T[kk][i] = O[i][kk]: M contiguous
-        a.lda = r;
-        a.strideA = strideO;
-        a.B = M_in;
-        a.ldb = ldm;
-        a.strideB = sm;
-        a.C = M_out;
-        a.ldc = ldm;
-        a.strideC = sm;
-        a.M = r;
-        a.N = static_cast<int>(l);
-        a.K = r;
-        a.alpha = 1.0f;
-        a.beta = 0.0f;
-        GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kNContig, false, false, a, batch, stream));
-    }
-    return GALORE_OK;
+    return reexpress_moment(P_old, ld_old, so, P_new, ld_new, sn, s, r, M_in, ldm, sm, M_out, ldm, sm, l,
+                            static_cast<float*>(workspace), batch, stream);
 }
 
 int galore_lowrank_adam_step(const float* R, float* M, float* V, float* N, int64_t rows,
@@ -852,6 +860,126 @@ int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const flo
         GALORE_TRY(launch_gemm(ALayout::kMContig, BLayout::kKContig, false, false, a, batch, stream));
     }
     return GALORE_OK;
+}
+
+// Workspace of one scheduled step. Region X holds the subspace update's
+// workspace, reused after it for the projected gradient R (= N, packed
+// r x l) and the projection and back-projection planes; region Y holds what
+// lives across the update: sigma, the previous projector and the previous
+// first moment (for the switch) and the switch's overlap matrices.
+struct StepLayout {
+    size_t offR, offPws, offBws, pwsBytes, bwsBytes;
+    size_t offSigma, offPold, offMold, offAws, awsBytes, total;
+    int64_t strideR, stridePold, strideMold;
+};
+
+StepLayout make_step_layout(const Shape& sh, int r, int p, int batch, int32_t g_dtype, int32_t flags) {
+    StepLayout sl{};
+    const size_t rs = galore_rsvd_workspace_size(sh.m, sh.n, r, p, batch, g_dtype);
+    sl.strideR = static_cast<int64_t>(r) * sh.l;     // packed: Adam's one-pass kernel applies to contiguous M, V
+    sl.offR = 0;
+    sl.pwsBytes = galore_project_workspace_size(sh.m, sh.n, r, batch, g_dtype);
+    sl.bwsBytes = galore_project_back_workspace_size(sh.m, sh.n, r, batch);
+    sl.offPws = align_up(static_cast<size_t>(batch) * sl.strideR * sizeof(float), kAlign);
+    sl.offBws = sl.offPws + align_up(sl.pwsBytes, kAlign);
+    const size_t x = std::max(rs, sl.offBws + align_up(sl.bwsBytes, kAlign));
+    sl.offSigma = align_up(x, kAlign);
+    size_t off = sl.offSigma + align_up(static_cast<size_t>(batch) * r * sizeof(float), kAlign);
+    sl.stridePold = pad_elems(sh.s * r);
+    sl.strideMold = pad_elems(static_cast<int64_t>(r) * sh.l);
+    sl.offPold = off;
+    if (flags & GALORE_STEP_ALIGN) off += align_up(static_cast<size_t>(batch) * sl.stridePold * sizeof(float), kAlign);
+    sl.offMold = off;
+    sl.offAws = off;
+    if (flags & GALORE_STEP_REEXPRESS) {
+        off += align_up(static_cast<size_t>(batch) * sl.strideMold * sizeof(float), kAlign);
+        sl.offAws = off;
+        sl.awsBytes = galore_align_workspace_size(r, batch);
+        off += align_up(sl.awsBytes, kAlign);
+    }
+    sl.total = off;
+    return sl;
+}
+
+bool step_sizes_ok(int64_t m, int64_t n, int32_t r, int32_t p, int32_t q, int32_t batch, int32_t g_dtype) {
+    if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return false;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return false;
+    return r <= std::min(m, n) && static_cast<int64_t>(r) + p <= kMaxK;
+}
+
+size_t galore_step_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch, int32_t g_dtype,
+                                  int32_t flags) {
+    if (!step_sizes_ok(m, n, r, p, 0, batch, g_dtype)) return 0;
+    if ((flags & ~(GALORE_STEP_ALIGN | GALORE_STEP_REEXPRESS)) != 0) return 0;
+    if ((flags & GALORE_STEP_REEXPRESS) && !(flags & GALORE_STEP_ALIGN)) return 0;
+    return make_step_layout(make_shape(m, n, r, p), r, p, batch, g_dtype, flags).total;
+}
+
+int galore_step(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, float* W,
+                int64_t ldw, int64_t stride_w, float* P, int64_t ldp, int64_t stride_p, float* M, float* V,
+                int64_t ldm, int64_t stride_m, int32_t r, int32_t p, int32_t q, uint64_t seed,
+                uint64_t sketch_index0, int64_t tau, int32_t T, float beta1, float beta2, float eps, float lr,
+                float alpha, int32_t flags, int32_t* info, int32_t batch, void* workspace, size_t workspace_bytes,
+                hipStream_t stream) {
+    if (G == nullptr || W == nullptr || P == nullptr || M == nullptr || V == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
+    if (tau < 0 || T < 1) return GALORE_ERR_INVALID_ARG;
+    if ((flags & ~(GALORE_STEP_ALIGN | GALORE_STEP_REEXPRESS)) != 0) return GALORE_ERR_INVALID_ARG;
+    if ((flags & GALORE_STEP_REEXPRESS) && !(flags & GALORE_STEP_ALIGN)) return GALORE_ERR_INVALID_ARG;
+    if (!finite_f(beta1) || !finite_f(beta2) || !finite_f(eps) || !finite_f(lr) || !finite_f(alpha))
+        return GALORE_ERR_INVALID_ARG;
+    if (beta1 < 0.0f || beta1 >= 1.0f || beta2 < 0.0f || beta2 >= 1.0f || eps <= 0.0f) return GALORE_ERR_INVALID_ARG;
+    const double bc1 = 1.0 - pow(static_cast<double>(beta1), static_cast<double>(tau + 1));
+    const double bc2 = 1.0 - pow(static_cast<double>(beta2), static_cast<double>(tau + 1));
+    if (!(bc1 > 0.0) || !(bc2 > 0.0)) return GALORE_ERR_INVALID_ARG;
+    if (!step_sizes_ok(m, n, r, p, q, batch, g_dtype)) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, p);
+    if (ldg < n || ldw < n || ldp < r || ldm < sh.l) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_g < m * ldg || stride_w < m * ldw || stride_p < sh.s * ldp || stride_m < r * ldm))
+        return GALORE_ERR_SHAPE;
+    const int64_t sg = (batch > 1) ? stride_g : m * ldg;
+    const int64_t sw = (batch > 1) ? stride_w : m * ldw;
+    const int64_t sp = (batch > 1) ? stride_p : sh.s * ldp;
+    const int64_t sm = (batch > 1) ? stride_m : r * ldm;
+    const StepLayout sl = make_step_layout(sh, r, p, batch, g_dtype, flags);
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0) return GALORE_ERR_WORKSPACE;
+    if (workspace_bytes < sl.total) return GALORE_ERR_WORKSPACE;
+    char* ws = static_cast<char*>(workspace);
+    float* R = reinterpret_cast<float*>(ws + sl.offR);
+    float* sigma = reinterpret_cast<float*>(ws + sl.offSigma);
+
+    // Alg. 1: a new projector from the gradient of every T-th step
+    if (tau % T == 0) {
+        const bool align = (flags & GALORE_STEP_ALIGN) && tau > 0;
+        const bool reexpress = align && (flags & GALORE_STEP_REEXPRESS);
+        float* Pold = reinterpret_cast<float*>(ws + sl.offPold);
+        float* Mold = reinterpret_cast<float*>(ws + sl.offMold);
+        if (align)
+            GALORE_TRY(launch_copy_rows(P, ldp, sp, Pold, r, sl.stridePold, static_cast<int>(sh.s), r, batch,
+                                        stream));
+        if (reexpress)
+            GALORE_TRY(launch_copy_rows(M, ldm, sm, Mold, sh.l, sl.strideMold, r, static_cast<int>(sh.l), batch,
+                                        stream));
+        int st = galore_rsvd_update(G, g_dtype, m, n, ldg, sg, r, p, q, seed, sketch_index0, P, ldp, sp, sigma, r,
+                                    info, batch, ws, sl.offSigma, stream);
+        if (st != GALORE_OK) return st;
+        if (align)
+            GALORE_TRY(launch_align(Pold, r, sl.stridePold, P, ldp, sp, static_cast<int>(sh.s), r, nullptr, batch,
+                                    stream));
+        if (reexpress) {
+            st = reexpress_moment(Pold, r, sl.stridePold, P, ldp, sp, sh.s, r, Mold, sh.l, sl.strideMold, M, ldm, sm,
+                                  sh.l, reinterpret_cast<float*>(ws + sl.offAws), batch, stream);
+            if (st != GALORE_OK) return st;
+        }
+    }
+    // R = P^T A; Adam on (M, V) writes N over R; W -= lr alpha P N
+    int st = galore_project(P, ldp, sp, G, g_dtype, m, n, ldg, sg, r, R, sh.l, sl.strideR, batch,
+                            sl.pwsBytes ? ws + sl.offPws : nullptr, sl.pwsBytes, stream);
+    if (st != GALORE_OK) return st;
+    GALORE_TRY(launch_adam2(R, R, sh.l, sl.strideR, M, V, ldm, sm, r, sh.l, batch, beta1, beta2, eps,
+                            static_cast<float>(bc1), static_cast<float>(bc2), stream));
+    return galore_project_back(P, ldp, sp, R, sh.l, sl.strideR, W, m, n, ldw, sw, r, lr, alpha, batch,
+                               ws + sl.offBws, sl.bwsBytes, stream);
 }
 
 }  // extern "C"

@@ -212,3 +212,44 @@ def test_align_rejects():
         assert call(**kw) == -2, kw
     for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
         assert call(**kw) == -3, kw
+
+
+def test_step_workspace_size():
+    import paper_2504_20437_amd as gl
+    import torch
+    base = gl.galore_step_workspace_size(64, 96, 8, 4, 1)
+    rs = gl.galore_rsvd_workspace_size(64, 96, 8, 4, 1)
+    assert base >= rs and base % 256 == 0
+    al = gl.galore_step_workspace_size(64, 96, 8, 4, 1, flags=1)
+    rx = gl.galore_step_workspace_size(64, 96, 8, 4, 1, flags=3)
+    assert al >= base + 64 * 8 * 4 and rx >= al + 8 * 96 * 4
+    assert gl.galore_step_workspace_size(96, 64, 8, 4, 1, flags=3) == rx            # orientation
+    assert gl.galore_step_workspace_size(64, 96, 8, 4, 2, torch.bfloat16) >= gl.galore_rsvd_workspace_size(
+        64, 96, 8, 4, 2, torch.bfloat16)
+    assert gl.galore_step_workspace_size(64, 96, 8, 4, 1, flags=2) == 0             # REEXPRESS needs ALIGN
+    assert gl.galore_step_workspace_size(64, 96, 8, 4, 1, flags=4) == 0
+    assert gl.galore_step_workspace_size(64, 96, 65, 0, 1) == 0
+    assert gl.galore_step_workspace_size(64, 96, 8, 4, 0) == 0
+
+
+def test_step_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_step
+    ws = FAKE - FAKE % 256 + 256
+    need = gl.galore_step_workspace_size(64, 96, 8, 4, 1, flags=3)
+    ok = dict(G=FAKE, dt=0, m=64, n=96, ldg=96, sg=0, W=FAKE, ldw=96, sw=0, P=FAKE, ldp=8, sp=0, M=FAKE, V=FAKE,
+              ldm=96, sm=0, r=8, p=4, q=1, seed=1, idx=0, tau=0, T=10, b1=0.9, b2=0.999, eps=1e-8, lr=1e-3, al=0.25,
+              fl=3, info=None, b=1, ws=ws, wb=need)
+    keys = list(ok)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(*[a[k] for k in keys], None)
+    for kw in (dict(G=NULL), dict(W=NULL), dict(P=NULL), dict(M=NULL), dict(V=NULL), dict(dt=2), dict(tau=-1),
+               dict(T=0), dict(fl=2), dict(fl=8), dict(b1=1.0), dict(b2=-0.5), dict(eps=0.0),
+               dict(lr=float("nan")), dict(al=float("inf"))):
+        assert call(**kw) == -1, kw
+    for kw in (dict(m=0), dict(r=0), dict(r=65), dict(p=-1), dict(q=-1), dict(p=4090), dict(ldg=95), dict(ldw=95),
+               dict(ldp=7), dict(ldm=95), dict(b=0), dict(b=2), dict(b=2, sg=64 * 96, sw=64 * 96, sp=64 * 8)):
+        assert call(**kw) == -2, kw
+    for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
+        assert call(**kw) == -3, kw

@@ -513,3 +513,117 @@ def test_align_exact_cases(gl):
     _, flips, _ = gl.galore_align_projector(dev(E), Fd)
     assert flips.cpu().numpy().tolist() == [0, 1]
     assert host(Fd)[2, 0] == -1.0 and host(Fd)[1, 1] == 1.0
+
+
+# ---------------------------------------------------------------- scheduled step
+
+
+def _step_gradients(m, n, r, b, dtype, steps, seed0):
+    """per step: a batch of planted gradients (gap at r) with fresh singular vectors"""
+    s = min(m, n)
+    spec = gi.spectrum_gapped(gi.spectrum_power(s, 0.8), r) + 1e-3 * gi.spectrum_power(s, 0.0)
+    return [[gi.store(gi.planted_gradient(m, n, spec, 1e-4, seed=seed0 + 10 * t + i), dtype) for i in range(b)]
+            for t in range(steps)]
+
+
+def _dev_batch(Gs):
+    import torch
+    return torch.stack([dev_stored(x) for x in Gs])
+
+
+@pytest.mark.parametrize("m,n,dtype,flags", [(256, 520, "f32", 3), (520, 256, "bf16", 3), (300, 200, "f32", 1),
+                                             (256, 520, "bf16", 0)])
+def test_step_equals_entry_point_sequence(gl, m, n, dtype, flags):
+    """galore_step runs the separate entry points' kernels in Alg. 1's order:
+    five steps with T = 2 equal, bit for bit, the same calls made one by one
+    (subspace update, switch with or without re-expression, projection, Adam
+    with t = tau + 1, back-projection)."""
+    import torch
+    r, p, q, b, T = 24, 8, 1, 2, 2
+    s, l = min(m, n), max(m, n)
+    grads = _step_gradients(m, n, r, b, dtype, 5, 300)
+    W1 = dev(np.stack([gi.weights(m, n, 70 + i) for i in range(b)]))
+    P1 = torch.zeros((b, s, r), device="cuda")
+    M1 = torch.zeros((b, r, l), device="cuda")
+    V1 = torch.zeros_like(M1)
+    W2, P2, M2, V2 = W1.clone(), P1.clone(), M1.clone(), V1.clone()
+    hp = dict(beta1=0.9, beta2=0.999, eps=1e-8, lr=1e-3, alpha=0.25)
+    for tau in range(5):
+        G = _dev_batch(grads[tau])
+        seed = gi.sketch_seed(tau // T)
+        gl.galore_step(G, W1, P1, M1, V1, r, p, q, seed, tau, T, flags=flags, **hp)
+        if tau % T == 0:
+            align = bool(flags & 1) and tau > 0
+            Pold, Mold = P2.clone(), M2.clone()
+            gl.galore_rsvd_update(G, r, p, q, seed, 0, P=P2)
+            if align:
+                gl.galore_align_projector(Pold, P2, Mold if flags & 2 else None, M_out=M2 if flags & 2 else None)
+        R = gl.galore_project(P2, G)
+        gl.galore_lowrank_adam_step(R, M2, V2, R, hp["beta1"], hp["beta2"], hp["eps"], tau + 1)
+        gl.galore_project_back(P2, R, W2, hp["lr"], hp["alpha"])
+        torch.cuda.synchronize()
+        for a, c, nm in ((P1, P2, "P"), (M1, M2, "M"), (V1, V2, "V"), (W1, W2, "W")):
+            assert torch.equal(a, c), (tau, nm)
+
+
+@pytest.mark.parametrize("m,n,dtype", [(256, 520, "f32"), (520, 256, "bf16")])
+def test_step_matches_oracle(gl, orc, m, n, dtype):
+    """Per step against the oracle's Alg. 1 step from the same state: at update
+    steps the new projector is the oracle's (distance <= 1e-3, same column
+    signs after the switch); M, V and the weight change then follow from that
+    projector within first-order bounds of the fp32 projection error
+    |dR| <= 1e-5 |P|^T |A| (Adam's N = m^/(sqrt(v^) + eps) is ill-conditioned
+    where sqrt(v^) is near zero, and the bound on N carries that factor)."""
+    import torch
+    r, p, q, b, T = 24, 8, 2, 2, 2
+    b1, b2, eps, lr, al = 0.9, 0.999, 1e-8, 1e-3, 0.25
+    f32 = lambda x: float(np.float32(x))
+    b1, b2, eps, lr, al = f32(b1), f32(b2), f32(eps), f32(lr), f32(al)
+    s, l = min(m, n), max(m, n)
+    grads = _step_gradients(m, n, r, b, dtype, 5, 500)
+    W = dev(np.stack([gi.weights(m, n, 90 + i) for i in range(b)]))
+    P = torch.zeros((b, s, r), device="cuda")
+    M = torch.zeros((b, r, l), device="cuda")
+    V = torch.zeros_like(M)
+    u = 2.0 ** -24
+    for tau in range(5):
+        Wp, Pp, Mp, Vp = host(W), host(P), host(M), host(V)
+        G = _dev_batch(grads[tau])
+        seed = gi.sketch_seed(tau // T)
+        gl.galore_step(G, W, P, M, V, r, p, q, seed, tau, T, beta1=b1, beta2=b2, eps=eps, lr=lr, alpha=al, flags=3)
+        Wg, Pg, Mg, Vg = host(W), host(P), host(M), host(V)
+        for i in range(b):
+            Gx = grads[tau][i].exact
+            A = Gx if m <= n else Gx.T
+            upd = tau % T == 0
+            if upd:
+                Praw = orc.rsvd_update(Gx, r, p, q, seed, i)[0]
+                Pref = orc.align_projector(Pp[i], Praw)[0] if tau > 0 else Praw
+                assert proj_dist(Pg[i], Pref) <= 1e-3
+                assert np.all(np.einsum("ij,ij->j", Pg[i], Pref) > 0.99)
+            Wo, Po, Mo, Vo = orc.galore_step(Gx, Wp[i], Pp[i] if tau > 0 else None, Mp[i], Vp[i], r, p, q, seed,
+                                              tau, T, i, b1, b2, eps, lr, al, align=True, reexpress=True,
+                                              P_given=Pg[i] if upd else None)
+            assert np.array_equal(Po, Pg[i])          # the switch finds nothing to flip in the GPU's result
+            # first-order error bounds
+            Ro = Po.T @ A
+            dR = 1e-5 * (np.abs(Po).T @ np.abs(A))
+            Mpre = Mp[i]
+            if upd and tau > 0:
+                Mpre = (Po.T @ Pp[i]) @ Mp[i]
+                dMpre = 1e-5 * (np.abs(Po).T @ np.abs(Pp[i])) @ np.abs(Mp[i])
+            else:
+                dMpre = np.zeros_like(Mpre)
+            tolM = b1 * dMpre + (1 - b1) * dR + 4 * u * (b1 * np.abs(Mpre) + (1 - b1) * np.abs(Ro))
+            tolV = (1 - b2) * (2 * np.abs(Ro) * dR + dR ** 2) + 4 * u * (b2 * np.abs(Vp[i]) + (1 - b2) * Ro ** 2)
+            assert np.all(np.abs(Mg[i] - Mo) <= tolM + 1e-30)
+            assert np.all(np.abs(Vg[i] - Vo) <= tolV + 1e-30)
+            bc1, bc2 = 1 - b1 ** (tau + 1), 1 - b2 ** (tau + 1)
+            No = (Mo / bc1) / (np.sqrt(Vo / bc2) + eps)
+            den = eps + np.maximum(0.0, np.sqrt(np.maximum(Vo - tolV, 0.0) / bc2))
+            tolN = (tolM / bc1 + np.abs(No) * np.sqrt(tolV / bc2)) / den + 8 * u * np.abs(No)
+            dWtol = lr * al * (np.abs(Po) @ tolN + 8 * u * (np.abs(Po) @ np.abs(No)))
+            if m > n:
+                dWtol = dWtol.T
+            tolW = dWtol + 2 * u * np.abs(Wo)
+            assert np.all(np.abs(Wg[i] - Wo) <= tolW), (tau, i)
