@@ -20,6 +20,10 @@ What each function follows (paper = "GaLore 2", Su et al. 2025):
   align_projector  subspace switch: signs of a new P matched to the previous P
                    (paper §4.1.3 sign indeterminacy, Alg. 1 schedule), optional
                    first-moment re-expression in the new basis
+  quantize_projector / pack_codes / dequantize_projector
+                   low-bit projector (paper §4.2, after Q-GaLore): symmetric
+                   per-column int8 / int4 codes, decisions in binary32, and the
+                   byte layout the library stores them in
   galore_step      one step of paper Alg. 1: a new projector every T steps
                    (optionally followed by the subspace switch), projection,
                    Adam with bias exponent tau + 1, back-projection
@@ -83,6 +87,9 @@ def _load():
         lib.orc_align_projector.argtypes = [_f64p, _f64p, i64, i64, ctypes.POINTER(ctypes.c_int32), _f64p, _f64p,
                                             i64]
         lib.orc_align_projector.restype = None
+        lib.orc_quantize_projector.argtypes = [_f64p, i64, i64, i32, ctypes.POINTER(ctypes.c_int32),
+                                               ctypes.POINTER(ctypes.c_float)]
+        lib.orc_quantize_projector.restype = None
         _lib = lib
     return _lib
 
@@ -232,3 +239,38 @@ def galore_step(G, W, P, M, V, r: int, p: int, q: int, seed: int, tau: int, T: i
     M, V, N = adam(R, M, V, beta1, beta2, eps, tau + 1)
     W = project_back(P, N, W, lr, alpha)
     return W, P, M, V
+
+
+def quantize_projector(P, bits: int):
+    """(codes (s x r int32), scales (r float32)) of the fp32 projector P: scale_j
+    = max_i |P_ij| / qmax, code = round-half-even(P / scale) clamped to
+    [-qmax, qmax], qmax = 2^(bits-1) - 1, every step in binary32."""
+    assert bits in (4, 8)
+    P = _f64(P)
+    s, r = P.shape
+    codes = np.zeros((s, r), dtype=np.int32)
+    scales = np.zeros(r, dtype=np.float32)
+    _load().orc_quantize_projector(_ptr(P), s, r, bits, codes.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                   scales.ctypes.data_as(ctypes.POINTER(ctypes.c_float)))
+    return codes, scales
+
+
+def dequantize_projector(codes, scales) -> np.ndarray:
+    """code * scale, exact in fp64."""
+    return np.asarray(codes, dtype=np.float64) * np.asarray(scales, dtype=np.float64)[None, :]
+
+
+def pack_codes(codes, bits: int) -> np.ndarray:
+    """The bytes of a row-major s x r code matrix as stored: 8 bits -> one
+    two's-complement byte per code; 4 bits -> two codes per byte, column 2c in
+    the low nibble and 2c + 1 in the high nibble (4-bit two's complement), a
+    zero high nibble when r is odd. Shape (s, ceil(r * bits / 8)), uint8."""
+    codes = np.asarray(codes, dtype=np.int64)
+    s, r = codes.shape
+    if bits == 8:
+        return (codes & 0xFF).astype(np.uint8)
+    out = np.zeros((s, (r + 1) // 2), dtype=np.uint8)
+    for c in range(r):
+        nib = (codes[:, c] & 0xF).astype(np.uint8)
+        out[:, c // 2] |= nib if c % 2 == 0 else (nib << 4).astype(np.uint8)
+    return out

@@ -481,3 +481,36 @@ ORC_API void orc_align_projector(const double* P_old, double* P_new, int64_t s, 
         }
     free(O);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Low-bit projector (paper §4.2: GaLore 2 supports low-bit projection      */
+/* matrices, after Q-GaLore). Reading: symmetric per-column quantisation;   */
+/* qmax = 2^(bits-1) - 1 (127 for 8 bits, 7 for 4 bits);                    */
+/*   scale_j = max_i |P_ij| / qmax,  code_ij = round-half-even(P_ij/scale_j) */
+/* clamped to [-qmax, qmax]; a zero column has scale 0 and codes 0. Every   */
+/* step that decides a code is taken in binary32 (the precision P is held   */
+/* in): the absolute maximum, the division giving the scale, the division   */
+/* P/scale and its rounding. The dequantised projector is code * scale.     */
+/* P: s x r (fp32 values in doubles); codes: s x r ints; scales: r floats.  */
+/* ------------------------------------------------------------------------ */
+ORC_API void orc_quantize_projector(const double* P, int64_t s, int64_t r, int32_t bits, int32_t* codes,
+                                    float* scales) {
+    const int32_t qmax = (1 << (bits - 1)) - 1;
+    for (int64_t j = 0; j < r; ++j) {
+        float amax = 0.0f;
+        for (int64_t i = 0; i < s; ++i) {
+            const float a = fabsf((float)P[i * r + j]);
+            if (a > amax) amax = a;
+        }
+        const float scale = amax / (float)qmax;
+        scales[j] = scale;
+        for (int64_t i = 0; i < s; ++i) {
+            int32_t c = 0;
+            if (scale > 0.0f) {
+                const float q = rintf((float)P[i * r + j] / scale);
+                c = (q > (float)qmax) ? qmax : (q < (float)-qmax) ? -qmax : (int32_t)q;
+            }
+            codes[i * r + j] = c;
+        }
+    }
+}

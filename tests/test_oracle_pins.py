@@ -500,3 +500,67 @@ def test_step_update_lies_in_last_projector_span(orc):
         W = W1
         assert np.linalg.norm(dW - basis @ (basis.T @ dW)) <= 1e-6 * np.linalg.norm(dW)
         assert np.linalg.norm(P @ P.T - basis @ basis.T) < 1e-6
+
+
+# ---------------------------------------------------------------- low-bit projector
+
+
+def test_quantize_hand_example_ties_to_even(orc):
+    """Column 0 has max 127 * 2^-7, so its scale is exactly 2^-7 and the codes
+    are P / 2^-7 rounded half to even: 2.5 -> 2, 3.5 -> 4, -2.5 -> -2,
+    -0.5 -> 0. Column 1 (a single nonzero entry) gets the extreme code."""
+    P = np.array([[127, 1], [2.5, 0], [3.5, 0], [-2.5, 0], [-0.5, 0]], dtype=np.float64) * 2.0 ** -7
+    codes, scales = orc.quantize_projector(P, 8)
+    assert codes[:, 0].tolist() == [127, 2, 4, -2, 0]
+    assert codes[:, 1].tolist() == [127, 0, 0, 0, 0]
+    assert scales[0] == np.float32(2.0 ** -7)
+    codes4, scales4 = orc.quantize_projector(P, 4)
+    assert scales4[0] == np.float32(127 * 2.0 ** -7 / 7)
+    assert codes4[0, 0] == 7 and codes4[0, 1] == 7
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_quantize_exact_grid_and_zero_column(orc, bits):
+    """A projector whose columns lie on a grid c * 2^-e with an entry of
+    magnitude qmax * 2^-e is reproduced exactly (codes and scale); an all-zero
+    column gets scale 0 and codes 0."""
+    qmax = 2 ** (bits - 1) - 1
+    rng = np.random.default_rng(41)
+    s, r = 40, 6
+    c0 = rng.integers(-qmax, qmax + 1, size=(s, r))
+    c0[3, :] = np.where(rng.random(r) < 0.5, qmax, -qmax)
+    e = rng.integers(3, 12, size=r)
+    P = c0 * 2.0 ** -e.astype(np.float64)
+    P[:, 4] = 0.0
+    codes, scales = orc.quantize_projector(P, bits)
+    want = c0.copy()
+    want[:, 4] = 0
+    assert np.array_equal(codes, want)
+    assert scales[4] == 0.0
+    keep = [j for j in range(r) if j != 4]
+    assert np.array_equal(scales[keep], (2.0 ** -e[keep]).astype(np.float32) * np.float32(1.0))
+    assert np.array_equal(orc.dequantize_projector(codes, scales), P)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_quantize_error_bound_and_range(orc, bits):
+    """For a Haar projector: every code lies in [-qmax, qmax], each column's
+    largest-magnitude entry gets +-qmax, and the dequantised value is within
+    half a quantisation step of P (up to the fp32 rounding of P / scale)."""
+    qmax = 2 ** (bits - 1) - 1
+    rng = np.random.default_rng(42)
+    P = _haar(rng, 300, 20).astype(np.float32).astype(np.float64)
+    codes, scales = orc.quantize_projector(P, bits)
+    assert np.abs(codes).max() <= qmax
+    imax = np.argmax(np.abs(P), axis=0)
+    assert np.array_equal(codes[imax, np.arange(20)], (np.sign(P[imax, np.arange(20)]) * qmax).astype(np.int32))
+    err = np.abs(orc.dequantize_projector(codes, scales) - P)
+    assert np.all(err <= 0.5 * scales.astype(np.float64) * (1 + 2.0 ** -20))
+
+
+def test_pack_codes_layout(orc):
+    """8 bits: one two's-complement byte per code. 4 bits: column 2c in the low
+    nibble, 2c + 1 in the high nibble; an odd last column leaves the high nibble
+    zero: [1, -2, 7, -7, 3] -> 0xE1 0x97 0x03."""
+    assert orc.pack_codes(np.array([[1, -2, 7, -7, 3]]), 4).tolist() == [[0xE1, 0x97, 0x03]]
+    assert orc.pack_codes(np.array([[1, -2, 127, -127]]), 8).tolist() == [[0x01, 0xFE, 0x7F, 0x81]]
