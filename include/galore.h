@@ -261,6 +261,67 @@ GALORE_API int galore_align_projector(const float* P_old, int64_t ld_old, int64_
                                       int32_t batch, void* workspace, size_t workspace_bytes,
                                       hipStream_t stream);
 
+/*
+ * Low-bit projector (paper §4.2: GaLore 2 supports low-bit projection
+ * matrices, after Q-GaLore; the paper fixes no scheme). Each column j of the
+ * fp32 s x r projector P is quantised symmetrically:
+ *   qmax = 2^(bits-1) - 1 (127 for bits = 8, 7 for bits = 4)
+ *   scale_j = max_i |P_ij| / qmax            (binary32 division)
+ *   code_ij = P_ij / scale_j rounded half to even, clamped to [-qmax, qmax]
+ * and a zero column gets scale 0 and codes 0; the dequantised projector is
+ * code_ij * scale_j. Codes are row-major: bits = 8 one two's-complement byte
+ * each (ldq >= r bytes); bits = 4 two per byte, column 2c in the low nibble
+ * and 2c + 1 in the high nibble, 4-bit two's complement (ldq >= ceil(r / 2)).
+ * P: fp32 s x r (ld ldp, stride stride_p); Q: device bytes (ld ldq, stride
+ * stride_q); scales: fp32, r per matrix (stride stride_scales). Non-finite
+ * entries of P give unspecified codes.
+ * Errors: NULL pointers, bits not 4 or 8 -> INVALID_ARG; s, r < 1, r > s,
+ * ldp < r, ldq too small, strides too small -> SHAPE.
+ */
+GALORE_API int galore_quantize_projector(const float* P, int64_t ldp, int64_t stride_p, int64_t s, int32_t r,
+                                         int32_t bits, uint8_t* Q, int64_t ldq, int64_t stride_q, float* scales,
+                                         int64_t stride_scales, int32_t batch, hipStream_t stream);
+
+/* Bytes of workspace galore_project_quantized needs (0 for invalid sizes). */
+GALORE_API size_t galore_project_quantized_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch);
+
+/*
+ * Projection with the low-bit projector: R = Pq^T A with Pq = code * scale
+ * (galore_quantize_projector's codes and scales; paper §3 projection). With a
+ * bf16 gradient (16-byte aligned rows, s a multiple of 32 for m <= n) the
+ * codes form one exact bf16 plane, the product runs once on the bf16 matrix
+ * cores with fp32 accumulation and each row of R is multiplied by its scale;
+ * otherwise Pq is rounded to fp32 and the product runs on the fp32 matrix
+ * cores. Shapes and errors as galore_project, plus those of the codes;
+ * the workspace (galore_project_quantized_workspace_size bytes, device,
+ * 256-byte aligned, scratch) is required.
+ */
+GALORE_API int galore_project_quantized(const uint8_t* Q, int64_t ldq, int64_t stride_q, const float* scales,
+                                        int64_t stride_scales, int32_t bits, const void* G, int32_t g_dtype,
+                                        int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
+                                        int64_t ldr, int64_t stride_r, int32_t batch, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
+/* Bytes of workspace galore_project_back_quantized needs (0 for invalid sizes). */
+GALORE_API size_t galore_project_back_quantized_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch);
+
+/*
+ * Back-projection with the low-bit projector: W <- W - (lr * alpha) Pq N (or
+ * its transpose for m > n), Pq = code * scale (paper §3 back-projection). With
+ * r a multiple of 32 and 16-byte aligned planes the scales are folded into the
+ * rows of N (one fp32 rounding), N^T is split into three bf16 planes and the
+ * exact code plane multiplies them on the bf16 matrix cores (three products
+ * instead of six for an fp32 P); otherwise Pq is rounded to fp32 and the fp32
+ * matrix cores run it. Shapes and errors as galore_project_back, plus those of
+ * the codes; the workspace (galore_project_back_quantized_workspace_size bytes,
+ * device, 256-byte aligned, scratch) is required.
+ */
+GALORE_API int galore_project_back_quantized(const uint8_t* Q, int64_t ldq, int64_t stride_q, const float* scales,
+                                             int64_t stride_scales, int32_t bits, const float* N, int64_t ldn,
+                                             int64_t stride_n, float* W, int64_t m, int64_t n, int64_t ldw,
+                                             int64_t stride_w, int32_t r, float lr, float alpha, int32_t batch,
+                                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Options of galore_step (bit flags). */
 typedef enum {
     GALORE_STEP_ALIGN = 1,      /* after each update but the first, match the new projector's column

@@ -26,6 +26,8 @@ EXPORTED = (
     "galore_project_back_workspace_size", "galore_project_back",
     "galore_align_workspace_size", "galore_align_projector",
     "galore_step_workspace_size", "galore_step",
+    "galore_quantize_projector", "galore_project_quantized_workspace_size", "galore_project_quantized",
+    "galore_project_back_quantized_workspace_size", "galore_project_back_quantized",
 )
 
 GALORE_STEP_ALIGN = 1
@@ -82,6 +84,18 @@ def _declare(lib):
     lib.galore_step.argtypes = [vp, i32, i64, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, vp, i64, i64,
                                 i32, i32, i32, u64, u64, i64, i32, f32, f32, f32, f32, f32, i32, vp, i32, vp, sz, vp]
     lib.galore_step.restype = ctypes.c_int
+    lib.galore_quantize_projector.argtypes = [vp, i64, i64, i64, i32, i32, vp, i64, i64, vp, i64, i32, vp]
+    lib.galore_quantize_projector.restype = ctypes.c_int
+    lib.galore_project_quantized_workspace_size.argtypes = [i64, i64, i32, i32]
+    lib.galore_project_quantized_workspace_size.restype = sz
+    lib.galore_project_quantized.argtypes = [vp, i64, i64, vp, i64, i32, vp, i32, i64, i64, i64, i64, i32, vp, i64,
+                                             i64, i32, vp, sz, vp]
+    lib.galore_project_quantized.restype = ctypes.c_int
+    lib.galore_project_back_quantized_workspace_size.argtypes = [i64, i64, i32, i32]
+    lib.galore_project_back_quantized_workspace_size.restype = sz
+    lib.galore_project_back_quantized.argtypes = [vp, i64, i64, vp, i64, i32, vp, i64, i64, vp, i64, i64, i64, i64,
+                                                  i32, f32, f32, i32, vp, sz, vp]
+    lib.galore_project_back_quantized.restype = ctypes.c_int
     return lib
 
 
@@ -331,3 +345,71 @@ def galore_step(G: torch.Tensor, W: torch.Tensor, P: torch.Tensor, M: torch.Tens
                            seed, sketch_index0, tau, T, beta1, beta2, eps, lr, alpha, flags, info.data_ptr(), batch,
                            workspace.data_ptr(), workspace.numel(), _stream(stream)), "galore_step")
     return info
+
+
+class QuantizedProjector:
+    """Codes (uint8, (batch,) s x ldq bytes) and scales (fp32, (batch,) r) of a
+    low-bit projector, as galore_quantize_projector writes them."""
+
+    def __init__(self, codes: torch.Tensor, scales: torch.Tensor, bits: int, r: int):
+        self.codes, self.scales, self.bits, self.r = codes, scales, bits, r
+
+    def _args(self):
+        c = self.codes
+        if c.dim() == 2:
+            return c.data_ptr(), c.stride(0), c.shape[0] * c.stride(0), self.scales.data_ptr(), self.r, self.bits
+        return c.data_ptr(), c.stride(1), c.stride(0), self.scales.data_ptr(), self.scales.stride(0), self.bits
+
+
+def galore_quantize_projector(P: torch.Tensor, bits: int = 8, stream=None) -> QuantizedProjector:
+    """Symmetric per-column int8 / int4 codes and fp32 scales of the fp32 projector P."""
+    if P.dtype != torch.float32:
+        raise ValueError("P must be float32")
+    pp, s, r, ldp, sp, batch = _mat(P, "P")
+    ldq = r if bits == 8 else (r + 1) // 2
+    shape = (batch, s, ldq) if P.dim() == 3 else (s, ldq)
+    codes = torch.empty(shape, dtype=torch.uint8, device=P.device)
+    scales = torch.empty((batch, r) if P.dim() == 3 else (r,), dtype=torch.float32, device=P.device)
+    _check(lib.galore_quantize_projector(pp, ldp, sp, s, r, bits, codes.data_ptr(), ldq, s * ldq, scales.data_ptr(),
+                                         r, batch, _stream(stream)), "galore_quantize_projector")
+    return QuantizedProjector(codes, scales, bits, r)
+
+
+def galore_project_quantized_workspace_size(m: int, n: int, r: int, batch: int = 1) -> int:
+    return int(lib.galore_project_quantized_workspace_size(m, n, r, batch))
+
+
+def galore_project_back_quantized_workspace_size(m: int, n: int, r: int, batch: int = 1) -> int:
+    return int(lib.galore_project_back_quantized_workspace_size(m, n, r, batch))
+
+
+def galore_project_quantized(Pq: QuantizedProjector, G: torch.Tensor, R=None, workspace=None, stream=None):
+    """R = Pq^T A with the low-bit projector ((r, l) or (batch, r, l))."""
+    gp, m, n, ldg, sg, batch = _mat(G, "G")
+    l, r = max(m, n), Pq.r
+    if R is None:
+        R = torch.empty((batch, r, l) if G.dim() == 3 else (r, l), dtype=torch.float32, device=G.device)
+    rp, _, _, ldr, sr, _ = _mat(R, "R")
+    if workspace is None:
+        workspace = torch.empty((max(galore_project_quantized_workspace_size(m, n, r, batch), 1),), dtype=torch.uint8,
+                                device=G.device)
+    qp, ldq, sq, scp, ss, bits = Pq._args()
+    _check(lib.galore_project_quantized(qp, ldq, sq, scp, ss, bits, gp, _dtype_code(G), m, n, ldg, sg, r, rp, ldr,
+                                        sr, batch, workspace.data_ptr(), workspace.numel(), _stream(stream)),
+           "galore_project_quantized")
+    return R
+
+
+def galore_project_back_quantized(Pq: QuantizedProjector, N: torch.Tensor, W: torch.Tensor, lr: float, alpha: float,
+                                  workspace=None, stream=None):
+    """W <- W - lr * alpha * Pq N (transposed for m > n), in place."""
+    np_, r, l, ldn, sn, batch = _mat(N, "N")
+    wp, m, n, ldw, sw, wb = _mat(W, "W")
+    if workspace is None:
+        workspace = torch.empty((max(galore_project_back_quantized_workspace_size(m, n, r, batch), 1),),
+                                dtype=torch.uint8, device=W.device)
+    qp, ldq, sq, scp, ss, bits = Pq._args()
+    _check(lib.galore_project_back_quantized(qp, ldq, sq, scp, ss, bits, np_, ldn, sn, wp, m, n, ldw, sw, r, lr,
+                                             alpha, batch, workspace.data_ptr(), workspace.numel(), _stream(stream)),
+           "galore_project_back_quantized")
+    return W

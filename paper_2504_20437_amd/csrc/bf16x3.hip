@@ -73,16 +73,23 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* src
 // --------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void split3_transpose_kernel(const float* srcb, int64_t lds, int64_t strideS,
                                                                uint16_t* planesb, int64_t ldp, int64_t planeStride,
-                                                               int64_t strideP, int rows, int cols, int rows_pad) {
+                                                               int64_t strideP, int rows, int cols, int rows_pad,
+                                                               const float* rowscaleb, int64_t strideRS) {
     __shared__ float tile[64][65];
     const int b = blockIdx.z;
     const float* src = srcb + static_cast<int64_t>(b) * strideS;
     uint16_t* planes = planesb + static_cast<int64_t>(b) * strideP;
+    const float* rowscale = rowscaleb ? rowscaleb + static_cast<int64_t>(b) * strideRS : nullptr;
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     for (int i = ty; i < 64; i += 4) {
         const int r = r0 + i, c = c0 + tx;
-        tile[i][tx] = (r < rows && c < cols) ? src[static_cast<int64_t>(r) * lds + c] : 0.0f;
+        float x = 0.0f;
+        if (r < rows && c < cols) {
+            x = src[static_cast<int64_t>(r) * lds + c];
+            if (rowscale) x *= rowscale[r];     // one fp32 rounding, then an exact split
+        }
+        tile[i][tx] = x;
     }
     __syncthreads();
     for (int i = ty; i < 64; i += 4) {
@@ -170,6 +177,8 @@ struct Bx3Args {
     int b_upper;                // direct kernel: B upper triangular (B[kk][n] = 0 for kk > n)
     unsigned* cmax;             // direct kernel, row-major C: per-column max of |C| (bits; atomicMax), or null
     int64_t strideCM;
+    const float* nscale;        // direct kernel: C(m, n) scaled by nscale[n] (per matrix at strideNS), or null
+    int64_t strideNS;
 };
 
 __global__ __launch_bounds__(XT, 2) void gemm_bf16x3_kernel(Bx3Args g, int vec) {
@@ -342,14 +351,15 @@ __device__ __forceinline__ void wait_stages(int ahead) {
 // PA = 3: both operands hold three planes (fp32 x fp32): the six products
 // A_i B_j with i + j <= 4 (planes counted from 1); the three left out are below
 // 2^-26 of |A||B| in size, under fp32 rounding.
-template <int YK, int S, bool AT, int PA>
-__global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
+template <int YK, int S, bool AT, int PA, int PB = 3>
+__global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
     static_assert(!AT || YK == 32, "the M-contiguous A stage assumes 32-deep stages");
     static_assert(PA == 1 || (PA == 3 && !AT), "three A planes are K-contiguous");
+    static_assert(PB == 3 || (PB == 1 && PA == 1), "one B plane pairs with one A plane");
     constexpr int CPR = YK / 8;                          // 16-byte chunks per row
     constexpr int RB = YK * 2;                           // bytes per row
     constexpr int kStageA = PA * YM * RB;
-    constexpr int kStageB = 3 * YN * RB;
+    constexpr int kStageB = PB * YN * RB;
     constexpr int kStage = kStageA + kStageB;
     constexpr int LA = kStageA / 1024 / (YT / 64);       // direct loads per wave per stage (1 KB each)
     constexpr int LB = kStageB / 1024 / (YT / 64);
@@ -440,7 +450,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
 #pragma unroll
         for (int ks = 0; ks < YK / 16; ++ks) {
             const int c = 2 * ks + lk;
-            bf16x8 a[PA][4], bq[3][2];
+            bf16x8 a[PA][4], bq[PB][2];
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
                 if constexpr (AT) {
@@ -470,7 +480,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
                 }
             }
 #pragma unroll
-            for (int p = 0; p < 3; ++p)
+            for (int p = 0; p < PB; ++p)
 #pragma unroll
                 for (int y = 0; y < 2; ++y) {
                     const int r = wn * 64 + 32 * y + l32;
@@ -479,7 +489,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
                 }
             if constexpr (PA == 1) {
 #pragma unroll
-                for (int p = 0; p < 3; ++p)
+                for (int p = 0; p < PB; ++p)
 #pragma unroll
                     for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -510,12 +520,13 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
             for (int y = 0; y < 2; ++y) {
                 const int c = col0 + wn * 64 + 32 * y + l32;
                 if (c >= N) continue;
+                const float al = g.nscale ? alpha * g.nscale[static_cast<int64_t>(bz) * g.strideNS + c] : alpha;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int r = row0 + wm * 128 + 32 * x + 8 * q + 4 * lk;
                     float* dst = C + static_cast<int64_t>(c) * g.ldc + r;
-                    f32x4 val = {alpha * acc[x][y][4 * q], alpha * acc[x][y][4 * q + 1], alpha * acc[x][y][4 * q + 2],
-                                 alpha * acc[x][y][4 * q + 3]};
+                    f32x4 val = {al * acc[x][y][4 * q], al * acc[x][y][4 * q + 1], al * acc[x][y][4 * q + 2],
+                                 al * acc[x][y][4 * q + 3]};
                     if (v4 && r + 4 <= M) {
                         if (beta != 0.0f) {
                             const f32x4 old = *reinterpret_cast<const f32x4*>(dst);
@@ -539,12 +550,13 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + 3 * YN) * YK * 2 <= 81920) ? 2 
 #pragma unroll
         for (int y = 0; y < 2; ++y) {
             const int c = col0 + wn * 64 + 32 * y + l32;
+            const float al = (g.nscale && c < N) ? alpha * g.nscale[static_cast<int64_t>(bz) * g.strideNS + c] : alpha;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int r = row0 + wm * 128 + 32 * x + (v & 3) + 8 * (v >> 2) + 4 * lk;
                 if (r < M && c < N) {
                     float* dst = C + static_cast<int64_t>(r) * g.ldc + c;
-                    float val = alpha * acc[x][y][v];
+                    float val = al * acc[x][y][v];
                     if (beta != 0.0f) val += beta * (*dst);
                     *dst = val;
                     mx[y] = max(mx[y], __float_as_uint(fabsf(val)));
@@ -599,10 +611,11 @@ hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, 
 
 hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
                                    int64_t planeStride, int64_t strideP, int rows, int cols, int rows_pad,
-                                   int batch, hipStream_t stream) {
+                                   int batch, hipStream_t stream, const float* rowscale, int64_t strideRS) {
     dim3 grid((cols + 63) / 64, (rows_pad + 63) / 64, batch);
     hipLaunchKernelGGL(split3_transpose_kernel, grid, dim3(256), 0, stream, src, lds, strideS,
-                       static_cast<uint16_t*>(planes), ldp, planeStride, strideP, rows, cols, rows_pad);
+                       static_cast<uint16_t*>(planes), ldp, planeStride, strideP, rows, cols, rows_pad, rowscale,
+                       strideRS);
     return hipGetLastError();
 }
 
@@ -619,9 +632,11 @@ bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* B
 hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
                               int64_t ldb, int64_t planeStride, int64_t strideB, float* C, int64_t ldc,
                               int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
-                              hipStream_t stream, unsigned* cmax, int64_t strideCM) {
+                              hipStream_t stream, unsigned* cmax, int64_t strideCM, int planesB, const float* nscale,
+                              int64_t strideNS) {
     if (M <= 0 || N <= 0 || batch <= 0) return hipSuccess;
-    Bx3Args g;
+    if (planesB != 1 && planesB != 3) return hipErrorInvalidValue;
+    Bx3Args g{};
     g.A = static_cast<const uint16_t*>(A);
     g.lda = lda;
     g.strideA = strideA;
@@ -642,16 +657,26 @@ hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a
     g.b_upper = 0;
     g.cmax = c_trans ? nullptr : cmax;
     g.strideCM = strideCM;
+    g.nscale = nscale;
+    g.strideNS = strideNS;
     if (bf16x3_direct_ok(A, lda, strideA, Bplanes, ldb, planeStride, strideB, M, K, batch, a_mcontig)) {
         dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
-        if (a_mcontig)
+        if (planesB == 1) {
+            if (a_mcontig)
+                hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<32, kDirectST, true, 1, 1>), grid, dim3(YT), 0, stream, g);
+            else
+                hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false, 1, 1>), grid, dim3(YT), 0,
+                                   stream, g);
+        } else if (a_mcontig) {
             hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<32, kDirectST, true, 1>), grid, dim3(YT), 0, stream, g);
-        else
+        } else {
             hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kDirectK, kDirectS, false, 1>), grid, dim3(YT), 0, stream, g);
+        }
         return hipGetLastError();
     }
-    // the register-staged kernel: K-contiguous A, row-major C only, no column maxima
-    if (a_mcontig || c_trans || cmax != nullptr) return hipErrorInvalidValue;
+    // the register-staged kernel: K-contiguous A, three B planes, row-major C only,
+    // no column maxima or scales
+    if (a_mcontig || c_trans || cmax != nullptr || planesB != 3 || nscale != nullptr) return hipErrorInvalidValue;
     const int vec = (lda % 8 == 0) && (ldb % 8 == 0) && (planeStride % 8 == 0) &&
                     (batch == 1 || (strideA % 8 == 0 && strideB % 8 == 0)) &&
                     (reinterpret_cast<uintptr_t>(A) % 16 == 0) && (reinterpret_cast<uintptr_t>(Bplanes) % 16 == 0);
@@ -689,7 +714,7 @@ hipError_t launch_gemm_bf16x6(const void* Aplanes, int64_t lda, int64_t planeStr
     if (M <= 0 || N <= 0 || batch <= 0) return hipSuccess;
     if (!bf16x6_ok(Aplanes, lda, planeStrideA, strideA, Bplanes, ldb, planeStrideB, strideB, K, batch))
         return hipErrorInvalidValue;
-    Bx3Args g;
+    Bx3Args g{};
     g.A = static_cast<const uint16_t*>(Aplanes);
     g.lda = lda;
     g.strideA = strideA;

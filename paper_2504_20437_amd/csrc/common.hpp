@@ -127,6 +127,18 @@ hipError_t launch_adam(const float* R, float* M, float* V, float* N, int64_t row
 hipError_t launch_adam2(const float* R, float* N, int64_t ldrn, int64_t srn, float* M, float* V, int64_t ldmv,
                         int64_t smv, int64_t rows, int64_t cols, int batch, float beta1, float beta2, float eps,
                         float bc1, float bc2, hipStream_t stream);
+// Low-bit projector (quant.hip): codes of the s x r projector, 8 bits (one
+// byte each) or 4 bits (two per byte, even column in the low nibble).
+hipError_t launch_quantize(const float* P, int64_t ldp, int64_t strideP, int rows, int r, int bits, uint8_t* Q,
+                           int64_t ldq, int64_t strideQ, float* scales, int64_t strideS, int batch, hipStream_t stream);
+// bf16 plane of the codes: rows x cols_pad (zero past r), or transposed
+// r x rows_pad (zero past rows)
+hipError_t launch_codes_plane(const uint8_t* Q, int64_t ldq, int64_t strideQ, int bits, int rows, int r, uint16_t* plane,
+                              int64_t ldpl, int64_t stridePl, int pad, bool transpose, int batch, hipStream_t stream);
+// fp32 dequantised projector code * scale (rows x r, ld ldt)
+hipError_t launch_dequantize(const uint8_t* Q, int64_t ldq, int64_t strideQ, int bits, const float* scales,
+                             int64_t strideS, int rows, int r, float* Pt, int64_t ldt, int64_t strideT, int batch,
+                             hipStream_t stream);
 hipError_t launch_copy_rows(const float* src, int64_t lds, int64_t strideS, float* dst, int64_t ldd,
                             int64_t strideD, int rows, int cols, int batch, hipStream_t stream);
 
@@ -135,7 +147,8 @@ hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, 
                                  int64_t strideD, int rows, int cols, int batch, hipStream_t stream);
 hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
                                    int64_t planeStride, int64_t strideP, int rows, int cols, int rows_pad,
-                                   int batch, hipStream_t stream);
+                                   int batch, hipStream_t stream, const float* rowscale = nullptr,
+                                   int64_t strideRS = 0);
 // C (M x N, or its transpose when c_trans) = alpha A B + beta C with A bf16
 // (rows K-contiguous, A[i * lda + kk], or M-contiguous when a_mcontig,
 // A[kk * lda + i]) and B given as three bf16 planes, each N x K rows.
@@ -149,7 +162,8 @@ bool bf16x3_direct_ok(const void* A, int64_t lda, int64_t strideA, const void* B
 hipError_t launch_gemm_bf16x3(const void* A, int64_t lda, int64_t strideA, int a_mcontig, const void* Bplanes,
                               int64_t ldb, int64_t planeStride, int64_t strideB, float* C, int64_t ldc,
                               int64_t strideC, int c_trans, int M, int N, int K, float alpha, float beta, int batch,
-                              hipStream_t stream, unsigned* cmax = nullptr, int64_t strideCM = 0);
+                              hipStream_t stream, unsigned* cmax = nullptr, int64_t strideCM = 0, int planesB = 3,
+                              const float* nscale = nullptr, int64_t strideNS = 0);
 
 // fp32 x fp32 products on the bf16 matrix cores: both operands given as three
 // bf16 planes with K-contiguous rows (A: M rows, B: N rows), six plane products

@@ -862,6 +862,143 @@ int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const flo
     return GALORE_OK;
 }
 
+// ---- low-bit projector ------------------------------------------------------
+
+bool codes_shape_ok(int64_t s, int32_t r, int32_t bits, int64_t ldq) {
+    return ldq >= ((bits == 8) ? r : (static_cast<int64_t>(r) + 1) / 2) && s <= INT32_MAX;
+}
+
+int galore_quantize_projector(const float* P, int64_t ldp, int64_t stride_p, int64_t s, int32_t r, int32_t bits,
+                              uint8_t* Q, int64_t ldq, int64_t stride_q, float* scales, int64_t stride_scales,
+                              int32_t batch, hipStream_t stream) {
+    if (P == nullptr || Q == nullptr || scales == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (bits != 8 && bits != 4) return GALORE_ERR_INVALID_ARG;
+    if (s < 1 || r < 1 || r > s || batch < 1 || ldp < r || !codes_shape_ok(s, r, bits, ldq)) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_p < s * ldp || stride_q < s * ldq || stride_scales < r)) return GALORE_ERR_SHAPE;
+    GALORE_TRY(launch_quantize(P, ldp, (batch > 1) ? stride_p : s * ldp, static_cast<int>(s), r, bits, Q, ldq,
+                               (batch > 1) ? stride_q : s * ldq, scales, (batch > 1) ? stride_scales : r, batch,
+                               stream));
+    return GALORE_OK;
+}
+
+// Workspace of the low-bit projection and back-projection: the bf16 plane of
+// the codes (and, for the back-projection, three bf16 planes of the
+// scale-folded N^T), or the fp32 dequantised projector on the fp32 path; one
+// region serves whichever path runs.
+struct QuantLayout {
+    int64_t ldpl, plane, planeN, strideT;
+    size_t offN, total;
+};
+
+QuantLayout make_quant_layout(const Shape& sh, int r, int batch, bool back) {
+    QuantLayout q{};
+    q.strideT = pad_elems(sh.s * r);
+    const size_t fp32_path = align_up(static_cast<size_t>(batch) * q.strideT * sizeof(float), kAlign);
+    if (back) {
+        q.ldpl = pad8(r);
+        q.plane = pad_elems(sh.s * q.ldpl);
+        q.planeN = pad_elems(sh.l * q.ldpl);
+        q.offN = align_up(static_cast<size_t>(batch) * q.plane * sizeof(uint16_t), kAlign);
+        q.total = std::max(fp32_path, q.offN + align_up(static_cast<size_t>(batch) * 3 * q.planeN * sizeof(uint16_t),
+                                                        kAlign));
+    } else {
+        q.ldpl = pad8(sh.s);
+        q.plane = pad_elems(static_cast<int64_t>(r) * q.ldpl);
+        q.total = std::max(fp32_path, align_up(static_cast<size_t>(batch) * q.plane * sizeof(uint16_t), kAlign));
+    }
+    return q;
+}
+
+size_t galore_project_quantized_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch) {
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX || r > std::min(m, n)) return 0;
+    return make_quant_layout(make_shape(m, n, r, 0), r, batch, false).total;
+}
+
+size_t galore_project_back_quantized_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch) {
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX || r > std::min(m, n)) return 0;
+    return make_quant_layout(make_shape(m, n, r, 0), r, batch, true).total;
+}
+
+int galore_project_quantized(const uint8_t* Q, int64_t ldq, int64_t stride_q, const float* scales,
+                             int64_t stride_scales, int32_t bits, const void* G, int32_t g_dtype, int64_t m, int64_t n,
+                             int64_t ldg, int64_t stride_g, int32_t r, float* R, int64_t ldr, int64_t stride_r,
+                             int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (Q == nullptr || scales == nullptr || G == nullptr || R == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (bits != 8 && bits != 4) return GALORE_ERR_INVALID_ARG;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s || ldg < n || ldr < sh.l || !codes_shape_ok(sh.s, r, bits, ldq)) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_q < sh.s * ldq || stride_scales < r || stride_g < m * ldg || stride_r < r * ldr))
+        return GALORE_ERR_SHAPE;
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0) return GALORE_ERR_WORKSPACE;
+    const QuantLayout ql = make_quant_layout(sh, r, batch, false);
+    if (workspace_bytes < ql.total) return GALORE_ERR_WORKSPACE;
+    const int64_t sq = (batch > 1) ? stride_q : sh.s * ldq;
+    const int64_t ss = (batch > 1) ? stride_scales : r;
+    if (g_dtype == GALORE_BF16) {
+        uint16_t* plane = static_cast<uint16_t*>(workspace);
+        const int a_mc = sh.left ? 1 : 0;
+        if (bf16x3_direct_ok(G, ldg, stride_g, plane, ql.ldpl, 0, ql.plane, static_cast<int>(sh.l),
+                             static_cast<int>(sh.s), batch, a_mc)) {
+            // R^T (l x r) = A^T (codes^T)^T on the bf16 matrix cores, one plane of
+            // exact codes, each column of R^T (row of R) times its scale
+            GALORE_TRY(launch_codes_plane(Q, ldq, sq, bits, static_cast<int>(sh.s), r, plane, ql.ldpl, ql.plane,
+                                          static_cast<int>(ql.ldpl), true, batch, stream));
+            GALORE_TRY(launch_gemm_bf16x3(G, ldg, stride_g, a_mc, plane, ql.ldpl, 0, ql.plane, R, ldr, stride_r, 1,
+                                          static_cast<int>(sh.l), r, static_cast<int>(sh.s), 1.0f, 0.0f, batch,
+                                          stream, nullptr, 0, 1, scales, ss));
+            return GALORE_OK;
+        }
+    }
+    float* Pt = static_cast<float*>(workspace);
+    GALORE_TRY(launch_dequantize(Q, ldq, sq, bits, scales, ss, static_cast<int>(sh.s), r, Pt, r, ql.strideT, batch,
+                                 stream));
+    return galore_project(Pt, r, ql.strideT, G, g_dtype, m, n, ldg, stride_g, r, R, ldr, stride_r, batch, nullptr, 0,
+                          stream);
+}
+
+int galore_project_back_quantized(const uint8_t* Q, int64_t ldq, int64_t stride_q, const float* scales,
+                                  int64_t stride_scales, int32_t bits, const float* N, int64_t ldn, int64_t stride_n,
+                                  float* W, int64_t m, int64_t n, int64_t ldw, int64_t stride_w, int32_t r, float lr,
+                                  float alpha, int32_t batch, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+    if (Q == nullptr || scales == nullptr || N == nullptr || W == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (bits != 8 && bits != 4) return GALORE_ERR_INVALID_ARG;
+    if (!finite_f(lr) || !finite_f(alpha)) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s || ldn < sh.l || ldw < n || !codes_shape_ok(sh.s, r, bits, ldq)) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_q < sh.s * ldq || stride_scales < r || stride_n < r * ldn || stride_w < m * ldw))
+        return GALORE_ERR_SHAPE;
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0) return GALORE_ERR_WORKSPACE;
+    const QuantLayout ql = make_quant_layout(sh, r, batch, true);
+    if (workspace_bytes < ql.total) return GALORE_ERR_WORKSPACE;
+    const int64_t sq = (batch > 1) ? stride_q : sh.s * ldq;
+    const int64_t ss = (batch > 1) ? stride_scales : r;
+    uint16_t* plane = static_cast<uint16_t*>(workspace);
+    uint16_t* npl = reinterpret_cast<uint16_t*>(static_cast<char*>(workspace) + ql.offN);
+    if (bf16x3_direct_ok(plane, ql.ldpl, ql.plane, npl, ql.ldpl, ql.planeN, 3 * ql.planeN, static_cast<int>(sh.s), r,
+                         batch, 0)) {
+        // W (s x l, or its transpose) += -(lr alpha) codes (diag(scale) N): one
+        // exact plane of codes against three planes of the scale-folded N^T
+        GALORE_TRY(launch_codes_plane(Q, ldq, sq, bits, static_cast<int>(sh.s), r, plane, ql.ldpl, ql.plane,
+                                      static_cast<int>(ql.ldpl), false, batch, stream));
+        GALORE_TRY(launch_split3_transpose(N, ldn, (batch > 1) ? stride_n : r * ldn, npl, ql.ldpl, ql.planeN,
+                                           3 * ql.planeN, r, static_cast<int>(sh.l), static_cast<int>(ql.ldpl), batch,
+                                           stream, scales, ss));
+        GALORE_TRY(launch_gemm_bf16x3(plane, ql.ldpl, ql.plane, 0, npl, ql.ldpl, ql.planeN, 3 * ql.planeN, W, ldw,
+                                      (batch > 1) ? stride_w : m * ldw, sh.left ? 0 : 1, static_cast<int>(sh.s),
+                                      static_cast<int>(sh.l), r, -(lr * alpha), 1.0f, batch, stream));
+        return GALORE_OK;
+    }
+    float* Pt = static_cast<float*>(workspace);
+    GALORE_TRY(launch_dequantize(Q, ldq, sq, bits, scales, ss, static_cast<int>(sh.s), r, Pt, r, ql.strideT, batch,
+                                 stream));
+    return galore_project_back(Pt, r, ql.strideT, N, ldn, stride_n, W, m, n, ldw, stride_w, r, lr, alpha, batch,
+                               nullptr, 0, stream);
+}
+
 // Workspace of one scheduled step. Region X holds the subspace update's
 // workspace, reused after it for the projected gradient R (= N, packed
 // r x l) and the projection and back-projection planes; region Y holds what

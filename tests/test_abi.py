@@ -253,3 +253,68 @@ def test_step_rejects():
         assert call(**kw) == -2, kw
     for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
         assert call(**kw) == -3, kw
+
+
+def test_quantized_workspace_sizes():
+    import paper_2504_20437_amd as gl
+    pw = gl.galore_project_quantized_workspace_size(64, 96, 8, 1)
+    bw = gl.galore_project_back_quantized_workspace_size(64, 96, 8, 1)
+    assert pw >= 64 * 8 * 4 and pw % 256 == 0            # holds the fp32 dequantised projector
+    assert bw >= 64 * 8 * 2 + 3 * 96 * 8 * 2 and bw % 256 == 0
+    assert gl.galore_project_quantized_workspace_size(96, 64, 8, 1) == pw
+    assert gl.galore_project_quantized_workspace_size(64, 96, 65, 1) == 0
+    assert gl.galore_project_back_quantized_workspace_size(64, 96, 8, 0) == 0
+
+
+def test_quantize_projector_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_quantize_projector
+    ok = dict(P=FAKE, ldp=8, sp=0, s=64, r=8, bits=8, Q=FAKE, ldq=8, sq=0, sc=FAKE, ss=0, b=1)
+    keys = list(ok)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(*[a[k] for k in keys], None)
+    for kw in (dict(P=NULL), dict(Q=NULL), dict(sc=NULL), dict(bits=2), dict(bits=16)):
+        assert call(**kw) == -1, kw
+    for kw in (dict(s=0), dict(r=0), dict(r=65), dict(ldp=7), dict(ldq=7), dict(bits=4, ldq=3), dict(b=0), dict(b=2),
+               dict(b=2, sp=512, sq=512, ss=7)):
+        assert call(**kw) == -2, kw
+
+
+def test_project_quantized_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_project_quantized
+    ws = FAKE - FAKE % 256 + 256
+    need = gl.galore_project_quantized_workspace_size(64, 96, 8, 1)
+    ok = dict(Q=FAKE, ldq=8, sq=0, sc=FAKE, ss=0, bits=8, G=FAKE, dt=0, m=64, n=96, ldg=96, sg=0, r=8, R=FAKE,
+              ldr=96, sr=0, b=1, ws=ws, wb=need)
+    keys = list(ok)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(*[a[k] for k in keys], None)
+    for kw in (dict(Q=NULL), dict(sc=NULL), dict(G=NULL), dict(R=NULL), dict(bits=3), dict(dt=5)):
+        assert call(**kw) == -1, kw
+    for kw in (dict(m=0), dict(r=65), dict(ldg=95), dict(ldr=95), dict(ldq=7), dict(bits=4, ldq=3), dict(b=2)):
+        assert call(**kw) == -2, kw
+    for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
+        assert call(**kw) == -3, kw
+
+
+def test_project_back_quantized_rejects():
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_project_back_quantized
+    ws = FAKE - FAKE % 256 + 256
+    need = gl.galore_project_back_quantized_workspace_size(64, 96, 8, 1)
+    ok = dict(Q=FAKE, ldq=8, sq=0, sc=FAKE, ss=0, bits=8, N=FAKE, ldn=96, sn=0, W=FAKE, m=64, n=96, ldw=96, sw=0,
+              r=8, lr=1e-3, al=0.25, b=1, ws=ws, wb=need)
+    keys = list(ok)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(*[a[k] for k in keys], None)
+    for kw in (dict(Q=NULL), dict(sc=NULL), dict(N=NULL), dict(W=NULL), dict(bits=1), dict(lr=float("nan")),
+               dict(al=float("inf"))):
+        assert call(**kw) == -1, kw
+    for kw in (dict(m=0), dict(r=65), dict(ldn=95), dict(ldw=95), dict(ldq=7), dict(b=2)):
+        assert call(**kw) == -2, kw
+    for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
+        assert call(**kw) == -3, kw

@@ -627,3 +627,82 @@ def test_step_matches_oracle(gl, orc, m, n, dtype):
                 dWtol = dWtol.T
             tolW = dWtol + 2 * u * np.abs(Wo)
             assert np.all(np.abs(Wg[i] - Wo) <= tolW), (tau, i)
+
+
+# ---------------------------------------------------------------- low-bit projector
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("s,r,batch", [(300, 37, 1), (1024, 128, 2), (64, 1, 1), (200, 64, 3)])
+def test_quantize_projector_matches_oracle(gl, orc, bits, s, r, batch):
+    """Codes (as stored bytes) and scales are bit-exact: both sides take every
+    deciding step in binary32."""
+    rng = np.random.default_rng(s * 3 + r + bits)
+    Ps = [_haar(rng, s, r).astype(np.float32) for _ in range(batch)]
+    if r > 3:
+        Ps[0][:, 2] = 0.0                                              # zero column
+        Ps[0][:5, 3] = np.array([127, 2.5, 3.5, -2.5, -0.5]) * 2.0 ** -7   # ties
+        Ps[0][5:, 3] = 0.0
+    Pd = dev(np.stack(Ps)) if batch > 1 else dev(Ps[0])
+    q = gl.galore_quantize_projector(Pd, bits)
+    codes = q.codes.cpu().numpy().reshape(batch, s, -1)
+    scales = q.scales.cpu().numpy().reshape(batch, r)
+    for i in range(batch):
+        c, sc = orc.quantize_projector(Ps[i], bits)
+        assert np.array_equal(codes[i], orc.pack_codes(c, bits))
+        assert np.array_equal(scales[i].view(np.uint32), sc.view(np.uint32))
+
+
+def _qcase(orc, rng, s, r, bits):
+    P = _haar(rng, s, r).astype(np.float32)
+    c, sc = orc.quantize_projector(P, bits)
+    return P, orc.dequantize_projector(c, sc)
+
+
+# bf16 cases with s a multiple of 32 run on the bf16 matrix cores (one plane of
+# codes), the others through the fp32 dequantised projector
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("m,n,r,dtype", [(256, 688, 32, "bf16"), (688, 256, 64, "bf16"), (300, 517, 37, "bf16"),
+                                         (300, 517, 37, "f32"), (517, 300, 20, "f32"), (1024, 2048, 128, "bf16")])
+def test_project_quantized_matches_oracle(gl, orc, bits, m, n, r, dtype):
+    """R = Pq^T A with Pq the oracle's dequantised projector, within 1e-5 of
+    |Pq|^T |A| elementwise (fp32 accumulation of exact products)."""
+    s = min(m, n)
+    rng = np.random.default_rng(m + 2 * n + r)
+    G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.8), 1e-4, seed=m + n), dtype)
+    P, Pq = _qcase(orc, rng, s, r, bits)
+    q = gl.galore_quantize_projector(dev(P), bits)
+    R = host(gl.galore_project_quantized(q, dev_stored(G)))
+    ref = orc.project(Pq, G.exact)
+    A = G.exact if m <= n else G.exact.T
+    assert np.all(np.abs(R - ref) <= 1e-5 * (np.abs(Pq).T @ np.abs(A)) + 1e-30)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("m,n,r,batch", [(256, 688, 32, 1), (688, 256, 64, 2), (300, 300, 17, 1),
+                                         (1024, 2048, 128, 1), (2048, 1024, 96, 2)])
+def test_project_back_quantized_matches_oracle(gl, orc, bits, m, n, r, batch):
+    """The weight change -(lr alpha) Pq N (transposed for m > n) within 1e-5 of
+    lr alpha |Pq| |N| elementwise (with W = 0 the result is the change itself)."""
+    import torch
+    s, l = min(m, n), max(m, n)
+    rng = np.random.default_rng(m * 7 + n + bits)
+    cases = [_qcase(orc, rng, s, r, bits) for _ in range(batch)]
+    Ns = [rng.standard_normal((r, l)).astype(np.float32) for _ in range(batch)]
+    Pd = dev(np.stack([c[0] for c in cases]))
+    Nd = dev(np.stack(Ns))
+    Wd = torch.zeros((batch, m, n), dtype=torch.float32, device="cuda")
+    if batch == 1:
+        Pd, Nd, Wd = Pd[0], Nd[0], Wd[0]
+    q = gl.galore_quantize_projector(Pd, bits)
+    lr, al = float(np.float32(1e-3)), float(np.float32(0.25))
+    gl.galore_project_back_quantized(q, Nd, Wd, lr, al)
+    out = host(Wd).reshape(batch, m, n)
+    c = float(np.float32(np.float32(lr) * np.float32(al)))
+    for i in range(batch):
+        Pq, N = cases[i][1], Ns[i].astype(np.float64)
+        ref = orc.project_back(Pq, N, np.zeros((m, n)), lr, al)
+        bound = c * (np.abs(Pq) @ np.abs(N))
+        if m > n:
+            bound = bound.T
+        assert np.all(np.abs(out[i] - ref) <= 1e-5 * bound + 1e-30)
