@@ -437,6 +437,35 @@ def main():
     plain_ms = win[1].elapsed_time(win[10]) / 9.0
     del sws
 
+    # low-bit projector: quantise the batch's projectors once per update, then
+    # each step projects and back-projects with the codes
+    lowbit = {}
+    for bits in (8, 4):
+        qws = torch.empty((gl.galore_project_quantized_workspace_size(m, n, r, B),), dtype=torch.uint8, device=dev)
+        qbws = torch.empty((gl.galore_project_back_quantized_workspace_size(m, n, r, B),), dtype=torch.uint8,
+                           device=dev)
+        qe = [mk() for _ in range(8)]
+        for j in range(2):       # the second pass is timed
+            qe[0].record(stream)
+            Pq = gl.galore_quantize_projector(P, bits, stream=stream)
+            qe[1].record(stream)
+            gl.galore_project_quantized(Pq, G, R=R, workspace=qws, stream=stream)
+            qe[2].record(stream)
+            gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, 2, stream=stream)
+            qe[3].record(stream)
+            gl.galore_project_back_quantized(Pq, N, W, 1e-3, 0.25, workspace=qbws, stream=stream)
+            qe[4].record(stream)
+        torch.cuda.synchronize()
+        lowbit["int%d" % bits] = {
+            "quantize_ms": round(qe[0].elapsed_time(qe[1]), 3),
+            "project_ms": round(qe[1].elapsed_time(qe[2]), 3),
+            "adam_ms": round(qe[2].elapsed_time(qe[3]), 3),
+            "project_back_ms": round(qe[3].elapsed_time(qe[4]), 3),
+            "step_ms": round(qe[1].elapsed_time(qe[4]), 3),
+            "projector_bytes": int(Pq.codes.numel() + 4 * Pq.scales.numel()),
+        }
+        del qws, qbws, Pq
+
     out = {
         "metric": "rSVD subspace updates/sec at 4096x11008 r=1024; low-rank Adam step HBM GB/s",
         "value": round(B / (ms_per_step * 1e-3), 3),
@@ -465,6 +494,9 @@ def main():
                      "amortised_step_ms": round((upd_ms + (T_sched - 1) * plain_ms) / T_sched, 3),
                      "note": "galore_step on the whole batch: the update step (subspace update, switch with "
                              "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
+        "lowbit_projector": dict(lowbit, note="steps on a fixed projector with its int8 / int4 codes (whole batch): "
+                                               "projection, Adam, back-projection; fp32 projector bytes %d"
+                                               % (4 * B * s * r)),
         "switch_ms": round(switch_ms, 3),
         "switch_note": ("subspace switch of the whole batch (sign alignment + first-moment re-expression), "
                         "once per T steps: %.4f ms per step at T=200" % (switch_ms / 200.0)),
