@@ -24,6 +24,12 @@ What each function follows (paper = "GaLore 2", Su et al. 2025):
                    low-bit projector (paper §4.2, after Q-GaLore): symmetric
                    per-column int8 / int4 codes, decisions in binary32, and the
                    byte layout the library stores them in
+  fp8_encode / fp8_decode
+                   OCP 8-bit floating point E4M3 (fmt 0) and E5M2 (fmt 1),
+                   round half to even with saturation
+  adam8            8-bit block-wise low-rank Adam (paper §4.2, after the
+                   8-bit Adam of Dettmers et al.): M in E4M3, V in E5M2, one
+                   binary32 scale per block
   galore_step      one step of paper Alg. 1: a new projector every T steps
                    (optionally followed by the subspace switch), projection,
                    Adam with bias exponent tau + 1, back-projection
@@ -90,6 +96,14 @@ def _load():
         lib.orc_quantize_projector.argtypes = [_f64p, i64, i64, i32, ctypes.POINTER(ctypes.c_int32),
                                                ctypes.POINTER(ctypes.c_float)]
         lib.orc_quantize_projector.restype = None
+        lib.orc_fp8_encode.argtypes = [ctypes.c_float, i32]
+        lib.orc_fp8_encode.restype = ctypes.c_uint8
+        lib.orc_fp8_decode.argtypes = [ctypes.c_uint8, i32]
+        lib.orc_fp8_decode.restype = ctypes.c_double
+        u8p, f32p = ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_float)
+        lib.orc_adam8.argtypes = [_f64p, u8p, f32p, u8p, f32p, _f64p, i64, i64, ctypes.c_double, ctypes.c_double,
+                                  ctypes.c_double, i64, f32p, f32p]
+        lib.orc_adam8.restype = None
         _lib = lib
     return _lib
 
@@ -274,3 +288,44 @@ def pack_codes(codes, bits: int) -> np.ndarray:
         nib = (codes[:, c] & 0xF).astype(np.uint8)
         out[:, c // 2] |= nib if c % 2 == 0 else (nib << 4).astype(np.uint8)
     return out
+
+
+E4M3, E5M2 = 0, 1
+ADAM8_BLOCK = 2048
+
+
+def fp8_encode(x, fmt: int) -> np.ndarray:
+    """uint8 codes of the binary32 values x (OCP E4M3 or E5M2, RNE, saturating)."""
+    x = np.asarray(x, dtype=np.float32)
+    lib = _load()
+    return np.array([lib.orc_fp8_encode(float(v), fmt) for v in x.ravel()], dtype=np.uint8).reshape(x.shape)
+
+
+def fp8_decode(c, fmt: int) -> np.ndarray:
+    c = np.asarray(c, dtype=np.uint8)
+    lib = _load()
+    return np.array([lib.orc_fp8_decode(int(v), fmt) for v in c.ravel()], dtype=np.float64).reshape(c.shape)
+
+
+def adam8(R, M8, Ms, V8, Vs, beta1: float, beta2: float, eps: float, t: int, block: int = ADAM8_BLOCK):
+    """One 8-bit block-wise Adam step on the row-major state of one matrix.
+    Returns (M8, Ms, V8, Vs, N, M32, V32): the new codes and block scales, the
+    update N (fp64), and the binary32 moments that were encoded. Inputs are not
+    modified."""
+    R = _f64(R)
+    count = R.size
+    M8 = np.ascontiguousarray(M8, dtype=np.uint8).ravel().copy()
+    V8 = np.ascontiguousarray(V8, dtype=np.uint8).ravel().copy()
+    Ms = np.ascontiguousarray(Ms, dtype=np.float32).ravel().copy()
+    Vs = np.ascontiguousarray(Vs, dtype=np.float32).ravel().copy()
+    nb = (count + block - 1) // block
+    assert M8.size == count and V8.size == count and Ms.size == nb and Vs.size == nb
+    N = np.zeros(count)
+    m32 = np.zeros(count, dtype=np.float32)
+    v32 = np.zeros(count, dtype=np.float32)
+    u8p, f32p = ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_float)
+    _load().orc_adam8(_ptr(R), M8.ctypes.data_as(u8p), Ms.ctypes.data_as(f32p), V8.ctypes.data_as(u8p),
+                      Vs.ctypes.data_as(f32p), _ptr(N), count, block, beta1, beta2, eps, t, m32.ctypes.data_as(f32p),
+                      v32.ctypes.data_as(f32p))
+    sh = R.shape
+    return (M8.reshape(sh), Ms, V8.reshape(sh), Vs, N.reshape(sh), m32.reshape(sh), v32.reshape(sh))

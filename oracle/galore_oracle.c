@@ -514,3 +514,93 @@ ORC_API void orc_quantize_projector(const double* P, int64_t s, int64_t r, int32
         }
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* OCP 8-bit floating point (OCP 8-bit Floating Point Specification, 2023). */
+/* E4M3: exponent bias 7, 3 mantissa bits, largest finite 448, no infinity. */
+/* E5M2: exponent bias 15, 2 mantissa bits, largest finite 57344.           */
+/* Encoding rounds a binary32 value half to even and saturates at the       */
+/* largest finite value (never NaN or infinity); subnormals are kept.       */
+/* ------------------------------------------------------------------------ */
+static int orc_fp8_mbits(int32_t fmt) { return fmt == 0 ? 3 : 2; }
+static int orc_fp8_bias(int32_t fmt) { return fmt == 0 ? 7 : 15; }
+static int orc_fp8_maxcode(int32_t fmt) { return fmt == 0 ? 0x7E : 0x7B; }
+
+ORC_API uint8_t orc_fp8_encode(float x, int32_t fmt) {
+    const int mb = orc_fp8_mbits(fmt), bias = orc_fp8_bias(fmt), maxcode = orc_fp8_maxcode(fmt);
+    const uint8_t sign = signbit(x) ? 0x80 : 0x00;
+    const float y = fabsf(x);
+    if (y == 0.0f) return sign;
+    const int emin = 1 - bias;                 /* exponent of the smallest normal */
+    int e2;
+    frexpf(y, &e2);
+    int E = e2 - 1;                            /* y in [2^E, 2^(E+1)) */
+    if (E < emin) E = emin;
+    if (E > 30) return (uint8_t)(sign | maxcode);
+    float k = rintf(ldexpf(y, mb - E));        /* exact scaling by a power of two, then RNE */
+    if (k == (float)(2 << mb)) {               /* rounded up into the next binade */
+        E += 1;
+        k = (float)(1 << mb);
+    }
+    const int ki = (int)k;
+    if (ki < (1 << mb)) return (uint8_t)(sign | ki);    /* subnormal (E == emin) */
+    int code = ((E + bias) << mb) | (ki - (1 << mb));
+    if (code > maxcode) code = maxcode;
+    return (uint8_t)(sign | code);
+}
+
+ORC_API double orc_fp8_decode(uint8_t c, int32_t fmt) {
+    const int mb = orc_fp8_mbits(fmt), bias = orc_fp8_bias(fmt);
+    const int mag = c & 0x7F, ef = mag >> mb, m = mag & ((1 << mb) - 1);
+    const double v = (ef == 0) ? ldexp((double)m, 1 - bias - mb) : ldexp((double)((1 << mb) + m), ef - bias - mb);
+    return (c & 0x80) ? -v : v;
+}
+
+/* ------------------------------------------------------------------------ */
+/* 8-bit block-wise low-rank Adam (paper §4.2: GaLore 2 uses the 8-bit Adam  */
+/* of bitsandbytes, after Dettmers et al.). Reading: the moments of each     */
+/* matrix are stored in blocks of `block` consecutive elements of the        */
+/* row-major r x l state, M as E4M3 codes of M / scale_M and V as E5M2 codes */
+/* of V / scale_V, with scale = block max of |value| / largest finite value  */
+/* of the format (0 for an all-zero block, whose codes are 0). One step      */
+/* decodes the moments exactly, runs the Adam step of orc_adam on them in    */
+/* fp64 (N from the fresh moments), rounds the new moments to binary32 and   */
+/* re-encodes them with the new block scales, every deciding step in         */
+/* binary32. Mnew/Vnew (optional) receive the binary32 moments encoded.      */
+/* ------------------------------------------------------------------------ */
+ORC_API void orc_adam8(const double* R, uint8_t* M8, float* Ms, uint8_t* V8, float* Vs, double* N, int64_t count,
+                       int64_t block, double beta1, double beta2, double eps, int64_t t, float* Mnew,
+                       float* Vnew) {
+    const double bc1 = 1.0 - pow(beta1, (double)t);
+    const double bc2 = 1.0 - pow(beta2, (double)t);
+    const int64_t nb = (count + block - 1) / block;
+    float* mf = (float*)malloc(sizeof(float) * (size_t)block);
+    float* vf = (float*)malloc(sizeof(float) * (size_t)block);
+    for (int64_t b = 0; b < nb; ++b) {
+        const int64_t i0 = b * block, i1 = (i0 + block < count) ? i0 + block : count;
+        float am = 0.0f, av = 0.0f;
+        for (int64_t i = i0; i < i1; ++i) {
+            const double m = orc_fp8_decode(M8[i], 0) * (double)Ms[b];
+            const double v = orc_fp8_decode(V8[i], 1) * (double)Vs[b];
+            const double g = R[i];
+            const double m1 = beta1 * m + (1.0 - beta1) * g;
+            const double v1 = beta2 * v + (1.0 - beta2) * g * g;
+            N[i] = (m1 / bc1) / (sqrt(v1 / bc2) + eps);
+            mf[i - i0] = (float)m1;
+            vf[i - i0] = (float)v1;
+            if (fabsf(mf[i - i0]) > am) am = fabsf(mf[i - i0]);
+            if (fabsf(vf[i - i0]) > av) av = fabsf(vf[i - i0]);
+        }
+        const float sm = am / 448.0f, sv = av / 57344.0f;
+        Ms[b] = sm;
+        Vs[b] = sv;
+        for (int64_t i = i0; i < i1; ++i) {
+            M8[i] = (sm > 0.0f) ? orc_fp8_encode(mf[i - i0] / sm, 0) : 0;
+            V8[i] = (sv > 0.0f) ? orc_fp8_encode(vf[i - i0] / sv, 1) : 0;
+            if (Mnew) Mnew[i] = mf[i - i0];
+            if (Vnew) Vnew[i] = vf[i - i0];
+        }
+    }
+    free(mf);
+    free(vf);
+}

@@ -564,3 +564,102 @@ def test_pack_codes_layout(orc):
     zero: [1, -2, 7, -7, 3] -> 0xE1 0x97 0x03."""
     assert orc.pack_codes(np.array([[1, -2, 7, -7, 3]]), 4).tolist() == [[0xE1, 0x97, 0x03]]
     assert orc.pack_codes(np.array([[1, -2, 127, -127]]), 8).tolist() == [[0x01, 0xFE, 0x7F, 0x81]]
+
+
+# ---------------------------------------------------------------- 8-bit Adam
+
+
+def test_fp8_extreme_values(orc):
+    """Values the OCP 8-bit floating point specification states for its two
+    formats: E4M3 (bias 7) 1.0 = 0x38, largest finite 448 = 0x7E, smallest
+    subnormal 2^-9 = 0x01, largest subnormal 7 * 2^-9 = 0x07, smallest normal
+    2^-6 = 0x08; E5M2 (bias 15) 1.0 = 0x3C, largest finite 57344 = 0x7B,
+    smallest subnormal 2^-16 = 0x01, smallest normal 2^-14 = 0x04."""
+    e4 = {1.0: 0x38, 448.0: 0x7E, 2.0 ** -9: 0x01, 7 * 2.0 ** -9: 0x07, 2.0 ** -6: 0x08, -2.0: 0xC0}
+    e5 = {1.0: 0x3C, 57344.0: 0x7B, 2.0 ** -16: 0x01, 2.0 ** -14: 0x04, -1.0: 0xBC}
+    for fmt, table in ((orc.E4M3, e4), (orc.E5M2, e5)):
+        vals = np.array(list(table), dtype=np.float64)
+        codes = np.array(list(table.values()), dtype=np.uint8)
+        assert np.array_equal(orc.fp8_encode(vals, fmt), codes)
+        assert np.array_equal(orc.fp8_decode(codes, fmt), vals)
+    assert orc.fp8_encode([1e9, -1e9], orc.E4M3).tolist() == [0x7E, 0xFE]      # saturation
+    assert orc.fp8_encode([1e9], orc.E5M2).tolist() == [0x7B]
+
+
+@pytest.mark.parametrize("fmt,top", [(0, 0x7E), (1, 0x7B)])
+def test_fp8_round_trip_and_brute_force_rounding(orc, fmt, top):
+    """Every finite code decodes to a strictly increasing magnitude and encodes
+    back to itself; random binary32 values (and exact midpoints) encode to the
+    nearest representable value by brute force, ties to the even code."""
+    codes = np.arange(0, top + 1, dtype=np.uint8)
+    vals = orc.fp8_decode(codes, fmt)
+    assert np.all(np.diff(vals) > 0)
+    assert np.array_equal(orc.fp8_encode(vals, fmt), codes)
+    rng = np.random.default_rng(50 + fmt)
+    mids = (vals[:-1] + vals[1:]) / 2
+    ys = np.concatenate([np.exp(rng.uniform(np.log(vals[1] / 4), np.log(vals[-1]), 3000)), mids,
+                         rng.uniform(0, vals[8], 200)]).astype(np.float32)
+    got = orc.fp8_encode(ys, fmt)
+    for y, c in zip(ys.astype(np.float64), got):
+        d = np.abs(vals - y)
+        best = np.flatnonzero(d == d.min())
+        want = best[0] if len(best) == 1 else [b for b in best if b % 2 == 0][0]
+        if y > vals[-1]:
+            want = top
+        assert c == want, (y, c, want)
+
+
+def test_adam8_first_step_equals_adam(orc):
+    """From the all-zero state the decoded moments are exactly zero, so the
+    first 8-bit step's N equals the (pinned) fp64 Adam step's N."""
+    rng = np.random.default_rng(51)
+    R = rng.standard_normal((7, 700))
+    count = R.size
+    nb = (count + 2047) // 2048
+    z8, zs = np.zeros(count, np.uint8), np.zeros(nb, np.float32)
+    _, _, _, _, N, _, _ = orc.adam8(R, z8, zs, z8, zs, 0.9, 0.999, 1e-8, 1)
+    _, _, Nref = orc.adam(R, np.zeros_like(R), np.zeros_like(R), 0.9, 0.999, 1e-8, 1)
+    assert np.array_equal(N, Nref)
+
+
+def test_adam8_grid_block_is_encoded_exactly(orc):
+    """With beta1 = 0 the new first moment is the gradient itself; a block whose
+    values are E4M3 values times 2^-5 with maximum 448 * 2^-5 has scale 2^-5
+    and is encoded exactly (codes equal those values' own E4M3 codes)."""
+    rng = np.random.default_rng(52)
+    codes = rng.integers(0, 0x7F, size=2048).astype(np.uint8) | (rng.integers(0, 2, 2048) * 0x80).astype(np.uint8)
+    codes[codes & 0x7F == 0x7F] = 0x7E
+    codes[17] = 0x7E
+    g = orc.fp8_decode(codes, orc.E4M3) * 2.0 ** -5
+    M8, Ms, _, _, _, _, _ = orc.adam8(g, np.zeros(2048, np.uint8), np.zeros(1, np.float32), np.zeros(2048, np.uint8),
+                                      np.zeros(1, np.float32), 0.0, 0.5, 1e-8, 1)
+    assert Ms[0] == np.float32(2.0 ** -5)
+    dec = orc.fp8_decode(M8, orc.E4M3)
+    assert np.array_equal(dec, orc.fp8_decode(codes, orc.E4M3))
+
+
+def test_adam8_quantisation_error_and_block_independence(orc):
+    """Over three steps: each decoded moment is within half an E4M3 / E5M2 step
+    of the binary32 moment that was encoded (relative 2^-4 / 2^-3 for normal
+    values, half the subnormal spacing below), and changing the gradient in one
+    block leaves every other block's codes and scales untouched; the last block
+    is ragged (3 * 700 = 2100 elements = 2048 + 52)."""
+    rng = np.random.default_rng(53)
+    shape = (3, 700)
+    count = 2100
+    M8, V8 = np.zeros(count, np.uint8), np.zeros(count, np.uint8)
+    Ms, Vs = np.zeros(2, np.float32), np.zeros(2, np.float32)
+    for t in range(1, 4):
+        R = rng.standard_normal(shape) * np.exp(rng.uniform(-3, 3, shape))
+        M8, Ms, V8, Vs, N, m32, v32 = orc.adam8(R, M8, Ms, V8, Vs, 0.9, 0.999, 1e-8, t)
+        blk = np.arange(count).reshape(shape) // 2048
+        dm = orc.fp8_decode(M8, orc.E4M3) * Ms[blk]
+        dv = orc.fp8_decode(V8, orc.E5M2) * Vs[blk]
+        assert np.all(np.abs(dm - m32) <= np.maximum(2.0 ** -4 * np.abs(m32), 2.0 ** -10 * Ms[blk]) * (1 + 1e-6))
+        assert np.all(np.abs(dv - v32) <= np.maximum(2.0 ** -3 * np.abs(v32), 2.0 ** -17 * Vs[blk]) * (1 + 1e-6))
+    R2 = R.copy()
+    R2.ravel()[2050] += 1.0                      # inside the second block
+    a = orc.adam8(R, M8, Ms, V8, Vs, 0.9, 0.999, 1e-8, 4)
+    b = orc.adam8(R2, M8, Ms, V8, Vs, 0.9, 0.999, 1e-8, 4)
+    assert np.array_equal(a[0].ravel()[:2048], b[0].ravel()[:2048]) and a[1][0] == b[1][0]
+    assert np.array_equal(a[2].ravel()[:2048], b[2].ravel()[:2048]) and a[3][0] == b[3][0]
