@@ -262,6 +262,36 @@ GALORE_API int galore_align_projector(const float* P_old, int64_t ld_old, int64_
                                       hipStream_t stream);
 
 /*
+ * Number of fp32 block scales galore_lowrank_adam8_step keeps per moment and
+ * matrix for a rows x cols state: ceil(rows * cols / 2048). 0 for invalid sizes.
+ */
+GALORE_API int64_t galore_adam8_scale_count(int64_t rows, int64_t cols);
+
+/*
+ * 8-bit block-wise low-rank Adam (paper §4.2: GaLore 2 uses the 8-bit Adam
+ * optimizer of bitsandbytes, after Dettmers et al.; the paper fixes no data
+ * type). The moments of each matrix are stored in blocks of 2048 consecutive
+ * elements of the packed row-major rows x cols state:
+ *   M8: OCP FP8 E4M3 codes of M / Ms[block]   (Ms = block max |M| / 448)
+ *   V8: OCP FP8 E5M2 codes of V / Vs[block]   (Vs = block max V / 57344)
+ * (round half to even, saturating, subnormals kept; an all-zero block has
+ * scale 0 and codes 0, so zero-filled codes and scales are the zero state).
+ * One call decodes the moments, applies galore_lowrank_adam_step's update in
+ * fp32 (N from the new moments, bias exponent t), and re-encodes the new
+ * moments with new block scales.
+ * R, N: fp32 rows x cols (ld ld, batch stride stride); N may alias R.
+ * M8, V8: device bytes, rows * cols per matrix, packed, matrix b at b * rows * cols.
+ * Ms, Vs: device fp32, galore_adam8_scale_count(rows, cols) per matrix, packed.
+ * All state is updated in place.
+ * Errors: NULL pointers, betas outside [0, 1), eps <= 0, non-finite scalars,
+ * t < 1 -> INVALID_ARG; rows/cols < 1, ld < cols, batch < 1, stride too small -> SHAPE.
+ */
+GALORE_API int galore_lowrank_adam8_step(const float* R, float* N, int64_t ld, int64_t stride, uint8_t* M8,
+                                         float* Ms, uint8_t* V8, float* Vs, int64_t rows, int64_t cols,
+                                         int32_t batch, float beta1, float beta2, float eps, int64_t t,
+                                         hipStream_t stream);
+
+/*
  * Low-bit projector (paper §4.2: GaLore 2 supports low-bit projection
  * matrices, after Q-GaLore; the paper fixes no scheme). Each column j of the
  * fp32 s x r projector P is quantised symmetrically:

@@ -28,6 +28,7 @@ EXPORTED = (
     "galore_step_workspace_size", "galore_step",
     "galore_quantize_projector", "galore_project_quantized_workspace_size", "galore_project_quantized",
     "galore_project_back_quantized_workspace_size", "galore_project_back_quantized",
+    "galore_adam8_scale_count", "galore_lowrank_adam8_step",
 )
 
 GALORE_STEP_ALIGN = 1
@@ -96,6 +97,10 @@ def _declare(lib):
     lib.galore_project_back_quantized.argtypes = [vp, i64, i64, vp, i64, i32, vp, i64, i64, vp, i64, i64, i64, i64,
                                                   i32, f32, f32, i32, vp, sz, vp]
     lib.galore_project_back_quantized.restype = ctypes.c_int
+    lib.galore_adam8_scale_count.argtypes = [i64, i64]
+    lib.galore_adam8_scale_count.restype = i64
+    lib.galore_lowrank_adam8_step.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, i64, i64, i32, f32, f32, f32, i64, vp]
+    lib.galore_lowrank_adam8_step.restype = ctypes.c_int
     return lib
 
 
@@ -413,3 +418,40 @@ def galore_project_back_quantized(Pq: QuantizedProjector, N: torch.Tensor, W: to
                                              alpha, batch, workspace.data_ptr(), workspace.numel(), _stream(stream)),
            "galore_project_back_quantized")
     return W
+
+
+def galore_adam8_scale_count(rows: int, cols: int) -> int:
+    return int(lib.galore_adam8_scale_count(rows, cols))
+
+
+class Adam8State:
+    """8-bit moments of a batch of rows x cols low-rank states: M8/V8 codes
+    (uint8, (batch, rows, cols)) and block scales Ms/Vs (fp32, (batch, nblocks));
+    zero-filled = the zero state."""
+
+    def __init__(self, rows: int, cols: int, batch: int = 1, device="cuda"):
+        nb = galore_adam8_scale_count(rows, cols)
+        self.rows, self.cols, self.batch = rows, cols, batch
+        self.M8 = torch.zeros((batch, rows, cols), dtype=torch.uint8, device=device)
+        self.V8 = torch.zeros_like(self.M8)
+        self.Ms = torch.zeros((batch, nb), dtype=torch.float32, device=device)
+        self.Vs = torch.zeros_like(self.Ms)
+
+
+def galore_lowrank_adam8_step(R: torch.Tensor, state: Adam8State, N=None, beta1=0.9, beta2=0.999, eps=1e-8, t=1,
+                              stream=None):
+    """8-bit block-wise Adam step on the state (updated in place); returns N (may be R itself)."""
+    if N is None:
+        N = torch.empty_like(R)
+    rp, rows, cols, ld, st_, batch = _mat(R, "R")
+    if N.shape != R.shape or N.stride() != R.stride() or N.dtype != torch.float32 or R.dtype != torch.float32:
+        raise ValueError("N must match R in shape, strides and dtype (float32)")
+    if (state.rows, state.cols, state.batch) != (rows, cols, batch):
+        raise ValueError("state does not match R")
+    for x in (state.M8, state.V8, state.Ms, state.Vs):
+        if not x.is_contiguous():
+            raise ValueError("8-bit state must be contiguous")
+    _check(lib.galore_lowrank_adam8_step(rp, N.data_ptr(), ld, st_, state.M8.data_ptr(), state.Ms.data_ptr(),
+                                         state.V8.data_ptr(), state.Vs.data_ptr(), rows, cols, batch, beta1, beta2,
+                                         eps, t, _stream(stream)), "galore_lowrank_adam8_step")
+    return N

@@ -139,6 +139,12 @@ hipError_t launch_codes_plane(const uint8_t* Q, int64_t ldq, int64_t strideQ, in
 hipError_t launch_dequantize(const uint8_t* Q, int64_t ldq, int64_t strideQ, int bits, const float* scales,
                              int64_t strideS, int rows, int r, float* Pt, int64_t ldt, int64_t strideT, int batch,
                              hipStream_t stream);
+// 8-bit block-wise Adam (adam8.hip): blocks of 2048 elements of the packed
+// row-major state; R and N share (ld, stride)
+int64_t adam8_block_count(int64_t rows, int64_t cols);
+hipError_t launch_adam8(const float* R, float* N, int64_t ld, int64_t stride, uint8_t* M8, float* Ms, uint8_t* V8,
+                        float* Vs, int64_t rows, int64_t cols, int batch, float beta1, float beta2, float eps,
+                        float bc1, float bc2, hipStream_t stream);
 hipError_t launch_copy_rows(const float* src, int64_t lds, int64_t strideS, float* dst, int64_t ldd,
                             int64_t strideD, int rows, int cols, int batch, hipStream_t stream);
 

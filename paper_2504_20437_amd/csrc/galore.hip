@@ -862,6 +862,31 @@ int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const flo
     return GALORE_OK;
 }
 
+// ---- 8-bit Adam -------------------------------------------------------------
+
+int64_t galore_adam8_scale_count(int64_t rows, int64_t cols) {
+    if (rows < 1 || cols < 1) return 0;
+    return adam8_block_count(rows, cols);
+}
+
+int galore_lowrank_adam8_step(const float* R, float* N, int64_t ld, int64_t stride, uint8_t* M8, float* Ms,
+                              uint8_t* V8, float* Vs, int64_t rows, int64_t cols, int32_t batch, float beta1,
+                              float beta2, float eps, int64_t t, hipStream_t stream) {
+    if (R == nullptr || N == nullptr || M8 == nullptr || Ms == nullptr || V8 == nullptr || Vs == nullptr)
+        return GALORE_ERR_INVALID_ARG;
+    if (!finite_f(beta1) || !finite_f(beta2) || !finite_f(eps)) return GALORE_ERR_INVALID_ARG;
+    if (beta1 < 0.0f || beta1 >= 1.0f || beta2 < 0.0f || beta2 >= 1.0f || eps <= 0.0f || t < 1)
+        return GALORE_ERR_INVALID_ARG;
+    if (rows < 1 || cols < 1 || ld < cols || batch < 1) return GALORE_ERR_SHAPE;
+    if (batch > 1 && stride < rows * ld) return GALORE_ERR_SHAPE;
+    const double bc1 = 1.0 - pow(static_cast<double>(beta1), static_cast<double>(t));
+    const double bc2 = 1.0 - pow(static_cast<double>(beta2), static_cast<double>(t));
+    if (!(bc1 > 0.0) || !(bc2 > 0.0)) return GALORE_ERR_INVALID_ARG;
+    GALORE_TRY(launch_adam8(R, N, ld, (batch > 1) ? stride : rows * ld, M8, Ms, V8, Vs, rows, cols, batch, beta1,
+                            beta2, eps, static_cast<float>(bc1), static_cast<float>(bc2), stream));
+    return GALORE_OK;
+}
+
 // ---- low-bit projector ------------------------------------------------------
 
 bool codes_shape_ok(int64_t s, int32_t r, int32_t bits, int64_t ldq) {

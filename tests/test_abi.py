@@ -318,3 +318,22 @@ def test_project_back_quantized_rejects():
         assert call(**kw) == -2, kw
     for kw in (dict(ws=NULL), dict(ws=ws + 8), dict(wb=need - 1)):
         assert call(**kw) == -3, kw
+
+
+def test_adam8_rejects_and_scale_count():
+    import paper_2504_20437_amd as gl
+    assert gl.galore_adam8_scale_count(1024, 11008) == 5504
+    assert gl.galore_adam8_scale_count(3, 700) == 2
+    assert gl.galore_adam8_scale_count(0, 5) == 0
+    f = gl.lib.galore_lowrank_adam8_step
+    ok = dict(R=FAKE, N=FAKE, ld=96, st=0, M8=FAKE, Ms=FAKE, V8=FAKE, Vs=FAKE, rows=8, cols=96, b=1, b1=0.9,
+              b2=0.999, eps=1e-8, t=1)
+    keys = list(ok)
+    def call(**kw):
+        a = dict(ok); a.update(kw)
+        return f(*[a[k] for k in keys], None)
+    for kw in (dict(R=NULL), dict(N=NULL), dict(M8=NULL), dict(Ms=NULL), dict(V8=NULL), dict(Vs=NULL),
+               dict(b1=1.0), dict(b2=-0.1), dict(eps=0.0), dict(eps=float("nan")), dict(t=0)):
+        assert call(**kw) == -1, kw
+    for kw in (dict(rows=0), dict(cols=0), dict(ld=95), dict(b=0), dict(b=2, st=8 * 96 - 1)):
+        assert call(**kw) == -2, kw

@@ -706,3 +706,58 @@ def test_project_back_quantized_matches_oracle(gl, orc, bits, m, n, r, batch):
         if m > n:
             bound = bound.T
         assert np.all(np.abs(out[i] - ref) <= 1e-5 * bound + 1e-30)
+
+
+# ---------------------------------------------------------------- 8-bit Adam
+
+
+def _code_rank(c, fmt):
+    """signed position of a code on the number line (adjacent values differ by 1)"""
+    c = np.asarray(c, dtype=np.int64)
+    mag = c & 0x7F
+    return np.where(c & 0x80, -mag, mag)
+
+
+@pytest.mark.parametrize("rows,cols,batch", [(7, 700, 1), (32, 2048, 2), (24, 1000, 3), (1, 100, 1), (16, 11008, 1)])
+def test_adam8_matches_oracle(gl, orc, rows, cols, batch):
+    """Four steps from the zero state; each step is compared with the oracle
+    started from the GPU's own previous codes and scales. Scales agree to a few
+    ulps; a code may differ only by one step, and only where the oracle's
+    binary32 moment lies closer to the rounding boundary between the two codes
+    than the fp32 rounding of the moment's two terms can move it; N agrees
+    within 1e-5 relative plus 8 ulps of the moment's terms over its denominator."""
+    import torch
+    st = gl.Adam8State(rows, cols, batch)
+    rng = np.random.default_rng(rows * 31 + cols + batch)
+    b1, b2, eps = (float(np.float32(x)) for x in (0.9, 0.999, 1e-8))
+    u = 2.0 ** -24
+    for t in range(1, 5):
+        R = (rng.standard_normal((batch, rows, cols)) * np.exp(rng.uniform(-4, 2, (batch, rows, 1)))).astype(np.float32)
+        M8h, Msh = st.M8.cpu().numpy().copy(), st.Ms.cpu().numpy().copy()
+        V8h, Vsh = st.V8.cpu().numpy().copy(), st.Vs.cpu().numpy().copy()
+        N = host(gl.galore_lowrank_adam8_step(dev(R), st, beta1=b1, beta2=b2, eps=eps, t=t))
+        M8g, Msg = st.M8.cpu().numpy(), st.Ms.cpu().numpy()
+        V8g, Vsg = st.V8.cpu().numpy(), st.Vs.cpu().numpy()
+        for i in range(batch):
+            M8o, Mso, V8o, Vso, No, m32, v32 = orc.adam8(R[i], M8h[i], Msh[i], V8h[i], Vsh[i], b1, b2, eps, t)
+            assert np.all(np.abs(Msg[i] - Mso) <= 4 * u * Mso) and np.all(np.abs(Vsg[i] - Vso) <= 4 * u * Vso)
+            blk = (np.arange(rows * cols) // 2048).reshape(rows, cols)
+            mdec = orc.fp8_decode(M8h[i], orc.E4M3) * Msh[i][blk]
+            vdec = orc.fp8_decode(V8h[i], orc.E5M2) * Vsh[i][blk]
+            # relative uncertainty of the binary32 moment that decides the code
+            relm = 8 * u * (b1 * np.abs(mdec) + (1 - b1) * np.abs(R[i])) / np.maximum(np.abs(m32), 1e-300) + 8 * u
+            relv = 8 * u * (b2 * vdec + (1 - b2) * R[i].astype(np.float64) ** 2) / np.maximum(v32, 1e-300) + 8 * u
+            for codes_g, codes_o, scal, x32, rel, fmt in ((M8g[i], M8o, Mso, m32, relm, orc.E4M3),
+                                                          (V8g[i], V8o, Vso, v32, relv, orc.E5M2)):
+                bad = codes_g != codes_o
+                assert bad.mean() < 1e-3
+                if bad.any():
+                    cg, co = codes_g[bad], codes_o[bad]
+                    assert np.all(np.abs(_code_rank(cg, fmt) - _code_rank(co, fmt)) == 1)
+                    mid = (orc.fp8_decode(cg, fmt) + orc.fp8_decode(co, fmt)) / 2
+                    y = x32[bad].astype(np.float64) / scal[blk[bad]].astype(np.float64)
+                    assert np.all(np.abs(y - mid) <= rel[bad] * np.abs(mid))
+            bc1, bc2 = 1 - b1 ** t, 1 - b2 ** t
+            den = np.sqrt(v32.astype(np.float64) / bc2) + eps
+            tol = 1e-5 * np.abs(No) + 8 * u * (b1 * np.abs(mdec) + (1 - b1) * np.abs(R[i])) / bc1 / den
+            assert np.all(np.abs(N[i] - No) <= tol), (t, i)
