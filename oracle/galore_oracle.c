@@ -561,13 +561,21 @@ ORC_API double orc_fp8_decode(uint8_t c, int32_t fmt) {
 /* of bitsandbytes, after Dettmers et al.). Reading: the moments of each     */
 /* matrix are stored in blocks of `block` consecutive elements of the        */
 /* row-major r x l state, M as E4M3 codes of M / scale_M and V as E5M2 codes */
-/* of V / scale_V, with scale = block max of |value| / largest finite value  */
-/* of the format (0 for an all-zero block, whose codes are 0). One step      */
-/* decodes the moments exactly, runs the Adam step of orc_adam on them in    */
-/* fp64 (N from the fresh moments), rounds the new moments to binary32 and   */
-/* re-encodes them with the new block scales, every deciding step in         */
-/* binary32. Mnew/Vnew (optional) receive the binary32 moments encoded.      */
+/* of V / scale_V. A block's scale is the smallest power of two 2^k with     */
+/* block max |value| <= 2^k * (largest finite value of the format), so that  */
+/* scaling is exact and only the format's own rounding decides a code (0    */
+/* for an all-zero block, whose codes are 0). One step decodes the moments   */
+/* exactly, runs the Adam step of orc_adam on them in fp64 (N from the fresh */
+/* moments), rounds the new moments to binary32 and re-encodes them with the */
+/* new block scales. Mnew/Vnew (optional) receive the binary32 moments.      */
 /* ------------------------------------------------------------------------ */
+static float orc_pow2_scale(float amax, float maxval) {
+    if (!(amax > 0.0f)) return 0.0f;
+    int e, em;
+    const float f = frexpf(amax, &e), fm = frexpf(maxval, &em);
+    return ldexpf(1.0f, e - em + (f > fm ? 1 : 0));
+}
+
 ORC_API void orc_adam8(const double* R, uint8_t* M8, float* Ms, uint8_t* V8, float* Vs, double* N, int64_t count,
                        int64_t block, double beta1, double beta2, double eps, int64_t t, float* Mnew,
                        float* Vnew) {
@@ -591,11 +599,11 @@ ORC_API void orc_adam8(const double* R, uint8_t* M8, float* Ms, uint8_t* V8, flo
             if (fabsf(mf[i - i0]) > am) am = fabsf(mf[i - i0]);
             if (fabsf(vf[i - i0]) > av) av = fabsf(vf[i - i0]);
         }
-        const float sm = am / 448.0f, sv = av / 57344.0f;
+        const float sm = orc_pow2_scale(am, 448.0f), sv = orc_pow2_scale(av, 57344.0f);
         Ms[b] = sm;
         Vs[b] = sv;
         for (int64_t i = i0; i < i1; ++i) {
-            M8[i] = (sm > 0.0f) ? orc_fp8_encode(mf[i - i0] / sm, 0) : 0;
+            M8[i] = (sm > 0.0f) ? orc_fp8_encode(mf[i - i0] / sm, 0) : 0;   /* exact division by 2^k */
             V8[i] = (sv > 0.0f) ? orc_fp8_encode(vf[i - i0] / sv, 1) : 0;
             if (Mnew) Mnew[i] = mf[i - i0];
             if (Vnew) Vnew[i] = vf[i - i0];

@@ -663,3 +663,21 @@ def test_adam8_quantisation_error_and_block_independence(orc):
     b = orc.adam8(R2, M8, Ms, V8, Vs, 0.9, 0.999, 1e-8, 4)
     assert np.array_equal(a[0].ravel()[:2048], b[0].ravel()[:2048]) and a[1][0] == b[1][0]
     assert np.array_equal(a[2].ravel()[:2048], b[2].ravel()[:2048]) and a[3][0] == b[3][0]
+
+
+@pytest.mark.parametrize("amax,k", [(448.0 * 2 ** -3, -3), (448.0 * 2 ** -3 * (1 + 2 ** -20), -2),
+                                    (224.5 * 2 ** -3, -3), (224.0 * 2 ** -3, -4)])
+def test_adam8_block_scale_is_smallest_power_of_two(orc, amax, k):
+    """A block's M scale is the smallest 2^k with max |M| <= 448 * 2^k (the
+    E4M3 largest finite value): exactly at 448 * 2^k it is 2^k, just above it
+    2^(k+1), and at 224 * 2^k the next lower power already suffices."""
+    g = np.zeros(2048)
+    g[5] = -amax
+    g[9] = amax / 3
+    M8, Ms, V8, Vs, _, m32, v32 = orc.adam8(g, np.zeros(2048, np.uint8), np.zeros(1, np.float32),
+                                            np.zeros(2048, np.uint8), np.zeros(1, np.float32), 0.0, 0.0, 1e-8, 1)
+    assert Ms[0] == np.float32(2.0 ** k)
+    vmax = np.float64(np.float32(amax) ** 2)
+    kv = int(np.ceil(np.log2(vmax / 57344.0)))
+    assert Vs[0] == np.float32(2.0 ** kv) and vmax <= 57344.0 * 2.0 ** kv and vmax > 57344.0 * 2.0 ** (kv - 1)
+    assert orc.fp8_decode(M8[5], orc.E4M3) * Ms[0] == pytest.approx(-amax, rel=2 ** -4)
