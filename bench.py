@@ -466,6 +466,21 @@ def main():
         }
         del qws, qbws, Pq
 
+    # 8-bit moments (E4M3 / E5M2 codes, one scale per 2048-element block)
+    st8 = gl.Adam8State(r, l, B, device=dev)
+    a8 = [mk() for _ in range(4)]
+    for j in range(2):
+        a8[2 * j].record(stream)
+        gl.galore_lowrank_adam8_step(R, st8, N=N, beta1=0.9, beta2=0.999, eps=1e-8, t=j + 1, stream=stream)
+        a8[2 * j + 1].record(stream)
+    torch.cuda.synchronize()
+    adam8_ms = a8[2].elapsed_time(a8[3])
+    adam8 = {"ms": round(adam8_ms, 3), "hbm_gbs": round(12.0 * B * r * l / (adam8_ms * 1e-3) / 1e9, 1),
+             "state_bytes": int(2 * (st8.M8.numel() + 4 * st8.Ms.numel())),
+             "note": "8-bit block-wise Adam on the whole batch: 12 bytes per element (R, N fp32; M, V one byte each "
+                     "in and out); fp32 moments take %d bytes" % (8 * B * r * l)}
+    del st8
+
     out = {
         "metric": "rSVD subspace updates/sec at 4096x11008 r=1024; low-rank Adam step HBM GB/s",
         "value": round(B / (ms_per_step * 1e-3), 3),
@@ -494,6 +509,7 @@ def main():
                      "amortised_step_ms": round((upd_ms + (T_sched - 1) * plain_ms) / T_sched, 3),
                      "note": "galore_step on the whole batch: the update step (subspace update, switch with "
                              "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
+        "adam8": adam8,
         "lowbit_projector": dict(lowbit, note="steps on a fixed projector with its int8 / int4 codes (whole batch): "
                                                "projection, Adam, back-projection; fp32 projector bytes %d"
                                                % (4 * B * s * r)),

@@ -272,10 +272,13 @@ GALORE_API int64_t galore_adam8_scale_count(int64_t rows, int64_t cols);
  * optimizer of bitsandbytes, after Dettmers et al.; the paper fixes no data
  * type). The moments of each matrix are stored in blocks of 2048 consecutive
  * elements of the packed row-major rows x cols state:
- *   M8: OCP FP8 E4M3 codes of M / Ms[block]   (Ms = block max |M| / 448)
- *   V8: OCP FP8 E5M2 codes of V / Vs[block]   (Vs = block max V / 57344)
- * (round half to even, saturating, subnormals kept; an all-zero block has
- * scale 0 and codes 0, so zero-filled codes and scales are the zero state).
+ *   M8: OCP FP8 E4M3 codes of M / Ms[block]
+ *   V8: OCP FP8 E5M2 codes of V / Vs[block]
+ * where a block's scale is the smallest power of two 2^k with block max
+ * |value| <= 2^k * 448 (E4M3) or 2^k * 57344 (E5M2), the formats' largest
+ * finite values (round half to even, saturating, subnormals kept; an all-zero
+ * block has scale 0 and codes 0, so zero-filled codes and scales are the zero
+ * state).
  * One call decodes the moments, applies galore_lowrank_adam_step's update in
  * fp32 (N from the new moments, bias exponent t), and re-encodes the new
  * moments with new block scales.

@@ -721,8 +721,8 @@ def _code_rank(c, fmt):
 @pytest.mark.parametrize("rows,cols,batch", [(7, 700, 1), (32, 2048, 2), (24, 1000, 3), (1, 100, 1), (16, 11008, 1)])
 def test_adam8_matches_oracle(gl, orc, rows, cols, batch):
     """Four steps from the zero state; each step is compared with the oracle
-    started from the GPU's own previous codes and scales. Scales agree to a few
-    ulps; a code may differ only by one step, and only where the oracle's
+    started from the GPU's own previous codes and scales. Block scales agree; a
+    code may differ only by one step, and only where the oracle's
     binary32 moment lies closer to the rounding boundary between the two codes
     than the fp32 rounding of the moment's two terms can move it; N agrees
     within 1e-5 relative plus 8 ulps of the moment's terms over its denominator."""
@@ -740,16 +740,28 @@ def test_adam8_matches_oracle(gl, orc, rows, cols, batch):
         V8g, Vsg = st.V8.cpu().numpy(), st.Vs.cpu().numpy()
         for i in range(batch):
             M8o, Mso, V8o, Vso, No, m32, v32 = orc.adam8(R[i], M8h[i], Msh[i], V8h[i], Vsh[i], b1, b2, eps, t)
-            assert np.all(np.abs(Msg[i] - Mso) <= 4 * u * Mso) and np.all(np.abs(Vsg[i] - Vso) <= 4 * u * Vso)
             blk = (np.arange(rows * cols) // 2048).reshape(rows, cols)
             mdec = orc.fp8_decode(M8h[i], orc.E4M3) * Msh[i][blk]
             vdec = orc.fp8_decode(V8h[i], orc.E5M2) * Vsh[i][blk]
             # relative uncertainty of the binary32 moment that decides the code
             relm = 8 * u * (b1 * np.abs(mdec) + (1 - b1) * np.abs(R[i])) / np.maximum(np.abs(m32), 1e-300) + 8 * u
             relv = 8 * u * (b2 * vdec + (1 - b2) * R[i].astype(np.float64) ** 2) / np.maximum(v32, 1e-300) + 8 * u
-            for codes_g, codes_o, scal, x32, rel, fmt in ((M8g[i], M8o, Mso, m32, relm, orc.E4M3),
-                                                          (V8g[i], V8o, Vso, v32, relv, orc.E5M2)):
-                bad = codes_g != codes_o
+            for codes_g, codes_o, sg, scal, x32, rel, fmt, top in (
+                    (M8g[i], M8o, Msg[i], Mso, m32, relm, orc.E4M3, 448.0),
+                    (V8g[i], V8o, Vsg[i], Vso, v32, relv, orc.E5M2, 57344.0)):
+                # power-of-two block scales agree unless the block maximum sits within
+                # its rounding uncertainty of a boundary top * 2^k (then that block's
+                # codes are not compared)
+                skip = np.zeros(rows * cols, bool)
+                for bk in np.flatnonzero(sg != scal):
+                    sel = slice(bk * 2048, min((bk + 1) * 2048, rows * cols))
+                    xs, rs = np.abs(x32.ravel()[sel]).astype(np.float64), rel.ravel()[sel]
+                    j = np.argmax(xs)
+                    edge = top * max(float(sg[bk]), float(scal[bk])) / 2
+                    assert sg[bk] in (2 * scal[bk], scal[bk] / 2) and abs(xs[j] - edge) <= rs[j] * edge
+                    skip[sel] = True
+                skip = skip.reshape(rows, cols)
+                bad = (codes_g != codes_o) & ~skip
                 assert bad.mean() < 1e-3
                 if bad.any():
                     cg, co = codes_g[bad], codes_o[bad]
