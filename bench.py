@@ -466,6 +466,30 @@ def main():
         }
         del qws, qbws, Pq
 
+    # exact SVD (k = s) against the randomized one on the same 8 matrices
+    if s <= 4096:
+        Bx = min(B, 8)
+        xws = torch.empty((gl.galore_svd_workspace_size(m, n, r, Bx, G.dtype),), dtype=torch.uint8, device=dev)
+        xe = [mk() for _ in range(8)]
+        for j in range(2):
+            xe[4 * j].record(stream)
+            _, _, xinfo = gl.galore_svd_update(G[:Bx], r, workspace=xws, stream=stream)
+            xe[4 * j + 1].record(stream)
+            gl.galore_rsvd_update(G[:Bx], r, p, q, gi.sketch_seed(0), 0, P=P[:Bx], sigma=sigma[:Bx], info=info[:Bx],
+                                  workspace=chunks[0]["ws"], stream=stream)
+            xe[4 * j + 2].record(stream)
+        torch.cuda.synchronize()
+        if int((xinfo != 0).sum()):
+            raise RuntimeError("exact SVD did not converge")
+        x_ms, rs_ms = xe[4].elapsed_time(xe[5]), xe[5].elapsed_time(xe[6])
+        exact_svd = {"batch": Bx, "exact_ms_per_matrix": round(x_ms / Bx, 3),
+                     "rsvd_ms_per_matrix": round(rs_ms / Bx, 3), "speedup": round(x_ms / rs_ms, 2),
+                     "note": "exact top-r SVD (sketch as wide as the short side, k = %d, no power iteration) against "
+                             "the randomized update (k = %d, q = %d) on the same %d matrices" % (s, k, q, Bx)}
+        del xws
+    else:
+        exact_svd = None
+
     # 8-bit moments (E4M3 / E5M2 codes, one scale per 2048-element block)
     st8 = gl.Adam8State(r, l, B, device=dev)
     a8 = [mk() for _ in range(4)]
@@ -510,6 +534,7 @@ def main():
                      "note": "galore_step on the whole batch: the update step (subspace update, switch with "
                              "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
         "adam8": adam8,
+        "exact_svd": exact_svd,
         "lowbit_projector": dict(lowbit, note="steps on a fixed projector with its int8 / int4 codes (whole batch): "
                                                "projection, Adam, back-projection; fp32 projector bytes %d"
                                                % (4 * B * s * r)),

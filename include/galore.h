@@ -120,6 +120,22 @@ GALORE_API int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int
                        void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * Exact SVD projector (the full SVD that paper §4.1.2 replaces by the
+ * randomized one): galore_rsvd_update with the sketch as wide as the short
+ * side (k = s, p = s - r) and no power iteration. The sketch then spans the
+ * whole short side, Q is an orthonormal basis of it and the SVD of B = Q^T A
+ * is the SVD of A, so P and sigma are the exact top-r singular vectors and
+ * values up to rounding. Arguments as galore_rsvd_update (no seed: the result
+ * does not depend on the sketch). s <= 4096.
+ * Errors: as galore_rsvd_update; s > 4096 -> SHAPE.
+ */
+GALORE_API size_t galore_svd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch, int32_t g_dtype);
+GALORE_API int galore_svd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
+                                 int64_t stride_g, int32_t r, float* P, int64_t ldp, int64_t stride_p, float* sigma,
+                                 int64_t stride_sigma, int32_t* info, int32_t batch, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/*
  * Stages of the subspace update reported by galore_rsvd_update_traced.
  */
 typedef enum {

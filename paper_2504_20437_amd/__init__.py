@@ -29,6 +29,7 @@ EXPORTED = (
     "galore_quantize_projector", "galore_project_quantized_workspace_size", "galore_project_quantized",
     "galore_project_back_quantized_workspace_size", "galore_project_back_quantized",
     "galore_adam8_scale_count", "galore_lowrank_adam8_step",
+    "galore_svd_workspace_size", "galore_svd_update",
 )
 
 GALORE_STEP_ALIGN = 1
@@ -101,6 +102,10 @@ def _declare(lib):
     lib.galore_adam8_scale_count.restype = i64
     lib.galore_lowrank_adam8_step.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, i64, i64, i32, f32, f32, f32, i64, vp]
     lib.galore_lowrank_adam8_step.restype = ctypes.c_int
+    lib.galore_svd_workspace_size.argtypes = [i64, i64, i32, i32, i32]
+    lib.galore_svd_workspace_size.restype = sz
+    lib.galore_svd_update.argtypes = [vp, i32, i64, i64, i64, i64, i32, vp, i64, i64, vp, i64, vp, i32, vp, sz, vp]
+    lib.galore_svd_update.restype = ctypes.c_int
     return lib
 
 
@@ -455,3 +460,29 @@ def galore_lowrank_adam8_step(R: torch.Tensor, state: Adam8State, N=None, beta1=
                                          state.V8.data_ptr(), state.Vs.data_ptr(), rows, cols, batch, beta1, beta2,
                                          eps, t, _stream(stream)), "galore_lowrank_adam8_step")
     return N
+
+
+def galore_svd_workspace_size(m: int, n: int, r: int, batch: int = 1, dtype=torch.float32) -> int:
+    code = GALORE_BF16 if dtype in (torch.bfloat16, GALORE_BF16, "bf16") else GALORE_F32
+    return int(lib.galore_svd_workspace_size(m, n, r, batch, code))
+
+
+def galore_svd_update(G: torch.Tensor, r: int, P=None, sigma=None, info=None, workspace=None, stream=None):
+    """Exact top-r SVD projector of G ((m, n) or (batch, m, n)); returns (P, sigma, info)."""
+    gp, m, n, ldg, sg, batch = _mat(G, "G")
+    s = min(m, n)
+    dev = G.device
+    if P is None:
+        P = torch.empty((batch, s, r) if G.dim() == 3 else (s, r), dtype=torch.float32, device=dev)
+    pp, _, _, ldp, sp, _ = _mat(P, "P")
+    if sigma is None:
+        sigma = torch.empty((batch, r) if G.dim() == 3 else (r,), dtype=torch.float32, device=dev)
+    if info is None:
+        info = torch.empty((batch,), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = torch.empty((max(galore_svd_workspace_size(m, n, r, batch, G.dtype), 1),), dtype=torch.uint8,
+                                device=dev)
+    _check(lib.galore_svd_update(gp, _dtype_code(G), m, n, ldg, sg, r, pp, ldp, sp, sigma.data_ptr(),
+                                 sigma.stride(0) if sigma.dim() == 2 else r, info.data_ptr(), batch,
+                                 workspace.data_ptr(), workspace.numel(), _stream(stream)), "galore_svd_update")
+    return P, sigma, info

@@ -640,6 +640,21 @@ int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t m, int64_t
     return st;
 }
 
+size_t galore_svd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch, int32_t g_dtype) {
+    if (m < 1 || n < 1 || r < 1 || std::min(m, n) > kMaxK) return 0;
+    return galore_rsvd_workspace_size(m, n, r, static_cast<int32_t>(std::min(m, n) - r), batch, g_dtype);
+}
+
+int galore_svd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r,
+                      float* P, int64_t ldp, int64_t stride_p, float* sigma, int64_t stride_sigma, int32_t* info,
+                      int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (m < 1 || n < 1 || r < 1 || std::min(m, n) > kMaxK || r > std::min(m, n)) return GALORE_ERR_SHAPE;
+    // k = s: the sketch spans the whole short side, so no power iteration is needed
+    Tracer tr{nullptr, nullptr, 0, 0, stream};
+    return rsvd_impl(G, g_dtype, m, n, ldg, stride_g, r, static_cast<int32_t>(std::min(m, n) - r), 0, 0, 0, P, ldp,
+                     stride_p, sigma, stride_sigma, info, batch, workspace, workspace_bytes, stream, tr);
+}
+
 // Workspace of the projection with a bf16 gradient: the three bf16 planes of
 // P^T (r x pad8(s) each) per matrix.
 struct ProjLayout {

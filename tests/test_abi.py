@@ -337,3 +337,16 @@ def test_adam8_rejects_and_scale_count():
         assert call(**kw) == -1, kw
     for kw in (dict(rows=0), dict(cols=0), dict(ld=95), dict(b=0), dict(b=2, st=8 * 96 - 1)):
         assert call(**kw) == -2, kw
+
+
+def test_svd_workspace_and_rejects():
+    import paper_2504_20437_amd as gl
+    assert gl.galore_svd_workspace_size(64, 96, 8, 1) == gl.galore_rsvd_workspace_size(64, 96, 8, 56, 1)
+    assert gl.galore_svd_workspace_size(96, 64, 8, 1) == gl.galore_rsvd_workspace_size(96, 64, 8, 56, 1)
+    assert gl.galore_svd_workspace_size(4097, 5000, 8, 1) == 0
+    assert gl.galore_svd_workspace_size(64, 96, 65, 1) == 0
+    f = gl.lib.galore_svd_update
+    args = [FAKE, 0, 64, 96, 96, 0, 8, FAKE, 8, 0, None, 8, None, 1, FAKE - FAKE % 256 + 256, 1 << 40, None]
+    assert f(*args[:2], 4097, 5000, 5000, *args[5:]) == -2
+    assert f(*args[:6], 65, *args[7:]) == -2
+    assert f(NULL, *args[1:]) == -1

@@ -105,3 +105,27 @@ def test_full_size_path(gl, orc, m, n, r, p):
         else:
             ref = np.array([W0h[b][i, j] - c * (Ph[b][j, :] @ Nh[b][:, i]) for i, j in zip(wi, wj)])
         assert max_rel_violation(Wh[b][wi, wj], ref, 1e-5, 1e-6) <= 1.0
+
+
+def test_exact_svd_full_size(gl):
+    """The exact-SVD projector at the bench's shape (4096 x 11008 bf16,
+    (i+1)^-0.7 spectrum + 1e-4 noise, r = 1024, so k = s = 4096): sigma against
+    LAPACK's eigenvalues of G G^T (fp64), relative 5e-4 (the fp32 pipeline's
+    absolute error is about sqrt(s) ulps of sigma_1, and sigma_1 / sigma_r is
+    about 130 here); the residual energy ||G - P P^T G||_F^2 equals the sum of the
+    eigenvalues past r (rank-r optimality) to 1e-6; P^T P = I."""
+    import torch
+    m, n, r = 4096, 11008, 1024
+    G = gi.torch_planted_group(m, n, 1, gi.spectrum_power(m, 0.7), 1e-4, seed=5000, dtype="bf16")
+    P, sig, info = gl.galore_svd_update(G, r)
+    torch.cuda.synchronize()
+    assert int(info.cpu()[0]) == 0
+    g = G[0].double()
+    lam = np.linalg.eigvalsh((g @ g.t().contiguous()).cpu().numpy())[::-1]
+    sv = np.sqrt(lam[:r])
+    s0 = sig[0].double().cpu().numpy()
+    assert np.all(np.abs(s0 - sv) <= 5e-4 * sv)
+    Pd = P[0].double()
+    res = g - Pd @ (Pd.t().contiguous() @ g)
+    assert abs(float((res * res).sum()) - lam[r:].sum()) <= 1e-6 * lam[r:].sum()
+    assert orth_err(P[0].cpu().numpy().astype(np.float64)) < 1e-4

@@ -773,3 +773,25 @@ def test_adam8_matches_oracle(gl, orc, rows, cols, batch):
             den = np.sqrt(v32.astype(np.float64) / bc2) + eps
             tol = 1e-5 * np.abs(No) + 8 * u * (b1 * np.abs(mdec) + (1 - b1) * np.abs(R[i])) / bc1 / den
             assert np.all(np.abs(N[i] - No) <= tol), (t, i)
+
+
+# ---------------------------------------------------------------- exact SVD
+
+
+@pytest.mark.parametrize("m,n,r,dtype", [(256, 700, 32, "f32"), (700, 256, 20, "bf16"), (1024, 1536, 128, "bf16"),
+                                         (520, 1100, 130, "f32")])
+def test_svd_update_matches_oracle(gl, orc, m, n, r, dtype):
+    """The exact-SVD projector (k = s, no power iteration) against the oracle's
+    k = s update (pinned to LAPACK's SVD) on spectra with a gap at r."""
+    s = min(m, n)
+    spec = gi.spectrum_gapped(gi.spectrum_power(s, 0.8), r) + 1e-3 * gi.spectrum_power(s, 0.3)
+    G = gi.store(gi.planted_gradient(m, n, spec, 1e-5, seed=m + 3 * n), dtype)
+    P, sig, info = gl.galore_svd_update(dev_stored(G), r)
+    P, sig = host(P), host(sig)
+    assert int(info.cpu()[0]) == 0
+    Pr, sr, _ = orc.rsvd_update(G.exact, r, s - r, 0, 1)
+    assert orth_err(P) < 1e-4
+    assert max_rel_violation(sig, sr, 1e-4, 1e-30) <= 1.0
+    assert proj_dist(P, Pr) <= 1e-3
+    idx_max = np.argmax(np.abs(P), axis=0)
+    assert np.all(P[idx_max, np.arange(r)] > 0)
