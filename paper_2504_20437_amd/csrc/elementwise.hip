@@ -6,6 +6,10 @@
 //  * lowrank_adam: the low-rank Adam update (paper §3 moment equations and the
 //    bias correction of paper Alg. 1) streaming R, M, V in and M, V, N out:
 //    24 bytes per element, one pass over HBM, 16-byte vector accesses.
+//  * align: the subspace switch's column-sign matching of a new projector to
+//    the previous one (paper §4.1.3 sign indeterminacy).
+//  * copy_rows: batched strided copy (the previous projector and first moment
+//    kept for the switch inside the scheduled step).
 #include "common.hpp"
 
 namespace galore {
