@@ -72,6 +72,8 @@ def _load():
         lib.orc_philox4x64_10.restype = None
         lib.orc_normal_from_words.argtypes = [u64, u64]
         lib.orc_normal_from_words.restype = ctypes.c_double
+        lib.orc_round_bf16.argtypes = [ctypes.c_double]
+        lib.orc_round_bf16.restype = ctypes.c_double
         lib.orc_sketch.argtypes = [i64, i64, u64, u64, _f64p]
         lib.orc_sketch.restype = None
         lib.orc_householder_qr.argtypes = [i64, i64, _f64p, _f64p, _f64p]
@@ -134,8 +136,14 @@ def normal_from_words(x0: int, x1: int) -> float:
     return float(_load().orc_normal_from_words(int(x0), int(x1)))
 
 
+def round_bf16(z: float) -> float:
+    """The bfloat16 value nearest to the fp64 z (ties to even), rounded once."""
+    return float(_load().orc_round_bf16(float(z)))
+
+
 def sketch(l: int, k: int, seed: int, sketch_index: int = 0) -> np.ndarray:
-    """Omega (l x k) as fp64 holding fp32-rounded N(0,1) draws."""
+    """Omega (l x k) as fp64 holding bfloat16-rounded N(0,1) draws (two rows per
+    Philox block)."""
     out = np.zeros((l, k), dtype=np.float64)
     _load().orc_sketch(l, k, seed, sketch_index, _ptr(out))
     return out

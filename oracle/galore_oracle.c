@@ -79,16 +79,30 @@ ORC_API double orc_normal_from_words(uint64_t x0, uint64_t x1) {
     return sqrt(-2.0 * log(u1)) * cos(two_pi * u2);
 }
 
+/* fp64 -> nearest bfloat16 value (8 significant bits, ties to even), rounded */
+/* once from the fp64 value; finite nonzero inputs in bfloat16's normal range. */
+ORC_API double orc_round_bf16(double z) {
+    if (z == 0.0 || !isfinite(z)) return z;
+    int e;
+    const double m = frexp(z, &e);            /* |m| in [0.5, 1) */
+    return ldexp(rint(ldexp(m, 8)), e - 8);   /* rint: round half to even */
+}
+
+/* Entries (2 i2, j) and (2 i2 + 1, j) of the l x k sketch share one Philox   */
+/* block: counter (j * ceil(l / 2) + i2, sketch_index, 0, 0), key (seed, 0);  */
+/* words 0, 1 give the even row's normal and words 2, 3 the odd row's. Each   */
+/* entry is the Box-Muller normal rounded to bfloat16.                         */
 ORC_API void orc_sketch(int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index, double* omega) {
+    const int64_t l2 = (l + 1) / 2;
     #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < l; ++i) {
         for (int64_t j = 0; j < k; ++j) {
-            uint64_t ctr[4] = {(uint64_t)(j * l + i), sketch_index, 0, 0};
+            uint64_t ctr[4] = {(uint64_t)(j * l2 + i / 2), sketch_index, 0, 0};
             uint64_t key[2] = {seed, 0};
             uint64_t w[4];
             orc_philox4x64_10(ctr, key, w);
-            double z = orc_normal_from_words(w[0], w[1]);
-            omega[i * k + j] = (double)(float)z;
+            const double z = (i % 2 == 0) ? orc_normal_from_words(w[0], w[1]) : orc_normal_from_words(w[2], w[3]);
+            omega[i * k + j] = orc_round_bf16(z);
         }
     }
 }

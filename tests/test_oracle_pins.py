@@ -55,31 +55,58 @@ def test_box_muller_edges(orc):
 
 
 def test_sketch_is_standard_normal(orc):
-    """Halko §4 needs i.i.d. N(0,1) entries: moments and a KS test on 1e6 draws."""
+    """Halko §4 needs i.i.d. N(0,1) entries: moments of 1e6 sketch entries, and a
+    KS test of the normals before their bfloat16 rounding (the rounded values
+    form a lattice, which a continuous KS test would reject by construction;
+    the rounding moves each entry by at most 2^-8 of its magnitude)."""
     from scipy import stats
     om = orc.sketch(1000, 1000, seed=7, sketch_index=3)
     x = om.ravel()
     assert abs(x.mean()) < 5e-3
     assert abs(x.var() - 1.0) < 5e-3
     assert abs(stats.skew(x)) < 1e-2 and abs(stats.kurtosis(x)) < 2e-2
-    assert stats.kstest(x, "norm").pvalue > 1e-3
-    # independent columns / rows: the sample correlation of neighbours is tiny
+    rng = np.random.default_rng(8)
+    z = np.array([orc.normal_from_words(int(a), int(b))
+                  for a, b in rng.integers(0, 2 ** 63, size=(20000, 2), dtype=np.int64) * 2 + 1])
+    assert stats.kstest(z, "norm").pvalue > 1e-3
+    # independent columns / rows (including the two rows of one Philox block)
     assert abs(np.corrcoef(om[:, 0], om[:, 1])[0, 1]) < 0.15
     assert abs(np.mean(om[:-1, :] * om[1:, :])) < 5e-3
+    assert abs(np.mean(om[0::2, :] * om[1::2, :])) < 5e-3
+
+
+def test_round_bf16_ties_and_single_rounding(orc):
+    """bfloat16 keeps 8 significant bits: near 1 the spacing is 2^-7. 1 + 2^-8 is
+    a tie and goes to the even 1.0; 1 + 3 * 2^-8 goes to the even 1 + 2^-6; 1 +
+    2^-8 + 2^-30 lies above the tie and rounds up (rounding through binary32
+    first would lose the 2^-30 and round down); signs are symmetric."""
+    assert orc.round_bf16(1 + 2.0 ** -8) == 1.0
+    assert orc.round_bf16(1 + 3 * 2.0 ** -8) == 1 + 2.0 ** -6
+    assert orc.round_bf16(1 + 2.0 ** -8 + 2.0 ** -30) == 1 + 2.0 ** -7
+    assert orc.round_bf16(-(1 + 2.0 ** -8 + 2.0 ** -30)) == -(1 + 2.0 ** -7)
+    assert orc.round_bf16(3.0) == 3.0 and orc.round_bf16(0.0) == 0.0
 
 
 def test_sketch_structure(orc):
     a = orc.sketch(37, 9, seed=11, sketch_index=0)
     b = orc.sketch(37, 5, seed=11, sketch_index=0)
     assert np.array_equal(a[:, :5], b)                      # columns do not depend on k
-    assert np.array_equal(a.astype(np.float32).astype(np.float64), a)   # fp32 values
+    bits = a.astype(np.float32).view(np.uint32)
+    assert np.array_equal(a.astype(np.float32).astype(np.float64), a) and not np.any(bits & 0xFFFF)   # bf16 values
     c = orc.sketch(37, 9, seed=11, sketch_index=1)
     d = orc.sketch(37, 9, seed=12, sketch_index=0)
     assert not np.any(a == c) or np.mean(a == c) < 0.05
     assert np.mean(a == d) < 0.05
-    # entry (i, j) uses counter e = j*l + i, key (seed, 0), words 0 and 1
-    w = orc.philox4x64_10([4 * 37 + 10, 0, 0, 0], [11, 0])
-    assert a[10, 4] == np.float64(np.float32(orc.normal_from_words(int(w[0]), int(w[1]))))
+    # entries (2 i2, j) and (2 i2 + 1, j) use counter j * ceil(l / 2) + i2, key
+    # (seed, 0): words 0, 1 for the even row and 2, 3 for the odd row, rounded
+    # to bfloat16 (within half its spacing, at most 2^-8 relative)
+    w = orc.philox4x64_10([4 * 19 + 5, 0, 0, 0], [11, 0])
+    z0, z1 = orc.normal_from_words(int(w[0]), int(w[1])), orc.normal_from_words(int(w[2]), int(w[3]))
+    assert a[10, 4] == orc.round_bf16(z0) and a[11, 4] == orc.round_bf16(z1)
+    assert abs(a[10, 4] - z0) <= 2.0 ** -8 * abs(z0) and abs(a[11, 4] - z1) <= 2.0 ** -8 * abs(z1)
+    # the last row of an odd l uses the even words of its block
+    w = orc.philox4x64_10([2 * 19 + 18, 0, 0, 0], [11, 0])
+    assert a[36, 2] == orc.round_bf16(orc.normal_from_words(int(w[0]), int(w[1])))
 
 
 # ---------------------------------------------------------------- Householder QR
