@@ -90,6 +90,11 @@ hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const G
 
 hipError_t launch_sketch(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
                          uint64_t sketch_index0, int batch, hipStream_t stream);
+// the sketch as the one bf16 plane of Omega^T (k rows of ldp, zero past l);
+// zero_rest also zeroes the next two planes
+hipError_t launch_sketch_plane(uint16_t* planes, int64_t ldp, int64_t planeStride, int64_t stride, int64_t l,
+                               int64_t k, uint64_t seed, uint64_t sketch_index0, bool zero_rest, int batch,
+                               hipStream_t stream);
 
 // Cholesky of the k x k fp64 Gram (in place, upper factor R in the upper
 // triangle). xinv (k x k fp64) receives the inverses of the diagonal blocks

@@ -251,9 +251,11 @@ struct Tracer {
         if ((tr).end() != hipSuccess) return GALORE_ERR_HIP;  \
     } while (0)
 
-// Y (s x k) = A X, X (l x k)
+// Y (s x k) = A X, X (l x k). With planes1 (bf16 G only) X is not read: the
+// planes already hold X^T as one bf16 plane (exact), two more zero planes when
+// the product cannot read G in place.
 int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, float* Y, int64_t strideY,
-              bool& cmax_ready) {
+              bool& cmax_ready, bool planes1 = false) {
     const Shape& sh = *P.sh;
     const Layout& L = *P.L;
     cmax_ready = false;
@@ -262,9 +264,10 @@ int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, fl
         return GALORE_OK;
     }
     const int k = sh.k, s = static_cast<int>(sh.s), l = static_cast<int>(sh.l);
-    GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
-                  launch_split3_transpose(X, k, strideX, P.planes, L.ldpl, L.planeStride, L.stridePl, l, k,
-                                          static_cast<int>(L.ldpl), P.batch, P.st));
+    if (!planes1)
+        GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
+                      launch_split3_transpose(X, k, strideX, P.planes, L.ldpl, L.planeStride, L.stridePl, l, k,
+                                              static_cast<int>(L.ldpl), P.batch, P.st));
     // left: A = G (K-contiguous); right: A = G^T, read in place (M-contiguous)
     // or from the transposed copy
     const bool inplace = sh.left || P.direct;
@@ -275,7 +278,8 @@ int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, fl
     GALORE_TRACED(tr, GALORE_STAGE_PRODUCT_A,
                   launch_gemm_bf16x3(A, lda, strideA, sh.left ? 0 : (P.direct ? 1 : 0), P.planes, L.ldpl,
                                      L.planeStride, L.stridePl, Y, k, strideY, 0, s, k, l, 1.0f, 0.0f, P.batch,
-                                     P.st, cmax_ready ? P.cmax : nullptr, P.strideCM));
+                                     P.st, cmax_ready ? P.cmax : nullptr, P.strideCM,
+                                     (planes1 && P.direct) ? 1 : 3));
     return GALORE_OK;
 }
 
@@ -458,9 +462,15 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                                                 static_cast<int>(n), batch, stream));
     }
 
-    // a1-a3: sketch, range sample, orthonormalise
-    GALORE_TRACED(tr, GALORE_STAGE_SKETCH, launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
-    GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Sa, L.strideS, ready));
+    // a1-a3: sketch, range sample, orthonormalise (a bf16 G takes the sketch as
+    // the bf16 plane of its transpose: one exact bf16 product)
+    if (L.bf16)
+        GALORE_TRACED(tr, GALORE_STAGE_SKETCH,
+                      launch_sketch_plane(prod.planes, L.ldpl, L.planeStride, L.stridePl, l, k, seed, sketch_index0,
+                                          !prod.direct, batch, stream));
+    else
+        GALORE_TRACED(tr, GALORE_STAGE_SKETCH, launch_sketch(L1, l, k, L.strideL, seed, sketch_index0, batch, stream));
+    GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Sa, L.strideS, ready, L.bf16));
     float* Q = Sa;
     float* Qtmp = Sb;
     auto orth_s = [&](int passes) -> int {

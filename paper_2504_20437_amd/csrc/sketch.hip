@@ -1,14 +1,20 @@
 // Gaussian sketch for the randomized range finder (Halko, Martinsson & Tropp
 // 2011, §4), adopted for the subspace update in paper §4.1.2.
 //
-// Counter-based: entry (i, j) of the l x k sketch is a pure function of
-// (seed, sketch index, j*l + i), so any thread can produce any entry, batches
-// of matrices get independent sketches through the second counter word, and a
-// column does not depend on k.
+// Counter-based: entries (2 i2, j) and (2 i2 + 1, j) of the l x k sketch are a
+// pure function of (seed, sketch index, j * ceil(l/2) + i2), so any thread can
+// produce any pair, batches of matrices get independent sketches through the
+// second counter word, and a column does not depend on k.
 //   Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011): key (seed, 0),
-//   counter (j*l + i, sketch_index, 0, 0); output words 0 and 1.
+//   counter (j * ceil(l/2) + i2, sketch_index, 0, 0); output words 0, 1 give
+//   row 2 i2 and words 2, 3 row 2 i2 + 1.
 //   Box-Muller (1958) in fp64 on the top 53 bits: u1 in (0, 1], u2 in [0, 1),
-//   z = sqrt(-2 ln u1) cos(2 pi u2); the entry is z rounded to fp32.
+//   z = sqrt(-2 ln u1) cos(2 pi u2); the entry is z rounded once to the
+//   nearest bfloat16 (ties to even).
+// The sketch is written either as fp32 values (row-major l x k), or, for the
+// bf16 matrix cores, directly as the one bf16 plane of its transpose (k rows
+// of ldp, zero past l): with a bf16-valued sketch the first range sample A
+// Omega is a single exact bf16 product.
 #include "common.hpp"
 
 namespace galore {
@@ -47,33 +53,91 @@ __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
     return out;
 }
 
-__global__ __launch_bounds__(256) void sketch_kernel(float* omega, int64_t l, int64_t k,
-                                                     int64_t stride, uint64_t seed,
+__device__ __forceinline__ double normal_from(uint64_t x0, uint64_t x1) {
+    const double two_pow_m53 = 1.0 / 9007199254740992.0;
+    const double two_pi = 6.283185307179586;
+    const double u1 = static_cast<double>((x0 >> 11) + 1) * two_pow_m53;
+    const double u2 = static_cast<double>(x1 >> 11) * two_pow_m53;
+    return sqrt(-2.0 * log(u1)) * cos(two_pi * u2);
+}
+
+// bits of the bfloat16 nearest to z (ties to even), rounded once from fp64
+__device__ __forceinline__ uint32_t bf16_bits(double z) {
+    if (z == 0.0) return signbit(z) ? 0x8000u : 0u;
+    int e;
+    const double m = frexp(z, &e);
+    const double r = ldexp(rint(ldexp(m, 8)), e - 8);   // 8 significant bits: exact in fp32
+    return __float_as_uint(static_cast<float>(r)) >> 16;
+}
+
+// fp32 values, row-major l x k; one thread per row pair and column
+__global__ __launch_bounds__(256) void sketch_kernel(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
                                                      uint64_t sketch_index0) {
     const int b = blockIdx.y;
     float* out = omega + static_cast<int64_t>(b) * stride;
     const uint64_t sidx = sketch_index0 + static_cast<uint64_t>(b);
-    const int64_t total = l * k;
-    const double two_pow_m53 = 1.0 / 9007199254740992.0;
-    const double two_pi = 6.283185307179586;
+    const int64_t l2 = (l + 1) / 2;
+    const int64_t total = l2 * k;
     for (int64_t pos = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; pos < total;
          pos += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t i = pos / k;
-        const int64_t j = pos - i * k;
-        const uint64_t e = static_cast<uint64_t>(j * l + i);
-        const u64x4 w = philox4x64_10(e, sidx, 0, 0, seed, 0);
-        const double u1 = static_cast<double>((w.v[0] >> 11) + 1) * two_pow_m53;
-        const double u2 = static_cast<double>(w.v[1] >> 11) * two_pow_m53;
-        const double z = sqrt(-2.0 * log(u1)) * cos(two_pi * u2);
-        out[pos] = static_cast<float>(z);
+        const int64_t i2 = pos / k;
+        const int64_t j = pos - i2 * k;
+        const u64x4 w = philox4x64_10(static_cast<uint64_t>(j * l2 + i2), sidx, 0, 0, seed, 0);
+        out[2 * i2 * k + j] = __uint_as_float(bf16_bits(normal_from(w.v[0], w.v[1])) << 16);
+        if (2 * i2 + 1 < l) out[(2 * i2 + 1) * k + j] = __uint_as_float(bf16_bits(normal_from(w.v[2], w.v[3])) << 16);
+    }
+}
+
+// the bf16 plane of Omega^T: plane[j][i] = Omega[i][j] (k rows of ldp, zero for
+// l <= i < ldp); with zero_rest the next two planes (at planeStride) are zeroed
+__global__ __launch_bounds__(256) void sketch_plane_kernel(uint16_t* planes, int64_t ldp, int64_t planeStride,
+                                                           int64_t stride, int64_t l, int64_t k, uint64_t seed,
+                                                           uint64_t sketch_index0, int zero_rest) {
+    const int b = blockIdx.y;
+    uint16_t* pl = planes + static_cast<int64_t>(b) * stride;
+    const uint64_t sidx = sketch_index0 + static_cast<uint64_t>(b);
+    const int64_t l2 = (l + 1) / 2;
+    const int64_t half = ldp / 2;           // ldp is even
+    const int64_t total = k * half;
+    for (int64_t pos = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; pos < total;
+         pos += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t j = pos / half;
+        const int64_t i2 = pos - j * half;
+        uint32_t v = 0;
+        if (2 * i2 < l) {
+            const u64x4 w = philox4x64_10(static_cast<uint64_t>(j * l2 + i2), sidx, 0, 0, seed, 0);
+            v = bf16_bits(normal_from(w.v[0], w.v[1]));
+            if (2 * i2 + 1 < l) v |= bf16_bits(normal_from(w.v[2], w.v[3])) << 16;
+        }
+        uint32_t* dst = reinterpret_cast<uint32_t*>(pl + j * ldp + 2 * i2);
+        dst[0] = v;
+        if (zero_rest) {
+            *reinterpret_cast<uint32_t*>(pl + planeStride + j * ldp + 2 * i2) = 0u;
+            *reinterpret_cast<uint32_t*>(pl + 2 * planeStride + j * ldp + 2 * i2) = 0u;
+        }
     }
 }
 
 }  // namespace
 
+hipError_t launch_sketch_plane(uint16_t* planes, int64_t ldp, int64_t planeStride, int64_t stride, int64_t l,
+                               int64_t k, uint64_t seed, uint64_t sketch_index0, bool zero_rest, int batch,
+                               hipStream_t stream) {
+    if (ldp % 2 != 0 || ldp < l || planeStride % 2 != 0 || stride % 2 != 0 ||
+        reinterpret_cast<uintptr_t>(planes) % 4 != 0)
+        return hipErrorInvalidValue;
+    const int64_t total = k * (ldp / 2);
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    dim3 grid(static_cast<unsigned>(blocks), batch);
+    hipLaunchKernelGGL(sketch_plane_kernel, grid, dim3(256), 0, stream, planes, ldp, planeStride, stride, l, k, seed,
+                       sketch_index0, zero_rest ? 1 : 0);
+    return hipGetLastError();
+}
+
 hipError_t launch_sketch(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
                          uint64_t sketch_index0, int batch, hipStream_t stream) {
-    const int64_t total = l * k;
+    const int64_t total = (l + 1) / 2 * k;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     dim3 grid(static_cast<unsigned>(blocks), batch);
