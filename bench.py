@@ -317,10 +317,18 @@ def main():
             per_stage[st] += d
             if st != "rsvd":
                 launches.setdefault(st, []).append(d)
+        first_a = True
         for i, name in enumerate(stl):
             d = sev[2 * i].elapsed_time(sev[2 * i + 1])
             sub[name] = sub.get(name, 0.0) + d
-            launches.setdefault(name, []).append(d)
+            # with a bf16 gradient the first A product takes the bf16-valued sketch
+            # as one exact plane: a different launch shape, timed on its own
+            key = name
+            if name == "product_A" and first_a:
+                first_a = False
+                if args.dtype == "bf16":
+                    key = "product_A_sketch"
+            launches.setdefault(key, []).append(d)
     per_stage = {st: v / args.steps for st, v in per_stage.items()}
     sub = {st: v / args.steps for st, v in sub.items()}
     ms_per_step = wall * 1000.0 / args.steps
@@ -336,6 +344,7 @@ def main():
     prod_bound = "mfma_bf16x3" if args.dtype == "bf16" else "mfma"
     work = {
         "product_A": (prod_bound, 2.0 * s * l * k * C),
+        "product_A_sketch": ("mfma_bf16" if args.dtype == "bf16" else "mfma", 2.0 * s * l * k * C),
         "product_At": (prod_bound, 2.0 * s * l * k * C),
         "projector": ("mfma", 2.0 * s * k * r * C),
         "project": (prod_bound, 2.0 * r * s * l * C),
@@ -380,6 +389,7 @@ def main():
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
     else:
         peak = {"mfma": FP32_MFMA_PEAK_TFS, "mfma64": FP64_MFMA_PEAK_TFS, "mfma_bf16x3": BF16_MFMA_PEAK_TFS,
+                "mfma_bf16": BF16_MFMA_PEAK_TFS,
                 "mfma_bf16x6": BF16_MFMA_PEAK_TFS, "mfma_i8x9": INT8_MFMA_PEAK_TOPS}[bound]
         ach = units / (avg_ms * 1e-3) / 1e12
         roof = {"kernel": kern, "bound": "mfma", "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
