@@ -72,6 +72,8 @@ def _load():
         lib.orc_philox4x64_10.restype = None
         lib.orc_normal_from_words.argtypes = [u64, u64]
         lib.orc_normal_from_words.restype = ctypes.c_double
+        lib.orc_normal_pair_from_words.argtypes = [u64, u64, _f64p]
+        lib.orc_normal_pair_from_words.restype = None
         lib.orc_round_bf16.argtypes = [ctypes.c_double]
         lib.orc_round_bf16.restype = ctypes.c_double
         lib.orc_sketch.argtypes = [i64, i64, u64, u64, _f64p]
@@ -136,14 +138,21 @@ def normal_from_words(x0: int, x1: int) -> float:
     return float(_load().orc_normal_from_words(int(x0), int(x1)))
 
 
+def normal_pair_from_words(x0: int, x1: int):
+    """(r cos 2 pi u2, r sin 2 pi u2): both normals of the Box-Muller pair."""
+    z = np.zeros(2)
+    _load().orc_normal_pair_from_words(x0, x1, _ptr(z))
+    return float(z[0]), float(z[1])
+
+
 def round_bf16(z: float) -> float:
     """The bfloat16 value nearest to the fp64 z (ties to even), rounded once."""
     return float(_load().orc_round_bf16(float(z)))
 
 
 def sketch(l: int, k: int, seed: int, sketch_index: int = 0) -> np.ndarray:
-    """Omega (l x k) as fp64 holding bfloat16-rounded N(0,1) draws (two rows per
-    Philox block)."""
+    """Omega (l x k) as fp64 holding bfloat16-rounded N(0,1) draws (four rows per
+    Philox block: two Box-Muller pairs)."""
     out = np.zeros((l, k), dtype=np.float64)
     _load().orc_sketch(l, k, seed, sketch_index, _ptr(out))
     return out

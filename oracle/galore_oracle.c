@@ -88,21 +88,40 @@ ORC_API double orc_round_bf16(double z) {
     return ldexp(rint(ldexp(m, 8)), e - 8);   /* rint: round half to even */
 }
 
-/* Entries (2 i2, j) and (2 i2 + 1, j) of the l x k sketch share one Philox   */
-/* block: counter (j * ceil(l / 2) + i2, sketch_index, 0, 0), key (seed, 0);  */
-/* words 0, 1 give the even row's normal and words 2, 3 the odd row's. Each   */
-/* entry is the Box-Muller normal rounded to bfloat16.                         */
+/* Both normals of one Box-Muller pair (1958): radius sqrt(-2 ln u1) times   */
+/* cos and sin of 2 pi u2, u1 and u2 from the top 53 bits of x0 and x1 as in */
+/* orc_normal_from_words (which is the cos member).                           */
+ORC_API void orc_normal_pair_from_words(uint64_t x0, uint64_t x1, double* z) {
+    const double two_pow_m53 = 1.0 / 9007199254740992.0; /* 2^-53 */
+    const double u1 = (double)((x0 >> 11) + 1) * two_pow_m53;
+    const double u2 = (double)(x1 >> 11) * two_pow_m53;
+    const double two_pi = 6.283185307179586;
+    const double rad = sqrt(-2.0 * log(u1));
+    z[0] = rad * cos(two_pi * u2);
+    z[1] = rad * sin(two_pi * u2);
+}
+
+/* Entries (4 i4 + t, j), t = 0..3, of the l x k sketch share one Philox      */
+/* block: counter (j * ceil(l / 4) + i4, sketch_index, 0, 0), key (seed, 0);  */
+/* words 0, 1 give the Box-Muller pair of rows 4 i4 and 4 i4 + 1 (cos, sin)   */
+/* and words 2, 3 the pair of rows 4 i4 + 2 and 4 i4 + 3. Each entry is its   */
+/* normal rounded once to bfloat16.                                           */
 ORC_API void orc_sketch(int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index, double* omega) {
-    const int64_t l2 = (l + 1) / 2;
+    const int64_t l4 = (l + 3) / 4;
     #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < l; ++i) {
         for (int64_t j = 0; j < k; ++j) {
-            uint64_t ctr[4] = {(uint64_t)(j * l2 + i / 2), sketch_index, 0, 0};
+            uint64_t ctr[4] = {(uint64_t)(j * l4 + i / 4), sketch_index, 0, 0};
             uint64_t key[2] = {seed, 0};
             uint64_t w[4];
+            double z[2];
             orc_philox4x64_10(ctr, key, w);
-            const double z = (i % 2 == 0) ? orc_normal_from_words(w[0], w[1]) : orc_normal_from_words(w[2], w[3]);
-            omega[i * k + j] = orc_round_bf16(z);
+            const int t = (int)(i % 4);
+            if (t < 2)
+                orc_normal_pair_from_words(w[0], w[1], z);
+            else
+                orc_normal_pair_from_words(w[2], w[3], z);
+            omega[i * k + j] = orc_round_bf16(z[t % 2]);
         }
     }
 }

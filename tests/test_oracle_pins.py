@@ -43,6 +43,19 @@ def test_philox_matches_numpy_bit_generator(orc, seed):
         assert np.array_equal(got.astype(np.uint64), ref.astype(np.uint64))
 
 
+def test_box_muller_pair(orc):
+    """The pair's radius is shared: z0^2 + z1^2 = -2 ln u1; u2 = 1/4 puts the
+    whole radius in the sin member, u2 = 0 in the cos member."""
+    r2 = -2.0 * np.log(2.0 ** -53)
+    z0, z1 = orc.normal_pair_from_words(0, 1 << 62)          # u1 = 2^-53, u2 = 1/4
+    assert abs(z0) < 1e-12 and abs(z1 - np.sqrt(r2)) < 1e-12
+    z0, z1 = orc.normal_pair_from_words(0, 0)
+    assert abs(z0 - np.sqrt(r2)) < 1e-12 and z1 == 0.0
+    z0, z1 = orc.normal_pair_from_words(12345 << 11, 777 << 20)
+    u1 = (12345 + 1) * 2.0 ** -53
+    assert abs(z0 * z0 + z1 * z1 + 2.0 * np.log(u1)) < 1e-12
+
+
 def test_box_muller_edges(orc):
     # u1 = 1 exactly (all top bits set) -> radius 0
     assert orc.normal_from_words(U64, 12345) == 0.0
@@ -69,10 +82,12 @@ def test_sketch_is_standard_normal(orc):
     z = np.array([orc.normal_from_words(int(a), int(b))
                   for a, b in rng.integers(0, 2 ** 63, size=(20000, 2), dtype=np.int64) * 2 + 1])
     assert stats.kstest(z, "norm").pvalue > 1e-3
-    # independent columns / rows (including the two rows of one Philox block)
+    # independent columns / rows (including the rows of one Philox block: the
+    # two members of a Box-Muller pair, and the two pairs)
     assert abs(np.corrcoef(om[:, 0], om[:, 1])[0, 1]) < 0.15
     assert abs(np.mean(om[:-1, :] * om[1:, :])) < 5e-3
-    assert abs(np.mean(om[0::2, :] * om[1::2, :])) < 5e-3
+    for a, b in ((0, 1), (2, 3), (0, 2), (1, 3)):
+        assert abs(np.mean(om[a::4, :] * om[b::4, :])) < 1e-2
 
 
 def test_round_bf16_ties_and_single_rounding(orc):
@@ -97,16 +112,19 @@ def test_sketch_structure(orc):
     d = orc.sketch(37, 9, seed=12, sketch_index=0)
     assert not np.any(a == c) or np.mean(a == c) < 0.05
     assert np.mean(a == d) < 0.05
-    # entries (2 i2, j) and (2 i2 + 1, j) use counter j * ceil(l / 2) + i2, key
-    # (seed, 0): words 0, 1 for the even row and 2, 3 for the odd row, rounded
-    # to bfloat16 (within half its spacing, at most 2^-8 relative)
-    w = orc.philox4x64_10([4 * 19 + 5, 0, 0, 0], [11, 0])
-    z0, z1 = orc.normal_from_words(int(w[0]), int(w[1])), orc.normal_from_words(int(w[2]), int(w[3]))
-    assert a[10, 4] == orc.round_bf16(z0) and a[11, 4] == orc.round_bf16(z1)
-    assert abs(a[10, 4] - z0) <= 2.0 ** -8 * abs(z0) and abs(a[11, 4] - z1) <= 2.0 ** -8 * abs(z1)
-    # the last row of an odd l uses the even words of its block
-    w = orc.philox4x64_10([2 * 19 + 18, 0, 0, 0], [11, 0])
-    assert a[36, 2] == orc.round_bf16(orc.normal_from_words(int(w[0]), int(w[1])))
+    # entries (4 i4 + t, j) use counter j * ceil(l / 4) + i4, key (seed, 0):
+    # words 0, 1 give rows 4 i4 and 4 i4 + 1 (cos and sin of one Box-Muller
+    # pair), words 2, 3 rows 4 i4 + 2 and 4 i4 + 3; each rounded to bfloat16
+    # (within half its spacing, at most 2^-8 relative)
+    w = orc.philox4x64_10([4 * 10 + 2, 0, 0, 0], [11, 0])
+    z = orc.normal_pair_from_words(int(w[0]), int(w[1])) + orc.normal_pair_from_words(int(w[2]), int(w[3]))
+    assert z[0] == orc.normal_from_words(int(w[0]), int(w[1]))
+    for t in range(4):
+        assert a[8 + t, 4] == orc.round_bf16(z[t])
+        assert abs(a[8 + t, 4] - z[t]) <= 2.0 ** -8 * abs(z[t])
+    # the last row (l = 37 = 4 * 9 + 1) uses the cos member of its block's first pair
+    w = orc.philox4x64_10([2 * 10 + 9, 0, 0, 0], [11, 0])
+    assert a[36, 2] == orc.round_bf16(orc.normal_pair_from_words(int(w[0]), int(w[1]))[0])
 
 
 # ---------------------------------------------------------------- Householder QR
