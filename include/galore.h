@@ -64,12 +64,13 @@ GALORE_API int galore_version(void);
 /*
  * Gaussian sketch (randomized range finder of Halko, Martinsson & Tropp 2011,
  * adopted by paper §4.1.2): writes the l x k fp32 matrix Omega (row-major,
- * ld = k). Entries (2 i2, j) and (2 i2 + 1, j) share one Philox4x64-10 block
- * (Salmon et al. 2011) with key (seed, 0) and counter (j * ceil(l/2) + i2,
- * sketch_index, 0, 0); for the even row the top 53 bits of output words 0 and
- * 1 (for the odd row, of words 2 and 3) give u1 in (0,1] and u2 in [0,1), and
- * the entry is sqrt(-2 ln u1) cos(2 pi u2) computed in fp64 (Box-Muller) and
- * rounded once to the nearest bfloat16 (ties to even), stored as fp32.
+ * ld = k). Entries (4 i4 + t, j), t = 0..3, share one Philox4x64-10 block
+ * (Salmon et al. 2011) with key (seed, 0) and counter (j * ceil(l/4) + i4,
+ * sketch_index, 0, 0); the top 53 bits of output words 0 and 1 give u1 in
+ * (0,1] and u2 in [0,1) for rows 4 i4 (sqrt(-2 ln u1) cos(2 pi u2)) and 4 i4 + 1
+ * (the sin member of the same Box-Muller pair), words 2 and 3 likewise for rows
+ * 4 i4 + 2 and 4 i4 + 3; each normal is computed in fp64 and rounded once to
+ * the nearest bfloat16 (ties to even), stored as fp32.
  * Exposed so that callers and tests can inspect the sketch the subspace
  * update uses. Errors: omega NULL -> INVALID_ARG; l < 1 or k < 1 -> SHAPE.
  */

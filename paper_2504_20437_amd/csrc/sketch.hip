@@ -1,16 +1,17 @@
 // Gaussian sketch for the randomized range finder (Halko, Martinsson & Tropp
 // 2011, §4), adopted for the subspace update in paper §4.1.2.
 //
-// Counter-based: entries (2 i2, j) and (2 i2 + 1, j) of the l x k sketch are a
-// pure function of (seed, sketch index, j * ceil(l/2) + i2), so any thread can
-// produce any pair, batches of matrices get independent sketches through the
+// Counter-based: entries (4 i4 + t, j), t = 0..3, of the l x k sketch are a
+// pure function of (seed, sketch index, j * ceil(l/4) + i4), so any thread can
+// produce any group, batches of matrices get independent sketches through the
 // second counter word, and a column does not depend on k.
 //   Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011): key (seed, 0),
-//   counter (j * ceil(l/2) + i2, sketch_index, 0, 0); output words 0, 1 give
-//   row 2 i2 and words 2, 3 row 2 i2 + 1.
+//   counter (j * ceil(l/4) + i4, sketch_index, 0, 0); output words 0, 1 give
+//   the Box-Muller pair of rows 4 i4 and 4 i4 + 1, words 2, 3 that of rows
+//   4 i4 + 2 and 4 i4 + 3.
 //   Box-Muller (1958) in fp64 on the top 53 bits: u1 in (0, 1], u2 in [0, 1),
-//   z = sqrt(-2 ln u1) cos(2 pi u2); the entry is z rounded once to the
-//   nearest bfloat16 (ties to even).
+//   radius sqrt(-2 ln u1) times cos and sin of 2 pi u2; each entry is rounded
+//   once to the nearest bfloat16 (ties to even).
 // The sketch is written either as fp32 values (row-major l x k), or, for the
 // bf16 matrix cores, directly as the one bf16 plane of its transpose (k rows
 // of ldp, zero past l): with a bf16-valued sketch the first range sample A
@@ -53,12 +54,16 @@ __device__ __forceinline__ u64x4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_
     return out;
 }
 
-__device__ __forceinline__ double normal_from(uint64_t x0, uint64_t x1) {
+__device__ __forceinline__ void normal_pair(uint64_t x0, uint64_t x1, double& z0, double& z1) {
     const double two_pow_m53 = 1.0 / 9007199254740992.0;
     const double two_pi = 6.283185307179586;
     const double u1 = static_cast<double>((x0 >> 11) + 1) * two_pow_m53;
     const double u2 = static_cast<double>(x1 >> 11) * two_pow_m53;
-    return sqrt(-2.0 * log(u1)) * cos(two_pi * u2);
+    const double rad = sqrt(-2.0 * log(u1));
+    double sn, cs;
+    sincos(two_pi * u2, &sn, &cs);
+    z0 = rad * cs;
+    z1 = rad * sn;
 }
 
 // bits of the bfloat16 nearest to z (ties to even), rounded once from fp64
@@ -70,21 +75,40 @@ __device__ __forceinline__ uint32_t bf16_bits(double z) {
     return __float_as_uint(static_cast<float>(r)) >> 16;
 }
 
-// fp32 values, row-major l x k; one thread per row pair and column
+// the four entries of group (i4, j) as bf16 bits (rows past l are not drawn)
+__device__ __forceinline__ void group4(int64_t l, int64_t l4, int64_t i4, int64_t j, uint64_t sidx, uint64_t seed,
+                                       uint32_t* h) {
+    const u64x4 w = philox4x64_10(static_cast<uint64_t>(j * l4 + i4), sidx, 0, 0, seed, 0);
+    double z0, z1, z2, z3;
+    normal_pair(w.v[0], w.v[1], z0, z1);
+    h[0] = bf16_bits(z0);
+    h[1] = bf16_bits(z1);
+    if (4 * i4 + 2 < l) {
+        normal_pair(w.v[2], w.v[3], z2, z3);
+        h[2] = bf16_bits(z2);
+        h[3] = bf16_bits(z3);
+    } else {
+        h[2] = h[3] = 0u;
+    }
+}
+
+// fp32 values, row-major l x k; one thread per group of four rows and column
 __global__ __launch_bounds__(256) void sketch_kernel(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
                                                      uint64_t sketch_index0) {
     const int b = blockIdx.y;
     float* out = omega + static_cast<int64_t>(b) * stride;
     const uint64_t sidx = sketch_index0 + static_cast<uint64_t>(b);
-    const int64_t l2 = (l + 1) / 2;
-    const int64_t total = l2 * k;
+    const int64_t l4 = (l + 3) / 4;
+    const int64_t total = l4 * k;
     for (int64_t pos = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; pos < total;
          pos += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t i2 = pos / k;
-        const int64_t j = pos - i2 * k;
-        const u64x4 w = philox4x64_10(static_cast<uint64_t>(j * l2 + i2), sidx, 0, 0, seed, 0);
-        out[2 * i2 * k + j] = __uint_as_float(bf16_bits(normal_from(w.v[0], w.v[1])) << 16);
-        if (2 * i2 + 1 < l) out[(2 * i2 + 1) * k + j] = __uint_as_float(bf16_bits(normal_from(w.v[2], w.v[3])) << 16);
+        const int64_t i4 = pos / k;
+        const int64_t j = pos - i4 * k;
+        uint32_t h[4];
+        group4(l, l4, i4, j, sidx, seed, h);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            if (4 * i4 + t < l) out[(4 * i4 + t) * k + j] = __uint_as_float(h[t] << 16);
     }
 }
 
@@ -96,24 +120,27 @@ __global__ __launch_bounds__(256) void sketch_plane_kernel(uint16_t* planes, int
     const int b = blockIdx.y;
     uint16_t* pl = planes + static_cast<int64_t>(b) * stride;
     const uint64_t sidx = sketch_index0 + static_cast<uint64_t>(b);
-    const int64_t l2 = (l + 1) / 2;
-    const int64_t half = ldp / 2;           // ldp is even
-    const int64_t total = k * half;
+    const int64_t l4 = (l + 3) / 4;
+    const int64_t quarter = ldp / 4;        // ldp is a multiple of 4
+    const int64_t total = k * quarter;
     for (int64_t pos = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; pos < total;
          pos += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-        const int64_t j = pos / half;
-        const int64_t i2 = pos - j * half;
-        uint32_t v = 0;
-        if (2 * i2 < l) {
-            const u64x4 w = philox4x64_10(static_cast<uint64_t>(j * l2 + i2), sidx, 0, 0, seed, 0);
-            v = bf16_bits(normal_from(w.v[0], w.v[1]));
-            if (2 * i2 + 1 < l) v |= bf16_bits(normal_from(w.v[2], w.v[3])) << 16;
+        const int64_t j = pos / quarter;
+        const int64_t i4 = pos - j * quarter;
+        uint2 v = make_uint2(0u, 0u);
+        if (4 * i4 < l) {
+            uint32_t h[4];
+            group4(l, l4, i4, j, sidx, seed, h);
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (4 * i4 + t >= l) h[t] = 0u;
+            v = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
         }
-        uint32_t* dst = reinterpret_cast<uint32_t*>(pl + j * ldp + 2 * i2);
-        dst[0] = v;
+        const int64_t o = j * ldp + 4 * i4;
+        *reinterpret_cast<uint2*>(pl + o) = v;
         if (zero_rest) {
-            *reinterpret_cast<uint32_t*>(pl + planeStride + j * ldp + 2 * i2) = 0u;
-            *reinterpret_cast<uint32_t*>(pl + 2 * planeStride + j * ldp + 2 * i2) = 0u;
+            *reinterpret_cast<uint2*>(pl + planeStride + o) = make_uint2(0u, 0u);
+            *reinterpret_cast<uint2*>(pl + 2 * planeStride + o) = make_uint2(0u, 0u);
         }
     }
 }
@@ -123,10 +150,10 @@ __global__ __launch_bounds__(256) void sketch_plane_kernel(uint16_t* planes, int
 hipError_t launch_sketch_plane(uint16_t* planes, int64_t ldp, int64_t planeStride, int64_t stride, int64_t l,
                                int64_t k, uint64_t seed, uint64_t sketch_index0, bool zero_rest, int batch,
                                hipStream_t stream) {
-    if (ldp % 2 != 0 || ldp < l || planeStride % 2 != 0 || stride % 2 != 0 ||
-        reinterpret_cast<uintptr_t>(planes) % 4 != 0)
+    if (ldp % 4 != 0 || ldp < l || planeStride % 4 != 0 || stride % 4 != 0 ||
+        reinterpret_cast<uintptr_t>(planes) % 8 != 0)
         return hipErrorInvalidValue;
-    const int64_t total = k * (ldp / 2);
+    const int64_t total = k * (ldp / 4);
     int64_t blocks = (total + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     dim3 grid(static_cast<unsigned>(blocks), batch);
@@ -137,7 +164,7 @@ hipError_t launch_sketch_plane(uint16_t* planes, int64_t ldp, int64_t planeStrid
 
 hipError_t launch_sketch(float* omega, int64_t l, int64_t k, int64_t stride, uint64_t seed,
                          uint64_t sketch_index0, int batch, hipStream_t stream) {
-    const int64_t total = (l + 1) / 2 * k;
+    const int64_t total = (l + 3) / 4 * k;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 8192) blocks = 8192;
     dim3 grid(static_cast<unsigned>(blocks), batch);
