@@ -129,3 +129,82 @@ def test_exact_svd_full_size(gl):
     res = g - Pd @ (Pd.t().contiguous() @ g)
     assert abs(float((res * res).sum()) - lam[r:].sum()) <= 1e-6 * lam[r:].sum()
     assert orth_err(P[0].cpu().numpy().astype(np.float64)) < 1e-4
+
+
+def test_adam8_full_size_sampled_blocks(gl, orc):
+    """8-bit Adam on the bench's whole state (64 x 1024 x 11008, 5504 blocks per
+    matrix), two steps; blocks are independent, so sampled blocks are checked
+    against the oracle started from the GPU's codes and scales of the previous
+    step: scales equal, codes equal except one-step moves at rounding
+    boundaries, N within 1e-5 relative plus the moment's rounding over its
+    denominator."""
+    import torch
+    B, r, l = 64, 1024, 11008
+    st = gl.Adam8State(r, l, B)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(77)
+    rng = np.random.default_rng(78)
+    u = 2.0 ** -24
+    for t in (1, 2):
+        R = torch.randn((B, r, l), generator=gen, device="cuda") * 1e-3
+        M8h, Msh = st.M8.cpu().numpy(), st.Ms.cpu().numpy()
+        V8h, Vsh = st.V8.cpu().numpy(), st.Vs.cpu().numpy()
+        N = gl.galore_lowrank_adam8_step(R, st, t=t)
+        torch.cuda.synchronize()
+        Rh = R.cpu().numpy().reshape(B, -1)
+        Nh = N.cpu().numpy().reshape(B, -1)
+        M8g, Msg = st.M8.cpu().numpy().reshape(B, -1), st.Ms.cpu().numpy()
+        V8g, Vsg = st.V8.cpu().numpy().reshape(B, -1), st.Vs.cpu().numpy()
+        for b, blk in zip(rng.integers(0, B, 12), rng.integers(0, r * l // 2048, 12)):
+            sl = slice(blk * 2048, (blk + 1) * 2048)
+            M8o, Mso, V8o, Vso, No, m32, v32 = orc.adam8(Rh[b, sl], M8h[b].reshape(-1)[sl], Msh[b, blk:blk + 1],
+                                                        V8h[b].reshape(-1)[sl], Vsh[b, blk:blk + 1], 0.9, 0.999,
+                                                        float(np.float32(1e-8)), t)
+            assert Msg[b, blk] == Mso[0] and Vsg[b, blk] == Vso[0]
+            rank = lambda c: np.where(c & 0x80, -(c.astype(np.int64) & 0x7F), c.astype(np.int64) & 0x7F)
+            for cg, co in ((M8g[b, sl], M8o), (V8g[b, sl], V8o)):
+                bad = cg != co
+                assert bad.mean() < 1e-2
+                assert np.all(np.abs(rank(cg[bad]) - rank(co[bad])) == 1)
+            bc1, bc2 = 1 - 0.9 ** t, 1 - 0.999 ** t
+            mdec = orc.fp8_decode(M8h[b].reshape(-1)[sl], orc.E4M3) * Msh[b, blk]
+            den = np.sqrt(v32.astype(np.float64) / bc2) + 1e-8
+            tol = 1e-5 * np.abs(No) + 8 * u * (0.9 * np.abs(mdec) + 0.1 * np.abs(Rh[b, sl])) / bc1 / den
+            assert np.all(np.abs(Nh[b, sl] - No) <= tol)
+
+
+def test_lowbit_projector_full_size_sampled(gl, orc):
+    """Low-bit projector at the bench's shape (64 x 4096 x 11008 bf16 G, r =
+    1024): codes and scales of sampled matrices bit-exact with the oracle;
+    sampled entries of R = Pq^T A and of the weight change -(lr alpha) Pq N
+    within 1e-5 of their absolute-value bound, from the codes read back."""
+    import torch
+    m, n, r, B = 4096, 11008, 1024, 64
+    G = gi.torch_planted_group(m, n, B, gi.spectrum_power(m, 0.7), 1e-4, seed=5000, dtype="bf16")
+    P, _, info = gl.galore_rsvd_update(G, r, 32, 1, 5)
+    assert (info.cpu().numpy() == 0).all()
+    for bits in (8, 4):
+        q = gl.galore_quantize_projector(P, bits)
+        R = gl.galore_project_quantized(q, G)
+        Nn = torch.randn((B, r, n), generator=torch.Generator(device="cuda").manual_seed(bits), device="cuda")
+        W = torch.zeros((B, m, n), device="cuda")
+        gl.galore_project_back_quantized(q, Nn, W, 1e-3, 0.25)
+        torch.cuda.synchronize()
+        rng = np.random.default_rng(bits)
+        for b in rng.integers(0, B, 3):
+            Pb = P[b].cpu().numpy().astype(np.float64)
+            codes, scales = orc.quantize_projector(Pb, bits)
+            assert np.array_equal(q.codes[b].cpu().numpy(), orc.pack_codes(codes, bits))
+            assert np.array_equal(q.scales[b].cpu().numpy().view(np.uint32), scales.view(np.uint32))
+            Pq = orc.dequantize_projector(codes, scales)
+            Gb = G[b].float().cpu().numpy().astype(np.float64)
+            Rb, Nb, Wb = R[b].cpu().numpy(), Nn[b].cpu().numpy().astype(np.float64), W[b].cpu().numpy()
+            ii, jj = rng.integers(0, r, 64), rng.integers(0, n, 64)
+            ref = np.array([Pq[:, i] @ Gb[:, j] for i, j in zip(ii, jj)])
+            bound = np.array([np.abs(Pq[:, i]) @ np.abs(Gb[:, j]) for i, j in zip(ii, jj)])
+            assert np.all(np.abs(Rb[ii, jj] - ref) <= 1e-5 * bound)
+            c = float(np.float32(np.float32(1e-3) * np.float32(0.25)))
+            wi, wj = rng.integers(0, m, 64), rng.integers(0, n, 64)
+            ref = np.array([-c * (Pq[i, :] @ Nb[:, j]) for i, j in zip(wi, wj)])
+            bound = np.array([c * (np.abs(Pq[i, :]) @ np.abs(Nb[:, j])) for i, j in zip(wi, wj)])
+            assert np.all(np.abs(Wb[wi, wj] - ref) <= 1e-5 * bound)
