@@ -208,3 +208,37 @@ def test_lowbit_projector_full_size_sampled(gl, orc):
             ref = np.array([-c * (Pq[i, :] @ Nb[:, j]) for i, j in zip(wi, wj)])
             bound = np.array([c * (np.abs(Pq[i, :]) @ np.abs(Nb[:, j])) for i, j in zip(wi, wj)])
             assert np.all(np.abs(Wb[wi, wj] - ref) <= 1e-5 * bound)
+
+
+def test_scheduled_step_full_shape(gl):
+    """galore_step at the bench's matrix shape (8 x 4096 x 11008 bf16, r = 1024,
+    p = 32, q = 2), three steps with T = 2 (update, plain step, update with the
+    subspace switch and first-moment re-expression) equal, bit for bit, the
+    separate entry points called in the same order."""
+    import torch
+    m, n, r, p, q, B, T = 4096, 11008, 1024, 32, 2, 8, 2
+    s, l = min(m, n), max(m, n)
+    W1 = torch.randn((B, m, n), generator=torch.Generator(device="cuda").manual_seed(1), device="cuda") * 0.02
+    P1 = torch.zeros((B, s, r), device="cuda")
+    M1 = torch.zeros((B, r, l), device="cuda")
+    V1 = torch.zeros_like(M1)
+    W2, P2, M2, V2 = W1.clone(), P1.clone(), M1.clone(), V1.clone()
+    ws = torch.empty((gl.galore_step_workspace_size(m, n, r, p, B, torch.bfloat16, 3),), dtype=torch.uint8,
+                     device="cuda")
+    for tau in range(3):
+        G = gi.torch_planted_group(m, n, B, gi.spectrum_power(m, 0.7), 1e-4, seed=6000 + tau, dtype="bf16")
+        seed = gi.sketch_seed(tau // T)
+        gl.galore_step(G, W1, P1, M1, V1, r, p, q, seed, tau, T, flags=3, workspace=ws)
+        if tau % T == 0:
+            Pold, Mold = P2.clone(), M2.clone()
+            gl.galore_rsvd_update(G, r, p, q, seed, 0, P=P2)
+            if tau > 0:
+                gl.galore_align_projector(Pold, P2, Mold, M_out=M2)
+            del Pold, Mold
+        R = gl.galore_project(P2, G)
+        gl.galore_lowrank_adam_step(R, M2, V2, R, 0.9, 0.999, 1e-8, tau + 1)
+        gl.galore_project_back(P2, R, W2, 1e-3, 0.25)
+        torch.cuda.synchronize()
+        for a, c, nm in ((P1, P2, "P"), (M1, M2, "M"), (V1, V2, "V"), (W1, W2, "W")):
+            assert torch.equal(a, c), (tau, nm)
+        del R, G
