@@ -43,6 +43,10 @@ namespace {
 
 constexpr int JB = kJacobiBlock;   // columns per block
 constexpr int JW = 2 * JB;         // columns per pair (64)
+#ifndef GALORE_JAC_INNER
+#define GALORE_JAC_INNER 1
+#endif
+constexpr int kInnerSweeps = GALORE_JAC_INNER;   // inner sweeps of a pair's 64 x 64 Gram per visit
 constexpr int JT = 256;            // threads (4 waves)
 constexpr int GR = 64;             // rows per Gram chunk (two fp32 chunks fill the LDS buffer)
 constexpr int AR = 64;             // rows per apply chunk
@@ -444,16 +448,19 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
             }
             __syncthreads();
                 };
-        for (int t = 0; t < JW; t += 2) {
-            round(std::integral_constant<int, 0>());
-            round(std::integral_constant<int, 1>());
-        }
-        // ---- Theta to LDS in fp32 for the matrix cores; the sweep reversed the
-        //      slot order, so output column j is slot 63 - j (a pair whose
-        //      rotations are all small keeps its columns in place)
+        for (int isw = 0; isw < kInnerSweeps; ++isw)
+            for (int t = 0; t < JW; t += 2) {
+                round(std::integral_constant<int, 0>());
+                round(std::integral_constant<int, 1>());
+            }
+        // ---- Theta to LDS in fp32 for the matrix cores; a sweep reverses the
+        //      slot order, so after an odd number of sweeps output column j is
+        //      slot 63 - j (a pair whose rotations are all small keeps its
+        //      columns in place)
         float (*Tf0)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) Tf0[x][JW - 1 - (c0 + j)] = static_cast<float>(tv[j]);
+        for (int j = 0; j < 16; ++j)
+            Tf0[x][(kInnerSweeps & 1) ? JW - 1 - (c0 + j) : c0 + j] = static_cast<float>(tv[j]);
         __syncthreads();
     }
     // ---- 4. Y_P <- Y_P Theta on the fp32 matrix cores: 64-row chunks through

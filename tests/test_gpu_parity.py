@@ -795,3 +795,54 @@ def test_svd_update_matches_oracle(gl, orc, m, n, r, dtype):
     assert proj_dist(P, Pr) <= 1e-3
     idx_max = np.argmax(np.abs(P), axis=0)
     assert np.all(P[idx_max, np.arange(r)] > 0)
+
+
+def test_adam8_in_place_and_strided(gl):
+    """N may alias R (the update overwrites the projected gradient), and R / N
+    may have a padded leading dimension and batch stride: both give the same
+    codes, scales and N, bit for bit, as the packed, separate-N call."""
+    import torch
+    rows, cols, b = 24, 1000, 3
+    rng = np.random.default_rng(9)
+    R = dev((rng.standard_normal((b, rows, cols)) * 1e-2).astype(np.float32))
+    s1, s2, s3 = gl.Adam8State(rows, cols, b), gl.Adam8State(rows, cols, b), gl.Adam8State(rows, cols, b)
+    for t in (1, 2, 3):
+        N1 = gl.galore_lowrank_adam8_step(R, s1, t=t)
+        R2 = R.clone()
+        N2 = gl.galore_lowrank_adam8_step(R2, s2, N=R2, t=t)
+        Rp = torch.zeros((b, rows + 2, cols + 12), device="cuda")
+        Rp[:, :rows, :cols] = R
+        N3 = gl.galore_lowrank_adam8_step(Rp[:, :rows, :cols], s3, N=Rp[:, :rows, :cols], t=t)
+        torch.cuda.synchronize()
+        assert torch.equal(N1, N2) and torch.equal(N1, N3)
+        for x in ("M8", "V8", "Ms", "Vs"):
+            assert torch.equal(getattr(s1, x), getattr(s2, x)) and torch.equal(getattr(s1, x), getattr(s3, x))
+        R = R * 0.5 + 1e-3
+
+
+def test_lowbit_batched_strided_matches_single(gl, orc):
+    """A batch of low-bit projections and back-projections with padded operands
+    equals the single-matrix calls bit for bit, and the codes are the oracle's."""
+    import torch
+    m, n, r, b = 256, 688, 64, 3
+    rng = np.random.default_rng(10)
+    Ps = np.stack([_haar(rng, m, r) for _ in range(b)]).astype(np.float32)
+    Gs = [gi.store(gi.planted_gradient(m, n, gi.spectrum_power(m, 0.8), 1e-4, seed=90 + i), "bf16") for i in range(b)]
+    G = torch.stack([dev_stored(x) for x in Gs])
+    Pp = torch.zeros((b, m + 3, r + 8), device="cuda")
+    Pp[:, :m, :r] = dev(Ps)
+    q = gl.galore_quantize_projector(Pp[:, :m, :r], 8)
+    R = gl.galore_project_quantized(q, G)
+    N = dev(rng.standard_normal((b, r, n)).astype(np.float32))
+    W = torch.zeros((b, m, n), device="cuda")
+    gl.galore_project_back_quantized(q, N, W, 1.0, 1.0)
+    for i in range(b):
+        qi = gl.galore_quantize_projector(dev(Ps[i]), 8)
+        c, sc = orc.quantize_projector(Ps[i], 8)
+        assert np.array_equal(qi.codes.cpu().numpy(), orc.pack_codes(c, 8))
+        assert torch.equal(qi.codes, q.codes[i]) and torch.equal(qi.scales, q.scales[i])
+        Ri = gl.galore_project_quantized(qi, G[i])
+        Wi = torch.zeros((m, n), device="cuda")
+        gl.galore_project_back_quantized(qi, N[i].contiguous(), Wi, 1.0, 1.0)
+        torch.cuda.synchronize()
+        assert torch.equal(Ri, R[i]) and torch.equal(Wi, W[i])
