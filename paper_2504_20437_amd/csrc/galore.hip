@@ -604,7 +604,7 @@ const char* galore_status_string(int status) {
     }
 }
 
-int galore_version(void) { return 100; }
+int galore_version(void) { return 200; }
 
 int galore_sketch(float* omega, int64_t l, int64_t k, uint64_t seed, uint64_t sketch_index,
                   hipStream_t stream) {
