@@ -133,6 +133,9 @@ def parse():
                     help="split the batch into this many equal chunks, each on its own stream (default "
                          "priority), so that one chunk's latency-bound stages overlap another's products")
     ap.add_argument("--cpu-baseline", type=int, default=1, help="time the oracle on the host (0/1)")
+    ap.add_argument("--whole-model", type=int, default=1,
+                    help="also time a subspace update and a projected Adam step of all 224 Llama-7B-shaped "
+                         "matrices (0/1; needs the default 4096x11008 batch of 64 on one stream)")
     ap.add_argument("--roofline-kernel", default="auto", choices=["auto"] + sorted(KERNEL_CLASSES))
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before the workload, copy a buffer of this many MiB device to device once (a "
@@ -500,6 +503,72 @@ def main():
     else:
         exact_svd = None
 
+    # the whole Llama-7B-shaped model on this GPU: 128 square (q, k, v, o),
+    # 64 gate/up (the batch above) and 32 down matrices; a subspace update of
+    # all 224 with q = 1 and with q = 2, and one projected Adam step over all
+    whole_model = None
+    if args.whole_model and (m, n, B, S) == (4096, 11008, 64, 1):
+        groups = [{"name": "q,k,v,o 4096x4096", "m": 4096, "n": 4096, "count": 128, "seed": 5100},
+                  {"name": "down 11008x4096", "m": 11008, "n": 4096, "count": 32, "seed": 5200}]
+        for gr in groups:
+            gm, gn, gc = gr["m"], gr["n"], gr["count"]
+            gs, gl_ = min(gm, gn), max(gm, gn)
+            print("bench: generating %d x %dx%d %s gradients" % (gc, gm, gn, args.dtype), file=sys.stderr, flush=True)
+            gr["G"] = gi.torch_planted_group(gm, gn, gc, gi.spectrum_power(gs, 0.7), 1e-4, seed=gr["seed"],
+                                             dtype=args.dtype)
+            gr["W"] = torch.zeros((gc, gm, gn), dtype=torch.float32, device=dev)
+            gr["P"] = torch.empty((gc, gs, r), dtype=torch.float32, device=dev)
+            gr["sigma"] = torch.empty((gc, r), dtype=torch.float32, device=dev)
+            gr["info"] = torch.empty((gc,), dtype=torch.int32, device=dev)
+            gr["R"] = torch.empty((gc, r, gl_), dtype=torch.float32, device=dev)
+            gr["M"] = torch.zeros_like(gr["R"])
+            gr["V"] = torch.zeros_like(gr["R"])
+            gr["ws"] = torch.empty((gl.galore_rsvd_workspace_size(gm, gn, r, p, gc, G.dtype),), dtype=torch.uint8,
+                                   device=dev)
+            pw = gl.galore_project_workspace_size(gm, gn, r, gc, G.dtype)
+            gr["pws"] = torch.empty((pw,), dtype=torch.uint8, device=dev) if pw > 0 else False
+            gr["bws"] = torch.empty((gl.galore_project_back_workspace_size(gm, gn, r, gc),), dtype=torch.uint8,
+                                    device=dev)
+        groups.insert(1, {"name": "gate/up 4096x11008", "m": m, "n": n, "count": B, "G": G, "W": W, "P": P,
+                          "sigma": sigma, "info": info, "R": R, "M": M, "V": V, "ws": chunks[0]["ws"],
+                          "pws": chunks[0]["pws"], "bws": chunks[0]["bws"]})
+        torch.cuda.synchronize()
+        wm_ms = {}
+        for qq in (1, 2):
+            e0, e1 = mk(), mk()
+            e0.record(stream)
+            for gr in groups:
+                gl.galore_rsvd_update(gr["G"], r, p, qq, gi.sketch_seed(qq), 0, P=gr["P"], sigma=gr["sigma"],
+                                      info=gr["info"], workspace=gr["ws"], stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            wm_ms["update_q%d" % qq] = e0.elapsed_time(e1)
+            if any(int((gr["info"] != 0).sum()) for gr in groups):
+                raise RuntimeError("small SVD did not converge in the whole-model update")
+        e0, e1 = mk(), mk()
+        e0.record(stream)
+        for gr in groups:
+            gl.galore_project(gr["P"], gr["G"], R=gr["R"], workspace=gr["pws"], stream=stream)
+            gl.galore_lowrank_adam_step(gr["R"], gr["M"], gr["V"], gr["R"], 0.9, 0.999, 1e-8, 1, stream=stream)
+            gl.galore_project_back(gr["P"], gr["R"], gr["W"], 1e-3, 0.25, workspace=gr["bws"], stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wm_ms["adam_step"] = e0.elapsed_time(e1)
+        nmat = sum(gr["count"] for gr in groups)
+        whole_model = {"matrices": nmat,
+                       "update_q1_ms": round(wm_ms["update_q1"], 1), "update_q2_ms": round(wm_ms["update_q2"], 1),
+                       "projected_adam_step_ms": round(wm_ms["adam_step"], 1),
+                       "note": "Llama-7B-shaped model, all %d projection matrices on this GPU (128 x 4096x4096, "
+                               "64 x 4096x11008, 32 x 11008x4096, %s, r=%d p=%d): one subspace update of every "
+                               "matrix with q = 1 and with q = 2, and one projected Adam step (projection, Adam, "
+                               "weight update) over all" % (nmat, args.dtype, r, p)}
+        for gr in groups:
+            if gr["name"].startswith("gate"):
+                continue
+            for key in ("G", "W", "P", "R", "M", "V", "ws", "pws", "bws"):
+                gr[key] = None
+        torch.cuda.empty_cache()
+
     # 8-bit moments (E4M3 / E5M2 codes, one scale per 2048-element block)
     st8 = gl.Adam8State(r, l, B, device=dev)
     a8 = [mk() for _ in range(4)]
@@ -543,6 +612,7 @@ def main():
                      "amortised_step_ms": round((upd_ms + (T_sched - 1) * plain_ms) / T_sched, 3),
                      "note": "galore_step on the whole batch: the update step (subspace update, switch with "
                              "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
+        "whole_model": whole_model,
         "adam8": adam8,
         "exact_svd": exact_svd,
         "lowbit_projector": dict(lowbit, note="steps on a fixed projector with its int8 / int4 codes (whole batch): "
