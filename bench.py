@@ -417,6 +417,36 @@ def main():
             a = sum(launches[c]) / len(launches[c])
             rates[c] = round(units_c / (a * 1e-3) / (1e9 if bd == "hbm" else 1e12), 2)
 
+    # the chip's own peaks under load: sustained bf16 matrix-core rate (probe
+    # kernel, register operands only) and device-to-device copy bandwidth
+    sink = torch.empty((2048 * 256,), dtype=torch.float32, device=dev)
+    pe = [mk() for _ in range(4)]
+    for j in range(2):
+        pe[2 * j].record(stream)
+        probe_flops = gl.galore_probe_mfma_bf16(2000, 2048, sink, stream=stream)
+        pe[2 * j + 1].record(stream)
+    torch.cuda.synchronize()
+    mfma_meas = probe_flops / (pe[2].elapsed_time(pe[3]) * 1e-3) / 1e12
+    csrc_t = torch.empty((1 << 28,), dtype=torch.float32, device=dev)
+    cdst_t = torch.empty_like(csrc_t)
+    ce = [mk() for _ in range(4)]
+    for j in range(2):
+        ce[2 * j].record(stream)
+        gl.galore_probe_copy(csrc_t, cdst_t, stream=stream)
+        ce[2 * j + 1].record(stream)
+    torch.cuda.synchronize()
+    hbm_meas = 2.0 * csrc_t.numel() * 4 / (ce[2].elapsed_time(ce[3]) * 1e-3) / 1e9
+    del sink, csrc_t, cdst_t
+    measured_peaks = {"bf16_mfma_tflops": round(mfma_meas, 1), "hbm_copy_gbs": round(hbm_meas, 1),
+                      "note": "sustained bf16 MFMA rate of a register-only probe kernel (2048 workgroups); "
+                              "streaming copy probe of 1 GiB, one 16-byte vector per thread (bytes read + written)"}
+    if roof["bound"] == "hbm":
+        roof["peak_measured"] = measured_peaks["hbm_copy_gbs"]
+    elif roof.get("mfma_dtype", "").startswith("bf16"):
+        roof["peak_measured"] = measured_peaks["bf16_mfma_tflops"]
+    if "peak_measured" in roof:
+        roof["frac_measured"] = round(roof["achieved"] / roof["peak_measured"], 4)
+
     # subspace switch (once per T steps): signs of a new projector matched to
     # the previous one and the first moment re-expressed in the new basis;
     # timed outside the step on a copy of the current projector
@@ -612,6 +642,7 @@ def main():
                      "amortised_step_ms": round((upd_ms + (T_sched - 1) * plain_ms) / T_sched, 3),
                      "note": "galore_step on the whole batch: the update step (subspace update, switch with "
                              "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
+        "measured_peaks": measured_peaks,
         "whole_model": whole_model,
         "adam8": adam8,
         "exact_svd": exact_svd,

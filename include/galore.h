@@ -374,6 +374,30 @@ GALORE_API int galore_project_back_quantized(const uint8_t* Q, int64_t ldq, int6
                                              int64_t stride_w, int32_t r, float lr, float alpha, int32_t batch,
                                              void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Measurement helper (not part of the method): launches `blocks` workgroups of
+ * four waves, each wave running `iterations` x 4 independent bf16 matrix-core
+ * products (v_mfma_f32_32x32x16_bf16) on register operands, and writes one
+ * float per thread to `sink` (device, blocks * 256 floats). *flops (host)
+ * receives the matrix-core work of the launch; divided by the launch time
+ * (timed by the caller on `stream`) it is the sustained bf16 MFMA rate of the
+ * chip under load, the measured counterpart of the dense peak.
+ * Errors: NULL sink/flops -> INVALID_ARG; iterations or blocks < 1 -> SHAPE.
+ */
+GALORE_API int galore_probe_mfma_bf16(int64_t iterations, int32_t blocks, float* sink, double* flops,
+                                      hipStream_t stream);
+
+/*
+ * Measurement helper (not part of the method): copies `bytes` from src to dst
+ * (device, 16-byte aligned, not overlapping; bytes a multiple of 16) with one
+ * 16-byte non-temporal load and store per thread, the access pattern of the
+ * element-wise kernels. 2 * bytes divided by the launch time is the measured
+ * streaming bandwidth, the counterpart of the HBM peak.
+ * Errors: NULL, misaligned or overlapping buffers -> INVALID_ARG; bytes 0 or
+ * not a multiple of 16 -> SHAPE.
+ */
+GALORE_API int galore_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
 /* Options of galore_step (bit flags). */
 typedef enum {
     GALORE_STEP_ALIGN = 1,      /* after each update but the first, match the new projector's column

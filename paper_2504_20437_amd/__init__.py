@@ -29,7 +29,7 @@ EXPORTED = (
     "galore_quantize_projector", "galore_project_quantized_workspace_size", "galore_project_quantized",
     "galore_project_back_quantized_workspace_size", "galore_project_back_quantized",
     "galore_adam8_scale_count", "galore_lowrank_adam8_step",
-    "galore_svd_workspace_size", "galore_svd_update",
+    "galore_svd_workspace_size", "galore_svd_update", "galore_probe_mfma_bf16", "galore_probe_copy",
 )
 
 GALORE_STEP_ALIGN = 1
@@ -106,6 +106,10 @@ def _declare(lib):
     lib.galore_svd_workspace_size.restype = sz
     lib.galore_svd_update.argtypes = [vp, i32, i64, i64, i64, i64, i32, vp, i64, i64, vp, i64, vp, i32, vp, sz, vp]
     lib.galore_svd_update.restype = ctypes.c_int
+    lib.galore_probe_mfma_bf16.argtypes = [i64, i32, vp, ctypes.POINTER(ctypes.c_double), vp]
+    lib.galore_probe_mfma_bf16.restype = ctypes.c_int
+    lib.galore_probe_copy.argtypes = [vp, vp, sz, vp]
+    lib.galore_probe_copy.restype = ctypes.c_int
     return lib
 
 
@@ -486,3 +490,21 @@ def galore_svd_update(G: torch.Tensor, r: int, P=None, sigma=None, info=None, wo
                                  sigma.stride(0) if sigma.dim() == 2 else r, info.data_ptr(), batch,
                                  workspace.data_ptr(), workspace.numel(), _stream(stream)), "galore_svd_update")
     return P, sigma, info
+
+
+def galore_probe_mfma_bf16(iterations: int, blocks: int, sink: torch.Tensor, stream=None) -> float:
+    """Enqueue the bf16 matrix-core probe; returns its flops (time it on the stream)."""
+    fl = ctypes.c_double(0.0)
+    if sink.numel() < blocks * 256 or sink.dtype != torch.float32 or not sink.is_cuda:
+        raise ValueError("sink must be a float32 device tensor of blocks * 256 elements")
+    _check(lib.galore_probe_mfma_bf16(iterations, blocks, sink.data_ptr(), ctypes.byref(fl), _stream(stream)),
+           "galore_probe_mfma_bf16")
+    return fl.value
+
+
+def galore_probe_copy(src: torch.Tensor, dst: torch.Tensor, stream=None):
+    """Enqueue the streaming-copy probe of src into dst (same byte size)."""
+    nb = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nb or not (src.is_cuda and dst.is_cuda):
+        raise ValueError("src and dst must be device tensors of the same byte size")
+    _check(lib.galore_probe_copy(src.data_ptr(), dst.data_ptr(), nb, _stream(stream)), "galore_probe_copy")

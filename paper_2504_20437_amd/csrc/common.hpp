@@ -150,6 +150,9 @@ int64_t adam8_block_count(int64_t rows, int64_t cols);
 hipError_t launch_adam8(const float* R, float* N, int64_t ld, int64_t stride, uint8_t* M8, float* Ms, uint8_t* V8,
                         float* Vs, int64_t rows, int64_t cols, int batch, float beta1, float beta2, float eps,
                         float bc1, float bc2, hipStream_t stream);
+// measurement helper (probe.hip): blocks x 256 threads of sustained bf16 MFMA chains
+hipError_t launch_mfma_probe(int64_t iters, int blocks, float* sink, hipStream_t stream);
+hipError_t launch_copy_probe(const void* src, void* dst, int64_t nvec, hipStream_t stream);
 hipError_t launch_copy_rows(const float* src, int64_t lds, int64_t strideS, float* dst, int64_t ldd,
                             int64_t strideD, int rows, int cols, int batch, hipStream_t stream);
 

@@ -887,6 +887,28 @@ int galore_project_back(const float* P, int64_t ldp, int64_t stride_p, const flo
     return GALORE_OK;
 }
 
+// ---- measurement helper -----------------------------------------------------
+
+int galore_probe_mfma_bf16(int64_t iterations, int32_t blocks, float* sink, double* flops, hipStream_t stream) {
+    if (sink == nullptr || flops == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (iterations < 1 || blocks < 1) return GALORE_ERR_SHAPE;
+    // four waves per block, four chains per wave, 32 x 32 x 16 x 2 flop per MFMA
+    *flops = static_cast<double>(blocks) * 4.0 * 4.0 * static_cast<double>(iterations) * 32768.0;
+    GALORE_TRY(launch_mfma_probe(iterations, blocks, sink, stream));
+    return GALORE_OK;
+}
+
+int galore_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+    if (src == nullptr || dst == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (bytes == 0 || bytes % 16 != 0) return GALORE_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) % 16 != 0) return GALORE_ERR_INVALID_ARG;
+    const char* s0 = static_cast<const char*>(src);
+    const char* d0 = static_cast<const char*>(dst);
+    if (s0 < d0 + bytes && d0 < s0 + bytes) return GALORE_ERR_INVALID_ARG;
+    GALORE_TRY(launch_copy_probe(src, dst, static_cast<int64_t>(bytes / 16), stream));
+    return GALORE_OK;
+}
+
 // ---- 8-bit Adam -------------------------------------------------------------
 
 int64_t galore_adam8_scale_count(int64_t rows, int64_t cols) {

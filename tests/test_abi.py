@@ -350,3 +350,20 @@ def test_svd_workspace_and_rejects():
     assert f(*args[:2], 4097, 5000, 5000, *args[5:]) == -2
     assert f(*args[:6], 65, *args[7:]) == -2
     assert f(NULL, *args[1:]) == -1
+
+
+def test_probe_rejects():
+    import ctypes
+    import paper_2504_20437_amd as gl
+    fl = ctypes.c_double(0.0)
+    f = gl.lib.galore_probe_mfma_bf16
+    assert f(10, 4, None, ctypes.byref(fl), None) == -1
+    assert f(10, 4, FAKE, None, None) == -1
+    assert f(0, 4, FAKE, ctypes.byref(fl), None) == -2
+    assert f(10, 0, FAKE, ctypes.byref(fl), None) == -2
+    g = gl.lib.galore_probe_copy
+    assert g(None, FAKE, 256, None) == -1
+    assert g(FAKE, FAKE + 8, 256, None) == -1          # misaligned and overlapping
+    assert g(FAKE, FAKE + 128, 256, None) == -1        # overlapping
+    assert g(FAKE, FAKE + 4096, 0, None) == -2
+    assert g(FAKE, FAKE + 4096, 100, None) == -2
