@@ -172,14 +172,32 @@ def cpu_baseline(args):
     _, _, N = oracle.adam(R, Mz, Mz, f32(0.9), f32(0.999), f32(1e-8), 1)
     oracle.project_back(P, N, W, f32(1e-3), f32(0.25))
     dt = time.perf_counter() - t0
-    return {
+    cpu_model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    out = {
         "value": 1.0 / dt,
         "unit": "updates/s",
         "cores": oracle.num_threads(),
         "kind": "oracle",
         "sample": "one %dx%d %s matrix of the workload, r=%d p=%d q=%d, whole path (update, projection, "
                   "Adam step, weight update) once: %.1f s" % (m, n, args.dtype, r, p, q, dt),
+        "cpu_model": cpu_model,
     }
+    if (m, n) == (4096, 11008):
+        # every term of the oracle's update and step scales with l = max(m, n) at
+        # fixed s and k, so a 4096x4096 matrix costs about 4096/11008 of this one
+        # and an 11008x4096 matrix the same: 64 + 32 + 128 * 0.372 = 143.6 of them
+        out["whole_model_estimate_s"] = round(dt * (96 + 128 * 4096.0 / 11008.0), 1)
+        out["whole_model_note"] = ("extrapolated from the measured matrix, not run: the 224 Llama-7B-shaped "
+                                   "matrices weighted by l")
+    return out
 
 
 def main():
