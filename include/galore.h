@@ -299,8 +299,9 @@ GALORE_API int64_t galore_adam8_scale_count(int64_t rows, int64_t cols);
  * block has scale 0 and codes 0, so zero-filled codes and scales are the zero
  * state).
  * One call decodes the moments, applies galore_lowrank_adam_step's update in
- * fp32 (N from the new moments, bias exponent t), and re-encodes the new
- * moments with new block scales.
+ * fp32 (N from the new moments, bias exponent t; N is formed with the hardware
+ * reciprocal and square root, within a few ulps of the correctly rounded
+ * operations), and re-encodes the new moments with new block scales.
  * R, N: fp32 rows x cols (ld ld, batch stride stride); N may alias R.
  * M8, V8: device bytes, rows * cols per matrix, packed, matrix b at b * rows * cols.
  * Ms, Vs: device fp32, galore_adam8_scale_count(rows, cols) per matrix, packed.
