@@ -110,15 +110,6 @@ __device__ __forceinline__ void mma64_pairs(const double* Ap, const double* Bp, 
                 acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s][bi], bv[s][bj], acc[bi][bj], 0, 0, 0);
 }
 
-// S[r][c] = M[(r0 + r) * ld + c0 + c] for r < nr, c < nc; zero elsewhere
-__device__ __forceinline__ void load_tile(double (*S)[LP], const double* M, int64_t ld, int r0, int c0,
-                                          int nr, int nc) {
-    for (int idx = threadIdx.x; idx < CB * CB; idx += CT) {
-        const int r = idx / CB, c = idx % CB;
-        S[r][c] = (r < nr && c < nc) ? M[static_cast<int64_t>(r0 + r) * ld + c0 + c] : 0.0;
-    }
-}
-
 // S[c][r] = M[(r0 + r) * ld + c0 + c] (transposed load)
 __device__ __forceinline__ void load_tile_t(double (*S)[LP], const double* M, int64_t ld, int r0, int c0,
                                             int nr, int nc) {

@@ -104,27 +104,11 @@ __device__ __forceinline__ void rotation(double a, double b, double g, double& c
     s = y * t;
 }
 
-// Cross-lane moves of an fp64 value within a wave (DPP, no LDS traffic).
+// Cross-lane moves of an fp32 value within a wave (DPP, no LDS traffic).
 // dpp_swap_pairs: lane x receives lane x ^ 1. dpp_odd_partner: an odd lane x
-// receives lane x + 1, an even lane x - 1 (lanes 0 and 63 get their own value).
-__device__ __forceinline__ double dpp_swap_pairs(double v) {
-    const int lo = __double2loint(v), hi = __double2hiint(v);
-    const int l2 = __builtin_amdgcn_update_dpp(lo, lo, 0xB1, 0xf, 0xf, false);   // quad_perm [1,0,3,2]
-    const int h2 = __builtin_amdgcn_update_dpp(hi, hi, 0xB1, 0xf, 0xf, false);
-    return __hiloint2double(h2, l2);
-}
-__device__ __forceinline__ double dpp_odd_partner(double v, bool odd) {
-    const int lo = __double2loint(v), hi = __double2hiint(v);
-    const int ll = __builtin_amdgcn_update_dpp(lo, lo, 0x130, 0xf, 0xf, false);  // wave_shl:1 (from x + 1)
-    const int hl = __builtin_amdgcn_update_dpp(hi, hi, 0x130, 0xf, 0xf, false);
-    const int lr = __builtin_amdgcn_update_dpp(lo, lo, 0x138, 0xf, 0xf, false);  // wave_shr:1 (from x - 1)
-    const int hr = __builtin_amdgcn_update_dpp(hi, hi, 0x138, 0xf, 0xf, false);
-    return __hiloint2double(odd ? hl : hr, odd ? ll : lr);
-}
-
-// fp32 versions: lanes without a source (0 and 63 in the odd pattern) read 0,
-// which only idle lanes consume; a zero old value and bound_ctrl let the
-// compiler fold the lane move into the multiply that uses it
+// receives lane x + 1, an even lane x - 1. Lanes without a source (0 and 63 in
+// the odd pattern) read 0, which only idle lanes consume; a zero old value and
+// bound_ctrl let the compiler fold the lane move into the multiply that uses it
 __device__ __forceinline__ float dpp_swap_pairs(float v) {
     const int i = __float_as_int(v);
     return __int_as_float(__builtin_amdgcn_update_dpp(0, i, 0xB1, 0xf, 0xf, true));
