@@ -846,3 +846,25 @@ def test_lowbit_batched_strided_matches_single(gl, orc):
         gl.galore_project_back_quantized(qi, N[i].contiguous(), Wi, 1.0, 1.0)
         torch.cuda.synchronize()
         assert torch.equal(Ri, R[i]) and torch.equal(Wi, W[i])
+
+
+@pytest.mark.parametrize("m,n,r,p,q,dtype", [(1, 40, 1, 0, 1, "f32"), (40, 1, 1, 0, 1, "f32"), (5, 9, 5, 0, 1, "f32"),
+                                             (40, 300, 40, 0, 1, "bf16"), (33, 33, 32, 1, 2, "f32")])
+def test_rsvd_smallest_shapes(gl, orc, m, n, r, p, q, dtype):
+    """Degenerate sizes: a single row or column (s = 1), r = s (P is a square
+    orthogonal matrix, so P P^T = I and sigma are all singular values), and
+    k = s = 33 one past a Jacobi block."""
+    s = min(m, n)
+    rng = np.random.default_rng(m * 100 + n)
+    G = gi.store(rng.standard_normal((m, n)) * (0.8 ** np.arange(m))[:, None], dtype)
+    P, sig, info = gl.galore_rsvd_update(dev_stored(G), r, p, q, 3)
+    P, sig = host(P), host(sig)
+    assert int(info.cpu()[0]) == 0
+    ss = np.linalg.svd(G.exact, compute_uv=False)
+    assert max_rel_violation(sig, ss[:r], 1e-4, 1e-30) <= 1.0
+    assert orth_err(P) < 1e-4
+    if r == s:
+        assert np.abs(P @ P.T - np.eye(s)).max() < 1e-4
+    else:
+        Pr, _, _ = orc.rsvd_update(G.exact, r, p, q, 3)
+        assert proj_dist(P, Pr) <= 1e-3
