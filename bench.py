@@ -374,9 +374,10 @@ def main():
         # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches;
         # exact on the int8 matrix cores as nine digit-plane products (gram_i8.hip)
         "gram": ("mfma_i8x9", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * C / (n_gram_s + n_gram_l)),
-        # Q = Y R^-1 with triangular R^-1: rows * k * (k + 1) flops, averaged
-        "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * C
-                                / max(1, n_gram_s + n_gram_l - 1))),
+        # Y R^-1 with triangular R^-1: s * k * (k + 1) flops; every launch has s
+        # rows (the l x k side of a power iteration is orthonormalised by
+        # association, (A Z) R_Z^-1)
+        "triangular": ("mfma", s * k * (k + 1.0) * C),
     }
     work["products"] = work["product_A"]          # both products run the same kernel on the same work
     for cls, (members, _, _) in KERNEL_CLASSES.items():
@@ -418,6 +419,9 @@ def main():
         if bound == "mfma_bf16x3":
             roof["mfma_dtype"] = "bf16 (3 exact bf16 products per fp32-accurate product)"
             roof["frac_of_3x_ceiling"] = round(3.0 * ach / peak, 4)
+            # the same fp32-accurate product on the fp32 matrix cores would be
+            # capped at their dense peak
+            roof["vs_fp32_mfma_peak"] = {"peak": FP32_MFMA_PEAK_TFS, "frac": round(ach / FP32_MFMA_PEAK_TFS, 4)}
         if bound == "mfma_i8x9":
             roof["mfma_dtype"] = "int8 (9 exact digit-plane products per fp32-input Gram entry)"
             roof["frac_of_9x_ceiling"] = round(9.0 * ach / peak, 4)
