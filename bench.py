@@ -374,10 +374,9 @@ def main():
         # symmetric Gram X^T X: rows * k * (k + 1) flops, averaged over its launches;
         # exact on the int8 matrix cores as nine digit-plane products (gram_i8.hip)
         "gram": ("mfma_i8x9", (n_gram_s * s + n_gram_l * l) * k * (k + 1.0) * C / (n_gram_s + n_gram_l)),
-        # Y R^-1 with triangular R^-1: s * k * (k + 1) flops; every launch has s
-        # rows (the l x k side of a power iteration is orthonormalised by
-        # association, (A Z) R_Z^-1)
-        "triangular": ("mfma", s * k * (k + 1.0) * C),
+        # Q = Y R^-1 with triangular R^-1: rows * k * (k + 1) flops, averaged
+        "triangular": ("mfma", ((n_gram_s * s + (n_gram_l - 1) * l) * k * (k + 1.0) * C
+                                / max(1, n_gram_s + n_gram_l - 1))),
     }
     work["products"] = work["product_A"]          # both products run the same kernel on the same work
     for cls, (members, _, _) in KERNEL_CLASSES.items():

@@ -53,7 +53,7 @@ Shape make_shape(int64_t m, int64_t n, int r, int p) {
 // Workspace regions, each holding `batch` matrices at a fixed element stride.
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
-    size_t offL1, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
+    size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
         offTheta;
     int64_t strideTheta;
     // bf16-stored gradients only: transposed copy of G (n x ldgt) and three
@@ -84,6 +84,7 @@ Layout make_layout(const Shape& sh, int r, int batch, bool bf16) {
     };
     const size_t B = static_cast<size_t>(batch);
     L.offL1 = take(B * L.strideL * sizeof(float));
+    L.offL2 = take(B * L.strideL * sizeof(float));
     L.offS1 = take(B * L.strideS * sizeof(float));
     L.offS2 = take(B * L.strideS * sizeof(float));
     L.offC = take(B * L.strideKK * sizeof(double));
@@ -391,10 +392,12 @@ GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, i
     return g;
 }
 
-// Factor of a Cholesky-QR pass: R^T R = In^T In (exact Gram of the
-// fixed-point image of In, fp64 factor), with R^-1 for the apply step.
-int factor_pass(const Work& w, const float* In, int64_t stride, int rows, int k, int batch, hipStream_t st,
-                Tracer& tr, bool cmax_ready) {
+// One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In (exact Gram of the
+// fixed-point image of In, fp64 factor);
+// columns found dependent are replaced by generic unit vectors.
+int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
+              hipStream_t st, Tracer& tr, bool cmax_ready) {
+    const Layout& L = *w.L;
     GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k, cmax_ready), batch, st));
     if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
     {
@@ -402,26 +405,10 @@ int factor_pass(const Work& w, const float* In, int64_t stride, int rows, int k,
         if (e != GALORE_OK) return e;
     }
     if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
-    return GALORE_OK;
-}
-
-// Apply step: Out = In R^-1 with the last factor; the columns it found
-// dependent are replaced by generic unit vectors.
-int apply_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
-               hipStream_t st, Tracer& tr) {
-    const Layout& L = *w.L;
     GALORE_TRACED(tr, GALORE_STAGE_TRIANGULAR,
                   gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st));
     GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st));
     return GALORE_OK;
-}
-
-// One Cholesky-QR pass: Out = In R^-1 with R^T R = In^T In.
-int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
-              hipStream_t st, Tracer& tr, bool cmax_ready) {
-    const int e = factor_pass(w, In, stride, rows, k, batch, st, tr, cmax_ready);
-    if (e != GALORE_OK) return e;
-    return apply_pass(w, In, Out, stride, rows, k, batch, st, tr);
 }
 
 #define GALORE_CHECK(expr)               \
@@ -453,6 +440,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     const int s = static_cast<int>(sh.s);
     const int l = static_cast<int>(sh.l);
     float* L1 = w.f(L.offL1);
+    float* L2 = w.f(L.offL2);
     float* Sa = w.f(L.offS1);
     float* Sb = w.f(L.offS2);
 
@@ -496,17 +484,16 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
         return GALORE_OK;
     };
     GALORE_CHECK(orth_s(q == 0 ? 2 : 1));
-    // a4: power iterations with re-orthonormalisation after every product.
-    // The l x k side is orthonormalised by association: with Z = A^T Q =
-    // Q_Z R_Z, the next sample A Q_Z is formed as (A Z) R_Z^-1, so the
-    // triangular product runs on s rows instead of l (the same value; both
-    // orders carry rounding of order eps cond(R_Z)).
+    // a4: power iterations with re-orthonormalisation after every product
     for (int it = 0; it < q; ++it) {
         GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready));
-        GALORE_CHECK(factor_pass(w, L1, L.strideL, l, k, batch, stream, tr, ready));
-        GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Qtmp, L.strideS, ready));
-        GALORE_CHECK(apply_pass(w, Qtmp, Q, L.strideS, s, k, batch, stream, tr));
-        ready = false;   // the maxima the product took are of A Z, not of Y
+        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, tr, ready));
+        GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS, ready));
+        {
+            float* t = Q;
+            Q = Qtmp;
+            Qtmp = t;
+        }
         GALORE_CHECK(orth_s(it == q - 1 ? 2 : 1));
     }
     // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
