@@ -114,7 +114,10 @@ GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, in
  *          threads are safe; they serialise only while enqueuing the sweeps.
  * Errors:  NULL G/P/workspace -> INVALID_ARG; m,n,r < 1, r > s, p < 0, q < 0,
  *          r + p > 4096 (largest supported sketch width), ldg < n, ldp < r,
- *          batch < 1 -> SHAPE; workspace_bytes too small -> WORKSPACE.
+ *          batch < 1, or 3 * (k rounded up to 128) * (l rounded up to 128) above
+ *          2^31 - 1 (the exact Gram's digit planes of one matrix, addressed with
+ *          32-bit offsets; e.g. l up to about 600000 at k = 1056) -> SHAPE;
+ *          workspace_bytes too small -> WORKSPACE.
  */
 GALORE_API int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                        int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,

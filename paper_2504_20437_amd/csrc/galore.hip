@@ -50,6 +50,12 @@ Shape make_shape(int64_t m, int64_t n, int r, int p) {
     return sh;
 }
 
+// The exact Gram's kernel addresses one matrix's three int8 digit planes
+// ((k padded) x (l padded) bytes each) with 32-bit offsets.
+bool digits_fit(const Shape& sh) {
+    return gram_i8_digit_bytes(static_cast<int>(sh.l), sh.k) <= static_cast<int64_t>(INT32_MAX);
+}
+
 // Workspace regions, each holding `batch` matrices at a fixed element stride.
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
@@ -426,7 +432,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1) return GALORE_ERR_SHAPE;
     if (m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
     const Shape sh = make_shape(m, n, r, p);
-    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK) return GALORE_ERR_SHAPE;
+    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK || !digits_fit(sh)) return GALORE_ERR_SHAPE;
     if (ldg < n || ldp < r) return GALORE_ERR_SHAPE;
     if (batch > 1 && (stride_g < m * ldg || stride_p < sh.s * ldp)) return GALORE_ERR_SHAPE;
     if (sigma != nullptr && batch > 1 && stride_sigma < r) return GALORE_ERR_SHAPE;
@@ -619,7 +625,7 @@ size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, in
     if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return 0;
     if (m > INT32_MAX || n > INT32_MAX) return 0;
     const Shape sh = make_shape(m, n, r, p);
-    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK) return 0;
+    if (r > sh.s || static_cast<int64_t>(r) + p > kMaxK || !digits_fit(sh)) return 0;
     return make_layout(sh, r, batch, g_dtype == GALORE_BF16).total;
 }
 
@@ -1113,7 +1119,7 @@ StepLayout make_step_layout(const Shape& sh, int r, int p, int batch, int32_t g_
 bool step_sizes_ok(int64_t m, int64_t n, int32_t r, int32_t p, int32_t q, int32_t batch, int32_t g_dtype) {
     if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return false;
     if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return false;
-    return r <= std::min(m, n) && static_cast<int64_t>(r) + p <= kMaxK;
+    return r <= std::min(m, n) && static_cast<int64_t>(r) + p <= kMaxK && digits_fit(make_shape(m, n, r, p));
 }
 
 size_t galore_step_workspace_size(int64_t m, int64_t n, int32_t r, int32_t p, int32_t batch, int32_t g_dtype,

@@ -296,7 +296,8 @@ hipError_t launch_gram_i8(const GramI8Args& g, int batch, hipStream_t stream) {
     const int cpad = gram_i8_cols_pad(g.cols);
     const int64_t planeStride = static_cast<int64_t>(cpad) * ldq;
     const int64_t strideD = 3 * planeStride;
-    if (strideD > g.strideD || g.ldc < g.cols) return hipErrorInvalidValue;
+    // the Gram kernel addresses the digit planes with 32-bit offsets
+    if (strideD > g.strideD || strideD > INT32_MAX || g.ldc < g.cols) return hipErrorInvalidValue;
     if (!g.cmax_ready) {
         const hipError_t e = launch_fill_u32(g.cmax, g.strideCM * batch, stream);
         if (e != hipSuccess) return e;

@@ -48,6 +48,10 @@ def test_workspace_size():
     assert gl.galore_rsvd_workspace_size(10, 20, 11, 0, 1) == 0                  # r > s
     assert gl.galore_rsvd_workspace_size(0, 20, 1, 0, 1) == 0
     assert gl.galore_rsvd_workspace_size(5000, 9000, 4090, 10, 1) == 0           # sketch too wide
+    # the exact Gram's digit planes (3 x k x l bytes, padded) must stay below 2^31
+    assert gl.galore_rsvd_workspace_size(1056, 600000, 1024, 32, 1) > 0
+    assert gl.galore_rsvd_workspace_size(1056, 700000, 1024, 32, 1) == 0
+    assert gl.galore_rsvd_workspace_size(300000, 4096, 4000, 96, 1) == 0
     # a bf16 gradient also keeps room for its transposed copy and the split sketch operand
     import torch
     bf = gl.galore_rsvd_workspace_size(4096, 11008, 1024, 32, 1, torch.bfloat16)
@@ -77,6 +81,7 @@ def rsvd(**kw):
     (dict(m=0), -2), (dict(n=-3), -2), (dict(r=0), -2), (dict(r=65), -2), (dict(p=-1), -2),
     (dict(q=-1), -2), (dict(ldg=95), -2), (dict(ldp=7), -2), (dict(batch=0), -2),
     (dict(batch=2, stride_g=10), -2), (dict(r=8, p=5000), -2),
+    (dict(m=1056, n=700000, ldg=700000, stride_g=0, r=1024, p=32, ldp=1024, stride_p=0, stride_sigma=1024), -2),
     (dict(ws_bytes=1000), -3), (dict(ws=FAKE + 8), -3),
 ])
 def test_rsvd_rejects(kw, code):
