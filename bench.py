@@ -255,11 +255,13 @@ def main():
         pws_bytes = gl.galore_project_workspace_size(m, n, r, C, G.dtype)
         chunks.append(dict(
             sl=sl, stream=torch.cuda.current_stream() if ci == 0 else torch.cuda.Stream(),
+            aux=torch.cuda.Stream(),     # second stream for the latency-bound stages (default priority)
             ws=torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, C, G.dtype),), dtype=torch.uint8, device=dev),
             pws=torch.empty((pws_bytes,), dtype=torch.uint8, device=dev) if pws_bytes > 0 else False,
             bws=torch.empty((gl.galore_project_back_workspace_size(m, n, r, C),), dtype=torch.uint8, device=dev)))
     torch.cuda.synchronize()
     stream = chunks[0]["stream"]      # stage events are recorded on chunk 0's stream
+    aux0 = chunks[0]["aux"]
     outer = ("rsvd", "project", "adam", "project_back")
     cap = 96   # stage instances recorded per subspace update
 
@@ -269,12 +271,12 @@ def main():
             ev[0].record(st)
         if sev is None:
             gl.galore_rsvd_update(G[sl], r, p, q, gi.sketch_seed(t), sl.start, P=P[sl], sigma=sigma[sl], info=info[sl],
-                                  workspace=ch["ws"], stream=st)
+                                  workspace=ch["ws"], stream=st, aux_stream=ch["aux"])
             stages = None
         else:
             _, _, _, stages = gl.galore_rsvd_update_traced(G[sl], r, p, q, gi.sketch_seed(t), sev, sl.start, P=P[sl],
                                                            sigma=sigma[sl], info=info[sl], workspace=ch["ws"],
-                                                           stream=st)
+                                                           stream=st, aux_stream=ch["aux"])
         if ev is not None:
             ev[1].record(st)
         gl.galore_project(P[sl], G[sl], R=R[sl], workspace=ch["pws"], stream=st)
@@ -492,7 +494,7 @@ def main():
     win[0].record(stream)
     for j in range(10):
         gl.galore_step(G, W, P, M, V, r, p, q, gi.sketch_seed(1), T_sched + j, T_sched, flags=3, info=sinfo,
-                       workspace=sws, stream=stream)
+                       workspace=sws, stream=stream, aux_stream=aux0)
         win[j + 1].record(stream)
     torch.cuda.synchronize()
     if int((sinfo != 0).sum()):
@@ -537,10 +539,10 @@ def main():
         xe = [mk() for _ in range(8)]
         for j in range(2):
             xe[4 * j].record(stream)
-            _, _, xinfo = gl.galore_svd_update(G[:Bx], r, workspace=xws, stream=stream)
+            _, _, xinfo = gl.galore_svd_update(G[:Bx], r, workspace=xws, stream=stream, aux_stream=aux0)
             xe[4 * j + 1].record(stream)
             gl.galore_rsvd_update(G[:Bx], r, p, q, gi.sketch_seed(0), 0, P=P[:Bx], sigma=sigma[:Bx], info=info[:Bx],
-                                  workspace=chunks[0]["ws"], stream=stream)
+                                  workspace=chunks[0]["ws"], stream=stream, aux_stream=aux0)
             xe[4 * j + 2].record(stream)
         torch.cuda.synchronize()
         if int((xinfo != 0).sum()):
@@ -590,7 +592,7 @@ def main():
             e0.record(stream)
             for gr in groups:
                 gl.galore_rsvd_update(gr["G"], r, p, qq, gi.sketch_seed(qq), 0, P=gr["P"], sigma=gr["sigma"],
-                                      info=gr["info"], workspace=gr["ws"], stream=stream)
+                                      info=gr["info"], workspace=gr["ws"], stream=stream, aux_stream=aux0)
             e1.record(stream)
             torch.cuda.synchronize()
             wm_ms["update_q%d" % qq] = e0.elapsed_time(e1)

@@ -7,10 +7,11 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - All matrix pointers are DEVICE pointers, row-major, owned by the caller.
- *    The library never allocates or frees device memory and never
- *    synchronises the device: work is enqueued on `stream` and every entry
- *    point returns as soon as it is enqueued (galore_rsvd_update also uses one
- *    stream of its own, joined back into `stream`; see there).
+ *    The library never allocates or frees device memory, creates no stream
+ *    and never synchronises the device: work is enqueued on the caller's
+ *    `stream` (and, where an entry point takes one, on the caller's optional
+ *    second stream `aux_stream`, forked from and joined back into `stream`),
+ *    and every entry point returns as soon as it is enqueued.
  *  - G is the m x n gradient as produced by autograd (+grad). s = min(m, n) is
  *    the projected side, l = max(m, n). A denotes G when m <= n and G^T when
  *    m > n, so A is always s x l (paper §3: left singular vectors when m <= n,
@@ -22,7 +23,11 @@
  *  - Status: every call validates its arguments on the host before enqueuing
  *    anything and returns a galore_status_t (< 0 on error, nothing enqueued).
  *    A launch failure reported by the HIP runtime returns GALORE_ERR_HIP.
- *    NaN/Inf inputs are not checked: they propagate to the outputs.
+ *    NaN/Inf inputs are not checked on the host: they propagate to the
+ *    outputs, and the subspace update also reports them in `info` (see
+ *    galore_rsvd_update). Signed zeros and subnormal inputs are ordinary
+ *    values; a gradient whose entries all lie in the subnormal range keeps
+ *    only the precision fp32 arithmetic has there.
  */
 #ifndef GALORE_H_
 #define GALORE_H_
@@ -102,16 +107,25 @@ GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, in
  * Inputs:  G (g_dtype, m x n, ld ldg, batch stride stride_g elements).
  * Outputs: P (fp32, s x r, ld ldp >= r, stride stride_p);
  *          sigma (fp32, r values per matrix at stride stride_sigma; may be NULL);
- *          info (device int32[batch]; may be NULL): 0 = converged, > 0 = the
- *          small SVD did not converge within its sweep limit (value = sweeps).
+ *          info (device int32[batch]; may be NULL): 0 = converged; 24 = the
+ *          small SVD did not converge within its sweep limit of 24 sweeps;
+ *          25 = a column of the small SVD has a NaN or Inf norm (NaN or Inf
+ *          in G): sigma and P then hold NaN or Inf and must not be used.
+ *          Every non-zero value means failure. The work enqueued is bounded
+ *          either way: the sweep count is fixed on the host, every device loop
+ *          is bounded by the sizes, and no address depends on a computed value.
  * Workspace: device buffer of at least galore_rsvd_workspace_size(...) bytes,
  *          256-byte aligned; contents are scratch and may be reused afterwards.
- * Streams: with batch >= 2 the small SVD's sweeps for the second half of the
- *          batch run on a library-owned stream of the current device (created
- *          on first use with default priority, kept for the process), forked
- *          from `stream` and joined back into it with events; everything else,
- *          and all completion, is ordered on `stream`. Calls from several host
- *          threads are safe; they serialise only while enqueuing the sweeps.
+ * Streams: everything is enqueued on `stream` when aux_stream is NULL (or
+ *          equal to `stream`, or batch < 2). Otherwise aux_stream, a second
+ *          stream of the caller on the same device, takes the Cholesky
+ *          factorisations and the small SVD's sweeps of the second half of the
+ *          batch: it is forked from `stream` and joined back into it with two
+ *          events the library creates once per device, so all completion is
+ *          still ordered on `stream` and the results are bit-identical either
+ *          way (the halves' latency-bound launch chains then overlap). Calls
+ *          from several host threads are safe; they serialise only while
+ *          enqueuing the fork and join.
  * Errors:  NULL G/P/workspace -> INVALID_ARG; m,n,r < 1, r > s, p < 0, q < 0,
  *          r + p > 4096 (largest supported sketch width), ldg < n, ldp < r,
  *          batch < 1, or 3 * (k rounded up to 128) * (l rounded up to 128) above
@@ -123,7 +137,8 @@ GALORE_API int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int
                        int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
                        uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
                        float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
-                       void* workspace, size_t workspace_bytes, hipStream_t stream);
+                       void* workspace, size_t workspace_bytes, hipStream_t stream,
+                       hipStream_t aux_stream);
 
 /*
  * Exact SVD projector (the full SVD that paper §4.1.2 replaces by the
@@ -139,7 +154,7 @@ GALORE_API size_t galore_svd_workspace_size(int64_t m, int64_t n, int32_t r, int
 GALORE_API int galore_svd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                                  int64_t stride_g, int32_t r, float* P, int64_t ldp, int64_t stride_p, float* sigma,
                                  int64_t stride_sigma, int32_t* info, int32_t batch, void* workspace,
-                                 size_t workspace_bytes, hipStream_t stream);
+                                 size_t workspace_bytes, hipStream_t stream, hipStream_t aux_stream);
 
 /*
  * Stages of the subspace update reported by galore_rsvd_update_traced.
@@ -154,8 +169,9 @@ typedef enum {
     GALORE_STAGE_JACOBI = 6,      /* small SVD: all Jacobi sweeps and the sort                  */
     GALORE_STAGE_PROJECTOR = 7,   /* P = Q U_B[:, :r], fp32 matrix cores (1 launch)             */
     GALORE_STAGE_OTHER = 8,       /* small kernels: dependent-column fill, sign convention      */
-    GALORE_STAGE_OPERAND = 9      /* bf16 G only: transposed copy of G, bf16 split of an fp32    */
+    GALORE_STAGE_OPERAND = 9,     /* bf16 G only: transposed copy of G, bf16 split of an fp32    */
                                   /* operand (1 launch each)                                    */
+    GALORE_STAGE_REFINE = 10      /* fp64 refinement of the small SVD's vectors                 */
 } galore_stage_t;
 
 /*
@@ -176,7 +192,8 @@ GALORE_API int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t
                               uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
                               float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
                               void* workspace, size_t workspace_bytes, hipStream_t stream,
-                              hipEvent_t* events, int32_t* stages, int32_t capacity, int32_t* count);
+                              hipStream_t aux_stream, hipEvent_t* events, int32_t* stages, int32_t capacity,
+                              int32_t* count);
 
 /*
  * Bytes of workspace galore_project uses for `batch` m x n matrices with rank
@@ -440,7 +457,7 @@ GALORE_API size_t galore_step_workspace_size(int64_t m, int64_t n, int32_t r, in
  * Workspace: at least galore_step_workspace_size(...) bytes, device, 256-byte
  * aligned, scratch (holds the projected gradient, the update's workspace and,
  * with the flags, copies of the previous P and M).
- * Streams: as galore_rsvd_update.
+ * Streams: as galore_rsvd_update (aux_stream may be NULL).
  * Errors: NULL G/W/P/M/V, bad dtype, tau < 0, T < 1, unknown flags or
  *         REEXPRESS without ALIGN, betas/eps/lr/alpha as galore_lowrank_adam_step
  *         and galore_project_back -> INVALID_ARG; sizes, ld or strides invalid,
@@ -452,7 +469,8 @@ GALORE_API int galore_step(const void* G, int32_t g_dtype, int64_t m, int64_t n,
                            float* M, float* V, int64_t ldm, int64_t stride_m, int32_t r, int32_t p, int32_t q,
                            uint64_t seed, uint64_t sketch_index0, int64_t tau, int32_t T, float beta1,
                            float beta2, float eps, float lr, float alpha, int32_t flags, int32_t* info,
-                           int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream);
+                           int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                           hipStream_t aux_stream);
 
 #ifdef __cplusplus
 }

@@ -108,16 +108,35 @@ hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, dou
 // Replace columns flagged deficient by a deterministic generic unit vector.
 hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, const int* defic,
                                  int batch, hipStream_t stream);
-// Yt (k x k, column c contiguous) = columns of Y = R^T in fp32 from the fp64
-// factor (the row-major upper triangle of R); clears the rotation counters.
+// Yt (k x k, column c contiguous) = columns of 2^e Y, Y = R^T, in fp32 from the
+// fp64 factor (the row-major upper triangle of R), with the power of two e of
+// each matrix (written to exps[b]) taken from the diagonal diag (k fp64 per
+// matrix) of the Gram that R factors; clears the rotation counters.
 hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Yt, int64_t strideX,
-                                 int* rot, int max_sweeps, int batch, hipStream_t stream);
+                                 int* rot, int max_sweeps, const double* diag, int* exps, int batch,
+                                 hipStream_t stream);
 hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
                               int max_sweeps, double tol, int batch, hipStream_t stream);
-// scratch: at least 2 k + r doubles per matrix at stride strideScratch (doubles)
+// scratch: at least 2 k + r doubles per matrix at stride strideScratch (doubles);
+// exps: the per-matrix exponents launch_jacobi_prepare wrote (sigma = 2^-e |y|);
+// Xa (optional, k x k fp32 per matrix at strideX): all k ordered unit columns
+// (column j contiguous) for launch_refine, flags[b] = 1 when matrix b has them
+// (every column norm finite and positive), else 0
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
                                   float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
-                                  double* scratch, int64_t strideScratch, int batch, hipStream_t stream);
+                                  double* scratch, int64_t strideScratch, const int* exps, float* Xa, int* flags,
+                                  int batch, hipStream_t stream);
+// fp64 refinement of the small SVD's vectors (refine.hip): one Ogita-Aishima
+// step on H = R^T R (R: the row-major upper triangle of the fp64 Cholesky
+// factor) from the vectors in the rows of Xa, then the r refined vectors of
+// largest Rayleigh quotient re-orthonormalised among themselves and written as
+// the columns of Ur (k x r) with sigma = sqrt(lambda). Xa, Xb: fp32 k x k
+// (scratch afterwards); T, S, G: fp64 k x k scratch at strideKK; lam: k doubles
+// per matrix. Only the matrices whose flag is set are touched.
+hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb, int64_t strideX, double* T,
+                         double* S, double* G, int64_t strideKK, double* lam, int k, int r, float* Ur,
+                         int64_t strideUr, float* sigma, int64_t stride_sigma, const int* flags, int batch,
+                         hipStream_t stream);
 // Subspace switch: negate the columns of P_new whose overlap with the same
 // column of P_old is negative (rows x r each); flips (batch x r, may be null)
 // receives 1 for a negated column.

@@ -60,7 +60,7 @@ bool digits_fit(const Shape& sh) {
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
     size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
-        offTheta;
+        offJexp, offTheta, offXb, offS, offGg, offLam, offFlags;
     int64_t strideTheta;
     // bf16-stored gradients only: transposed copy of G (n x ldgt) and three
     // bf16 planes of the split fp32 operand (k x ldpl each)
@@ -101,6 +101,16 @@ Layout make_layout(const Shape& sh, int r, int batch, bool bf16) {
     L.offDef = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(int));
     L.offDiag0 = take(B * static_cast<size_t>(pad_elems(k)) * sizeof(double));
     L.offRot = take(B * kMaxSweeps * sizeof(int));
+    L.offJexp = take(B * sizeof(int));
+    // fp64 refinement of the small SVD: a second fp32 k x k vector buffer, the
+    // symmetric S and G, the Rayleigh quotients and the per-matrix flags (the
+    // first vector buffer and T reuse the fp32 and fp64 inverse regions, free
+    // after the last Cholesky)
+    L.offXb = take(B * L.strideKK * sizeof(float));
+    L.offS = take(B * L.strideKK * sizeof(double));
+    L.offGg = take(B * L.strideKK * sizeof(double));
+    L.offLam = take(B * static_cast<size_t>(k) * sizeof(double));
+    L.offFlags = take(B * sizeof(int));
     // scratch of the orthonormal completion in the small-SVD finalize: 2k + r doubles
     L.strideTheta = 2 * pad_elems(2 * k + r);
     L.offTheta = take(B * L.strideTheta * sizeof(float));
@@ -317,47 +327,47 @@ int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, f
     return GALORE_OK;
 }
 
-// Latency-bound stages (the small SVD's sweeps, the blocked Cholesky) run the
-// second half of the batch on a library-owned stream (one per device, default
-// priority, non-blocking), forked from and joined back into the caller's
-// stream with events: the two halves' launch sequences then run side by side,
-// so that one half's small or phase-bound launches overlap the other's
-// (measured on 64 x 4096x11008: Jacobi 103 -> 95 ms; four streams 91 ms, eight
-// far slower once the process's hardware queues are oversubscribed). The
-// enqueue sequence holds a lock, so concurrent callers on one device cannot
-// interleave their fork and join events.
-struct AuxStream {
-    hipStream_t stream = nullptr;
+// Latency-bound stages (the small SVD's sweeps, the blocked Cholesky) can run
+// the second half of the batch on a second stream supplied by the caller,
+// forked from and joined back into the caller's main stream with events: the
+// two halves' launch sequences then run side by side, so that one half's small
+// or phase-bound launches overlap the other's (measured on 64 x 4096x11008:
+// Jacobi 103 -> 95 ms, Cholesky 28 -> 25 ms). Without a second stream
+// everything runs in order on the main stream. The library creates no stream;
+// the two fork/join events of each device are created on first use and kept
+// for the process, and the enqueue sequence holds a lock, so concurrent
+// callers on one device cannot interleave their fork and join records.
+struct ForkJoin {
     hipEvent_t fork = nullptr, join = nullptr;
 };
-std::mutex g_aux_mutex;
-std::map<int, AuxStream> g_aux;   // by device
+std::mutex g_fj_mutex;
+std::map<int, ForkJoin> g_fj;   // by device
 
 // f(first, count, stream) enqueues the work of matrices [first, first + count)
 template <typename F>
-int on_two_streams(int batch, hipStream_t stream, F&& f) {
-    if (batch < 2) return f(0, batch, stream);
-    std::lock_guard<std::mutex> lock(g_aux_mutex);
+int on_two_streams(int batch, hipStream_t stream, hipStream_t aux, F&& f) {
+    if (batch < 2 || aux == nullptr || aux == stream) return f(0, batch, stream);
+    std::lock_guard<std::mutex> lock(g_fj_mutex);
     int dev = 0;
     GALORE_TRY(hipGetDevice(&dev));
-    AuxStream& aux = g_aux[dev];
-    if (aux.stream == nullptr) {
-        GALORE_TRY(hipStreamCreateWithFlags(&aux.stream, hipStreamNonBlocking));
-        GALORE_TRY(hipEventCreateWithFlags(&aux.fork, hipEventDisableTiming));
-        GALORE_TRY(hipEventCreateWithFlags(&aux.join, hipEventDisableTiming));
+    ForkJoin& fj = g_fj[dev];
+    if (fj.fork == nullptr) {
+        GALORE_TRY(hipEventCreateWithFlags(&fj.fork, hipEventDisableTiming));
+        GALORE_TRY(hipEventCreateWithFlags(&fj.join, hipEventDisableTiming));
     }
     const int h1 = batch / 2;
-    GALORE_TRY(hipEventRecord(aux.fork, stream));
-    GALORE_TRY(hipStreamWaitEvent(aux.stream, aux.fork, 0));
+    GALORE_TRY(hipEventRecord(fj.fork, stream));
+    GALORE_TRY(hipStreamWaitEvent(aux, fj.fork, 0));
     int e = f(0, h1, stream);
-    if (e == GALORE_OK) e = f(h1, batch - h1, aux.stream);
-    GALORE_TRY(hipEventRecord(aux.join, aux.stream));
-    GALORE_TRY(hipStreamWaitEvent(stream, aux.join, 0));
+    if (e == GALORE_OK) e = f(h1, batch - h1, aux);
+    GALORE_TRY(hipEventRecord(fj.join, aux));
+    GALORE_TRY(hipStreamWaitEvent(stream, fj.join, 0));
     return e;
 }
 
-int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, int batch, hipStream_t stream) {
-    return on_two_streams(batch, stream, [&](int b0, int cnt, hipStream_t st) -> int {
+int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, int batch, hipStream_t stream,
+                          hipStream_t aux) {
+    return on_two_streams(batch, stream, aux, [&](int b0, int cnt, hipStream_t st) -> int {
         for (int sw = 0; sw < kMaxSweeps; ++sw)
             for (int stp = 0; stp < nb - 1; ++stp)
                 GALORE_TRY(launch_jacobi_step(Yt + b0 * strideKK, k, strideKK, nb, stp, sw, rot + b0 * kMaxSweeps,
@@ -367,9 +377,9 @@ int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, 
 }
 
 // Cholesky of the k x k Gram region (and, with rinv, the inverse of the factor)
-int enqueue_cholesky(const Work& w, int k, bool with_inverse, int batch, hipStream_t stream) {
+int enqueue_cholesky(const Work& w, int k, bool with_inverse, int batch, hipStream_t stream, hipStream_t aux) {
     const Layout& L = *w.L;
-    return on_two_streams(batch, stream, [&](int b0, int cnt, hipStream_t st) -> int {
+    return on_two_streams(batch, stream, aux, [&](int b0, int cnt, hipStream_t st) -> int {
         const int64_t o = b0 * L.strideKK;
         GALORE_TRY(launch_cholesky(w.d(L.offC) + o, k, L.strideKK, with_inverse ? w.f(L.offRinv) + o : nullptr,
                                    w.d(L.offXinv) + o, L.strideKK, w.i(L.offDef) + static_cast<int64_t>(b0) * k,
@@ -402,12 +412,12 @@ GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, i
 // fixed-point image of In, fp64 factor);
 // columns found dependent are replaced by generic unit vectors.
 int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
-              hipStream_t st, Tracer& tr, bool cmax_ready) {
+              hipStream_t st, hipStream_t aux, Tracer& tr, bool cmax_ready) {
     const Layout& L = *w.L;
     GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k, cmax_ready), batch, st));
     if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
     {
-        const int e = enqueue_cholesky(w, k, true, batch, st);
+        const int e = enqueue_cholesky(w, k, true, batch, st, aux);
         if (e != GALORE_OK) return e;
     }
     if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
@@ -426,7 +436,7 @@ int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int ro
 int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r,
               int32_t p, int32_t q, uint64_t seed, uint64_t sketch_index0, float* P, int64_t ldp,
               int64_t stride_p, float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
-              void* workspace, size_t workspace_bytes, hipStream_t stream, Tracer& tr) {
+              void* workspace, size_t workspace_bytes, hipStream_t stream, hipStream_t aux, Tracer& tr) {
     if (G == nullptr || P == nullptr || workspace == nullptr) return GALORE_ERR_INVALID_ARG;
     if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
     if (m < 1 || n < 1 || r < 1 || p < 0 || q < 0 || batch < 1) return GALORE_ERR_SHAPE;
@@ -481,7 +491,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     float* Qtmp = Sb;
     auto orth_s = [&](int passes) -> int {
         for (int ps = 0; ps < passes; ++ps) {
-            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, tr, ps == 0 && ready);
+            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, aux, tr, ps == 0 && ready);
             if (e != GALORE_OK) return e;
             float* t = Q;
             Q = Qtmp;
@@ -493,7 +503,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     // a4: power iterations with re-orthonormalisation after every product
     for (int it = 0; it < q; ++it) {
         GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready));
-        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, tr, ready));
+        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, aux, tr, ready));
         GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS, ready));
         {
             float* t = Q;
@@ -508,7 +518,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
         GALORE_TRACED(tr, GALORE_STAGE_GRAM,
                       launch_gram_i8(gram_args(w, L1, L.strideL, l, k, ready), batch, stream));
         if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
-        GALORE_CHECK(enqueue_cholesky(w, k, false, batch, stream));
+        GALORE_CHECK(enqueue_cholesky(w, k, false, batch, stream, aux));
         if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
     }
     // a6: one-sided Jacobi on the columns of Y = R^T: Y W = U Sigma, U = left
@@ -517,15 +527,21 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     int* rot = w.i(L.offRot);
     float* Ur = w.f(L.offUr);
     if (tr.begin(GALORE_STAGE_JACOBI) != hipSuccess) return GALORE_ERR_HIP;
-    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Yt, L.strideKK, rot, kMaxSweeps, batch,
-                                     stream));
+    int* jexp = w.i(L.offJexp);
+    GALORE_TRY(launch_jacobi_prepare(w.d(L.offC), k, L.strideKK, Yt, L.strideKK, rot, kMaxSweeps, w.d(L.offDiag0),
+                                     jexp, batch, stream));
     const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
     const int nb = nblk_real + (nblk_real & 1);
-    GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, batch, stream));
+    GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, batch, stream, aux));
     GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
                                       kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
-                                      L.strideTheta / 2, batch, stream));
+                                      L.strideTheta / 2, jexp, w.f(L.offRinv), w.i(L.offFlags), batch, stream));
     if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
+    // fp64 refinement of the vectors the fp32 sweeps produced
+    GALORE_TRACED(tr, GALORE_STAGE_REFINE,
+                  launch_refine(w.d(L.offC), L.strideKK, w.f(L.offRinv), w.f(L.offXb), L.strideKK, w.d(L.offXinv),
+                                w.d(L.offS), w.d(L.offGg), L.strideKK, w.d(L.offLam), k, r, Ur, L.strideUr, sigma,
+                                stride_sigma, w.i(L.offFlags), batch, stream));
     // a7: P = Q U_B[:, :r], canonical signs
     {
         GemmArgs a{};
@@ -633,17 +649,17 @@ int galore_rsvd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int
                        int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
                        uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
                        float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
-                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                       void* workspace, size_t workspace_bytes, hipStream_t stream, hipStream_t aux_stream) {
     Tracer tr{nullptr, nullptr, 0, 0, stream};
     return rsvd_impl(G, g_dtype, m, n, ldg, stride_g, r, p, q, seed, sketch_index0, P, ldp, stride_p, sigma,
-                     stride_sigma, info, batch, workspace, workspace_bytes, stream, tr);
+                     stride_sigma, info, batch, workspace, workspace_bytes, stream, aux_stream, tr);
 }
 
 int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                               int64_t stride_g, int32_t r, int32_t p, int32_t q, uint64_t seed,
                               uint64_t sketch_index0, float* P, int64_t ldp, int64_t stride_p,
                               float* sigma, int64_t stride_sigma, int32_t* info, int32_t batch,
-                              void* workspace, size_t workspace_bytes, hipStream_t stream,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream, hipStream_t aux_stream,
                               hipEvent_t* events, int32_t* stages, int32_t capacity, int32_t* count) {
     if (capacity < 0 || (capacity > 0 && (events == nullptr || stages == nullptr)) || count == nullptr)
         return GALORE_ERR_INVALID_ARG;
@@ -651,7 +667,7 @@ int galore_rsvd_update_traced(const void* G, int32_t g_dtype, int64_t m, int64_t
         if (events[i] == nullptr) return GALORE_ERR_INVALID_ARG;
     Tracer tr{events, stages, capacity, 0, stream};
     const int st = rsvd_impl(G, g_dtype, m, n, ldg, stride_g, r, p, q, seed, sketch_index0, P, ldp, stride_p,
-                             sigma, stride_sigma, info, batch, workspace, workspace_bytes, stream, tr);
+                             sigma, stride_sigma, info, batch, workspace, workspace_bytes, stream, aux_stream, tr);
     *count = tr.count;
     return st;
 }
@@ -663,12 +679,13 @@ size_t galore_svd_workspace_size(int64_t m, int64_t n, int32_t r, int32_t batch,
 
 int galore_svd_update(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r,
                       float* P, int64_t ldp, int64_t stride_p, float* sigma, int64_t stride_sigma, int32_t* info,
-                      int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                      int32_t batch, void* workspace, size_t workspace_bytes, hipStream_t stream,
+                      hipStream_t aux_stream) {
     if (m < 1 || n < 1 || r < 1 || std::min(m, n) > kMaxK || r > std::min(m, n)) return GALORE_ERR_SHAPE;
     // k = s: the sketch spans the whole short side, so no power iteration is needed
     Tracer tr{nullptr, nullptr, 0, 0, stream};
     return rsvd_impl(G, g_dtype, m, n, ldg, stride_g, r, static_cast<int32_t>(std::min(m, n) - r), 0, 0, 0, P, ldp,
-                     stride_p, sigma, stride_sigma, info, batch, workspace, workspace_bytes, stream, tr);
+                     stride_p, sigma, stride_sigma, info, batch, workspace, workspace_bytes, stream, aux_stream, tr);
 }
 
 // Workspace of the projection with a bf16 gradient: the three bf16 planes of
@@ -1135,7 +1152,7 @@ int galore_step(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ld
                 int64_t ldm, int64_t stride_m, int32_t r, int32_t p, int32_t q, uint64_t seed,
                 uint64_t sketch_index0, int64_t tau, int32_t T, float beta1, float beta2, float eps, float lr,
                 float alpha, int32_t flags, int32_t* info, int32_t batch, void* workspace, size_t workspace_bytes,
-                hipStream_t stream) {
+                hipStream_t stream, hipStream_t aux_stream) {
     if (G == nullptr || W == nullptr || P == nullptr || M == nullptr || V == nullptr) return GALORE_ERR_INVALID_ARG;
     if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
     if (tau < 0 || T < 1) return GALORE_ERR_INVALID_ARG;
@@ -1176,7 +1193,7 @@ int galore_step(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ld
             GALORE_TRY(launch_copy_rows(M, ldm, sm, Mold, sh.l, sl.strideMold, r, static_cast<int>(sh.l), batch,
                                         stream));
         int st = galore_rsvd_update(G, g_dtype, m, n, ldg, sg, r, p, q, seed, sketch_index0, P, ldp, sp, sigma, r,
-                                    info, batch, ws, sl.offSigma, stream);
+                                    info, batch, ws, sl.offSigma, stream, aux_stream);
         if (st != GALORE_OK) return st;
         if (align)
             GALORE_TRY(launch_align(Pold, r, sl.stridePold, P, ldp, sp, static_cast<int>(sh.s), r, nullptr, batch,

@@ -34,6 +34,8 @@
 // If one of them is among the r leading columns, the finalize kernel replaces
 // it by an orthonormal completion (unit vectors orthogonalised twice against
 // the columns already kept), the singular value staying 0.
+#include <float.h>
+
 #include <type_traits>
 
 #include "common.hpp"
@@ -62,13 +64,43 @@ __device__ __forceinline__ int ring_slot(int pos, int step, int n) {
     return 1 + v;
 }
 
+// Power-of-two exponent e of each matrix with 2^e sqrt(max_j d_j) in [1/2, 1),
+// d = the diagonal of the Gram Z^T Z that R factors (the squared column norms
+// of B^T). Y = R^T enters the sweeps as 2^e R^T: the fp32 columns and the
+// fp32 matrix-core partial sums of their Gram then neither underflow nor
+// overflow whatever the gradient's scale (a gradient with singular values near
+// 1e-20 would otherwise give partial products below the fp32 range and pass
+// as converged), and sigma is scaled back by 2^-e, exactly. A zero or
+// non-finite maximum gives e = 0.
+__global__ __launch_bounds__(256) void jacobi_scale_kernel(const double* diagb, int k, int* expb) {
+    const int b = blockIdx.x;
+    const double* d = diagb + static_cast<int64_t>(b) * k;
+    __shared__ double red[4];
+    double mx = 0.0;
+    for (int i = threadIdx.x; i < k; i += blockDim.x) mx = fmax(mx, d[i]);   // fmax drops NaN
+    for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o));
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        mx = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+        int e = 0;
+        if (mx > 0.0 && mx <= DBL_MAX) {
+            int ex;
+            frexp(sqrt(mx), &ex);      // sqrt(mx) = f 2^ex, f in [1/2, 1)
+            e = -ex;
+        }
+        expb[b] = e;
+    }
+}
+
 __global__ __launch_bounds__(256) void jacobi_prepare_kernel(const double* Rb, int k,
                                                              int64_t strideR, float* Ytb,
                                                              int64_t strideX, int* rotb,
-                                                             int max_sweeps) {
+                                                             int max_sweeps, const int* expb) {
     const int b = blockIdx.y;
     const double* R = Rb + static_cast<int64_t>(b) * strideR;
     float* Yt = Ytb + static_cast<int64_t>(b) * strideX;
+    const int e = expb[b];
     if (blockIdx.x == 0 && threadIdx.x < static_cast<unsigned>(max_sweeps))
         rotb[static_cast<int64_t>(b) * max_sweeps + threadIdx.x] = 0;
     const int64_t total = static_cast<int64_t>(k) * k;
@@ -77,7 +109,7 @@ __global__ __launch_bounds__(256) void jacobi_prepare_kernel(const double* Rb, i
          pos += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int c = static_cast<int>(pos / k);
         const int i = static_cast<int>(pos - static_cast<int64_t>(c) * k);
-        Yt[pos] = (i >= c) ? static_cast<float>(R[pos]) : 0.0f;
+        Yt[pos] = (i >= c) ? static_cast<float>(ldexp(R[pos], e)) : 0.0f;
     }
 }
 
@@ -260,8 +292,10 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
     }
 
     // ---- 2. convergence test: every column pair orthogonal to the tolerance?
-    //         |g_pq| <= tol sqrt(g_pp g_qq), compared squared; zero columns
-    //         never count, a NaN entry does (it must not pass as converged)
+    //         |g_pq| <= tol sqrt(g_pp g_qq), compared squared; a pair with a
+    //         zero column never counts, a pair with a NaN or Inf entry always
+    //         does (non-finite input must not pass as converged: such a matrix
+    //         runs every sweep and reports the sweep limit)
     {
         const double tol2 = tol * tol;
         int need = 0;
@@ -270,7 +304,7 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
             if (q > p) {
                 const double dd = G[p][p] * G[q][q];
                 const double gpq = G[p][q];
-                if (dd > 0.0 && !(gpq * gpq <= tol2 * dd)) need = 1;
+                if (dd != 0.0 && (!(dd <= DBL_MAX) || !(gpq * gpq <= tol2 * dd))) need = 1;
             }
         }
         need = __syncthreads_or(need);
@@ -522,7 +556,8 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
                                                               int r, float* Urb, int64_t strideUr,
                                                               float* sigma, int64_t stride_sigma,
                                                               const int* rotb, int max_sweeps, int* info,
-                                                              double* scratchb, int64_t strideScratch) {
+                                                              double* scratchb, int64_t strideScratch,
+                                                              const int* expb, float* Xab, int* flags) {
     extern __shared__ unsigned char smem[];
     double* sig = reinterpret_cast<double*>(smem);
     int* perm = reinterpret_cast<int*>(sig + k);
@@ -557,7 +592,7 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
     }
     if (sigma != nullptr) {
         for (int j = tid; j < r; j += blockDim.x) {
-            const double v = sig[perm[j]];
+            const double v = ldexp(sig[perm[j]], -expb[b]);     // undo the sweeps' scaling
             sigma[static_cast<int64_t>(b) * stride_sigma + j] = (v > 0.0 || v != v) ? static_cast<float>(v) : 0.0f;
         }
     }
@@ -570,12 +605,34 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
         const int c = perm[j];
         Ur[static_cast<int64_t>(i) * r + j] = static_cast<float>(static_cast<double>(Yt[static_cast<int64_t>(c) * k + i]) / sig[c]);
     }
+    if (Xab != nullptr) {
+        // all k columns, ordered and normalised (column j of the result
+        // contiguous), for the fp64 refinement; only when every column norm is
+        // finite and positive (rank-deficient and non-finite matrices keep the
+        // vectors above and are not refined)
+        const bool refinable = (nkeep == r) && sig[perm[k - 1]] > 0.0 && sig[perm[0]] <= DBL_MAX;
+        if (tid == 0) flags[b] = refinable ? 1 : 0;
+        if (refinable) {
+            float* Xa = Xab + static_cast<int64_t>(b) * strideX;
+            const int64_t kk = static_cast<int64_t>(k) * k;
+            for (int64_t pos = tid; pos < kk; pos += blockDim.x) {
+                const int j = static_cast<int>(pos / k);
+                const int i = static_cast<int>(pos - static_cast<int64_t>(j) * k);
+                const int c = perm[j];
+                Xa[pos] = static_cast<float>(static_cast<double>(Yt[static_cast<int64_t>(c) * k + i]) / sig[c]);
+            }
+        }
+    }
     if (tid == 0 && info != nullptr) {
+        // 0: converged; max_sweeps: no sweep came out rotation-free;
+        // max_sweeps + 1: a column norm is NaN or Inf (non-finite input)
         const int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
         int result = max_sweeps;
         for (int w = 0; w < max_sweeps; ++w) {
             if (rot[w] == 0) { result = 0; break; }
         }
+        for (int c = 0; c < k; ++c)
+            if (!(sig[c] <= DBL_MAX)) result = max_sweeps + 1;
         info[b] = result;
     }
     if (nkeep >= r) return;
@@ -651,11 +708,13 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
 }  // namespace
 
 hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Yt, int64_t strideX,
-                                 int* rot, int max_sweeps, int batch, hipStream_t stream) {
+                                 int* rot, int max_sweeps, const double* diag, int* exps, int batch,
+                                 hipStream_t stream) {
+    hipLaunchKernelGGL(jacobi_scale_kernel, dim3(batch), dim3(256), 0, stream, diag, k, exps);
     int64_t blocks = (static_cast<int64_t>(k) * k + 255) / 256;
     if (blocks > 4096) blocks = 4096;
     hipLaunchKernelGGL(jacobi_prepare_kernel, dim3(static_cast<unsigned>(blocks), batch), dim3(256),
-                       0, stream, R, k, strideR, Yt, strideX, rot, max_sweeps);
+                       0, stream, R, k, strideR, Yt, strideX, rot, max_sweeps, exps);
     return hipGetLastError();
 }
 
@@ -671,10 +730,11 @@ hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, in
 
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
                                   float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
-                                  double* scratch, int64_t strideScratch, int batch, hipStream_t stream) {
+                                  double* scratch, int64_t strideScratch, const int* exps, float* Xa, int* flags,
+                                  int batch, hipStream_t stream) {
     const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
     hipLaunchKernelGGL(jacobi_finalize_kernel, dim3(batch), dim3(256), shmem, stream, Yt, k, strideX, r, Ur,
-                       strideUr, sigma, stride_sigma, rot, max_sweeps, info, scratch, strideScratch);
+                       strideUr, sigma, stride_sigma, rot, max_sweeps, info, scratch, strideScratch, exps, Xa, flags);
     return hipGetLastError();
 }
 

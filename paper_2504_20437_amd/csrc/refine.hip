@@ -1,0 +1,361 @@
+// fp64 refinement of the small SVD's singular vectors (Ogita & Aishima 2018,
+// "Iterative refinement for symmetric eigenvalue decomposition", Japan J.
+// Indust. Appl. Math. 35: one Newton-type correction built from matrix
+// products only).
+//
+// The left singular vectors of B (paper §4.1.2: the direct SVD of the small
+// projected matrix of Halko et al. 2011) are the eigenvectors of
+// H = B B^T = R^T R, with R the fp64 Cholesky factor of the exact Gram. The
+// block Jacobi (jacobi.hip) produces them in fp32: its columns live in fp32 and
+// each of the ~330 rotations a column takes adds fp32 rounding, so two
+// singular vectors whose singular values differ by a relative 3e-4 (the gap at
+// r of a spectrum whose tail is in the noise bulk) stay mixed at the 1e-3
+// level. Each refinement step, with X the current vectors (columns, fp32):
+//   T = R X                         (fp64)
+//   S = T^T T = X^T H X,  G = X^T X (fp64, symmetric)
+//   lambda_i = S_ii / G_ii
+//   E_ij = (S_ij + lambda_j (delta_ij - G_ij)) / (lambda_j - lambda_i)   i != j
+//        = (delta_ij - G_ij) / 2                                          otherwise
+//   X <- X + X E
+// where "otherwise" is the diagonal and every pair whose correction would
+// exceed 0.1 (a pair of near-equal eigenvalues, whose individual vectors are
+// not determined by H at this accuracy: it is only re-orthogonalised). The
+// step leaves the span of the r leading vectors accurate to second order in
+// the error before it (1e-3 -> about 1e-6), but their basis only orthonormal to
+// first order (the corrections of near-equal pairs are large); so the r vectors
+// of largest lambda are then re-orthonormalised among themselves, which keeps
+// their span: X_r <- X_r (I - D / 2), D = X_r^T X_r - I, first-order Lowdin
+// (orthonormal to O(|D|^2)).
+//
+// Layouts (per matrix, k x k, ld = k): X is stored by columns (Xt: column c
+// contiguous, i.e. X^T row-major, as the Jacobi stores its columns); R is the
+// row-major upper triangle left by the Cholesky (the lower triangle holds
+// stale data and is masked); T is stored as T^T; S and G are full symmetric;
+// E is stored transposed (Et[j][i] = E_ij).
+// The products run on the fp64 matrix cores (v_mfma_f64_16x16x4f64), 64 x 64
+// output tiles, four waves of 32 x 32, operands loaded straight into registers
+// as pairs along the contraction index.
+#include <float.h>
+
+#include "common.hpp"
+
+namespace galore {
+namespace {
+
+constexpr int RT = 64;      // output tile
+constexpr double kEmax = 0.1;
+
+typedef double f64x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// (M[row * ld + t], M[row * ld + t + 1]) in fp64, zero outside row < nr, t < nt
+template <typename T>
+__device__ __forceinline__ f64x2 pair_at(const T* M, int64_t ld, int row, int t, int nr, int nt, bool vec) {
+    f64x2 p = {0.0, 0.0};
+    if (row < nr) {
+        const T* q = M + static_cast<int64_t>(row) * ld + t;
+        if (vec && t + 1 < nt) {
+            if constexpr (sizeof(T) == 8) {
+                p = *reinterpret_cast<const f64x2*>(q);
+            } else {
+                const f32x2 f = *reinterpret_cast<const f32x2*>(q);
+                p = f64x2{static_cast<double>(f[0]), static_cast<double>(f[1])};
+            }
+        } else {
+            if (t < nt) p[0] = static_cast<double>(q[0]);
+            if (t + 1 < nt) p[1] = static_cast<double>(q[1]);
+        }
+    }
+    return p;
+}
+
+// C[m][n] = sum_{t < kc} A[m][t] B[n][t] for m, n < nn (both operands row-major
+// with the contraction index contiguous, row pitch ld; C row pitch ldc). TRI: B
+// is upper triangular (B[n][t] = 0 for t < n; the stored lower part is
+// ignored). SYM: A == B, only the upper tiles are computed and each off-diagonal
+// tile is also stored mirrored, so C is full and symmetric. Every matrix whose
+// flag is 0 is skipped. grid: (tiles, batch).
+template <typename TA, typename TB, bool TRI, bool SYM>
+__global__ __launch_bounds__(256) void refine_nt_kernel(const TA* Ab, int64_t strideA, const TB* Bb, int64_t strideB,
+                                                        double* Cb, int64_t strideC, int nn, int kc, int64_t ld,
+                                                        int64_t ldc, const int* flags) {
+    const int b = blockIdx.y;
+    if (flags[b] == 0) return;
+    const int nt = (nn + RT - 1) / RT;
+    int tm, tn;
+    if (SYM) {
+        int idx = blockIdx.x, u = 0;
+        while (idx >= nt - u) {
+            idx -= nt - u;
+            ++u;
+        }
+        tm = u;
+        tn = u + idx;
+    } else {
+        tm = blockIdx.x / nt;
+        tn = blockIdx.x % nt;
+    }
+    const TA* A = Ab + static_cast<int64_t>(b) * strideA;
+    const TB* B = Bb + static_cast<int64_t>(b) * strideB;
+    double* C = Cb + static_cast<int64_t>(b) * strideC;
+    const int m0 = RT * tm, n0 = RT * tn;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l16 = lane & 15, g = lane >> 4;
+    const bool vec = (ld & 1) == 0;
+    // B[n][t] = 0 for t < n: the tile needs t >= n0 only
+    const int tlo = TRI ? n0 : 0;
+    int ra[2], rb[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        ra[x] = m0 + 32 * wm + 16 * x + l16;
+        rb[x] = n0 + 32 * wn + 16 * x + l16;
+    }
+    f64x4 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+    auto load = [&](int t0, f64x2* a, f64x2* bv) {
+        const int t = t0 + 2 * g;
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            a[x] = pair_at(A, ld, ra[x], t, nn, kc, vec);
+            f64x2 q = pair_at(B, ld, rb[x], t, nn, kc, vec);
+            if (TRI) {
+                if (t < rb[x]) q[0] = 0.0;
+                if (t + 1 < rb[x]) q[1] = 0.0;
+            }
+            bv[x] = q;
+        }
+    };
+    f64x2 a[2], bv[2], an[2] = {}, bn[2] = {};
+    load(tlo, a, bv);
+    for (int t0 = tlo; t0 < kc; t0 += 8) {
+        if (t0 + 8 < kc) load(t0 + 8, an, bn);
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x][e], bv[y][e], acc[x][y], 0, 0, 0);
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            a[x] = an[x];
+            bv[x] = bn[x];
+        }
+    }
+    // accumulator register v of block (x, y): row 32 wm + 16 x + 4 v + g, column 32 wn + 16 y + l16
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = m0 + 32 * wm + 16 * x + 4 * v + g;
+                const int col = n0 + 32 * wn + 16 * y + l16;
+                if (row < nn && col < nn) {
+                    C[static_cast<int64_t>(row) * ldc + col] = acc[x][y][v];
+                    if (SYM && tm != tn) C[static_cast<int64_t>(col) * ldc + row] = acc[x][y][v];
+                }
+            }
+}
+
+// lambda_i = S_ii / G_ii; grid (batch), flags as above
+__global__ __launch_bounds__(256) void refine_lambda_kernel(const double* Sb, const double* Gb, int64_t strideKK,
+                                                            double* lamb, int k, const int* flags) {
+    const int b = blockIdx.x;
+    if (flags[b] == 0) return;
+    const double* S = Sb + static_cast<int64_t>(b) * strideKK;
+    const double* G = Gb + static_cast<int64_t>(b) * strideKK;
+    double* lam = lamb + static_cast<int64_t>(b) * k;
+    for (int i = threadIdx.x; i < k; i += blockDim.x) {
+        const int64_t d = static_cast<int64_t>(i) * k + i;
+        lam[i] = S[d] / G[d];
+    }
+}
+
+// Et[j][i] = E_ij (see the file comment); grid (ceil(k*k / 256), batch)
+__global__ __launch_bounds__(256) void refine_e_kernel(const double* Sb, const double* Gb, int64_t strideKK,
+                                                       const double* lamb, double* Etb, int k, const int* flags) {
+    const int b = blockIdx.y;
+    if (flags[b] == 0) return;
+    const int64_t pos = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (pos >= static_cast<int64_t>(k) * k) return;
+    const int j = static_cast<int>(pos / k);
+    const int i = static_cast<int>(pos - static_cast<int64_t>(j) * k);
+    const double* S = Sb + static_cast<int64_t>(b) * strideKK;
+    const double* G = Gb + static_cast<int64_t>(b) * strideKK;
+    const double* lam = lamb + static_cast<int64_t>(b) * k;
+    // S and G are symmetric: row j, column i holds S_ij and G_ij
+    const double rr = ((i == j) ? 1.0 : 0.0) - G[pos];
+    double e = 0.5 * rr;
+    if (i != j) {
+        const double lj = lam[j], li = lam[i];
+        const double num = S[pos] + lj * rr;
+        const double dl = lj - li;
+        if (dl != 0.0 && fabs(num) <= kEmax * fabs(dl)) e = num / dl;
+    }
+    Etb[static_cast<int64_t>(b) * strideKK + pos] = e;
+}
+
+// Xn[j][a] = X[j][a] + alpha sum_{i < nn} (M[j][i] - shift delta_ji) X[i][a] for
+// j < nn, a < kc: rows of X are vectors (row pitch ld), M is nn x nn fp64 (row
+// pitch ldm). With Ur != nullptr the result is written transposed,
+// Ur[a][j] (row pitch ldu), instead of into Xn.
+__global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, int64_t strideM, int64_t ldm,
+                                                            const float* Xb, int64_t strideX, float* Xnb, int nn,
+                                                            int kc, int64_t ld, double alpha, double shift,
+                                                            float* Urb, int64_t strideUr, int64_t ldu,
+                                                            const int* flags) {
+    const int b = blockIdx.y;
+    if (flags[b] == 0) return;
+    const int ntm = (nn + RT - 1) / RT, ntn = (kc + RT - 1) / RT;
+    const int tm = blockIdx.x / ntn, tn = blockIdx.x % ntn;
+    if (tm >= ntm) return;
+    const double* M = Mb + static_cast<int64_t>(b) * strideM;
+    const float* X = Xb + static_cast<int64_t>(b) * strideX;
+    const int m0 = RT * tm, n0 = RT * tn;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l16 = lane & 15, g = lane >> 4;
+    const bool vec = (ldm & 1) == 0;
+    int ra[2], cb[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+        ra[x] = m0 + 32 * wm + 16 * x + l16;
+        cb[x] = n0 + 32 * wn + 16 * x + l16;
+    }
+    f64x4 acc[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+    auto load = [&](int t0, f64x2* a, f64x2* bv) {
+        const int t = t0 + 2 * g;
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            f64x2 p = pair_at(M, ldm, ra[x], t, nn, nn, vec);
+            if (t == ra[x]) p[0] -= shift;
+            if (t + 1 == ra[x]) p[1] -= shift;
+            a[x] = p;
+            f64x2 q = {0.0, 0.0};
+            if (cb[x] < kc) {
+                if (t < nn) q[0] = static_cast<double>(X[static_cast<int64_t>(t) * ld + cb[x]]);
+                if (t + 1 < nn) q[1] = static_cast<double>(X[static_cast<int64_t>(t + 1) * ld + cb[x]]);
+            }
+            bv[x] = q;
+        }
+    };
+    f64x2 a[2], bv[2], an[2] = {}, bn[2] = {};
+    load(0, a, bv);
+    for (int t0 = 0; t0 < nn; t0 += 8) {
+        if (t0 + 8 < nn) load(t0 + 8, an, bn);
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+#pragma unroll
+            for (int x = 0; x < 2; ++x)
+#pragma unroll
+                for (int y = 0; y < 2; ++y)
+                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x][e], bv[y][e], acc[x][y], 0, 0, 0);
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+            a[x] = an[x];
+            bv[x] = bn[x];
+        }
+    }
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = m0 + 32 * wm + 16 * x + 4 * v + g;
+                const int col = n0 + 32 * wn + 16 * y + l16;
+                if (row < nn && col < kc) {
+                    const int64_t o = static_cast<int64_t>(row) * ld + col;
+                    const float val = static_cast<float>(static_cast<double>(X[o]) + alpha * acc[x][y][v]);
+                    if (Urb != nullptr)
+                        Urb[static_cast<int64_t>(b) * strideUr + static_cast<int64_t>(col) * ldu + row] = val;
+                    else
+                        Xnb[static_cast<int64_t>(b) * strideX + o] = val;
+                }
+            }
+}
+
+// Order the refined vectors by lambda (descending, ties by index; a NaN last)
+// and copy the r leading ones, in that order, to the rows of Xs (row pitch k),
+// with sigma = sqrt(lambda). grid (batch); dynamic LDS: k doubles + k ints.
+__global__ __launch_bounds__(256) void refine_sort_kernel(const float* Xtb, int64_t strideX, const double* lamb,
+                                                          int k, int r, float* Xsb, float* sigma,
+                                                          int64_t stride_sigma, const int* flags) {
+    const int b = blockIdx.x;
+    if (flags[b] == 0) return;
+    extern __shared__ unsigned char smem[];
+    double* lam = reinterpret_cast<double*>(smem);
+    int* perm = reinterpret_cast<int*>(lam + k);
+    const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
+    float* Xs = Xsb + static_cast<int64_t>(b) * strideX;
+    for (int i = threadIdx.x; i < k; i += blockDim.x) {
+        const double v = lamb[static_cast<int64_t>(b) * k + i];
+        lam[i] = (v == v) ? v : -DBL_MAX;
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < k; c += blockDim.x) {
+        const double vc = lam[c];
+        int rank = 0;
+        for (int c2 = 0; c2 < k; ++c2) rank += (lam[c2] > vc) || (lam[c2] == vc && c2 < c);
+        perm[rank] = c;
+    }
+    __syncthreads();
+    if (sigma != nullptr)
+        for (int j = threadIdx.x; j < r; j += blockDim.x)
+            sigma[static_cast<int64_t>(b) * stride_sigma + j] = static_cast<float>(sqrt(fmax(lam[perm[j]], 0.0)));
+    const int64_t total = static_cast<int64_t>(r) * k;
+    for (int64_t pos = threadIdx.x; pos < total; pos += blockDim.x) {
+        const int j = static_cast<int>(pos / k);
+        const int i = static_cast<int>(pos - static_cast<int64_t>(j) * k);
+        Xs[pos] = Xt[static_cast<int64_t>(perm[j]) * k + i];
+    }
+}
+
+}  // namespace
+
+hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb, int64_t strideX, double* T,
+                         double* S, double* G, int64_t strideKK, double* lam, int k, int r, float* Ur,
+                         int64_t strideUr, float* sigma, int64_t stride_sigma, const int* flags, int batch,
+                         hipStream_t stream) {
+    const int nt = (k + RT - 1) / RT, ntr = (r + RT - 1) / RT;
+    const dim3 full(nt * nt, batch), upper(nt * (nt + 1) / 2, batch);
+    // one step: T^T = X^T R^T (C[c][a] = sum_t Xa[c][t] R[a][t], R upper triangular)
+    hipLaunchKernelGGL((refine_nt_kernel<float, double, true, false>), full, dim3(256), 0, stream, Xa, strideX, R,
+                       strideR, T, strideKK, k, k, static_cast<int64_t>(k), static_cast<int64_t>(k), flags);
+    // S = T^T T and G = X^T X, both full symmetric
+    hipLaunchKernelGGL((refine_nt_kernel<double, double, false, true>), upper, dim3(256), 0, stream, T, strideKK, T,
+                       strideKK, S, strideKK, k, k, static_cast<int64_t>(k), static_cast<int64_t>(k), flags);
+    hipLaunchKernelGGL((refine_nt_kernel<float, float, false, true>), upper, dim3(256), 0, stream, Xa, strideX, Xa,
+                       strideX, G, strideKK, k, k, static_cast<int64_t>(k), static_cast<int64_t>(k), flags);
+    hipLaunchKernelGGL(refine_lambda_kernel, dim3(batch), dim3(256), 0, stream, S, G, strideKK, lam, k, flags);
+    // E^T into T's buffer (T is no longer needed), then Xb = Xa + Xa E
+    const int64_t kk = static_cast<int64_t>(k) * k;
+    hipLaunchKernelGGL(refine_e_kernel, dim3(static_cast<unsigned>((kk + 255) / 256), batch), dim3(256), 0, stream, S,
+                       G, strideKK, lam, T, k, flags);
+    hipLaunchKernelGGL(refine_update_kernel, full, dim3(256), 0, stream, T, strideKK, static_cast<int64_t>(k), Xa,
+                       strideX, Xb, k, k, static_cast<int64_t>(k), 1.0, 0.0, static_cast<float*>(nullptr),
+                       static_cast<int64_t>(0), static_cast<int64_t>(0), flags);
+    // the r vectors of largest lambda, in order, into the rows of Xa
+    const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
+    hipLaunchKernelGGL(refine_sort_kernel, dim3(batch), dim3(256), shmem, stream, Xb, strideX, lam, k, r, Xa, sigma,
+                       stride_sigma, flags);
+    // their Gram D = X_r^T X_r (into S), then Ur = (X_r (I - (D - I) / 2))^T
+    const dim3 upper_r(ntr * (ntr + 1) / 2, batch), full_r(ntr * nt, batch);
+    hipLaunchKernelGGL((refine_nt_kernel<float, float, false, true>), upper_r, dim3(256), 0, stream, Xa, strideX, Xa,
+                       strideX, S, strideKK, r, k, static_cast<int64_t>(k), static_cast<int64_t>(r), flags);
+    hipLaunchKernelGGL(refine_update_kernel, full_r, dim3(256), 0, stream, S, strideKK, static_cast<int64_t>(r), Xa,
+                       strideX, static_cast<float*>(nullptr), r, k, static_cast<int64_t>(k), -0.5, 1.0, Ur, strideUr,
+                       static_cast<int64_t>(r), flags);
+    return hipGetLastError();
+}
+
+}  // namespace galore

@@ -73,7 +73,7 @@ def rsvd(**kw):
     return gl.lib.galore_rsvd_update(a["G"], a["g_dtype"], a["m"], a["n"], a["ldg"], a["stride_g"], a["r"],
                                      a["p"], a["q"], a["seed"], a["si"], a["P"], a["ldp"], a["stride_p"],
                                      a["sigma"], a["stride_sigma"], a["info"], a["batch"], a["ws"],
-                                     a["ws_bytes"], a["stream"])
+                                     a["ws_bytes"], a["stream"], None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -174,7 +174,7 @@ def test_rsvd_traced_rejects():
     import paper_2504_20437_amd as gl
     f = gl.lib.galore_rsvd_update_traced
     base = [FAKE, 0, 64, 96, 96, 64 * 96, 8, 4, 1, 1, 0, FAKE, 8, 64 * 8, FAKE, 8, FAKE, 1,
-            FAKE - FAKE % 256 + 256, 1 << 40, None]
+            FAKE - FAKE % 256 + 256, 1 << 40, None, None]
     cnt = ctypes.c_int32(-1)
     ev = (ctypes.c_void_p * 2)(FAKE, None)          # second handle missing
     st = (ctypes.c_int32 * 1)()
@@ -248,7 +248,7 @@ def test_step_rejects():
     keys = list(ok)
     def call(**kw):
         a = dict(ok); a.update(kw)
-        return f(*[a[k] for k in keys], None)
+        return f(*[a[k] for k in keys], None, None)
     for kw in (dict(G=NULL), dict(W=NULL), dict(P=NULL), dict(M=NULL), dict(V=NULL), dict(dt=2), dict(tau=-1),
                dict(T=0), dict(fl=2), dict(fl=8), dict(b1=1.0), dict(b2=-0.5), dict(eps=0.0),
                dict(lr=float("nan")), dict(al=float("inf"))):
@@ -351,7 +351,7 @@ def test_svd_workspace_and_rejects():
     assert gl.galore_svd_workspace_size(4097, 5000, 8, 1) == 0
     assert gl.galore_svd_workspace_size(64, 96, 65, 1) == 0
     f = gl.lib.galore_svd_update
-    args = [FAKE, 0, 64, 96, 96, 0, 8, FAKE, 8, 0, None, 8, None, 1, FAKE - FAKE % 256 + 256, 1 << 40, None]
+    args = [FAKE, 0, 64, 96, 96, 0, 8, FAKE, 8, 0, None, 8, None, 1, FAKE - FAKE % 256 + 256, 1 << 40, None, None]
     assert f(*args[:2], 4097, 5000, 5000, *args[5:]) == -2
     assert f(*args[:6], 65, *args[7:]) == -2
     assert f(NULL, *args[1:]) == -1
@@ -372,3 +372,79 @@ def test_probe_rejects():
     assert g(FAKE, FAKE + 128, 256, None) == -1        # overlapping
     assert g(FAKE, FAKE + 4096, 0, None) == -2
     assert g(FAKE, FAKE + 4096, 100, None) == -2
+
+
+# ---------------------------------------------------------------- binding-side validation (no GPU)
+
+
+def _t(*shape, dtype=None):
+    import torch
+    return torch.zeros(shape, dtype=dtype or torch.float32)
+
+
+def _raises(fn, match):
+    with pytest.raises(ValueError, match=match):
+        fn()
+
+
+def test_binding_rejects_mismatched_tensors():
+    """The binding checks every tensor against the shapes derived from G (or W)
+    before any pointer reaches the library: a 2-D output with a batched G, a
+    sigma of the wrong length, an int64 info, a float64 P, a transposed N or a
+    low-bit projector of another batch would otherwise make the kernels write
+    past the end of a buffer. Host tensors of the right shapes are rejected as
+    not being on the device."""
+    import torch
+    import paper_2504_20437_amd as gl
+    G = _t(3, 64, 96)                                   # batch 3, s = 64, l = 96
+    r = 8
+    # subspace update
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1, P=_t(64, r)), "P must hold 3 matrices")
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1, P=_t(3, 64, r, dtype=torch.float64)), "P must be")
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1, sigma=_t(r)), "sigma must have shape")
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1, sigma=_t(3, r + 1)), "sigma must have shape")
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1, info=_t(3, dtype=torch.int64)), "info must be")
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1, info=_t(2, dtype=torch.int32)), "info must be")
+    _raises(lambda: gl.galore_rsvd_update(G.double(), r, 4, 1, 1), "gradient dtype")
+    _raises(lambda: gl.galore_rsvd_update(G, r, 4, 1, 1), "device tensor")
+    _raises(lambda: gl.galore_svd_update(G, r, P=_t(3, 96, r)), "P must hold")
+    _raises(lambda: gl.galore_rsvd_update_traced(G, r, 4, 1, 1, [], sigma=_t(r)), "sigma must have shape")
+    # projection
+    _raises(lambda: gl.galore_project(_t(3, 64, r), G, R=_t(r, 96)), "R must hold 3 matrices")
+    _raises(lambda: gl.galore_project(_t(3, 96, r), G), "P must hold")
+    _raises(lambda: gl.galore_project(_t(64, r), G), "P must hold 3 matrices")
+    _raises(lambda: gl.galore_project(_t(3, 64, r), G, R=_t(3, r, 96, dtype=torch.float64)), "R must be")
+    _raises(lambda: gl.galore_project(_t(3, 64, r), G), "device tensor")
+    # back-projection: W (m x n) fixes s, l and the batch
+    W = _t(3, 64, 96)
+    _raises(lambda: gl.galore_project_back(_t(3, 64, r), _t(r, 96), W, 1e-3, 0.25), "N must hold 3 matrices")
+    _raises(lambda: gl.galore_project_back(_t(3, 64, r), _t(3, 96, r), W, 1e-3, 0.25), "N must hold")
+    _raises(lambda: gl.galore_project_back(_t(3, 64, r), _t(3, r, 96), _t(3, 64, 96, dtype=torch.float64),
+                                           1e-3, 0.25), "W must be")
+    _raises(lambda: gl.galore_project_back(_t(3, 64, r), _t(3, r, 96), W, 1e-3, 0.25), "device tensor")
+    # Adam
+    R = _t(3, r, 96)
+    _raises(lambda: gl.galore_lowrank_adam_step(R, _t(3, r, 95), _t(3, r, 96)), "M must match")
+    _raises(lambda: gl.galore_lowrank_adam_step(R.double(), R.double(), R.double()), "R must be float32")
+    # scheduled step
+    Pm, M, V = _t(3, 64, r), _t(3, r, 96), _t(3, r, 96)
+    _raises(lambda: gl.galore_step(G, _t(64, 96), Pm, M, V, r, 4, 1, 1, 0, 10), "W must hold 3 matrices")
+    _raises(lambda: gl.galore_step(G, W, Pm, M, V, r, 4, 1, 1, 0, 10, info=_t(3, dtype=torch.int64)), "info")
+    # subspace switch
+    _raises(lambda: gl.galore_align_projector(Pm, _t(3, 64, r + 1)), "P_new must hold")
+    _raises(lambda: gl.galore_align_projector(Pm, Pm.clone(), M, M_out=_t(3, r, 97)), "M_out must hold")
+    _raises(lambda: gl.galore_align_projector(Pm, Pm.clone(), M_out=M), "M_out needs M")
+    # low-bit projector: codes of another batch, scales of another rank
+    q = gl.QuantizedProjector(_t(2, 64, r, dtype=torch.uint8), _t(2, r), 8, r)
+    _raises(lambda: gl.galore_project_quantized(q, G), "codes hold 2 matrices")
+    _raises(lambda: gl.galore_project_back_quantized(q, _t(3, r, 96), W, 1e-3, 0.25), "codes hold 2 matrices")
+    q3 = gl.QuantizedProjector(_t(3, 64, r, dtype=torch.uint8), _t(3, r - 1), 8, r)
+    _raises(lambda: gl.galore_project_quantized(q3, G), "scales must have shape")
+    q3 = gl.QuantizedProjector(_t(3, 64, r, dtype=torch.uint8), _t(3, r), 8, r)
+    _raises(lambda: gl.galore_project_back_quantized(q3, _t(3, r + 1, 96), W, 1e-3, 0.25), "N must hold")
+    # 8-bit Adam state of another shape
+    st = gl.Adam8State.__new__(gl.Adam8State)
+    st.rows, st.cols, st.batch = r, 96, 3
+    st.M8, st.V8 = _t(3, r, 96, dtype=torch.uint8), _t(3, r, 96, dtype=torch.uint8)
+    st.Ms, st.Vs = _t(3, 2), _t(3, 1)
+    _raises(lambda: gl.galore_lowrank_adam8_step(R, st), "8-bit state Ms")

@@ -3,11 +3,15 @@
 
 * The subspace update is compared with the fp64 oracle on the whole matrix, on
   spectra with a gap at r (s_i = (i+1)^-0.7 for i < r, 0 beyond, before bf16
-  rounding): projector distance <= 1e-3, singular values rtol 1e-4.
-* Projection, Adam and the weight update are checked on sampled entries, each
-  recomputed one by one on the host in fp64 from the GPU's own inputs
-  (|x - x_ref| <= 1e-6 + 1e-5 |x_ref|), plus invariants of the whole outputs
-  (P^T P = I, sign convention, sigma descending).
+  rounding): projector distance <= 1e-3, singular values rtol 1e-4; and on the
+  benchmarked gradients themselves (no gap at r): sigma rtol 1e-4, projector
+  distance reported and held to 6e-4.
+* Projection and Adam are checked on sampled entries, each recomputed one by
+  one on the host in fp64 from the GPU's own inputs (|x - x_ref| <= 1e-6 +
+  1e-5 |x_ref|); the weight update on sampled entries of the change W1 - W0
+  against -(lr alpha) P N (1e-5 lr alpha |P||N| plus the rounding of the last
+  addition); plus invariants of the whole outputs (P^T P = I, sign
+  convention, sigma descending).
 """
 import numpy as np
 import pytest
@@ -43,7 +47,8 @@ def gapped_bf16(m, n, r, seed):
     return gi.store(gi.planted_gradient(m, n, spec, 1e-6, seed=seed, rank=r), "bf16")
 
 
-@pytest.mark.parametrize("m,n,r,p", [(4096, 11008, 1024, 32), (11008, 4096, 1024, 32), (2048, 5461, 512, 16)])
+@pytest.mark.parametrize("m,n,r,p", [(4096, 11008, 1024, 32), (11008, 4096, 1024, 32), (2048, 5461, 512, 16),
+                                     (4096, 4096, 1024, 32)])
 def test_full_size_path(gl, orc, m, n, r, p):
     import torch
     q = 2
@@ -99,12 +104,46 @@ def test_full_size_path(gl, orc, m, n, r, p):
     wi = rng.integers(0, m, 64)
     wj = rng.integers(0, n, 64)
     c = f32(1e-3) * f32(0.25)
+    # the weight change W1 - W0 (exact in fp64) against -(lr alpha) P N, within
+    # 1e-5 lr alpha |P| |N| plus the fp32 rounding of the final addition
     for b in range(2):
         if m <= n:
-            ref = np.array([W0h[b][i, j] - c * (Ph[b][i, :] @ Nh[b][:, j]) for i, j in zip(wi, wj)])
+            pr = [(Ph[b][i, :], Nh[b][:, j]) for i, j in zip(wi, wj)]
         else:
-            ref = np.array([W0h[b][i, j] - c * (Ph[b][j, :] @ Nh[b][:, i]) for i, j in zip(wi, wj)])
-        assert max_rel_violation(Wh[b][wi, wj], ref, 1e-5, 1e-6) <= 1.0
+            pr = [(Ph[b][j, :], Nh[b][:, i]) for i, j in zip(wi, wj)]
+        ref = np.array([-c * (x @ y) for x, y in pr])
+        bound = np.array([c * (np.abs(x) @ np.abs(y)) for x, y in pr])
+        dW = Wh[b][wi, wj] - W0h[b][wi, wj]
+        assert np.all(np.abs(dW - ref) <= 1e-5 * bound + 2.0 ** -24 * np.abs(Wh[b][wi, wj]))
+
+
+# the bench's own inputs: the device generator with the bench's seeds, its
+# spectra ((i+1)^-0.7 at 4096 x 11008, (i+1)^-0.8 at 2048 x 5461, 1e-4 noise,
+# bf16), no gap at r
+@pytest.mark.parametrize("m,n,r,p,q,expo,seed", [(4096, 11008, 1024, 32, 2, 0.7, 5000),
+                                                 (4096, 11008, 1024, 32, 1, 0.7, 5000),
+                                                 (2048, 5461, 512, 16, 2, 0.8, 5300)])
+def test_bench_inputs_match_oracle(gl, orc, m, n, r, p, q, expo, seed):
+    """The subspace update on the benchmarked gradients themselves (no gap at
+    r: the relative gap there is about 3e-4 to 6e-4, so the projector is
+    sensitive to rounding in the weakest sketch directions) against the
+    oracle on the same stored bits and sketch: sigma within rtol 1e-4, and the
+    projector distance reported and held to 6e-4, the bound of the ungapped
+    60M- and 350M-shaped cases (the fp32 path measures about 1e-4 there)."""
+    import torch
+    s = min(m, n)
+    G = gi.torch_planted_group(m, n, 2, gi.spectrum_power(s, expo), 1e-4, seed=seed, dtype="bf16")
+    P, sig, info = gl.galore_rsvd_update(G, r, p, q, gi.sketch_seed(0), 0)
+    Ph, sh = host(P), host(sig)
+    assert (info.cpu().numpy() == 0).all()
+    Gx = G[0].float().cpu().numpy().astype(np.float64)      # the stored bf16 values, exactly
+    Pr, sr, _ = orc.rsvd_update(Gx, r, p, q, gi.sketch_seed(0), 0)
+    d = proj_dist(Ph[0], Pr)
+    srel = float(np.max(np.abs(sh[0] - sr) / sr))
+    print("bench input %dx%d q=%d: projector distance %.3e, sigma rel %.3e" % (m, n, q, d, srel))
+    assert srel <= 1e-4
+    assert d <= 6e-4, d
+    assert orth_err(Ph[0]) < 1e-4
 
 
 def test_exact_svd_full_size(gl):
