@@ -224,6 +224,31 @@ GALORE_API int galore_project(const float* P, int64_t ldp, int64_t stride_p, con
                    hipStream_t stream);
 
 /*
+ * galore_project without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving or training loops,
+ * harnesses that forbid allocation): the same projection, kernels and results
+ * as galore_project with a workspace of galore_project_workspace_size(...)
+ * bytes, with that scratch held instead in a fixed-size device array inside
+ * the library (galore_project_noalloc_max_bytes() bytes, 64 MiB; one copy on
+ * each device the library runs on, kept until the process ends). The caller
+ * passes inputs and outputs as for galore_project; the call allocates nothing
+ * (no hipMalloc, no allocating library routine). The first call on a device
+ * looks up that device's copy of the array (under a lock).
+ * Every call on a device shares that device's array: calls that overlap on one
+ * device (concurrent streams or host threads) race and must be serialised by
+ * the caller. The array needs no initial contents (each call writes every byte
+ * it reads).
+ * Errors: as galore_project; a bf16 gradient whose workspace size
+ * (galore_project_workspace_size) exceeds galore_project_noalloc_max_bytes()
+ * -> WORKSPACE, checked before any device call; the lookup of the array failing
+ * -> HIP. An fp32 gradient needs no scratch (fp32 matrix cores).
+ */
+GALORE_API size_t galore_project_noalloc_max_bytes(void);
+GALORE_API int galore_project_noalloc(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype,
+                                      int64_t m, int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R,
+                                      int64_t ldr, int64_t stride_r, int32_t batch, hipStream_t stream);
+
+/*
  * Low-rank Adam on the rows x cols projected state (paper §3 moment equations;
  * paper Alg. 1 with its bias correction applied to temporaries, the stored
  * moments staying uncorrected):

@@ -30,6 +30,7 @@ EXPORTED = (
     "galore_project_back_quantized_workspace_size", "galore_project_back_quantized",
     "galore_adam8_scale_count", "galore_lowrank_adam8_step",
     "galore_svd_workspace_size", "galore_svd_update", "galore_probe_mfma_bf16", "galore_probe_copy",
+    "galore_project_noalloc_max_bytes", "galore_project_noalloc",
 )
 
 GALORE_STEP_ALIGN = 1
@@ -112,6 +113,10 @@ def _declare(lib):
     lib.galore_probe_mfma_bf16.restype = ctypes.c_int
     lib.galore_probe_copy.argtypes = [vp, vp, sz, vp]
     lib.galore_probe_copy.restype = ctypes.c_int
+    lib.galore_project_noalloc_max_bytes.argtypes = []
+    lib.galore_project_noalloc_max_bytes.restype = sz
+    lib.galore_project_noalloc.argtypes = [vp, i64, i64, vp, i32, i64, i64, i64, i64, i32, vp, i64, i64, i32, vp]
+    lib.galore_project_noalloc.restype = ctypes.c_int
     return lib
 
 
@@ -363,6 +368,30 @@ def galore_project(P: torch.Tensor, G: torch.Tensor, R=None, workspace=None, str
         rp, _, _, ldr, sr, _ = _mat(R, "R")
         _check(lib.galore_project(pp, ldp, sp, gp, _dtype_code(G), m, n, ldg, sg, r, rp, ldr, sr, batch, wp, wb,
                                   _handle(ts)), "galore_project")
+    return R
+
+
+def galore_project_noalloc_max_bytes() -> int:
+    return int(lib.galore_project_noalloc_max_bytes())
+
+
+def galore_project_noalloc(P: torch.Tensor, G: torch.Tensor, R: torch.Tensor, stream=None):
+    """R = P^T A like galore_project with a workspace, the scratch held in the
+    library's own device array (no allocation in the call; R must be given)."""
+    m, n, _, _, batch = _geom(G, "G")
+    _dtype_code(G)
+    s, l = min(m, n), max(m, n)
+    r = _geom(P, "P")[1]
+    _expect(P, "P", s, r, batch)
+    _expect(R, "R", r, l, batch)
+    _on_device(None, G=G)
+    _on_device(G.device, P=P, R=R)
+    ts = _torch_stream(stream, G.device)
+    pp, _, _, ldp, sp, _ = _mat(P, "P")
+    gp, _, _, ldg, sg, _ = _mat(G, "G")
+    rp, _, _, ldr, sr, _ = _mat(R, "R")
+    _check(lib.galore_project_noalloc(pp, ldp, sp, gp, _dtype_code(G), m, n, ldg, sg, r, rp, ldr, sr, batch,
+                                      _handle(ts)), "galore_project_noalloc")
     return R
 
 

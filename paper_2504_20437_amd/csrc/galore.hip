@@ -611,6 +611,31 @@ int reexpress_moment(const float* P_old, int64_t ldo, int64_t so, const float* P
     return GALORE_OK;
 }
 
+// ---- the no-allocation projection's scratch ----------------------------------
+// galore_project_noalloc keeps the three bf16 planes of P^T in this file-scope
+// device array instead of a caller workspace. Every device the library runs on
+// holds its own copy for the life of the process. Host code never uses the
+// array's name as an address: the device address of each device's copy is
+// looked up once (hipGetSymbolAddress, with that device current) and kept.
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+std::mutex g_scratch_mutex;
+std::map<int, void*> g_scratch_ptr;   // by device
+
+// the current device's copy of `scratch` (nullptr if the lookup failed)
+void* scratch_on_current_device() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    auto it = g_scratch_ptr.find(dev);
+    if (it != g_scratch_ptr.end()) return it->second;
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return nullptr;
+    g_scratch_ptr[dev] = ptr;
+    return ptr;
+}
+
 }  // namespace
 
 extern "C" {
@@ -762,6 +787,29 @@ int galore_project(const float* P, int64_t ldp, int64_t stride_p, const void* G,
     GALORE_TRY(launch_gemm(ALayout::kMContig, sh.left ? BLayout::kNContig : BLayout::kKContig, false,
                            g_dtype == GALORE_BF16, a, batch, stream));
     return GALORE_OK;
+}
+
+size_t galore_project_noalloc_max_bytes(void) { return kStaticScratchBytes; }
+
+int galore_project_noalloc(const float* P, int64_t ldp, int64_t stride_p, const void* G, int32_t g_dtype, int64_t m,
+                           int64_t n, int64_t ldg, int64_t stride_g, int32_t r, float* R, int64_t ldr,
+                           int64_t stride_r, int32_t batch, hipStream_t stream) {
+    // the arguments galore_project validates, checked before any device call
+    if (P == nullptr || G == nullptr || R == nullptr) return GALORE_ERR_INVALID_ARG;
+    if (g_dtype != GALORE_F32 && g_dtype != GALORE_BF16) return GALORE_ERR_INVALID_ARG;
+    if (m < 1 || n < 1 || r < 1 || batch < 1 || m > INT32_MAX || n > INT32_MAX) return GALORE_ERR_SHAPE;
+    const Shape sh = make_shape(m, n, r, 0);
+    if (r > sh.s || ldp < r || ldg < n || ldr < sh.l) return GALORE_ERR_SHAPE;
+    if (batch > 1 && (stride_p < sh.s * ldp || stride_g < m * ldg || stride_r < r * ldr)) return GALORE_ERR_SHAPE;
+    if (g_dtype == GALORE_F32)   // the fp32 path needs no scratch
+        return galore_project(P, ldp, stride_p, G, g_dtype, m, n, ldg, stride_g, r, R, ldr, stride_r, batch, nullptr,
+                              0, stream);
+    const size_t need = make_proj_layout(sh, r, batch).total;
+    if (need > kStaticScratchBytes) return GALORE_ERR_WORKSPACE;
+    void* ws = scratch_on_current_device();
+    if (ws == nullptr) return GALORE_ERR_HIP;
+    return galore_project(P, ldp, stride_p, G, g_dtype, m, n, ldg, stride_g, r, R, ldr, stride_r, batch, ws, need,
+                          stream);
 }
 
 size_t galore_align_workspace_size(int32_t r, int32_t batch) {

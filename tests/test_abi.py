@@ -448,3 +448,22 @@ def test_binding_rejects_mismatched_tensors():
     st.M8, st.V8 = _t(3, r, 96, dtype=torch.uint8), _t(3, r, 96, dtype=torch.uint8)
     st.Ms, st.Vs = _t(3, 2), _t(3, 1)
     _raises(lambda: gl.galore_lowrank_adam8_step(R, st), "8-bit state Ms")
+
+
+def test_project_noalloc_rejects_before_any_device_call():
+    """The no-allocation projection validates like galore_project and rejects a
+    bf16 workspace need above its fixed scratch (64 MiB) with WORKSPACE, all on
+    the host (the pointers below are never dereferenced)."""
+    import paper_2504_20437_amd as gl
+    f = gl.lib.galore_project_noalloc
+    cap = gl.galore_project_noalloc_max_bytes()
+    assert cap == 64 << 20
+    m, n, r = 4096, 11008, 1024
+    one = gl.galore_project_workspace_size(m, n, r, 1, 1)
+    assert 2 * one <= cap < 3 * one                      # two bench-shaped matrices fit, three do not
+    args = lambda **kw: [kw.get(k, v) for k, v in (("P", FAKE), ("ldp", r), ("sp", m * r), ("G", FAKE), ("dt", 1),
+                                                     ("m", m), ("n", n), ("ldg", n), ("sg", m * n), ("r", r),
+                                                     ("R", FAKE), ("ldr", n), ("sr", r * n), ("b", 1), ("st", None))]
+    assert f(*args(b=3)) == -3
+    assert f(*args(P=NULL)) == -1 and f(*args(R=NULL)) == -1 and f(*args(dt=5)) == -1
+    assert f(*args(r=4097)) == -2 and f(*args(ldg=n - 1)) == -2 and f(*args(b=2, sg=m * n - 1)) == -2
