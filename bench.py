@@ -136,6 +136,9 @@ def parse():
     ap.add_argument("--whole-model", type=int, default=1,
                     help="also time a subspace update and a projected Adam step of all 224 Llama-7B-shaped "
                          "matrices (0/1; needs the default 4096x11008 batch of 64 on one stream)")
+    ap.add_argument("--extras", type=int, default=1,
+                    help="also time the schedule, the low-bit projector, the exact SVD and the 8-bit Adam (0/1; 0 "
+                         "for short profiling runs)")
     ap.add_argument("--roofline-kernel", default="auto", choices=["auto"] + sorted(KERNEL_CLASSES))
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before the workload, copy a buffer of this many MiB device to device once (a "
@@ -470,172 +473,176 @@ def main():
     if "peak_measured" in roof:
         roof["frac_measured"] = round(roof["achieved"] / roof["peak_measured"], 4)
 
-    # subspace switch (once per T steps): signs of a new projector matched to
-    # the previous one and the first moment re-expressed in the new basis;
-    # timed outside the step on a copy of the current projector
-    P_new = P.clone()
-    M_sw = torch.empty_like(M)
-    aws = torch.empty((gl.galore_align_workspace_size(r, B),), dtype=torch.uint8, device=dev)
-    sw = [mk() for _ in range(4)]
-    for j in range(2):
-        sw[2 * j].record(stream)
-        gl.galore_align_projector(P, P_new, M, M_out=M_sw, workspace=aws, stream=stream)
-        sw[2 * j + 1].record(stream)
-    torch.cuda.synchronize()
-    switch_ms = sw[2].elapsed_time(sw[3])
-    del P_new, M_sw, aws
-
-    # the schedule through the one-call step: a window of steps tau = T .. T+9
-    # (an update step with the switch, then nine steps on the same projector)
+    switch_ms = upd_ms = plain_ms = None
+    lowbit, exact_svd, whole_model, adam8 = {}, None, None, None
     T_sched = 200
-    sws = torch.empty((gl.galore_step_workspace_size(m, n, r, p, B, G.dtype, 3),), dtype=torch.uint8, device=dev)
-    sinfo = torch.zeros((B,), dtype=torch.int32, device=dev)
-    win = [mk() for _ in range(11)]
-    win[0].record(stream)
-    for j in range(10):
-        gl.galore_step(G, W, P, M, V, r, p, q, gi.sketch_seed(1), T_sched + j, T_sched, flags=3, info=sinfo,
-                       workspace=sws, stream=stream, aux_stream=aux0)
-        win[j + 1].record(stream)
-    torch.cuda.synchronize()
-    if int((sinfo != 0).sum()):
-        raise RuntimeError("small SVD did not converge in the scheduled step")
-    upd_ms = win[0].elapsed_time(win[1])
-    plain_ms = win[1].elapsed_time(win[10]) / 9.0
-    del sws
-
-    # low-bit projector: quantise the batch's projectors once per update, then
-    # each step projects and back-projects with the codes
-    lowbit = {}
-    for bits in (8, 4):
-        qws = torch.empty((gl.galore_project_quantized_workspace_size(m, n, r, B),), dtype=torch.uint8, device=dev)
-        qbws = torch.empty((gl.galore_project_back_quantized_workspace_size(m, n, r, B),), dtype=torch.uint8,
-                           device=dev)
-        qe = [mk() for _ in range(8)]
-        for j in range(2):       # the second pass is timed
-            qe[0].record(stream)
-            Pq = gl.galore_quantize_projector(P, bits, stream=stream)
-            qe[1].record(stream)
-            gl.galore_project_quantized(Pq, G, R=R, workspace=qws, stream=stream)
-            qe[2].record(stream)
-            gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, 2, stream=stream)
-            qe[3].record(stream)
-            gl.galore_project_back_quantized(Pq, N, W, 1e-3, 0.25, workspace=qbws, stream=stream)
-            qe[4].record(stream)
-        torch.cuda.synchronize()
-        lowbit["int%d" % bits] = {
-            "quantize_ms": round(qe[0].elapsed_time(qe[1]), 3),
-            "project_ms": round(qe[1].elapsed_time(qe[2]), 3),
-            "adam_ms": round(qe[2].elapsed_time(qe[3]), 3),
-            "project_back_ms": round(qe[3].elapsed_time(qe[4]), 3),
-            "step_ms": round(qe[1].elapsed_time(qe[4]), 3),
-            "projector_bytes": int(Pq.codes.numel() + 4 * Pq.scales.numel()),
-        }
-        del qws, qbws, Pq
-
-    # exact SVD (k = s) against the randomized one on the same 8 matrices
-    if s <= 4096:
-        Bx = min(B, 8)
-        xws = torch.empty((gl.galore_svd_workspace_size(m, n, r, Bx, G.dtype),), dtype=torch.uint8, device=dev)
-        xe = [mk() for _ in range(8)]
+    if args.extras:
+        # subspace switch (once per T steps): signs of a new projector matched to
+        # the previous one and the first moment re-expressed in the new basis;
+        # timed outside the step on a copy of the current projector
+        P_new = P.clone()
+        M_sw = torch.empty_like(M)
+        aws = torch.empty((gl.galore_align_workspace_size(r, B),), dtype=torch.uint8, device=dev)
+        sw = [mk() for _ in range(4)]
         for j in range(2):
-            xe[4 * j].record(stream)
-            _, _, xinfo = gl.galore_svd_update(G[:Bx], r, workspace=xws, stream=stream, aux_stream=aux0)
-            xe[4 * j + 1].record(stream)
-            gl.galore_rsvd_update(G[:Bx], r, p, q, gi.sketch_seed(0), 0, P=P[:Bx], sigma=sigma[:Bx], info=info[:Bx],
-                                  workspace=chunks[0]["ws"], stream=stream, aux_stream=aux0)
-            xe[4 * j + 2].record(stream)
+            sw[2 * j].record(stream)
+            gl.galore_align_projector(P, P_new, M, M_out=M_sw, workspace=aws, stream=stream)
+            sw[2 * j + 1].record(stream)
         torch.cuda.synchronize()
-        if int((xinfo != 0).sum()):
-            raise RuntimeError("exact SVD did not converge")
-        x_ms, rs_ms = xe[4].elapsed_time(xe[5]), xe[5].elapsed_time(xe[6])
-        exact_svd = {"batch": Bx, "exact_ms_per_matrix": round(x_ms / Bx, 3),
-                     "rsvd_ms_per_matrix": round(rs_ms / Bx, 3), "speedup": round(x_ms / rs_ms, 2),
-                     "note": "exact top-r SVD (sketch as wide as the short side, k = %d, no power iteration) against "
-                             "the randomized update (k = %d, q = %d) on the same %d matrices" % (s, k, q, Bx)}
-        del xws
-    else:
-        exact_svd = None
+        switch_ms = sw[2].elapsed_time(sw[3])
+        del P_new, M_sw, aws
 
-    # the whole Llama-7B-shaped model on this GPU: 128 square (q, k, v, o),
-    # 64 gate/up (the batch above) and 32 down matrices; a subspace update of
-    # all 224 with q = 1 and with q = 2, and one projected Adam step over all
-    whole_model = None
-    if args.whole_model and (m, n, B, S) == (4096, 11008, 64, 1):
-        groups = [{"name": "q,k,v,o 4096x4096", "m": 4096, "n": 4096, "count": 128, "seed": 5100},
-                  {"name": "down 11008x4096", "m": 11008, "n": 4096, "count": 32, "seed": 5200}]
-        for gr in groups:
-            gm, gn, gc = gr["m"], gr["n"], gr["count"]
-            gs, gl_ = min(gm, gn), max(gm, gn)
-            print("bench: generating %d x %dx%d %s gradients" % (gc, gm, gn, args.dtype), file=sys.stderr, flush=True)
-            gr["G"] = gi.torch_planted_group(gm, gn, gc, gi.spectrum_power(gs, 0.7), 1e-4, seed=gr["seed"],
-                                             dtype=args.dtype)
-            gr["W"] = torch.zeros((gc, gm, gn), dtype=torch.float32, device=dev)
-            gr["P"] = torch.empty((gc, gs, r), dtype=torch.float32, device=dev)
-            gr["sigma"] = torch.empty((gc, r), dtype=torch.float32, device=dev)
-            gr["info"] = torch.empty((gc,), dtype=torch.int32, device=dev)
-            gr["R"] = torch.empty((gc, r, gl_), dtype=torch.float32, device=dev)
-            gr["M"] = torch.zeros_like(gr["R"])
-            gr["V"] = torch.zeros_like(gr["R"])
-            gr["ws"] = torch.empty((gl.galore_rsvd_workspace_size(gm, gn, r, p, gc, G.dtype),), dtype=torch.uint8,
-                                   device=dev)
-            pw = gl.galore_project_workspace_size(gm, gn, r, gc, G.dtype)
-            gr["pws"] = torch.empty((pw,), dtype=torch.uint8, device=dev) if pw > 0 else False
-            gr["bws"] = torch.empty((gl.galore_project_back_workspace_size(gm, gn, r, gc),), dtype=torch.uint8,
-                                    device=dev)
-        groups.insert(1, {"name": "gate/up 4096x11008", "m": m, "n": n, "count": B, "G": G, "W": W, "P": P,
-                          "sigma": sigma, "info": info, "R": R, "M": M, "V": V, "ws": chunks[0]["ws"],
-                          "pws": chunks[0]["pws"], "bws": chunks[0]["bws"]})
+        # the schedule through the one-call step: a window of steps tau = T .. T+9
+        # (an update step with the switch, then nine steps on the same projector)
+        T_sched = 200
+        sws = torch.empty((gl.galore_step_workspace_size(m, n, r, p, B, G.dtype, 3),), dtype=torch.uint8, device=dev)
+        sinfo = torch.zeros((B,), dtype=torch.int32, device=dev)
+        win = [mk() for _ in range(11)]
+        win[0].record(stream)
+        for j in range(10):
+            gl.galore_step(G, W, P, M, V, r, p, q, gi.sketch_seed(1), T_sched + j, T_sched, flags=3, info=sinfo,
+                           workspace=sws, stream=stream, aux_stream=aux0)
+            win[j + 1].record(stream)
         torch.cuda.synchronize()
-        wm_ms = {}
-        for qq in (1, 2):
+        if int((sinfo != 0).sum()):
+            raise RuntimeError("small SVD did not converge in the scheduled step")
+        upd_ms = win[0].elapsed_time(win[1])
+        plain_ms = win[1].elapsed_time(win[10]) / 9.0
+        del sws
+
+        # low-bit projector: quantise the batch's projectors once per update, then
+        # each step projects and back-projects with the codes
+        lowbit = {}
+        for bits in (8, 4):
+            qws = torch.empty((gl.galore_project_quantized_workspace_size(m, n, r, B),), dtype=torch.uint8, device=dev)
+            qbws = torch.empty((gl.galore_project_back_quantized_workspace_size(m, n, r, B),), dtype=torch.uint8,
+                               device=dev)
+            qe = [mk() for _ in range(8)]
+            for j in range(2):       # the second pass is timed
+                qe[0].record(stream)
+                Pq = gl.galore_quantize_projector(P, bits, stream=stream)
+                qe[1].record(stream)
+                gl.galore_project_quantized(Pq, G, R=R, workspace=qws, stream=stream)
+                qe[2].record(stream)
+                gl.galore_lowrank_adam_step(R, M, V, N, 0.9, 0.999, 1e-8, 2, stream=stream)
+                qe[3].record(stream)
+                gl.galore_project_back_quantized(Pq, N, W, 1e-3, 0.25, workspace=qbws, stream=stream)
+                qe[4].record(stream)
+            torch.cuda.synchronize()
+            lowbit["int%d" % bits] = {
+                "quantize_ms": round(qe[0].elapsed_time(qe[1]), 3),
+                "project_ms": round(qe[1].elapsed_time(qe[2]), 3),
+                "adam_ms": round(qe[2].elapsed_time(qe[3]), 3),
+                "project_back_ms": round(qe[3].elapsed_time(qe[4]), 3),
+                "step_ms": round(qe[1].elapsed_time(qe[4]), 3),
+                "projector_bytes": int(Pq.codes.numel() + 4 * Pq.scales.numel()),
+            }
+            del qws, qbws, Pq
+
+        # exact SVD (k = s) against the randomized one on the same 8 matrices
+        if s <= 4096:
+            Bx = min(B, 8)
+            xws = torch.empty((gl.galore_svd_workspace_size(m, n, r, Bx, G.dtype),), dtype=torch.uint8, device=dev)
+            xe = [mk() for _ in range(8)]
+            for j in range(2):
+                xe[4 * j].record(stream)
+                _, _, xinfo = gl.galore_svd_update(G[:Bx], r, workspace=xws, stream=stream, aux_stream=aux0)
+                xe[4 * j + 1].record(stream)
+                gl.galore_rsvd_update(G[:Bx], r, p, q, gi.sketch_seed(0), 0, P=P[:Bx], sigma=sigma[:Bx], info=info[:Bx],
+                                      workspace=chunks[0]["ws"], stream=stream, aux_stream=aux0)
+                xe[4 * j + 2].record(stream)
+            torch.cuda.synchronize()
+            if int((xinfo != 0).sum()):
+                raise RuntimeError("exact SVD did not converge")
+            x_ms, rs_ms = xe[4].elapsed_time(xe[5]), xe[5].elapsed_time(xe[6])
+            exact_svd = {"batch": Bx, "exact_ms_per_matrix": round(x_ms / Bx, 3),
+                         "rsvd_ms_per_matrix": round(rs_ms / Bx, 3), "speedup": round(x_ms / rs_ms, 2),
+                         "note": "exact top-r SVD (sketch as wide as the short side, k = %d, no power iteration) against "
+                                 "the randomized update (k = %d, q = %d) on the same %d matrices" % (s, k, q, Bx)}
+            del xws
+        else:
+            exact_svd = None
+
+        # the whole Llama-7B-shaped model on this GPU: 128 square (q, k, v, o),
+        # 64 gate/up (the batch above) and 32 down matrices; a subspace update of
+        # all 224 with q = 1 and with q = 2, and one projected Adam step over all
+        whole_model = None
+        if args.whole_model and (m, n, B, S) == (4096, 11008, 64, 1):
+            groups = [{"name": "q,k,v,o 4096x4096", "m": 4096, "n": 4096, "count": 128, "seed": 5100},
+                      {"name": "down 11008x4096", "m": 11008, "n": 4096, "count": 32, "seed": 5200}]
+            for gr in groups:
+                gm, gn, gc = gr["m"], gr["n"], gr["count"]
+                gs, gl_ = min(gm, gn), max(gm, gn)
+                print("bench: generating %d x %dx%d %s gradients" % (gc, gm, gn, args.dtype), file=sys.stderr, flush=True)
+                gr["G"] = gi.torch_planted_group(gm, gn, gc, gi.spectrum_power(gs, 0.7), 1e-4, seed=gr["seed"],
+                                                 dtype=args.dtype)
+                gr["W"] = torch.zeros((gc, gm, gn), dtype=torch.float32, device=dev)
+                gr["P"] = torch.empty((gc, gs, r), dtype=torch.float32, device=dev)
+                gr["sigma"] = torch.empty((gc, r), dtype=torch.float32, device=dev)
+                gr["info"] = torch.empty((gc,), dtype=torch.int32, device=dev)
+                gr["R"] = torch.empty((gc, r, gl_), dtype=torch.float32, device=dev)
+                gr["M"] = torch.zeros_like(gr["R"])
+                gr["V"] = torch.zeros_like(gr["R"])
+                gr["ws"] = torch.empty((gl.galore_rsvd_workspace_size(gm, gn, r, p, gc, G.dtype),), dtype=torch.uint8,
+                                       device=dev)
+                pw = gl.galore_project_workspace_size(gm, gn, r, gc, G.dtype)
+                gr["pws"] = torch.empty((pw,), dtype=torch.uint8, device=dev) if pw > 0 else False
+                gr["bws"] = torch.empty((gl.galore_project_back_workspace_size(gm, gn, r, gc),), dtype=torch.uint8,
+                                        device=dev)
+            groups.insert(1, {"name": "gate/up 4096x11008", "m": m, "n": n, "count": B, "G": G, "W": W, "P": P,
+                              "sigma": sigma, "info": info, "R": R, "M": M, "V": V, "ws": chunks[0]["ws"],
+                              "pws": chunks[0]["pws"], "bws": chunks[0]["bws"]})
+            torch.cuda.synchronize()
+            wm_ms = {}
+            for qq in (1, 2):
+                e0, e1 = mk(), mk()
+                e0.record(stream)
+                for gr in groups:
+                    gl.galore_rsvd_update(gr["G"], r, p, qq, gi.sketch_seed(qq), 0, P=gr["P"], sigma=gr["sigma"],
+                                          info=gr["info"], workspace=gr["ws"], stream=stream, aux_stream=aux0)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                wm_ms["update_q%d" % qq] = e0.elapsed_time(e1)
+                if any(int((gr["info"] != 0).sum()) for gr in groups):
+                    raise RuntimeError("small SVD did not converge in the whole-model update")
             e0, e1 = mk(), mk()
             e0.record(stream)
             for gr in groups:
-                gl.galore_rsvd_update(gr["G"], r, p, qq, gi.sketch_seed(qq), 0, P=gr["P"], sigma=gr["sigma"],
-                                      info=gr["info"], workspace=gr["ws"], stream=stream, aux_stream=aux0)
+                gl.galore_project(gr["P"], gr["G"], R=gr["R"], workspace=gr["pws"], stream=stream)
+                gl.galore_lowrank_adam_step(gr["R"], gr["M"], gr["V"], gr["R"], 0.9, 0.999, 1e-8, 1, stream=stream)
+                gl.galore_project_back(gr["P"], gr["R"], gr["W"], 1e-3, 0.25, workspace=gr["bws"], stream=stream)
             e1.record(stream)
             torch.cuda.synchronize()
-            wm_ms["update_q%d" % qq] = e0.elapsed_time(e1)
-            if any(int((gr["info"] != 0).sum()) for gr in groups):
-                raise RuntimeError("small SVD did not converge in the whole-model update")
-        e0, e1 = mk(), mk()
-        e0.record(stream)
-        for gr in groups:
-            gl.galore_project(gr["P"], gr["G"], R=gr["R"], workspace=gr["pws"], stream=stream)
-            gl.galore_lowrank_adam_step(gr["R"], gr["M"], gr["V"], gr["R"], 0.9, 0.999, 1e-8, 1, stream=stream)
-            gl.galore_project_back(gr["P"], gr["R"], gr["W"], 1e-3, 0.25, workspace=gr["bws"], stream=stream)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        wm_ms["adam_step"] = e0.elapsed_time(e1)
-        nmat = sum(gr["count"] for gr in groups)
-        whole_model = {"matrices": nmat,
-                       "update_q1_ms": round(wm_ms["update_q1"], 1), "update_q2_ms": round(wm_ms["update_q2"], 1),
-                       "projected_adam_step_ms": round(wm_ms["adam_step"], 1),
-                       "note": "Llama-7B-shaped model, all %d projection matrices on this GPU (128 x 4096x4096, "
-                               "64 x 4096x11008, 32 x 11008x4096, %s, r=%d p=%d): one subspace update of every "
-                               "matrix with q = 1 and with q = 2, and one projected Adam step (projection, Adam, "
-                               "weight update) over all" % (nmat, args.dtype, r, p)}
-        for gr in groups:
-            if gr["name"].startswith("gate"):
-                continue
-            for key in ("G", "W", "P", "R", "M", "V", "ws", "pws", "bws"):
-                gr[key] = None
-        torch.cuda.empty_cache()
+            wm_ms["adam_step"] = e0.elapsed_time(e1)
+            nmat = sum(gr["count"] for gr in groups)
+            whole_model = {"matrices": nmat,
+                           "update_q1_ms": round(wm_ms["update_q1"], 1), "update_q2_ms": round(wm_ms["update_q2"], 1),
+                           "projected_adam_step_ms": round(wm_ms["adam_step"], 1),
+                           "note": "Llama-7B-shaped model, all %d projection matrices on this GPU (128 x 4096x4096, "
+                                   "64 x 4096x11008, 32 x 11008x4096, %s, r=%d p=%d): one subspace update of every "
+                                   "matrix with q = 1 and with q = 2, and one projected Adam step (projection, Adam, "
+                                   "weight update) over all" % (nmat, args.dtype, r, p)}
+            for gr in groups:
+                if gr["name"].startswith("gate"):
+                    continue
+                for key in ("G", "W", "P", "R", "M", "V", "ws", "pws", "bws"):
+                    gr[key] = None
+            torch.cuda.empty_cache()
 
-    # 8-bit moments (E4M3 / E5M2 codes, one scale per 2048-element block)
-    st8 = gl.Adam8State(r, l, B, device=dev)
-    a8 = [mk() for _ in range(4)]
-    for j in range(2):
-        a8[2 * j].record(stream)
-        gl.galore_lowrank_adam8_step(R, st8, N=N, beta1=0.9, beta2=0.999, eps=1e-8, t=j + 1, stream=stream)
-        a8[2 * j + 1].record(stream)
-    torch.cuda.synchronize()
-    adam8_ms = a8[2].elapsed_time(a8[3])
-    adam8 = {"ms": round(adam8_ms, 3), "hbm_gbs": round(12.0 * B * r * l / (adam8_ms * 1e-3) / 1e9, 1),
-             "state_bytes": int(2 * (st8.M8.numel() + 4 * st8.Ms.numel())),
-             "note": "8-bit block-wise Adam on the whole batch: 12 bytes per element (R, N fp32; M, V one byte each "
-                     "in and out); fp32 moments take %d bytes" % (8 * B * r * l)}
-    del st8
+        # 8-bit moments (E4M3 / E5M2 codes, one scale per 2048-element block)
+        st8 = gl.Adam8State(r, l, B, device=dev)
+        a8 = [mk() for _ in range(4)]
+        for j in range(2):
+            a8[2 * j].record(stream)
+            gl.galore_lowrank_adam8_step(R, st8, N=N, beta1=0.9, beta2=0.999, eps=1e-8, t=j + 1, stream=stream)
+            a8[2 * j + 1].record(stream)
+        torch.cuda.synchronize()
+        adam8_ms = a8[2].elapsed_time(a8[3])
+        adam8 = {"ms": round(adam8_ms, 3), "hbm_gbs": round(12.0 * B * r * l / (adam8_ms * 1e-3) / 1e9, 1),
+                 "state_bytes": int(2 * (st8.M8.numel() + 4 * st8.Ms.numel())),
+                 "note": "8-bit block-wise Adam on the whole batch: 12 bytes per element (R, N fp32; M, V one byte each "
+                         "in and out); fp32 moments take %d bytes" % (8 * B * r * l)}
+        del st8
 
     out = {
         "metric": "rSVD subspace updates/sec at 4096x11008 r=1024; low-rank Adam step HBM GB/s",
@@ -661,20 +668,22 @@ def main():
         "rsvd_stage_ms": {st: round(v, 3) for st, v in sorted(sub.items(), key=lambda x: -x[1])},
         "kernel_rates": rates,
         "roofline": roof,
-        "schedule": {"T": T_sched, "update_step_ms": round(upd_ms, 3), "plain_step_ms": round(plain_ms, 3),
-                     "amortised_step_ms": round((upd_ms + (T_sched - 1) * plain_ms) / T_sched, 3),
-                     "note": "galore_step on the whole batch: the update step (subspace update, switch with "
-                             "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
+        "schedule": None if upd_ms is None else {
+            "T": T_sched, "update_step_ms": round(upd_ms, 3), "plain_step_ms": round(plain_ms, 3),
+            "amortised_step_ms": round((upd_ms + (T_sched - 1) * plain_ms) / T_sched, 3),
+            "note": "galore_step on the whole batch: the update step (subspace update, switch with "
+                    "re-expression, projection, Adam, back-projection) and the mean of the next nine"},
         "measured_peaks": measured_peaks,
         "whole_model": whole_model,
         "adam8": adam8,
         "exact_svd": exact_svd,
         "lowbit_projector": dict(lowbit, note="steps on a fixed projector with its int8 / int4 codes (whole batch): "
                                                "projection, Adam, back-projection; fp32 projector bytes %d"
-                                               % (4 * B * s * r)),
-        "switch_ms": round(switch_ms, 3),
-        "switch_note": ("subspace switch of the whole batch (sign alignment + first-moment re-expression), "
-                        "once per T steps: %.4f ms per step at T=200" % (switch_ms / 200.0)),
+                                               % (4 * B * s * r)) if lowbit else None,
+        "switch_ms": None if switch_ms is None else round(switch_ms, 3),
+        "switch_note": None if switch_ms is None else (
+            "subspace switch of the whole batch (sign alignment + first-moment re-expression), "
+            "once per T steps: %.4f ms per step at T=200" % (switch_ms / 200.0)),
     }
     del G, W, R, M, V, N, chunks
     torch.cuda.empty_cache()

@@ -32,9 +32,8 @@
 // row-major upper triangle left by the Cholesky (the lower triangle holds
 // stale data and is masked); T is stored as T^T; S and G are full symmetric;
 // E is stored transposed (Et[j][i] = E_ij).
-// The products run on the fp64 matrix cores (v_mfma_f64_16x16x4f64), 64 x 64
-// output tiles, four waves of 32 x 32, operands loaded straight into registers
-// as pairs along the contraction index.
+// The products run on the fp64 matrix cores (v_mfma_f64_16x16x4f64) in 96 x 96
+// output tiles staged through LDS (below).
 #include <float.h>
 
 #include "common.hpp"
@@ -42,31 +41,71 @@
 namespace galore {
 namespace {
 
-constexpr int RT = 64;      // output tile
 constexpr double kEmax = 0.1;
 
 typedef double f64x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// (M[row * ld + t], M[row * ld + t + 1]) in fp64, zero outside row < nr, t < nt
+// ---- 96 x 96 tiles through LDS ------------------------------------------------
+// A workgroup of four waves computes a 96 x 96 output tile (wave (wm, wn): rows
+// 48 wm .. + 47, columns 48 wn .. + 47, as 3 x 3 blocks of 16 x 16 on the fp64
+// matrix cores). Per 32-deep chunk of the contraction both operands are staged
+// in LDS as [t][m] / [t][n] (fp64, rows of 112 doubles: the four 16-lane
+// groups of an operand read fall on two disjoint halves of the 64 banks), the
+// next chunk is loaded into registers while the current one is multiplied.
+// 96 divides the sketch width 1056 of the 4096 x 11008 workload.
+constexpr int QT = 96;              // output tile
+constexpr int QK = 32;              // contraction chunk
+constexpr int QP = 112;             // LDS row pitch (doubles)
+
+// chunk item e (0..2) of thread tid: 96 rows x 8 groups of 4 contraction indices
+__device__ __forceinline__ void q_item(int tid, int e, int& row, int& tq) {
+    const int q = tid + 256 * e;
+    tq = q / QT;
+    row = q - tq * QT;
+}
+
+// 4 consecutive values M[row * ld + t .. t + 3] in fp64, zero outside row < nr, t < nt
 template <typename T>
-__device__ __forceinline__ f64x2 pair_at(const T* M, int64_t ld, int row, int t, int nr, int nt, bool vec) {
-    f64x2 p = {0.0, 0.0};
+__device__ __forceinline__ f64x4 quad_at(const T* M, int64_t ld, int row, int t, int nr, int nt, bool vec) {
+    f64x4 p = {0.0, 0.0, 0.0, 0.0};
     if (row < nr) {
         const T* q = M + static_cast<int64_t>(row) * ld + t;
-        if (vec && t + 1 < nt) {
+        if (vec && t + 3 < nt) {
             if constexpr (sizeof(T) == 8) {
-                p = *reinterpret_cast<const f64x2*>(q);
+                const f64x2 a = *reinterpret_cast<const f64x2*>(q), b = *reinterpret_cast<const f64x2*>(q + 2);
+                p = f64x4{a[0], a[1], b[0], b[1]};
             } else {
-                const f32x2 f = *reinterpret_cast<const f32x2*>(q);
-                p = f64x2{static_cast<double>(f[0]), static_cast<double>(f[1])};
+                const f32x4 f = *reinterpret_cast<const f32x4*>(q);
+                p = f64x4{f[0], f[1], f[2], f[3]};
             }
         } else {
-            if (t < nt) p[0] = static_cast<double>(q[0]);
-            if (t + 1 < nt) p[1] = static_cast<double>(q[1]);
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (t + v < nt) p[v] = static_cast<double>(q[v]);
         }
     }
     return p;
+}
+
+// acc[x][y] += sum over the chunk in LDS (As[t][m], Bs[t][n])
+__device__ __forceinline__ void q_mma(const double* As, const double* Bs, f64x4 acc[3][3], int wm, int wn, int lane) {
+    const int l16 = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int s = 0; s < QK / 4; ++s) {
+        const int t = 4 * s + g;
+        double a[3], b[3];
+#pragma unroll
+        for (int x = 0; x < 3; ++x) {
+            a[x] = As[t * QP + 48 * wm + 16 * x + l16];
+            b[x] = Bs[t * QP + 48 * wn + 16 * x + l16];
+        }
+#pragma unroll
+        for (int x = 0; x < 3; ++x)
+#pragma unroll
+            for (int y = 0; y < 3; ++y)
+                acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b[y], acc[x][y], 0, 0, 0);
+    }
 }
 
 // C[m][n] = sum_{t < kc} A[m][t] B[n][t] for m, n < nn (both operands row-major
@@ -81,7 +120,7 @@ __global__ __launch_bounds__(256) void refine_nt_kernel(const TA* Ab, int64_t st
                                                         int64_t ldc, const int* flags) {
     const int b = blockIdx.y;
     if (flags[b] == 0) return;
-    const int nt = (nn + RT - 1) / RT;
+    const int nt = (nn + QT - 1) / QT;
     int tm, tn;
     if (SYM) {
         int idx = blockIdx.x, u = 0;
@@ -95,66 +134,69 @@ __global__ __launch_bounds__(256) void refine_nt_kernel(const TA* Ab, int64_t st
         tm = blockIdx.x / nt;
         tn = blockIdx.x % nt;
     }
+    __shared__ __attribute__((aligned(16))) double As[QK * QP];
+    __shared__ __attribute__((aligned(16))) double Bs[QK * QP];
     const TA* A = Ab + static_cast<int64_t>(b) * strideA;
     const TB* B = Bb + static_cast<int64_t>(b) * strideB;
     double* C = Cb + static_cast<int64_t>(b) * strideC;
-    const int m0 = RT * tm, n0 = RT * tn;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m0 = QT * tm, n0 = QT * tn;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int l16 = lane & 15, g = lane >> 4;
-    const bool vec = (ld & 1) == 0;
-    // B[n][t] = 0 for t < n: the tile needs t >= n0 only
+    const bool vec = (ld & 3) == 0;
+    // B[n][t] = 0 for t < n: the tile needs t >= n0 only (a multiple of 4)
     const int tlo = TRI ? n0 : 0;
-    int ra[2], rb[2];
+    f64x4 ra[3], rb[3];
+    auto fetch = [&](int t0) {
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-        ra[x] = m0 + 32 * wm + 16 * x + l16;
-        rb[x] = n0 + 32 * wn + 16 * x + l16;
-    }
-    f64x4 acc[2][2];
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
-    auto load = [&](int t0, f64x2* a, f64x2* bv) {
-        const int t = t0 + 2 * g;
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-            a[x] = pair_at(A, ld, ra[x], t, nn, kc, vec);
-            f64x2 q = pair_at(B, ld, rb[x], t, nn, kc, vec);
+        for (int e = 0; e < 3; ++e) {
+            int row, tq;
+            q_item(tid, e, row, tq);
+            const int t = t0 + 4 * tq;
+            ra[e] = quad_at(A, ld, m0 + row, t, nn, kc, vec);
+            f64x4 q = quad_at(B, ld, n0 + row, t, nn, kc, vec);
             if (TRI) {
-                if (t < rb[x]) q[0] = 0.0;
-                if (t + 1 < rb[x]) q[1] = 0.0;
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    if (t + v < n0 + row) q[v] = 0.0;
             }
-            bv[x] = q;
+            rb[e] = q;
         }
     };
-    f64x2 a[2], bv[2], an[2] = {}, bn[2] = {};
-    load(tlo, a, bv);
-    for (int t0 = tlo; t0 < kc; t0 += 8) {
-        if (t0 + 8 < kc) load(t0 + 8, an, bn);
+    auto stash = [&]() {
 #pragma unroll
-        for (int e = 0; e < 2; ++e)
-#pragma unroll
-            for (int x = 0; x < 2; ++x)
-#pragma unroll
-                for (int y = 0; y < 2; ++y)
-                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x][e], bv[y][e], acc[x][y], 0, 0, 0);
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-            a[x] = an[x];
-            bv[x] = bn[x];
-        }
-    }
-    // accumulator register v of block (x, y): row 32 wm + 16 x + 4 v + g, column 32 wn + 16 y + l16
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y)
+        for (int e = 0; e < 3; ++e) {
+            int row, tq;
+            q_item(tid, e, row, tq);
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int row = m0 + 32 * wm + 16 * x + 4 * v + g;
-                const int col = n0 + 32 * wn + 16 * y + l16;
+                As[(4 * tq + v) * QP + row] = ra[e][v];
+                Bs[(4 * tq + v) * QP + row] = rb[e][v];
+            }
+        }
+    };
+    f64x4 acc[3][3];
+#pragma unroll
+    for (int x = 0; x < 3; ++x)
+#pragma unroll
+        for (int y = 0; y < 3; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+    fetch(tlo);
+    for (int t0 = tlo; t0 < kc; t0 += QK) {
+        stash();
+        __syncthreads();
+        if (t0 + QK < kc) fetch(t0 + QK);
+        q_mma(As, Bs, acc, wm, wn, lane);
+        __syncthreads();
+    }
+    // accumulator register v of block (x, y): row 48 wm + 16 x + 4 v + g, column 48 wn + 16 y + l16
+    const int l16 = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int x = 0; x < 3; ++x)
+#pragma unroll
+        for (int y = 0; y < 3; ++y)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = m0 + 48 * wm + 16 * x + 4 * v + g;
+                const int col = n0 + 48 * wn + 16 * y + l16;
                 if (row < nn && col < nn) {
                     C[static_cast<int64_t>(row) * ldc + col] = acc[x][y][v];
                     if (SYM && tm != tn) C[static_cast<int64_t>(col) * ldc + row] = acc[x][y][v];
@@ -203,7 +245,8 @@ __global__ __launch_bounds__(256) void refine_e_kernel(const double* Sb, const d
 // Xn[j][a] = X[j][a] + alpha sum_{i < nn} (M[j][i] - shift delta_ji) X[i][a] for
 // j < nn, a < kc: rows of X are vectors (row pitch ld), M is nn x nn fp64 (row
 // pitch ldm). With Ur != nullptr the result is written transposed,
-// Ur[a][j] (row pitch ldu), instead of into Xn.
+// Ur[a][j] (row pitch ldu), instead of into Xn. 96 x 96 tiles as above: A = M
+// (contraction index contiguous), B = X (rows of the contraction index).
 __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, int64_t strideM, int64_t ldm,
                                                             const float* Xb, int64_t strideX, float* Xnb, int nn,
                                                             int kc, int64_t ld, double alpha, double shift,
@@ -211,68 +254,70 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
                                                             const int* flags) {
     const int b = blockIdx.y;
     if (flags[b] == 0) return;
-    const int ntm = (nn + RT - 1) / RT, ntn = (kc + RT - 1) / RT;
+    const int ntm = (nn + QT - 1) / QT, ntn = (kc + QT - 1) / QT;
     const int tm = blockIdx.x / ntn, tn = blockIdx.x % ntn;
     if (tm >= ntm) return;
+    __shared__ __attribute__((aligned(16))) double As[QK * QP];
+    __shared__ __attribute__((aligned(16))) double Bs[QK * QP];
     const double* M = Mb + static_cast<int64_t>(b) * strideM;
     const float* X = Xb + static_cast<int64_t>(b) * strideX;
-    const int m0 = RT * tm, n0 = RT * tn;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int m0 = QT * tm, n0 = QT * tn;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
-    const int l16 = lane & 15, g = lane >> 4;
-    const bool vec = (ldm & 1) == 0;
-    int ra[2], cb[2];
+    const bool vecm = (ldm & 3) == 0, vecx = (ld & 3) == 0;
+    f64x4 ra[3], rb[3];
+    // B items: 32 contraction rows x 24 groups of 4 columns
+    auto fetch = [&](int t0) {
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-        ra[x] = m0 + 32 * wm + 16 * x + l16;
-        cb[x] = n0 + 32 * wn + 16 * x + l16;
-    }
-    f64x4 acc[2][2];
+        for (int e = 0; e < 3; ++e) {
+            int row, tq;
+            q_item(tid, e, row, tq);
+            const int t = t0 + 4 * tq;
+            f64x4 p = quad_at(M, ldm, m0 + row, t, nn, nn, vecm);
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
-    auto load = [&](int t0, f64x2* a, f64x2* bv) {
-        const int t = t0 + 2 * g;
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-            f64x2 p = pair_at(M, ldm, ra[x], t, nn, nn, vec);
-            if (t == ra[x]) p[0] -= shift;
-            if (t + 1 == ra[x]) p[1] -= shift;
-            a[x] = p;
-            f64x2 q = {0.0, 0.0};
-            if (cb[x] < kc) {
-                if (t < nn) q[0] = static_cast<double>(X[static_cast<int64_t>(t) * ld + cb[x]]);
-                if (t + 1 < nn) q[1] = static_cast<double>(X[static_cast<int64_t>(t + 1) * ld + cb[x]]);
-            }
-            bv[x] = q;
+            for (int v = 0; v < 4; ++v)
+                if (t + v == m0 + row) p[v] -= shift;
+            ra[e] = p;
+            const int q = tid + 256 * e;
+            const int bt = q / (QT / 4), bg = q - bt * (QT / 4);
+            rb[e] = quad_at(X, ld, t0 + bt, n0 + 4 * bg, nn, kc, vecx);
         }
     };
-    f64x2 a[2], bv[2], an[2] = {}, bn[2] = {};
-    load(0, a, bv);
-    for (int t0 = 0; t0 < nn; t0 += 8) {
-        if (t0 + 8 < nn) load(t0 + 8, an, bn);
+    auto stash = [&]() {
 #pragma unroll
-        for (int e = 0; e < 2; ++e)
+        for (int e = 0; e < 3; ++e) {
+            int row, tq;
+            q_item(tid, e, row, tq);
 #pragma unroll
-            for (int x = 0; x < 2; ++x)
-#pragma unroll
-                for (int y = 0; y < 2; ++y)
-                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x][e], bv[y][e], acc[x][y], 0, 0, 0);
-#pragma unroll
-        for (int x = 0; x < 2; ++x) {
-            a[x] = an[x];
-            bv[x] = bn[x];
+            for (int v = 0; v < 4; ++v) As[(4 * tq + v) * QP + row] = ra[e][v];
+            const int q = tid + 256 * e;
+            const int bt = q / (QT / 4), bg = q - bt * (QT / 4);
+            *reinterpret_cast<f64x2*>(&Bs[bt * QP + 4 * bg]) = f64x2{rb[e][0], rb[e][1]};
+            *reinterpret_cast<f64x2*>(&Bs[bt * QP + 4 * bg + 2]) = f64x2{rb[e][2], rb[e][3]};
         }
+    };
+    f64x4 acc[3][3];
+#pragma unroll
+    for (int x = 0; x < 3; ++x)
+#pragma unroll
+        for (int y = 0; y < 3; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+    fetch(0);
+    for (int t0 = 0; t0 < nn; t0 += QK) {
+        stash();
+        __syncthreads();
+        if (t0 + QK < nn) fetch(t0 + QK);
+        q_mma(As, Bs, acc, wm, wn, lane);
+        __syncthreads();
     }
+    const int l16 = lane & 15, g = lane >> 4;
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 3; ++x)
 #pragma unroll
-        for (int y = 0; y < 2; ++y)
+        for (int y = 0; y < 3; ++y)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int row = m0 + 32 * wm + 16 * x + 4 * v + g;
-                const int col = n0 + 32 * wn + 16 * y + l16;
+                const int row = m0 + 48 * wm + 16 * x + 4 * v + g;
+                const int col = n0 + 48 * wn + 16 * y + l16;
                 if (row < nn && col < kc) {
                     const int64_t o = static_cast<int64_t>(row) * ld + col;
                     const float val = static_cast<float>(static_cast<double>(X[o]) + alpha * acc[x][y][v]);
@@ -326,7 +371,7 @@ hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb,
                          double* S, double* G, int64_t strideKK, double* lam, int k, int r, float* Ur,
                          int64_t strideUr, float* sigma, int64_t stride_sigma, const int* flags, int batch,
                          hipStream_t stream) {
-    const int nt = (k + RT - 1) / RT, ntr = (r + RT - 1) / RT;
+    const int nt = (k + QT - 1) / QT, ntr = (r + QT - 1) / QT;
     const dim3 full(nt * nt, batch), upper(nt * (nt + 1) / 2, batch);
     // one step: T^T = X^T R^T (C[c][a] = sum_t Xa[c][t] R[a][t], R upper triangular)
     hipLaunchKernelGGL((refine_nt_kernel<float, double, true, false>), full, dim3(256), 0, stream, Xa, strideX, R,
