@@ -119,22 +119,25 @@ hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, in
                               int max_sweeps, double tol, int batch, hipStream_t stream);
 // scratch: at least 2 k + r doubles per matrix at stride strideScratch (doubles);
 // exps: the per-matrix exponents launch_jacobi_prepare wrote (sigma = 2^-e |y|);
-// Xa (optional, k x k fp32 per matrix at strideX): all k ordered unit columns
-// (column j contiguous) for launch_refine, flags[b] = 1 when matrix b has them
-// (every column norm finite and positive), else 0
+// norms (k fp64) and perm (k int) per matrix: scratch for the column norms and
+// their order; Xa (optional, k x k fp32 per matrix at strideX, with flags):
+// all k ordered unit columns (column j contiguous) for launch_refine, flags[b] =
+// 1 when matrix b has them (every column norm finite and positive; Ur is then
+// left to launch_refine), else 0
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
                                   float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
-                                  double* scratch, int64_t strideScratch, const int* exps, float* Xa, int* flags,
-                                  int batch, hipStream_t stream);
+                                  double* scratch, int64_t strideScratch, const int* exps, double* norms, int* perm,
+                                  float* Xa, int* flags, int batch, hipStream_t stream);
 // fp64 refinement of the small SVD's vectors (refine.hip): one Ogita-Aishima
 // step on H = R^T R (R: the row-major upper triangle of the fp64 Cholesky
 // factor) from the vectors in the rows of Xa, then the r refined vectors of
 // largest Rayleigh quotient re-orthonormalised among themselves and written as
 // the columns of Ur (k x r) with sigma = sqrt(lambda). Xa, Xb: fp32 k x k
-// (scratch afterwards); T, S, G: fp64 k x k scratch at strideKK; lam: k doubles
-// per matrix. Only the matrices whose flag is set are touched.
+// (scratch afterwards); T, S, G: fp64 k x k scratch at strideKK; lam (k doubles)
+// and perm (k int) per matrix: scratch. Only the matrices whose flag is set are
+// touched.
 hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb, int64_t strideX, double* T,
-                         double* S, double* G, int64_t strideKK, double* lam, int k, int r, float* Ur,
+                         double* S, double* G, int64_t strideKK, double* lam, int* perm, int k, int r, float* Ur,
                          int64_t strideUr, float* sigma, int64_t stride_sigma, const int* flags, int batch,
                          hipStream_t stream);
 // Subspace switch: negate the columns of P_new whose overlap with the same

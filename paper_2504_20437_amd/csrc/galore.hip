@@ -60,7 +60,7 @@ bool digits_fit(const Shape& sh) {
 struct Layout {
     int64_t strideL, strideS, strideKK, strideUr;
     size_t offL1, offL2, offS1, offS2, offC, offXinv, offRinv, offYt, offUr, offDef, offDiag0, offRot,
-        offJexp, offTheta, offXb, offS, offGg, offLam, offFlags;
+        offJexp, offTheta, offXb, offS, offGg, offLam, offFlags, offNorm, offPerm;
     int64_t strideTheta;
     // bf16-stored gradients only: transposed copy of G (n x ldgt) and three
     // bf16 planes of the split fp32 operand (k x ldpl each)
@@ -111,6 +111,8 @@ Layout make_layout(const Shape& sh, int r, int batch, bool bf16) {
     L.offGg = take(B * L.strideKK * sizeof(double));
     L.offLam = take(B * static_cast<size_t>(k) * sizeof(double));
     L.offFlags = take(B * sizeof(int));
+    L.offNorm = take(B * static_cast<size_t>(k) * sizeof(double));
+    L.offPerm = take(B * static_cast<size_t>(k) * sizeof(int));
     // scratch of the orthonormal completion in the small-SVD finalize: 2k + r doubles
     L.strideTheta = 2 * pad_elems(2 * k + r);
     L.offTheta = take(B * L.strideTheta * sizeof(float));
@@ -535,12 +537,14 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, batch, stream, aux));
     GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
                                       kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
-                                      L.strideTheta / 2, jexp, w.f(L.offRinv), w.i(L.offFlags), batch, stream));
+                                      L.strideTheta / 2, jexp, w.d(L.offNorm), w.i(L.offPerm), w.f(L.offRinv),
+                                      w.i(L.offFlags), batch, stream));
     if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
     // fp64 refinement of the vectors the fp32 sweeps produced
     GALORE_TRACED(tr, GALORE_STAGE_REFINE,
                   launch_refine(w.d(L.offC), L.strideKK, w.f(L.offRinv), w.f(L.offXb), L.strideKK, w.d(L.offXinv),
-                                w.d(L.offS), w.d(L.offGg), L.strideKK, w.d(L.offLam), k, r, Ur, L.strideUr, sigma,
+                                w.d(L.offS), w.d(L.offGg), L.strideKK, w.d(L.offLam), w.i(L.offPerm), k, r, Ur,
+                                L.strideUr, sigma,
                                 stride_sigma, w.i(L.offFlags), batch, stream));
     // a7: P = Q U_B[:, :r], canonical signs
     {

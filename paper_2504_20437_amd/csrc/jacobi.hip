@@ -549,6 +549,36 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
     }
 }
 
+// norms[b][c] = |y_c| in fp64, one wave per column (coalesced over the
+// column's k contiguous entries); grid (ceil(k / 4), batch)
+__global__ __launch_bounds__(256) void jacobi_norms_kernel(const float* Ytb, int k, int64_t strideX,
+                                                           double* normsb) {
+    const int b = blockIdx.y;
+    const int c = 4 * blockIdx.x + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (c >= k) return;
+    const float* y = Ytb + static_cast<int64_t>(b) * strideX + static_cast<int64_t>(c) * k;
+    double s = 0.0;
+    for (int i = lane; i < k; i += 64) s += static_cast<double>(y[i]) * static_cast<double>(y[i]);
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) normsb[static_cast<int64_t>(b) * k + c] = sqrt(s);
+}
+
+// Xa[j][:] = y_perm(j) / sigma_perm(j) (row j of the result contiguous) for the
+// matrices finalize marked refinable; one workgroup per row j; grid (k, batch)
+__global__ __launch_bounds__(256) void jacobi_gather_kernel(const float* Ytb, int k, int64_t strideX,
+                                                            const double* normsb, const int* permb,
+                                                            const int* flags, float* Xab) {
+    const int b = blockIdx.y;
+    if (flags[b] == 0) return;
+    const int j = blockIdx.x;
+    const int c = permb[static_cast<int64_t>(b) * k + j];
+    const double inv = 1.0 / normsb[static_cast<int64_t>(b) * k + c];
+    const float* y = Ytb + static_cast<int64_t>(b) * strideX + static_cast<int64_t>(c) * k;
+    float* x = Xab + static_cast<int64_t>(b) * strideX + static_cast<int64_t>(j) * k;
+    for (int i = threadIdx.x; i < k; i += blockDim.x) x[i] = static_cast<float>(static_cast<double>(y[i]) * inv);
+}
+
 // sigma_j = |y_j| (fp64), order descending (ties by index, NaN last);
 // Ur[:, j] = y_perm(j) / sigma_perm(j) for the r leading columns, zero columns
 // completed orthonormally. scratch: 2 k + r doubles per matrix.
@@ -557,7 +587,8 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
                                                               float* sigma, int64_t stride_sigma,
                                                               const int* rotb, int max_sweeps, int* info,
                                                               double* scratchb, int64_t strideScratch,
-                                                              const int* expb, float* Xab, int* flags) {
+                                                              const int* expb, const double* normsb, int* permb,
+                                                              int* flags) {
     extern __shared__ unsigned char smem[];
     double* sig = reinterpret_cast<double*>(smem);
     int* perm = reinterpret_cast<int*>(sig + k);
@@ -568,12 +599,7 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
     float* Ur = Urb + static_cast<int64_t>(b) * strideUr;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    for (int c = tid; c < k; c += blockDim.x) {
-        double s = 0.0;
-        const float* y = Yt + static_cast<int64_t>(c) * k;
-        for (int i = 0; i < k; ++i) s += static_cast<double>(y[i]) * static_cast<double>(y[i]);
-        sig[c] = sqrt(s);
-    }
+    for (int c = tid; c < k; c += blockDim.x) sig[c] = normsb[static_cast<int64_t>(b) * k + c];
     __syncthreads();
     for (int c = tid; c < k; c += blockDim.x) {
         const double vc = (sig[c] == sig[c]) ? sig[c] : -1.0;
@@ -598,29 +624,23 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
     }
     __syncthreads();
     const int nkeep = nkeep_s;
-    const int64_t total = static_cast<int64_t>(k) * nkeep;
-    for (int64_t pos = tid; pos < total; pos += blockDim.x) {
-        const int i = static_cast<int>(pos / nkeep);
-        const int j = static_cast<int>(pos - static_cast<int64_t>(i) * nkeep);
-        const int c = perm[j];
-        Ur[static_cast<int64_t>(i) * r + j] = static_cast<float>(static_cast<double>(Yt[static_cast<int64_t>(c) * k + i]) / sig[c]);
-    }
-    if (Xab != nullptr) {
-        // all k columns, ordered and normalised (column j of the result
-        // contiguous), for the fp64 refinement; only when every column norm is
-        // finite and positive (rank-deficient and non-finite matrices keep the
-        // vectors above and are not refined)
-        const bool refinable = (nkeep == r) && sig[perm[k - 1]] > 0.0 && sig[perm[0]] <= DBL_MAX;
+    // refinable: every column norm finite and positive; those matrices get all
+    // k ordered columns (jacobi_gather_kernel, from permb) and their Ur from the
+    // fp64 refinement; the others (rank-deficient, non-finite) keep the vectors
+    // written here
+    const bool refinable = flags != nullptr && (nkeep == r) && sig[perm[k - 1]] > 0.0 && sig[perm[0]] <= DBL_MAX;
+    if (flags != nullptr) {
         if (tid == 0) flags[b] = refinable ? 1 : 0;
-        if (refinable) {
-            float* Xa = Xab + static_cast<int64_t>(b) * strideX;
-            const int64_t kk = static_cast<int64_t>(k) * k;
-            for (int64_t pos = tid; pos < kk; pos += blockDim.x) {
-                const int j = static_cast<int>(pos / k);
-                const int i = static_cast<int>(pos - static_cast<int64_t>(j) * k);
-                const int c = perm[j];
-                Xa[pos] = static_cast<float>(static_cast<double>(Yt[static_cast<int64_t>(c) * k + i]) / sig[c]);
-            }
+        for (int j = tid; j < k; j += blockDim.x) permb[static_cast<int64_t>(b) * k + j] = perm[j];
+    }
+    if (!refinable) {
+        const int64_t total = static_cast<int64_t>(k) * nkeep;
+        for (int64_t pos = tid; pos < total; pos += blockDim.x) {
+            const int i = static_cast<int>(pos / nkeep);
+            const int j = static_cast<int>(pos - static_cast<int64_t>(i) * nkeep);
+            const int c = perm[j];
+            Ur[static_cast<int64_t>(i) * r + j] =
+                static_cast<float>(static_cast<double>(Yt[static_cast<int64_t>(c) * k + i]) / sig[c]);
         }
     }
     if (tid == 0 && info != nullptr) {
@@ -730,11 +750,16 @@ hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, in
 
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
                                   float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
-                                  double* scratch, int64_t strideScratch, const int* exps, float* Xa, int* flags,
-                                  int batch, hipStream_t stream) {
+                                  double* scratch, int64_t strideScratch, const int* exps, double* norms,
+                                  int* perm, float* Xa, int* flags, int batch, hipStream_t stream) {
+    hipLaunchKernelGGL(jacobi_norms_kernel, dim3((k + 3) / 4, batch), dim3(256), 0, stream, Yt, k, strideX, norms);
     const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
     hipLaunchKernelGGL(jacobi_finalize_kernel, dim3(batch), dim3(256), shmem, stream, Yt, k, strideX, r, Ur,
-                       strideUr, sigma, stride_sigma, rot, max_sweeps, info, scratch, strideScratch, exps, Xa, flags);
+                       strideUr, sigma, stride_sigma, rot, max_sweeps, info, scratch, strideScratch, exps, norms,
+                       perm, flags);
+    if (Xa != nullptr)
+        hipLaunchKernelGGL(jacobi_gather_kernel, dim3(k, batch), dim3(256), 0, stream, Yt, k, strideX, norms, perm,
+                           flags, Xa);
     return hipGetLastError();
 }
 

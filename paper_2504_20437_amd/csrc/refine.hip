@@ -329,19 +329,16 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
             }
 }
 
-// Order the refined vectors by lambda (descending, ties by index; a NaN last)
-// and copy the r leading ones, in that order, to the rows of Xs (row pitch k),
-// with sigma = sqrt(lambda). grid (batch); dynamic LDS: k doubles + k ints.
-__global__ __launch_bounds__(256) void refine_sort_kernel(const float* Xtb, int64_t strideX, const double* lamb,
-                                                          int k, int r, float* Xsb, float* sigma,
+// Order the refined vectors by lambda (descending, ties by index; a NaN last):
+// permb[b][j] = index of the j-th, sigma_j = sqrt(lambda). grid (batch);
+// dynamic LDS: k doubles.
+__global__ __launch_bounds__(256) void refine_rank_kernel(const double* lamb, int k, int r, int* permb, float* sigma,
                                                           int64_t stride_sigma, const int* flags) {
     const int b = blockIdx.x;
     if (flags[b] == 0) return;
     extern __shared__ unsigned char smem[];
     double* lam = reinterpret_cast<double*>(smem);
-    int* perm = reinterpret_cast<int*>(lam + k);
-    const float* Xt = Xtb + static_cast<int64_t>(b) * strideX;
-    float* Xs = Xsb + static_cast<int64_t>(b) * strideX;
+    int* perm = permb + static_cast<int64_t>(b) * k;
     for (int i = threadIdx.x; i < k; i += blockDim.x) {
         const double v = lamb[static_cast<int64_t>(b) * k + i];
         lam[i] = (v == v) ? v : -DBL_MAX;
@@ -352,23 +349,27 @@ __global__ __launch_bounds__(256) void refine_sort_kernel(const float* Xtb, int6
         int rank = 0;
         for (int c2 = 0; c2 < k; ++c2) rank += (lam[c2] > vc) || (lam[c2] == vc && c2 < c);
         perm[rank] = c;
+        if (sigma != nullptr && rank < r)
+            sigma[static_cast<int64_t>(b) * stride_sigma + rank] = static_cast<float>(sqrt(fmax(vc, 0.0)));
     }
-    __syncthreads();
-    if (sigma != nullptr)
-        for (int j = threadIdx.x; j < r; j += blockDim.x)
-            sigma[static_cast<int64_t>(b) * stride_sigma + j] = static_cast<float>(sqrt(fmax(lam[perm[j]], 0.0)));
-    const int64_t total = static_cast<int64_t>(r) * k;
-    for (int64_t pos = threadIdx.x; pos < total; pos += blockDim.x) {
-        const int j = static_cast<int>(pos / k);
-        const int i = static_cast<int>(pos - static_cast<int64_t>(j) * k);
-        Xs[pos] = Xt[static_cast<int64_t>(perm[j]) * k + i];
-    }
+}
+
+// Xs[j][:] = Xt[perm[j]][:] for the r leading vectors; grid (r, batch)
+__global__ __launch_bounds__(256) void refine_gather_kernel(const float* Xtb, int64_t strideX, const int* permb, int k,
+                                                            float* Xsb, const int* flags) {
+    const int b = blockIdx.y;
+    if (flags[b] == 0) return;
+    const int j = blockIdx.x;
+    const int c = permb[static_cast<int64_t>(b) * k + j];
+    const float* x = Xtb + static_cast<int64_t>(b) * strideX + static_cast<int64_t>(c) * k;
+    float* y = Xsb + static_cast<int64_t>(b) * strideX + static_cast<int64_t>(j) * k;
+    for (int i = threadIdx.x; i < k; i += blockDim.x) y[i] = x[i];
 }
 
 }  // namespace
 
 hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb, int64_t strideX, double* T,
-                         double* S, double* G, int64_t strideKK, double* lam, int k, int r, float* Ur,
+                         double* S, double* G, int64_t strideKK, double* lam, int* perm, int k, int r, float* Ur,
                          int64_t strideUr, float* sigma, int64_t stride_sigma, const int* flags, int batch,
                          hipStream_t stream) {
     const int nt = (k + QT - 1) / QT, ntr = (r + QT - 1) / QT;
@@ -390,9 +391,9 @@ hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb,
                        strideX, Xb, k, k, static_cast<int64_t>(k), 1.0, 0.0, static_cast<float*>(nullptr),
                        static_cast<int64_t>(0), static_cast<int64_t>(0), flags);
     // the r vectors of largest lambda, in order, into the rows of Xa
-    const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
-    hipLaunchKernelGGL(refine_sort_kernel, dim3(batch), dim3(256), shmem, stream, Xb, strideX, lam, k, r, Xa, sigma,
-                       stride_sigma, flags);
+    hipLaunchKernelGGL(refine_rank_kernel, dim3(batch), dim3(256), static_cast<size_t>(k) * sizeof(double), stream,
+                       lam, k, r, perm, sigma, stride_sigma, flags);
+    hipLaunchKernelGGL(refine_gather_kernel, dim3(r, batch), dim3(256), 0, stream, Xb, strideX, perm, k, Xa, flags);
     // their Gram D = X_r^T X_r (into S), then Ur = (X_r (I - (D - I) / 2))^T
     const dim3 upper_r(ntr * (ntr + 1) / 2, batch), full_r(ntr * nt, batch);
     hipLaunchKernelGGL((refine_nt_kernel<float, float, false, true>), upper_r, dim3(256), 0, stream, Xa, strideX, Xa,
