@@ -132,10 +132,15 @@ def parse():
     ap.add_argument("--streams", type=int, default=1,
                     help="split the batch into this many equal chunks, each on its own stream (default "
                          "priority), so that one chunk's latency-bound stages overlap another's products")
-    ap.add_argument("--cpu-baseline", type=int, default=1, help="time the oracle on the host (0/1)")
+    ap.add_argument("--cpu-baseline", type=int, default=1,
+                    help="time the oracle on the host (0: no, 1: one matrix of the workload, 2: also one thread, "
+                         "q = 1 and the other two shapes of the model; minutes of host time)")
     ap.add_argument("--whole-model", type=int, default=1,
                     help="also time a subspace update and a projected Adam step of all 224 Llama-7B-shaped "
                          "matrices (0/1; needs the default 4096x11008 batch of 64 on one stream)")
+    ap.add_argument("--configs", type=int, default=1,
+                    help="also time the smaller workloads of the same family (single 256x688 matrix, the 60M-, "
+                         "350M- and 1B-shaped layer sets) as extra keys (0/1)")
     ap.add_argument("--extras", type=int, default=1,
                     help="also time the schedule, the low-bit projector, the exact SVD and the 8-bit Adam (0/1; 0 "
                          "for short profiling runs)")
@@ -154,44 +159,76 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(args):
-    """The oracle timed on the host on a bounded sample of the workload: one of
-    its matrices (same shape, spectrum and storage, r, p, q), run through the
-    whole path: subspace update, projection, Adam step and weight update."""
-    import numpy as np
-
-    import galore_inputs as gi
-    import oracle
-
-    m, n, r, p, q = args.m, args.n, args.r, args.p, args.q
-    s = min(m, n)
-    G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.7), 1e-4, seed=7000), args.dtype)
-    W = gi.weights(m, n, seed=7001).astype(np.float64)
-    f32 = lambda x: float(np.float32(x))
-    t0 = time.perf_counter()
-    P, sig, _ = oracle.rsvd_update(G.exact, r, p, q, gi.sketch_seed(0))
-    R = oracle.project(P, G.exact)
-    Mz = np.zeros_like(R)
-    _, _, N = oracle.adam(R, Mz, Mz, f32(0.9), f32(0.999), f32(1e-8), 1)
-    oracle.project_back(P, N, W, f32(1e-3), f32(0.25))
-    dt = time.perf_counter() - t0
-    cpu_model = ""
+def _cpu_model() -> str:
+    """The host CPU as /proc/cpuinfo names it, with family/model/stepping, cache
+    and the number of CPUs this process may run on."""
+    fields = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
-                    cpu_model = line.split(":", 1)[1].strip()
-                    break
+                if ":" not in line:
+                    continue
+                key, val = (x.strip() for x in line.split(":", 1))
+                if key in ("model name", "cpu family", "model", "stepping", "cache size") and key not in fields:
+                    fields[key] = val
     except OSError:
         pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count()
+    return "%s (family %s, model %s, stepping %s, cache %s; %s CPUs usable by this process)" % (
+        fields.get("model name", "?"), fields.get("cpu family", "?"), fields.get("model", "?"),
+        fields.get("stepping", "?"), fields.get("cache size", "?"), usable)
+
+
+def _oracle_path(oracle, gi, m, n, r, p, q, dtype, seed):
+    """One matrix through the oracle's whole path; seconds per stage."""
+    import numpy as np
+
+    s = min(m, n)
+    G = gi.store(gi.planted_gradient(m, n, gi.spectrum_power(s, 0.7), 1e-4, seed=seed), dtype)
+    W = gi.weights(m, n, seed=seed + 1).astype(np.float64)
+    f32 = lambda x: float(np.float32(x))
+    t = [time.perf_counter()]
+    P, _, _ = oracle.rsvd_update(G.exact, r, p, q, gi.sketch_seed(0))
+    t.append(time.perf_counter())
+    R = oracle.project(P, G.exact)
+    t.append(time.perf_counter())
+    Mz = np.zeros_like(R)
+    _, _, N = oracle.adam(R, Mz, Mz, f32(0.9), f32(0.999), f32(1e-8), 1)
+    t.append(time.perf_counter())
+    oracle.project_back(P, N, W, f32(1e-3), f32(0.25))
+    t.append(time.perf_counter())
+    d = [b - a for a, b in zip(t, t[1:])]
+    return {"update_s": round(d[0], 3), "project_s": round(d[1], 3), "adam_s": round(d[2], 4),
+            "project_back_s": round(d[3], 3), "total_s": round(sum(d), 3)}
+
+
+def cpu_baseline(args):
+    """The oracle timed on the host on a bounded sample of the workload: one of
+    its matrices (same shape, spectrum and storage, r, p, q), run through the
+    whole path: subspace update, projection, Adam step and weight update, each
+    stage timed. With --cpu-baseline 2 also: the same matrix on one thread,
+    q = 1, and the 4096x4096 and 11008x4096 shapes of the same model (several
+    minutes of host time; not part of the default run)."""
+    import oracle
+
+    import galore_inputs as gi
+
+    m, n, r, p, q = args.m, args.n, args.r, args.p, args.q
+    threads = oracle.num_threads()
+    main = _oracle_path(oracle, gi, m, n, r, p, q, args.dtype, 7000)
+    dt = main["total_s"]
     out = {
         "value": 1.0 / dt,
         "unit": "updates/s",
-        "cores": oracle.num_threads(),
+        "cores": threads,
         "kind": "oracle",
         "sample": "one %dx%d %s matrix of the workload, r=%d p=%d q=%d, whole path (update, projection, "
                   "Adam step, weight update) once: %.1f s" % (m, n, args.dtype, r, p, q, dt),
-        "cpu_model": cpu_model,
+        "stage_s": main,
+        "cpu_model": _cpu_model(),
     }
     if (m, n) == (4096, 11008):
         # every term of the oracle's update and step scales with l = max(m, n) at
@@ -200,6 +237,198 @@ def cpu_baseline(args):
         out["whole_model_estimate_s"] = round(dt * (96 + 128 * 4096.0 / 11008.0), 1)
         out["whole_model_note"] = ("extrapolated from the measured matrix, not run: the 224 Llama-7B-shaped "
                                    "matrices weighted by l")
+    if args.cpu_baseline >= 2:
+        ext = {}
+        print("bench: oracle, q = 1", file=sys.stderr, flush=True)
+        ext["q1_%dthreads" % threads] = _oracle_path(oracle, gi, m, n, r, p, 1, args.dtype, 7000)
+        for (mm, nn) in ((4096, 4096), (11008, 4096)):
+            print("bench: oracle, %dx%d" % (mm, nn), file=sys.stderr, flush=True)
+            ext["%dx%d_%dthreads" % (mm, nn, threads)] = _oracle_path(oracle, gi, mm, nn, r, p, q, args.dtype, 7000)
+        print("bench: oracle, one thread", file=sys.stderr, flush=True)
+        oracle.set_num_threads(1)
+        try:
+            ext["%dx%d_1thread" % (m, n)] = _oracle_path(oracle, gi, m, n, r, p, q, args.dtype, 7000)
+        finally:
+            oracle.set_num_threads(threads)
+        if (m, n) == (4096, 11008):
+            ext["whole_model_s_%dthreads" % threads] = round(
+                64 * dt + 32 * ext["11008x4096_%dthreads" % threads]["total_s"]
+                + 128 * ext["4096x4096_%dthreads" % threads]["total_s"], 1)
+        ext["note"] = ("same spectrum, storage and r, p; whole_model = 64 x 4096x11008 + 32 x 11008x4096 + "
+                       "128 x 4096x4096 of the measured per-matrix times")
+        out["extended"] = ext
+    return out
+
+
+def time_configs(gl, gi, torch, dev):
+    """The other workloads of the family, each on one stream (a second stream
+    of this process for the small SVD's halves) and timed with HIP events
+    around the library's calls only (gradient generation is outside them):
+      single-256x688  one fp32 gradient, 1 subspace update + 1 projected Adam step
+      llama-60m       56 fp32 gradients; 1 update, then 200 projected Adam steps,
+                      each with fresh noise on the same planted singular vectors
+      llama-350m      168 fp32 gradients; 600 steps of the scheduled step with an
+                      update every T = 200 steps (Alg. 1; fixed gradients)
+      llama-1b        168 bf16 gradients; one batched update of all, then one
+                      projected Adam sweep (projection, Adam, weight update)"""
+    st = torch.cuda.current_stream()
+    aux = torch.cuda.Stream()
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    b1, b2, eps, lr, al = 0.9, 0.999, 1e-8, 1e-3, 0.25
+
+    def groups(w, noise):
+        out = []
+        for gidx, (label, m, n, count) in enumerate(w.groups):
+            s, l = min(m, n), max(m, n)
+            G = gi.torch_planted_group(m, n, count, w.spectrum(s), noise, seed=8000 + 17 * gidx, dtype=w.dtype)
+            out.append(dict(label=label, m=m, n=n, count=count, s=s, l=l, G=G,
+                            W=torch.zeros((count, m, n), dtype=torch.float32, device=dev),
+                            P=torch.empty((count, s, w.r), dtype=torch.float32, device=dev),
+                            R=torch.empty((count, w.r, l), dtype=torch.float32, device=dev),
+                            M=torch.zeros((count, w.r, l), dtype=torch.float32, device=dev),
+                            V=torch.zeros((count, w.r, l), dtype=torch.float32, device=dev),
+                            info=torch.zeros((count,), dtype=torch.int32, device=dev)))
+            workspaces(out[-1], w)
+        return out
+
+    def workspaces(g, w):
+        dt = g["G"].dtype
+        g["ws"] = torch.empty((gl.galore_rsvd_workspace_size(g["m"], g["n"], w.r, w.p, g["count"], dt),),
+                              dtype=torch.uint8, device=dev)
+        pw = gl.galore_project_workspace_size(g["m"], g["n"], w.r, g["count"], dt)
+        g["pws"] = torch.empty((pw,), dtype=torch.uint8, device=dev) if pw > 0 else False
+        g["bws"] = torch.empty((gl.galore_project_back_workspace_size(g["m"], g["n"], w.r, g["count"]),),
+                               dtype=torch.uint8, device=dev)
+
+    def update_all(grs, w, idx):
+        for g in grs:
+            gl.galore_rsvd_update(g["G"], w.r, w.p, w.q, gi.sketch_seed(idx), 0, P=g["P"], info=g["info"],
+                                  workspace=g["ws"], stream=st, aux_stream=aux)
+
+    def adam_all(grs, t):
+        for g in grs:
+            gl.galore_project(g["P"], g["G"], R=g["R"], workspace=g["pws"], stream=st)
+            gl.galore_lowrank_adam_step(g["R"], g["M"], g["V"], g["R"], b1, b2, eps, t, stream=st)
+            gl.galore_project_back(g["P"], g["R"], g["W"], lr, al, workspace=g["bws"], stream=st)
+
+    def check(grs):
+        if any(int((g["info"] != 0).sum()) for g in grs):
+            raise RuntimeError("small SVD did not converge")
+
+    def timed(fn):
+        e0, e1 = mk(), mk()
+        e0.record(st)
+        fn()
+        e1.record(st)
+        return e0, e1
+
+    out = {}
+    # single 256 x 688 gradient
+    w = gi.WORKLOADS["single-256x688"]
+    grs = [dict(label="single", m=256, n=688, count=1, s=256, l=688,
+                G=torch.from_numpy(gi.store(gi.planted_gradient(256, 688, w.spectrum(256), w.noise, seed=1000),
+                                            "f32").data).to(dev).unsqueeze(0))]
+    g = grs[0]
+    g.update(W=torch.zeros((1, 256, 688), device=dev), P=torch.empty((1, 256, w.r), device=dev),
+             R=torch.empty((1, w.r, 688), device=dev), M=torch.zeros((1, w.r, 688), device=dev),
+             V=torch.zeros((1, w.r, 688), device=dev), info=torch.zeros((1,), dtype=torch.int32, device=dev))
+    workspaces(g, w)
+    for _ in range(2):       # the second pass is timed
+        u = timed(lambda: update_all(grs, w, 0))
+        a = timed(lambda: adam_all(grs, 1))
+    torch.cuda.synchronize()
+    check(grs)
+    out["single_256x688"] = {"update_ms": round(u[0].elapsed_time(u[1]), 4),
+                             "adam_step_ms": round(a[0].elapsed_time(a[1]), 4),
+                             "note": "one fp32 gradient, r=32 p=8 q=2: one subspace update, then one projected "
+                                     "Adam step (projection, Adam, weight update); launch-bound"}
+    del grs, g
+    # Llama-60M-shaped: 1 update, then 200 steps with fresh noise
+    w = gi.WORKLOADS["llama-60m"]
+    grs = groups(w, 0.0)          # the noiseless planted part; noise drawn per step
+    for g in grs:
+        g["base"] = g["G"].clone()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(8100)
+
+    def fresh():
+        for g in grs:
+            g["G"].copy_(g["base"])
+            g["G"].add_(torch.randn(g["G"].shape, generator=gen, device=dev), alpha=w.noise)
+    fresh()
+    update_all(grs, w, 0)          # warm-up of the shapes
+    torch.cuda.synchronize()
+    fresh()
+    u = timed(lambda: update_all(grs, w, 1))
+    steps = []
+    for t in range(1, 201):
+        fresh()
+        steps.append(timed(lambda: adam_all(grs, t)))
+    torch.cuda.synchronize()
+    check(grs)
+    um = u[0].elapsed_time(u[1])
+    sm = [a.elapsed_time(b) for a, b in steps]
+    n60 = sum(g["count"] for g in grs)
+    out["llama_60m"] = {"matrices": n60, "update_ms": round(um, 3), "updates_per_s": round(n60 / (um * 1e-3), 1),
+                        "adam_step_ms_mean": round(sum(sm) / len(sm), 4), "run_200_steps_ms": round(um + sum(sm), 2),
+                        "note": "56 fp32 gradients (8 layers x q,k,v,o 512x512, gate,up 512x1376, down 1376x512), "
+                                "0.9^i + 1e-4 noise, r=128 p=8 q=2: one subspace update, then 200 projected Adam "
+                                "steps with fresh noise on the same planted singular vectors"}
+    del grs
+    torch.cuda.empty_cache()
+    # Llama-350M-shaped: 600 scheduled steps, update every 200
+    w = gi.WORKLOADS["llama-350m"]
+    grs = groups(w, w.noise)
+    T = 200
+    for g in grs:
+        g["sws"] = torch.empty((gl.galore_step_workspace_size(g["m"], g["n"], w.r, w.p, g["count"], g["G"].dtype, 0),),
+                               dtype=torch.uint8, device=dev)
+
+    def step_all(tau):
+        for g in grs:
+            gl.galore_step(g["G"], g["W"], g["P"], g["M"], g["V"], w.r, w.p, w.q, gi.sketch_seed(tau // T), tau, T,
+                           beta1=b1, beta2=b2, eps=eps, lr=lr, alpha=al, flags=0, info=g["info"], workspace=g["sws"],
+                           stream=st, aux_stream=aux)
+    step_all(0)                    # warm-up of the shapes
+    torch.cuda.synchronize()
+    for g in grs:
+        g["M"].zero_()
+        g["V"].zero_()
+    evs = [timed(lambda tau=tau: step_all(tau)) for tau in range(600)]
+    torch.cuda.synchronize()
+    check(grs)
+    ms = [a.elapsed_time(b) for a, b in evs]
+    upd = [x for tau, x in enumerate(ms) if tau % T == 0]
+    plain = [x for tau, x in enumerate(ms) if tau % T != 0]
+    n350 = sum(g["count"] for g in grs)
+    out["llama_350m"] = {"matrices": n350, "steps": 600, "T": T, "run_ms": round(sum(ms), 2),
+                         "update_step_ms_mean": round(sum(upd) / len(upd), 3),
+                         "plain_step_ms_mean": round(sum(plain) / len(plain), 4),
+                         "note": "168 fp32 gradients (24 layers x q,k,v,o 1024x1024, gate,up 1024x2736, down "
+                                 "2736x1024), (i+1)^-1 + 1e-4 noise, r=256 p=16 q=2: 600 calls of the scheduled "
+                                 "step (Alg. 1: a subspace update when tau mod 200 = 0, projection, Adam and weight "
+                                 "update every step; the same gradients each step)"}
+    del grs, evs
+    torch.cuda.empty_cache()
+    # Llama-1B-shaped: one batched update of all 168, then one sweep
+    w = gi.WORKLOADS["llama-1b"]
+    grs = groups(w, w.noise)
+    update_all(grs, w, 0)          # warm-up of the shapes
+    adam_all(grs, 1)
+    torch.cuda.synchronize()
+    u = timed(lambda: update_all(grs, w, 1))
+    a = timed(lambda: adam_all(grs, 2))
+    torch.cuda.synchronize()
+    check(grs)
+    um, am = u[0].elapsed_time(u[1]), a[0].elapsed_time(a[1])
+    n1b = sum(g["count"] for g in grs)
+    out["llama_1b"] = {"matrices": n1b, "update_ms": round(um, 2), "updates_per_s": round(n1b / (um * 1e-3), 1),
+                       "sweep_ms": round(am, 3),
+                       "note": "168 bf16 gradients (24 layers x q,k,v,o 2048x2048, gate,up 2048x5461, down "
+                               "5461x2048), (i+1)^-0.8 + 1e-4 noise, r=512 p=16 q=2: one subspace update of all, "
+                               "then one projected Adam sweep over all"}
+    del grs
+    torch.cuda.empty_cache()
     return out
 
 
@@ -687,6 +916,9 @@ def main():
     }
     del G, W, R, M, V, N, chunks
     torch.cuda.empty_cache()
+    if args.configs:
+        print("bench: timing the other workloads", file=sys.stderr, flush=True)
+        out["configs"] = time_configs(gl, gi, torch, dev)
     if args.cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(args)

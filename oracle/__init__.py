@@ -68,6 +68,8 @@ def _load():
         i64, i32, u64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_uint64
         lib.orc_num_threads.argtypes = []
         lib.orc_num_threads.restype = ctypes.c_int
+        lib.orc_set_num_threads.argtypes = [ctypes.c_int]
+        lib.orc_set_num_threads.restype = None
         lib.orc_philox4x64_10.argtypes = [_u64p, _u64p, _u64p]
         lib.orc_philox4x64_10.restype = None
         lib.orc_normal_from_words.argtypes = [u64, u64]
@@ -123,6 +125,11 @@ def _ptr(a: np.ndarray):
 def num_threads() -> int:
     """OpenMP threads the oracle's loops run on."""
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the oracle's later OpenMP loops (n > 0)."""
+    _load().orc_set_num_threads(int(n))
 
 
 def philox4x64_10(counter, key) -> np.ndarray:

@@ -28,8 +28,9 @@
 
 #define ORC_API __attribute__((visibility("default")))
 
-/* Threads the OpenMP loops of the oracle use (for reporting only). */
+/* Threads the OpenMP loops of the oracle use (for reporting and timing). */
 ORC_API int orc_num_threads(void) { return omp_get_max_threads(); }
+ORC_API void orc_set_num_threads(int n) { if (n > 0) omp_set_num_threads(n); }
 
 /* ------------------------------------------------------------------------ */
 /* Philox4x64-10 counter-based generator (Salmon, Moraes, Dror, Shaw,        */
