@@ -133,8 +133,8 @@ def parse():
                     help="split the batch into this many equal chunks, each on its own stream (default "
                          "priority), so that one chunk's latency-bound stages overlap another's products")
     ap.add_argument("--cpu-baseline", type=int, default=1,
-                    help="time the oracle on the host (0: no, 1: one matrix of the workload, 2: also one thread, "
-                         "q = 1 and the other two shapes of the model; minutes of host time)")
+                    help="time the oracle on the host (0: no, 1: one matrix of the workload, 2: also q = 1, the "
+                         "other two shapes of the model and one thread on a 2048x5461 matrix; minutes of host time)")
     ap.add_argument("--whole-model", type=int, default=1,
                     help="also time a subspace update and a projected Adam step of all 224 Llama-7B-shaped "
                          "matrices (0/1; needs the default 4096x11008 batch of 64 on one stream)")
@@ -183,7 +183,8 @@ def _cpu_model() -> str:
 
 
 def _oracle_path(oracle, gi, m, n, r, p, q, dtype, seed):
-    """One matrix through the oracle's whole path; seconds per stage."""
+    """One matrix through the oracle's whole path; seconds per stage (each
+    printed to stderr as it ends)."""
     import numpy as np
 
     s = min(m, n)
@@ -191,15 +192,20 @@ def _oracle_path(oracle, gi, m, n, r, p, q, dtype, seed):
     W = gi.weights(m, n, seed=seed + 1).astype(np.float64)
     f32 = lambda x: float(np.float32(x))
     t = [time.perf_counter()]
+
+    def mark(stage):
+        t.append(time.perf_counter())
+        print("bench: oracle %dx%d r=%d q=%d %s: %.2f s" % (m, n, r, q, stage, t[-1] - t[-2]), file=sys.stderr,
+              flush=True)
     P, _, _ = oracle.rsvd_update(G.exact, r, p, q, gi.sketch_seed(0))
-    t.append(time.perf_counter())
+    mark("update")
     R = oracle.project(P, G.exact)
-    t.append(time.perf_counter())
+    mark("projection")
     Mz = np.zeros_like(R)
     _, _, N = oracle.adam(R, Mz, Mz, f32(0.9), f32(0.999), f32(1e-8), 1)
-    t.append(time.perf_counter())
+    mark("Adam")
     oracle.project_back(P, N, W, f32(1e-3), f32(0.25))
-    t.append(time.perf_counter())
+    mark("back-projection")
     d = [b - a for a, b in zip(t, t[1:])]
     return {"update_s": round(d[0], 3), "project_s": round(d[1], 3), "adam_s": round(d[2], 4),
             "project_back_s": round(d[3], 3), "total_s": round(sum(d), 3)}
@@ -210,8 +216,9 @@ def cpu_baseline(args):
     its matrices (same shape, spectrum and storage, r, p, q), run through the
     whole path: subspace update, projection, Adam step and weight update, each
     stage timed. With --cpu-baseline 2 also: the same matrix on one thread,
-    q = 1, and the 4096x4096 and 11008x4096 shapes of the same model (several
-    minutes of host time; not part of the default run)."""
+    q = 1, the 4096x4096 and 11008x4096 shapes of the same model, and a
+    2048x5461 matrix on all threads and on one (a few minutes of host time;
+    not part of the default run)."""
     import oracle
 
     import galore_inputs as gi
@@ -244,12 +251,16 @@ def cpu_baseline(args):
         for (mm, nn) in ((4096, 4096), (11008, 4096)):
             print("bench: oracle, %dx%d" % (mm, nn), file=sys.stderr, flush=True)
             ext["%dx%d_%dthreads" % (mm, nn, threads)] = _oracle_path(oracle, gi, mm, nn, r, p, q, args.dtype, 7000)
-        print("bench: oracle, one thread", file=sys.stderr, flush=True)
-        oracle.set_num_threads(1)
-        try:
-            ext["%dx%d_1thread" % (m, n)] = _oracle_path(oracle, gi, m, n, r, p, q, args.dtype, 7000)
-        finally:
-            oracle.set_num_threads(threads)
+        # one thread on the 1B-shaped gate/up matrix (2048x5461, r=512 p=16: an
+        # eighth of the work of the matrix above), beside the same on all threads
+        for nt in (threads, 1):
+            print("bench: oracle, 2048x5461 on %d thread(s)" % nt, file=sys.stderr, flush=True)
+            oracle.set_num_threads(nt)
+            try:
+                ext["2048x5461_r512_%dthread%s" % (nt, "s" if nt > 1 else "")] = _oracle_path(
+                    oracle, gi, 2048, 5461, 512, 16, q, args.dtype, 7000)
+            finally:
+                oracle.set_num_threads(threads)
         if (m, n) == (4096, 11008):
             ext["whole_model_s_%dthreads" % threads] = round(
                 64 * dt + 32 * ext["11008x4096_%dthreads" % threads]["total_s"]
