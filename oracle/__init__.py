@@ -44,7 +44,10 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "galore_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_DEFAULT_LIB = os.path.join(_HERE, "liboracle.so")
+# GALORE_ORACLE_LIB selects another build of galore_oracle.c (the tests'
+# sanitizer build, see build_sanitized); by default the in-tree liboracle.so
+_LIB_PATH = os.environ.get("GALORE_ORACLE_LIB") or _DEFAULT_LIB
 _lib = None
 
 _f64p = ctypes.POINTER(ctypes.c_double)
@@ -52,12 +55,24 @@ _u64p = ctypes.POINTER(ctypes.c_uint64)
 
 
 def build(force: bool = False) -> str:
-    """Compile the oracle with gcc (plain -O2 + OpenMP)."""
+    """Compile the oracle with gcc (plain -O2 + OpenMP); a build selected by
+    GALORE_ORACLE_LIB is used as it is."""
+    if _LIB_PATH != _DEFAULT_LIB:
+        return _LIB_PATH
     if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
+
+
+def build_sanitized(out_path: str) -> str:
+    """The oracle with AddressSanitizer + UndefinedBehaviorSanitizer (gcc; any
+    finding aborts). Load it with GALORE_ORACLE_LIB=out_path in a process that
+    preloads gcc's libasan."""
+    subprocess.check_call(["gcc", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                           "-fno-sanitize-recover=all", "-fopenmp", "-shared", "-fPIC", "-o", out_path, _SRC, "-lm"])
+    return out_path
 
 
 def _load():

@@ -13,7 +13,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libgalore.so")
+# GALORE_LIB selects another build of the same sources (the tests' host-side
+# sanitizer build); by default the in-tree libgalore.so
+LIB_PATH = os.environ.get("GALORE_LIB") or os.path.join(_HERE, "libgalore.so")
 
 GALORE_F32 = 0
 GALORE_BF16 = 1
@@ -122,8 +124,8 @@ def _declare(lib):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError("libgalore.so is not built (run __graft_entry__.build()); "
-                          "there is no fallback path")
+        raise ImportError("%s is not built (run __graft_entry__.build()); "
+                          "there is no fallback path" % LIB_PATH)
     return _declare(ctypes.CDLL(LIB_PATH))
 
 

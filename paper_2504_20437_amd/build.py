@@ -38,5 +38,20 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized(out_path: str) -> str:
+    """The same sources with AddressSanitizer + UndefinedBehaviorSanitizer on
+    the host code only (argument validation, workspace layout, launch set-up;
+    any finding aborts). Device code is built as usual. Load it with
+    GALORE_LIB=out_path in a process that preloads clang's ASan runtime."""
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    flags = [f for f in HIPCC_FLAGS if f != "-O3"] + ["-O1", "-g"]
+    for f in ("-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer"):
+        flags += ["-Xarch_host", f]
+    res = subprocess.run([hipcc] + flags + ["-o", out_path] + sources(), capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
+    return out_path
+
+
 if __name__ == "__main__":
     print(build(verbose=False))
