@@ -14,17 +14,18 @@
 // tournament pairs the blocks so that every step is a set of disjoint pairs
 // (with an odd number of blocks, the pair with the padding block is not
 // launched). A step is one launch, one workgroup per pair and matrix, which
-//   1. forms the 64 x 64 Gram of its two blocks in fp64 from fp32 matrix-core
-//      partial sums of 8 products (v_mfma_f32_16x16x4f32), row chunks staged
-//      in LDS;
+//   1. forms the 64 x 64 Gram of its two blocks: 32-row chunks split exactly
+//      into three bf16 planes in LDS, six plane products per tile on the bf16
+//      matrix cores (v_mfma_f32_16x16x32_bf16) summed in fp32 per chunk and
+//      in fp64 across chunks;
 //   2. skips the pair if every column pair is already orthogonal to the
 //      tolerance (relative off-diagonal), otherwise
 //   3. reduces the small Gram by one sweep of two-sided Jacobi held in
 //      registers (fp32 entries, fp64 diagonal and angles; odd-even ordering,
 //      64 rounds of up to 32 disjoint rotations, accumulating the rotation
 //      Theta), and
-//   4. applies Theta to the pair's 64 columns of Y on the fp32 matrix cores
-//      (v_mfma_f32_32x32x2f32), 64-row chunks staged through LDS.
+//   4. applies Theta to the pair's 64 columns of Y on the bf16 matrix cores,
+//      Theta and the 32-row chunks of Y split into three planes as in 1.
 // A sweep is nb - 1 steps; the matrix has converged when a whole sweep
 // rotates nothing (rotation counts per sweep live in device memory, so no
 // host synchronisation is needed).
@@ -50,8 +51,6 @@ constexpr int JW = 2 * JB;         // columns per pair (64)
 #endif
 constexpr int kInnerSweeps = GALORE_JAC_INNER;   // inner sweeps of a pair's 64 x 64 Gram per visit
 constexpr int JT = 256;            // threads (4 waves)
-constexpr int GR = 64;             // rows per Gram chunk (two fp32 chunks fill the LDS buffer)
-constexpr int AR = 64;             // rows per apply chunk
 constexpr int PD = JW + 1;         // padded LDS row
 
 static_assert(JW == 64, "the pair kernels assume 64 columns per pair");
@@ -152,6 +151,100 @@ __device__ __forceinline__ float dpp_odd_partner(float v, bool odd) {
     return __int_as_float(odd ? l : r);
 }
 
+// ---- bf16 planes of the pair's columns (Gram and rotation phases) ----------
+// A 32-row chunk of the pair's 64 columns is held in LDS as three bf16 planes
+// (h, m, l with x = h + m + l exactly: each plane takes the leading 8
+// significant bits of what the previous ones left, by truncation, and an fp32
+// significand has 24). Plane p of buffer s starts at s * kChunkBytes +
+// p * kPlaneBytes; column c is 64 bytes (32 rows), its row octet o stored at
+// 16-byte slot o ^ ((c >> 2) & 3), which keeps the 16-byte fragment reads, the
+// transposing reads and the stores free of bank conflicts.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int PC = 32;                         // rows per plane chunk
+constexpr int kPlaneBytes = JW * PC * 2;
+constexpr int kChunkBytes = 3 * kPlaneBytes;
+// plane products kept: h h, h m, m h, m m, h l, l h (the others are below
+// 2^-25 of |a| |b|)
+constexpr int kPlanePairs[6][2] = {{0, 0}, {0, 1}, {1, 0}, {1, 1}, {0, 2}, {2, 0}};
+
+__device__ __forceinline__ void split8(f32x4 a, f32x4 b, bf16x8& h, bf16x8& m, bf16x8& l) {
+    const float x[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    u32x4 ph, pm, pl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const unsigned u0 = __float_as_uint(x[2 * i]), u1 = __float_as_uint(x[2 * i + 1]);
+        const float r0 = x[2 * i] - __uint_as_float(u0 & 0xffff0000u);
+        const float r1 = x[2 * i + 1] - __uint_as_float(u1 & 0xffff0000u);
+        const unsigned v0 = __float_as_uint(r0), v1 = __float_as_uint(r1);
+        const float q0 = r0 - __uint_as_float(v0 & 0xffff0000u);
+        const float q1 = r1 - __uint_as_float(v1 & 0xffff0000u);
+        ph[i] = (u0 >> 16) | (u1 & 0xffff0000u);
+        pm[i] = (v0 >> 16) | (v1 & 0xffff0000u);
+        pl[i] = (__float_as_uint(q0) >> 16) | (__float_as_uint(q1) & 0xffff0000u);
+    }
+    h = __builtin_bit_cast(bf16x8, ph);
+    m = __builtin_bit_cast(bf16x8, pm);
+    l = __builtin_bit_cast(bf16x8, pl);
+}
+
+// thread t loads rows r0 + 8 (t & 3) .. + 7 of pair column t >> 2 (zeros past
+// k and for padding columns)
+__device__ __forceinline__ void pair_fetch(const float* X, int k, const int* col, int tid, int r0, f32x4& a,
+                                           f32x4& b) {
+    const int c = col[tid >> 2];
+    const int rr = r0 + 8 * (tid & 3);
+    const int64_t base = static_cast<int64_t>(c) * k + rr;
+    if (c >= 0 && (k & 3) == 0 && rr + 8 <= k) {
+        a = *reinterpret_cast<const f32x4*>(X + base);
+        b = *reinterpret_cast<const f32x4*>(X + base + 4);
+    } else {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            a[v] = (c >= 0 && rr + v < k) ? X[base + v] : 0.0f;
+            b[v] = (c >= 0 && rr + 4 + v < k) ? X[base + 4 + v] : 0.0f;
+        }
+    }
+}
+
+__device__ __forceinline__ void pair_stash(unsigned char* lds, int s, int tid, f32x4 a, f32x4 b) {
+    bf16x8 h, m, l;
+    split8(a, b, h, m, l);
+    const int c = tid >> 2, o = tid & 3;
+    unsigned char* dst = lds + s * kChunkBytes + c * 64 + 16 * (o ^ ((c >> 2) & 3));
+    *reinterpret_cast<bf16x8*>(dst) = h;
+    *reinterpret_cast<bf16x8*>(dst + kPlaneBytes) = m;
+    *reinterpret_cast<bf16x8*>(dst + 2 * kPlaneBytes) = l;
+}
+
+// Gram operand (A and B alike) of 16-column block blk: lane l holds column
+// 16 blk + (l & 15), rows 8 (l >> 4) .. + 7 of the chunk
+__device__ __forceinline__ bf16x8 gram_frag(const unsigned char* lds, int s, int p, int blk, int lane) {
+    const int c = 16 * blk + (lane & 15), o = lane >> 4;
+    return *reinterpret_cast<const bf16x8*>(lds + s * kChunkBytes + p * kPlaneBytes + c * 64 +
+                                            16 * (o ^ ((c >> 2) & 3)));
+}
+
+// Rotation operand A (rows of Y_P): lane l holds row 16 tm + (l & 15) of the
+// chunk, columns 32 ks + 8 (l >> 4) .. + 7. Two transposing reads: in each
+// group of 16 lanes, lane j receives element j % 4 of the 8 bytes that lane
+// 4 e + j / 4 points at (e = 0..3); lane L points at column w0 + L / 4, rows
+// 16 tm + 4 (L % 4) .. + 3, so lane j gets row 16 tm + j, columns w0 .. w0 + 3.
+__device__ __forceinline__ bf16x8 apply_frag(const unsigned char* lds, int s, int p, int tm, int ks, int lane) {
+    const int L = lane & 15;
+    const int t = 16 * tm + 4 * (L & 3);
+    bf16x4 q[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int w = 32 * ks + 8 * (lane >> 4) + 4 * h + (L >> 2);
+        const int off = s * kChunkBytes + p * kPlaneBytes + w * 64 + 16 * ((t >> 3) ^ ((w >> 2) & 3)) + 2 * (t & 7);
+        q[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(reinterpret_cast<__attribute__((address_space(3))) bf16x4*>(
+            reinterpret_cast<__attribute__((address_space(3))) unsigned char*>(reinterpret_cast<size_t>(lds)) + off));
+    }
+    return __builtin_shufflevector(q[0], q[1], 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // Element type of the inner sweep's Gram and accumulated rotation. fp32: the
 // rotation is applied to fp32 columns on the fp32 matrix cores anyway, the
 // sweep only has to produce an orthogonal Theta that reduces the pair's
@@ -199,90 +292,90 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
     }
     __syncthreads();
 
-    // ---- 1. Gram of the pair's columns: the 10 upper 16 x 16 tiles of the
-    //         64 x 64 result spread over the 4 waves, row chunks of GR rows
-    //         double-buffered in LDS (fp32, as stored) with the next chunk
-    //         prefetched in registers. Products on the fp32 matrix cores, two
-    //         4-term MFMAs per partial sum, each partial sum added into fp64:
-    //         an entry's error stays below about 8 fp32 ulps of
-    //         sum_t |y_tp y_tq| <= |y_p| |y_q|, far under the tolerance the
-    //         test and the rotations work to.
+    unsigned char* lds = reinterpret_cast<unsigned char*>(&G[0][0]);
+    static_assert(2 * kChunkBytes <= JW * PD * static_cast<int>(sizeof(double)), "two plane chunks fit the buffer");
+    f32x4 pre0, pre1;
+
+    // ---- 1. Gram of the pair's columns on the bf16 matrix cores: every
+    //         32-row chunk of the 64 columns is split exactly into three bf16
+    //         planes (x = h + m + l, 8 significant bits each, so the split of
+    //         an fp32 value loses nothing) and staged in LDS, double-buffered,
+    //         the next chunk in flight in registers. A 16 x 16 tile of the Gram
+    //         sums the six plane products h h, h m, m h, m m, h l, l h
+    //         (v_mfma_f32_16x16x32_bf16; the three left out are below 2^-25 of
+    //         |y_p| |y_q|) in fp32 per chunk, each chunk's sum added into fp64.
+    //         Tiles per wave: waves 0 and 1 the three upper tiles of blocks
+    //         {0, 1} and {2, 3}, waves 2 and 3 the tiles (0, 2), (1, 2) and
+    //         (0, 3), (1, 3), so a wave reads the fragments of at most three
+    //         16-column blocks.
     {
-        float (*Xs0)[PD] = reinterpret_cast<float (*)[PD]>(&regB[0][0]);   // rows 0 .. GR-1
-        float (*Xs1)[PD] = Xs0 + GR;                                      // rows GR .. 2GR-1
-        // tiles (ti, tj), ti <= tj, per wave; -1 = none
-        const int tiles[4][3][2] = {{{0, 0}, {0, 1}, {0, 2}}, {{0, 3}, {1, 1}, {1, 2}},
-                                    {{1, 3}, {2, 2}, {-1, -1}}, {{2, 3}, {3, 3}, {-1, -1}}};
         f64x4 acc[3];
 #pragma unroll
         for (int x = 0; x < 3; ++x) acc[x] = f64x4{0.0, 0.0, 0.0, 0.0};
-        const int l16 = lane & 15;
-        const int lk = lane >> 4;
-        // loader: thread t moves rows 4 q .. 4 q + 3 (q = t % 16) of columns
-        // t / 16 + 16 e, e < 4, as 16-byte vectors (lanes of a column read
-        // 256 contiguous bytes; the LDS writes hit 64 distinct banks)
-        const bool vec4 = (k & 3) == 0;
-        f32x4 pre[4];
-        auto fetch = [&](int r0) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int w = (tid >> 4) + 16 * e, q = tid & 15;
-                const int c = col[w];
-                const int rr = r0 + 4 * q;
-                const int64_t base = static_cast<int64_t>(c) * k + rr;
-                if (c >= 0 && vec4 && rr + 4 <= k) {
-                    pre[e] = *reinterpret_cast<const f32x4*>(Xt + base);
-                } else {
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) pre[e][v] = (c >= 0 && rr + v < k) ? Xt[base + v] : 0.0f;
-                }
-            }
-        };
-        auto stash = [&](float (*Xs)[PD]) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int w = (tid >> 4) + 16 * e, q = tid & 15;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) Xs[4 * q + v][w] = pre[e][v];
-            }
-        };
-        const int nchunk = (k + GR - 1) / GR;
-        fetch(0);
-        stash(Xs0);
+        const int nchunk = (k + PC - 1) / PC;
+        pair_fetch(Xt, k, col, tid, 0, pre0, pre1);
+        pair_stash(lds, 0, tid, pre0, pre1);
         __syncthreads();
+        const bool diag = wave < 2;
+        const int a0 = (wave == 1) ? 2 : 0, a1 = a0 + 1, bb = wave;     // bb: third block of waves 2, 3
         for (int ch = 0; ch < nchunk; ++ch) {
-            float (*cur)[PD] = (ch & 1) ? Xs1 : Xs0;
-            float (*nxt)[PD] = (ch & 1) ? Xs0 : Xs1;
-            if (ch + 1 < nchunk) fetch((ch + 1) * GR);
+            const int s = ch & 1;
+            if (ch + 1 < nchunk) pair_fetch(Xt, k, col, tid, (ch + 1) * PC, pre0, pre1);
+            bf16x8 f0[3], f1[3];
 #pragma unroll
-            for (int x = 0; x < 3; ++x) {
-                const int ti = tiles[wave][x][0], tj = tiles[wave][x][1];
-                if (ti >= 0) {
-#pragma unroll
-                    for (int kk = 0; kk < GR; kk += 8) {
-                        f32x4 part = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            cur[kk + lk][16 * ti + l16], cur[kk + lk][16 * tj + l16], f32x4{0.0f, 0.0f, 0.0f, 0.0f},
-                            0, 0, 0);
-                        part = __builtin_amdgcn_mfma_f32_16x16x4f32(cur[kk + 4 + lk][16 * ti + l16],
-                                                                    cur[kk + 4 + lk][16 * tj + l16], part, 0, 0, 0);
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) acc[x][v] += static_cast<double>(part[v]);
-                    }
-                }
+            for (int p = 0; p < 3; ++p) {
+                f0[p] = gram_frag(lds, s, p, a0, lane);
+                f1[p] = gram_frag(lds, s, p, a1, lane);
             }
-            if (ch + 1 < nchunk) stash(nxt);
+            if (diag) {
+                f32x4 part[3];
+#pragma unroll
+                for (int x = 0; x < 3; ++x) part[x] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    const int pa = kPlanePairs[q][0], pb = kPlanePairs[q][1];
+                    part[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f0[pa], f0[pb], part[0], 0, 0, 0);
+                    part[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f0[pa], f1[pb], part[1], 0, 0, 0);
+                    part[2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f1[pa], f1[pb], part[2], 0, 0, 0);
+                }
+#pragma unroll
+                for (int x = 0; x < 3; ++x)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) acc[x][v] += static_cast<double>(part[x][v]);
+            } else {
+                bf16x8 f2[3];
+#pragma unroll
+                for (int p = 0; p < 3; ++p) f2[p] = gram_frag(lds, s, p, bb, lane);
+                f32x4 part[2];
+#pragma unroll
+                for (int x = 0; x < 2; ++x) part[x] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    const int pa = kPlanePairs[q][0], pb = kPlanePairs[q][1];
+                    part[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f0[pa], f2[pb], part[0], 0, 0, 0);
+                    part[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f1[pa], f2[pb], part[1], 0, 0, 0);
+                }
+#pragma unroll
+                for (int x = 0; x < 2; ++x)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) acc[x][v] += static_cast<double>(part[x][v]);
+            }
+            if (ch + 1 < nchunk) pair_stash(lds, s ^ 1, tid, pre0, pre1);
             __syncthreads();
         }
-        // fp32 16x16 block layout: lane holds column (lane & 15); accumulator
-        // register v holds row 4 (lane >> 4) + v.
+        // 16 x 16 block layout: lane holds column (lane & 15); accumulator
+        // register v holds row 4 (lane >> 4) + v. The planes are dead: the
+        // last barrier above ends every read of them.
+        const int ntile = diag ? 3 : 2;
 #pragma unroll
         for (int x = 0; x < 3; ++x) {
-            const int ti = tiles[wave][x][0], tj = tiles[wave][x][1];
-            if (ti >= 0) {
+            if (x < ntile) {
+                const int ti = diag ? ((x == 2) ? a1 : a0) : ((x == 0) ? a0 : a1);
+                const int tj = diag ? ((x == 0) ? a0 : a1) : bb;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int i = 16 * ti + 4 * lk + v;
-                    const int j = 16 * tj + l16;
+                    const int i = 16 * ti + 4 * (lane >> 4) + v;
+                    const int j = 16 * tj + (lane & 15);
                     G[i][j] = acc[x][v];
                     G[j][i] = acc[x][v];
                 }
@@ -481,71 +574,77 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
             Tf0[x][(kInnerSweeps & 1) ? JW - 1 - (c0 + j) : c0 + j] = static_cast<float>(tv[j]);
         __syncthreads();
     }
-    // ---- 4. Y_P <- Y_P Theta on the fp32 matrix cores: 64-row chunks through
-    //         LDS (the next chunk in flight in registers), results stored from
-    //         the accumulators (a lane writes four consecutive rows of a column)
-    float (*Tf)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]);          // 64 x 65 fp32
-    float (*Xc)[PD] = reinterpret_cast<float (*)[PD]>(&G[0][0]) + JW;     // Xc[w][t]: column w, row t
-    float* Y = Xtb + static_cast<int64_t>(b) * strideX;
-    const bool vec4 = (k & 3) == 0;
-    // loader: thread t moves rows 4 (t % 16) .. +3 of columns t / 16 + 16 e, e < 4
-    const int aq = tid & 15, aw = tid >> 4;
-    f32x4 pre[4];
-    auto fetch = [&](int r0) {
+    // ---- 4. Y_P <- Y_P Theta on the bf16 matrix cores: Theta split into
+    //         three planes once (the wave's B fragments stay in registers),
+    //         32-row chunks of Y_P split and staged as in the Gram, the A
+    //         fragments (8 consecutive columns of one row) read with the
+    //         transposing LDS read; six plane products per output, as in the
+    //         Gram. Wave (tm, tn) writes rows 16 tm .. 16 tm + 15 of each chunk,
+    //         columns 32 tn .. 32 tn + 31 (two 16 x 16 tiles), a lane four
+    //         consecutive rows of one column per tile.
+    {
+        const int tm = wave >> 1, tn = wave & 1;
+        const float (*Tf)[PD] = reinterpret_cast<const float (*)[PD]>(&G[0][0]);   // Theta[w][c], fp32
+        bf16x8 bq[2][2][3];   // [column tile][K step of 32][plane]
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int w = aw + 16 * e;
-            const int c = col[w];
-            const int rr = r0 + 4 * aq;
-            const int64_t base = static_cast<int64_t>(c) * k + rr;
-            if (c >= 0 && vec4 && rr + 4 <= k) {
-                pre[e] = *reinterpret_cast<const f32x4*>(Y + base);
-            } else {
+        for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) pre[e][v] = (c >= 0 && rr + v < k) ? Y[base + v] : 0.0f;
+            for (int ks = 0; ks < 2; ++ks) {
+                const int c = 32 * tn + 16 * ct + (lane & 15);
+                const int w0 = 32 * ks + 8 * (lane >> 4);
+                f32x4 t0, t1;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    t0[v] = Tf[w0 + v][c];
+                    t1[v] = Tf[w0 + 4 + v][c];
+                }
+                split8(t0, t1, bq[ct][ks][0], bq[ct][ks][1], bq[ct][ks][2]);
             }
-        }
-    };
-    const int tm = wave >> 1, tn = wave & 1;
-    const int l32 = lane & 31, lk2 = lane >> 5;
-    const int nch = (k + AR - 1) / AR;
-    fetch(0);
-    for (int ch = 0; ch < nch; ++ch) {
-        const int r0 = ch * AR;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) Xc[aw + 16 * e][4 * aq + v] = pre[e][v];
+        __syncthreads();                       // the Y_P planes overwrite Theta
+        float* Y = Xtb + static_cast<int64_t>(b) * strideX;
+        const int nch = (k + PC - 1) / PC;
+        pair_fetch(Y, k, col, tid, 0, pre0, pre1);
+        pair_stash(lds, 0, tid, pre0, pre1);
         __syncthreads();
-        if (ch + 1 < nch) fetch(r0 + AR);
-        f32x16 acc;
+        const int cst[2] = {col[32 * tn + (lane & 15)], col[32 * tn + 16 + (lane & 15)]};
+        const bool vec4 = (k & 3) == 0;
+        for (int ch = 0; ch < nch; ++ch) {
+            const int s = ch & 1;
+            const int r0 = ch * PC;
+            if (ch + 1 < nch) pair_fetch(Y, k, col, tid, r0 + PC, pre0, pre1);
+            f32x4 acc[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-#pragma unroll 8
-        for (int kk = 0; kk < JW; kk += 2) {
-            const float a = Xc[kk + lk2][32 * tm + l32];   // A[t][w] = Y[t][w]
-            const float bv = Tf[kk + lk2][32 * tn + l32];  // B[w][c] = Theta[w][c]
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bv, acc, 0, 0, 0);
-        }
-        // 32x32 block layout: lane holds column (lane & 31) and rows
-        // (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
-        const int c = col[32 * tn + l32];
-        if (c >= 0) {
-            float* dst = Y + static_cast<int64_t>(c) * k + r0;
+            for (int ks = 0; ks < 2; ++ks) {
+                bf16x8 af[3];
 #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-                const int t0 = 32 * tm + 8 * g4 + 4 * lk2;
-                if (vec4 && r0 + t0 + 4 <= k) {
-                    *reinterpret_cast<f32x4*>(dst + t0) =
-                        f32x4{acc[4 * g4 + 0], acc[4 * g4 + 1], acc[4 * g4 + 2], acc[4 * g4 + 3]};
-                } else {
+                for (int p = 0; p < 3; ++p) af[p] = apply_frag(lds, s, p, tm, ks, lane);
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        if (r0 + t0 + v < k) dst[t0 + v] = acc[4 * g4 + v];
+                for (int q = 0; q < 6; ++q)
+#pragma unroll
+                    for (int ct = 0; ct < 2; ++ct)
+                        acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[kPlanePairs[q][0]],
+                                                                          bq[ct][ks][kPlanePairs[q][1]], acc[ct], 0,
+                                                                          0, 0);
+            }
+            // rows r0 + 16 tm + 4 (lane >> 4) + v of column cst[ct]
+            const int rr = r0 + 16 * tm + 4 * (lane >> 4);
+#pragma unroll
+            for (int ct = 0; ct < 2; ++ct) {
+                const int c = cst[ct];
+                if (c >= 0) {
+                    float* dst = Y + static_cast<int64_t>(c) * k + rr;
+                    if (vec4 && rr + 4 <= k) {
+                        *reinterpret_cast<f32x4*>(dst) = acc[ct];
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            if (rr + v < k) dst[v] = acc[ct][v];
+                    }
                 }
             }
+            if (ch + 1 < nch) pair_stash(lds, s ^ 1, tid, pre0, pre1);
+            __syncthreads();
         }
-        __syncthreads();
     }
 }
 
