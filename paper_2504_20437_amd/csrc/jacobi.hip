@@ -115,40 +115,42 @@ __global__ __launch_bounds__(256) void jacobi_prepare_kernel(const double* Rb, i
 // Jacobi rotation (c, s) that zeroes the off-diagonal of [[a, g], [g, b]]
 // under column p' = c p - s q, q' = s p + c q: t = tan(theta) is the smaller
 // root of t^2 + 2 zeta t - 1 = 0, zeta = (b - a) / (2 g) (Rutishauser's
-// form). The angle only has to be close (a residual off-diagonal is removed
-// by later sweeps), so zeta and t use the hardware fp64 reciprocal and fp32
-// square root; the rotation itself must be orthogonal to fp64 rounding, so
-// c = 1 / sqrt(1 + t^2) is refined by two Newton steps from v_rsq_f64 and
-// s = c t, giving c^2 + s^2 = 1 to within a few ulp.
-__device__ __forceinline__ void rotation(double a, double b, double g, double& c, double& s) {
-    const double zeta = (b - a) * 0.5 * __builtin_amdgcn_rcp(g);
-    const float zf = static_cast<float>(zeta);
+// form), b - a taken in fp64. The rotation is applied to fp32 entries, so
+// fp32 suffices for the rest: the hardware reciprocal, square root and
+// reciprocal square root (c = 1 / sqrt(1 + t^2), s = c t: c^2 + s^2 = 1 to a
+// few fp32 ulp). The angle only has to be close: a residual off-diagonal is
+// removed by later sweeps, and every visit recomputes the pair's Gram from the
+// columns in fp64. |zeta| past the fp32 range gives t = 0.
+__device__ __forceinline__ void rotation(double a, double b, float g, float& c, float& s) {
+    const float zf = static_cast<float>(b - a) * 0.5f * __builtin_amdgcn_rcpf(g);
     const float az = fabsf(zf);
     float tf = __builtin_amdgcn_rcpf(az + __builtin_amdgcn_sqrtf(fmaf(az, az, 1.0f)));   // |zeta| huge: 0
     tf = (zf >= 0.0f) ? tf : -tf;                                                         // sign(0) = +1
-    const double t = static_cast<double>(tf);
-    const double x = fma(t, t, 1.0);
-    double y = __builtin_amdgcn_rsq(x);
-    y = y * fma(-0.5 * x * y, y, 1.5);
-    y = y * fma(-0.5 * x * y, y, 1.5);
-    c = y;
-    s = y * t;
+    c = __builtin_amdgcn_rsqf(fmaf(tf, tf, 1.0f));
+    s = c * tf;
 }
 
 // Cross-lane moves of an fp32 value within a wave (DPP, no LDS traffic).
-// dpp_swap_pairs: lane x receives lane x ^ 1. dpp_odd_partner: an odd lane x
-// receives lane x + 1, an even lane x - 1. Lanes without a source (0 and 63 in
-// the odd pattern) read 0, which only idle lanes consume; a zero old value and
-// bound_ctrl let the compiler fold the lane move into the multiply that uses it
+// dpp_swap_pairs: lane x receives lane x ^ 1. dpp_from_next / dpp_from_prev:
+// lane x receives lane x + 1 / x - 1 (whole-wave shifts); lanes without a
+// source (63 / 0) read 0. A zero old value and bound_ctrl let the compiler
+// fold the lane move into the multiply that uses it.
 __device__ __forceinline__ float dpp_swap_pairs(float v) {
     const int i = __float_as_int(v);
     return __int_as_float(__builtin_amdgcn_update_dpp(0, i, 0xB1, 0xf, 0xf, true));
 }
-__device__ __forceinline__ float dpp_odd_partner(float v, bool odd) {
-    const int i = __float_as_int(v);
-    const int l = __builtin_amdgcn_update_dpp(0, i, 0x130, 0xf, 0xf, true);
-    const int r = __builtin_amdgcn_update_dpp(0, i, 0x138, 0xf, 0xf, true);
-    return __int_as_float(odd ? l : r);
+__device__ __forceinline__ float dpp_from_next(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x130, 0xf, 0xf, true));
+}
+__device__ __forceinline__ float dpp_from_prev(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x138, 0xf, 0xf, true));
+}
+// odd rounds: an odd lane's partner row is lane x + 1, an even lane's x - 1;
+// with cn = c on odd lanes (0 on even ones) and cp the other way round, the
+// partner term is cn * v[x + 1] + cp * v[x - 1], both lane moves folded into
+// their multiplies
+__device__ __forceinline__ float rotate_odd(float v, float sg, float cn, float cp) {
+    return fmaf(sg, v, fmaf(cp, dpp_from_prev(v), cn * dpp_from_next(v)));
 }
 
 // ---- bf16 planes of the pair's columns (Gram and rotation phases) ----------
@@ -471,21 +473,23 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
                 const int q = p + 1;
                 const int wq = q >> 4, jq = q & 15;
                 const double a = Dc[p], b = Dc[q];
-                const double g = static_cast<double>(Bc[(wq * 16 + jq) * 16 + jq]);
-                double cr = 1.0, sr = 0.0;
-                if (g * g > 1e-30 * (a * b)) rotation(a, b, g, cr, sr);
+                const jreal gf = Bc[(wq * 16 + jq) * 16 + jq];
+                const double g = static_cast<double>(gf);
+                jreal cf = 1.0f, sf = 0.0f;
+                if (g * g > 1e-30 * (a * b)) rotation(a, b, gf, cf, sf);
                 // rotated slot p' = c p - s q goes to slot q, q' = s p + c q to slot p
                 if (x == p) {
                     if ((p >> 4) == wave) {
+                        const double cr = cf, sr = sf;
                         const double cs2 = 2.0 * cr * sr * g;
                         Dn[p] = sr * sr * a + cs2 + cr * cr * b;
                         Dn[q] = cr * cr * a - cs2 + sr * sr * b;
                     }
-                    CSw[(wave * JW + p) * 2 + 0] = static_cast<jreal>(cr);
-                    CSw[(wave * JW + p) * 2 + 1] = static_cast<jreal>(sr);
+                    CSw[(wave * JW + p) * 2 + 0] = cf;
+                    CSw[(wave * JW + p) * 2 + 1] = sf;
                 }
-                c = static_cast<jreal>(cr);
-                sg = static_cast<jreal>((x == p) ? sr : -sr);
+                c = cf;
+                sg = (x == p) ? sf : -sf;
             } else if ((x >> 4) == wave) {
                 Dn[x] = Dc[x];
             }
@@ -496,10 +500,11 @@ __global__ __launch_bounds__(JT, 4) void jacobi_pair_kernel(float* Xtb, int k, i
                 for (int j = 0; j < 16; ++j) gv[j] = sg * gv[j] + c * dpp_swap_pairs(gv[j]);
             } else {
                 const bool odd = (x & 1) != 0;
+                const jreal cn = odd ? c : jreal(0), cp = odd ? jreal(0) : c;
 #pragma unroll
-                for (int j = 0; j < 16; ++j) gv[j] = sg * gv[j] + c * dpp_odd_partner(gv[j], odd);
-                hgL = sg * hgL + c * dpp_odd_partner(hgL, odd);
-                hgR = sg * hgR + c * dpp_odd_partner(hgR, odd);
+                for (int j = 0; j < 16; ++j) gv[j] = rotate_odd(gv[j], sg, cn, cp);
+                hgL = rotate_odd(hgL, sg, cn, cp);
+                hgR = rotate_odd(hgR, sg, cn, cp);
             }
             // (c, s) of this wave's column pairs, published by their first rows
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
