@@ -115,8 +115,13 @@ hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, con
 hipError_t launch_jacobi_prepare(const double* R, int k, int64_t strideR, float* Yt, int64_t strideX,
                                  int* rot, int max_sweeps, const double* diag, int* exps, int batch,
                                  hipStream_t stream);
+// order of the columns for sweep `sweep` (by decreasing norm) into jperm
+// (k per matrix), with the column norms in norms (k per matrix); matrices
+// converged in the previous sweep are skipped
+hipError_t launch_jacobi_order(const float* Yt, int k, int64_t strideX, double* norms, int* jperm, const int* rot,
+                               int max_sweeps, int sweep, int batch, hipStream_t stream);
 hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, int step, int sweep, int* rot,
-                              int max_sweeps, double tol, int batch, hipStream_t stream);
+                              int max_sweeps, double tol, const int* jperm, int batch, hipStream_t stream);
 // scratch: at least 2 k + r doubles per matrix at stride strideScratch (doubles);
 // exps: the per-matrix exponents launch_jacobi_prepare wrote (sigma = 2^-e |y|);
 // norms (k fp64) and perm (k int) per matrix: scratch for the column norms and

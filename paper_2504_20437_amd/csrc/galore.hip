@@ -367,13 +367,17 @@ int on_two_streams(int batch, hipStream_t stream, hipStream_t aux, F&& f) {
     return e;
 }
 
-int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, int batch, hipStream_t stream,
-                          hipStream_t aux) {
+int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, double* norms, int* jperm,
+                          int batch, hipStream_t stream, hipStream_t aux) {
     return on_two_streams(batch, stream, aux, [&](int b0, int cnt, hipStream_t st) -> int {
-        for (int sw = 0; sw < kMaxSweeps; ++sw)
+        const int64_t ko = static_cast<int64_t>(b0) * k;
+        for (int sw = 0; sw < kMaxSweeps; ++sw) {
+            GALORE_TRY(launch_jacobi_order(Yt + b0 * strideKK, k, strideKK, norms + ko, jperm + ko,
+                                           rot + b0 * kMaxSweeps, kMaxSweeps, sw, cnt, st));
             for (int stp = 0; stp < nb - 1; ++stp)
                 GALORE_TRY(launch_jacobi_step(Yt + b0 * strideKK, k, strideKK, nb, stp, sw, rot + b0 * kMaxSweeps,
-                                              kMaxSweeps, kJacobiTol, cnt, st));
+                                              kMaxSweeps, kJacobiTol, jperm + ko, cnt, st));
+        }
         return GALORE_OK;
     });
 }
@@ -534,7 +538,8 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
                                      jexp, batch, stream));
     const int nblk_real = (k + kJacobiBlock - 1) / kJacobiBlock;
     const int nb = nblk_real + (nblk_real & 1);
-    GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, batch, stream, aux));
+    GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, w.d(L.offNorm), w.i(L.offPerm), batch, stream,
+                                       aux));
     GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
                                       kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
                                       L.strideTheta / 2, jexp, w.d(L.offNorm), w.i(L.offPerm), w.f(L.offRinv),
