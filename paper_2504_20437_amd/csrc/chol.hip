@@ -6,18 +6,24 @@
 // small SVD works on.
 //
 // Right-looking, blocked by CB = 64 rows; every launch covers all matrices of
-// the batch (grid z / y = matrix), so the chip is filled by (tiles x batch)
-// workgroups rather than one workgroup per matrix:
+// the batch (grid y = matrix), so the chip is filled by (tiles x batch)
+// workgroups rather than one workgroup per matrix. The inverse X = R'^-1 is
+// built alongside, column block by column block (X R' = I gives
+// X_IJ = -(sum_{U<J} X_IU R_UJ) D_J), its partial sums P_IJ accumulated by the
+// trailing launches in X's own upper blocks, so no separate inverse phase runs:
+//   diag 0   factor the 64 x 64 diagonal block 0 in registers (unblocked,
+//            fp64) and invert it (D_0 = R'_00^-1, kept in X's diagonal block);
 //   for each block row J:
-//     diag     factor the 64 x 64 diagonal block in registers (unblocked, fp64)
-//              and invert it (D_J = R'_JJ^-1, kept in the fp64 inverse buffer);
-//     panel    R_JT = D_J^T C_JT for every block column T > J;
-//     trailing C_T1T2 -= R_JT1^T R_JT2 on the upper tiles T1 <= T2 right of J.
-//   inverse  X = R'^-1 by levels d = T - I: X_IT = -D_I sum_{I<U<=T} R_IU X_UT,
-//            written in fp64 and as fp32 (lower triangle zero) for the GEMM
-//            that applies it.
-// The panel, trailing and inverse tiles are 64 x 64 x 64 products on the fp64
-// matrix cores.
+//     panel+X  R_JT = D_J^T C_JT for every block column T > J, and block column J
+//              of the inverse, X_IJ = -P_IJ D_J for I < J (fp64 and fp32, the
+//              fp32 copy's lower tiles zero for the GEMM that applies it);
+//     trailing C_T1T2 -= R_JT1^T R_JT2 on the upper tiles J < T1 <= T2, and
+//              P_IT (+)= X_IJ R_JT for I <= J < T; the workgroup of tile
+//              (J + 1, J + 1) then factors and inverts that diagonal block
+//              (step J + 1's diagonal), whose last update it just made.
+// The panel, inverse, trailing and partial-sum tiles are 64 x 64 x 64 products
+// on the fp64 matrix cores, operands loaded from memory straight into
+// registers. Two launches per block row (with the factor's inverse or without).
 // R overwrites the upper triangle of C; the lower triangle is not used.
 //
 // Semi-definite inputs: a pivot d <= tau_rel * (original diagonal) marks the
@@ -32,31 +38,6 @@ namespace {
 
 constexpr int CB = 64;     // block size
 constexpr int CT = 256;    // threads per workgroup (4 waves)
-constexpr int LP = CB + 1; // padded LDS row
-
-// acc[bi][bj] += sum_{t < CB} As[t][32 wm + 16 bi + i] * Bs[t][32 wn + 16 bj + j] on the
-// fp64 matrix cores: wave (wm, wn) owns a 32 x 32 quadrant of the 64 x 64
-// result as 2 x 2 blocks of 16 x 16. Operand layout of the 16x16x4 fp64 MFMA:
-// lane l supplies A[l & 15][l >> 4] and B[l >> 4][l & 15]; accumulator
-// register v of lane l holds C[4 v + (l >> 4)][l & 15]. Rows of As / Bs
-// beyond the live extent are zero, so the full depth CB is always run.
-__device__ __forceinline__ void mma64_tn(double (*As)[LP], double (*Bs)[LP], f64x4 acc[2][2], int wm,
-                                         int wn, int lane) {
-    const int l16 = lane & 15, lk = lane >> 4;
-#pragma unroll 4
-    for (int t = 0; t < CB; t += 4) {
-        double a[2], bv[2];
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi) a[bi] = As[t + lk][32 * wm + 16 * bi + l16];
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj) bv[bj] = Bs[t + lk][32 * wn + 16 * bj + l16];
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-            for (int bj = 0; bj < 2; ++bj)
-                acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[bi], bv[bj], acc[bi][bj], 0, 0, 0);
-    }
-}
 
 __device__ __forceinline__ void zero_acc(f64x4 acc[2][2]) {
 #pragma unroll
@@ -94,28 +75,29 @@ __device__ __forceinline__ f64x2 ld_pair(const double* M, int64_t ld, int row, i
 __device__ __forceinline__ void mma64_pairs(const double* Ap, const double* Bp, int64_t ld, int nt, int na,
                                             int nbc, bool vec, f64x4 acc[2][2], int wm, int wn, int lane) {
     const int l16 = lane & 15, lk = lane >> 4;
-    f64x2 av[16], bv[16];
+    // four groups of four steps, the next group's operands in flight while the
+    // current one is multiplied (keeps the kernels within 128 registers)
+    f64x2 av[2][4], bv[2][4];
+    auto load = [&](int g, int buf) {
 #pragma unroll
-    for (int s = 0; s < 16; ++s) {
-        const int t = 4 * s + lk;
-        av[s] = ld_pair(Ap, ld, t, 32 * wm + 2 * l16, nt, na, vec);
-        bv[s] = ld_pair(Bp, ld, t, 32 * wn + 2 * l16, nt, nbc, vec);
-    }
+        for (int i = 0; i < 4; ++i) {
+            const int t = 4 * (4 * g + i) + lk;
+            av[buf][i] = ld_pair(Ap, ld, t, 32 * wm + 2 * l16, nt, na, vec);
+            bv[buf][i] = ld_pair(Bp, ld, t, 32 * wn + 2 * l16, nt, nbc, vec);
+        }
+    };
+    load(0, 0);
 #pragma unroll
-    for (int s = 0; s < 16; ++s)
+    for (int g = 0; g < 4; ++g) {
+        if (g + 1 < 4) load(g + 1, (g + 1) & 1);
 #pragma unroll
-        for (int bi = 0; bi < 2; ++bi)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int bj = 0; bj < 2; ++bj)
-                acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[s][bi], bv[s][bj], acc[bi][bj], 0, 0, 0);
-}
-
-// S[c][r] = M[(r0 + r) * ld + c0 + c] (transposed load)
-__device__ __forceinline__ void load_tile_t(double (*S)[LP], const double* M, int64_t ld, int r0, int c0,
-                                            int nr, int nc) {
-    for (int idx = threadIdx.x; idx < CB * CB; idx += CT) {
-        const int r = idx / CB, c = idx % CB;
-        S[c][r] = (r < nr && c < nc) ? M[static_cast<int64_t>(r0 + r) * ld + c0 + c] : 0.0;
+            for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                for (int bj = 0; bj < 2; ++bj)
+                    acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[g & 1][i][bi], bv[g & 1][i][bj],
+                                                                       acc[bi][bj], 0, 0, 0);
     }
 }
 
@@ -130,14 +112,9 @@ __device__ __forceinline__ void load_tile_t(double (*S)[LP], const double* M, in
 //  * inverse D = R'^-1 (R' = R with unit rows for the dependent pivots), by
 //    columns from the last: row i of D is final once rows t > i are
 //    eliminated from it, D_i = X_i / R'_ii, then X_a -= R_ai D_i for a < i.
-__global__ __launch_bounds__(CT) void chol_diag_kernel(double* Cb, int k, int64_t strideC, int J,
-                                                       double* diag0b, int* deficB, double* Xb,
-                                                       float* Rib, int64_t strideInv, double tau_rel) {
-    const int b = blockIdx.x;
-    double* C = Cb + static_cast<int64_t>(b) * strideC;
-    double* diag0 = diag0b + static_cast<int64_t>(b) * k;
-    int* defic = deficB + static_cast<int64_t>(b) * k;
-    double* X = Xb + static_cast<int64_t>(b) * strideInv;
+// (the body of one matrix's diagonal step; every thread of the workgroup calls it)
+__device__ __forceinline__ void diag_block(double* C, int k, int J, double* diag0, int* defic, double* X, float* Ri,
+                                           double tau_rel) {
     const int tid = threadIdx.x;
     const int tx = tid & 15, ty = tid >> 4;
     const int j0 = J * CB;
@@ -261,180 +238,227 @@ __global__ __launch_bounds__(CT) void chol_diag_kernel(double* Cb, int k, int64_
             if (r < jb && c < jb) {
                 const double v = (c >= r) ? x[q][w] : 0.0;
                 X[static_cast<int64_t>(j0 + r) * k + j0 + c] = v;
-                if (Rib != nullptr)
-                    Rib[static_cast<int64_t>(b) * strideInv + static_cast<int64_t>(j0 + r) * k + j0 + c] =
-                        static_cast<float>(v);
+                if (Ri != nullptr) Ri[static_cast<int64_t>(j0 + r) * k + j0 + c] = static_cast<float>(v);
             }
         }
 }
 
-// R_JT = D_J^T C_JT (deficient rows zero), in place in C, for T = J + 1 + blockIdx.x
-__global__ __launch_bounds__(CT) void chol_panel_kernel(double* Cb, int k, int64_t strideC, int J,
-                                                        const int* deficB, const double* Xb,
-                                                        int64_t strideInv) {
-    const int b = blockIdx.y;
-    double* C = Cb + static_cast<int64_t>(b) * strideC;
-    const int* defic = deficB + static_cast<int64_t>(b) * k;
-    const double* X = Xb + static_cast<int64_t>(b) * strideInv;
-    const int j0 = J * CB;
-    const int jb = min(CB, k - j0);
-    const int c0 = (J + 1 + blockIdx.x) * CB;
-    const int cb = min(CB, k - c0);
-    const bool vec = (k & 1) == 0;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int l16 = lane & 15, lk = lane >> 4;
-    f64x4 acc[2][2];
-    zero_acc(acc);
-    // A[i][t] = D[t][i] (rows j0 + t of the block inverse), B[t][c] = C_JT[t][c]
-    mma64_pairs(X + static_cast<int64_t>(j0) * k + j0, C + static_cast<int64_t>(j0) * k + c0, k, jb, jb, cb,
-                vec, acc, wm, wn, lane);
-    __syncthreads();   // every wave has its operands before the tile is overwritten
-#pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = 32 * wm + 2 * (4 * v + lk) + bi;
-            if (r >= jb) continue;
-            const bool def = defic[j0 + r] != 0;
-            const int c = 32 * wn + 2 * l16;
-            double* dst = C + static_cast<int64_t>(j0 + r) * k + c0 + c;
-            const double o0 = def ? 0.0 : acc[bi][0][v], o1 = def ? 0.0 : acc[bi][1][v];
-            if (vec && c + 1 < cb) {
-                *reinterpret_cast<f64x2*>(dst) = f64x2{o0, o1};
-            } else {
-                if (c < cb) dst[0] = o0;
-                if (c + 1 < cb) dst[1] = o1;
-            }
-        }
+__global__ __launch_bounds__(CT) void chol_diag_kernel(double* Cb, int k, int64_t strideC, int J,
+                                                       double* diag0b, int* deficB, double* Xb,
+                                                       float* Rib, int64_t strideInv, double tau_rel) {
+    const int b = blockIdx.x;
+    diag_block(Cb + static_cast<int64_t>(b) * strideC, k, J, diag0b + static_cast<int64_t>(b) * k,
+               deficB + static_cast<int64_t>(b) * k, Xb + static_cast<int64_t>(b) * strideInv,
+               Rib != nullptr ? Rib + static_cast<int64_t>(b) * strideInv : nullptr, tau_rel);
 }
 
-// C_T1T2 -= R_JT1^T R_JT2 for J < T1 <= T2; blockIdx.x enumerates the upper tiles
-__global__ __launch_bounds__(CT) void chol_trailing_kernel(double* Cb, int k, int64_t strideC, int J,
-                                                           int nb) {
-    const int b = blockIdx.y;
-    double* C = Cb + static_cast<int64_t>(b) * strideC;
-    const int n = nb - J - 1;
-    // blockIdx.x -> (u, vt) with 0 <= u <= vt < n, row-major over the upper triangle
-    int idx = blockIdx.x, u = 0;
-    while (idx >= n - u) {
-        idx -= n - u;
-        ++u;
-    }
-    const int vt = u + idx;
-    const int j0 = J * CB;
-    const int jb = min(CB, k - j0);
-    const int r0 = (J + 1 + u) * CB, rb = min(CB, k - r0);
-    const int c0 = (J + 1 + vt) * CB, cb = min(CB, k - c0);
-    const bool vec = (k & 1) == 0;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+// acc += A B for one 64 x 64 x 64 tile with A given by rows (A[i * ld + t], t
+// contiguous) and B by contraction rows (B[t * ld + c]), operands straight from
+// global memory into registers: contraction step s takes t = 8 (s / 2) +
+// 2 (lane >> 4) + s % 2, so a lane's A entries A[i][t], A[i][t + 1] are one
+// 16-byte pair. The result lands in the pair layout of mma64_pairs (row
+// 32 wm + 2 (4 v + (lane >> 4)) + bi, column 32 wn + 2 (lane & 15) + bj).
+__device__ __forceinline__ void mma64_rowA(const double* Ap, const double* Bp, int64_t ld, int nar, int nt, int nbc,
+                                           bool vec, f64x4 acc[2][2], int wm, int wn, int lane) {
     const int l16 = lane & 15, lk = lane >> 4;
-    // on a diagonal tile the quadrant below the diagonal is not needed
-    if (u == vt && wm > wn) return;
-    f64x4 acc[2][2];
-    zero_acc(acc);
-    // operands: rows j0 + t of the block row J just finished (R_JT1, R_JT2);
-    // the tile updated lies in a later block row, so no wave reads what
-    // another one writes
-    mma64_pairs(C + static_cast<int64_t>(j0) * k + r0, C + static_cast<int64_t>(j0) * k + c0, k, jb, rb, cb,
-                vec, acc, wm, wn, lane);
+    // four groups of four steps (two A pairs per row block), double-buffered as
+    // in mma64_pairs
+    f64x2 a2[2][2][2], b2[2][4];
+    auto load = [&](int g, int buf) {
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = 32 * wm + 2 * (4 * v + lk) + bi;
-            if (r >= rb) continue;
-            const int c = 32 * wn + 2 * l16;
-            const bool k0 = c < cb && (u != vt || c >= r);
-            const bool k1 = c + 1 < cb && (u != vt || c + 1 >= r);
-            double* dst = C + static_cast<int64_t>(r0 + r) * k + c0 + c;
-            if (vec && k0 && k1) {
-                f64x2 o = *reinterpret_cast<f64x2*>(dst);
-                o[0] -= acc[bi][0][v];
-                o[1] -= acc[bi][1][v];
-                *reinterpret_cast<f64x2*>(dst) = o;
-            } else {
-                if (k0) dst[0] -= acc[bi][0][v];
-                if (k1) dst[1] -= acc[bi][1][v];
-            }
-        }
-}
-
-// Level d of the inverse: tile (I, I + d) for I = blockIdx.x.
-__global__ __launch_bounds__(CT) void chol_inverse_level_kernel(const double* Cb, int k, int64_t strideC,
-                                                                int d, double* Xb, float* Rib,
-                                                                int64_t strideInv) {
-    const int b = blockIdx.y;
-    const double* C = Cb + static_cast<int64_t>(b) * strideC;
-    double* X = Xb + static_cast<int64_t>(b) * strideInv;
-    float* Ri = Rib + static_cast<int64_t>(b) * strideInv;
-    const int I = blockIdx.x, Jc = I + d;
-    const int i0 = I * CB, ib = min(CB, k - i0);
-    const int c0 = Jc * CB, cb = min(CB, k - c0);
-    __shared__ double As[CB][LP];
-    __shared__ double Bs[CB][LP];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
-    const int l16 = lane & 15, lk = lane >> 4;
-    // S = sum_{U = I+1 .. Jc} R_IU X_UJc, operands straight from global memory:
-    // contraction step s = 2 m + e takes t = 8 m + 2 (lane >> 4) + e, so a
-    // lane's A entries R_IU[a][t], R_IU[a][t + 1] are one 16-byte pair; S lands
-    // in the pair layout of mma64_pairs (row 32 wm + 2 (4 v + lk) + bi, column
-    // 32 wn + 2 l16 + bj)
-    const bool vec = (k & 1) == 0;
-    f64x4 acc[2][2];
-    zero_acc(acc);
-    for (int U = I + 1; U <= Jc; ++U) {
-        const int u0 = U * CB, ub = min(CB, k - u0);
-        const double* Rp = C + static_cast<int64_t>(i0) * k + u0;
-        const double* Xp = X + static_cast<int64_t>(u0) * k + c0;
-        f64x2 a2[2][8], b2[16];
-#pragma unroll
-        for (int m = 0; m < 8; ++m)
+        for (int mm = 0; mm < 2; ++mm)
 #pragma unroll
             for (int bi = 0; bi < 2; ++bi)
-                a2[bi][m] = ld_pair(Rp, k, 32 * wm + 2 * l16 + bi, 8 * m + 2 * lk, ib, ub, vec);
+                a2[buf][mm][bi] = ld_pair(Ap, ld, 32 * wm + 2 * l16 + bi, 8 * (2 * g + mm) + 2 * lk, nar, nt, vec);
 #pragma unroll
-        for (int s = 0; s < 16; ++s)
-            b2[s] = ld_pair(Xp, k, 8 * (s >> 1) + 2 * lk + (s & 1), 32 * wn + 2 * l16, ub, cb, vec);
+        for (int i = 0; i < 4; ++i) {
+            const int s = 4 * g + i;
+            b2[buf][i] = ld_pair(Bp, ld, 8 * (s >> 1) + 2 * lk + (s & 1), 32 * wn + 2 * l16, nt, nbc, vec);
+        }
+    };
+    load(0, 0);
 #pragma unroll
-        for (int s = 0; s < 16; ++s)
+    for (int g = 0; g < 4; ++g) {
+        if (g + 1 < 4) load(g + 1, (g + 1) & 1);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
                 for (int bj = 0; bj < 2; ++bj)
-                    acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a2[bi][s >> 1][s & 1], b2[s][bj],
+                    acc[bi][bj] = __builtin_amdgcn_mfma_f64_16x16x4f64(a2[g & 1][i >> 1][bi][i & 1], b2[g & 1][i][bj],
                                                                        acc[bi][bj], 0, 0, 0);
     }
-    // X_IJc = -D_I S
-    load_tile_t(As, X, k, i0, i0, ib, ib);       // As[t][a] = D_I[a][t]
+}
+
+// Step J, after the diagonal block J (factor R_JJ and D_J = R'_JJ^-1):
+//  * blockIdx.x < n (n = nb - J - 1): the panel tile T = J + 1 + blockIdx.x,
+//    R_JT = D_J^T C_JT (deficient rows zero), in place in C;
+//  * with the inverse, blockIdx.x = n + I (I < J): block column J of the
+//    inverse X = R'^-1, X_IJ = -P_IJ D_J, where P_IJ (held in X's block (I, J))
+//    is the sum over U < J of X_IU R_UJ that the trailing steps accumulated;
+//    written in fp64 and as fp32, whose mirrored (lower) tile is set to zero.
+__global__ __launch_bounds__(CT, 4) void chol_panel_x_kernel(double* Cb, int k, int64_t strideC, int J, int n,
+                                                          const int* deficB, double* Xb, float* Rib,
+                                                          int64_t strideInv) {
+    const int b = blockIdx.y;
+    double* C = Cb + static_cast<int64_t>(b) * strideC;
+    const int* defic = deficB + static_cast<int64_t>(b) * k;
+    double* X = Xb + static_cast<int64_t>(b) * strideInv;
+    const int j0 = J * CB;
+    const int jb = min(CB, k - j0);
+    const bool vec = (k & 1) == 0;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l16 = lane & 15, lk = lane >> 4;
+    f64x4 acc[2][2];
+    zero_acc(acc);
+    if (static_cast<int>(blockIdx.x) < n) {
+        const int c0 = (J + 1 + blockIdx.x) * CB;
+        const int cb = min(CB, k - c0);
+        // A[i][t] = D[t][i] (rows j0 + t of the block inverse), B[t][c] = C_JT[t][c]
+        mma64_pairs(X + static_cast<int64_t>(j0) * k + j0, C + static_cast<int64_t>(j0) * k + c0, k, jb, jb, cb,
+                    vec, acc, wm, wn, lane);
+        __syncthreads();   // every wave has its operands before the tile is overwritten
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+        for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
-        for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) Bs[32 * wm + 2 * (4 * v + lk) + bi][32 * wn + 2 * l16 + bj] = acc[bi][bj][v];
-    __syncthreads();
-    f64x4 out[2][2];
-    zero_acc(out);
-    mma64_tn(As, Bs, out, wm, wn, lane);
+            for (int v = 0; v < 4; ++v) {
+                const int r = 32 * wm + 2 * (4 * v + lk) + bi;
+                if (r >= jb) continue;
+                const bool def = defic[j0 + r] != 0;
+                const int c = 32 * wn + 2 * l16;
+                double* dst = C + static_cast<int64_t>(j0 + r) * k + c0 + c;
+                const double o0 = def ? 0.0 : acc[bi][0][v], o1 = def ? 0.0 : acc[bi][1][v];
+                if (vec && c + 1 < cb) {
+                    *reinterpret_cast<f64x2*>(dst) = f64x2{o0, o1};
+                } else {
+                    if (c < cb) dst[0] = o0;
+                    if (c + 1 < cb) dst[1] = o1;
+                }
+            }
+        return;
+    }
+    const int I = blockIdx.x - n;
+    const int i0 = I * CB;
+    // A = P_IJ (rows i0.., columns j0..), B = D_J (rows j0 + t)
+    mma64_rowA(X + static_cast<int64_t>(i0) * k + j0, X + static_cast<int64_t>(j0) * k + j0, k, CB, jb, jb, vec, acc,
+               wm, wn, lane);
+    __syncthreads();       // P_IJ is overwritten by X_IJ below
+    float* Ri = Rib + static_cast<int64_t>(b) * strideInv;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int r = 32 * wm + 16 * bi + 4 * v + lk;
-                const int c = 32 * wn + 16 * bj + l16;
-                if (r < ib && c < cb) {
-                    const double val = -out[bi][bj][v];
-                    X[static_cast<int64_t>(i0 + r) * k + c0 + c] = val;
-                    if (Rib != nullptr) Ri[static_cast<int64_t>(i0 + r) * k + c0 + c] = static_cast<float>(val);
+                const int r = 32 * wm + 2 * (4 * v + lk) + bi;
+                const int c = 32 * wn + 2 * l16 + bj;
+                if (c < jb) {
+                    const double val = -acc[bi][bj][v];
+                    X[static_cast<int64_t>(i0 + r) * k + j0 + c] = val;
+                    Ri[static_cast<int64_t>(i0 + r) * k + j0 + c] = static_cast<float>(val);
                 }
                 // the mirrored (lower) tile of the fp32 inverse is zero
-                if (Rib != nullptr && r < cb && c < ib) Ri[static_cast<int64_t>(c0 + r) * k + i0 + c] = 0.0f;
+                if (r < jb) Ri[static_cast<int64_t>(j0 + r) * k + i0 + c] = 0.0f;
             }
+}
+
+// Step J's updates, after the panel:
+//  * blockIdx.x < n (n + 1) / 2: C_T1T2 -= R_JT1^T R_JT2 on the upper tiles
+//    J < T1 <= T2; the workgroup of tile (J + 1, J + 1) then factors that
+//    diagonal block (step J + 1's diagonal), whose last update this was;
+//  * with the inverse, the rest: P_IT (+)= X_IJ R_JT for I <= J < T, the
+//    partial sums block column T of the inverse needs (I = J starts the sum).
+__global__ __launch_bounds__(CT, 4) void chol_trailing_p_kernel(double* Cb, int k, int64_t strideC, int J, int nb,
+                                                             double* diag0b, int* deficB, double* Xb, float* Rib,
+                                                             int64_t strideInv, double tau_rel) {
+    const int b = blockIdx.y;
+    double* C = Cb + static_cast<int64_t>(b) * strideC;
+    double* X = Xb + static_cast<int64_t>(b) * strideInv;
+    const int n = nb - J - 1;
+    const int ntrail = n * (n + 1) / 2;
+    const int j0 = J * CB;
+    const int jb = min(CB, k - j0);
+    const bool vec = (k & 1) == 0;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l16 = lane & 15, lk = lane >> 4;
+    f64x4 acc[2][2];
+    zero_acc(acc);
+    if (static_cast<int>(blockIdx.x) < ntrail) {
+        // blockIdx.x -> (u, vt) with 0 <= u <= vt < n, row-major over the upper triangle
+        int idx = blockIdx.x, u = 0;
+        while (idx >= n - u) {
+            idx -= n - u;
+            ++u;
+        }
+        const int vt = u + idx;
+        const int r0 = (J + 1 + u) * CB, rb = min(CB, k - r0);
+        const int c0 = (J + 1 + vt) * CB, cb = min(CB, k - c0);
+        // on a diagonal tile the quadrant below the diagonal is not needed
+        if (!(u == vt && wm > wn)) {
+            // operands: rows j0 + t of the block row J just finished (R_JT1, R_JT2);
+            // the tile updated lies in a later block row, so no wave reads what
+            // another one writes
+            mma64_pairs(C + static_cast<int64_t>(j0) * k + r0, C + static_cast<int64_t>(j0) * k + c0, k, jb, rb, cb,
+                        vec, acc, wm, wn, lane);
+#pragma unroll
+            for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int r = 32 * wm + 2 * (4 * v + lk) + bi;
+                    if (r >= rb) continue;
+                    const int c = 32 * wn + 2 * l16;
+                    const bool k0 = c < cb && (u != vt || c >= r);
+                    const bool k1 = c + 1 < cb && (u != vt || c + 1 >= r);
+                    double* dst = C + static_cast<int64_t>(r0 + r) * k + c0 + c;
+                    if (vec && k0 && k1) {
+                        f64x2 o = *reinterpret_cast<f64x2*>(dst);
+                        o[0] -= acc[bi][0][v];
+                        o[1] -= acc[bi][1][v];
+                        *reinterpret_cast<f64x2*>(dst) = o;
+                    } else {
+                        if (k0) dst[0] -= acc[bi][0][v];
+                        if (k1) dst[1] -= acc[bi][1][v];
+                    }
+                }
+        }
+        if (blockIdx.x == 0) {
+            // tile (J + 1, J + 1) is final: factor it (its updates above are
+            // visible to the whole workgroup past the barrier)
+            __syncthreads();
+            diag_block(C, k, J + 1, diag0b + static_cast<int64_t>(b) * k, deficB + static_cast<int64_t>(b) * k, X,
+                       Rib != nullptr ? Rib + static_cast<int64_t>(b) * strideInv : nullptr, tau_rel);
+        }
+        return;
+    }
+    const int p = blockIdx.x - ntrail;
+    const int I = p / n, T = J + 1 + p % n;
+    const int i0 = I * CB;
+    const int c0 = T * CB, cb = min(CB, k - c0);
+    // A = X_IJ (rows i0.., columns j0..), B = R_JT (rows j0 + t of C)
+    mma64_rowA(X + static_cast<int64_t>(i0) * k + j0, C + static_cast<int64_t>(j0) * k + c0, k, CB, jb, cb, vec, acc,
+               wm, wn, lane);
+    const bool first = (I == J);
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int r = 32 * wm + 2 * (4 * v + lk) + bi;
+            if (i0 + r >= k) continue;
+            const int c = 32 * wn + 2 * l16;
+            double* dst = X + static_cast<int64_t>(i0 + r) * k + c0 + c;
+            if (vec && c + 1 < cb) {
+                f64x2 o = first ? f64x2{0.0, 0.0} : *reinterpret_cast<f64x2*>(dst);
+                o[0] += acc[bi][0][v];
+                o[1] += acc[bi][1][v];
+                *reinterpret_cast<f64x2*>(dst) = o;
+            } else {
+                if (c < cb) dst[0] = (first ? 0.0 : dst[0]) + acc[bi][0][v];
+                if (c + 1 < cb) dst[1] = (first ? 0.0 : dst[1]) + acc[bi][1][v];
+            }
+        }
 }
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
@@ -464,21 +488,19 @@ hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, dou
                            int64_t strideInv, int* defic, double* diag0, double tau_rel, int batch,
                            hipStream_t stream) {
     const int nb = (k + CB - 1) / CB;
+    const bool inv = rinv32 != nullptr;
+    hipLaunchKernelGGL(chol_diag_kernel, dim3(batch), dim3(CT), 0, stream, C, k, strideC, 0, diag0, defic, xinv,
+                       rinv32, strideInv, tau_rel);
     for (int J = 0; J < nb; ++J) {
-        hipLaunchKernelGGL(chol_diag_kernel, dim3(batch), dim3(CT), 0, stream, C, k, strideC, J, diag0,
-                           defic, xinv, rinv32, strideInv, tau_rel);
         const int n = nb - J - 1;
-        if (n > 0) {
-            hipLaunchKernelGGL(chol_panel_kernel, dim3(n, batch), dim3(CT), 0, stream, C, k, strideC, J,
-                               defic, xinv, strideInv);
-            hipLaunchKernelGGL(chol_trailing_kernel, dim3(n * (n + 1) / 2, batch), dim3(CT), 0, stream, C,
-                               k, strideC, J, nb);
-        }
-    }
-    if (rinv32 != nullptr) {
-        for (int d = 1; d < nb; ++d)
-            hipLaunchKernelGGL(chol_inverse_level_kernel, dim3(nb - d, batch), dim3(CT), 0, stream, C, k,
-                               strideC, d, xinv, rinv32, strideInv);
+        const int px = n + (inv ? J : 0);
+        if (px > 0)
+            hipLaunchKernelGGL(chol_panel_x_kernel, dim3(px, batch), dim3(CT), 0, stream, C, k, strideC, J, n, defic,
+                               xinv, rinv32, strideInv);
+        if (n > 0)
+            hipLaunchKernelGGL(chol_trailing_p_kernel, dim3(n * (n + 1) / 2 + (inv ? (J + 1) * n : 0), batch),
+                               dim3(CT), 0, stream, C, k, strideC, J, nb, diag0, defic, xinv, rinv32, strideInv,
+                               tau_rel);
     }
     return hipGetLastError();
 }
