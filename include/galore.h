@@ -108,7 +108,8 @@ GALORE_API size_t galore_rsvd_workspace_size(int64_t m, int64_t n, int32_t r, in
  * Outputs: P (fp32, s x r, ld ldp >= r, stride stride_p);
  *          sigma (fp32, r values per matrix at stride stride_sigma; may be NULL);
  *          info (device int32[batch]; may be NULL): 0 = converged; 24 = the
- *          small SVD did not converge within its sweep limit of 24 sweeps;
+ *          small SVD did not converge within its sweep limit (16 sweeps for
+ *          k = min(r + p, s) <= 2048, 24 above);
  *          25 = a column of the small SVD has a NaN or Inf norm (NaN or Inf
  *          in G): sigma and P then hold NaN or Inf and must not be used.
  *          Every non-zero value means failure. The work enqueued is bounded

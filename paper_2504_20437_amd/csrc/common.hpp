@@ -130,7 +130,8 @@ hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, in
 // 1 when matrix b has them (every column norm finite and positive; Ur is then
 // left to launch_refine), else 0
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
-                                  float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
+                                  float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int nsweeps,
+                                  int* info,
                                   double* scratch, int64_t strideScratch, const int* exps, double* norms, int* perm,
                                   float* Xa, int* flags, int batch, hipStream_t stream);
 // fp64 refinement of the small SVD's vectors (refine.hip): one Ogita-Aishima
@@ -222,5 +223,7 @@ hipError_t launch_gemm_bf16x6(const void* Aplanes, int64_t lda, int64_t planeStr
                               float alpha, float beta, int batch, hipStream_t stream);
 
 constexpr int kJacobiBlock = 32;     // columns per Jacobi block (pairs of 64)
+constexpr int kInfoSweepLimit = 24;  // info: the small SVD's sweeps ran out before a rotation-free sweep
+constexpr int kInfoNonFinite = 25;   // info: a column norm of the small SVD is NaN or Inf
 
 }  // namespace galore

@@ -17,7 +17,10 @@ using namespace galore;
 namespace {
 
 constexpr int kMaxK = 4096;          // largest sketch width supported by the small-SVD kernels
-constexpr int kMaxSweeps = 24;       // Jacobi sweep limit of the small SVD
+constexpr int kMaxSweeps = 24;       // Jacobi sweep limit of the small SVD (k > 2048)
+constexpr int kMaxSweepsSmall = 16;  // and for k <= 2048 (the workloads here converge in 6-10)
+
+int jacobi_sweeps(int k) { return k <= 2048 ? kMaxSweepsSmall : kMaxSweeps; }
 constexpr double kJacobiTol = 1e-6;  // relative off-diagonal below which a pair is orthogonal
 constexpr double kDeficTol = 1e-10;  // relative pivot below which a column is dependent
 constexpr size_t kAlign = 256;
@@ -371,7 +374,7 @@ int enqueue_jacobi_sweeps(float* Yt, int k, int64_t strideKK, int nb, int* rot, 
                           int batch, hipStream_t stream, hipStream_t aux) {
     return on_two_streams(batch, stream, aux, [&](int b0, int cnt, hipStream_t st) -> int {
         const int64_t ko = static_cast<int64_t>(b0) * k;
-        for (int sw = 0; sw < kMaxSweeps; ++sw) {
+        for (int sw = 0; sw < jacobi_sweeps(k); ++sw) {
             GALORE_TRY(launch_jacobi_order(Yt + b0 * strideKK, k, strideKK, norms + ko, jperm + ko,
                                            rot + b0 * kMaxSweeps, kMaxSweeps, sw, cnt, st));
             for (int stp = 0; stp < nb - 1; ++stp)
@@ -541,7 +544,7 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(enqueue_jacobi_sweeps(Yt, k, L.strideKK, nb, rot, w.d(L.offNorm), w.i(L.offPerm), batch, stream,
                                        aux));
     GALORE_TRY(launch_jacobi_finalize(Yt, k, L.strideKK, r, Ur, L.strideUr, sigma, stride_sigma, rot,
-                                      kMaxSweeps, info, reinterpret_cast<double*>(w.f(L.offTheta)),
+                                      kMaxSweeps, jacobi_sweeps(k), info, reinterpret_cast<double*>(w.f(L.offTheta)),
                                       L.strideTheta / 2, jexp, w.d(L.offNorm), w.i(L.offPerm), w.f(L.offRinv),
                                       w.i(L.offFlags), batch, stream));
     if (tr.end() != hipSuccess) return GALORE_ERR_HIP;

@@ -722,7 +722,7 @@ __global__ __launch_bounds__(256) void jacobi_gather_kernel(const float* Ytb, in
 __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, int k, int64_t strideX,
                                                               int r, float* Urb, int64_t strideUr,
                                                               float* sigma, int64_t stride_sigma,
-                                                              const int* rotb, int max_sweeps, int* info,
+                                                              const int* rotb, int max_sweeps, int nsweeps, int* info,
                                                               double* scratchb, int64_t strideScratch,
                                                               const int* expb, const double* normsb, int* permb,
                                                               int* flags) {
@@ -781,15 +781,16 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
         }
     }
     if (tid == 0 && info != nullptr) {
-        // 0: converged; max_sweeps: no sweep came out rotation-free;
-        // max_sweeps + 1: a column norm is NaN or Inf (non-finite input)
+        // 0: converged; kInfoSweepLimit: none of the nsweeps sweeps run came
+        // out rotation-free; kInfoNonFinite: a column norm is NaN or Inf
+        // (non-finite input)
         const int* rot = rotb + static_cast<int64_t>(b) * max_sweeps;
-        int result = max_sweeps;
-        for (int w = 0; w < max_sweeps; ++w) {
+        int result = kInfoSweepLimit;
+        for (int w = 0; w < nsweeps; ++w) {
             if (rot[w] == 0) { result = 0; break; }
         }
         for (int c = 0; c < k; ++c)
-            if (!(sig[c] <= DBL_MAX)) result = max_sweeps + 1;
+            if (!(sig[c] <= DBL_MAX)) result = kInfoNonFinite;
         info[b] = result;
     }
     if (nkeep >= r) return;
@@ -895,14 +896,16 @@ hipError_t launch_jacobi_step(float* Yt, int k, int64_t strideX, int nblocks, in
 }
 
 hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r, float* Ur, int64_t strideUr,
-                                  float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int* info,
+                                  float* sigma, int64_t stride_sigma, const int* rot, int max_sweeps, int nsweeps,
+                                  int* info,
                                   double* scratch, int64_t strideScratch, const int* exps, double* norms,
                                   int* perm, float* Xa, int* flags, int batch, hipStream_t stream) {
     hipLaunchKernelGGL(jacobi_norms_kernel, dim3((k + 3) / 4, batch), dim3(256), 0, stream, Yt, k, strideX, norms,
                        static_cast<const int*>(nullptr), 0, 0);
     const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
     hipLaunchKernelGGL(jacobi_finalize_kernel, dim3(batch), dim3(256), shmem, stream, Yt, k, strideX, r, Ur,
-                       strideUr, sigma, stride_sigma, rot, max_sweeps, info, scratch, strideScratch, exps, norms,
+                       strideUr, sigma, stride_sigma, rot, max_sweeps, nsweeps, info, scratch, strideScratch, exps,
+                       norms,
                        perm, flags);
     if (Xa != nullptr)
         hipLaunchKernelGGL(jacobi_gather_kernel, dim3(k, batch), dim3(256), 0, stream, Yt, k, strideX, norms, perm,
