@@ -146,6 +146,65 @@ def test_bench_inputs_match_oracle(gl, orc, m, n, r, p, q, expo, seed):
     assert orth_err(Ph[0]) < 1e-4
 
 
+def test_bench_launch_configuration(gl):
+    """The headline benchmark's own launch: the 64 gate/up-shaped gradients of
+    its generator (4096 x 11008 bf16, seed 5000), one batched update with the
+    second stream (r = 1024, p = 32, q = 2), then projection, Adam step and
+    weight update with workspaces, as bench.py times them. All 64: info 0, P
+    orthonormal, sigma descending and positive; matrices 0, 31, 32 and 63 equal
+    bit for bit to their updates run alone (one matrix, one stream; matrix 0
+    alone is held to the oracle by test_bench_inputs_match_oracle, on the same
+    bits); projection and weight change of matrices 0 and 63 on sampled entries
+    against host fp64."""
+    import torch
+    m, n, r, p, q, B = 4096, 11008, 1024, 32, 2, 64
+    G = gi.torch_planted_group(m, n, B, gi.spectrum_power(m, 0.7), 1e-4, seed=5000, dtype="bf16")
+    aux = torch.cuda.Stream()
+    ws = torch.empty((gl.galore_rsvd_workspace_size(m, n, r, p, B, G.dtype),), dtype=torch.uint8, device="cuda")
+    P, sig, info = gl.galore_rsvd_update(G, r, p, q, gi.sketch_seed(0), 0, workspace=ws, aux_stream=aux)
+    torch.cuda.synchronize()
+    del ws
+    assert int((info != 0).sum()) == 0
+    PtP = torch.bmm(P.transpose(1, 2).contiguous(), P)
+    PtP -= torch.eye(r, device=P.device)
+    assert float(PtP.abs().max()) < 1e-4
+    del PtP
+    sh = host(sig)
+    assert np.all(sh > 0)
+    assert np.all(np.diff(sh, axis=1) <= 1e-6 * sh[:, :1])
+    for b in (0, 31, 32, 63):
+        P1, s1, i1 = gl.galore_rsvd_update(G[b:b + 1], r, p, q, gi.sketch_seed(0), b)
+        torch.cuda.synchronize()
+        assert int(i1[0]) == 0
+        assert torch.equal(P1[0], P[b]) and torch.equal(s1[0], sig[b]), b
+    # the per-step path of the bench, with its workspaces
+    R = torch.empty((B, r, n), dtype=torch.float32, device="cuda")
+    pws = torch.empty((gl.galore_project_workspace_size(m, n, r, B, G.dtype),), dtype=torch.uint8, device="cuda")
+    gl.galore_project(P, G, R=R, workspace=pws)
+    del pws
+    M = torch.zeros_like(R)
+    V = torch.zeros_like(R)
+    N = gl.galore_lowrank_adam_step(R, M, V, None, 0.9, 0.999, 1e-8, 1)
+    W = torch.zeros((B, m, n), dtype=torch.float32, device="cuda")
+    bws = torch.empty((gl.galore_project_back_workspace_size(m, n, r, B),), dtype=torch.uint8, device="cuda")
+    gl.galore_project_back(P, N, W, 1e-3, 0.25, workspace=bws)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(64)
+    c = float(np.float32(1e-3)) * float(np.float32(0.25))
+    for b in (0, 63):
+        Ph = host(P[b])
+        Gx = G[b].float().cpu().numpy().astype(np.float64)
+        Rb, Nb, Wb = host(R[b]), host(N[b]), host(W[b])
+        ii, jj = rng.integers(0, r, 64), rng.integers(0, n, 64)
+        ref = np.array([Ph[:, i] @ Gx[:, j] for i, j in zip(ii, jj)])
+        assert max_rel_violation(Rb[ii, jj], ref, 1e-5, 1e-6) <= 1.0
+        wi, wj = rng.integers(0, m, 64), rng.integers(0, n, 64)
+        pr = [(Ph[i, :], Nb[:, j]) for i, j in zip(wi, wj)]
+        dref = np.array([-c * (x @ y) for x, y in pr])
+        bound = np.array([c * (np.abs(x) @ np.abs(y)) for x, y in pr])
+        assert np.all(np.abs(Wb[wi, wj] - dref) <= 1e-5 * bound + 2.0 ** -24 * np.abs(Wb[wi, wj]))
+
+
 def test_exact_svd_full_size(gl):
     """The exact-SVD projector at the bench's shape (4096 x 11008 bf16,
     (i+1)^-0.7 spectrum + 1e-4 noise, r = 1024, so k = s = 4096): sigma against
