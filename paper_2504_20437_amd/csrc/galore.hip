@@ -21,7 +21,11 @@ constexpr int kMaxSweeps = 24;       // Jacobi sweep limit of the small SVD (k >
 constexpr int kMaxSweepsSmall = 16;  // and for k <= 2048 (the workloads here converge in 6-10)
 
 int jacobi_sweeps(int k) { return k <= 2048 ? kMaxSweepsSmall : kMaxSweeps; }
-constexpr double kJacobiTol = 1e-6;  // relative off-diagonal below which a pair is orthogonal
+// relative off-diagonal below which a pair is orthogonal: well above the
+// rounding of the pair Gram (fp32 plane products, about 1e-7), and small
+// enough that the fp64 refinement step that follows, whose error is quadratic
+// in what the sweeps leave, ends below the fp32 rounding of the projector
+constexpr double kJacobiTol = 1e-5;
 constexpr double kDeficTol = 1e-10;  // relative pivot below which a column is dependent
 constexpr size_t kAlign = 256;
 
