@@ -69,42 +69,73 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* src
 
 // --------------------------------------------------------------------------
 // plane_p (cols x rows, ld ldp) = split_p(src)^T, src fp32 rows x cols (ld lds);
-// planes at planeStride elements from each other; rows..ldp-1 zero-filled
+// planes at planeStride elements from each other; rows..rows_pad-1 zero-filled.
+// No LDS: in a 64 x 64 tile, thread t takes the 4 x 4 block of columns
+// 4 (t >> 4) .. + 3 and rows 4 (t & 15) .. + 3 (four 16-byte row loads) and
+// writes, per plane and column, its four rows as one 8-byte store, so that the
+// 16 threads of a column quad fill 128 contiguous bytes of each plane row
+// (measured: 911 us per launch of the headline step's mix against 982 us for
+// 128-row x 32-column tiles and 1076 us for the LDS transpose it replaced).
 // --------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void split3_transpose_kernel(const float* srcb, int64_t lds, int64_t strideS,
                                                                uint16_t* planesb, int64_t ldp, int64_t planeStride,
                                                                int64_t strideP, int rows, int cols, int rows_pad,
-                                                               const float* rowscaleb, int64_t strideRS) {
-    __shared__ float tile[64][65];
+                                                               const float* rowscaleb, int64_t strideRS, int vload,
+                                                               int vstore) {
     const int b = blockIdx.z;
     const float* src = srcb + static_cast<int64_t>(b) * strideS;
     uint16_t* planes = planesb + static_cast<int64_t>(b) * strideP;
     const float* rowscale = rowscaleb ? rowscaleb + static_cast<int64_t>(b) * strideRS : nullptr;
-    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int i = ty; i < 64; i += 4) {
-        const int r = r0 + i, c = c0 + tx;
-        float x = 0.0f;
-        if (r < rows && c < cols) {
-            x = src[static_cast<int64_t>(r) * lds + c];
-            if (rowscale) x *= rowscale[r];     // one fp32 rounding, then an exact split
+    const int c0 = blockIdx.x * 64 + 4 * (threadIdx.x >> 4);
+    const int rb = blockIdx.y * 64 + 4 * (threadIdx.x & 15);
+    if (c0 >= cols || rb >= rows_pad) return;
+    float x[4][4];   // [row][column]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = rb + i;
+        const float* row = src + static_cast<int64_t>(r) * lds + c0;
+        if (r < rows && vload && c0 + 4 <= cols) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(row);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[i][e] = v[e];
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[i][e] = (r < rows && c0 + e < cols) ? row[e] : 0.0f;
         }
-        tile[i][tx] = x;
+        if (rowscale && r < rows) {
+            const float sc = rowscale[r];   // one fp32 rounding, then an exact split
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[i][e] *= sc;
+        }
     }
-    __syncthreads();
-    for (int i = ty; i < 64; i += 4) {
-        const int c = c0 + i, r = r0 + tx;
-        if (c < cols && r < rows_pad) {
-            const float x = tile[tx][i];
-            const uint16_t h1 = bf16_bits_rn(x);
-            const float r1 = x - bf16_bits_to_f32(h1);
-            const uint16_t h2 = bf16_bits_rn(r1);
-            const float r2 = r1 - bf16_bits_to_f32(h2);
-            const uint16_t h3 = bf16_bits_rn(r2);
-            const int64_t o = static_cast<int64_t>(c) * ldp + r;
-            planes[o] = h1;
-            planes[o + planeStride] = h2;
-            planes[o + 2 * planeStride] = h3;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int c = c0 + e;
+        if (c >= cols) break;
+        uint16_t h[3][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float v = x[i][e];
+            h[0][i] = bf16_bits_rn(v);
+            const float r1 = v - bf16_bits_to_f32(h[0][i]);
+            h[1][i] = bf16_bits_rn(r1);
+            const float r2 = r1 - bf16_bits_to_f32(h[1][i]);
+            h[2][i] = bf16_bits_rn(r2);
+        }
+        uint16_t* dst = planes + static_cast<int64_t>(c) * ldp + rb;
+        if (vstore && rb + 4 <= rows_pad) {
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+                *reinterpret_cast<uint2*>(dst + p * planeStride) =
+                    make_uint2(h[p][0] | (static_cast<uint32_t>(h[p][1]) << 16),
+                               h[p][2] | (static_cast<uint32_t>(h[p][3]) << 16));
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (rb + i < rows_pad) {
+#pragma unroll
+                    for (int p = 0; p < 3; ++p) dst[p * planeStride + i] = h[p][i];
+                }
         }
     }
 }
@@ -612,10 +643,16 @@ hipError_t launch_transpose_bf16(const void* src, int64_t lds, int64_t strideS, 
 hipError_t launch_split3_transpose(const float* src, int64_t lds, int64_t strideS, void* planes, int64_t ldp,
                                    int64_t planeStride, int64_t strideP, int rows, int cols, int rows_pad,
                                    int batch, hipStream_t stream, const float* rowscale, int64_t strideRS) {
+    if (rows <= 0 || cols <= 0 || rows_pad <= 0 || batch <= 0) return hipSuccess;
+    // 16-byte row loads and 8-byte plane stores where every row start is aligned
+    const int vload = (lds % 4 == 0) && (batch == 1 || strideS % 4 == 0) &&
+                      (reinterpret_cast<uintptr_t>(src) % 16 == 0);
+    const int vstore = (ldp % 4 == 0) && (planeStride % 4 == 0) && (batch == 1 || strideP % 4 == 0) &&
+                       (reinterpret_cast<uintptr_t>(planes) % 8 == 0);
     dim3 grid((cols + 63) / 64, (rows_pad + 63) / 64, batch);
     hipLaunchKernelGGL(split3_transpose_kernel, grid, dim3(256), 0, stream, src, lds, strideS,
                        static_cast<uint16_t*>(planes), ldp, planeStride, strideP, rows, cols, rows_pad, rowscale,
-                       strideRS);
+                       strideRS, vload, vstore);
     return hipGetLastError();
 }
 
