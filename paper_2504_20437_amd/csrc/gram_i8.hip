@@ -27,8 +27,9 @@
 //             so that the Gram reads K-contiguous 16-byte fragments;
 //   gram      128 x 128 tiles of the upper triangle, 8 waves of 32 x 64, nine
 //             v_mfma_i32_32x32x32_i8 per 32 x 32 block and 32 rows of X, digit
-//             rows staged through LDS by direct loads, 64 rows per stage, the
-//             next stage in flight while the current one is multiplied.
+//             rows staged through LDS by direct buffer loads (32-bit lane
+//             offsets), 64 rows per stage, the next stage in flight while the
+//             current one is multiplied.
 // Only the upper triangle of C (blocks on or above the diagonal) is written:
 // the Cholesky factorisation reads nothing else.
 #include "common.hpp"
@@ -139,11 +140,12 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* Xb, int64_t 
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 
-// one 16-byte direct load per lane into LDS (lane i writes bytes 16 i .. of the wave's 1 KB)
-__device__ __forceinline__ void load_lds16(const void* src, void* lds_base) {
-    __builtin_amdgcn_global_load_lds((glb_void_t*)src, (lds_void_t*)lds_base, 16, 0, 0);
+// one 16-byte buffer load per lane into LDS (lane i writes bytes 16 i .. of the
+// wave's 1 KB); byte address voff + soff within the buffer
+constexpr int kBufferDword3 = 0x00020000;   // raw buffer: 32-bit data format, no swizzle
+__device__ __forceinline__ void buffer_load_lds16(__amdgpu_buffer_rsrc_t rsrc, int voff, int soff, void* lds_base) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)lds_base, 16, voff, soff, 0, 0);
 }
 
 constexpr int GK = 64;                   // rows of X (contraction) per LDS stage
@@ -151,6 +153,13 @@ constexpr int kPlaneB = GT * GK;         // one plane of one side in a stage (8 
 constexpr int kSideB = 3 * kPlaneB;      // three planes (24 KB)
 constexpr int kStageB = 2 * kSideB;      // p side and q side (48 KB)
 constexpr int kSegStages = 1016;         // stages per exact int32 segment (65024 rows)
+// stages in LDS (two or three: 96 or 144 KB); measured on the headline step,
+// 2466 us per launch with two against 2496 with three
+#ifndef GALORE_GRAM_STAGES
+#define GALORE_GRAM_STAGES 2
+#endif
+constexpr int kGramStages = GALORE_GRAM_STAGES;
+static_assert(kGramStages == 2 || kGramStages == 3, "two or three Gram stages");
 
 // Upper GT x GT tiles (u <= v) of C, one workgroup of 8 waves each: wave
 // (wm, wn) owns rows 32 wm .. + 31 and columns 64 wn .. + 63 of the tile (two
@@ -159,11 +168,11 @@ constexpr int kSegStages = 1016;         // stages per exact int32 segment (6502
 // (three digit planes each; a diagonal tile loads the p side only) through
 // direct loads; a digit row's four 16-byte chunks sit at slot
 // chunk ^ ((row / 4) % 4), so the 16 lanes of a fragment read hit 64 distinct
-// banks. Next stage in flight while the current one is multiplied.
+// banks. The next stage in flight while the current one is multiplied.
 __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64_t ldq, int64_t planeStride,
                                                          int64_t strideD, const unsigned* cmaxb, int64_t strideCM,
                                                          double* Cb, int64_t ldc, int64_t strideC, int cols, int nt) {
-    __shared__ __attribute__((aligned(16))) int8_t sm[2 * kStageB];
+    __shared__ __attribute__((aligned(16))) int8_t sm[kGramStages * kStageB];
     const int ntiles = nt * (nt + 1) / 2;
     const int logical = xcd_logical_id(blockIdx.x + ntiles * blockIdx.y, ntiles * gridDim.y);
     const int b = logical / ntiles;
@@ -196,6 +205,11 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
         const int chunk = (lane & 3) ^ ((lane >> 4) & 3);          // (rloc / 4) % 4 == (lane / 16) % 4
         src[i] = static_cast<int>(pl * planeStride + static_cast<int64_t>(row) * ldq) + 16 * chunk;
     }
+    // the matrix's digit planes as one buffer (strideD < 2^31 bytes): 32-bit
+    // lane offsets and a scalar stage offset, so no 64-bit lane addresses are
+    // kept in registers
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(D), 0, static_cast<int>(strideD), kBufferDword3);
     const int qside = diag ? 0 : kSideB;
     const int KT = static_cast<int>(ldq / GK);
 
@@ -213,21 +227,30 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
                 for (int r = 0; r < 16; ++r) acc[w][y][r] = 0;
         auto issue = [&](int buf, int kt) {
             int8_t* base = sm + buf * kStageB;
-            const int64_t off = static_cast<int64_t>(kt) * GK;
 #pragma unroll
             for (int i = 0; i < 6; ++i) {
                 const int j = 6 * wave + i;     // LDS destination: side j / 24, plane (j / 8) % 3, rows 16 (j % 8) ..
                 if (i < nload)
-                    load_lds16(D + src[i] + off, base + (j / 24) * kSideB + ((j / 8) % 3) * kPlaneB + (j % 8) * 1024);
+                    buffer_load_lds16(rsrc, src[i], kt * GK,
+                                      base + (j / 24) * kSideB + ((j / 8) % 3) * kPlaneB + (j % 8) * 1024);
             }
         };
         __syncthreads();                       // the previous segment's last stage is read
-        issue(0, sg);
+#pragma unroll
+        for (int st = 0; st < kGramStages - 1; ++st)
+            if (sg + st < se) issue(st, sg + st);
         for (int kt = sg; kt < se; ++kt) {
-            asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-            if (kt + 1 < se) issue((kt + 1 - sg) & 1, kt + 1);
+            // stage kt landed (a wave issues 6 or no loads per stage, so with
+            // the next stage already in flight at most 6 may stay outstanding),
+            // then for every wave; past the barrier every wave has also
+            // finished stage kt - 1, whose buffer the next issue refills
+            if (kGramStages == 3 && kt + 1 < se)
+                asm volatile("s_waitcnt vmcnt(6)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+            else
+                asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+            if (kt + kGramStages - 1 < se) issue((kt + kGramStages - 1 - sg) % kGramStages, kt + kGramStages - 1);
             if (idle) continue;
-            const int8_t* sp = sm + ((kt - sg) & 1) * kStageB;
+            const int8_t* sp = sm + ((kt - sg) % kGramStages) * kStageB;
             const int8_t* sq = sp + qside;
 #pragma unroll 1
             for (int ks = 0; ks < 2; ++ks) {
