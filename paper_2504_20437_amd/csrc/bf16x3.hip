@@ -387,6 +387,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
     static_assert(!AT || YK == 32, "the M-contiguous A stage assumes 32-deep stages");
     static_assert(PA == 1 || (PA == 3 && !AT), "three A planes are K-contiguous");
     static_assert(PB == 3 || (PB == 1 && PA == 1), "one B plane pairs with one A plane");
+    constexpr int kFragBufs = AT ? 2 : 1;               // fragment register buffers (see the main loop)
     constexpr int CPR = YK / 8;                          // 16-byte chunks per row
     constexpr int RB = YK * 2;                           // bytes per row
     constexpr int kStageA = PA * YM * RB;
@@ -475,13 +476,12 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
         // every wave has also finished iteration kt - 1, so its stage is refilled
         wait_stages<LA + LB, S>(min(S - 2, KT - 1 - kt));
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
         const unsigned char* sa = ysm + (kt % S) * kStage;
         const unsigned char* sb = sa + kStageA;
-#pragma unroll
-        for (int ks = 0; ks < YK / 16; ++ks) {
+        // fragments of 16-deep step ks into register buffer fb
+        bf16x8 a[kFragBufs][PA][4], bq[kFragBufs][PB][2];
+        auto fetch = [&](int fb, int ks) {
             const int c = 2 * ks + lk;
-            bf16x8 a[PA][4], bq[PB][2];
 #pragma unroll
             for (int x = 0; x < 4; ++x) {
                 if constexpr (AT) {
@@ -501,13 +501,13 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
                                 reinterpret_cast<__attribute__((address_space(3))) unsigned char*>(
                                     reinterpret_cast<size_t>(sa)) + off));
                     }
-                    a[0][x] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
+                    a[fb][0][x] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
                 } else {
                     const int r = wm * 128 + 32 * x + l32;
 #pragma unroll
                     for (int pa = 0; pa < PA; ++pa)
-                        a[pa][x] = *reinterpret_cast<const bf16x8*>(sa + pa * (YM * RB) + r * RB +
-                                                                    16 * (c ^ ((r / RPB) % CPR)));
+                        a[fb][pa][x] = *reinterpret_cast<const bf16x8*>(sa + pa * (YM * RB) + r * RB +
+                                                                        16 * (c ^ ((r / RPB) % CPR)));
                 }
             }
 #pragma unroll
@@ -515,9 +515,11 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
 #pragma unroll
                 for (int y = 0; y < 2; ++y) {
                     const int r = wn * 64 + 32 * y + l32;
-                    bq[p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * RB) + r * RB +
-                                                                16 * (c ^ ((r / RPB) % CPR)));
+                    bq[fb][p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * RB) + r * RB +
+                                                                    16 * (c ^ ((r / RPB) % CPR)));
                 }
+        };
+        auto multiply = [&](int fb) {
             if constexpr (PA == 1) {
 #pragma unroll
                 for (int p = 0; p < PB; ++p)
@@ -525,7 +527,8 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
                     for (int x = 0; x < 4; ++x)
 #pragma unroll
                         for (int y = 0; y < 2; ++y)
-                            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][x], bq[p][y], acc[x][y], 0, 0, 0);
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[fb][0][x], bq[fb][p][y], acc[x][y],
+                                                                                 0, 0, 0);
             } else {
                 constexpr int pairs[6][2] = {{0, 0}, {0, 1}, {1, 0}, {0, 2}, {1, 1}, {2, 0}};
 #pragma unroll
@@ -534,8 +537,37 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
                     for (int x = 0; x < 4; ++x)
 #pragma unroll
                         for (int y = 0; y < 2; ++y)
-                            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pairs[q][0]][x], bq[pairs[q][1]][y],
-                                                                                 acc[x][y], 0, 0, 0);
+                            acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                a[fb][pairs[q][0]][x], bq[fb][pairs[q][1]][y], acc[x][y], 0, 0, 0);
+            }
+        };
+        if constexpr (AT) {
+            // the compiler cannot tell the transposing LDS reads from the LDS
+            // that the direct loads in flight may write, and before any such
+            // read issued after those loads it waits for all of them (a whole
+            // memory latency per stage). So the stage's two steps are read
+            // before the next stage's loads are issued: step 0's fragments,
+            // its MFMAs, step 1's fragments while they run, then the loads,
+            // then step 1's MFMAs (measured: 15.9 against 17.9 ms per launch
+            // of 64 A^T Q products with the loads first, 16.6 with all reads
+            // before any MFMA). The K-contiguous variant keeps the compiler's
+            // interleaving of reads and MFMAs (an explicit two-step order
+            // measured 18.8 against 17.8 ms).
+            fetch(0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            multiply(0);
+            __builtin_amdgcn_sched_barrier(0);
+            fetch(1, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
+            __builtin_amdgcn_sched_barrier(0);
+            multiply(1);
+        } else {
+            if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
+#pragma unroll
+            for (int ks = 0; ks < YK / 16; ++ks) {
+                fetch(0, ks);
+                multiply(0);
             }
         }
     }
