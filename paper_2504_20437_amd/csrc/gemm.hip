@@ -188,16 +188,26 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
             load_a((kt + 1) * BK);
             load_b((kt + 1) * BK);
         }
+        // operands of step kk + 2 read while step kk's MFMAs run (two
+        // register sets): the matrix pipe does not wait for the LDS between
+        // steps
+        float fa[2][2], fb[2][2];
+        auto read_step = [&](int fbuf, int kk) {
+            fa[fbuf][0] = As[cur][kk + lk][wm * 64 + lrow];
+            fa[fbuf][1] = As[cur][kk + lk][wm * 64 + 32 + lrow];
+            fb[fbuf][0] = Bs[cur][kk + lk][wn * 64 + lrow];
+            fb[fbuf][1] = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
+        };
+        read_step(0, 0);
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 2) {
-            const float a0 = As[cur][kk + lk][wm * 64 + lrow];
-            const float a1 = As[cur][kk + lk][wm * 64 + 32 + lrow];
-            const float b0 = Bs[cur][kk + lk][wn * 64 + lrow];
-            const float b1 = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            const int fbuf = (kk >> 1) & 1;
+            if (kk + 2 < BK) read_step(fbuf ^ 1, kk + 2);
+            __builtin_amdgcn_sched_barrier(0);
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][0], acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][1], acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][0], acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][1], acc[1][1], 0, 0, 0);
         }
         if (more) {
             store_a(cur ^ 1);
