@@ -32,8 +32,10 @@
 // row-major upper triangle left by the Cholesky (the lower triangle holds
 // stale data and is masked); T is stored as T^T; S and G are full symmetric;
 // E is stored transposed (Et[j][i] = E_ij).
-// The products run on the fp64 matrix cores (v_mfma_f64_16x16x4f64) in 96 x 96
-// output tiles staged through LDS (below).
+// T, S and G are formed on the fp64 matrix cores (v_mfma_f64_16x16x4f64), the
+// two updates' small correction sums on the fp32 ones (v_mfma_f32_16x16x4f32,
+// see refine_update_kernel), all in 96 x 96 output tiles staged through LDS
+// (below).
 #include <float.h>
 
 #include "common.hpp"
@@ -88,13 +90,15 @@ __device__ __forceinline__ f64x4 quad_at(const T* M, int64_t ld, int row, int t,
     return p;
 }
 
-// acc[x][y] += sum over the chunk in LDS (As[t][m], Bs[t][n])
-__device__ __forceinline__ void q_mma(const double* As, const double* Bs, f64x4 acc[3][3], int wm, int wn, int lane) {
+// acc[x][y] += sum over the chunk in LDS (As[t][m], Bs[t][n]); fp64 or fp32
+// matrix cores by the element type
+template <typename T, typename V>
+__device__ __forceinline__ void q_mma(const T* As, const T* Bs, V acc[3][3], int wm, int wn, int lane) {
     const int l16 = lane & 15, g = lane >> 4;
 #pragma unroll
     for (int s = 0; s < QK / 4; ++s) {
         const int t = 4 * s + g;
-        double a[3], b[3];
+        T a[3], b[3];
 #pragma unroll
         for (int x = 0; x < 3; ++x) {
             a[x] = As[t * QP + 48 * wm + 16 * x + l16];
@@ -103,8 +107,12 @@ __device__ __forceinline__ void q_mma(const double* As, const double* Bs, f64x4 
 #pragma unroll
         for (int x = 0; x < 3; ++x)
 #pragma unroll
-            for (int y = 0; y < 3; ++y)
-                acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b[y], acc[x][y], 0, 0, 0);
+            for (int y = 0; y < 3; ++y) {
+                if constexpr (sizeof(T) == 8)
+                    acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b[y], acc[x][y], 0, 0, 0);
+                else
+                    acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[x], b[y], acc[x][y], 0, 0, 0);
+            }
     }
 }
 
@@ -247,6 +255,14 @@ __global__ __launch_bounds__(256) void refine_e_kernel(const double* Sb, const d
 // pitch ldm). With Ur != nullptr the result is written transposed,
 // Ur[a][j] (row pitch ldu), instead of into Xn. 96 x 96 tiles as above: A = M
 // (contraction index contiguous), B = X (rows of the contraction index).
+// P = float: the correction sum runs on the fp32 matrix cores (twice the fp64
+// rate). M - shift I is formed in fp64 and then rounded to fp32; both updates
+// of a step apply a small correction (entries of E are at most 0.1 and of
+// order 1e-5 outside near-equal pairs; D - I is the orthogonality error), so
+// the fp32 sum's error, of order 2^-24 sum_i |M - shift I|_ji |X_ia|, stays far
+// under the fp32 rounding of X itself, to which the sum is added once, in
+// fp64, before the result is rounded to fp32.
+template <typename P>
 __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, int64_t strideM, int64_t ldm,
                                                             const float* Xb, int64_t strideX, float* Xnb, int nn,
                                                             int kc, int64_t ld, double alpha, double shift,
@@ -257,8 +273,8 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
     const int ntm = (nn + QT - 1) / QT, ntn = (kc + QT - 1) / QT;
     const int tm = blockIdx.x / ntn, tn = blockIdx.x % ntn;
     if (tm >= ntm) return;
-    __shared__ __attribute__((aligned(16))) double As[QK * QP];
-    __shared__ __attribute__((aligned(16))) double Bs[QK * QP];
+    __shared__ __attribute__((aligned(16))) P As[QK * QP];
+    __shared__ __attribute__((aligned(16))) P Bs[QK * QP];
     const double* M = Mb + static_cast<int64_t>(b) * strideM;
     const float* X = Xb + static_cast<int64_t>(b) * strideX;
     const int m0 = QT * tm, n0 = QT * tn;
@@ -289,18 +305,25 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
             int row, tq;
             q_item(tid, e, row, tq);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) As[(4 * tq + v) * QP + row] = ra[e][v];
+            for (int v = 0; v < 4; ++v) As[(4 * tq + v) * QP + row] = static_cast<P>(ra[e][v]);
             const int q = tid + 256 * e;
             const int bt = q / (QT / 4), bg = q - bt * (QT / 4);
-            *reinterpret_cast<f64x2*>(&Bs[bt * QP + 4 * bg]) = f64x2{rb[e][0], rb[e][1]};
-            *reinterpret_cast<f64x2*>(&Bs[bt * QP + 4 * bg + 2]) = f64x2{rb[e][2], rb[e][3]};
+            if constexpr (sizeof(P) == 8) {
+                *reinterpret_cast<f64x2*>(&Bs[bt * QP + 4 * bg]) = f64x2{rb[e][0], rb[e][1]};
+                *reinterpret_cast<f64x2*>(&Bs[bt * QP + 4 * bg + 2]) = f64x2{rb[e][2], rb[e][3]};
+            } else {
+                *reinterpret_cast<f32x4*>(&Bs[bt * QP + 4 * bg]) =
+                    f32x4{static_cast<float>(rb[e][0]), static_cast<float>(rb[e][1]), static_cast<float>(rb[e][2]),
+                          static_cast<float>(rb[e][3])};
+            }
         }
     };
-    f64x4 acc[3][3];
+    typedef P pv4 __attribute__((ext_vector_type(4)));
+    pv4 acc[3][3];
 #pragma unroll
     for (int x = 0; x < 3; ++x)
 #pragma unroll
-        for (int y = 0; y < 3; ++y) acc[x][y] = f64x4{0.0, 0.0, 0.0, 0.0};
+        for (int y = 0; y < 3; ++y) acc[x][y] = pv4{P(0), P(0), P(0), P(0)};
     fetch(0);
     for (int t0 = 0; t0 < nn; t0 += QK) {
         stash();
@@ -316,11 +339,13 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
         for (int y = 0; y < 3; ++y)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int row = m0 + 48 * wm + 16 * x + 4 * v + g;
+                // register v of a 16 x 16 block: row 4 v + g (fp64), 4 g + v (fp32)
+                const int row = m0 + 48 * wm + 16 * x + ((sizeof(P) == 8) ? 4 * v + g : 4 * g + v);
                 const int col = n0 + 48 * wn + 16 * y + l16;
                 if (row < nn && col < kc) {
                     const int64_t o = static_cast<int64_t>(row) * ld + col;
-                    const float val = static_cast<float>(static_cast<double>(X[o]) + alpha * acc[x][y][v]);
+                    const float val = static_cast<float>(static_cast<double>(X[o]) +
+                                                         alpha * static_cast<double>(acc[x][y][v]));
                     if (Urb != nullptr)
                         Urb[static_cast<int64_t>(b) * strideUr + static_cast<int64_t>(col) * ldu + row] = val;
                     else
@@ -387,8 +412,8 @@ hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb,
     const int64_t kk = static_cast<int64_t>(k) * k;
     hipLaunchKernelGGL(refine_e_kernel, dim3(static_cast<unsigned>((kk + 255) / 256), batch), dim3(256), 0, stream, S,
                        G, strideKK, lam, T, k, flags);
-    hipLaunchKernelGGL(refine_update_kernel, full, dim3(256), 0, stream, T, strideKK, static_cast<int64_t>(k), Xa,
-                       strideX, Xb, k, k, static_cast<int64_t>(k), 1.0, 0.0, static_cast<float*>(nullptr),
+    hipLaunchKernelGGL(refine_update_kernel<float>, full, dim3(256), 0, stream, T, strideKK, static_cast<int64_t>(k),
+                       Xa, strideX, Xb, k, k, static_cast<int64_t>(k), 1.0, 0.0, static_cast<float*>(nullptr),
                        static_cast<int64_t>(0), static_cast<int64_t>(0), flags);
     // the r vectors of largest lambda, in order, into the rows of Xa
     hipLaunchKernelGGL(refine_rank_kernel, dim3(batch), dim3(256), static_cast<size_t>(k) * sizeof(double), stream,
@@ -398,9 +423,9 @@ hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb,
     const dim3 upper_r(ntr * (ntr + 1) / 2, batch), full_r(ntr * nt, batch);
     hipLaunchKernelGGL((refine_nt_kernel<float, float, false, true>), upper_r, dim3(256), 0, stream, Xa, strideX, Xa,
                        strideX, S, strideKK, r, k, static_cast<int64_t>(k), static_cast<int64_t>(r), flags);
-    hipLaunchKernelGGL(refine_update_kernel, full_r, dim3(256), 0, stream, S, strideKK, static_cast<int64_t>(r), Xa,
-                       strideX, static_cast<float*>(nullptr), r, k, static_cast<int64_t>(k), -0.5, 1.0, Ur, strideUr,
-                       static_cast<int64_t>(r), flags);
+    hipLaunchKernelGGL(refine_update_kernel<float>, full_r, dim3(256), 0, stream, S, strideKK,
+                       static_cast<int64_t>(r), Xa, strideX, static_cast<float*>(nullptr), r, k,
+                       static_cast<int64_t>(k), -0.5, 1.0, Ur, strideUr, static_cast<int64_t>(r), flags);
     return hipGetLastError();
 }
 
