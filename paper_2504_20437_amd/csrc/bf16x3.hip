@@ -387,7 +387,11 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
     static_assert(!AT || YK == 32, "the M-contiguous A stage assumes 32-deep stages");
     static_assert(PA == 1 || (PA == 3 && !AT), "three A planes are K-contiguous");
     static_assert(PB == 3 || (PB == 1 && PA == 1), "one B plane pairs with one A plane");
-    constexpr int kFragBufs = AT ? 2 : 1;               // fragment register buffers (see the main loop)
+    // the stage's two steps read and multiplied in order, the next stage's
+    // loads issued after the reads (see the main loop): needed with the
+    // transposing reads, and faster for three B planes either way
+    constexpr bool kSplit = AT || (PA == 1 && PB == 3 && YK == 32);
+    constexpr int kFragBufs = kSplit ? 2 : 1;           // fragment register buffers
     constexpr int CPR = YK / 8;                          // 16-byte chunks per row
     constexpr int RB = YK * 2;                           // bytes per row
     constexpr int kStageA = PA * YM * RB;
@@ -541,18 +545,18 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
                                 a[fb][pairs[q][0]][x], bq[fb][pairs[q][1]][y], acc[x][y], 0, 0, 0);
             }
         };
-        if constexpr (AT) {
+        if constexpr (kSplit) {
             // the compiler cannot tell the transposing LDS reads from the LDS
             // that the direct loads in flight may write, and before any such
             // read issued after those loads it waits for all of them (a whole
             // memory latency per stage). So the stage's two steps are read
             // before the next stage's loads are issued: step 0's fragments,
             // its MFMAs, step 1's fragments while they run, then the loads,
-            // then step 1's MFMAs (measured: 15.9 against 17.9 ms per launch
-            // of 64 A^T Q products with the loads first, 16.6 with all reads
-            // before any MFMA). The K-contiguous variant keeps the compiler's
-            // interleaving of reads and MFMAs (an explicit two-step order
-            // measured 18.8 against 17.8 ms).
+            // then step 1's MFMAs (measured per launch of 64 products: A^T Q
+            // 15.9 against 17.9 ms with the loads first and 16.6 with all reads
+            // before any MFMA; A X 16.9 against 17.8 ms with the compiler's
+            // interleaving; the one-plane sketch product is faster with the
+            // latter, 8.2 against 9.1 ms, and keeps it).
             fetch(0, 0);
             __builtin_amdgcn_sched_barrier(0);
             multiply(0);
