@@ -333,23 +333,60 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
         __syncthreads();
     }
     const int l16 = lane & 15, g = lane >> 4;
+    // register v of a 16 x 16 block: row 4 v + g (fp64), 4 g + v (fp32)
+    auto out_row = [&](int x, int v) { return m0 + 48 * wm + 16 * x + ((sizeof(P) == 8) ? 4 * v + g : 4 * g + v); };
+    auto out_col = [&](int y) { return n0 + 48 * wn + 16 * y + l16; };
+    // the lane's 36 values of X read together before any store (one memory
+    // latency, not one per value); outside the nn x kc block they read its
+    // last row or column, whose values are not stored
+    float xo[3][3][4];
+#pragma unroll
+    for (int x = 0; x < 3; ++x)
+#pragma unroll
+        for (int y = 0; y < 3; ++y)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                xo[x][y][v] = X[static_cast<int64_t>(min(out_row(x, v), nn - 1)) * ld + min(out_col(y), kc - 1)];
+    // a tile inside the block stores without per-value branches (the two
+    // choices below are uniform): at the joins of such branches the compiler
+    // waits for every memory operation in flight again
+    auto value = [&](int x, int y, int v) {
+        return static_cast<float>(static_cast<double>(xo[x][y][v]) + alpha * static_cast<double>(acc[x][y][v]));
+    };
+    float* Ur = (Urb != nullptr) ? Urb + static_cast<int64_t>(b) * strideUr : nullptr;
+    float* Xn = (Urb != nullptr) ? nullptr : Xnb + static_cast<int64_t>(b) * strideX;
+    if (m0 + QT <= nn && n0 + QT <= kc) {
+        if (Ur != nullptr) {
+#pragma unroll
+            for (int x = 0; x < 3; ++x)
+#pragma unroll
+                for (int y = 0; y < 3; ++y)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        Ur[static_cast<int64_t>(out_col(y)) * ldu + out_row(x, v)] = value(x, y, v);
+        } else {
+#pragma unroll
+            for (int x = 0; x < 3; ++x)
+#pragma unroll
+                for (int y = 0; y < 3; ++y)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        Xn[static_cast<int64_t>(out_row(x, v)) * ld + out_col(y)] = value(x, y, v);
+        }
+        return;
+    }
 #pragma unroll
     for (int x = 0; x < 3; ++x)
 #pragma unroll
         for (int y = 0; y < 3; ++y)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                // register v of a 16 x 16 block: row 4 v + g (fp64), 4 g + v (fp32)
-                const int row = m0 + 48 * wm + 16 * x + ((sizeof(P) == 8) ? 4 * v + g : 4 * g + v);
-                const int col = n0 + 48 * wn + 16 * y + l16;
+                const int row = out_row(x, v), col = out_col(y);
                 if (row < nn && col < kc) {
-                    const int64_t o = static_cast<int64_t>(row) * ld + col;
-                    const float val = static_cast<float>(static_cast<double>(X[o]) +
-                                                         alpha * static_cast<double>(acc[x][y][v]));
-                    if (Urb != nullptr)
-                        Urb[static_cast<int64_t>(b) * strideUr + static_cast<int64_t>(col) * ldu + row] = val;
+                    if (Ur != nullptr)
+                        Ur[static_cast<int64_t>(col) * ldu + row] = value(x, y, v);
                     else
-                        Xnb[static_cast<int64_t>(b) * strideX + o] = val;
+                        Xn[static_cast<int64_t>(row) * ld + col] = value(x, y, v);
                 }
             }
 }
