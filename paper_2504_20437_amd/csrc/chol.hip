@@ -319,6 +319,12 @@ __global__ __launch_bounds__(CT, 4) void chol_panel_x_kernel(double* Cb, int k, 
         // A[i][t] = D[t][i] (rows j0 + t of the block inverse), B[t][c] = C_JT[t][c]
         mma64_pairs(X + static_cast<int64_t>(j0) * k + j0, C + static_cast<int64_t>(j0) * k + c0, k, jb, jb, cb,
                     vec, acc, wm, wn, lane);
+        // the deficiency flags of the lane's eight rows, read together
+        bool dfl[2][4];
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) dfl[bi][v] = defic[j0 + min(32 * wm + 2 * (4 * v + lk) + bi, jb - 1)] != 0;
         __syncthreads();   // every wave has its operands before the tile is overwritten
 #pragma unroll
         for (int bi = 0; bi < 2; ++bi)
@@ -326,7 +332,7 @@ __global__ __launch_bounds__(CT, 4) void chol_panel_x_kernel(double* Cb, int k, 
             for (int v = 0; v < 4; ++v) {
                 const int r = 32 * wm + 2 * (4 * v + lk) + bi;
                 if (r >= jb) continue;
-                const bool def = defic[j0 + r] != 0;
+                const bool def = dfl[bi][v];
                 const int c = 32 * wn + 2 * l16;
                 double* dst = C + static_cast<int64_t>(j0 + r) * k + c0 + c;
                 const double o0 = def ? 0.0 : acc[bi][0][v], o1 = def ? 0.0 : acc[bi][1][v];
@@ -403,6 +409,26 @@ __global__ __launch_bounds__(CT, 4) void chol_trailing_p_kernel(double* Cb, int 
             // another one writes
             mma64_pairs(C + static_cast<int64_t>(j0) * k + r0, C + static_cast<int64_t>(j0) * k + c0, k, jb, rb, cb,
                         vec, acc, wm, wn, lane);
+            if (vec && rb == CB && cb == CB && u != vt) {
+                // an interior tile off the diagonal (uniform): the lane's eight
+                // pairs are read together, then written (read-modify-write one
+                // pair at a time waited a memory latency per pair)
+                const int c = 32 * wn + 2 * l16;
+                f64x2 o[2][4];
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        o[bi][v] = *reinterpret_cast<const f64x2*>(
+                            C + static_cast<int64_t>(r0 + 32 * wm + 2 * (4 * v + lk) + bi) * k + c0 + c);
+#pragma unroll
+                for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        *reinterpret_cast<f64x2*>(C + static_cast<int64_t>(r0 + 32 * wm + 2 * (4 * v + lk) + bi) * k +
+                                                  c0 + c) =
+                            f64x2{o[bi][v][0] - acc[bi][0][v], o[bi][v][1] - acc[bi][1][v]};
+            } else {
 #pragma unroll
             for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
@@ -423,6 +449,7 @@ __global__ __launch_bounds__(CT, 4) void chol_trailing_p_kernel(double* Cb, int 
                         if (k1) dst[1] -= acc[bi][1][v];
                     }
                 }
+            }
         }
         if (blockIdx.x == 0) {
             // tile (J + 1, J + 1) is final: factor it (its updates above are
@@ -441,6 +468,25 @@ __global__ __launch_bounds__(CT, 4) void chol_trailing_p_kernel(double* Cb, int 
     mma64_rowA(X + static_cast<int64_t>(i0) * k + j0, C + static_cast<int64_t>(j0) * k + c0, k, CB, jb, cb, vec, acc,
                wm, wn, lane);
     const bool first = (I == J);
+    if (vec && i0 + CB <= k && cb == CB) {
+        // a whole tile (uniform): the lane's eight pairs read together first
+        const int c = 32 * wn + 2 * l16;
+        f64x2 o[2][4];
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                o[bi][v] = first ? f64x2{0.0, 0.0}
+                                 : *reinterpret_cast<const f64x2*>(
+                                       X + static_cast<int64_t>(i0 + 32 * wm + 2 * (4 * v + lk) + bi) * k + c0 + c);
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                *reinterpret_cast<f64x2*>(X + static_cast<int64_t>(i0 + 32 * wm + 2 * (4 * v + lk) + bi) * k + c0 + c) =
+                    f64x2{o[bi][v][0] + acc[bi][0][v], o[bi][v][1] + acc[bi][1][v]};
+        return;
+    }
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
