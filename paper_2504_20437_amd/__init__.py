@@ -277,7 +277,11 @@ def _validate_update(G, r, P, sigma, info, workspace):
 
 def _update_outputs(G, r, P, sigma, info, workspace, need):
     """P, sigma, info and the workspace of a subspace update of G, allocated on
-    the current stream where not given."""
+    the current stream where not given. A workspace allocated here is released
+    to torch's caching allocator when the call returns, before the kernels
+    have run: the allocator hands that memory out again only to later work on
+    the same stream, which runs after them (the second stream's share of the
+    work is joined back into that stream before the call returns)."""
     m, n, _, _, batch = _geom(G, "G")
     s, dev = min(m, n), G.device
     if P is None:
