@@ -36,13 +36,6 @@ constexpr int XK = 64;
 constexpr int XKP = XK + 8;     // padded LDS row (bf16): 144 bytes, 16-byte lane reads conflict-free
 constexpr int XT = 256;
 
-__device__ __forceinline__ uint16_t bf16_bits_rn(float x) {
-    // round to nearest even (inputs here are finite or propagate NaN)
-    const uint32_t u = __float_as_uint(x);
-    if ((u & 0x7f800000u) == 0x7f800000u) return static_cast<uint16_t>((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-    return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-}
-__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 // --------------------------------------------------------------------------
 // dst (cols x rows, ld ldd) = src^T (src rows x cols, ld lds), bf16, 64 x 64 tiles
@@ -114,14 +107,7 @@ __global__ __launch_bounds__(256) void split3_transpose_kernel(const float* srcb
         if (c >= cols) break;
         uint16_t h[3][4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float v = x[i][e];
-            h[0][i] = bf16_bits_rn(v);
-            const float r1 = v - bf16_bits_to_f32(h[0][i]);
-            h[1][i] = bf16_bits_rn(r1);
-            const float r2 = r1 - bf16_bits_to_f32(h[1][i]);
-            h[2][i] = bf16_bits_rn(r2);
-        }
+        for (int i = 0; i < 4; ++i) split3_rn(x[i][e], h[0][i], h[1][i], h[2][i]);
         uint16_t* dst = planes + static_cast<int64_t>(c) * ldp + rb;
         if (vstore && rb + 4 <= rows_pad) {
 #pragma unroll
@@ -145,14 +131,6 @@ __global__ __launch_bounds__(256) void split3_transpose_kernel(const float* srcb
 // cols..cols_pad-1 zero-filled; four consecutive columns per thread (one
 // 16-byte load, one 8-byte store per plane when aligned)
 // --------------------------------------------------------------------------
-__device__ __forceinline__ void split3(float x, uint16_t& h1, uint16_t& h2, uint16_t& h3) {
-    h1 = bf16_bits_rn(x);
-    const float r1 = x - bf16_bits_to_f32(h1);
-    h2 = bf16_bits_rn(r1);
-    const float r2 = r1 - bf16_bits_to_f32(h2);
-    h3 = bf16_bits_rn(r2);
-}
-
 __global__ __launch_bounds__(256) void split3_rows_kernel(const float* srcb, int64_t lds, int64_t strideS,
                                                           uint16_t* planesb, int64_t ldp, int64_t planeStride,
                                                           int64_t strideP, int rows, int cols, int cols_pad,
@@ -175,7 +153,7 @@ __global__ __launch_bounds__(256) void split3_rows_kernel(const float* srcb, int
     }
     uint16_t h[3][4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) split3(x[e], h[0][e], h[1][e], h[2][e]);
+    for (int e = 0; e < 4; ++e) split3_rn(x[e], h[0][e], h[1][e], h[2][e]);
     const int64_t o = static_cast<int64_t>(r) * ldp + c0;
 #pragma unroll
     for (int p = 0; p < 3; ++p) {

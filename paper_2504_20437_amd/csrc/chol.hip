@@ -528,6 +528,27 @@ __global__ __launch_bounds__(256) void fill_deficient_kernel(float* Qb, int rows
     }
 }
 
+// The same generic unit vector written as the three bf16 planes of column j
+// (plane row j, transposed layout of GemmArgs::planes), for a Q that exists
+// only as its planes; rows past `rows` keep the zeros the product wrote.
+__global__ __launch_bounds__(256) void fill_deficient_planes_kernel(uint16_t* planesb, int64_t ldpl, int64_t planeStride,
+                                                                    int64_t stridePl, int rows, int k,
+                                                                    const int* deficB) {
+    const int b = blockIdx.y;
+    const int j = blockIdx.x;
+    if (!deficB[static_cast<int64_t>(b) * k + j]) return;
+    uint16_t* pl = planesb + static_cast<int64_t>(b) * stridePl + static_cast<int64_t>(j) * ldpl;
+    const float scale = 1.0f / sqrtf(static_cast<float>(rows));
+    for (int i = threadIdx.x; i < rows; i += blockDim.x) {
+        const uint64_t h = mix64((static_cast<uint64_t>(j) << 32) | static_cast<uint32_t>(i));
+        uint16_t h1, h2, h3;
+        split3_rn((h & 1ULL) ? scale : -scale, h1, h2, h3);
+        pl[i] = h1;
+        pl[planeStride + i] = h2;
+        pl[2 * planeStride + i] = h3;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, double* xinv,
@@ -555,6 +576,13 @@ hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, con
                                  int batch, hipStream_t stream) {
     hipLaunchKernelGGL(fill_deficient_kernel, dim3(k, batch), dim3(256), 0, stream, Q, rows, k,
                        strideQ, defic);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_deficient_planes(uint16_t* planes, int64_t ldpl, int64_t planeStride, int64_t stridePl,
+                                        int rows, int k, const int* defic, int batch, hipStream_t stream) {
+    hipLaunchKernelGGL(fill_deficient_planes_kernel, dim3(k, batch), dim3(256), 0, stream, planes, ldpl, planeStride,
+                       stridePl, rows, k, defic);
     return hipGetLastError();
 }
 

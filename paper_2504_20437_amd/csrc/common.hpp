@@ -19,6 +19,25 @@ __device__ __forceinline__ float to_f32(bf16_t x) {
     return __uint_as_float(static_cast<uint32_t>(x.bits) << 16);
 }
 
+// bits of the bfloat16 nearest to x (ties to even; NaN stays NaN), and back
+__device__ __forceinline__ uint16_t bf16_bits_rn(float x) {
+    // round to nearest even (inputs here are finite or propagate NaN)
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7f800000u) == 0x7f800000u) return static_cast<uint16_t>((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+// x = h1 + h2 + h3 with the three bf16 terms rounded to nearest in turn (the
+// three planes of an fp32 operand of the bf16 matrix-core products)
+__device__ __forceinline__ void split3_rn(float x, uint16_t& h1, uint16_t& h2, uint16_t& h3) {
+    h1 = bf16_bits_rn(x);
+    const float r1 = x - bf16_bits_to_f32(h1);
+    h2 = bf16_bits_rn(r1);
+    const float r2 = r1 - bf16_bits_to_f32(h2);
+    h3 = bf16_bits_rn(r2);
+}
+
 // MI355X deals workgroups to its 8 XCDs round-robin by linear id (x fastest,
 // then y, then z) and every XCD has its own L2. xcd_logical_id remaps the
 // linear id so that XCD x receives the contiguous range [x * per, (x+1) * per)
@@ -61,6 +80,13 @@ struct GemmArgs {
     int M, N, K;
     float alpha, beta;   // C = alpha * op(A) op(B) + beta * C  (beta == 0: C not read)
     int b_upper;         // op(B) upper triangular: column tile j0 only needs k < j0 + tile width
+    // planes != nullptr (beta == 0 only): instead of C, the three bf16 planes
+    // of alpha op(A) op(B) (split3_rn), transposed: plane p of matrix b holds
+    // element (i, j) at planes[b * stridePl + p * planeStride + j * ldpl + i],
+    // rows M <= i < rows_pad written as zero (rows_pad <= M rounded up to 128)
+    uint16_t* planes;
+    int64_t ldpl, planeStride, stridePl;
+    int rows_pad;
 };
 
 // Exact Gram of the fixed-point image of X on the int8 matrix cores (gram_i8.hip):
@@ -108,6 +134,9 @@ hipError_t launch_cholesky(double* C, int k, int64_t strideC, float* rinv32, dou
 // Replace columns flagged deficient by a deterministic generic unit vector.
 hipError_t launch_fill_deficient(float* Q, int rows, int k, int64_t strideQ, const int* defic,
                                  int batch, hipStream_t stream);
+// the same into the three bf16 planes of Q (GemmArgs::planes layout)
+hipError_t launch_fill_deficient_planes(uint16_t* planes, int64_t ldpl, int64_t planeStride, int64_t stridePl,
+                                        int rows, int k, const int* defic, int batch, hipStream_t stream);
 // Yt (k x k, column c contiguous) = columns of 2^e Y, Y = R^T, in fp32 from the
 // fp64 factor (the row-major upper triangle of R), with the power of two e of
 // each matrix (written to exps[b]) taken from the diagonal diag (k fp64 per

@@ -218,10 +218,27 @@ bool cmax_prepare(const Products& P) {
     return launch_fill_u32(P.cmax, P.strideCM * P.batch, P.st) == hipSuccess;
 }
 
-// Out (rows x k) = In (rows x k) * Rinv (k x k)
+// Three bf16 planes that a product's epilogue writes in place of its fp32
+// output (the operand layout of the bf16 matrix-core products).
+struct PlaneOut {
+    uint16_t* planes;
+    int64_t ldpl, planeStride, stridePl;
+    int rows_pad;
+};
+
+// Out (rows x k) = In (rows x k) * Rinv (k x k), or, with po, only the three
+// bf16 planes of that product
 hipError_t gemm_right_tri(const float* In, float* Out, int64_t stride, int rows, int k,
-                          const float* Rinv, int64_t strideKK, int batch, hipStream_t st) {
+                          const float* Rinv, int64_t strideKK, int batch, hipStream_t st,
+                          const PlaneOut* po = nullptr) {
     GemmArgs a{};
+    if (po != nullptr) {
+        a.planes = po->planes;
+        a.ldpl = po->ldpl;
+        a.planeStride = po->planeStride;
+        a.stridePl = po->stridePl;
+        a.rows_pad = po->rows_pad;
+    }
     a.A = In;
     a.lda = k;
     a.strideA = stride;
@@ -280,7 +297,7 @@ struct Tracer {
 // planes already hold X^T as one bf16 plane (exact), two more zero planes when
 // the product cannot read G in place.
 int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, float* Y, int64_t strideY,
-              bool& cmax_ready, bool planes1 = false) {
+              bool& cmax_ready, bool planes1 = false, bool planes_ready = false) {
     const Shape& sh = *P.sh;
     const Layout& L = *P.L;
     cmax_ready = false;
@@ -289,7 +306,7 @@ int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, fl
         return GALORE_OK;
     }
     const int k = sh.k, s = static_cast<int>(sh.s), l = static_cast<int>(sh.l);
-    if (!planes1)
+    if (!planes1 && !planes_ready)
         GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
                       launch_split3_transpose(X, k, strideX, P.planes, L.ldpl, L.planeStride, L.stridePl, l, k,
                                               static_cast<int>(L.ldpl), P.batch, P.st));
@@ -310,7 +327,7 @@ int product_A(const Products& P, Tracer& tr, const float* X, int64_t strideX, fl
 
 // Z (l x k) = A^T Q, Q (s x k)
 int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, float* Z, int64_t strideZ,
-               bool& cmax_ready) {
+               bool& cmax_ready, bool planes_ready = false) {
     const Shape& sh = *P.sh;
     const Layout& L = *P.L;
     cmax_ready = false;
@@ -319,9 +336,10 @@ int product_At(const Products& P, Tracer& tr, const float* Q, int64_t strideQ, f
         return GALORE_OK;
     }
     const int k = sh.k, s = static_cast<int>(sh.s), l = static_cast<int>(sh.l);
-    GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
-                  launch_split3_transpose(Q, k, strideQ, P.planes, L.ldpl, L.planeStride, L.stridePl, s, k,
-                                          static_cast<int>(pad8(s)), P.batch, P.st));
+    if (!planes_ready)
+        GALORE_TRACED(tr, GALORE_STAGE_OPERAND,
+                      launch_split3_transpose(Q, k, strideQ, P.planes, L.ldpl, L.planeStride, L.stridePl, s, k,
+                                              static_cast<int>(pad8(s)), P.batch, P.st));
     // left: A^T = G^T, read in place (M-contiguous) or from the transposed
     // copy; right: A^T = G (K-contiguous)
     const bool inplace = !sh.left || P.direct;
@@ -425,7 +443,7 @@ GramI8Args gram_args(const Work& w, const float* X, int64_t strideX, int rows, i
 // fixed-point image of In, fp64 factor);
 // columns found dependent are replaced by generic unit vectors.
 int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int rows, int k, int batch,
-              hipStream_t st, hipStream_t aux, Tracer& tr, bool cmax_ready) {
+              hipStream_t st, hipStream_t aux, Tracer& tr, bool cmax_ready, const PlaneOut* po = nullptr) {
     const Layout& L = *w.L;
     GALORE_TRACED(tr, GALORE_STAGE_GRAM, launch_gram_i8(gram_args(w, In, stride, rows, k, cmax_ready), batch, st));
     if (tr.begin(GALORE_STAGE_CHOLESKY) != hipSuccess) return GALORE_ERR_HIP;
@@ -435,8 +453,13 @@ int orth_pass(const Work& w, const float* In, float* Out, int64_t stride, int ro
     }
     if (tr.end() != hipSuccess) return GALORE_ERR_HIP;
     GALORE_TRACED(tr, GALORE_STAGE_TRIANGULAR,
-                  gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st));
-    GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st));
+                  gemm_right_tri(In, Out, stride, rows, k, w.f(L.offRinv), L.strideKK, batch, st, po));
+    if (po != nullptr)
+        GALORE_TRACED(tr, GALORE_STAGE_OTHER,
+                      launch_fill_deficient_planes(po->planes, po->ldpl, po->planeStride, po->stridePl, rows, k,
+                                                   w.i(L.offDef), batch, st));
+    else
+        GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_fill_deficient(Out, rows, k, stride, w.i(L.offDef), batch, st));
     return GALORE_OK;
 }
 
@@ -502,10 +525,19 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(product_A(prod, tr, L1, L.strideL, Sa, L.strideS, ready, L.bf16));
     float* Q = Sa;
     float* Qtmp = Sb;
+    // with a bf16 G an orthonormal panel that only feeds the next product is
+    // written by Y R^-1 straight as that product's three bf16 planes (the same
+    // bits the split of its fp32 values gives), and never in fp32
+    const PlaneOut po_s{prod.planes, L.ldpl, L.planeStride, L.stridePl, static_cast<int>(pad8(s))};
+    const PlaneOut po_l{prod.planes, L.ldpl, L.planeStride, L.stridePl, static_cast<int>(L.ldpl)};
+    bool q_planes = false;   // Q exists only as the planes of the next product
     auto orth_s = [&](int passes) -> int {
         for (int ps = 0; ps < passes; ++ps) {
-            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, aux, tr, ps == 0 && ready);
+            const bool to_planes = L.bf16 && passes == 1;
+            const int e = orth_pass(w, Q, Qtmp, L.strideS, s, k, batch, stream, aux, tr, ps == 0 && ready,
+                                    to_planes ? &po_s : nullptr);
             if (e != GALORE_OK) return e;
+            q_planes = to_planes;
             float* t = Q;
             Q = Qtmp;
             Qtmp = t;
@@ -515,9 +547,9 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
     GALORE_CHECK(orth_s(q == 0 ? 2 : 1));
     // a4: power iterations with re-orthonormalisation after every product
     for (int it = 0; it < q; ++it) {
-        GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready));
-        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, aux, tr, ready));
-        GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS, ready));
+        GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready, q_planes));
+        GALORE_CHECK(orth_pass(w, L1, L2, L.strideL, l, k, batch, stream, aux, tr, ready, L.bf16 ? &po_l : nullptr));
+        GALORE_CHECK(product_A(prod, tr, L2, L.strideL, Qtmp, L.strideS, ready, false, L.bf16));
         {
             float* t = Q;
             Q = Qtmp;
@@ -525,8 +557,9 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
         }
         GALORE_CHECK(orth_s(it == q - 1 ? 2 : 1));
     }
-    // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R
-    GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready));
+    // a5: B^T = Z = A^T Q (l x k); its Gram B B^T = Z^T Z = R^T R (the last Q
+    // came from two passes, in fp32)
+    GALORE_CHECK(product_At(prod, tr, Q, L.strideS, L1, L.strideL, ready, q_planes));
     {
         GALORE_TRACED(tr, GALORE_STAGE_GRAM,
                       launch_gram_i8(gram_args(w, L1, L.strideL, l, k, ready), batch, stream));

@@ -118,10 +118,12 @@ struct KContigTile {
     }
 };
 
-template <ALayout LA, BLayout LB, typename TA, typename TB>
+template <ALayout LA, BLayout LB, typename TA, typename TB, bool PLANES = false>
 __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, int b_vec) {
-    __shared__ float As[2][BK][BM];
-    __shared__ float Bs[2][BK][BN];
+    // the two operand stages; the plane epilogue reuses the same 64 KB
+    __shared__ __attribute__((aligned(16))) float smem[2 * BK * BM + 2 * BK * BN];
+    float (*As)[BK][BM] = reinterpret_cast<float (*)[BK][BM]>(smem);
+    float (*Bs)[BK][BN] = reinterpret_cast<float (*)[BK][BN]>(smem + 2 * BK * BM);
 
     // XCD-aware, row-grouped tile order (grid = n tiles x m tiles x batch)
     const int num_n = gridDim.x, num_m = gridDim.y;
@@ -219,6 +221,66 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
     // ---- epilogue: 32x32 block layout, lane holds column (lane & 31) and rows
     //      (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
     const float alpha = g.alpha, beta = g.beta;
+    if constexpr (PLANES) {
+        // the three bf16 planes of the result, transposed (plane row c holds
+        // column c), through LDS so that each column's 128 rows go out as
+        // whole 16-byte pieces: per half of the tile's columns, the waves that
+        // hold them write T[c][r] (fp32, row pitch TP), then thread t splits
+        // rows 32 (t & 3) .. + 31 of column t >> 2 and stores 64 bytes per plane
+        constexpr int TP = BM + 1;
+        static_assert(64 * TP <= 2 * BK * BM + 2 * BK * BN, "plane staging exceeds the operand stages");
+        float* T = smem;
+        uint16_t* pl = g.planes + static_cast<int64_t>(bz) * g.stridePl;
+        const bool v16 = (g.ldpl % 8) == 0 && (g.planeStride % 8) == 0 && (g.stridePl % 8) == 0 &&
+                         (reinterpret_cast<uintptr_t>(g.planes) % 16) == 0;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            if (wn == half) {
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                    for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            const int rl = wm * 64 + mi * 32 + (v & 3) + 8 * (v >> 2) + 4 * lk;
+                            T[(ni * 32 + lrow) * TP + rl] = (row0 + rl < M) ? alpha * acc[mi][ni][v] : 0.0f;
+                        }
+            }
+            __syncthreads();
+            const int cl = t >> 2, seg = t & 3;
+            const int c = col0 + half * 64 + cl;
+            const int r = row0 + 32 * seg;
+            if (c < N && r < g.rows_pad) {
+                uint16_t* dst = pl + static_cast<int64_t>(c) * g.ldpl + r;
+                const float* src = T + cl * TP + 32 * seg;
+                if (v16 && r + 32 <= g.rows_pad) {
+#pragma unroll
+                    for (int e8 = 0; e8 < 4; ++e8) {
+                        uint16_t h[3][8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) split3_rn(src[8 * e8 + e], h[0][e], h[1][e], h[2][e]);
+#pragma unroll
+                        for (int p = 0; p < 3; ++p)
+                            *reinterpret_cast<uint4*>(dst + p * g.planeStride + 8 * e8) =
+                                make_uint4(h[p][0] | (static_cast<uint32_t>(h[p][1]) << 16),
+                                           h[p][2] | (static_cast<uint32_t>(h[p][3]) << 16),
+                                           h[p][4] | (static_cast<uint32_t>(h[p][5]) << 16),
+                                           h[p][6] | (static_cast<uint32_t>(h[p][7]) << 16));
+                    }
+                } else {
+                    for (int e = 0; e < 32 && r + e < g.rows_pad; ++e) {
+                        uint16_t h1, h2, h3;
+                        split3_rn(src[e], h1, h2, h3);
+                        dst[e] = h1;
+                        dst[g.planeStride + e] = h2;
+                        dst[2 * g.planeStride + e] = h3;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        return;
+    }
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi) {
 #pragma unroll
@@ -238,7 +300,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
     }
 }
 
-template <ALayout LA, BLayout LB, typename TA, typename TB>
+template <ALayout LA, BLayout LB, typename TA, typename TB, bool PLANES = false>
 hipError_t launch_one(const GemmArgs& g, int batch, hipStream_t stream) {
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, batch);
     // 16-byte vector loads need every row start 16-byte aligned
@@ -248,7 +310,7 @@ hipError_t launch_one(const GemmArgs& g, int batch, hipStream_t stream) {
                       (reinterpret_cast<uintptr_t>(g.A) % 16 == 0);
     const int b_vec = (g.ldb % bmul == 0) && (batch == 1 || g.strideB % bmul == 0) &&
                       (reinterpret_cast<uintptr_t>(g.B) % 16 == 0);
-    hipLaunchKernelGGL((gemm_f32_kernel<LA, LB, TA, TB>), grid, dim3(NT), 0, stream, g, a_vec, b_vec);
+    hipLaunchKernelGGL((gemm_f32_kernel<LA, LB, TA, TB, PLANES>), grid, dim3(NT), 0, stream, g, a_vec, b_vec);
     return hipGetLastError();
 }
 
@@ -265,6 +327,15 @@ hipError_t dispatch_types(bool a_bf16, bool b_bf16, const GemmArgs& g, int batch
 hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const GemmArgs& g, int batch,
                        hipStream_t stream) {
     if (g.M <= 0 || g.N <= 0 || batch <= 0) return hipSuccess;
+    if (g.planes != nullptr) {
+        // plane output: fp32 operands, A K-contiguous and B N-contiguous only
+        // (the product Y R^-1 of the orthonormalisation)
+        if (la != ALayout::kKContig || lb != BLayout::kNContig || a_bf16 || b_bf16 || g.beta != 0.0f ||
+            g.rows_pad < g.M || g.rows_pad > (g.M + BM - 1) / BM * BM || g.ldpl < g.rows_pad ||
+            g.planeStride < g.ldpl * g.N || (batch > 1 && g.stridePl < 3 * g.planeStride))
+            return hipErrorInvalidValue;
+        return launch_one<ALayout::kKContig, BLayout::kNContig, float, float, true>(g, batch, stream);
+    }
     if (la == ALayout::kKContig && lb == BLayout::kNContig)
         return dispatch_types<ALayout::kKContig, BLayout::kNContig>(a_bf16, b_bf16, g, batch, stream);
     if (la == ALayout::kMContig && lb == BLayout::kNContig)
