@@ -18,31 +18,72 @@ namespace {
 constexpr int SF_COLS = 64;
 constexpr int SF_GROUPS = 4;
 
+// A workgroup owns 64 columns of one matrix: thread t scans column quad
+// t & 15 (four columns, one 16-byte load per row when the rows are aligned) over
+// the rows t >> 4, t >> 4 + 16, ... in increasing order, four rows in flight;
+// the 16 row groups are reduced through LDS (larger magnitude, then lower
+// row), and the columns whose chosen entry is negative are negated in a
+// second pass with the same access pattern.
+constexpr int SF_QUADS = SF_COLS / 4;                 // 16 column quads
+constexpr int SF_RGROUPS = SF_COLS * SF_GROUPS / SF_QUADS;   // 16 row groups
+
 __global__ __launch_bounds__(SF_COLS* SF_GROUPS) void sign_fix_kernel(float* Pb, int rows, int r,
-                                                                      int64_t ldp, int64_t strideP) {
+                                                                      int64_t ldp, int64_t strideP, int vec) {
     const int b = blockIdx.y;
     float* P = Pb + static_cast<int64_t>(b) * strideP;
-    const int tc = threadIdx.x & (SF_COLS - 1);
-    const int grp = threadIdx.x / SF_COLS;
-    const int c = blockIdx.x * SF_COLS + tc;
-    __shared__ float best_abs[SF_GROUPS][SF_COLS];
-    __shared__ int best_row[SF_GROUPS][SF_COLS];
+    const int cq = threadIdx.x % SF_QUADS, rg = threadIdx.x / SF_QUADS;
+    const int c0 = blockIdx.x * SF_COLS + 4 * cq;
+    __shared__ float best_abs[SF_RGROUPS][SF_COLS];
+    __shared__ int best_row[SF_RGROUPS][SF_COLS];
     __shared__ float flip[SF_COLS];
-    float ba = -1.0f;
-    int br = 0x7fffffff;
-    if (c < r) {
-        for (int i = grp; i < rows; i += SF_GROUPS) {
-            const float a = fabsf(P[static_cast<int64_t>(i) * ldp + c]);
-            if (a > ba) { ba = a; br = i; }          // rows visited in increasing order
+    const bool full = vec && c0 + 4 <= r;
+    auto quad = [&](int i) {
+        const float* q = P + static_cast<int64_t>(i) * ldp + c0;
+        f32x4 x;
+        if (full) {
+            x = *reinterpret_cast<const f32x4*>(q);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = (c0 + e < r) ? q[e] : 0.0f;
+        }
+        return x;
+    };
+    float ba[4] = {-1.0f, -1.0f, -1.0f, -1.0f};
+    int br[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    if (c0 < r) {
+        int i = rg;
+        for (; i + 3 * SF_RGROUPS < rows; i += 4 * SF_RGROUPS) {
+            f32x4 x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) x[u] = quad(i + u * SF_RGROUPS);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float a = fabsf(x[u][e]);
+                    if (a > ba[e]) { ba[e] = a; br[e] = i + u * SF_RGROUPS; }   // rows in increasing order
+                }
+        }
+        for (; i < rows; i += SF_RGROUPS) {
+            const f32x4 x = quad(i);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float a = fabsf(x[e]);
+                if (a > ba[e]) { ba[e] = a; br[e] = i; }
+            }
         }
     }
-    best_abs[grp][tc] = ba;
-    best_row[grp][tc] = br;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        best_abs[rg][4 * cq + e] = ba[e];
+        best_row[rg][4 * cq + e] = br[e];
+    }
     __syncthreads();
-    if (grp == 0) {
+    if (threadIdx.x < SF_COLS) {
+        const int tc = threadIdx.x, c = blockIdx.x * SF_COLS + tc;
         float a = best_abs[0][tc];
         int rr = best_row[0][tc];
-        for (int g = 1; g < SF_GROUPS; ++g) {
+        for (int g = 1; g < SF_RGROUPS; ++g) {
             const float a2 = best_abs[g][tc];
             const int r2 = best_row[g][tc];
             if (a2 > a || (a2 == a && r2 < rr)) { a = a2; rr = r2; }
@@ -52,10 +93,20 @@ __global__ __launch_bounds__(SF_COLS* SF_GROUPS) void sign_fix_kernel(float* Pb,
         flip[tc] = f;
     }
     __syncthreads();
-    if (c < r && flip[tc] < 0.0f) {
-        for (int i = grp; i < rows; i += SF_GROUPS) {
-            float* q = P + static_cast<int64_t>(i) * ldp + c;
-            *q = -*q;
+    if (c0 >= r) return;
+    const float f[4] = {flip[4 * cq], flip[4 * cq + 1], flip[4 * cq + 2], flip[4 * cq + 3]};
+    if (f[0] > 0.0f && f[1] > 0.0f && f[2] > 0.0f && f[3] > 0.0f) return;
+    for (int i = rg; i < rows; i += SF_RGROUPS) {
+        float* q = P + static_cast<int64_t>(i) * ldp + c0;
+        if (full) {
+            f32x4 x = *reinterpret_cast<const f32x4*>(q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] *= f[e];
+            *reinterpret_cast<f32x4*>(q) = x;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (c0 + e < r && f[e] < 0.0f) q[e] = -q[e];
         }
     }
 }
@@ -192,8 +243,9 @@ __global__ __launch_bounds__(256) void copy_rows_kernel(const float* src, int64_
 hipError_t launch_sign_fix(float* P, int rows, int r, int64_t ldp, int64_t strideP, int batch,
                            hipStream_t stream) {
     dim3 grid((r + SF_COLS - 1) / SF_COLS, batch);
+    const int vec = (ldp % 4 == 0) && (batch == 1 || strideP % 4 == 0) && (reinterpret_cast<uintptr_t>(P) % 16 == 0);
     hipLaunchKernelGGL(sign_fix_kernel, grid, dim3(SF_COLS * SF_GROUPS), 0, stream, P, rows, r, ldp,
-                       strideP);
+                       strideP, vec);
     return hipGetLastError();
 }
 
