@@ -275,6 +275,14 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
                 }
             }
         }
+        // the column maxima of the tile's p and q columns, staged in the
+        // (now unused) digit stages once every wave is past the last one: the
+        // epilogue reads one per stored entry, which from global memory waited
+        // a latency per entry
+        __syncthreads();
+        unsigned* cms = reinterpret_cast<unsigned*>(sm);
+        if (t < 2 * GT) cms[t] = cmax[min((t < GT ? GT * u : GT * v - GT) + t, cols - 1)];
+        __syncthreads();
         if (idle) continue;
         // 32 x 32 accumulator layout: lane holds column (lane & 31), register r
         // holds row (r & 3) + 8 (r >> 2) + 4 (lane >> 5)
@@ -282,13 +290,13 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
         for (int y = 0; y < 2; ++y) {
             const int q = GT * v + 64 * wn + 32 * y + l32;
             if (q >= cols) continue;
-            const unsigned bq = cmax[q];
+            const unsigned bq = cms[GT + 64 * wn + 32 * y + l32];
             const int shq = col_shift(bq);
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int p = GT * u + 32 * wm + (r & 3) + 8 * (r >> 2) + 4 * lk;
                 if (p >= cols) continue;
-                const unsigned bp = cmax[p];
+                const unsigned bp = cms[32 * wm + (r & 3) + 8 * (r >> 2) + 4 * lk];
                 double* dstc = C + static_cast<int64_t>(p) * ldc + q;
                 if (bp >= 0x7f800000u || bq >= 0x7f800000u) {
                     *dstc = __builtin_nan("");
@@ -299,7 +307,12 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
                                    ldexp(static_cast<double>(acc[2][y][r]), 16) +
                                    ldexp(static_cast<double>(acc[3][y][r]), 8) + static_cast<double>(acc[4][y][r]);
                 const double val = ldexp(sum, -(col_shift(bp) + shq));
-                *dstc = (sg == 0) ? val : *dstc + val;
+                // the first segment stores (a select with the old value would
+                // read it, and wait for it, before every store)
+                if (sg == 0)
+                    *dstc = val;
+                else
+                    *dstc += val;
             }
         }
     }
