@@ -183,40 +183,53 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
 
     const int lrow = lane & 31;
     const int lk = lane >> 5;
-    for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        const bool more = (kt + 1 < KT);
-        if (more) {
-            load_a((kt + 1) * BK);
-            load_b((kt + 1) * BK);
-        }
-        // operands of step kk + 2 read while step kk's MFMAs run (two
-        // register sets): the matrix pipe does not wait for the LDS between
-        // steps
-        float fa[2][2], fb[2][2];
-        auto read_step = [&](int fbuf, int kk) {
-            fa[fbuf][0] = As[cur][kk + lk][wm * 64 + lrow];
-            fa[fbuf][1] = As[cur][kk + lk][wm * 64 + 32 + lrow];
-            fb[fbuf][0] = Bs[cur][kk + lk][wn * 64 + lrow];
-            fb[fbuf][1] = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
-        };
-        read_step(0, 0);
+    // NB = the wave's 32-column blocks that hold columns below N (wave-uniform):
+    // a block past N (the last tile column of N = 1056, say) takes no MFMAs
+    auto kloop = [&](auto nbc) {
+        constexpr int NB = decltype(nbc)::value;
+        for (int kt = 0; kt < KT; ++kt) {
+            const int cur = kt & 1;
+            const bool more = (kt + 1 < KT);
+            if (more) {
+                load_a((kt + 1) * BK);
+                load_b((kt + 1) * BK);
+            }
+            if constexpr (NB > 0) {
+                // operands of step kk + 2 read while step kk's MFMAs run (two
+                // register sets): the matrix pipe does not wait for the LDS
+                // between steps
+                float fa[2][2], fb[2][2];
+                auto read_step = [&](int fbuf, int kk) {
+                    fa[fbuf][0] = As[cur][kk + lk][wm * 64 + lrow];
+                    fa[fbuf][1] = As[cur][kk + lk][wm * 64 + 32 + lrow];
+                    fb[fbuf][0] = Bs[cur][kk + lk][wn * 64 + lrow];
+                    if constexpr (NB > 1) fb[fbuf][1] = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
+                };
+                read_step(0, 0);
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 2) {
-            const int fbuf = (kk >> 1) & 1;
-            if (kk + 2 < BK) read_step(fbuf ^ 1, kk + 2);
-            __builtin_amdgcn_sched_barrier(0);
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][0], acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][1], acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][0], acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][1], acc[1][1], 0, 0, 0);
+                for (int kk = 0; kk < BK; kk += 2) {
+                    const int fbuf = (kk >> 1) & 1;
+                    if (kk + 2 < BK) read_step(fbuf ^ 1, kk + 2);
+                    __builtin_amdgcn_sched_barrier(0);
+                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][0], acc[0][0], 0, 0, 0);
+                    if constexpr (NB > 1)
+                        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][1], acc[0][1], 0, 0, 0);
+                    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][0], acc[1][0], 0, 0, 0);
+                    if constexpr (NB > 1)
+                        acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][1], acc[1][1], 0, 0, 0);
+                }
+            }
+            if (more) {
+                store_a(cur ^ 1);
+                store_b(cur ^ 1);
+            }
+            __syncthreads();
         }
-        if (more) {
-            store_a(cur ^ 1);
-            store_b(cur ^ 1);
-        }
-        __syncthreads();
-    }
+    };
+    const int cw = col0 + wn * 64;
+    if (cw + 32 < N) kloop(std::integral_constant<int, 2>());
+    else if (cw < N) kloop(std::integral_constant<int, 1>());
+    else kloop(std::integral_constant<int, 0>());
 
     // ---- epilogue: 32x32 block layout, lane holds column (lane & 31) and rows
     //      (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
