@@ -187,8 +187,13 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
     const int lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int l32 = lane & 31, lk = lane >> 5;
-    // on a diagonal tile, a wave whose rows all lie below its columns has nothing to do
-    const bool idle = diag && (wm >= 2 * wn + 2);
+    // on a diagonal tile, a wave whose rows all lie below its columns has nothing
+    // to do, nor has a wave whose rows all lie past the last column (the last
+    // tile row of cols = 1056, say); ny = the wave's 32-column blocks with
+    // columns before cols (the others are not stored)
+    const bool idle = (diag && (wm >= 2 * wn + 2)) || GT * u + 32 * wm >= cols;
+    const int qw = GT * v + 64 * wn;
+    const int ny = __builtin_amdgcn_readfirstlane(qw >= cols ? 0 : (qw + 32 >= cols ? 1 : 2));
     const int8_t* D = Db + static_cast<int64_t>(b) * strideD;
 
     // this wave's direct loads: j = 6 wave + i -> side j / 24, plane (j / 8) % 3,
@@ -262,6 +267,7 @@ __global__ __launch_bounds__(512, 1) void gram_i8_kernel(const int8_t* Db, int64
                     fp[a] = *reinterpret_cast<const i32x4*>(sp + a * kPlaneB + rp * GK + 16 * (c ^ ((rp >> 2) & 3)));
 #pragma unroll
                 for (int y = 0; y < 2; ++y) {
+                    if (y >= ny) break;
                     const int rq = 64 * wn + 32 * y + l32;
                     i32x4 fq[3];
 #pragma unroll
