@@ -147,10 +147,21 @@ __device__ __forceinline__ float dpp_from_prev(float v) {
 }
 // odd rounds: an odd lane's partner row is lane x + 1, an even lane's x - 1;
 // with cn = c on odd lanes (0 on even ones) and cp the other way round, the
-// partner term is cn * v[x + 1] + cp * v[x - 1], both lane moves folded into
-// their multiplies
+// partner term is fma(v[x - 1], cp, cn * v[x + 1]). Both lane moves are folded
+// into the two instructions that use them (the compiler's own DPP folding
+// leaves one or both as separate moves here: five instructions per value
+// instead of three); lanes 0 and 63 read 0 for their missing neighbour, as
+// the moves above do. The leading s_nop gives the two wait states a DPP read
+// needs after a VALU write of its source (not checked by the compiler inside
+// inline assembly).
 __device__ __forceinline__ float rotate_odd(float v, float sg, float cn, float cp) {
-    return fmaf(sg, v, fmaf(cp, dpp_from_prev(v), cn * dpp_from_next(v)));
+    float t;
+    asm("s_nop 1\n\t"
+        "v_mul_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+        "v_fmac_f32_dpp %0, %1, %3 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+        : "=&v"(t)
+        : "v"(v), "v"(cn), "v"(cp));
+    return fmaf(sg, v, t);
 }
 
 // ---- bf16 planes of the pair's columns (Gram and rotation phases) ----------
