@@ -360,11 +360,15 @@ __device__ __forceinline__ void wait_stages(int ahead) {
 // PA = 3: both operands hold three planes (fp32 x fp32): the six products
 // A_i B_j with i + j <= 4 (planes counted from 1); the three left out are below
 // 2^-26 of |A||B| in size, under fp32 rounding.
-template <int YK, int S, bool AT, int PA, int PB = 3>
-__global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
+template <int YK, int S, bool AT, int PA, int PB = 3, int WN = 2>
+__global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <= 81920) ? 2 : 1) void gemm_bf16x3_direct_kernel(Bx3Args g) {
     static_assert(!AT || YK == 32, "the M-contiguous A stage assumes 32-deep stages");
     static_assert(PA == 1 || (PA == 3 && !AT), "three A planes are K-contiguous");
     static_assert(PB == 3 || (PB == 1 && PA == 1), "one B plane pairs with one A plane");
+    static_assert(WN == 2 || (WN == 4 && !AT), "four waves across N: K-contiguous A only");
+    // WN waves across the tile's columns (64 each), two down its rows (128 each)
+    constexpr int YN = 64 * WN;
+    constexpr int YT = 128 * WN;
     // the stage's two steps read and multiplied in order, the next stage's
     // loads issued after the reads (see the main loop): needed with the
     // transposing reads, and faster for three B planes either way
@@ -377,6 +381,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
     constexpr int kStage = kStageA + kStageB;
     constexpr int LA = kStageA / 1024 / (YT / 64);       // direct loads per wave per stage (1 KB each)
     constexpr int LB = kStageB / 1024 / (YT / 64);
+    static_assert(kStageA % (1024 * (YT / 64)) == 0 && kStageB % (1024 * (YT / 64)) == 0, "whole direct loads per wave");
     constexpr int RPI = 64 / CPR;                        // rows per direct load
     constexpr int RPB = 256 / RB;                        // rows per 256 bytes (one sweep of the 64 banks)
     __shared__ __attribute__((aligned(16))) unsigned char ysm[S * kStage];
@@ -395,7 +400,7 @@ __global__ __launch_bounds__(YT, (S * (PA * YM + PB * YN) * YK * 2 <= 81920) ? 2
     const int row0 = tm * YM, col0 = tn * YN;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
 
     // chunk c of stage row r sits at slot c ^ ((r / RPB) % CPR). A direct load
     // fills RPI rows; lane i -> (row RPI j + i / CPR, slot i % CPR), so it
@@ -741,14 +746,25 @@ constexpr int kDirectS = GALORE_BX3_S;     // stages in LDS
 #define GALORE_BX3T_S 2
 #endif
 constexpr int kDirectST = GALORE_BX3T_S;   // stages of the M-contiguous-A kernel (32 deep each)
+// Three A planes (the back-projection): 256 x 256 tiles of eight waves (four
+// across N), three 48 KB stages of K = 16, one workgroup per CU. Measured on
+// 64 x 4096x11008, r = 1024, per launch: 30.8 ms against 35.2-37.4 ms with
+// 256 x 128 tiles of four waves and two 36 KB stages (two workgroups per CU),
+// 31.3 ms with the wide tile and two stages: with two stages each stage's
+// loads had one stage of matrix-core time to land, and a tile that waited on
+// a miss held its workgroup at the barrier.
 #ifndef GALORE_BX6_K
 #define GALORE_BX6_K 16
 #endif
 #ifndef GALORE_BX6_S
-#define GALORE_BX6_S 2
+#define GALORE_BX6_S 3
 #endif
-constexpr int kX6K = GALORE_BX6_K;         // the same for three A planes (two 72 KB stages at K = 16:
-constexpr int kX6S = GALORE_BX6_S;         // two workgroups per CU)
+#ifndef GALORE_BX6_WN
+#define GALORE_BX6_WN 4
+#endif
+constexpr int kX6K = GALORE_BX6_K;         // K depth of a stage
+constexpr int kX6S = GALORE_BX6_S;         // stages in LDS
+constexpr int kX6WN = GALORE_BX6_WN;       // waves across N (tile 256 x 64 WN)
 
 }  // namespace
 
@@ -892,8 +908,9 @@ hipError_t launch_gemm_bf16x6(const void* Aplanes, int64_t lda, int64_t planeStr
     g.b_upper = b_upper;
     g.cmax = nullptr;
     g.strideCM = 0;
-    dim3 grid((N + YN - 1) / YN, (M + YM - 1) / YM, batch);
-    hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kX6K, kX6S, false, 3>), grid, dim3(YT), 0, stream, g);
+    dim3 grid((N + 64 * kX6WN - 1) / (64 * kX6WN), (M + YM - 1) / YM, batch);
+    hipLaunchKernelGGL((gemm_bf16x3_direct_kernel<kX6K, kX6S, false, 3, 3, kX6WN>), grid, dim3(128 * kX6WN), 0, stream,
+                       g);
     return hipGetLastError();
 }
 
