@@ -183,6 +183,35 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
 
     const int lrow = lane & 31;
     const int lk = lane >> 5;
+    const int cw = col0 + wn * 64;   // the wave's first column
+    // one stage's MFMAs for the column blocks in MASK (bit ni: block ni),
+    // the operands of step kk + 2 read while step kk's MFMAs run (two register
+    // sets): the matrix pipe does not wait for the LDS between steps
+    auto kstep = [&](int cur, auto maskc) {
+        constexpr int MASK = decltype(maskc)::value;
+        float fa[2][2], fb[2][2];
+        auto read_step = [&](int fbuf, int kk) {
+            fa[fbuf][0] = As[cur][kk + lk][wm * 64 + lrow];
+            fa[fbuf][1] = As[cur][kk + lk][wm * 64 + 32 + lrow];
+            if constexpr (MASK & 1) fb[fbuf][0] = Bs[cur][kk + lk][wn * 64 + lrow];
+            if constexpr (MASK & 2) fb[fbuf][1] = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
+        };
+        read_step(0, 0);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const int fbuf = (kk >> 1) & 1;
+            if (kk + 2 < BK) read_step(fbuf ^ 1, kk + 2);
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (MASK & 1) {
+                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][0], acc[0][0], 0, 0, 0);
+                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][0], acc[1][0], 0, 0, 0);
+            }
+            if constexpr (MASK & 2) {
+                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][1], acc[0][1], 0, 0, 0);
+                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][1], acc[1][1], 0, 0, 0);
+            }
+        }
+    };
     // NB = the wave's 32-column blocks that hold columns below N (wave-uniform):
     // a block past N (the last tile column of N = 1056, say) takes no MFMAs
     auto kloop = [&](auto nbc) {
@@ -195,28 +224,15 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
                 load_b((kt + 1) * BK);
             }
             if constexpr (NB > 0) {
-                // operands of step kk + 2 read while step kk's MFMAs run (two
-                // register sets): the matrix pipe does not wait for the LDS
-                // between steps
-                float fa[2][2], fb[2][2];
-                auto read_step = [&](int fbuf, int kk) {
-                    fa[fbuf][0] = As[cur][kk + lk][wm * 64 + lrow];
-                    fa[fbuf][1] = As[cur][kk + lk][wm * 64 + 32 + lrow];
-                    fb[fbuf][0] = Bs[cur][kk + lk][wn * 64 + lrow];
-                    if constexpr (NB > 1) fb[fbuf][1] = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
-                };
-                read_step(0, 0);
-#pragma unroll
-                for (int kk = 0; kk < BK; kk += 2) {
-                    const int fbuf = (kk >> 1) & 1;
-                    if (kk + 2 < BK) read_step(fbuf ^ 1, kk + 2);
-                    __builtin_amdgcn_sched_barrier(0);
-                    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][0], acc[0][0], 0, 0, 0);
-                    if constexpr (NB > 1)
-                        acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][1], acc[0][1], 0, 0, 0);
-                    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][0], acc[1][0], 0, 0, 0);
-                    if constexpr (NB > 1)
-                        acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][1], acc[1][1], 0, 0, 0);
+                // with an upper-triangular op(B) (b_upper), a 32-column block
+                // needs only the rows up to its last column: in the tile's last
+                // K stages the block (or the wave) whose columns all lie before
+                // this stage's rows skips its MFMAs (their B operands are zero)
+                const int k0 = kt * BK;
+                if (!g.b_upper || k0 < cw + 32) {
+                    kstep(cur, std::integral_constant<int, (NB > 1) ? 3 : 1>());
+                } else if (NB > 1 && k0 < cw + 64) {
+                    kstep(cur, std::integral_constant<int, 2>());
                 }
             }
             if (more) {
@@ -226,7 +242,6 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
             __syncthreads();
         }
     };
-    const int cw = col0 + wn * 64;
     if (cw + 32 < N) kloop(std::integral_constant<int, 2>());
     else if (cw < N) kloop(std::integral_constant<int, 1>());
     else kloop(std::integral_constant<int, 0>());
