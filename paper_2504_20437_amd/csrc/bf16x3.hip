@@ -549,6 +549,17 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
             if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
             __builtin_amdgcn_sched_barrier(0);
             multiply(1);
+        } else if constexpr (PA == 3 && YK == 16) {
+            // the six-plane product (one 16-deep step per stage, three stages):
+            // the next loads issued after the stage's fragment reads, so that
+            // their LDS writes do not meet those reads (29.96 against 30.7 ms
+            // per launch of 64 with the loads first; they still land two
+            // stages ahead)
+            fetch(0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
+            __builtin_amdgcn_sched_barrier(0);
+            multiply(0);
         } else {
             if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
 #pragma unroll
