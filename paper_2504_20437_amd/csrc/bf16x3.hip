@@ -335,6 +335,7 @@ constexpr int YT = 256;
 constexpr int kDirectGroup = GALORE_BX3_GROUP;   // tile rows per group of the tile order
 constexpr bool kDirectXcd = GALORE_BX3_XCD != 0;  // XCD-contiguous logical tile ids
 
+
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
@@ -373,7 +374,12 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
     // loads issued after the reads (see the main loop): needed with the
     // transposing reads, and faster for three B planes either way
     constexpr bool kSplit = AT || (PA == 1 && PB == 3 && YK == 32);
-    constexpr int kFragBufs = kSplit ? 2 : 1;           // fragment register buffers
+    // the one-plane product reads both steps' fragments, then issues the next
+    // stage's loads, then runs its MFMAs (7.97 against 8.20 ms per launch of
+    // 64 with the loads first; the same order slows the three-plane A X, 18.4
+    // against 16.9 ms)
+    constexpr bool kReadFirst = !AT && YK == 32 && PB == 1;
+    constexpr int kFragBufs = (kSplit || kReadFirst) ? 2 : 1;   // fragment register buffers
     constexpr int CPR = YK / 8;                          // 16-byte chunks per row
     constexpr int RB = YK * 2;                           // bytes per row
     constexpr int kStageA = PA * YM * RB;
@@ -528,7 +534,15 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
                                 a[fb][pairs[q][0]][x], bq[fb][pairs[q][1]][y], acc[x][y], 0, 0, 0);
             }
         };
-        if constexpr (kSplit) {
+        if constexpr (kReadFirst) {
+            fetch(0, 0);
+            fetch(kFragBufs - 1, 1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (kt + S - 1 < KT) issue((kt + S - 1) % S, (kt + S - 1) * YK);
+            __builtin_amdgcn_sched_barrier(0);
+            multiply(0);
+            multiply(kFragBufs - 1);
+        } else if constexpr (kSplit) {
             // the compiler cannot tell the transposing LDS reads from the LDS
             // that the direct loads in flight may write, and before any such
             // read issued after those loads it waits for all of them (a whole
