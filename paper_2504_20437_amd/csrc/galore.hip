@@ -608,8 +608,27 @@ int rsvd_impl(const void* G, int32_t g_dtype, int64_t m, int64_t n, int64_t ldg,
         a.K = k;
         a.alpha = 1.0f;
         a.beta = 0.0f;
-        GALORE_TRACED(tr, GALORE_STAGE_PROJECTOR,
-                      launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, stream));
+        // with the bf16 path's plane region (free once the last product has run)
+        // Q is split by rows into three bf16 planes there and U_r^T into the
+        // refinement's fp64 scratch (free after it), and the product runs on the
+        // bf16 matrix cores as six plane products (k a multiple of 16); every
+        // other case on the fp32 matrix cores
+        uint16_t* qpl = L.bf16 ? reinterpret_cast<uint16_t*>(w.base + L.offPl) : nullptr;
+        uint16_t* upl = reinterpret_cast<uint16_t*>(w.base + L.offS);
+        const int64_t qps = static_cast<int64_t>(s) * k, ups = static_cast<int64_t>(r) * k;
+        if (qpl != nullptr && k % 16 == 0 &&
+            bf16x6_ok(qpl, k, qps, L.stridePl, upl, k, ups, 3 * ups, k, batch)) {
+            GALORE_TRACED(tr, GALORE_STAGE_PROJECTOR,
+                          launch_split3_rows(Q, k, L.strideS, qpl, k, qps, L.stridePl, s, k, k, batch, stream));
+            GALORE_TRACED(tr, GALORE_STAGE_PROJECTOR,
+                          launch_split3_transpose(Ur, r, L.strideUr, upl, k, ups, 3 * ups, k, r, k, batch, stream));
+            GALORE_TRACED(tr, GALORE_STAGE_PROJECTOR,
+                          launch_gemm_bf16x6(qpl, k, qps, L.stridePl, upl, k, ups, 3 * ups, P, ldp, stride_p, 0, 0, s,
+                                             r, k, 1.0f, 0.0f, batch, stream));
+        } else {
+            GALORE_TRACED(tr, GALORE_STAGE_PROJECTOR,
+                          launch_gemm(ALayout::kKContig, BLayout::kNContig, false, false, a, batch, stream));
+        }
     }
     GALORE_TRACED(tr, GALORE_STAGE_OTHER, launch_sign_fix(P, s, r, ldp, stride_p, batch, stream));
     return GALORE_OK;
