@@ -688,10 +688,13 @@ __global__ __launch_bounds__(256) void jacobi_norms_kernel(const float* Ytb, int
 // the blocks of a norm-ordered matrix pairs columns of like size first and
 // cuts the rotations the later sweeps need (about 17% fewer pair rotations
 // and one sweep fewer on the 4096 x 11008 workload in a CPU model of these
-// sweeps). One workgroup per matrix; converged matrices are skipped.
-__global__ __launch_bounds__(1024) void jacobi_order_kernel(const double* normsb, int k, int* jpermb,
-                                                            const int* rotb, int max_sweeps, int sweep) {
-    const int b = blockIdx.x;
+// sweeps). The rank of column c is the number of columns ahead of it; one
+// thread per column, (k / 256) workgroups per matrix, each with the matrix's
+// norms in LDS (one workgroup of 1024 threads per matrix took 63-124 us a
+// sweep); converged matrices are skipped.
+__global__ __launch_bounds__(256) void jacobi_order_kernel(const double* normsb, int k, int* jpermb,
+                                                           const int* rotb, int max_sweeps, int sweep) {
+    const int b = blockIdx.y;
     if (sweep > 0 && rotb[static_cast<int64_t>(b) * max_sweeps + sweep - 1] == 0) return;
     extern __shared__ unsigned char smem[];
     double* nv = reinterpret_cast<double*>(smem);
@@ -700,16 +703,15 @@ __global__ __launch_bounds__(1024) void jacobi_order_kernel(const double* normsb
         nv[c] = (v == v) ? v : -1.0;
     }
     __syncthreads();
-    int* perm = jpermb + static_cast<int64_t>(b) * k;
-    for (int c = threadIdx.x; c < k; c += blockDim.x) {
-        const double vc = nv[c];
-        int rank = 0;
-        for (int c2 = 0; c2 < k; ++c2) {
-            const double v2 = nv[c2];
-            rank += (v2 > vc) || (v2 == vc && c2 < c);
-        }
-        perm[rank] = c;
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= k) return;
+    const double vc = nv[c];
+    int rank = 0;
+    for (int c2 = 0; c2 < k; ++c2) {
+        const double v2 = nv[c2];
+        rank += (v2 > vc) || (v2 == vc && c2 < c);
     }
+    jpermb[static_cast<int64_t>(b) * k + rank] = c;
 }
 
 // Xa[j][:] = y_perm(j) / sigma_perm(j) (row j of the result contiguous) for the
@@ -891,8 +893,8 @@ hipError_t launch_jacobi_order(const float* Yt, int k, int64_t strideX, double* 
                                int max_sweeps, int sweep, int batch, hipStream_t stream) {
     hipLaunchKernelGGL(jacobi_norms_kernel, dim3((k + 3) / 4, batch), dim3(256), 0, stream, Yt, k, strideX, norms, rot,
                        max_sweeps, sweep);
-    hipLaunchKernelGGL(jacobi_order_kernel, dim3(batch), dim3(1024), static_cast<size_t>(k) * sizeof(double), stream,
-                       norms, k, jperm, rot, max_sweeps, sweep);
+    hipLaunchKernelGGL(jacobi_order_kernel, dim3((k + 255) / 256, batch), dim3(256), static_cast<size_t>(k) * sizeof(double),
+                       stream, norms, k, jperm, rot, max_sweeps, sweep);
     return hipGetLastError();
 }
 
