@@ -50,14 +50,34 @@ __global__ __launch_bounds__(256) void fill_u32_kernel(unsigned* p, int64_t n) {
 }
 
 // cmax[j] = max over rows of the bits of |x_ij| (non-negative floats order
-// like their bit patterns; NaN and Inf compare above every finite value)
+// like their bit patterns; NaN and Inf compare above every finite value).
+// Thread t of a workgroup takes column quad t (16-byte row loads, 8 rows in
+// flight) when vec (rows 16-byte aligned, cols a multiple of 4), else single
+// columns; grid (ceil(rows / rb), batch).
 __global__ __launch_bounds__(256) void colmax_kernel(const float* Xb, int64_t ldx, int64_t strideX, int rows,
-                                                     int cols, int rb, unsigned* cmaxb, int64_t strideCM) {
+                                                     int cols, int rb, unsigned* cmaxb, int64_t strideCM, int vec) {
     const int b = blockIdx.y;
     const float* X = Xb + static_cast<int64_t>(b) * strideX;
     unsigned* cmax = cmaxb + static_cast<int64_t>(b) * strideCM;
     const int i0 = blockIdx.x * rb;
     const int i1 = min(rows, i0 + rb);
+    if (vec) {
+        for (int q = threadIdx.x; 4 * q < cols; q += blockDim.x) {
+            unsigned m[4] = {0u, 0u, 0u, 0u};
+            for (int i = i0; i < i1; i += 8) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    if (i + e < i1) {
+                        const f32x4 x = *reinterpret_cast<const f32x4*>(X + static_cast<int64_t>(i + e) * ldx + 4 * q);
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) m[c] = max(m[c], __float_as_uint(fabsf(x[c])));
+                    }
+            }
+#pragma unroll
+            for (int c = 0; c < 4; ++c) atomicMax(cmax + 4 * q + c, m[c]);
+        }
+        return;
+    }
     for (int j = threadIdx.x; j < cols; j += blockDim.x) {
         unsigned m[16];
 #pragma unroll
@@ -347,8 +367,10 @@ hipError_t launch_gram_i8(const GramI8Args& g, int batch, hipStream_t stream) {
         if (e != hipSuccess) return e;
         const int rb = 128;
         dim3 grid((g.rows + rb - 1) / rb, batch);
+        const int vec = (g.cols % 4 == 0) && (g.ldx % 4 == 0) && (batch == 1 || g.strideX % 4 == 0) &&
+                        (reinterpret_cast<uintptr_t>(g.X) % 16 == 0);
         hipLaunchKernelGGL(colmax_kernel, grid, dim3(256), 0, stream, g.X, g.ldx, g.strideX, g.rows, g.cols, rb,
-                           g.cmax, g.strideCM);
+                           g.cmax, g.strideCM, vec);
     }
     {
         // 16-byte row loads where every row start of X is aligned (the digit

@@ -392,28 +392,28 @@ __global__ __launch_bounds__(256) void refine_update_kernel(const double* Mb, in
 }
 
 // Order the refined vectors by lambda (descending, ties by index; a NaN last):
-// permb[b][j] = index of the j-th, sigma_j = sqrt(lambda). grid (batch);
-// dynamic LDS: k doubles.
+// permb[b][j] = index of the j-th, sigma_j = sqrt(lambda). One thread per
+// vector, its rank the number of vectors ahead of it; grid (ceil(k / 256),
+// batch), each workgroup with the matrix's lambdas in LDS (dynamic: k doubles).
 __global__ __launch_bounds__(256) void refine_rank_kernel(const double* lamb, int k, int r, int* permb, float* sigma,
                                                           int64_t stride_sigma, const int* flags) {
-    const int b = blockIdx.x;
+    const int b = blockIdx.y;
     if (flags[b] == 0) return;
     extern __shared__ unsigned char smem[];
     double* lam = reinterpret_cast<double*>(smem);
-    int* perm = permb + static_cast<int64_t>(b) * k;
     for (int i = threadIdx.x; i < k; i += blockDim.x) {
         const double v = lamb[static_cast<int64_t>(b) * k + i];
         lam[i] = (v == v) ? v : -DBL_MAX;
     }
     __syncthreads();
-    for (int c = threadIdx.x; c < k; c += blockDim.x) {
-        const double vc = lam[c];
-        int rank = 0;
-        for (int c2 = 0; c2 < k; ++c2) rank += (lam[c2] > vc) || (lam[c2] == vc && c2 < c);
-        perm[rank] = c;
-        if (sigma != nullptr && rank < r)
-            sigma[static_cast<int64_t>(b) * stride_sigma + rank] = static_cast<float>(sqrt(fmax(vc, 0.0)));
-    }
+    const int c = blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= k) return;
+    const double vc = lam[c];
+    int rank = 0;
+    for (int c2 = 0; c2 < k; ++c2) rank += (lam[c2] > vc) || (lam[c2] == vc && c2 < c);
+    permb[static_cast<int64_t>(b) * k + rank] = c;
+    if (sigma != nullptr && rank < r)
+        sigma[static_cast<int64_t>(b) * stride_sigma + rank] = static_cast<float>(sqrt(fmax(vc, 0.0)));
 }
 
 // Xs[j][:] = Xt[perm[j]][:] for the r leading vectors; grid (r, batch)
@@ -453,8 +453,8 @@ hipError_t launch_refine(const double* R, int64_t strideR, float* Xa, float* Xb,
                        Xa, strideX, Xb, k, k, static_cast<int64_t>(k), 1.0, 0.0, static_cast<float*>(nullptr),
                        static_cast<int64_t>(0), static_cast<int64_t>(0), flags);
     // the r vectors of largest lambda, in order, into the rows of Xa
-    hipLaunchKernelGGL(refine_rank_kernel, dim3(batch), dim3(256), static_cast<size_t>(k) * sizeof(double), stream,
-                       lam, k, r, perm, sigma, stride_sigma, flags);
+    hipLaunchKernelGGL(refine_rank_kernel, dim3((k + 255) / 256, batch), dim3(256), static_cast<size_t>(k) * sizeof(double),
+                       stream, lam, k, r, perm, sigma, stride_sigma, flags);
     hipLaunchKernelGGL(refine_gather_kernel, dim3(r, batch), dim3(256), 0, stream, Xb, strideX, perm, k, Xa, flags);
     // their Gram D = X_r^T X_r (into S), then Ur = (X_r (I - (D - I) / 2))^T
     const dim3 upper_r(ntr * (ntr + 1) / 2, batch), full_r(ntr * nt, batch);
