@@ -737,7 +737,7 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
                                                               float* sigma, int64_t stride_sigma,
                                                               const int* rotb, int max_sweeps, int nsweeps, int* info,
                                                               double* scratchb, int64_t strideScratch,
-                                                              const int* expb, const double* normsb, int* permb,
+                                                              const int* expb, const double* normsb, const int* permb,
                                                               int* flags) {
     extern __shared__ unsigned char smem[];
     double* sig = reinterpret_cast<double*>(smem);
@@ -749,16 +749,11 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
     float* Ur = Urb + static_cast<int64_t>(b) * strideUr;
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    for (int c = tid; c < k; c += blockDim.x) sig[c] = normsb[static_cast<int64_t>(b) * k + c];
-    __syncthreads();
+    // the descending order of the norms (ties by index, NaN last), ranked by
+    // jacobi_order_kernel into permb before this kernel
     for (int c = tid; c < k; c += blockDim.x) {
-        const double vc = (sig[c] == sig[c]) ? sig[c] : -1.0;
-        int rank = 0;
-        for (int c2 = 0; c2 < k; ++c2) {
-            const double v2 = (sig[c2] == sig[c2]) ? sig[c2] : -1.0;
-            rank += (v2 > vc) || (v2 == vc && c2 < c);
-        }
-        perm[rank] = c;
+        sig[c] = normsb[static_cast<int64_t>(b) * k + c];
+        perm[c] = permb[static_cast<int64_t>(b) * k + c];
     }
     __syncthreads();
     if (tid == 0) {
@@ -779,10 +774,7 @@ __global__ __launch_bounds__(256) void jacobi_finalize_kernel(const float* Ytb, 
     // fp64 refinement; the others (rank-deficient, non-finite) keep the vectors
     // written here
     const bool refinable = flags != nullptr && (nkeep == r) && sig[perm[k - 1]] > 0.0 && sig[perm[0]] <= DBL_MAX;
-    if (flags != nullptr) {
-        if (tid == 0) flags[b] = refinable ? 1 : 0;
-        for (int j = tid; j < k; j += blockDim.x) permb[static_cast<int64_t>(b) * k + j] = perm[j];
-    }
+    if (flags != nullptr && tid == 0) flags[b] = refinable ? 1 : 0;
     if (!refinable) {
         const int64_t total = static_cast<int64_t>(k) * nkeep;
         for (int64_t pos = tid; pos < total; pos += blockDim.x) {
@@ -915,6 +907,9 @@ hipError_t launch_jacobi_finalize(const float* Yt, int k, int64_t strideX, int r
                                   int* perm, float* Xa, int* flags, int batch, hipStream_t stream) {
     hipLaunchKernelGGL(jacobi_norms_kernel, dim3((k + 3) / 4, batch), dim3(256), 0, stream, Yt, k, strideX, norms,
                        static_cast<const int*>(nullptr), 0, 0);
+    // their descending order into perm (sweep 0: no convergence check)
+    hipLaunchKernelGGL(jacobi_order_kernel, dim3((k + 255) / 256, batch), dim3(256), static_cast<size_t>(k) * sizeof(double),
+                       stream, norms, k, perm, static_cast<const int*>(nullptr), 0, 0);
     const size_t shmem = static_cast<size_t>(k) * (sizeof(double) + sizeof(int));
     hipLaunchKernelGGL(jacobi_finalize_kernel, dim3(batch), dim3(256), shmem, stream, Yt, k, strideX, r, Ur,
                        strideUr, sigma, stride_sigma, rot, max_sweeps, nsweeps, info, scratch, strideScratch, exps,
