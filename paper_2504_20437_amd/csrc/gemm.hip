@@ -118,7 +118,7 @@ struct KContigTile {
     }
 };
 
-template <ALayout LA, BLayout LB, typename TA, typename TB, bool PLANES = false>
+template <ALayout LA, BLayout LB, typename TA, typename TB, bool PLANES = false, bool TRIL = false>
 __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, int b_vec) {
     // the two operand stages; the plane epilogue reuses the same 64 KB
     __shared__ __attribute__((aligned(16))) float smem[2 * BK * BM + 2 * BK * BN];
@@ -170,11 +170,20 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
     auto store_a = [&](int buf) { TileA::store(As[buf], t, ra); };
     auto store_b = [&](int buf) { TileB::store(Bs[buf], t, rb); };
 
-    f32x16 acc[2][2];
+    // wave layout: 2 x 2 waves of 64 x 64 (two 32-row and two 32-column blocks
+    // each), or, for an upper-triangular op(B) (TRIL), 4 x 1 waves of 32 rows
+    // by all 128 columns: in a tile's last K stages every wave then drops the
+    // same column blocks, where the 2 x 2 layout left the waves of the first
+    // 64 columns idle at the stage barriers
+    constexpr int WMB = TRIL ? 1 : 2;            // 32-row blocks per wave
+    constexpr int WNB = TRIL ? 4 : 2;            // 32-column blocks per wave
+    const int wr = TRIL ? 32 * wave : 64 * wm;   // the wave's first row in the tile
+    const int wc = TRIL ? 0 : 64 * wn;           // the wave's first column in the tile
+    f32x16 acc[WMB][WNB];
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < WMB; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
+        for (int ni = 0; ni < WNB; ++ni)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.0f;
 
@@ -188,18 +197,19 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
 
     const int lrow = lane & 31;
     const int lk = lane >> 5;
-    const int cw = col0 + wn * 64;   // the wave's first column
+    const int cw = col0 + wc;   // the wave's first column
     // one stage's MFMAs for the column blocks in MASK (bit ni: block ni),
     // the operands of step kk + 2 read while step kk's MFMAs run (two register
     // sets): the matrix pipe does not wait for the LDS between steps
     auto kstep = [&](int cur, auto maskc) {
         constexpr int MASK = decltype(maskc)::value;
-        float fa[2][2], fb[2][2];
+        float fa[2][WMB], fb[2][WNB];
         auto read_step = [&](int fbuf, int kk) {
-            fa[fbuf][0] = As[cur][kk + lk][wm * 64 + lrow];
-            fa[fbuf][1] = As[cur][kk + lk][wm * 64 + 32 + lrow];
-            if constexpr (MASK & 1) fb[fbuf][0] = Bs[cur][kk + lk][wn * 64 + lrow];
-            if constexpr (MASK & 2) fb[fbuf][1] = Bs[cur][kk + lk][wn * 64 + 32 + lrow];
+#pragma unroll
+            for (int mi = 0; mi < WMB; ++mi) fa[fbuf][mi] = As[cur][kk + lk][wr + 32 * mi + lrow];
+#pragma unroll
+            for (int ni = 0; ni < WNB; ++ni)
+                if ((MASK >> ni) & 1) fb[fbuf][ni] = Bs[cur][kk + lk][wc + 32 * ni + lrow];
         };
         read_step(0, 0);
 #pragma unroll
@@ -207,20 +217,24 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
             const int fbuf = (kk >> 1) & 1;
             if (kk + 2 < BK) read_step(fbuf ^ 1, kk + 2);
             __builtin_amdgcn_sched_barrier(0);
-            if constexpr (MASK & 1) {
-                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][0], acc[0][0], 0, 0, 0);
-                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][0], acc[1][0], 0, 0, 0);
-            }
-            if constexpr (MASK & 2) {
-                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][0], fb[fbuf][1], acc[0][1], 0, 0, 0);
-                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][1], fb[fbuf][1], acc[1][1], 0, 0, 0);
-            }
+#pragma unroll
+            for (int ni = 0; ni < WNB; ++ni)
+                if ((MASK >> ni) & 1) {
+#pragma unroll
+                    for (int mi = 0; mi < WMB; ++mi)
+                        acc[mi][ni] =
+                            __builtin_amdgcn_mfma_f32_32x32x2f32(fa[fbuf][mi], fb[fbuf][ni], acc[mi][ni], 0, 0, 0);
+                }
         }
     };
     // NB = the wave's 32-column blocks that hold columns below N (wave-uniform):
-    // a block past N (the last tile column of N = 1056, say) takes no MFMAs
+    // a block past N (the last tile column of N = 1056, say) takes no MFMAs.
+    // With an upper-triangular op(B) (b_upper) a block needs only the rows up
+    // to its last column: in the tile's last K stages the blocks whose columns
+    // all lie before the stage's rows skip their MFMAs (zero B operands).
     auto kloop = [&](auto nbc) {
         constexpr int NB = decltype(nbc)::value;
+        constexpr int FULL = (1 << NB) - 1;
         for (int kt = 0; kt < KT; ++kt) {
             const int cur = kt & 1;
             const bool more = (kt + 1 < KT);
@@ -229,15 +243,21 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
                 load_b((kt + 1) * BK);
             }
             if constexpr (NB > 0) {
-                // with an upper-triangular op(B) (b_upper), a 32-column block
-                // needs only the rows up to its last column: in the tile's last
-                // K stages the block (or the wave) whose columns all lie before
-                // this stage's rows skips its MFMAs (their B operands are zero)
                 const int k0 = kt * BK;
                 if (!g.b_upper || k0 < cw + 32) {
-                    kstep(cur, std::integral_constant<int, (NB > 1) ? 3 : 1>());
+                    kstep(cur, std::integral_constant<int, FULL>());
+                } else if constexpr (TRIL) {
+                    // blocks d .. of the wave's four (k0 = cw + 32 d, d = 1 .. 3)
+                    const int d = (k0 - cw) >> 5;
+                    if (d == 1) {
+                        if constexpr ((FULL & 0xE) != 0) kstep(cur, std::integral_constant<int, FULL & 0xE>());
+                    } else if (d == 2) {
+                        if constexpr ((FULL & 0xC) != 0) kstep(cur, std::integral_constant<int, FULL & 0xC>());
+                    } else if (d == 3) {
+                        if constexpr ((FULL & 0x8) != 0) kstep(cur, std::integral_constant<int, FULL & 0x8>());
+                    }
                 } else if (NB > 1 && k0 < cw + 64) {
-                    kstep(cur, std::integral_constant<int, 2>());
+                    kstep(cur, std::integral_constant<int, (NB > 1) ? 2 : 0>());
                 }
             }
             if (more) {
@@ -247,9 +267,18 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
             __syncthreads();
         }
     };
-    if (cw + 32 < N) kloop(std::integral_constant<int, 2>());
-    else if (cw < N) kloop(std::integral_constant<int, 1>());
-    else kloop(std::integral_constant<int, 0>());
+    if constexpr (TRIL) {
+        const int nv = (N - cw + 31) / 32;
+        if (nv >= 4) kloop(std::integral_constant<int, 4>());
+        else if (nv == 3) kloop(std::integral_constant<int, 3>());
+        else if (nv == 2) kloop(std::integral_constant<int, 2>());
+        else if (nv == 1) kloop(std::integral_constant<int, 1>());
+        else kloop(std::integral_constant<int, 0>());
+    } else {
+        if (cw + 32 < N) kloop(std::integral_constant<int, 2>());
+        else if (cw < N) kloop(std::integral_constant<int, 1>());
+        else kloop(std::integral_constant<int, 0>());
+    }
 
     // ---- epilogue: 32x32 block layout, lane holds column (lane & 31) and rows
     //      (v & 3) + 8 (v >> 2) + 4 (lane >> 5) for accumulator register v.
@@ -268,16 +297,17 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
                          (reinterpret_cast<uintptr_t>(g.planes) % 16) == 0;
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-            if (wn == half) {
 #pragma unroll
-                for (int mi = 0; mi < 2; ++mi)
+            for (int ni = 0; ni < WNB; ++ni) {
+                const int cl = wc + 32 * ni;           // the block's first column in the tile
+                if ((cl >> 6) != half) continue;
 #pragma unroll
-                    for (int ni = 0; ni < 2; ++ni)
+                for (int mi = 0; mi < WMB; ++mi)
 #pragma unroll
-                        for (int v = 0; v < 16; ++v) {
-                            const int rl = wm * 64 + mi * 32 + (v & 3) + 8 * (v >> 2) + 4 * lk;
-                            T[(ni * 32 + lrow) * TP + rl] = (row0 + rl < M) ? alpha * acc[mi][ni][v] : 0.0f;
-                        }
+                    for (int v = 0; v < 16; ++v) {
+                        const int rl = wr + mi * 32 + (v & 3) + 8 * (v >> 2) + 4 * lk;
+                        T[(cl - 64 * half + lrow) * TP + rl] = (row0 + rl < M) ? alpha * acc[mi][ni][v] : 0.0f;
+                    }
             }
             __syncthreads();
             const int cl = t >> 2, seg = t & 3;
@@ -315,13 +345,13 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
         return;
     }
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
+    for (int mi = 0; mi < WMB; ++mi) {
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni) {
-            const int c = col0 + wn * 64 + ni * 32 + lrow;
+        for (int ni = 0; ni < WNB; ++ni) {
+            const int c = col0 + wc + ni * 32 + lrow;
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const int r = row0 + wm * 64 + mi * 32 + (v & 3) + 8 * (v >> 2) + 4 * lk;
+                const int r = row0 + wr + mi * 32 + (v & 3) + 8 * (v >> 2) + 4 * lk;
                 if (r < M && c < N) {
                     float* dst = C + static_cast<int64_t>(r) * g.ldc + c;
                     float val = alpha * acc[mi][ni][v];
@@ -333,7 +363,7 @@ __global__ __launch_bounds__(NT, 2) void gemm_f32_kernel(GemmArgs g, int a_vec, 
     }
 }
 
-template <ALayout LA, BLayout LB, typename TA, typename TB, bool PLANES = false>
+template <ALayout LA, BLayout LB, typename TA, typename TB, bool PLANES = false, bool TRIL = false>
 hipError_t launch_one(const GemmArgs& g, int batch, hipStream_t stream) {
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, batch);
     // 16-byte vector loads need every row start 16-byte aligned
@@ -343,7 +373,7 @@ hipError_t launch_one(const GemmArgs& g, int batch, hipStream_t stream) {
                       (reinterpret_cast<uintptr_t>(g.A) % 16 == 0);
     const int b_vec = (g.ldb % bmul == 0) && (batch == 1 || g.strideB % bmul == 0) &&
                       (reinterpret_cast<uintptr_t>(g.B) % 16 == 0);
-    hipLaunchKernelGGL((gemm_f32_kernel<LA, LB, TA, TB, PLANES>), grid, dim3(NT), 0, stream, g, a_vec, b_vec);
+    hipLaunchKernelGGL((gemm_f32_kernel<LA, LB, TA, TB, PLANES, TRIL>), grid, dim3(NT), 0, stream, g, a_vec, b_vec);
     return hipGetLastError();
 }
 
@@ -367,8 +397,12 @@ hipError_t launch_gemm(ALayout la, BLayout lb, bool a_bf16, bool b_bf16, const G
             g.rows_pad < g.M || g.rows_pad > (g.M + BM - 1) / BM * BM || g.ldpl < g.rows_pad ||
             g.planeStride < g.ldpl * g.N || (batch > 1 && g.stridePl < 3 * g.planeStride))
             return hipErrorInvalidValue;
-        return launch_one<ALayout::kKContig, BLayout::kNContig, float, float, true>(g, batch, stream);
+        return g.b_upper ? launch_one<ALayout::kKContig, BLayout::kNContig, float, float, true, true>(g, batch, stream)
+                         : launch_one<ALayout::kKContig, BLayout::kNContig, float, float, true>(g, batch, stream);
     }
+    // an upper-triangular op(B) (Y R^-1): the 4 x 1 wave layout
+    if (g.b_upper && la == ALayout::kKContig && lb == BLayout::kNContig && !a_bf16 && !b_bf16)
+        return launch_one<ALayout::kKContig, BLayout::kNContig, float, float, false, true>(g, batch, stream);
     if (la == ALayout::kKContig && lb == BLayout::kNContig)
         return dispatch_types<ALayout::kKContig, BLayout::kNContig>(a_bf16, b_bf16, g, batch, stream);
     if (la == ALayout::kMContig && lb == BLayout::kNContig)
