@@ -22,6 +22,8 @@
 // 32 x 32), LDS rows padded to 72 bf16 (144 bytes: the 16 lanes of a 16-byte
 // read fall on distinct banks), next tile prefetched in registers, XCD-aware
 // row-grouped tile order.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace galore {
@@ -464,6 +466,11 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
 #pragma unroll
     for (int st = 0; st < S - 1; ++st)
         if (st < KT) issue(st, st * YK);
+    // NB = this wave's 32-column blocks that lie inside N (the last tile of a
+    // 1056-wide product holds 32 valid columns): the fragment reads and MFMAs
+    // of the blocks past N are skipped, the wave still issues its loads
+    auto kloop = [&](auto nbc) {
+    constexpr int NB = decltype(nbc)::value;
     for (int kt = 0; kt < KT; ++kt) {
         // stage kt landed for this wave, then for every wave; past the barrier
         // every wave has also finished iteration kt - 1, so its stage is refilled
@@ -506,7 +513,7 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
 #pragma unroll
             for (int p = 0; p < PB; ++p)
 #pragma unroll
-                for (int y = 0; y < 2; ++y) {
+                for (int y = 0; y < NB; ++y) {
                     const int r = wn * 64 + 32 * y + l32;
                     bq[fb][p][y] = *reinterpret_cast<const bf16x8*>(sb + p * (YN * RB) + r * RB +
                                                                     16 * (c ^ ((r / RPB) % CPR)));
@@ -519,7 +526,7 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
 #pragma unroll
                     for (int x = 0; x < 4; ++x)
 #pragma unroll
-                        for (int y = 0; y < 2; ++y)
+                        for (int y = 0; y < NB; ++y)
                             acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[fb][0][x], bq[fb][p][y], acc[x][y],
                                                                                  0, 0, 0);
             } else {
@@ -529,7 +536,7 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
 #pragma unroll
                     for (int x = 0; x < 4; ++x)
 #pragma unroll
-                        for (int y = 0; y < 2; ++y)
+                        for (int y = 0; y < NB; ++y)
                             acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                                 a[fb][pairs[q][0]][x], bq[fb][pairs[q][1]][y], acc[x][y], 0, 0, 0);
             }
@@ -583,6 +590,13 @@ __global__ __launch_bounds__(128 * WN, (S * (PA * YM + PB * 64 * WN) * YK * 2 <=
             }
         }
     }
+    };
+    // (the six-plane kernel keeps one loop: its launches here have N a
+    // multiple of the tile width, and the extra loops measured 0.6% slower)
+    const int nb = PA == 3 ? 2 : __builtin_amdgcn_readfirstlane(min(2, max(0, (N - col0 - wn * 64 + 31) / 32)));
+    if (PA == 3 || nb >= 2) kloop(std::integral_constant<int, 2>());
+    else if (nb == 1) kloop(std::integral_constant<int, 1>());
+    else kloop(std::integral_constant<int, 0>());
 
     const float alpha = g.alpha, beta = g.beta;
     unsigned mx[2] = {0u, 0u};   // bits of the largest |C| of this lane's two columns
